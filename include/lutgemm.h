@@ -1,0 +1,207 @@
+/*
+ * lutgemm.h -- C ABI of an MI355X (gfx950) library for LUT-based
+ * mixed-precision GEMM (mpGEMM) between low-bit weights and FP16 / INT8
+ * activations, after "LUT Tensor Core: A Software-Hardware Co-Design for
+ * LUT-Based Low-Bit LLM Inference" (arXiv 2408.06003).
+ *
+ * The operation (the paper's LMMA semantics, Section 3.3.1):
+ *
+ *     O[M, N] = A[M, K] x W[N, K]^T  (+ O[M, N] when accumulating)
+ *
+ * with real weights r = s (q - z) (Section 3.1.2, Eq. 1) and the dot product
+ * evaluated by table lookup (Section 3.1, Eq. 3-6):
+ *   - lutgemm_precompute builds, for every 4 activations, the 8-entry half
+ *     table of signed partial sums made possible by reading weight bits {0,1}
+ *     as {-1,+1} (Eq. 4-5), as an independent operator (Section 3.1.1);
+ *   - lutgemm_pack_weights is the offline weight mapping: bit-serial planes
+ *     (Section 3.1), reinterpretation (Eq. 2) and offline bit-level negation
+ *     (Eq. 6);
+ *   - lutgemm_mpgemm is the bit-serial lookup-accumulate with the
+ *     scale / zero-point epilogue of Eq. 3.
+ * lutgemm_mpgemm_dequant is a dequantize-to-FP16 + matrix-core comparison path
+ * (the "indirect mpGEMM with dequantization" of Section 2.2).
+ *
+ * Conventions for every entry point:
+ *   - Device pointers must be 16-byte aligned device memory; host pointers are
+ *     marked as such.  The caller allocates and owns every buffer; the library
+ *     never allocates, frees or retains a pointer after the call returns.
+ *   - `stream` is a hipStream_t (NULL = the default stream).  Work is enqueued
+ *     asynchronously; no call synchronizes the host with the device.
+ *   - Arguments are validated on the host before anything is enqueued: on any
+ *     status other than LUTGEMM_SUCCESS nothing was launched.  A failed launch
+ *     returns LUTGEMM_ERROR_HIP.
+ *   - Calls on distinct streams with distinct workspaces are thread-safe.
+ */
+#ifndef LUTGEMM_H
+#define LUTGEMM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    LUTGEMM_SUCCESS = 0,
+    LUTGEMM_ERROR_INVALID_VALUE = 1,     /* null pointer, negative size, misaligned pointer, bad enum */
+    LUTGEMM_ERROR_NOT_SUPPORTED = 2,     /* a valid but unsupported combination (see lutgemm_validate) */
+    LUTGEMM_ERROR_INSUFFICIENT_SIZE = 3, /* a buffer smaller than its size query */
+    LUTGEMM_ERROR_HIP = 4                /* the HIP runtime reported an error */
+} lutgemm_status_t;
+
+/* Weight formats (Section 3.1.2).  `codes` is [N][K], K contiguous. */
+enum {
+    LUTGEMM_WFMT_UINT = 0,    /* uint8 codes q in [0, 2^b), r = s (q - z); s, z FP16 per group   */
+    LUTGEMM_WFMT_BINARY = 1,  /* uint8 codes q in {0,1} standing for {-1,+1}, r = s (2q - 1)        */
+    LUTGEMM_WFMT_TERNARY = 2  /* int8 codes w in {-1,0,+1}, stored as q = w + 1 with b = 2, r = s w  */
+};
+
+/* Activation / table types. */
+enum {
+    LUTGEMM_ACT_FP16 = 0,     /* FP16 activations -> FP16 tables, FP32 accumulation              */
+    LUTGEMM_ACT_INT8 = 1      /* FP16 activations quantized per token to INT8 (absmax) -> INT16
+                                 tables, exact INT32 accumulation (BINARY / TERNARY weights)     */
+};
+
+/* Output types. */
+enum {
+    LUTGEMM_OUT_FP16 = 0,
+    LUTGEMM_OUT_FP32 = 1,
+    LUTGEMM_OUT_INT32 = 2     /* INT8 path only: the exact integer dot product sum_k q_a w       */
+};
+
+/*
+ * Problem description.
+ *   K, N        reduction length and number of output columns (weight rows); K % 128 == 0, N >= 1
+ *   w_bits      b: 1, 2 or 4 for UINT; 1 for BINARY; 2 for TERNARY
+ *   wfmt        LUTGEMM_WFMT_*
+ *   group_size  quantization group along K: a multiple of 128 that divides K (K = per channel),
+ *               or 0 = a single scale (and zero) for the whole tensor
+ *   scale_fp32  0: scales (and zeros) are FP16; 1: the scale is FP32 (per-tensor only, no zeros)
+ *   act         LUTGEMM_ACT_*
+ */
+typedef struct {
+    int64_t K;
+    int64_t N;
+    int32_t w_bits;
+    int32_t wfmt;
+    int32_t group_size;
+    int32_t scale_fp32;
+    int32_t act;
+    int32_t reserved; /* must be 0 */
+} lutgemm_problem_t;
+
+/* Static string for a status code. */
+const char *lutgemm_status_string(lutgemm_status_t status);
+
+/* Library version string. */
+const char *lutgemm_version(void);
+
+/*
+ * Host-only check of a problem and token count M (M >= 1; pass M = 1 when M does
+ * not matter).  Needs no GPU.  Returns LUTGEMM_ERROR_INVALID_VALUE for malformed
+ * input (null, K or N <= 0, unknown enum, reserved != 0) and
+ * LUTGEMM_ERROR_NOT_SUPPORTED for: K % 128 != 0; group_size not 0 and not a
+ * multiple of 128 dividing K; w_bits not allowed for wfmt; scale_fp32 with
+ * group_size != 0 or with UINT; ACT_INT8 with UINT weights or with a group
+ * smaller than K.
+ */
+lutgemm_status_t lutgemm_validate(const lutgemm_problem_t *problem, int64_t M);
+
+/* Bytes of the packed-weight buffer (opaque layout).  0 for an invalid problem. */
+size_t lutgemm_packed_weight_size(const lutgemm_problem_t *problem);
+
+/*
+ * Bytes of the table buffer written by lutgemm_precompute for M tokens.  The
+ * layout is public so that another kernel can produce it (e.g. fused into the
+ * operator that produces the activations, Section 3.1.1), with J = K/4 table
+ * groups and Q = K/group_size quantization groups (Q = 1 per-tensor):
+ *   offset 0:      T[M][J][8]   half tables, FP16 (ACT_FP16) or INT16 (ACT_INT8);
+ *                  T[m][j][i] = sum_{e<4} x_{4j+e} (2 b_e - 1) where b_0 = 0 and
+ *                  b_e = bit (3-e) of i (Eq. 5: the first activation of the group
+ *                  is the pattern's MSB), x = a * 2^-e_m (FP16) or q_a (INT8)
+ *   offset s_off:  S[M][Q]      sum of x over each quantization group, FP32 or INT32
+ *   offset t_off:  t[M]         per-token factor, FP32: 2^e_m for ACT_FP16, where
+ *                  max_k |a[m,k]| = f 2^e_m with f in [0.5, 1) (1 for an all-zero row);
+ *                  the absmax scale s_a = amax / 127 for ACT_INT8
+ * with s_off = align256(16 M J) and t_off = align256(s_off + 4 M Q).
+ * 0 for an invalid problem.
+ */
+size_t lutgemm_table_size(const lutgemm_problem_t *problem, int64_t M);
+
+/* Offsets of S and t inside the table buffer (see lutgemm_table_size). */
+lutgemm_status_t lutgemm_table_offsets(const lutgemm_problem_t *problem, int64_t M,
+                                       size_t *s_offset, size_t *t_offset);
+
+/*
+ * Bytes of scratch memory lutgemm_mpgemm needs for M tokens (split-K partial
+ * sums and arrival counters); may be 0.  The workspace must be zero-filled
+ * before its first use; every completed call leaves its counters at zero again,
+ * so a workspace can be reused by later calls on the same stream.
+ */
+size_t lutgemm_workspace_size(const lutgemm_problem_t *problem, int64_t M);
+
+/*
+ * Offline weight packing (Section 3.1.2, Eq. 2 and Eq. 6; Section 3.1 bit-serial
+ * planes).  Enqueues one kernel on `stream`.
+ *   codes   device [N][K]: uint8 (UINT, BINARY) or int8 (TERNARY).  UINT codes are
+ *           taken modulo 2^b, BINARY codes modulo 2; TERNARY values outside
+ *           {-1,0,1} are clamped.
+ *   scales  device: FP16 [N][K/group] (FP32 or FP16 [1] when group_size == 0)
+ *   zeros   device FP16, same shape as scales, UINT only (NULL otherwise)
+ *   packed  device, packed_bytes >= lutgemm_packed_weight_size(problem)
+ * Each weight bit-plane is stored as 4-bit table indices: the pattern of 4
+ * consecutive weights (the first weight is the MSB) with the low 3 bits inverted
+ * when the MSB is set (Eq. 6); scale and zero are stored as given and
+ * reinterpreted (s' = s/2, z' = 2z + 1 - 2^b, Eq. 2) in FP32 where they are used.
+ */
+lutgemm_status_t lutgemm_pack_weights(const lutgemm_problem_t *problem, const void *codes,
+                                      const void *scales, const void *zeros, void *packed,
+                                      size_t packed_bytes, void *stream);
+
+/*
+ * Table precompute (Section 3.1.1 "independent operator"; Eq. 4-5): one kernel
+ * that reads act [M][K] FP16 (device) and writes the table buffer described at
+ * lutgemm_table_size.  For ACT_INT8 it first quantizes each token:
+ * amax = max |a|, q_a = clamp(rint(a * (127 / amax)), -127, 127) in FP32
+ * (q_a = 0 when amax == 0).
+ */
+lutgemm_status_t lutgemm_precompute(const lutgemm_problem_t *problem, int64_t M, const void *act,
+                                    void *tables, size_t table_bytes, void *stream);
+
+/*
+ * LUT mpGEMM (Section 3.1 bit-serial lookup with Eq. 3, 5-6; LMMA semantics
+ * O = A x W^T + Acc, Section 3.3.1).
+ *   tables     device, written by lutgemm_precompute (or the same layout)
+ *   packed     device, written by lutgemm_pack_weights
+ *   out        device [M][N] row-major, of out_dtype; read first when accumulate != 0
+ *   out_dtype  LUTGEMM_OUT_FP16 / FP32; LUTGEMM_OUT_INT32 for ACT_INT8 only
+ *   accumulate 0: O = A W^T;  1: O = O + A W^T (INT32: exact integer add;
+ *              FP: one FP32 add of the finished product, then the conversion)
+ *   workspace  device, workspace_bytes >= lutgemm_workspace_size(problem, M);
+ *              may be NULL when that size is 0
+ * FP path: O = t_m sum_q s'_q (sum_b 2^b sum_j L_{b,j} - z'_q S_q), FP32.
+ * INT8 path: acc = sum_k q_a w exactly; O = acc (INT32) or (float(acc) s_a) s_w.
+ * The result is bitwise reproducible run to run.
+ */
+lutgemm_status_t lutgemm_mpgemm(const lutgemm_problem_t *problem, int64_t M, const void *tables,
+                                const void *packed, void *out, int32_t out_dtype,
+                                int32_t accumulate, void *workspace, size_t workspace_bytes,
+                                void *stream);
+
+/*
+ * Comparison path (Section 2.2, dequantization-based mpGEMM): rebuilds FP16
+ * weights s (q - z) from the same packed buffer and multiplies them with FP16
+ * activations act [M][K] on the matrix cores (FP32 accumulation).  ACT_FP16
+ * problems only; out_dtype FP16 or FP32; accumulate as for lutgemm_mpgemm.
+ */
+lutgemm_status_t lutgemm_mpgemm_dequant(const lutgemm_problem_t *problem, int64_t M,
+                                        const void *act, const void *packed, void *out,
+                                        int32_t out_dtype, int32_t accumulate, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LUTGEMM_H */

@@ -1,0 +1,229 @@
+"""Python binding of ``liblutgemm.so`` (LUT-based mixed-precision GEMM for gfx950).
+
+Argument marshalling only: every step of the computation runs in the HIP kernels
+behind the C ABI declared in ``include/lutgemm.h``.  PyTorch is used for device
+memory and streams.  If the shared library has not been built, importing this
+package raises ``ImportError`` -- there is no CPU fallback.
+
+Low-level functions mirror the C entry points (``validate``, ``packed_weight_size``,
+``table_size``, ``table_offsets``, ``workspace_size``, ``pack_weights``,
+``precompute``, ``mpgemm``, ``mpgemm_dequant``); ``LutGemm`` is a small holder that
+allocates the packed weights, tables and workspace with torch and calls them.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "liblutgemm.so")
+
+# enums of include/lutgemm.h
+SUCCESS, ERROR_INVALID_VALUE, ERROR_NOT_SUPPORTED, ERROR_INSUFFICIENT_SIZE, ERROR_HIP = 0, 1, 2, 3, 4
+WFMT_UINT, WFMT_BINARY, WFMT_TERNARY = 0, 1, 2
+ACT_FP16, ACT_INT8 = 0, 1
+OUT_FP16, OUT_FP32, OUT_INT32 = 0, 1, 2
+
+EXPORTS = [
+    "lutgemm_status_string", "lutgemm_version", "lutgemm_validate", "lutgemm_packed_weight_size",
+    "lutgemm_table_size", "lutgemm_table_offsets", "lutgemm_workspace_size", "lutgemm_pack_weights",
+    "lutgemm_precompute", "lutgemm_mpgemm", "lutgemm_mpgemm_dequant",
+]
+
+
+class Problem(ctypes.Structure):
+    """``lutgemm_problem_t``."""
+    _fields_ = [("K", ctypes.c_int64), ("N", ctypes.c_int64), ("w_bits", ctypes.c_int32),
+                ("wfmt", ctypes.c_int32), ("group_size", ctypes.c_int32), ("scale_fp32", ctypes.c_int32),
+                ("act", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+
+    def __repr__(self):
+        return (f"Problem(K={self.K}, N={self.N}, w_bits={self.w_bits}, wfmt={self.wfmt}, "
+                f"group_size={self.group_size}, scale_fp32={self.scale_fp32}, act={self.act})")
+
+
+class LutGemmError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        super().__init__(f"{where}: {status_string(status)}")
+        self.status = status
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build() "
+                          "(or python paper_2408_06003_amd/build.py) first")
+    L = ctypes.CDLL(LIB_PATH)
+    P, I64, I32, SZ = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_size_t
+    PP = ctypes.POINTER(Problem)
+    L.lutgemm_status_string.restype = ctypes.c_char_p
+    L.lutgemm_status_string.argtypes = [ctypes.c_int]
+    L.lutgemm_version.restype = ctypes.c_char_p
+    L.lutgemm_version.argtypes = []
+    L.lutgemm_validate.restype = ctypes.c_int
+    L.lutgemm_validate.argtypes = [PP, I64]
+    L.lutgemm_packed_weight_size.restype = SZ
+    L.lutgemm_packed_weight_size.argtypes = [PP]
+    L.lutgemm_table_size.restype = SZ
+    L.lutgemm_table_size.argtypes = [PP, I64]
+    L.lutgemm_table_offsets.restype = ctypes.c_int
+    L.lutgemm_table_offsets.argtypes = [PP, I64, ctypes.POINTER(SZ), ctypes.POINTER(SZ)]
+    L.lutgemm_workspace_size.restype = SZ
+    L.lutgemm_workspace_size.argtypes = [PP, I64]
+    L.lutgemm_pack_weights.restype = ctypes.c_int
+    L.lutgemm_pack_weights.argtypes = [PP, P, P, P, P, SZ, P]
+    L.lutgemm_precompute.restype = ctypes.c_int
+    L.lutgemm_precompute.argtypes = [PP, I64, P, P, SZ, P]
+    L.lutgemm_mpgemm.restype = ctypes.c_int
+    L.lutgemm_mpgemm.argtypes = [PP, I64, P, P, P, I32, I32, P, SZ, P]
+    L.lutgemm_mpgemm_dequant.restype = ctypes.c_int
+    L.lutgemm_mpgemm_dequant.argtypes = [PP, I64, P, P, P, I32, I32, P]
+    return L
+
+
+lib = _load()
+
+
+def status_string(status: int) -> str:
+    return lib.lutgemm_status_string(int(status)).decode()
+
+
+def version() -> str:
+    return lib.lutgemm_version().decode()
+
+
+def problem(K: int, N: int, w_bits: int, wfmt: int, group_size: int, act: int = ACT_FP16,
+            scale_fp32: bool = False) -> Problem:
+    return Problem(K, N, w_bits, wfmt, group_size, 1 if scale_fp32 else 0, act, 0)
+
+
+def _ptr(x) -> Optional[int]:
+    """Device (or host) address of a torch tensor, an int, or None."""
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    return x.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def _check(status: int, where: str):
+    if status != SUCCESS:
+        raise LutGemmError(status, where)
+
+
+def validate(p: Problem, M: int = 1) -> int:
+    return lib.lutgemm_validate(ctypes.byref(p), M)
+
+
+def packed_weight_size(p: Problem) -> int:
+    return lib.lutgemm_packed_weight_size(ctypes.byref(p))
+
+
+def table_size(p: Problem, M: int) -> int:
+    return lib.lutgemm_table_size(ctypes.byref(p), M)
+
+
+def table_offsets(p: Problem, M: int):
+    s, t = ctypes.c_size_t(0), ctypes.c_size_t(0)
+    _check(lib.lutgemm_table_offsets(ctypes.byref(p), M, ctypes.byref(s), ctypes.byref(t)), "table_offsets")
+    return s.value, t.value
+
+
+def workspace_size(p: Problem, M: int) -> int:
+    return lib.lutgemm_workspace_size(ctypes.byref(p), M)
+
+
+def pack_weights(p: Problem, codes, scales, zeros, packed, stream=None, packed_bytes=None):
+    nbytes = packed_bytes if packed_bytes is not None else packed.numel() * packed.element_size()
+    _check(lib.lutgemm_pack_weights(ctypes.byref(p), _ptr(codes), _ptr(scales), _ptr(zeros), _ptr(packed),
+                                    nbytes, _stream(stream)), "lutgemm_pack_weights")
+
+
+def precompute(p: Problem, M: int, act, tables, stream=None, table_bytes=None):
+    nbytes = table_bytes if table_bytes is not None else tables.numel() * tables.element_size()
+    _check(lib.lutgemm_precompute(ctypes.byref(p), M, _ptr(act), _ptr(tables), nbytes, _stream(stream)),
+           "lutgemm_precompute")
+
+
+def mpgemm(p: Problem, M: int, tables, packed, out, out_dtype: int, accumulate: bool = False,
+           workspace=None, stream=None, workspace_bytes=None):
+    if workspace_bytes is None:
+        workspace_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(lib.lutgemm_mpgemm(ctypes.byref(p), M, _ptr(tables), _ptr(packed), _ptr(out), out_dtype,
+                              1 if accumulate else 0, _ptr(workspace), workspace_bytes, _stream(stream)),
+           "lutgemm_mpgemm")
+
+
+def mpgemm_dequant(p: Problem, M: int, act, packed, out, out_dtype: int, accumulate: bool = False,
+                   stream=None):
+    _check(lib.lutgemm_mpgemm_dequant(ctypes.byref(p), M, _ptr(act), _ptr(packed), _ptr(out), out_dtype,
+                                      1 if accumulate else 0, _stream(stream)), "lutgemm_mpgemm_dequant")
+
+
+class LutGemm:
+    """Packed low-bit weights plus the buffers one mpGEMM call needs (torch allocations).
+
+    ``codes``, ``scales``, ``zeros`` are device tensors in the layout of
+    ``lutgemm_pack_weights``; packing is enqueued on the current stream.
+    """
+
+    def __init__(self, p: Problem, codes, scales, zeros=None, device="cuda"):
+        import torch
+        st = validate(p, 1)
+        _check(st, "lutgemm_validate")
+        self.p = p
+        self.device = torch.device(device)
+        self.packed = torch.empty(packed_weight_size(p), dtype=torch.uint8, device=self.device)
+        pack_weights(p, codes, scales, zeros, self.packed)
+        self._tables = {}
+        self._ws = {}
+
+    def tables(self, M: int):
+        import torch
+        if M not in self._tables:
+            self._tables[M] = torch.empty(table_size(self.p, M), dtype=torch.uint8, device=self.device)
+        return self._tables[M]
+
+    def workspace(self, M: int):
+        import torch
+        n = workspace_size(self.p, M)
+        if n == 0:
+            return None
+        if M not in self._ws:
+            self._ws[M] = torch.zeros(n, dtype=torch.uint8, device=self.device)
+        return self._ws[M]
+
+    def out_dtype_code(self, dtype) -> int:
+        import torch
+        return {torch.float16: OUT_FP16, torch.float32: OUT_FP32, torch.int32: OUT_INT32}[dtype]
+
+    def __call__(self, act, out=None, out_dtype=None, accumulate=False, stream=None):
+        """out[M, N] (=|+=) act[M, K] x W^T through precompute + LUT mpGEMM."""
+        import torch
+        M = act.shape[0]
+        if out is None:
+            out = torch.empty((M, self.p.N), dtype=out_dtype or torch.float16, device=self.device)
+        t = self.tables(M)
+        precompute(self.p, M, act, t, stream=stream)
+        mpgemm(self.p, M, t, self.packed, out, self.out_dtype_code(out.dtype), accumulate,
+               workspace=self.workspace(M), stream=stream)
+        return out
+
+    def dequant(self, act, out=None, out_dtype=None, accumulate=False, stream=None):
+        """Comparison path: dequantize to FP16 + matrix cores."""
+        import torch
+        M = act.shape[0]
+        if out is None:
+            out = torch.empty((M, self.p.N), dtype=out_dtype or torch.float16, device=self.device)
+        mpgemm_dequant(self.p, M, act, self.packed, out, self.out_dtype_code(out.dtype), accumulate,
+                       stream=stream)
+        return out

@@ -1,0 +1,301 @@
+// C ABI of the LUT mpGEMM library: argument validation, size queries, launch
+// planning and dispatch.  Everything here runs on the host; the arithmetic of
+// every step runs in the HIP kernels of pack.hip, precompute.hip,
+// lut_mpgemm.hip and dequant_mfma.hip.
+#include <hip/hip_runtime.h>
+
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+
+#include "lutgemm_internal.h"
+
+using namespace lutgemm;
+
+namespace {
+
+constexpr int64_t MAX_M = int64_t(1) << 19;
+constexpr int64_t MAX_K = int64_t(1) << 20;
+constexpr int64_t MAX_N = int64_t(1) << 24;
+
+bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
+
+lutgemm_status_t check_problem(const lutgemm_problem_t *p, int64_t M) {
+    if (!p) return LUTGEMM_ERROR_INVALID_VALUE;
+    if (p->K <= 0 || p->N <= 0 || M <= 0 || p->reserved != 0) return LUTGEMM_ERROR_INVALID_VALUE;
+    if (p->wfmt < LUTGEMM_WFMT_UINT || p->wfmt > LUTGEMM_WFMT_TERNARY) return LUTGEMM_ERROR_INVALID_VALUE;
+    if (p->act != LUTGEMM_ACT_FP16 && p->act != LUTGEMM_ACT_INT8) return LUTGEMM_ERROR_INVALID_VALUE;
+    if (p->scale_fp32 != 0 && p->scale_fp32 != 1) return LUTGEMM_ERROR_INVALID_VALUE;
+    if (p->w_bits <= 0 || p->group_size < 0) return LUTGEMM_ERROR_INVALID_VALUE;
+    if (p->K > MAX_K || p->N > MAX_N || M > MAX_M) return LUTGEMM_ERROR_NOT_SUPPORTED;
+    if (p->K % KBLK != 0) return LUTGEMM_ERROR_NOT_SUPPORTED;
+    if (p->group_size != 0 && (p->group_size % KBLK != 0 || p->K % p->group_size != 0))
+        return LUTGEMM_ERROR_NOT_SUPPORTED;
+    switch (p->wfmt) {
+    case LUTGEMM_WFMT_UINT:
+        if (p->w_bits != 1 && p->w_bits != 2 && p->w_bits != 4) return LUTGEMM_ERROR_NOT_SUPPORTED;
+        if (p->scale_fp32) return LUTGEMM_ERROR_NOT_SUPPORTED;
+        break;
+    case LUTGEMM_WFMT_BINARY:
+        if (p->w_bits != 1) return LUTGEMM_ERROR_NOT_SUPPORTED;
+        break;
+    default:
+        if (p->w_bits != 2) return LUTGEMM_ERROR_NOT_SUPPORTED;
+        break;
+    }
+    if (p->scale_fp32 && p->group_size != 0) return LUTGEMM_ERROR_NOT_SUPPORTED;
+    if (p->act == LUTGEMM_ACT_INT8) {
+        if (p->wfmt == LUTGEMM_WFMT_UINT) return LUTGEMM_ERROR_NOT_SUPPORTED;
+        if (p->group_size != 0 && p->group_size != p->K) return LUTGEMM_ERROR_NOT_SUPPORTED;
+    }
+    return LUTGEMM_SUCCESS;
+}
+
+int env_int(const char *name, int dflt) {
+    const char *v = std::getenv(name);
+    if (!v || !*v) return dflt;
+    return std::atoi(v);
+}
+
+lutgemm_status_t hip_status(int e) { return e == 0 ? LUTGEMM_SUCCESS : LUTGEMM_ERROR_HIP; }
+
+}  // namespace
+
+namespace lutgemm {
+
+// Work decomposition.  One lane per column; a workgroup covers 256 columns.
+// Single-token GEMV: KBS 128-blocks of K per workgroup (all its weight words are
+// loaded up front, at most 8 per lane), halved until the grid holds about four
+// workgroups per CU.  Several tokens: MT tokens per workgroup, K split only when
+// the token x column grid is smaller than that.
+LutPlan plan_lut(const Layout &L, int64_t M) {
+    LutPlan P{};
+    P.n_tiles = L.N_pad / NTILE;
+    const int64_t target = env_int("LUTGEMM_TARGET_BLOCKS", 1024);
+    if (M <= 2) {
+        P.kind = 0;
+        P.mt = 1;
+        P.m_tiles = M;
+        int kbs = 8 / L.bits;
+        const int forced = env_int("LUTGEMM_KBS", 0);
+        if (forced == 1 || forced == 2 || forced == 4 || forced == 8) {
+            kbs = forced > 8 / L.bits ? 8 / L.bits : forced;
+        } else {
+            while (kbs > 1 && P.n_tiles * M * ((L.KB + kbs - 1) / kbs) < target) kbs >>= 1;
+        }
+        P.kbs = kbs;
+        P.splits = (int)((L.KB + kbs - 1) / kbs);
+    } else {
+        P.kind = 1;
+        P.mt = (M <= 4 || L.bits == 4) ? 4 : 8;
+        P.m_tiles = (M + P.mt - 1) / P.mt;
+        const int64_t base = P.n_tiles * P.m_tiles;
+        int64_t splits = 1;
+        if (base < target) splits = (target + base - 1) / base;
+        const int64_t max_splits = (L.KB + 1) / 2;  // at least two 128-blocks per split
+        if (splits > max_splits) splits = max_splits;
+        if (splits < 1) splits = 1;
+        int64_t kbs = (L.KB + splits - 1) / splits;
+        kbs = (kbs + 1) / 2 * 2;
+        P.kbs = (int)kbs;
+        P.splits = (int)((L.KB + kbs - 1) / kbs);
+    }
+    if (P.splits > 1) {
+        P.ws_counters_bytes = align256((size_t)P.m_tiles * P.n_tiles * 4);
+        P.ws_partials_off = P.ws_counters_bytes;
+        P.ws_bytes = P.ws_partials_off + align256((size_t)P.splits * P.m_tiles * P.mt * L.N_pad * 4);
+    } else {
+        P.ws_counters_bytes = P.ws_partials_off = P.ws_bytes = 0;
+    }
+    return P;
+}
+
+}  // namespace lutgemm
+
+extern "C" {
+
+const char *lutgemm_status_string(lutgemm_status_t s) {
+    switch (s) {
+    case LUTGEMM_SUCCESS: return "LUTGEMM_SUCCESS";
+    case LUTGEMM_ERROR_INVALID_VALUE: return "LUTGEMM_ERROR_INVALID_VALUE";
+    case LUTGEMM_ERROR_NOT_SUPPORTED: return "LUTGEMM_ERROR_NOT_SUPPORTED";
+    case LUTGEMM_ERROR_INSUFFICIENT_SIZE: return "LUTGEMM_ERROR_INSUFFICIENT_SIZE";
+    case LUTGEMM_ERROR_HIP: return "LUTGEMM_ERROR_HIP";
+    }
+    return "LUTGEMM_UNKNOWN_STATUS";
+}
+
+const char *lutgemm_version(void) { return "lutgemm-gfx950 0.1.0"; }
+
+lutgemm_status_t lutgemm_validate(const lutgemm_problem_t *problem, int64_t M) {
+    return check_problem(problem, M);
+}
+
+size_t lutgemm_packed_weight_size(const lutgemm_problem_t *problem) {
+    if (check_problem(problem, 1) != LUTGEMM_SUCCESS) return 0;
+    return make_layout(*problem).packed_bytes;
+}
+
+size_t lutgemm_table_size(const lutgemm_problem_t *problem, int64_t M) {
+    if (check_problem(problem, M) != LUTGEMM_SUCCESS) return 0;
+    return make_table_layout(make_layout(*problem), M).total;
+}
+
+lutgemm_status_t lutgemm_table_offsets(const lutgemm_problem_t *problem, int64_t M, size_t *s_offset,
+                                       size_t *t_offset) {
+    lutgemm_status_t st = check_problem(problem, M);
+    if (st != LUTGEMM_SUCCESS) return st;
+    if (!s_offset || !t_offset) return LUTGEMM_ERROR_INVALID_VALUE;
+    TableLayout T = make_table_layout(make_layout(*problem), M);
+    *s_offset = T.s_off;
+    *t_offset = T.tok_off;
+    return LUTGEMM_SUCCESS;
+}
+
+size_t lutgemm_workspace_size(const lutgemm_problem_t *problem, int64_t M) {
+    if (check_problem(problem, M) != LUTGEMM_SUCCESS) return 0;
+    Layout L = make_layout(*problem);
+    return plan_lut(L, M).ws_bytes;
+}
+
+lutgemm_status_t lutgemm_pack_weights(const lutgemm_problem_t *problem, const void *codes,
+                                      const void *scales, const void *zeros, void *packed,
+                                      size_t packed_bytes, void *stream) {
+    lutgemm_status_t st = check_problem(problem, 1);
+    if (st != LUTGEMM_SUCCESS) return st;
+    if (!codes || !scales || !packed) return LUTGEMM_ERROR_INVALID_VALUE;
+    if (problem->wfmt == LUTGEMM_WFMT_UINT && !zeros) return LUTGEMM_ERROR_INVALID_VALUE;
+    if (!aligned16(codes) || !aligned16(scales) || !aligned16(packed)) return LUTGEMM_ERROR_INVALID_VALUE;
+    if (problem->wfmt == LUTGEMM_WFMT_UINT && !aligned16(zeros)) return LUTGEMM_ERROR_INVALID_VALUE;
+    Layout L = make_layout(*problem);
+    if (packed_bytes < L.packed_bytes) return LUTGEMM_ERROR_INSUFFICIENT_SIZE;
+    PackParams pp{};
+    pp.codes = codes;
+    pp.scales = scales;
+    pp.zeros = problem->wfmt == LUTGEMM_WFMT_UINT ? zeros : nullptr;
+    pp.planes = (uint4 *)packed;
+    pp.meta = (char *)packed + L.meta_off;
+    pp.K = L.K;
+    pp.N = L.N;
+    pp.N_pad = L.N_pad;
+    pp.KB = L.KB;
+    pp.Q = L.Q;
+    pp.G = L.G;
+    pp.bits = L.bits;
+    pp.wfmt = L.wfmt;
+    pp.per_tensor = L.per_tensor ? 1 : 0;
+    pp.scale_fp32 = problem->scale_fp32;
+    return hip_status(launch_pack(pp, stream));
+}
+
+lutgemm_status_t lutgemm_precompute(const lutgemm_problem_t *problem, int64_t M, const void *act,
+                                    void *tables, size_t table_bytes, void *stream) {
+    lutgemm_status_t st = check_problem(problem, M);
+    if (st != LUTGEMM_SUCCESS) return st;
+    if (!act || !tables || !aligned16(act) || !aligned16(tables)) return LUTGEMM_ERROR_INVALID_VALUE;
+    Layout L = make_layout(*problem);
+    TableLayout T = make_table_layout(L, M);
+    if (table_bytes < T.total) return LUTGEMM_ERROR_INSUFFICIENT_SIZE;
+    PrecomputeParams pp{};
+    pp.act = (const uint16_t *)act;
+    pp.T = (uint4 *)tables;
+    pp.S = (char *)tables + T.s_off;
+    pp.tok = (float *)((char *)tables + T.tok_off);
+    pp.M = M;
+    pp.K = L.K;
+    pp.J = L.J;
+    pp.Q = L.Q;
+    pp.G = L.G;
+    return hip_status(launch_precompute(pp, L.act == LUTGEMM_ACT_INT8, stream));
+}
+
+lutgemm_status_t lutgemm_mpgemm(const lutgemm_problem_t *problem, int64_t M, const void *tables,
+                                const void *packed, void *out, int32_t out_dtype, int32_t accumulate,
+                                void *workspace, size_t workspace_bytes, void *stream) {
+    lutgemm_status_t st = check_problem(problem, M);
+    if (st != LUTGEMM_SUCCESS) return st;
+    if (!tables || !packed || !out) return LUTGEMM_ERROR_INVALID_VALUE;
+    if (!aligned16(tables) || !aligned16(packed) || !aligned16(out)) return LUTGEMM_ERROR_INVALID_VALUE;
+    if (out_dtype != LUTGEMM_OUT_FP16 && out_dtype != LUTGEMM_OUT_FP32 && out_dtype != LUTGEMM_OUT_INT32)
+        return LUTGEMM_ERROR_INVALID_VALUE;
+    if (out_dtype == LUTGEMM_OUT_INT32 && problem->act != LUTGEMM_ACT_INT8) return LUTGEMM_ERROR_NOT_SUPPORTED;
+    if (accumulate != 0 && accumulate != 1) return LUTGEMM_ERROR_INVALID_VALUE;
+    Layout L = make_layout(*problem);
+    LutPlan plan = plan_lut(L, M);
+    if (plan.ws_bytes > 0) {
+        if (!workspace || !aligned16(workspace)) return LUTGEMM_ERROR_INVALID_VALUE;
+        if (workspace_bytes < plan.ws_bytes) return LUTGEMM_ERROR_INSUFFICIENT_SIZE;
+    }
+    TableLayout T = make_table_layout(L, M);
+    LutParams lp{};
+    lp.T = (const uint4 *)tables;
+    lp.S = (const char *)tables + T.s_off;
+    lp.tok = (const float *)((const char *)tables + T.tok_off);
+    lp.planes = (const uint4 *)packed;
+    lp.meta = (const char *)packed + L.meta_off;
+    lp.out = out;
+    lp.part = plan.ws_bytes ? (float *)((char *)workspace + plan.ws_partials_off) : nullptr;
+    lp.counters = plan.ws_bytes ? (uint32_t *)workspace : nullptr;
+    lp.M = M;
+    lp.N = L.N;
+    lp.N_pad = L.N_pad;
+    lp.K = L.K;
+    lp.KB = L.KB;
+    lp.J = L.J;
+    lp.Q = L.Q;
+    lp.G = L.G;
+    lp.splits = plan.splits;
+    lp.kbs = plan.kbs;
+    lp.kpg = (int)(L.G / KBLK);
+    lp.per_tensor = L.per_tensor ? 1 : 0;
+    if (L.wfmt == LUTGEMM_WFMT_BINARY) {  // codes {0,1} read as {-1,+1}: s' = s, z' = 0
+        lp.cs = 1.f;
+        lp.cz = 0.f;
+        lp.c0 = 0.f;
+    } else if (L.wfmt == LUTGEMM_WFMT_TERNARY) {  // q = w + 1, z = 1, b = 2: s' = s/2, z' = -1
+        lp.cs = 0.5f;
+        lp.cz = 0.f;
+        lp.c0 = -1.f;
+    } else {  // Eq. 2: s' = s/2, z' = 2z + 1 - 2^b
+        lp.cs = 0.5f;
+        lp.cz = 2.f;
+        lp.c0 = 1.f - (float)(1 << L.bits);
+    }
+    lp.out_dtype = out_dtype;
+    lp.accumulate = accumulate;
+    if (env_int("LUTGEMM_LOG", 0))
+        std::fprintf(stderr, "lutgemm_mpgemm: M=%lld K=%lld N=%lld b=%d kind=%d kbs=%d splits=%d mt=%d grid=%lldx%dx%lld\n",
+                     (long long)M, (long long)L.K, (long long)L.N, L.bits, plan.kind, plan.kbs, plan.splits,
+                     plan.mt, (long long)plan.n_tiles, plan.splits, (long long)plan.m_tiles);
+    return hip_status(launch_lut(lp, L, plan, stream));
+}
+
+lutgemm_status_t lutgemm_mpgemm_dequant(const lutgemm_problem_t *problem, int64_t M, const void *act,
+                                        const void *packed, void *out, int32_t out_dtype,
+                                        int32_t accumulate, void *stream) {
+    lutgemm_status_t st = check_problem(problem, M);
+    if (st != LUTGEMM_SUCCESS) return st;
+    if (problem->act != LUTGEMM_ACT_FP16) return LUTGEMM_ERROR_NOT_SUPPORTED;
+    if (!act || !packed || !out) return LUTGEMM_ERROR_INVALID_VALUE;
+    if (!aligned16(act) || !aligned16(packed) || !aligned16(out)) return LUTGEMM_ERROR_INVALID_VALUE;
+    if (out_dtype != LUTGEMM_OUT_FP16 && out_dtype != LUTGEMM_OUT_FP32) return LUTGEMM_ERROR_INVALID_VALUE;
+    if (accumulate != 0 && accumulate != 1) return LUTGEMM_ERROR_INVALID_VALUE;
+    Layout L = make_layout(*problem);
+    DequantParams dp{};
+    dp.act = (const uint16_t *)act;
+    dp.planes = (const uint4 *)packed;
+    dp.meta = (const char *)packed + L.meta_off;
+    dp.out = out;
+    dp.M = M;
+    dp.N = L.N;
+    dp.N_pad = L.N_pad;
+    dp.K = L.K;
+    dp.KB = L.KB;
+    dp.Q = L.Q;
+    dp.G = L.G;
+    dp.out_dtype = out_dtype;
+    dp.accumulate = accumulate;
+    return hip_status(launch_dequant(dp, L, stream));
+}
+
+}  // extern "C"

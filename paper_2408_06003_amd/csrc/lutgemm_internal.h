@@ -1,0 +1,136 @@
+// Internal definitions shared by the host library and the HIP kernels.
+//
+// Packed-weight layout (opaque to callers, owned by this library):
+//   planes: [KB][b][N_pad] x 16 bytes, KB = K/128.  One 16-byte word holds the
+//           32 four-bit table indices of one bit-plane of one column over 128
+//           consecutive k (4-bit index i covers k = 128 kb + 4 i .. + 3, stored
+//           at bits 4(i % 8) of 32-bit word i / 8).  An index is the pattern of
+//           the plane's bits over those 4 weights, first weight as MSB, with the
+//           low 3 bits inverted when the MSB is set (Eq. 6): bit 3 = sign,
+//           bits 0-2 = half-table row.  Columns n >= N are zero words.
+//   meta:   per-group scales: [Q][N_pad] x (FP16 s, FP16 z) pairs (z = 0 unless
+//           UINT); per-tensor: two FP32 values (s, z).  Stored as given; the
+//           reinterpretation of Eq. 2 is applied in FP32 where they are used.
+// Consecutive columns are adjacent in memory so that a wavefront whose lanes are
+// 64 consecutive columns reads 1 KiB contiguous with 128-bit loads.
+#pragma once
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include "../../include/lutgemm.h"
+
+namespace lutgemm {
+
+constexpr int KBLK = 128;       // activations covered by one packed plane word
+constexpr int GPB = 32;         // 4-activation table groups per plane word
+constexpr int NTILE = 256;      // columns per workgroup (one column per lane)
+constexpr int FIX_SHIFT = 20;   // fixed-point fraction bits of FP table entries staged in LDS
+
+struct Layout {
+    int64_t K, N, N_pad, KB, J, Q, G;  // G = group size (K when per-tensor)
+    int bits, wfmt, act;
+    bool per_tensor;
+    size_t planes_bytes, meta_off, meta_bytes, packed_bytes;
+};
+
+inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+inline Layout make_layout(const lutgemm_problem_t &p) {
+    Layout L{};
+    L.K = p.K;
+    L.N = p.N;
+    L.N_pad = (p.N + NTILE - 1) / NTILE * NTILE;
+    L.KB = p.K / KBLK;
+    L.J = p.K / 4;
+    L.per_tensor = p.group_size == 0;
+    L.G = p.group_size ? p.group_size : p.K;
+    L.Q = p.group_size ? p.K / p.group_size : 1;
+    L.bits = p.w_bits;
+    L.wfmt = p.wfmt;
+    L.act = p.act;
+    L.planes_bytes = (size_t)L.KB * L.bits * L.N_pad * 16;
+    L.meta_off = align256(L.planes_bytes);
+    L.meta_bytes = L.per_tensor ? 256 : (size_t)L.Q * L.N_pad * 4;
+    L.packed_bytes = L.meta_off + align256(L.meta_bytes);
+    return L;
+}
+
+struct TableLayout {
+    size_t t_bytes, s_off, tok_off, total;
+};
+
+inline TableLayout make_table_layout(const Layout &L, int64_t M) {
+    TableLayout T{};
+    T.t_bytes = (size_t)M * L.J * 16;
+    T.s_off = align256(T.t_bytes);
+    T.tok_off = align256(T.s_off + (size_t)M * L.Q * 4);
+    T.total = align256(T.tok_off + (size_t)M * 4);
+    return T;
+}
+
+// Launch plan of the LUT mpGEMM for (problem, M).
+struct LutPlan {
+    int kind;        // 0: single-token GEMV kernel, 1: multi-token kernel
+    int kbs;         // 128-blocks of K per split
+    int splits;      // K splits (1 = no workspace)
+    int mt;          // tokens per workgroup (multi-token kernel)
+    int64_t m_tiles; // token tiles
+    int64_t n_tiles; // column tiles
+    size_t ws_counters_bytes, ws_partials_off, ws_bytes;
+};
+
+LutPlan plan_lut(const Layout &L, int64_t M);
+
+// Kernel parameter blocks.
+struct PackParams {
+    const void *codes;
+    const void *scales;
+    const void *zeros;
+    uint4 *planes;
+    void *meta;
+    int64_t K, N, N_pad, KB, Q, G;
+    int bits, wfmt, per_tensor, scale_fp32;
+};
+
+struct PrecomputeParams {
+    const uint16_t *act;   // FP16 bits [M][K]
+    uint4 *T;              // [M][J] x 8 entries
+    void *S;               // [M][Q]
+    float *tok;            // [M]
+    int64_t M, K, J, Q, G;
+};
+
+struct LutParams {
+    const uint4 *T;        // half tables
+    const void *S;         // group sums
+    const float *tok;      // per-token factor
+    const uint4 *planes;
+    const void *meta;
+    void *out;
+    float *part;           // split partial sums [splits][M][N_pad] (float or int bits)
+    uint32_t *counters;    // [m_tiles][n_tiles]
+    int64_t M, N, N_pad, K, KB, J, Q, G;
+    int splits, kbs, out_dtype, accumulate;
+    int kpg;               // 128-blocks of K per quantization group (G / 128)
+    int per_tensor;        // one (s, z) pair for the whole tensor, FP32
+    // Eq. 2 for the weight format: s' = cs * s, z' = cz * z + c0
+    float cs, cz, c0;
+};
+
+struct DequantParams {
+    const uint16_t *act;   // FP16 [M][K]
+    const uint4 *planes;
+    const void *meta;
+    void *out;
+    int64_t M, N, N_pad, K, KB, Q, G;
+    int out_dtype, accumulate;
+};
+
+// Launchers (return hipError_t as int).
+int launch_pack(const PackParams &p, void *stream);
+int launch_precompute(const PrecomputeParams &p, int act_int8, void *stream);
+int launch_lut(const LutParams &p, const Layout &L, const LutPlan &plan, void *stream);
+int launch_dequant(const DequantParams &p, const Layout &L, void *stream);
+
+}  // namespace lutgemm

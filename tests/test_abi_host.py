@@ -1,0 +1,129 @@
+"""Host-only checks of the C ABI: the library loads, exports every declared symbol,
+and validates arguments before launching anything.  No GPU is touched: every call
+here returns from host-side validation (size queries, invalid or unsupported
+arguments), so these run in the CPU suite."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "lutgemm.h")
+
+L = pytest.importorskip("paper_2408_06003_amd")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(lutgemm_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported():
+    names = declared_functions()
+    assert len(names) >= 11
+    for name in names:
+        assert hasattr(L.lib, name), f"{name} declared in lutgemm.h but not exported"
+    assert sorted(L.EXPORTS) == names
+
+
+def test_version_and_status_strings():
+    assert "gfx950" in L.version()
+    for s in range(5):
+        assert L.status_string(s).startswith("LUTGEMM_")
+    assert L.status_string(99) == "LUTGEMM_UNKNOWN_STATUS"
+
+
+def test_problem_struct_layout():
+    assert ctypes.sizeof(L.Problem) == 40
+
+
+@pytest.mark.parametrize("K,N,b,wfmt,G,act,fp32,expect", [
+    (4096, 4096, 2, L.WFMT_TERNARY, 0, L.ACT_INT8, True, L.SUCCESS),
+    (1024, 1024, 2, L.WFMT_UINT, 128, L.ACT_FP16, False, L.SUCCESS),
+    (11008, 4096, 4, L.WFMT_UINT, 128, L.ACT_FP16, False, L.SUCCESS),
+    (8192, 28672, 1, L.WFMT_BINARY, 8192, L.ACT_FP16, False, L.SUCCESS),
+    (8192, 100, 1, L.WFMT_BINARY, 8192, L.ACT_INT8, False, L.SUCCESS),
+    (1000, 64, 2, L.WFMT_UINT, 0, L.ACT_FP16, False, L.ERROR_NOT_SUPPORTED),      # K % 128
+    (1024, 64, 2, L.WFMT_UINT, 64, L.ACT_FP16, False, L.ERROR_NOT_SUPPORTED),     # G % 128
+    (1024, 64, 2, L.WFMT_UINT, 384, L.ACT_FP16, False, L.ERROR_NOT_SUPPORTED),    # K % G
+    (1024, 64, 3, L.WFMT_UINT, 128, L.ACT_FP16, False, L.ERROR_NOT_SUPPORTED),    # b = 3
+    (1024, 64, 2, L.WFMT_BINARY, 128, L.ACT_FP16, False, L.ERROR_NOT_SUPPORTED),  # binary is 1 bit
+    (1024, 64, 1, L.WFMT_TERNARY, 128, L.ACT_FP16, False, L.ERROR_NOT_SUPPORTED), # ternary is 2 bits
+    (1024, 64, 2, L.WFMT_UINT, 0, L.ACT_FP16, True, L.ERROR_NOT_SUPPORTED),       # fp32 scale needs no zero
+    (1024, 64, 2, L.WFMT_TERNARY, 128, L.ACT_FP16, True, L.ERROR_NOT_SUPPORTED),  # fp32 scale per-tensor only
+    (1024, 64, 2, L.WFMT_UINT, 128, L.ACT_INT8, False, L.ERROR_NOT_SUPPORTED),    # INT8 act needs int weights
+    (1024, 64, 2, L.WFMT_TERNARY, 128, L.ACT_INT8, False, L.ERROR_NOT_SUPPORTED), # INT8 act: per-channel at most
+    (0, 64, 2, L.WFMT_UINT, 0, L.ACT_FP16, False, L.ERROR_INVALID_VALUE),
+    (1024, 0, 2, L.WFMT_UINT, 0, L.ACT_FP16, False, L.ERROR_INVALID_VALUE),
+    (1024, 64, 2, 7, 0, L.ACT_FP16, False, L.ERROR_INVALID_VALUE),
+    (1024, 64, 2, L.WFMT_UINT, 0, 5, False, L.ERROR_INVALID_VALUE),
+    (1024, 64, 0, L.WFMT_UINT, 0, L.ACT_FP16, False, L.ERROR_INVALID_VALUE),
+    (1024, 64, 2, L.WFMT_UINT, -128, L.ACT_FP16, False, L.ERROR_INVALID_VALUE),
+])
+def test_validate(K, N, b, wfmt, G, act, fp32, expect):
+    p = L.problem(K, N, b, wfmt, G, act, fp32)
+    assert L.validate(p, 1) == expect
+    if expect == L.SUCCESS:
+        assert L.packed_weight_size(p) > 0 and L.table_size(p, 3) > 0
+    else:
+        assert L.packed_weight_size(p) == 0 and L.table_size(p, 1) == 0 and L.workspace_size(p, 1) == 0
+
+
+def test_validate_m_and_reserved():
+    p = L.problem(1024, 64, 2, L.WFMT_UINT, 128)
+    assert L.validate(p, 0) == L.ERROR_INVALID_VALUE
+    assert L.validate(p, -3) == L.ERROR_INVALID_VALUE
+    assert L.validate(p, 1 << 20) == L.ERROR_NOT_SUPPORTED
+    p.reserved = 1
+    assert L.validate(p, 1) == L.ERROR_INVALID_VALUE
+    assert L.lib.lutgemm_validate(None, 1) == L.ERROR_INVALID_VALUE
+
+
+def test_size_formulas():
+    """Eq. 7-8 read as storage sizes: tables are 2^(4-1) entries of 16 bits per 4 activations
+    and token; grouped binary weights are K x N x b bits (plus alignment of N and metadata)."""
+    M, K, N = 3, 4096, 1000
+    p = L.problem(K, N, 4, L.WFMT_UINT, 128)
+    s_off, t_off = L.table_offsets(p, M)
+    assert s_off >= M * (K // 4) * 8 * 2 and s_off % 256 == 0
+    assert t_off >= s_off + M * (K // 128) * 4 and t_off % 256 == 0
+    assert L.table_size(p, M) >= t_off + 4 * M
+    n_pad = 1024
+    planes = K * n_pad * 4 // 8
+    assert planes <= L.packed_weight_size(p) <= planes + (K // 128) * n_pad * 4 + 512
+
+
+def test_entry_points_reject_before_launch():
+    """Invalid pointers / sizes are rejected on the host; nothing reaches the GPU."""
+    p = L.problem(1024, 256, 2, L.WFMT_UINT, 128)
+    ok = 1 << 20  # an aligned fake address, never dereferenced because validation fails first
+    f = L.lib
+    bp = ctypes.byref(p)
+    big = 1 << 40
+    # null pointers
+    assert f.lutgemm_pack_weights(bp, None, ok, ok, ok, big, None) == L.ERROR_INVALID_VALUE
+    assert f.lutgemm_pack_weights(bp, ok, ok, None, ok, big, None) == L.ERROR_INVALID_VALUE  # UINT needs zeros
+    assert f.lutgemm_precompute(bp, 1, None, ok, big, None) == L.ERROR_INVALID_VALUE
+    assert f.lutgemm_mpgemm(bp, 1, ok, ok, None, L.OUT_FP16, 0, ok, big, None) == L.ERROR_INVALID_VALUE
+    # misaligned pointers
+    assert f.lutgemm_pack_weights(bp, ok + 4, ok, ok, ok, big, None) == L.ERROR_INVALID_VALUE
+    assert f.lutgemm_precompute(bp, 1, ok, ok + 8, big, None) == L.ERROR_INVALID_VALUE
+    assert f.lutgemm_mpgemm_dequant(bp, 1, ok + 2, ok, ok, L.OUT_FP16, 0, None) == L.ERROR_INVALID_VALUE
+    # too-small buffers
+    assert f.lutgemm_pack_weights(bp, ok, ok, ok, ok, 16, None) == L.ERROR_INSUFFICIENT_SIZE
+    assert f.lutgemm_precompute(bp, 1, ok, ok, 16, None) == L.ERROR_INSUFFICIENT_SIZE
+    # bad enums / unsupported output
+    assert f.lutgemm_mpgemm(bp, 1, ok, ok, ok, 9, 0, ok, big, None) == L.ERROR_INVALID_VALUE
+    assert f.lutgemm_mpgemm(bp, 1, ok, ok, ok, L.OUT_INT32, 0, ok, big, None) == L.ERROR_NOT_SUPPORTED
+    assert f.lutgemm_mpgemm(bp, 1, ok, ok, ok, L.OUT_FP16, 2, ok, big, None) == L.ERROR_INVALID_VALUE
+    assert f.lutgemm_mpgemm_dequant(bp, 1, ok, ok, ok, L.OUT_INT32, 0, None) == L.ERROR_INVALID_VALUE
+    pi = L.problem(1024, 256, 2, L.WFMT_TERNARY, 0, L.ACT_INT8, True)
+    assert f.lutgemm_mpgemm_dequant(ctypes.byref(pi), 1, ok, ok, ok, L.OUT_FP16, 0, None) == L.ERROR_NOT_SUPPORTED
+    # workspace required but missing / too small
+    pw = L.problem(4096, 4096, 2, L.WFMT_TERNARY, 0, L.ACT_INT8, True)
+    need = L.workspace_size(pw, 1)
+    assert need > 0
+    assert f.lutgemm_mpgemm(ctypes.byref(pw), 1, ok, ok, ok, L.OUT_INT32, 0, None, need, None) == L.ERROR_INVALID_VALUE
+    assert f.lutgemm_mpgemm(ctypes.byref(pw), 1, ok, ok, ok, L.OUT_INT32, 0, ok, need - 1, None) == L.ERROR_INSUFFICIENT_SIZE
