@@ -98,6 +98,10 @@ const char *lutgemm_status_string(lutgemm_status_t status);
 /* Library version string. */
 const char *lutgemm_version(void);
 
+/* Text of the HIP error behind the calling thread's most recent
+ * LUTGEMM_ERROR_HIP ("" if none).  Valid until the thread's next call. */
+const char *lutgemm_last_error(void);
+
 /*
  * Host-only check of a problem and token count M (M >= 1; pass M = 1 when M does
  * not matter).  Needs no GPU.  Returns LUTGEMM_ERROR_INVALID_VALUE for malformed

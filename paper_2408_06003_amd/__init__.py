@@ -16,6 +16,11 @@ import ctypes
 import os
 from typing import Optional
 
+# Load PyTorch's HIP runtime before the library: liblutgemm.so needs
+# libamdhip64.so.7, and the dynamic loader then binds it to the runtime already
+# in the process, so torch's streams and allocations are valid in our calls.
+import torch  # noqa: F401
+
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "liblutgemm.so")
 
@@ -26,7 +31,7 @@ ACT_FP16, ACT_INT8 = 0, 1
 OUT_FP16, OUT_FP32, OUT_INT32 = 0, 1, 2
 
 EXPORTS = [
-    "lutgemm_status_string", "lutgemm_version", "lutgemm_validate", "lutgemm_packed_weight_size",
+    "lutgemm_status_string", "lutgemm_version", "lutgemm_last_error", "lutgemm_validate", "lutgemm_packed_weight_size",
     "lutgemm_table_size", "lutgemm_table_offsets", "lutgemm_workspace_size", "lutgemm_pack_weights",
     "lutgemm_precompute", "lutgemm_mpgemm", "lutgemm_mpgemm_dequant",
 ]
@@ -45,7 +50,10 @@ class Problem(ctypes.Structure):
 
 class LutGemmError(RuntimeError):
     def __init__(self, status: int, where: str):
-        super().__init__(f"{where}: {status_string(status)}")
+        msg = f"{where}: {status_string(status)}"
+        if status == ERROR_HIP:
+            msg += f" [{lib.lutgemm_last_error().decode()}]"
+        super().__init__(msg)
         self.status = status
 
 
@@ -60,6 +68,8 @@ def _load():
     L.lutgemm_status_string.argtypes = [ctypes.c_int]
     L.lutgemm_version.restype = ctypes.c_char_p
     L.lutgemm_version.argtypes = []
+    L.lutgemm_last_error.restype = ctypes.c_char_p
+    L.lutgemm_last_error.argtypes = []
     L.lutgemm_validate.restype = ctypes.c_int
     L.lutgemm_validate.argtypes = [PP, I64]
     L.lutgemm_packed_weight_size.restype = SZ

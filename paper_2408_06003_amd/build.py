@@ -4,7 +4,8 @@ Every HIP source is compiled to an object under ``_build/`` and linked into
 ``paper_2408_06003_amd/liblutgemm.so``.  Flags: -O3, no FP contraction (the
 INT8 activation quantizer and the FP32 output rounding must follow the
 definition exactly), correctly rounded FP32 division, and packed-FP32
-instructions disabled.
+instructions disabled; code object version 5, which every ROCm 7 runtime
+(including the one bundled with PyTorch) loads.
 """
 from __future__ import annotations
 
@@ -22,7 +23,7 @@ SOURCES = ["api.cpp", "pack.hip", "precompute.hip", "lut_mpgemm.hip", "dequant_m
 ARCH = "gfx950"
 
 COMMON = [
-    "-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
+    "-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-mcode-object-version=5",
     "-ffp-contract=off", "-fhip-fp32-correctly-rounded-divide-sqrt",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-Wno-unused-command-line-argument",
@@ -46,7 +47,7 @@ def build(verbose: bool = True) -> str:
     with cf.ThreadPoolExecutor(max_workers=min(len(SOURCES), os.cpu_count() or 4)) as ex:
         objs = list(ex.map(_compile, SOURCES))
     tmp = LIB + ".tmp"
-    cmd = ["hipcc", f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs]
+    cmd = ["hipcc", f"--offload-arch={ARCH}", "-mcode-object-version=5", "-shared", "-fPIC", "-o", tmp, *objs]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"link failed:\n{r.stdout}\n{r.stderr}")

@@ -57,7 +57,14 @@ int env_int(const char *name, int dflt) {
     return std::atoi(v);
 }
 
-lutgemm_status_t hip_status(int e) { return e == 0 ? LUTGEMM_SUCCESS : LUTGEMM_ERROR_HIP; }
+thread_local char g_last_error[256] = "";
+
+lutgemm_status_t hip_status(int e) {
+    if (e == 0) return LUTGEMM_SUCCESS;
+    std::snprintf(g_last_error, sizeof(g_last_error), "%s (hipError_t %d)",
+                  hipGetErrorString((hipError_t)e), e);
+    return LUTGEMM_ERROR_HIP;
+}
 
 }  // namespace
 
@@ -126,6 +133,8 @@ const char *lutgemm_status_string(lutgemm_status_t s) {
 }
 
 const char *lutgemm_version(void) { return "lutgemm-gfx950 0.1.0"; }
+
+const char *lutgemm_last_error(void) { return g_last_error; }
 
 lutgemm_status_t lutgemm_validate(const lutgemm_problem_t *problem, int64_t M) {
     return check_problem(problem, M);

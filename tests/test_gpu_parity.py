@@ -98,7 +98,7 @@ FULL = [(cid, sid, M, K, N) for cid, w in W.WORKLOADS.items() for (sid, M, K, N)
 @pytest.mark.parametrize("cid,sid,M,K,N", FULL)
 def test_full_size_sampled(cid, sid, M, K, N):
     banner(f"full size config={cid} shape={sid} M={M} K={K} N={N}")
-    inp = W.make_inputs(cid, sid)
+    inp = W.make_inputs(cid, sid, M=M)
     gp = GpuProblem(inp)
     if inp.act_kind == W.ACT_INT8:
         check_int_path(gp)                            # all outputs, bit-exact
