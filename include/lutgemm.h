@@ -139,10 +139,9 @@ lutgemm_status_t lutgemm_table_offsets(const lutgemm_problem_t *problem, int64_t
                                        size_t *s_offset, size_t *t_offset);
 
 /*
- * Bytes of scratch memory lutgemm_mpgemm needs for M tokens (split-K partial
- * sums and arrival counters); may be 0.  The workspace must be zero-filled
- * before its first use; every completed call leaves its counters at zero again,
- * so a workspace can be reused by later calls on the same stream.
+ * Bytes of scratch memory lutgemm_mpgemm needs for M tokens (partial sums when
+ * K is split across workgroups); may be 0.  No initialization is required; a
+ * workspace must not be shared by calls that run concurrently.
  */
 size_t lutgemm_workspace_size(const lutgemm_problem_t *problem, int64_t M);
 
@@ -203,6 +202,18 @@ lutgemm_status_t lutgemm_mpgemm(const lutgemm_problem_t *problem, int64_t M, con
 lutgemm_status_t lutgemm_mpgemm_dequant(const lutgemm_problem_t *problem, int64_t M,
                                         const void *act, const void *packed, void *out,
                                         int32_t out_dtype, int32_t accumulate, void *stream);
+
+/*
+ * Measurement utility (not part of the method): reads `bytes` (rounded down to a
+ * multiple of 16) of device memory at `src` with 128-bit loads from `blocks`
+ * workgroups of 256 lanes and writes one 32-bit word per workgroup to `sink`
+ * (device, >= 4 * blocks bytes).  Timing it on the byte counts of an mpGEMM call
+ * gives the achievable streaming-read bandwidth the LUT kernels are compared with.
+ * Returns LUTGEMM_ERROR_INVALID_VALUE for null or misaligned pointers, bytes < 16
+ * or blocks outside [1, 65536].
+ */
+lutgemm_status_t lutgemm_calibrate_stream_read(const void *src, size_t bytes, void *sink,
+                                               int32_t blocks, void *stream);
 
 #ifdef __cplusplus
 }

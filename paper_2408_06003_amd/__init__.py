@@ -33,7 +33,7 @@ OUT_FP16, OUT_FP32, OUT_INT32 = 0, 1, 2
 EXPORTS = [
     "lutgemm_status_string", "lutgemm_version", "lutgemm_last_error", "lutgemm_validate", "lutgemm_packed_weight_size",
     "lutgemm_table_size", "lutgemm_table_offsets", "lutgemm_workspace_size", "lutgemm_pack_weights",
-    "lutgemm_precompute", "lutgemm_mpgemm", "lutgemm_mpgemm_dequant",
+    "lutgemm_precompute", "lutgemm_mpgemm", "lutgemm_mpgemm_dequant", "lutgemm_calibrate_stream_read",
 ]
 
 
@@ -88,6 +88,8 @@ def _load():
     L.lutgemm_mpgemm.argtypes = [PP, I64, P, P, P, I32, I32, P, SZ, P]
     L.lutgemm_mpgemm_dequant.restype = ctypes.c_int
     L.lutgemm_mpgemm_dequant.argtypes = [PP, I64, P, P, P, I32, I32, P]
+    L.lutgemm_calibrate_stream_read.restype = ctypes.c_int
+    L.lutgemm_calibrate_stream_read.argtypes = [P, SZ, P, I32, P]
     return L
 
 
@@ -177,6 +179,12 @@ def mpgemm_dequant(p: Problem, M: int, act, packed, out, out_dtype: int, accumul
                    stream=None):
     _check(lib.lutgemm_mpgemm_dequant(ctypes.byref(p), M, _ptr(act), _ptr(packed), _ptr(out), out_dtype,
                                       1 if accumulate else 0, _stream(stream)), "lutgemm_mpgemm_dequant")
+
+
+def calibrate_stream_read(src, nbytes: int, sink, blocks: int, stream=None):
+    """Launch the streaming-read calibration kernel over ``nbytes`` of ``src``."""
+    _check(lib.lutgemm_calibrate_stream_read(_ptr(src), nbytes, _ptr(sink), blocks, _stream(stream)),
+           "lutgemm_calibrate_stream_read")
 
 
 class LutGemm:

@@ -70,35 +70,76 @@ lutgemm_status_t hip_status(int e) {
 
 namespace lutgemm {
 
-// Work decomposition.  One lane per column; a workgroup covers 256 columns.
-// Single-token GEMV: KBS 128-blocks of K per workgroup (all its weight words are
-// loaded up front, at most 8 per lane), halved until the grid holds about four
-// workgroups per CU.  Several tokens: MT tokens per workgroup, K split only when
-// the token x column grid is smaller than that.
+// Work decomposition.
+// Single token (M <= 2, one grid layer per token): the GEMV kernel of
+// lut_gemv.hip; pick the widest lane decomposition (most columns per workgroup,
+// i.e. most table reuse) that still gives at least `target` workgroups, and
+// split K across workgroups only when even the narrowest one does not.
+// Several tokens: MT tokens per workgroup of 256 columns, K split only when the
+// token x column grid is smaller than `target`.
 LutPlan plan_lut(const Layout &L, int64_t M) {
     LutPlan P{};
-    P.n_tiles = L.N_pad / NTILE;
-    const int64_t target = env_int("LUTGEMM_TARGET_BLOCKS", 1024);
-    if (M <= 2) {
+    const int64_t target = env_int("LUTGEMM_TARGET_BLOCKS", 256);
+    const int64_t weight_bytes = L.KB * L.bits * L.N * 16;
+    int kind = M > 2 ? 1 : (weight_bytes <= (int64_t)env_int("LUTGEMM_WHOLEK_MAX_KB", 6000) * 1000 ? 0 : 2);
+    const int forced_kind = env_int("LUTGEMM_GEMV_KIND", -1);
+    if (M <= 2 && (forced_kind == 0 || forced_kind == 2)) kind = forced_kind;
+    if (kind == 0) {
         P.kind = 0;
         P.mt = 1;
         P.m_tiles = M;
-        int kbs = 8 / L.bits;
+        // (columns per workgroup, 128-blocks per chunk) of each decomposition, widest first
+        static const int b1[2][2] = {{64, 16}, {32, 32}};
+        static const int b2[3][2] = {{64, 8}, {32, 16}, {16, 32}};
+        static const int b4[2][2] = {{32, 8}, {16, 16}};
+        const int(*cfg)[2] = L.bits == 1 ? b1 : (L.bits == 2 ? b2 : b4);
+        const int ncfg = L.bits == 2 ? 3 : 2;
+        int pick = ncfg - 1;
+        for (int i = 0; i < ncfg; ++i)
+            if ((L.N + cfg[i][0] - 1) / cfg[i][0] * M >= target) {
+                pick = i;
+                break;
+            }
+        const int forced = env_int("LUTGEMM_GEMV_CFG", -1);
+        if (forced >= 0 && forced < ncfg) pick = forced;
+        P.gemv_cfg = pick;
+        const int cw = cfg[pick][0], ck = cfg[pick][1];
+        P.n_tiles = (L.N + cw - 1) / cw;
+        const int64_t blocks = P.n_tiles * M;
+        int64_t splits = 1;
+        if (blocks < target) splits = (target + blocks - 1) / blocks;
+        const int64_t max_splits = (L.KB + ck - 1) / ck;  // at least one chunk per split
+        if (splits > max_splits) splits = max_splits;
+        const int fs = env_int("LUTGEMM_SPLITS", 0);
+        if (fs > 0) splits = fs;
+        int64_t kbs = (L.KB + splits - 1) / splits;
+        kbs = (kbs + ck - 1) / ck * ck;
+        if (kbs > L.KB) kbs = L.KB;
+        P.kbs = (int)kbs;
+        P.splits = (int)((L.KB + kbs - 1) / kbs);
+    } else if (kind == 2) {
+        // split-K GEMV: 256 columns per workgroup, KBS 128-blocks each: four weight words
+        // per lane, halved while the grid has fewer than `2 * target` workgroups
+        P.kind = 2;
+        P.mt = 1;
+        P.m_tiles = M;
+        P.n_tiles = L.N_pad / NTILE;
+        int kbs = L.bits == 4 ? 1 : 4 / L.bits;
         const int forced = env_int("LUTGEMM_KBS", 0);
-        if (forced == 1 || forced == 2 || forced == 4 || forced == 8) {
+        if (forced == 1 || forced == 2 || forced == 4 || forced == 8)
             kbs = forced > 8 / L.bits ? 8 / L.bits : forced;
-        } else {
-            while (kbs > 1 && P.n_tiles * M * ((L.KB + kbs - 1) / kbs) < target) kbs >>= 1;
-        }
+        else
+            while (kbs > 1 && P.n_tiles * M * ((L.KB + kbs - 1) / kbs) < 2 * target) kbs >>= 1;
         P.kbs = kbs;
         P.splits = (int)((L.KB + kbs - 1) / kbs);
     } else {
         P.kind = 1;
         P.mt = (M <= 4 || L.bits == 4) ? 4 : 8;
         P.m_tiles = (M + P.mt - 1) / P.mt;
+        P.n_tiles = L.N_pad / NTILE;
         const int64_t base = P.n_tiles * P.m_tiles;
         int64_t splits = 1;
-        if (base < target) splits = (target + base - 1) / base;
+        if (base < 4 * target) splits = (4 * target + base - 1) / base;
         const int64_t max_splits = (L.KB + 1) / 2;  // at least two 128-blocks per split
         if (splits > max_splits) splits = max_splits;
         if (splits < 1) splits = 1;
@@ -107,13 +148,8 @@ LutPlan plan_lut(const Layout &L, int64_t M) {
         P.kbs = (int)kbs;
         P.splits = (int)((L.KB + kbs - 1) / kbs);
     }
-    if (P.splits > 1) {
-        P.ws_counters_bytes = align256((size_t)P.m_tiles * P.n_tiles * 4);
-        P.ws_partials_off = P.ws_counters_bytes;
-        P.ws_bytes = P.ws_partials_off + align256((size_t)P.splits * P.m_tiles * P.mt * L.N_pad * 4);
-    } else {
-        P.ws_counters_bytes = P.ws_partials_off = P.ws_bytes = 0;
-    }
+    const int64_t rows = P.kind == 1 ? P.m_tiles * P.mt : M;
+    P.ws_bytes = P.splits > 1 ? align256((size_t)P.splits * rows * L.N_pad * 4) : 0;
     return P;
 }
 
@@ -243,8 +279,7 @@ lutgemm_status_t lutgemm_mpgemm(const lutgemm_problem_t *problem, int64_t M, con
     lp.planes = (const uint4 *)packed;
     lp.meta = (const char *)packed + L.meta_off;
     lp.out = out;
-    lp.part = plan.ws_bytes ? (float *)((char *)workspace + plan.ws_partials_off) : nullptr;
-    lp.counters = plan.ws_bytes ? (uint32_t *)workspace : nullptr;
+    lp.part = plan.ws_bytes ? (float *)workspace : nullptr;
     lp.M = M;
     lp.N = L.N;
     lp.N_pad = L.N_pad;
@@ -257,6 +292,7 @@ lutgemm_status_t lutgemm_mpgemm(const lutgemm_problem_t *problem, int64_t M, con
     lp.kbs = plan.kbs;
     lp.kpg = (int)(L.G / KBLK);
     lp.per_tensor = L.per_tensor ? 1 : 0;
+    lp.inv_kpg = 1.0f / (float)lp.kpg;
     if (L.wfmt == LUTGEMM_WFMT_BINARY) {  // codes {0,1} read as {-1,+1}: s' = s, z' = 0
         lp.cs = 1.f;
         lp.cz = 0.f;
@@ -273,9 +309,9 @@ lutgemm_status_t lutgemm_mpgemm(const lutgemm_problem_t *problem, int64_t M, con
     lp.out_dtype = out_dtype;
     lp.accumulate = accumulate;
     if (env_int("LUTGEMM_LOG", 0))
-        std::fprintf(stderr, "lutgemm_mpgemm: M=%lld K=%lld N=%lld b=%d kind=%d kbs=%d splits=%d mt=%d grid=%lldx%dx%lld\n",
-                     (long long)M, (long long)L.K, (long long)L.N, L.bits, plan.kind, plan.kbs, plan.splits,
-                     plan.mt, (long long)plan.n_tiles, plan.splits, (long long)plan.m_tiles);
+        std::fprintf(stderr, "lutgemm_mpgemm: M=%lld K=%lld N=%lld b=%d kind=%d cfg=%d kbs=%d splits=%d mt=%d grid=%lldx%dx%lld\n",
+                     (long long)M, (long long)L.K, (long long)L.N, L.bits, plan.kind, plan.gemv_cfg, plan.kbs,
+                     plan.splits, plan.mt, (long long)plan.n_tiles, plan.splits, (long long)plan.m_tiles);
     return hip_status(launch_lut(lp, L, plan, stream));
 }
 

@@ -1,0 +1,157 @@
+// Device helpers shared by the LUT mpGEMM kernels (single-token GEMV and
+// multi-token GEMM): table expansion, the Eq. 2 / Eq. 3 epilogue operands,
+// output conversion and the fixed-order split-K sum.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <hip/hip_fp16.h>
+
+#include "lutgemm_internal.h"
+
+namespace lutgemm {
+
+// LDS-only barrier: waits for this wave's LDS writes (lgkmcnt) but not for its
+// global loads, so prefetches issued before it stay in flight.
+__device__ __forceinline__ void lds_barrier() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+__device__ __forceinline__ float h2f(uint32_t bits16) {
+    return __half2float(__ushort_as_half((unsigned short)bits16));
+}
+
+// (byte B of w) & 0x3C: a 4-bit index pre-shifted left by 2 becomes an INT32
+// table offset in one VALU op (SDWA byte select).
+template <int B>
+__device__ __forceinline__ uint32_t idx4(uint32_t w) {
+    uint32_t r;
+    if constexpr (B == 0)
+        asm("v_and_b32_sdwa %0, 60, %1 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_0"
+            : "=v"(r) : "v"(w));
+    else if constexpr (B == 1)
+        asm("v_and_b32_sdwa %0, 60, %1 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_1"
+            : "=v"(r) : "v"(w));
+    else if constexpr (B == 2)
+        asm("v_and_b32_sdwa %0, 60, %1 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_2"
+            : "=v"(r) : "v"(w));
+    else
+        asm("v_and_b32_sdwa %0, 60, %1 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_3"
+            : "=v"(r) : "v"(w));
+    return r;
+}
+
+__device__ __forceinline__ int lds_i32(const char *base, uint32_t off) {
+    return *(const int *)(base + off);
+}
+
+// Expand one half table (8 entries, 16 bytes) into a 16-entry INT32 signed table.
+template <bool INT8>
+__device__ __forceinline__ void expand_table(const uint4 h, int *dst) {
+    const uint32_t w[4] = {h.x, h.y, h.z, h.w};
+    int v[8];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        if (INT8) {
+            v[2 * i] = (int)(int16_t)(uint16_t)(w[i] & 0xFFFFu);
+            v[2 * i + 1] = (int)(int16_t)(uint16_t)(w[i] >> 16);
+        } else {
+            v[2 * i] = (int)rintf(h2f(w[i] & 0xFFFFu) * (float)(1 << FIX_SHIFT));
+            v[2 * i + 1] = (int)rintf(h2f(w[i] >> 16) * (float)(1 << FIX_SHIFT));
+        }
+    }
+    int4 *d4 = (int4 *)dst;
+    d4[0] = make_int4(v[0], v[1], v[2], v[3]);
+    d4[1] = make_int4(v[4], v[5], v[6], v[7]);
+    d4[2] = make_int4(-v[0], -v[1], -v[2], -v[3]);
+    d4[3] = make_int4(-v[4], -v[5], -v[6], -v[7]);
+}
+
+// Reinterpreted scale and zero (Eq. 2) of quantization group q, column n.
+struct SZ {
+    float sp, zp;
+};
+
+// Reinterpreted scale and zero (Eq. 2) of quantization group q, column n.
+// Branch-free, and every load is a vector load (the index is kept in a VGPR):
+// scalar loads share the completion counter of LDS reads and would serialize them.
+__device__ __forceinline__ SZ load_sz(const LutParams &p, int q, int64_t n) {
+    int64_t idx = p.per_tensor ? 0 : (int64_t)q * p.N_pad + n;
+    asm volatile("" : "+v"(idx));
+    const uint32_t *mw = (const uint32_t *)p.meta;
+    const uint32_t m0 = mw[idx];
+    const uint32_t m1 = mw[idx + (p.per_tensor ? 1 : 0)];
+    const float s = p.per_tensor ? __uint_as_float(m0) : h2f(m0 & 0xFFFFu);
+    const float z = p.per_tensor ? __uint_as_float(m1) : h2f(m0 >> 16);
+    SZ r;
+    r.sp = p.cs * s;
+    r.zp = fmaf(p.cz, z, p.c0);
+    return r;
+}
+
+// Per-column weight scale of the INT8 path (per-tensor or per-channel).
+__device__ __forceinline__ float int_weight_scale(const LutParams &p, bool per_tensor, int64_t n) {
+    if (per_tensor) return ((const float *)p.meta)[0];
+    return h2f(((const uint32_t *)p.meta)[n] & 0xFFFFu);
+}
+
+// Final value of output (m, n): scale, optional accumulate, dtype conversion.
+template <bool INT8>
+__device__ __forceinline__ void store_out(const LutParams &p, int wfmt, bool per_tensor, int64_t m,
+                                          int64_t n, float yf, int yi) {
+    if (n >= p.N) return;
+    const int64_t o = m * p.N + n;
+    if (INT8) {
+        const int y = (wfmt == LUTGEMM_WFMT_TERNARY) ? (yi >> 1) : yi;  // (A + S) / 2 is exact
+        if (p.out_dtype == LUTGEMM_OUT_INT32) {
+            int v = y;
+            if (p.accumulate) v += ((const int *)p.out)[o];
+            ((int *)p.out)[o] = v;
+            return;
+        }
+        float v = ((float)y * p.tok[m]) * int_weight_scale(p, per_tensor, n);
+        if (p.out_dtype == LUTGEMM_OUT_FP32) {
+            if (p.accumulate) v += ((const float *)p.out)[o];
+            ((float *)p.out)[o] = v;
+        } else {
+            if (p.accumulate) v += __half2float(((const __half *)p.out)[o]);
+            ((__half *)p.out)[o] = __float2half_rn(v);
+        }
+        return;
+    }
+    float v = p.tok[m] * yf;
+    if (p.out_dtype == LUTGEMM_OUT_FP32) {
+        if (p.accumulate) v += ((const float *)p.out)[o];
+        ((float *)p.out)[o] = v;
+    } else {
+        if (p.accumulate) v += __half2float(((const __half *)p.out)[o]);
+        ((__half *)p.out)[o] = __float2half_rn(v);
+    }
+}
+
+// Sum of the partials of row m, column n over all splits, in split order.  Loads
+// are issued 32 at a time so that one memory latency covers up to 32 splits.
+template <bool INT8>
+__device__ __forceinline__ void sum_partials(const LutParams &p, int64_t m_alloc, int64_t m, int64_t n,
+                                             float &sf, int &si) {
+    sf = 0.f;
+    si = 0;
+    const float *src = p.part + m * p.N_pad + n;
+    const int64_t stride = m_alloc * p.N_pad;
+    for (int s0 = 0; s0 < p.splits; s0 += 32) {
+        float v[32];
+#pragma unroll
+        for (int j = 0; j < 32; ++j) v[j] = (s0 + j < p.splits) ? src[(int64_t)(s0 + j) * stride] : 0.f;
+#pragma unroll
+        for (int j = 0; j < 32; ++j) {
+            if (INT8)
+                si += __float_as_int(v[j]);
+            else
+                sf += v[j];
+        }
+    }
+}
+
+
+}  // namespace lutgemm

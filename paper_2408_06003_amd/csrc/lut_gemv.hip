@@ -1,0 +1,365 @@
+// Single-token bit-serial LUT mpGEMM (LUT Tensor Core, Section 3.1 bit-serial
+// tables with Eq. 3, 5 and 6; LMMA semantics O = A x W^T + Acc, Section 3.3.1).
+//
+// gfx950 mapping.  A workgroup (4 wavefronts) owns CW output columns over its
+// whole K range, so no other workgroup has to combine its results.  The 64 lanes
+// of a wavefront are (column, bit-plane group, K slice): CW = 64 / (PW * SW)
+// columns, PW lanes per column splitting the b bit-planes, SW K slices.  The
+// four wavefronts add four more K slices.  At any LDS read every lane of a
+// wavefront addresses the table of the same 4-activation group in at most SW = 2
+// different 128-blocks of K, whose tables sit in opposite halves of the LDS
+// banks (padded block stride), so reads are conflict-free; each table entry is
+// reused by the CW x (b / PW) lookups of that group (table reuse across columns,
+// the "elongated N" idea of Section 3.2.2, here across lanes and planes).
+//
+// K is processed in chunks of CK 128-blocks.  For every chunk the half tables of
+// Eq. 5 (8 entries per 4 activations, the HBM format) are expanded into full
+// signed 16-entry tables in LDS, F[s i] = (s ? -T[i] : T[i]), so the stored Eq. 6
+// index addresses its entry directly (the inversion of Eq. 6 was done by the
+// packer and the negation here, once per workgroup, instead of per lookup).
+// Entries are INT32: exact integers on the INT8 path, and the FP16 entries times
+// 2^20 on the FP path (exact for |T| >= 2^-10, otherwise within 2^-21; tables
+// are normalized to |T| < 4 by the precompute).  Each chunk's half tables are
+// loaded before its weight words, so the expansion overlaps the weight stream.
+//
+// A lookup is one SDWA byte-add (table base + 4 * index), one ds_read_b32 and
+// half of a v_add3_u32.  Per 128-block the plane sums are combined as
+// sum_t 2^t acc_t (exact in INT32) and the Eq. 3 epilogue s' (A - z' S) is
+// applied in FP32; lanes of one column are then combined by a fixed butterfly
+// and the four wavefronts in order, so results are bitwise reproducible.
+#include "lut_common.h"
+
+namespace lutgemm {
+
+constexpr int KSTRIDE = GPB * 64 + 64;  // LDS bytes per 128-block: 32 tables x 16 INT32, + 64 B pad
+
+// base + (byte B of x), one VALU op (SDWA byte select).
+template <int B>
+__device__ __forceinline__ uint32_t add_byte(uint32_t base, uint32_t x) {
+    uint32_t r;
+    if constexpr (B == 0)
+        asm("v_add_u32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_0"
+            : "=v"(r) : "v"(base), "v"(x));
+    else if constexpr (B == 1)
+        asm("v_add_u32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_1"
+            : "=v"(r) : "v"(base), "v"(x));
+    else if constexpr (B == 2)
+        asm("v_add_u32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_2"
+            : "=v"(r) : "v"(base), "v"(x));
+    else
+        asm("v_add_u32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_3"
+            : "=v"(r) : "v"(base), "v"(x));
+    return r;
+}
+
+// Keeps a value in a VGPR so that loads indexed by it stay vector loads (scalar
+// loads share the LDS completion counter and would serialize the lookups).
+__device__ __forceinline__ int64_t lane_value(int64_t x) {
+    asm volatile("" : "+v"(x));
+    return x;
+}
+
+// One quarter (4 entries) of a 16-entry signed table from half (qr & 1) of an
+// 8-entry half table: quarters 0, 1 are T[0..3], T[4..7]; quarters 2, 3 negated.
+template <bool INT8>
+__device__ __forceinline__ int4 table_quarter(uint2 h, int qr) {
+    int v[4];
+    const uint32_t w[2] = {h.x, h.y};
+    if (INT8) {
+        const int sg = qr >= 2 ? -1 : 1;
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            v[2 * i] = sg * (int)(int16_t)(uint16_t)(w[i] & 0xFFFFu);
+            v[2 * i + 1] = sg * (int)(int16_t)(uint16_t)(w[i] >> 16);
+        }
+    } else {
+        const float f = qr >= 2 ? -(float)(1 << FIX_SHIFT) : (float)(1 << FIX_SHIFT);
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            v[2 * i] = (int)rintf(h2f(w[i] & 0xFFFFu) * f);
+            v[2 * i + 1] = (int)rintf(h2f(w[i] >> 16) * f);
+        }
+    }
+    return make_int4(v[0], v[1], v[2], v[3]);
+}
+
+template <int BITS, int PW, int SW, int TW, bool INT8>
+__global__ __launch_bounds__(256) void lut_gemv2_kernel(LutParams p, int wfmt) {
+    constexpr int CW = 64 / (PW * SW);    // columns per workgroup
+    constexpr int S = 4 * SW;              // K slices per workgroup
+    constexpr int CK = S * TW;             // 128-blocks per chunk
+    constexpr int NPL = BITS / PW;         // bit-planes per lane
+    constexpr int QPT = CK * GPB * 4 / 256;  // table quarters staged per thread and chunk
+    static_assert(TW * NPL <= 4, "at most four prefetched weight words per lane");
+    __shared__ __attribute__((aligned(16))) char F[CK * KSTRIDE];
+    __shared__ float redf[4][CW];
+    __shared__ int redi[4][CW];
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int c = lane % CW;
+    const int pl = (lane / CW) % PW;       // plane group of this lane
+    const int sl = lane / (CW * PW);       // in-wave K slice
+    const int sigma = wave * SW + sl;      // K slice within a chunk
+    const int64_t n = (int64_t)blockIdx.x * CW + c;
+    const int64_t m = blockIdx.z;
+    const int split = blockIdx.y;
+    const int64_t kbA = (int64_t)split * p.kbs;
+    const int64_t kbB = (kbA + p.kbs < p.KB) ? kbA + p.kbs : p.KB;
+
+    // Prefetch of one chunk: table quarters first, then the lane's weight words.
+    // Loads retire in issue order, so waiting for the tables never waits for the
+    // weights, which keep streaming in while the tables are expanded.
+    uint2 tq[QPT];
+    uint4 w[TW][NPL];
+    auto load_chunk = [&](int64_t kc) {
+        const int nkb = (int)((kbB - kc) < CK ? (kbB - kc) : CK);
+#pragma unroll
+        for (int r = 0; r < QPT; ++r) {
+            const int e = tid + 256 * r, g = e >> 2;
+            if (g < nkb * GPB) tq[r] = ((const uint2 *)(p.T + m * p.J + kc * GPB + g))[e & 1];
+        }
+#pragma unroll
+        for (int t = 0; t < TW; ++t) {
+            const int kbl = sigma + t * S;
+            if (kbl < nkb) {
+#pragma unroll
+                for (int i = 0; i < NPL; ++i)
+                    w[t][i] = p.planes[((kc + kbl) * BITS + pl * NPL + i) * p.N_pad + n];
+            }
+        }
+    };
+
+    float yf = 0.f;
+    int yi = 0;
+    for (int64_t kc = kbA; kc < kbB; kc += CK) {
+        const int nkb = (int)((kbB - kc) < CK ? (kbB - kc) : CK);
+        load_chunk(kc);
+        lds_barrier();  // the previous chunk's tables are no longer read
+#pragma unroll
+        for (int r = 0; r < QPT; ++r) {
+            const int e = tid + 256 * r, g = e >> 2;
+            if (g < nkb * GPB)
+                *(int4 *)(F + (g / GPB) * KSTRIDE + (g % GPB) * 64 + (e & 3) * 16) =
+                    table_quarter<INT8>(tq[r], e & 3);
+        }
+        // epilogue operands of this lane's 128-blocks (vector loads, issued before the lookups)
+        float esc[TW], ezr[TW];
+#pragma unroll
+        for (int t = 0; t < TW; ++t) {
+            esc[t] = 0.f;
+            ezr[t] = 0.f;
+            const int kbl = sigma + t * S;
+            if (!INT8 && kbl < nkb) {
+                const int64_t kb = kc + kbl;
+                const int q = (int)(((float)kb + 0.5f) * p.inv_kpg);
+                const SZ sz = load_sz(p, q, lane_value(n));
+                esc[t] = sz.sp * (1.0f / (float)(1 << FIX_SHIFT));
+                if (pl == 0 && kb == (int64_t)q * p.kpg)  // zero-point term once per group
+                    ezr[t] = sz.sp * sz.zp * ((const float *)p.S)[lane_value(m * p.Q + q)];
+            }
+        }
+        lds_barrier();
+#pragma unroll
+        for (int t = 0; t < TW; ++t) {
+            const int kbl = sigma + t * S;
+            if (kbl < nkb) {
+                const uint32_t base = (uint32_t)(kbl * KSTRIDE);
+                int tot = 0;
+#pragma unroll
+                for (int i = 0; i < NPL; ++i) {
+                    const uint32_t wd[4] = {w[t][i].x, w[t][i].y, w[t][i].z, w[t][i].w};
+                    int acc = 0;
+#pragma unroll
+                    for (int d = 0; d < 4; ++d) {
+                        const uint32_t lo = (wd[d] << 2) & 0x3C3C3C3Cu, hi = (wd[d] >> 2) & 0x3C3C3C3Cu;
+                        const char *Fg = F + d * 8 * 64;
+                        acc += lds_i32(Fg + 0 * 64, add_byte<0>(base, lo)) + lds_i32(Fg + 1 * 64, add_byte<0>(base, hi));
+                        acc += lds_i32(Fg + 2 * 64, add_byte<1>(base, lo)) + lds_i32(Fg + 3 * 64, add_byte<1>(base, hi));
+                        acc += lds_i32(Fg + 4 * 64, add_byte<2>(base, lo)) + lds_i32(Fg + 5 * 64, add_byte<2>(base, hi));
+                        acc += lds_i32(Fg + 6 * 64, add_byte<3>(base, lo)) + lds_i32(Fg + 7 * 64, add_byte<3>(base, hi));
+                    }
+                    // |sum_t 2^t acc_t| <= 15 * 32 * 2^22 < 2^31 on the FP path: exact in INT32
+                    tot += acc << (pl * NPL + i);
+                }
+                if (INT8)
+                    yi += tot;
+                else
+                    yf = fmaf(esc[t], (float)tot, yf) - ezr[t];
+            }
+        }
+    }
+
+    // combine the lanes of each column (fixed butterfly), then the four wavefronts in order
+#pragma unroll
+    for (int off = CW; off < 64; off <<= 1) {
+        if (INT8)
+            yi += __shfl_xor(yi, off, 64);
+        else
+            yf += __shfl_xor(yf, off, 64);
+    }
+    if (lane < CW) {
+        redf[wave][lane] = yf;
+        redi[wave][lane] = yi;
+    }
+    lds_barrier();
+    if (wave == 0 && lane < CW) {
+        const float sf = ((redf[0][lane] + redf[1][lane]) + redf[2][lane]) + redf[3][lane];
+        int si = redi[0][lane] + redi[1][lane] + redi[2][lane] + redi[3][lane];
+        if (INT8 && split == 0 && wfmt == LUTGEMM_WFMT_TERNARY) si += ((const int *)p.S)[m * p.Q];
+        if (p.splits == 1)
+            store_out<INT8>(p, wfmt, p.per_tensor != 0, m, n, sf, si);
+        else
+            p.part[((int64_t)split * p.M + m) * p.N_pad + n] = INT8 ? __int_as_float(si) : sf;
+    }
+}
+
+// Split-K variant for large N.  One lane per column and 256 columns per
+// workgroup, so each staged table serves 256 columns (the widest reuse); each
+// workgroup covers KBS 128-blocks of K and every load of the workgroup (its half
+// tables first, then all KBS x b weight words of each lane) is issued before
+// anything waits.  The 4 wavefronts read the same table at a time (no bank
+// conflicts) and the compile-time table offsets leave one SDWA AND per lookup.
+// With more than one K split the partial sums go to the workspace and
+// lut_finalize_kernel adds them in split order.
+template <int BITS, int KBS, bool INT8>
+__global__ __launch_bounds__(256) void lut_gemv_split_kernel(LutParams p, int wfmt) {
+    constexpr int QPT = (KBS * GPB * 4 + 255) / 256;  // table quarters per thread
+    __shared__ __attribute__((aligned(16))) char F[KBS * KSTRIDE];
+    const int tid = threadIdx.x;
+    const int64_t n = (int64_t)blockIdx.x * NTILE + tid;
+    const int split = blockIdx.y;
+    const int64_t m = blockIdx.z;
+    const int64_t kb0 = (int64_t)split * KBS;
+    const int nkb = (int)((p.KB - kb0) < KBS ? (p.KB - kb0) : KBS);
+
+    uint2 tq[QPT];
+#pragma unroll
+    for (int r = 0; r < QPT; ++r) {
+        const int e = tid + 256 * r, g = e >> 2;
+        if (g < nkb * GPB) tq[r] = ((const uint2 *)(p.T + m * p.J + kb0 * GPB + g))[e & 1];
+    }
+    uint4 w[KBS][BITS];
+#pragma unroll
+    for (int kbl = 0; kbl < KBS; ++kbl) {
+        if (kbl < nkb) {
+#pragma unroll
+            for (int t = 0; t < BITS; ++t) w[kbl][t] = p.planes[((kb0 + kbl) * BITS + t) * p.N_pad + n];
+        }
+    }
+    float esc[KBS], ezr[KBS];
+#pragma unroll
+    for (int kbl = 0; kbl < KBS; ++kbl) {
+        esc[kbl] = 0.f;
+        ezr[kbl] = 0.f;
+        if (!INT8 && kbl < nkb) {
+            const int64_t kb = kb0 + kbl;
+            const int q = (int)(((float)kb + 0.5f) * p.inv_kpg);
+            const SZ sz = load_sz(p, q, lane_value(n));
+            esc[kbl] = sz.sp * (1.0f / (float)(1 << FIX_SHIFT));
+            if (kb == (int64_t)q * p.kpg)  // zero-point term once per group
+                ezr[kbl] = sz.sp * sz.zp * ((const float *)p.S)[lane_value(m * p.Q + q)];
+        }
+    }
+    int s_total = 0;
+    if (INT8 && split == 0 && wfmt == LUTGEMM_WFMT_TERNARY) s_total = ((const int *)p.S)[lane_value(m * p.Q)];
+#pragma unroll
+    for (int r = 0; r < QPT; ++r) {
+        const int e = tid + 256 * r, g = e >> 2;
+        if (g < nkb * GPB)
+            *(int4 *)(F + (g / GPB) * KSTRIDE + (g % GPB) * 64 + (e & 3) * 16) = table_quarter<INT8>(tq[r], e & 3);
+    }
+    lds_barrier();
+
+    float yf = 0.f;
+    int yi = s_total;
+#pragma unroll
+    for (int kbl = 0; kbl < KBS; ++kbl) {
+        if (kbl < nkb) {
+            int tot = 0;
+#pragma unroll
+            for (int t = 0; t < BITS; ++t) {
+                const uint32_t wd[4] = {w[kbl][t].x, w[kbl][t].y, w[kbl][t].z, w[kbl][t].w};
+                int acc = 0;
+#pragma unroll
+                for (int d = 0; d < 4; ++d) {
+                    const uint32_t lo = wd[d] << 2, hi = wd[d] >> 2;
+                    const char *Fg = F + kbl * KSTRIDE + d * 8 * 64;
+                    acc += lds_i32(Fg + 0 * 64, idx4<0>(lo)) + lds_i32(Fg + 1 * 64, idx4<0>(hi));
+                    acc += lds_i32(Fg + 2 * 64, idx4<1>(lo)) + lds_i32(Fg + 3 * 64, idx4<1>(hi));
+                    acc += lds_i32(Fg + 4 * 64, idx4<2>(lo)) + lds_i32(Fg + 5 * 64, idx4<2>(hi));
+                    acc += lds_i32(Fg + 6 * 64, idx4<3>(lo)) + lds_i32(Fg + 7 * 64, idx4<3>(hi));
+                }
+                tot += acc << t;  // exact in INT32, see the kernel above
+            }
+            if (INT8)
+                yi += tot;
+            else
+                yf = fmaf(esc[kbl], (float)tot, yf) - ezr[kbl];
+        }
+    }
+    if (p.splits == 1)
+        store_out<INT8>(p, wfmt, p.per_tensor != 0, m, n, yf, yi);
+    else
+        p.part[((int64_t)split * p.M + m) * p.N_pad + n] = INT8 ? __int_as_float(yi) : yf;
+}
+
+template <int BITS, bool INT8>
+static void launch_split(const LutParams &p, const Layout &L, const LutPlan &plan, hipStream_t s) {
+    const dim3 grid((unsigned)(L.N_pad / NTILE), (unsigned)plan.splits, (unsigned)p.M);
+    switch (plan.kbs) {
+    case 1: hipLaunchKernelGGL((lut_gemv_split_kernel<BITS, 1, INT8>), grid, dim3(256), 0, s, p, L.wfmt); break;
+    case 2: hipLaunchKernelGGL((lut_gemv_split_kernel<BITS, 2, INT8>), grid, dim3(256), 0, s, p, L.wfmt); break;
+    case 4:
+        if constexpr (BITS <= 2)
+            hipLaunchKernelGGL((lut_gemv_split_kernel<BITS, 4, INT8>), grid, dim3(256), 0, s, p, L.wfmt);
+        break;
+    default:
+        if constexpr (BITS == 1)
+            hipLaunchKernelGGL((lut_gemv_split_kernel<BITS, 8, INT8>), grid, dim3(256), 0, s, p, L.wfmt);
+        break;
+    }
+}
+
+template <int BITS, int PW, int SW, int TW, bool INT8>
+static void launch_cfg(const LutParams &p, const Layout &L, const LutPlan &plan, hipStream_t s) {
+    constexpr int CW = 64 / (PW * SW);
+    const dim3 grid((unsigned)((L.N + CW - 1) / CW), (unsigned)plan.splits, (unsigned)p.M);
+    hipLaunchKernelGGL((lut_gemv2_kernel<BITS, PW, SW, TW, INT8>), grid, dim3(256), 0, s, p, L.wfmt);
+}
+
+// Lane decompositions (PW, SW, TW) offered per bit width, indexed by LutPlan::gemv_cfg:
+//   b = 1: 0 -> (1,1,4) CW=64 CK=16   1 -> (1,2,4) CW=32 CK=32
+//   b = 2: 0 -> (1,1,2) CW=64 CK=8    1 -> (2,1,4) CW=32 CK=16   2 -> (2,2,4) CW=16 CK=32
+//   b = 4: 0 -> (2,1,2) CW=32 CK=8    1 -> (4,1,4) CW=16 CK=16
+template <bool INT8>
+static int launch_gemv_bits(const LutParams &p, const Layout &L, const LutPlan &plan, hipStream_t s) {
+    if (L.bits == 1) {
+        if (plan.gemv_cfg == 0) launch_cfg<1, 1, 1, 4, INT8>(p, L, plan, s);
+        else launch_cfg<1, 1, 2, 4, INT8>(p, L, plan, s);
+    } else if (L.bits == 2) {
+        if (plan.gemv_cfg == 0) launch_cfg<2, 1, 1, 2, INT8>(p, L, plan, s);
+        else if (plan.gemv_cfg == 1) launch_cfg<2, 2, 1, 4, INT8>(p, L, plan, s);
+        else launch_cfg<2, 2, 2, 4, INT8>(p, L, plan, s);
+    } else {
+        if constexpr (!INT8) {
+            if (plan.gemv_cfg == 0) launch_cfg<4, 2, 1, 2, false>(p, L, plan, s);
+            else launch_cfg<4, 4, 1, 4, false>(p, L, plan, s);
+        }
+    }
+    return (int)hipGetLastError();
+}
+
+int launch_gemv(const LutParams &p, const Layout &L, const LutPlan &plan, void *stream) {
+    hipStream_t s = (hipStream_t)stream;
+    if (plan.kind == 2) {
+        const bool i8 = L.act == LUTGEMM_ACT_INT8;
+        if (L.bits == 1) i8 ? launch_split<1, true>(p, L, plan, s) : launch_split<1, false>(p, L, plan, s);
+        else if (L.bits == 2) i8 ? launch_split<2, true>(p, L, plan, s) : launch_split<2, false>(p, L, plan, s);
+        else launch_split<4, false>(p, L, plan, s);
+        return (int)hipGetLastError();
+    }
+    return L.act == LUTGEMM_ACT_INT8 ? launch_gemv_bits<true>(p, L, plan, s)
+                                      : launch_gemv_bits<false>(p, L, plan, s);
+}
+
+}  // namespace lutgemm

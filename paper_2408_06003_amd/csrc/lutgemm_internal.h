@@ -18,7 +18,7 @@
 #include <stddef.h>
 #include <stdint.h>
 
-#include "../../include/lutgemm.h"
+#include "lutgemm.h"
 
 namespace lutgemm {
 
@@ -71,13 +71,14 @@ inline TableLayout make_table_layout(const Layout &L, int64_t M) {
 
 // Launch plan of the LUT mpGEMM for (problem, M).
 struct LutPlan {
-    int kind;        // 0: single-token GEMV kernel, 1: multi-token kernel
+    int kind;        // 0: single-token whole-K GEMV, 1: multi-token kernel, 2: single-token split-K GEMV
+    int gemv_cfg;    // single-token kernel: lane decomposition (see lut_gemv.hip)
     int kbs;         // 128-blocks of K per split
     int splits;      // K splits (1 = no workspace)
     int mt;          // tokens per workgroup (multi-token kernel)
     int64_t m_tiles; // token tiles
     int64_t n_tiles; // column tiles
-    size_t ws_counters_bytes, ws_partials_off, ws_bytes;
+    size_t ws_bytes;
 };
 
 LutPlan plan_lut(const Layout &L, int64_t M);
@@ -108,12 +109,12 @@ struct LutParams {
     const uint4 *planes;
     const void *meta;
     void *out;
-    float *part;           // split partial sums [splits][M][N_pad] (float or int bits)
-    uint32_t *counters;    // [m_tiles][n_tiles]
+    float *part;           // split partial sums [splits][rows][N_pad] (float or int bits)
     int64_t M, N, N_pad, K, KB, J, Q, G;
     int splits, kbs, out_dtype, accumulate;
     int kpg;               // 128-blocks of K per quantization group (G / 128)
     int per_tensor;        // one (s, z) pair for the whole tensor, FP32
+    float inv_kpg;         // 1 / kpg (group index of a 128-block by one multiply)
     // Eq. 2 for the weight format: s' = cs * s, z' = cz * z + c0
     float cs, cz, c0;
 };
@@ -131,6 +132,7 @@ struct DequantParams {
 int launch_pack(const PackParams &p, void *stream);
 int launch_precompute(const PrecomputeParams &p, int act_int8, void *stream);
 int launch_lut(const LutParams &p, const Layout &L, const LutPlan &plan, void *stream);
+int launch_gemv(const LutParams &p, const Layout &L, const LutPlan &plan, void *stream);
 int launch_dequant(const DequantParams &p, const Layout &L, void *stream);
 
 }  // namespace lutgemm

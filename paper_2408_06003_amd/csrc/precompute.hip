@@ -1,17 +1,23 @@
 // Table precompute as an independent operator (LUT Tensor Core, Section 3.1.1),
 // building the symmetric half tables of Eq. 4-5.
 //
-// One workgroup per token m:
-//   1. amax = max_k |a[m,k]|.  FP16 tables: the token is scaled by 2^-e with
-//      amax = f 2^e, f in [0.5, 1), so every entry lies in (-4, 4) and neither
-//      overflows nor loses range in FP16 (the factor 2^e is returned in t[m]).
-//      INT8 tables: q_a = clamp(rint(a * (127 / amax)), -127, 127), FP32 with
-//      correctly rounded division, s_a = amax / 127.
-//   2. For every group j of 4 activations x_0..x_3 and row i in [0, 8):
-//      T[m][j][i] = -x_0 + sum_{e=1..3} (bit (3-e) of i ? x_e : -x_e), which is
-//      the entry of pattern 0 i of the full 16-entry table (Eq. 5); the other
-//      half is its negation (Eq. 4) and is never stored.
-//   3. S[m][q] = sum of x over quantization group q (zero-point term of Eq. 3).
+// Grid (ceil(J / 256), M): workgroup b of token m owns table groups
+// [256 b, 256 b + 256), one group of 4 activations per lane.
+//   1. amax = max_k |a[m,k]| over the whole token (every workgroup reads the
+//      token once, into LDS when K <= 32768, so steps 2-3 read no global memory;
+//      the token is at most a few tens of KiB and stays in L2).  FP16 tables: the
+//      token is scaled by 2^-e with amax = f 2^e, f in [0.5, 1), so every entry
+//      lies in (-4, 4) and FP16 neither overflows nor loses range (the factor 2^e
+//      is returned in t[m]).  INT8 tables: q_a = clamp(rint(a * (127 / amax)),
+//      -127, 127), FP32 with correctly rounded division, s_a = amax / 127.
+//   2. For its group j with activations x_0..x_3 and row i in [0, 8):
+//      T[m][j][i] = -x_0 + sum_{e=1..3} (bit (3-e) of i ? x_e : -x_e), the entry of
+//      pattern 0 i of the full 16-entry table (Eq. 5); the other half is its
+//      negation (Eq. 4) and is never stored.
+//   3. S[m][q] = sum of x over quantization group q (zero-point term of Eq. 3):
+//      groups of 128..1024 activations are reduced across the lanes that built
+//      them; larger ones are summed by the workgroup that holds their first
+//      activation.  All reductions have a fixed order.
 #include <hip/hip_runtime.h>
 #include <hip/hip_fp16.h>
 
@@ -45,23 +51,54 @@ __device__ __forceinline__ float token_value(float a, float scale) {
     return a * scale;  // exact: scale is a power of two
 }
 
-template <bool INT8>
-__global__ __launch_bounds__(256) void precompute_kernel(PrecomputeParams p) {
-    __shared__ float red[4];
-    const int64_t m = blockIdx.x;
-    const uint16_t *a = p.act + m * p.K;
-    const int tid = threadIdx.x;
+__device__ __forceinline__ float block_sum_f(float v, float *red) {
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    __syncthreads();
+    if (lane == 0) red[wave] = v;
+    __syncthreads();
+    return ((red[0] + red[1]) + red[2]) + red[3];
+}
 
-    // 1. absmax of the token
+__device__ __forceinline__ int block_sum_i(int v, int *red) {
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    __syncthreads();
+    if (lane == 0) red[wave] = v;
+    __syncthreads();
+    return red[0] + red[1] + red[2] + red[3];
+}
+
+constexpr int64_t ROW_LDS_MAX_K = 32768;  // tokens up to this length are staged in LDS once
+
+template <bool INT8, bool ROW_LDS>
+__global__ __launch_bounds__(256) void precompute_kernel(PrecomputeParams p) {
+    extern __shared__ __attribute__((aligned(16))) uint16_t row[];  // K halves when ROW_LDS
+    __shared__ float redf[4];
+    __shared__ int redi[4];
+    __shared__ float segf[4];
+    __shared__ int segi[4];
+    const int64_t m = blockIdx.y;
+    const uint16_t *ag = p.act + m * p.K;
+    const uint16_t *a = ROW_LDS ? row : ag;  // reads after step 1 come from the staged row
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int64_t j = (int64_t)blockIdx.x * 256 + tid;
+
+    // 1. absmax of the token, 8 activations per load
     float amax = 0.f;
-    for (int64_t k = (int64_t)tid * 4; k < p.K; k += 1024) {
-        const uint2 v = *(const uint2 *)(a + k);
-        amax = fmaxf(amax, fabsf(h2f(v.x & 0xFFFFu)));
-        amax = fmaxf(amax, fabsf(h2f(v.x >> 16)));
-        amax = fmaxf(amax, fabsf(h2f(v.y & 0xFFFFu)));
-        amax = fmaxf(amax, fabsf(h2f(v.y >> 16)));
+    for (int64_t c = tid; c < p.K / 8; c += 256) {
+        const uint4 v = ((const uint4 *)ag)[c];
+        if (ROW_LDS) ((uint4 *)row)[c] = v;
+        const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            amax = fmaxf(amax, fabsf(h2f(w[i] & 0xFFFFu)));
+            amax = fmaxf(amax, fabsf(h2f(w[i] >> 16)));
+        }
     }
-    amax = block_max(amax, red);
+    amax = block_max(amax, redf);  // its barrier also publishes the staged row
 
     float scale, tok;
     if (INT8) {
@@ -83,10 +120,12 @@ __global__ __launch_bounds__(256) void precompute_kernel(PrecomputeParams p) {
             tok = ldexpf(1.f, e);
         }
     }
-    if (tid == 0) p.tok[m] = tok;
+    if (blockIdx.x == 0 && tid == 0) p.tok[m] = tok;
 
-    // 2. half tables, one group of 4 activations per thread and step
-    for (int64_t j = tid; j < p.J; j += 256) {
+    // 2. half table of this lane's group
+    float g4f = 0.f;
+    int g4i = 0;
+    if (j < p.J) {
         const uint2 v = *(const uint2 *)(a + 4 * j);
         const float x0 = token_value<INT8>(h2f(v.x & 0xFFFFu), scale);
         const float x1 = token_value<INT8>(h2f(v.x >> 16), scale);
@@ -103,24 +142,74 @@ __global__ __launch_bounds__(256) void precompute_kernel(PrecomputeParams p) {
         }
         p.T[m * p.J + j] = make_uint4(e[0] | (e[1] << 16), e[2] | (e[3] << 16), e[4] | (e[5] << 16),
                                       e[6] | (e[7] << 16));
+        g4f = ((x0 + x1) + x2) + x3;
+        g4i = (int)x0 + (int)x1 + (int)x2 + (int)x3;
     }
 
-    // 3. group sums, one wavefront per quantization group, fixed summation order
-    const int wave = tid >> 6, lane = tid & 63;
-    for (int64_t q = wave; q < p.Q; q += 4) {
-        const uint16_t *aq = a + q * p.G;
-        if (INT8) {
-            int s = 0;
-            for (int64_t k = lane; k < p.G; k += 64) s += (int)token_value<true>(h2f(aq[k]), scale);
+    // 3. group sums
+    const int64_t seg = p.G / 4;  // table groups per quantization group
+    if (seg <= 256 && 256 % seg == 0) {
+        // reduce over `seg` consecutive lanes (butterfly within the wave, then waves in order)
+        const int width = seg < 64 ? (int)seg : 64;
+        float sf = g4f;
+        int si = g4i;
+        for (int off = width >> 1; off > 0; off >>= 1) {
+            if (INT8)
+                si += __shfl_xor(si, off, 64);
+            else
+                sf += __shfl_xor(sf, off, 64);
+        }
+        if (seg > 64) {
+            __syncthreads();
+            if (lane == 0) {
+                segf[wave] = sf;
+                segi[wave] = si;
+            }
+            __syncthreads();
+            const int wpq = (int)(seg / 64), w0 = wave - wave % wpq;
+            sf = segf[w0];
+            si = segi[w0];
+            for (int w = 1; w < wpq; ++w) {
+                sf += segf[w0 + w];
+                si += segi[w0 + w];
+            }
+        }
+        if (j < p.J && (j % seg) == 0) {
+            const int64_t q = j / seg;
+            if (INT8)
+                ((int *)p.S)[m * p.Q + q] = si;
+            else
+                ((float *)p.S)[m * p.Q + q] = sf;
+        }
+    } else {
+        // quantization groups starting in this workgroup's range, summed by the whole workgroup
+        const int64_t k_lo = (int64_t)blockIdx.x * 1024;
+        const int64_t k_hi = (k_lo + 1024 < p.K) ? k_lo + 1024 : p.K;
+        for (int64_t q = (k_lo + p.G - 1) / p.G; q * p.G < k_hi; ++q) {
+            const uint16_t *aq = a + q * p.G;
+            float sf = 0.f;
+            int si = 0;
+            for (int64_t c = tid; c < p.G / 8; c += 256) {
+                const uint4 v = ((const uint4 *)aq)[c];
+                const uint32_t w[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
-            for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off, 64);
-            if (lane == 0) ((int *)p.S)[m * p.Q + q] = s;
-        } else {
-            float s = 0.f;
-            for (int64_t k = lane; k < p.G; k += 64) s += token_value<false>(h2f(aq[k]), scale);
-#pragma unroll
-            for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off, 64);
-            if (lane == 0) ((float *)p.S)[m * p.Q + q] = s;
+                for (int i = 0; i < 4; ++i) {
+                    const float lo = token_value<INT8>(h2f(w[i] & 0xFFFFu), scale);
+                    const float hi = token_value<INT8>(h2f(w[i] >> 16), scale);
+                    if (INT8)
+                        si += (int)lo + (int)hi;
+                    else
+                        sf += lo + hi;
+                }
+            }
+            if (INT8) {
+                const int tot = block_sum_i(si, redi);
+                if (tid == 0) ((int *)p.S)[m * p.Q + q] = tot;
+            } else {
+                const float tot = block_sum_f(sf, redf);
+                if (tid == 0) ((float *)p.S)[m * p.Q + q] = tot;
+            }
+            __syncthreads();
         }
     }
 }
@@ -128,10 +217,16 @@ __global__ __launch_bounds__(256) void precompute_kernel(PrecomputeParams p) {
 int launch_precompute(const PrecomputeParams &p, int act_int8, void *stream) {
     hipStream_t s = (hipStream_t)stream;
     if (p.M <= 0) return 0;
-    if (act_int8)
-        hipLaunchKernelGGL(precompute_kernel<true>, dim3((unsigned)p.M), dim3(256), 0, s, p);
-    else
-        hipLaunchKernelGGL(precompute_kernel<false>, dim3((unsigned)p.M), dim3(256), 0, s, p);
+    const dim3 grid((unsigned)((p.J + 255) / 256), (unsigned)p.M);
+    const bool lds = p.K <= ROW_LDS_MAX_K;
+    const size_t shm = lds ? (size_t)p.K * 2 : 0;
+    if (act_int8) {
+        if (lds) hipLaunchKernelGGL((precompute_kernel<true, true>), grid, dim3(256), shm, s, p);
+        else hipLaunchKernelGGL((precompute_kernel<true, false>), grid, dim3(256), 0, s, p);
+    } else {
+        if (lds) hipLaunchKernelGGL((precompute_kernel<false, true>), grid, dim3(256), shm, s, p);
+        else hipLaunchKernelGGL((precompute_kernel<false, false>), grid, dim3(256), 0, s, p);
+    }
     return (int)hipGetLastError();
 }
 

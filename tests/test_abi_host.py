@@ -122,7 +122,7 @@ def test_entry_points_reject_before_launch():
     pi = L.problem(1024, 256, 2, L.WFMT_TERNARY, 0, L.ACT_INT8, True)
     assert f.lutgemm_mpgemm_dequant(ctypes.byref(pi), 1, ok, ok, ok, L.OUT_FP16, 0, None) == L.ERROR_NOT_SUPPORTED
     # workspace required but missing / too small
-    pw = L.problem(4096, 4096, 2, L.WFMT_TERNARY, 0, L.ACT_INT8, True)
+    pw = L.problem(8192, 1024, 2, L.WFMT_TERNARY, 0, L.ACT_INT8, True)  # too few columns: K is split
     need = L.workspace_size(pw, 1)
     assert need > 0
     assert f.lutgemm_mpgemm(ctypes.byref(pw), 1, ok, ok, ok, L.OUT_INT32, 0, None, need, None) == L.ERROR_INVALID_VALUE

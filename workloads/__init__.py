@@ -111,11 +111,11 @@ def draw(wfmt: int, bits: int, group: int, scale_fp32: bool, zero_max: float, ac
     n_groups = 1 if group == 0 else K // group
     # codes
     if wfmt == WFMT_UINT:
-        codes = rng.integers(0, 1 << bits, size=(N, K), dtype=np.int64).astype(np.uint8)
+        codes = rng.integers(0, 1 << bits, size=(N, K), dtype=np.uint8)
     elif wfmt == WFMT_BINARY:
-        codes = rng.integers(0, 2, size=(N, K), dtype=np.int64).astype(np.uint8)
+        codes = rng.integers(0, 2, size=(N, K), dtype=np.uint8)
     elif wfmt == WFMT_TERNARY:
-        codes = rng.integers(-1, 2, size=(N, K), dtype=np.int64).astype(np.int8)
+        codes = rng.integers(-1, 2, size=(N, K), dtype=np.int8)
     else:
         raise ValueError(f"unknown weight format {wfmt}")
     # scales
