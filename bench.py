@@ -35,7 +35,8 @@ HBM_PEAK_GBPS = 8000.0
 MFMA_FP16_PEAK_TFLOPS = 2500.0
 ROTATION_BYTES = 1 << 30
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "pmc_traffic.txt")
-KERNEL_SOURCE = os.path.join(ROOT, "paper_2408_06003_amd", "csrc", "lut_mpgemm.hip")
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2408_06003_amd", "csrc", f)
+                  for f in ("lut_gemv.hip", "lut_common.h", "lutgemm_internal.h", "api.cpp")]
 
 
 def log(msg):
@@ -74,8 +75,12 @@ def algorithmic_bytes(inp, out_bytes):
 
 
 def kernel_source_hash():
-    with open(KERNEL_SOURCE, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    """Hash of the sources that define the single-token mpGEMM kernels and their launch."""
+    h = hashlib.sha256()
+    for path in KERNEL_SOURCES:
+        with open(path, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
 
 
 def load_traffic(workload):

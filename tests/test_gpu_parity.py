@@ -50,7 +50,9 @@ def check_fp_path(gp, rows=None, cols=None, dequant=False, out_dtype=None, what=
     y = (gp.dequant(out_dtype=out_dtype) if dequant else gp.lut(out_dtype=out_dtype)).float().cpu().numpy()
     if rows is not None:
         y = y[np.ix_(rows, cols)]
-    return assert_fp_close(y, ref, what)
+    fro, mx = assert_fp_close(y, ref, what)
+    print(f"[err] {what}: relFro {fro:.3e} max/rms {mx:.3e}", flush=True)
+    return fro, mx
 
 
 # ----------------------------------------------------------------- reduced sizes, all outputs
