@@ -103,6 +103,7 @@ LutPlan plan_lut(const Layout &L, int64_t M) {
         const int forced = env_int("LUTGEMM_GEMV_CFG", -1);
         if (forced >= 0 && forced < ncfg) pick = forced;
         P.gemv_cfg = pick;
+        P.gemv_nw = env_int("LUTGEMM_GEMV_NW", 16);  // the most the decomposition allows (see lut_gemv.hip)
         const int cw = cfg[pick][0], ck = cfg[pick][1];
         P.n_tiles = (L.N + cw - 1) / cw;
         const int64_t blocks = P.n_tiles * M;
@@ -309,8 +310,8 @@ lutgemm_status_t lutgemm_mpgemm(const lutgemm_problem_t *problem, int64_t M, con
     lp.out_dtype = out_dtype;
     lp.accumulate = accumulate;
     if (env_int("LUTGEMM_LOG", 0))
-        std::fprintf(stderr, "lutgemm_mpgemm: M=%lld K=%lld N=%lld b=%d kind=%d cfg=%d kbs=%d splits=%d mt=%d grid=%lldx%dx%lld\n",
-                     (long long)M, (long long)L.K, (long long)L.N, L.bits, plan.kind, plan.gemv_cfg, plan.kbs,
+        std::fprintf(stderr, "lutgemm_mpgemm: M=%lld K=%lld N=%lld b=%d kind=%d cfg=%d nw=%d kbs=%d splits=%d mt=%d grid=%lldx%dx%lld\n",
+                     (long long)M, (long long)L.K, (long long)L.N, L.bits, plan.kind, plan.gemv_cfg, plan.gemv_nw, plan.kbs,
                      plan.splits, plan.mt, (long long)plan.n_tiles, plan.splits, (long long)plan.m_tiles);
     return hip_status(launch_lut(lp, L, plan, stream));
 }

@@ -92,42 +92,71 @@ __device__ __forceinline__ SZ load_sz(const LutParams &p, int q, int64_t n) {
 
 // Per-column weight scale of the INT8 path (per-tensor or per-channel).
 __device__ __forceinline__ float int_weight_scale(const LutParams &p, bool per_tensor, int64_t n) {
-    if (per_tensor) return ((const float *)p.meta)[0];
+    if (per_tensor) return ((const float *)p.meta)[n];  // n = 0: the one FP32 scale
     return h2f(((const uint32_t *)p.meta)[n] & 0xFFFFu);
 }
 
-// Final value of output (m, n): scale, optional accumulate, dtype conversion.
+// Keeps a value in a VGPR so that loads indexed by it stay vector loads (scalar
+// loads share the LDS completion counter and would serialize the lookups).
+__device__ __forceinline__ int64_t lane_value(int64_t x) {
+    asm volatile("" : "+v"(x));
+    return x;
+}
+
+// Operands of the output epilogue of (m, n): the per-token factor t[m], the INT8
+// path's weight scale, the previous output when accumulating, and the ternary
+// group sum S[m][0] (added by the first K split only).  Loaded ahead of the main
+// loop, so that their memory latency overlaps the lookups instead of following
+// them; every load is a vector load.
+struct Epi {
+    float tok, sw, prev;
+    int s0;
+};
+
 template <bool INT8>
-__device__ __forceinline__ void store_out(const LutParams &p, int wfmt, bool per_tensor, int64_t m,
-                                          int64_t n, float yf, int yi) {
+__device__ __forceinline__ Epi load_epi(const LutParams &p, int wfmt, int64_t m, int64_t n, bool first_split) {
+    Epi e{1.f, 1.f, 0.f, 0};
+    if (n >= p.N) return e;
+    const int64_t mv = lane_value(m), nv = lane_value(n), o = mv * p.N + nv;
+    e.tok = p.tok[mv];
+    if (INT8) {
+        e.sw = int_weight_scale(p, p.per_tensor != 0, p.per_tensor ? lane_value(0) : nv);
+        if (first_split && wfmt == LUTGEMM_WFMT_TERNARY) e.s0 = ((const int *)p.S)[mv * p.Q];
+    }
+    if (p.accumulate) {
+        if (INT8 && p.out_dtype == LUTGEMM_OUT_INT32)
+            e.prev = __int_as_float(((const int *)p.out)[o]);
+        else if (p.out_dtype == LUTGEMM_OUT_FP32)
+            e.prev = ((const float *)p.out)[o];
+        else
+            e.prev = __half2float(((const __half *)p.out)[o]);
+    }
+    return e;
+}
+
+// Final value of output (m, n): scale, optional accumulate, dtype conversion.
+// yi already includes the ternary group sum (Epi::s0).
+template <bool INT8>
+__device__ __forceinline__ void store_out(const LutParams &p, int wfmt, int64_t m, int64_t n, float yf, int yi,
+                                          const Epi &e) {
     if (n >= p.N) return;
     const int64_t o = m * p.N + n;
+    float v;
     if (INT8) {
         const int y = (wfmt == LUTGEMM_WFMT_TERNARY) ? (yi >> 1) : yi;  // (A + S) / 2 is exact
         if (p.out_dtype == LUTGEMM_OUT_INT32) {
-            int v = y;
-            if (p.accumulate) v += ((const int *)p.out)[o];
-            ((int *)p.out)[o] = v;
+            ((int *)p.out)[o] = p.accumulate ? y + __float_as_int(e.prev) : y;
             return;
         }
-        float v = ((float)y * p.tok[m]) * int_weight_scale(p, per_tensor, n);
-        if (p.out_dtype == LUTGEMM_OUT_FP32) {
-            if (p.accumulate) v += ((const float *)p.out)[o];
-            ((float *)p.out)[o] = v;
-        } else {
-            if (p.accumulate) v += __half2float(((const __half *)p.out)[o]);
-            ((__half *)p.out)[o] = __float2half_rn(v);
-        }
-        return;
-    }
-    float v = p.tok[m] * yf;
-    if (p.out_dtype == LUTGEMM_OUT_FP32) {
-        if (p.accumulate) v += ((const float *)p.out)[o];
-        ((float *)p.out)[o] = v;
+        v = ((float)y * e.tok) * e.sw;
     } else {
-        if (p.accumulate) v += __half2float(((const __half *)p.out)[o]);
-        ((__half *)p.out)[o] = __float2half_rn(v);
+        v = e.tok * yf;
     }
+    if (p.accumulate) v += e.prev;
+    if (p.out_dtype == LUTGEMM_OUT_FP32)
+        ((float *)p.out)[o] = v;
+    else
+        ((__half *)p.out)[o] = __float2half_rn(v);
 }
 
 // Sum of the partials of row m, column n over all splits, in split order.  Loads

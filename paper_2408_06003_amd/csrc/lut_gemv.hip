@@ -52,13 +52,6 @@ __device__ __forceinline__ uint32_t add_byte(uint32_t base, uint32_t x) {
     return r;
 }
 
-// Keeps a value in a VGPR so that loads indexed by it stay vector loads (scalar
-// loads share the LDS completion counter and would serialize the lookups).
-__device__ __forceinline__ int64_t lane_value(int64_t x) {
-    asm volatile("" : "+v"(x));
-    return x;
-}
-
 // One quarter (4 entries) of a 16-entry signed table from half (qr & 1) of an
 // 8-entry half table: quarters 0, 1 are T[0..3], T[4..7]; quarters 2, 3 negated.
 template <bool INT8>
@@ -83,17 +76,19 @@ __device__ __forceinline__ int4 table_quarter(uint2 h, int qr) {
     return make_int4(v[0], v[1], v[2], v[3]);
 }
 
-template <int BITS, int PW, int SW, int TW, bool INT8>
-__global__ __launch_bounds__(256) void lut_gemv2_kernel(LutParams p, int wfmt) {
+template <int BITS, int PW, int SW, int TW, int NW, bool INT8>
+__global__ __launch_bounds__(64 * NW) void lut_gemv2_kernel(LutParams p, int wfmt) {
+    constexpr int NT = 64 * NW;            // threads per workgroup
     constexpr int CW = 64 / (PW * SW);    // columns per workgroup
-    constexpr int S = 4 * SW;              // K slices per workgroup
+    constexpr int S = NW * SW;             // K slices per workgroup
     constexpr int CK = S * TW;             // 128-blocks per chunk
     constexpr int NPL = BITS / PW;         // bit-planes per lane
-    constexpr int QPT = CK * GPB * 4 / 256;  // table quarters staged per thread and chunk
+    constexpr int QPT = CK * GPB * 4 / NT; // table quarters staged per thread and chunk
+    static_assert(QPT * NT == CK * GPB * 4, "table quarters divide evenly over the threads");
     static_assert(TW * NPL <= 4, "at most four prefetched weight words per lane");
     __shared__ __attribute__((aligned(16))) char F[CK * KSTRIDE];
-    __shared__ float redf[4][CW];
-    __shared__ int redi[4][CW];
+    __shared__ float redf[NW][CW];
+    __shared__ int redi[NW][CW];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int c = lane % CW;
@@ -115,7 +110,7 @@ __global__ __launch_bounds__(256) void lut_gemv2_kernel(LutParams p, int wfmt) {
         const int nkb = (int)((kbB - kc) < CK ? (kbB - kc) : CK);
 #pragma unroll
         for (int r = 0; r < QPT; ++r) {
-            const int e = tid + 256 * r, g = e >> 2;
+            const int e = tid + NT * r, g = e >> 2;
             if (g < nkb * GPB) tq[r] = ((const uint2 *)(p.T + m * p.J + kc * GPB + g))[e & 1];
         }
 #pragma unroll
@@ -131,13 +126,15 @@ __global__ __launch_bounds__(256) void lut_gemv2_kernel(LutParams p, int wfmt) {
 
     float yf = 0.f;
     int yi = 0;
+    Epi ep{};
     for (int64_t kc = kbA; kc < kbB; kc += CK) {
         const int nkb = (int)((kbB - kc) < CK ? (kbB - kc) : CK);
         load_chunk(kc);
+        if (kc == kbA && p.splits == 1) ep = load_epi<INT8>(p, wfmt, m, n, true);
         lds_barrier();  // the previous chunk's tables are no longer read
 #pragma unroll
         for (int r = 0; r < QPT; ++r) {
-            const int e = tid + 256 * r, g = e >> 2;
+            const int e = tid + NT * r, g = e >> 2;
             if (g < nkb * GPB)
                 *(int4 *)(F + (g / GPB) * KSTRIDE + (g % GPB) * 64 + (e & 3) * 16) =
                     table_quarter<INT8>(tq[r], e & 3);
@@ -189,7 +186,7 @@ __global__ __launch_bounds__(256) void lut_gemv2_kernel(LutParams p, int wfmt) {
         }
     }
 
-    // combine the lanes of each column (fixed butterfly), then the four wavefronts in order
+    // combine the lanes of each column (fixed butterfly), then the wavefronts in order
 #pragma unroll
     for (int off = CW; off < 64; off <<= 1) {
         if (INT8)
@@ -203,11 +200,17 @@ __global__ __launch_bounds__(256) void lut_gemv2_kernel(LutParams p, int wfmt) {
     }
     lds_barrier();
     if (wave == 0 && lane < CW) {
-        const float sf = ((redf[0][lane] + redf[1][lane]) + redf[2][lane]) + redf[3][lane];
-        int si = redi[0][lane] + redi[1][lane] + redi[2][lane] + redi[3][lane];
-        if (INT8 && split == 0 && wfmt == LUTGEMM_WFMT_TERNARY) si += ((const int *)p.S)[m * p.Q];
+        float sf = redf[0][lane];
+        int si = redi[0][lane];
+#pragma unroll
+        for (int v = 1; v < NW; ++v) {
+            sf += redf[v][lane];
+            si += redi[v][lane];
+        }
         if (p.splits == 1)
-            store_out<INT8>(p, wfmt, p.per_tensor != 0, m, n, sf, si);
+            store_out<INT8>(p, wfmt, m, n, sf, si + ep.s0, ep);
+        else if (INT8 && split == 0 && wfmt == LUTGEMM_WFMT_TERNARY)
+            p.part[((int64_t)split * p.M + m) * p.N_pad + n] = __int_as_float(si + ((const int *)p.S)[m * p.Q]);
         else
             p.part[((int64_t)split * p.M + m) * p.N_pad + n] = INT8 ? __int_as_float(si) : sf;
     }
@@ -260,8 +263,12 @@ __global__ __launch_bounds__(256) void lut_gemv_split_kernel(LutParams p, int wf
                 ezr[kbl] = sz.sp * sz.zp * ((const float *)p.S)[lane_value(m * p.Q + q)];
         }
     }
-    int s_total = 0;
-    if (INT8 && split == 0 && wfmt == LUTGEMM_WFMT_TERNARY) s_total = ((const int *)p.S)[lane_value(m * p.Q)];
+    Epi ep{};
+    if (p.splits == 1)
+        ep = load_epi<INT8>(p, wfmt, m, n, true);
+    else if (INT8 && split == 0 && wfmt == LUTGEMM_WFMT_TERNARY)
+        ep.s0 = ((const int *)p.S)[lane_value(m * p.Q)];
+    const int s_total = ep.s0;
 #pragma unroll
     for (int r = 0; r < QPT; ++r) {
         const int e = tid + 256 * r, g = e >> 2;
@@ -298,7 +305,7 @@ __global__ __launch_bounds__(256) void lut_gemv_split_kernel(LutParams p, int wf
         }
     }
     if (p.splits == 1)
-        store_out<INT8>(p, wfmt, p.per_tensor != 0, m, n, yf, yi);
+        store_out<INT8>(p, wfmt, m, n, yf, yi, ep);
     else
         p.part[((int64_t)split * p.M + m) * p.N_pad + n] = INT8 ? __int_as_float(yi) : yf;
 }
@@ -320,11 +327,18 @@ static void launch_split(const LutParams &p, const Layout &L, const LutPlan &pla
     }
 }
 
+// NW wavefronts per workgroup with TW * NW fixed, so the chunk (and the LDS
+// footprint) is the same for every NW; more wavefronts hide more latency.
 template <int BITS, int PW, int SW, int TW, bool INT8>
 static void launch_cfg(const LutParams &p, const Layout &L, const LutPlan &plan, hipStream_t s) {
     constexpr int CW = 64 / (PW * SW);
     const dim3 grid((unsigned)((L.N + CW - 1) / CW), (unsigned)plan.splits, (unsigned)p.M);
-    hipLaunchKernelGGL((lut_gemv2_kernel<BITS, PW, SW, TW, INT8>), grid, dim3(256), 0, s, p, L.wfmt);
+    if (plan.gemv_nw == 16 && TW % 4 == 0)
+        hipLaunchKernelGGL((lut_gemv2_kernel<BITS, PW, SW, (TW + 3) / 4, 16, INT8>), grid, dim3(1024), 0, s, p, L.wfmt);
+    else if (plan.gemv_nw >= 8 && TW % 2 == 0)
+        hipLaunchKernelGGL((lut_gemv2_kernel<BITS, PW, SW, (TW + 1) / 2, 8, INT8>), grid, dim3(512), 0, s, p, L.wfmt);
+    else
+        hipLaunchKernelGGL((lut_gemv2_kernel<BITS, PW, SW, TW, 4, INT8>), grid, dim3(256), 0, s, p, L.wfmt);
 }
 
 // Lane decompositions (PW, SW, TW) offered per bit width, indexed by LutPlan::gemv_cfg:

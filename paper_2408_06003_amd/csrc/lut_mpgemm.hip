@@ -141,7 +141,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void l
     if (p.splits == 1) {
 #pragma unroll
         for (int r = 0; r < MT; ++r)
-            if (r < rows) store_out<INT8>(p, wfmt, per_tensor, m0 + r, n, yf[r], yi[r]);
+            if (r < rows) store_out<INT8>(p, wfmt, m0 + r, n, yf[r], yi[r], load_epi<INT8>(p, wfmt, m0 + r, n, false));
         return;
     }
     float vals[MT];
@@ -162,10 +162,11 @@ __global__ __launch_bounds__(64) void lut_finalize_kernel(LutParams p, int wfmt,
                                                           int64_t m_alloc) {
     const int64_t n = (int64_t)blockIdx.x * 64 + threadIdx.x;
     const int64_t m = blockIdx.y;
+    const Epi ep = load_epi<INT8>(p, wfmt, m, n, false);
     float sf;
     int si;
     sum_partials<INT8>(p, m_alloc, m, n, sf, si);
-    store_out<INT8>(p, wfmt, per_tensor_i != 0, m, n, sf, si);
+    store_out<INT8>(p, wfmt, m, n, sf, si, ep);
 }
 
 // ------------------------------------------------------------------ dispatch
