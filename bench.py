@@ -150,6 +150,14 @@ class Case:
         self.precompute()
         self.mpgemm(i)
 
+    def fused(self, i):
+        """The same step through lutgemm_mpgemm_fused (tables built inside the LUT kernel)."""
+        if not hasattr(self, "fws"):
+            n = self.L.fused_workspace_size(self.p, self.M)
+            self.fws = self.torch.empty(n, dtype=self.torch.uint8, device="cuda") if n else None
+        self.L.mpgemm_fused(self.p, self.M, self.act, self.packed[i % len(self.packed)], self.out,
+                            self.out_code, False, workspace=self.fws)
+
     def timed(self, fn, n, graph=True, check=None):
         """Average milliseconds per call over n back-to-back calls, timed with HIP events
         on the stream they run on.  With graph=True the n calls are captured once into a
@@ -210,6 +218,7 @@ class Case:
         wb = self.L.packed_weight_size(self.p)
         ms_rd = self.timed(lambda i: self.L.calibrate_stream_read(self.packed[i % len(self.packed)], wb, sink, 1024),
                            n_kernel)
+        ms_fu = self.timed(self.fused, n_kernel, check=lambda: self.out)
         rec = {"workload": self.name, "M": self.M, "K": self.K, "N": self.N, "bits": self.inp.bits,
                "mpgemm_us": round(ms_mp * 1e3, 3), "mpgemm_tops": round(self.effective_tops(ms_mp), 3),
                "mpgemm_gbps": round(gbps, 1), "hbm_frac": round(gbps / HBM_PEAK_GBPS, 4),
@@ -218,6 +227,7 @@ class Case:
                "frac_of_stream_read": round(ms_rd / ms_mp, 4),
                "precompute_us": round(ms_pre * 1e3, 3),
                "precompute_over_mpgemm": round(ms_pre / ms_mp, 4),
+               "fused_us": round(ms_fu * 1e3, 3), "fused_tops": round(self.effective_tops(ms_fu), 3),
                "algorithmic_bytes": b["total"], "rotation_copies": len(self.packed)}
         if self.M >= 16 and not self.int8:
             out = self.torch.empty((self.M, self.N), dtype=self.torch.float16, device="cuda")
@@ -298,6 +308,7 @@ def main():
     torch.cuda.synchronize()
     ms_step = head.timed(head.step, K, check=lambda: head.out)
     ms_step_eager = head.timed(head.step, K, graph=False)
+    ms_fused = head.timed(head.fused, K, check=lambda: head.out)
     kern = head.measure(max(K, 50), 5)
     log(f"headline: {ms_step * 1e3:.2f} us/step, mpgemm {kern['mpgemm_us']} us, {kern['mpgemm_gbps']} GB/s")
     achieved = kern["mpgemm_gbps"]
@@ -330,6 +341,8 @@ def main():
         "hbm_gbps_step": round(kern["algorithmic_bytes"] / (ms_step * 1e-3) / 1e9, 1),
         "roofline": roofline,
         "headline_kernels": kern,
+        "fused_step": {"us": round(ms_fused * 1e3, 3), "tops": round(head.effective_tops(ms_fused), 4),
+                       "entry": "lutgemm_mpgemm_fused"},
     }
     head_inp = head.inp
     head.release()

@@ -194,6 +194,38 @@ lutgemm_status_t lutgemm_mpgemm(const lutgemm_problem_t *problem, int64_t M, con
                                 void *stream);
 
 /*
+ * Bytes of scratch memory lutgemm_mpgemm_fused needs for M tokens; may be 0.  No
+ * initialization is required; a workspace must not be shared by calls that run
+ * concurrently.
+ */
+size_t lutgemm_fused_workspace_size(const lutgemm_problem_t *problem, int64_t M);
+
+/*
+ * Table precompute fused into the LUT mpGEMM (Section 3.1.1 splits the
+ * precompute out of the lookup so that it can be fused; this fuses it on the
+ * consumer side): O = A x W^T (+ O) from act [M][K] FP16 (device) and the packed
+ * weights, with the same activation quantization (ACT_INT8) or power-of-two
+ * token scaling (ACT_FP16) and the same FP16 / INT16 table entries as
+ * lutgemm_precompute + lutgemm_mpgemm.  For single tokens with weights the
+ * whole-K lookup kernel takes (at most a few MB), every workgroup builds its
+ * tables in LDS from the activations: one kernel (plus a split-K sum when K is
+ * split), no table buffer.  Otherwise it runs lutgemm_precompute into the
+ * workspace followed by lutgemm_mpgemm.
+ *   act        device FP16 [M][K]
+ *   packed, out, out_dtype, accumulate   as for lutgemm_mpgemm
+ *   workspace  device, workspace_bytes >= lutgemm_fused_workspace_size(problem, M);
+ *              may be NULL when that size is 0
+ * INT8 activations: results are bitwise those of lutgemm_precompute +
+ * lutgemm_mpgemm.  FP16 activations: the zero-point term is summed per 128-block
+ * instead of per quantization group, so results agree with the two-call path to
+ * FP32 rounding.  Bitwise reproducible run to run.
+ */
+lutgemm_status_t lutgemm_mpgemm_fused(const lutgemm_problem_t *problem, int64_t M, const void *act,
+                                      const void *packed, void *out, int32_t out_dtype,
+                                      int32_t accumulate, void *workspace, size_t workspace_bytes,
+                                      void *stream);
+
+/*
  * Comparison path (Section 2.2, dequantization-based mpGEMM): rebuilds FP16
  * weights s (q - z) from the same packed buffer and multiplies them with FP16
  * activations act [M][K] on the matrix cores (FP32 accumulation).  ACT_FP16

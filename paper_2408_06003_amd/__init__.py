@@ -7,7 +7,7 @@ package raises ``ImportError`` -- there is no CPU fallback.
 
 Low-level functions mirror the C entry points (``validate``, ``packed_weight_size``,
 ``table_size``, ``table_offsets``, ``workspace_size``, ``pack_weights``,
-``precompute``, ``mpgemm``, ``mpgemm_dequant``); ``LutGemm`` is a small holder that
+``precompute``, ``mpgemm``, ``fused_workspace_size``, ``mpgemm_fused``, ``mpgemm_dequant``); ``LutGemm`` is a small holder that
 allocates the packed weights, tables and workspace with torch and calls them.
 """
 from __future__ import annotations
@@ -34,6 +34,7 @@ EXPORTS = [
     "lutgemm_status_string", "lutgemm_version", "lutgemm_last_error", "lutgemm_validate", "lutgemm_packed_weight_size",
     "lutgemm_table_size", "lutgemm_table_offsets", "lutgemm_workspace_size", "lutgemm_pack_weights",
     "lutgemm_precompute", "lutgemm_mpgemm", "lutgemm_mpgemm_dequant", "lutgemm_calibrate_stream_read",
+    "lutgemm_fused_workspace_size", "lutgemm_mpgemm_fused",
 ]
 
 
@@ -88,6 +89,10 @@ def _load():
     L.lutgemm_mpgemm.argtypes = [PP, I64, P, P, P, I32, I32, P, SZ, P]
     L.lutgemm_mpgemm_dequant.restype = ctypes.c_int
     L.lutgemm_mpgemm_dequant.argtypes = [PP, I64, P, P, P, I32, I32, P]
+    L.lutgemm_fused_workspace_size.restype = SZ
+    L.lutgemm_fused_workspace_size.argtypes = [PP, I64]
+    L.lutgemm_mpgemm_fused.restype = ctypes.c_int
+    L.lutgemm_mpgemm_fused.argtypes = [PP, I64, P, P, P, I32, I32, P, SZ, P]
     L.lutgemm_calibrate_stream_read.restype = ctypes.c_int
     L.lutgemm_calibrate_stream_read.argtypes = [P, SZ, P, I32, P]
     return L
@@ -175,6 +180,19 @@ def mpgemm(p: Problem, M: int, tables, packed, out, out_dtype: int, accumulate: 
            "lutgemm_mpgemm")
 
 
+def fused_workspace_size(p: Problem, M: int) -> int:
+    return lib.lutgemm_fused_workspace_size(ctypes.byref(p), M)
+
+
+def mpgemm_fused(p: Problem, M: int, act, packed, out, out_dtype: int, accumulate: bool = False,
+                 workspace=None, stream=None, workspace_bytes=None):
+    if workspace_bytes is None:
+        workspace_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(lib.lutgemm_mpgemm_fused(ctypes.byref(p), M, _ptr(act), _ptr(packed), _ptr(out), out_dtype,
+                                    1 if accumulate else 0, _ptr(workspace), workspace_bytes, _stream(stream)),
+           "lutgemm_mpgemm_fused")
+
+
 def mpgemm_dequant(p: Problem, M: int, act, packed, out, out_dtype: int, accumulate: bool = False,
                    stream=None):
     _check(lib.lutgemm_mpgemm_dequant(ctypes.byref(p), M, _ptr(act), _ptr(packed), _ptr(out), out_dtype,
@@ -234,6 +252,26 @@ class LutGemm:
         precompute(self.p, M, act, t, stream=stream)
         mpgemm(self.p, M, t, self.packed, out, self.out_dtype_code(out.dtype), accumulate,
                workspace=self.workspace(M), stream=stream)
+        return out
+
+    def fused_workspace(self, M: int):
+        import torch
+        n = fused_workspace_size(self.p, M)
+        if n == 0:
+            return None
+        key = ("fused", M)
+        if key not in self._ws:
+            self._ws[key] = torch.empty(n, dtype=torch.uint8, device=self.device)
+        return self._ws[key]
+
+    def fused(self, act, out=None, out_dtype=None, accumulate=False, stream=None):
+        """Same product through lutgemm_mpgemm_fused (tables built inside the LUT kernel)."""
+        import torch
+        M = act.shape[0]
+        if out is None:
+            out = torch.empty((M, self.p.N), dtype=out_dtype or torch.float16, device=self.device)
+        mpgemm_fused(self.p, M, act, self.packed, out, self.out_dtype_code(out.dtype), accumulate,
+                     workspace=self.fused_workspace(M), stream=stream)
         return out
 
     def dequant(self, act, out=None, out_dtype=None, accumulate=False, stream=None):

@@ -1,7 +1,7 @@
 // C ABI of the LUT mpGEMM library: argument validation, size queries, launch
 // planning and dispatch.  Everything here runs on the host; the arithmetic of
-// every step runs in the HIP kernels of pack.hip, precompute.hip,
-// lut_mpgemm.hip and dequant_mfma.hip.
+// every step runs in the HIP kernels of pack.hip, precompute.hip, lut_gemv.hip,
+// lut_mpgemm.hip, lut_fused.hip and dequant_mfma.hip.
 #include <hip/hip_runtime.h>
 
 #include <cstdio>
@@ -156,6 +156,82 @@ LutPlan plan_lut(const Layout &L, int64_t M) {
 
 }  // namespace lutgemm
 
+namespace lutgemm {
+
+// Kernel parameters of one LUT mpGEMM call (tables in the layout of lutgemm_table_size).
+static LutParams lut_params(const Layout &L, const LutPlan &plan, int64_t M, const void *tables,
+                            const void *packed, void *out, int32_t out_dtype, int32_t accumulate,
+                            void *partials) {
+    TableLayout T = make_table_layout(L, M);
+    LutParams lp{};
+    lp.T = (const uint4 *)tables;
+    lp.S = tables ? (const char *)tables + T.s_off : nullptr;
+    lp.tok = tables ? (const float *)((const char *)tables + T.tok_off) : nullptr;
+    lp.planes = (const uint4 *)packed;
+    lp.meta = (const char *)packed + L.meta_off;
+    lp.out = out;
+    lp.part = plan.splits > 1 ? (float *)partials : nullptr;
+    lp.M = M;
+    lp.N = L.N;
+    lp.N_pad = L.N_pad;
+    lp.K = L.K;
+    lp.KB = L.KB;
+    lp.J = L.J;
+    lp.Q = L.Q;
+    lp.G = L.G;
+    lp.splits = plan.splits;
+    lp.kbs = plan.kbs;
+    lp.kpg = (int)(L.G / KBLK);
+    lp.per_tensor = L.per_tensor ? 1 : 0;
+    lp.inv_kpg = 1.0f / (float)lp.kpg;
+    if (L.wfmt == LUTGEMM_WFMT_BINARY) {  // codes {0,1} read as {-1,+1}: s' = s, z' = 0
+        lp.cs = 1.f;
+        lp.cz = 0.f;
+        lp.c0 = 0.f;
+    } else if (L.wfmt == LUTGEMM_WFMT_TERNARY) {  // q = w + 1, z = 1, b = 2: s' = s/2, z' = -1
+        lp.cs = 0.5f;
+        lp.cz = 0.f;
+        lp.c0 = -1.f;
+    } else {  // Eq. 2: s' = s/2, z' = 2z + 1 - 2^b
+        lp.cs = 0.5f;
+        lp.cz = 2.f;
+        lp.c0 = 1.f - (float)(1 << L.bits);
+    }
+    lp.out_dtype = out_dtype;
+    lp.accumulate = accumulate;
+    return lp;
+}
+
+static void log_plan(const char *who, const Layout &L, const LutPlan &plan, int64_t M) {
+    std::fprintf(stderr, "%s: M=%lld K=%lld N=%lld b=%d kind=%d cfg=%d nw=%d kbs=%d splits=%d mt=%d grid=%lldx%dx%lld\n",
+                 who, (long long)M, (long long)L.K, (long long)L.N, L.bits, plan.kind, plan.gemv_cfg, plan.gemv_nw,
+                 plan.kbs, plan.splits, plan.mt, (long long)plan.n_tiles, plan.splits, (long long)plan.m_tiles);
+}
+
+// Scratch of lutgemm_mpgemm_fused: the fused GEMV needs partial sums and the
+// per-token factors only when it splits K; otherwise tables, then the partials.
+struct FusedScratch {
+    bool fused;
+    size_t tables, part_off, tok_off, total;
+};
+
+static FusedScratch fused_scratch(const Layout &L, const LutPlan &plan, int64_t M) {
+    FusedScratch f{};
+    f.fused = plan.kind == 0;
+    if (f.fused) {
+        f.part_off = 0;
+        f.tok_off = plan.ws_bytes;
+        f.total = plan.splits > 1 ? plan.ws_bytes + align256((size_t)M * 4) : 0;
+    } else {
+        f.tables = make_table_layout(L, M).total;
+        f.part_off = align256(f.tables);
+        f.total = f.part_off + plan.ws_bytes;
+    }
+    return f;
+}
+
+}  // namespace lutgemm
+
 extern "C" {
 
 const char *lutgemm_status_string(lutgemm_status_t s) {
@@ -272,48 +348,52 @@ lutgemm_status_t lutgemm_mpgemm(const lutgemm_problem_t *problem, int64_t M, con
         if (!workspace || !aligned16(workspace)) return LUTGEMM_ERROR_INVALID_VALUE;
         if (workspace_bytes < plan.ws_bytes) return LUTGEMM_ERROR_INSUFFICIENT_SIZE;
     }
-    TableLayout T = make_table_layout(L, M);
-    LutParams lp{};
-    lp.T = (const uint4 *)tables;
-    lp.S = (const char *)tables + T.s_off;
-    lp.tok = (const float *)((const char *)tables + T.tok_off);
-    lp.planes = (const uint4 *)packed;
-    lp.meta = (const char *)packed + L.meta_off;
-    lp.out = out;
-    lp.part = plan.ws_bytes ? (float *)workspace : nullptr;
-    lp.M = M;
-    lp.N = L.N;
-    lp.N_pad = L.N_pad;
-    lp.K = L.K;
-    lp.KB = L.KB;
-    lp.J = L.J;
-    lp.Q = L.Q;
-    lp.G = L.G;
-    lp.splits = plan.splits;
-    lp.kbs = plan.kbs;
-    lp.kpg = (int)(L.G / KBLK);
-    lp.per_tensor = L.per_tensor ? 1 : 0;
-    lp.inv_kpg = 1.0f / (float)lp.kpg;
-    if (L.wfmt == LUTGEMM_WFMT_BINARY) {  // codes {0,1} read as {-1,+1}: s' = s, z' = 0
-        lp.cs = 1.f;
-        lp.cz = 0.f;
-        lp.c0 = 0.f;
-    } else if (L.wfmt == LUTGEMM_WFMT_TERNARY) {  // q = w + 1, z = 1, b = 2: s' = s/2, z' = -1
-        lp.cs = 0.5f;
-        lp.cz = 0.f;
-        lp.c0 = -1.f;
-    } else {  // Eq. 2: s' = s/2, z' = 2z + 1 - 2^b
-        lp.cs = 0.5f;
-        lp.cz = 2.f;
-        lp.c0 = 1.f - (float)(1 << L.bits);
-    }
-    lp.out_dtype = out_dtype;
-    lp.accumulate = accumulate;
-    if (env_int("LUTGEMM_LOG", 0))
-        std::fprintf(stderr, "lutgemm_mpgemm: M=%lld K=%lld N=%lld b=%d kind=%d cfg=%d nw=%d kbs=%d splits=%d mt=%d grid=%lldx%dx%lld\n",
-                     (long long)M, (long long)L.K, (long long)L.N, L.bits, plan.kind, plan.gemv_cfg, plan.gemv_nw, plan.kbs,
-                     plan.splits, plan.mt, (long long)plan.n_tiles, plan.splits, (long long)plan.m_tiles);
+    LutParams lp = lut_params(L, plan, M, tables, packed, out, out_dtype, accumulate, workspace);
+    if (env_int("LUTGEMM_LOG", 0)) log_plan("lutgemm_mpgemm", L, plan, M);
     return hip_status(launch_lut(lp, L, plan, stream));
+}
+
+size_t lutgemm_fused_workspace_size(const lutgemm_problem_t *problem, int64_t M) {
+    if (check_problem(problem, M) != LUTGEMM_SUCCESS) return 0;
+    Layout L = make_layout(*problem);
+    return fused_scratch(L, plan_lut(L, M), M).total;
+}
+
+lutgemm_status_t lutgemm_mpgemm_fused(const lutgemm_problem_t *problem, int64_t M, const void *act,
+                                      const void *packed, void *out, int32_t out_dtype, int32_t accumulate,
+                                      void *workspace, size_t workspace_bytes, void *stream) {
+    lutgemm_status_t st = check_problem(problem, M);
+    if (st != LUTGEMM_SUCCESS) return st;
+    if (!act || !packed || !out) return LUTGEMM_ERROR_INVALID_VALUE;
+    if (!aligned16(act) || !aligned16(packed) || !aligned16(out)) return LUTGEMM_ERROR_INVALID_VALUE;
+    if (out_dtype != LUTGEMM_OUT_FP16 && out_dtype != LUTGEMM_OUT_FP32 && out_dtype != LUTGEMM_OUT_INT32)
+        return LUTGEMM_ERROR_INVALID_VALUE;
+    if (out_dtype == LUTGEMM_OUT_INT32 && problem->act != LUTGEMM_ACT_INT8) return LUTGEMM_ERROR_NOT_SUPPORTED;
+    if (accumulate != 0 && accumulate != 1) return LUTGEMM_ERROR_INVALID_VALUE;
+    Layout L = make_layout(*problem);
+    LutPlan plan = plan_lut(L, M);
+    FusedScratch fs = fused_scratch(L, plan, M);
+    if (fs.total > 0) {
+        if (!workspace || !aligned16(workspace)) return LUTGEMM_ERROR_INVALID_VALUE;
+        if (workspace_bytes < fs.total) return LUTGEMM_ERROR_INSUFFICIENT_SIZE;
+    }
+    char *ws = (char *)workspace;
+    if (env_int("LUTGEMM_LOG", 0)) log_plan(fs.fused ? "lutgemm_mpgemm_fused" : "lutgemm_mpgemm_fused(unfused)", L, plan, M);
+    if (!fs.fused) {  // precompute into the workspace, then the table-fed kernels
+        st = lutgemm_precompute(problem, M, act, ws, fs.tables, stream);
+        if (st != LUTGEMM_SUCCESS) return st;
+        LutParams lp = lut_params(L, plan, M, ws, packed, out, out_dtype, accumulate, ws + fs.part_off);
+        return hip_status(launch_lut(lp, L, plan, stream));
+    }
+    LutParams lp = lut_params(L, plan, M, nullptr, packed, out, out_dtype, accumulate, ws + fs.part_off);
+    lp.act = (const uint16_t *)act;
+    lp.tok_out = plan.splits > 1 ? (float *)(ws + fs.tok_off) : nullptr;
+    int e = launch_fused_gemv(lp, L, plan, stream);
+    if (e == 0 && plan.splits > 1) {
+        lp.tok = lp.tok_out;  // the finalize kernel scales with the factors the fused kernel wrote
+        e = launch_finalize(lp, L, plan, stream);
+    }
+    return hip_status(e);
 }
 
 lutgemm_status_t lutgemm_mpgemm_dequant(const lutgemm_problem_t *problem, int64_t M, const void *act,

@@ -46,6 +46,48 @@ __device__ __forceinline__ int lds_i32(const char *base, uint32_t off) {
     return *(const int *)(base + off);
 }
 
+constexpr int KSTRIDE = GPB * 64 + 64;  // LDS bytes per 128-block: 32 tables x 16 INT32, + 64 B pad
+
+// base + (byte B of x), one VALU op (SDWA byte select).
+template <int B>
+__device__ __forceinline__ uint32_t add_byte(uint32_t base, uint32_t x) {
+    uint32_t r;
+    if constexpr (B == 0)
+        asm("v_add_u32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_0"
+            : "=v"(r) : "v"(base), "v"(x));
+    else if constexpr (B == 1)
+        asm("v_add_u32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_1"
+            : "=v"(r) : "v"(base), "v"(x));
+    else if constexpr (B == 2)
+        asm("v_add_u32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_2"
+            : "=v"(r) : "v"(base), "v"(x));
+    else
+        asm("v_add_u32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_3"
+            : "=v"(r) : "v"(base), "v"(x));
+    return r;
+}
+
+// Sum of the 32 entries addressed by one 16-byte plane word (the 4-bit indices of
+// one 128-block, index i at bits 4 (i % 8) of 32-bit word i / 8) in the signed
+// 16-entry INT32 tables of that block, which start at byte `base` of F with a
+// stride of 64 bytes per 4-activation group.  A lookup is one SDWA byte-add, one
+// ds_read_b32 and half a v_add3_u32.  On the FP path entries are below 2^22 in
+// magnitude, so sum_t 2^t (word sum of plane t) stays below 15 * 32 * 2^22 < 2^31.
+__device__ __forceinline__ int lookup_word(const char *F, uint32_t base, uint4 w) {
+    const uint32_t wd[4] = {w.x, w.y, w.z, w.w};
+    int acc = 0;
+#pragma unroll
+    for (int d = 0; d < 4; ++d) {
+        const uint32_t lo = (wd[d] << 2) & 0x3C3C3C3Cu, hi = (wd[d] >> 2) & 0x3C3C3C3Cu;
+        const char *Fg = F + d * 8 * 64;
+        acc += lds_i32(Fg + 0 * 64, add_byte<0>(base, lo)) + lds_i32(Fg + 1 * 64, add_byte<0>(base, hi));
+        acc += lds_i32(Fg + 2 * 64, add_byte<1>(base, lo)) + lds_i32(Fg + 3 * 64, add_byte<1>(base, hi));
+        acc += lds_i32(Fg + 4 * 64, add_byte<2>(base, lo)) + lds_i32(Fg + 5 * 64, add_byte<2>(base, hi));
+        acc += lds_i32(Fg + 6 * 64, add_byte<3>(base, lo)) + lds_i32(Fg + 7 * 64, add_byte<3>(base, hi));
+    }
+    return acc;
+}
+
 // Expand one half table (8 entries, 16 bytes) into a 16-entry INT32 signed table.
 template <bool INT8>
 __device__ __forceinline__ void expand_table(const uint4 h, int *dst) {
@@ -118,7 +160,7 @@ __device__ __forceinline__ Epi load_epi(const LutParams &p, int wfmt, int64_t m,
     Epi e{1.f, 1.f, 0.f, 0};
     if (n >= p.N) return e;
     const int64_t mv = lane_value(m), nv = lane_value(n), o = mv * p.N + nv;
-    e.tok = p.tok[mv];
+    if (p.tok) e.tok = p.tok[mv];
     if (INT8) {
         e.sw = int_weight_scale(p, p.per_tensor != 0, p.per_tensor ? lane_value(0) : nv);
         if (first_split && wfmt == LUTGEMM_WFMT_TERNARY) e.s0 = ((const int *)p.S)[mv * p.Q];

@@ -1,0 +1,350 @@
+// Single-token LUT mpGEMM with the table precompute fused into it on the consumer
+// side (LUT Tensor Core, Section 3.1.1: the precompute is split out of the
+// lookup so it can be fused; here it is fused into the lookup kernel itself).
+//
+// Each workgroup of the whole-K GEMV (lut_gemv.hip) reads the token's FP16
+// activations instead of precomputed half tables and builds its signed 16-entry
+// tables in LDS directly:
+//   1. amax = max |a| over the whole token (every workgroup reads the token,
+//      8 KiB at K = 4096, from L2); INT8 path: q = clamp(rint(a * (127 / amax)),
+//      -127, 127) and s_a = amax / 127; FP path: the token is scaled by 2^-e with
+//      amax = f 2^e, f in [0.5, 1).  Same FP32 operations as the precompute
+//      operator, so the tables are bitwise the ones it would produce.
+//   2. Per 4-activation group, the entries F[s i] = (s ? -1 : 1) T[i] of Eq. 4-5
+//      (T[i] = -x0 + sum_{e=1..3} (bit (3-e) of i ? x_e : -x_e), rounded to FP16
+//      on the FP path as in the stored tables), one quarter (4 entries) per lane.
+//   3. The activation sums: per 128-block S_kb on the FP path (zero-point term of
+//      Eq. 3), per chunk on the INT8 path (ternary integer offset), by fixed-order
+//      DPP sums over the lanes that built the tables.
+// Lane e of a round quantizes (or scales) activation e of the chunk once; the four
+// lanes of a DPP quad hold the four activations of one group and exchange them by
+// quad broadcasts, each then building one quarter of the group's table.
+// The weights of the chunk are loaded before any of this, so their memory latency
+// overlaps the table build; lookups and epilogue are those of lut_gemv.hip.  The
+// zero-point term is applied per 128-block: s'_q z'_q S_q = sum over the blocks
+// of group q of s'_q z'_q S_kb.
+#include "lut_common.h"
+
+namespace lutgemm {
+
+template <bool INT8>
+__device__ __forceinline__ float act_value(uint32_t bits16, float scale) {
+    const float a = h2f(bits16);
+    if (INT8) return fminf(fmaxf(rintf(a * scale), -127.f), 127.f);
+    return a * scale;  // exact: scale is a power of two
+}
+
+__device__ __forceinline__ float absmax4(uint2 v) {
+    return fmaxf(fmaxf(fabsf(h2f(v.x & 0xFFFFu)), fabsf(h2f(v.x >> 16))),
+                 fmaxf(fabsf(h2f(v.y & 0xFFFFu)), fabsf(h2f(v.y >> 16))));
+}
+
+// Entries 4 qr .. 4 qr + 3 of the signed 16-entry table of x0..x3: quarter qr
+// holds rows 4 (qr & 1) .. + 3 of the half table, negated when qr >= 2 (Eq. 4).
+// Sums are formed in the order ((-x0 + (+-x1)) + (+-x2)) + (+-x3).
+template <bool INT8>
+__device__ __forceinline__ int4 quarter_entries(float x0, float x1, float x2, float x3, int qr) {
+    const float b = -x0 + ((qr & 1) ? x1 : -x1);
+    const float u0 = b + (-x2), u1 = b + x2;
+    const float t[4] = {u0 + (-x3), u0 + x3, u1 + (-x3), u1 + x3};
+    int v[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        if (INT8)
+            v[i] = (int)t[i];  // |t| <= 508, exact
+        else
+            v[i] = (int)rintf(__half2float(__float2half_rn(t[i])) * (float)(1 << FIX_SHIFT));
+        if (qr >= 2) v[i] = -v[i];
+    }
+    return make_int4(v[0], v[1], v[2], v[3]);
+}
+
+// Value of lane 4 (l / 4) + I for lane l (DPP quad_perm broadcast).
+template <int I>
+__device__ __forceinline__ int quad_bcast(int v) {
+    return __builtin_amdgcn_mov_dpp(v, I * 0x55, 0xF, 0xF, false);
+}
+
+// Integer form of quarter_entries for the INT8 path (exact: |entry| <= 508).
+__device__ __forceinline__ int4 quarter_entries_int(int q0, int q1, int q2, int q3, int qr) {
+    const int sg = qr >= 2 ? -1 : 1;
+    const int b = sg * (((qr & 1) ? q1 : -q1) - q0);
+    const int p2 = sg * q2, p3 = sg * q3;
+    return make_int4(b - p2 - p3, b - p2 + p3, b + p2 - p3, b + p2 + p3);
+}
+
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ float dpp_f(float v) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, ROW_MASK, 0xF, true));
+}
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ int dpp_i(int v) {
+    return __builtin_amdgcn_update_dpp(0, v, CTRL, ROW_MASK, 0xF, true);
+}
+
+// Sum over the 64 lanes of a wavefront in a fixed order (row shifts 1, 2, 4, 8,
+// then row broadcasts 15 and 31); the total is in lane 63.
+__device__ __forceinline__ float wave_sum_f(float v) {
+    v += dpp_f<0x111, 0xF>(v);
+    v += dpp_f<0x112, 0xF>(v);
+    v += dpp_f<0x114, 0xF>(v);
+    v += dpp_f<0x118, 0xF>(v);
+    v += dpp_f<0x142, 0xA>(v);
+    v += dpp_f<0x143, 0xC>(v);
+    return v;
+}
+__device__ __forceinline__ int wave_sum_i(int v) {
+    v += dpp_i<0x111, 0xF>(v);
+    v += dpp_i<0x112, 0xF>(v);
+    v += dpp_i<0x114, 0xF>(v);
+    v += dpp_i<0x118, 0xF>(v);
+    v += dpp_i<0x142, 0xA>(v);
+    v += dpp_i<0x143, 0xC>(v);
+    return v;
+}
+// Maximum over the 64 lanes (any order gives the same result); in lane 63.
+__device__ __forceinline__ float wave_max(float v) {
+    v = fmaxf(v, dpp_f<0x111, 0xF>(v));
+    v = fmaxf(v, dpp_f<0x112, 0xF>(v));
+    v = fmaxf(v, dpp_f<0x114, 0xF>(v));
+    v = fmaxf(v, dpp_f<0x118, 0xF>(v));
+    v = fmaxf(v, dpp_f<0x142, 0xA>(v));
+    v = fmaxf(v, dpp_f<0x143, 0xC>(v));
+    return v;
+}
+
+template <int BITS, int PW, int SW, int TW, int NW, bool INT8>
+__global__ __launch_bounds__(64 * NW) void lut_fused_gemv_kernel(LutParams p, int wfmt) {
+    constexpr int NT = 64 * NW;            // threads per workgroup
+    constexpr int CW = 64 / (PW * SW);    // columns per workgroup
+    constexpr int S = NW * SW;             // K slices per workgroup
+    constexpr int CK = S * TW;             // 128-blocks per chunk
+    constexpr int NPL = BITS / PW;         // bit-planes per lane
+    constexpr int QPT = CK * GPB * 4 / NT; // table quarters built per thread and chunk
+    constexpr int BPR = NT / 128;          // 128-blocks covered by one round of quarters
+    static_assert(QPT * NT == CK * GPB * 4 && NT % 128 == 0, "quarters divide evenly over the threads");
+    static_assert(TW * NPL <= 4, "at most four prefetched weight words per lane");
+    __shared__ __attribute__((aligned(16))) char F[CK * KSTRIDE];
+    __shared__ float redf[NW][CW];
+    __shared__ int redi[NW][CW];
+    __shared__ float hsf[QPT * NW];  // FP path: half-block activation sums, [round][wave]
+    __shared__ int hsi[NW];          // INT8 path: activation sum of the chunk, per wave
+    __shared__ float wmax[NW];
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int c = lane % CW;
+    const int pl = (lane / CW) % PW;
+    const int sl = lane / (CW * PW);
+    const int sigma = wave * SW + sl;
+    const int64_t n = (int64_t)blockIdx.x * CW + c;
+    const int64_t m = blockIdx.z;
+    const int split = blockIdx.y;
+    const int64_t kbA = (int64_t)split * p.kbs;
+    const int64_t kbB = (kbA + p.kbs < p.KB) ? kbA + p.kbs : p.KB;
+    const uint16_t *a1 = p.act + m * p.K;
+    const uint2 *a4 = (const uint2 *)a1;  // one 4-activation group per element
+    const bool need_s = wfmt != LUTGEMM_WFMT_BINARY;   // binary weights have z' = 0
+
+    uint4 w[TW][NPL];
+    auto load_weights = [&](int64_t kc, int nkb) {
+#pragma unroll
+        for (int t = 0; t < TW; ++t) {
+            const int kbl = sigma + t * S;
+            if (kbl < nkb) {
+#pragma unroll
+                for (int i = 0; i < NPL; ++i)
+                    w[t][i] = p.planes[((kc + kbl) * BITS + pl * NPL + i) * p.N_pad + n];
+            }
+        }
+    };
+    // lane e of a round holds activation e of the chunk: the 4 lanes of a quad are the
+    // 4 activations of one table group, and build the group's 4 table quarters
+    uint32_t av[QPT];
+    auto load_acts = [&](int64_t kc, int nkb) {
+#pragma unroll
+        for (int r = 0; r < QPT; ++r) {
+            const int e = tid + NT * r;
+            av[r] = e < nkb * KBLK ? (uint32_t)a1[kc * KBLK + e] : 0u;
+        }
+    };
+
+    // weights and activations of the first chunk, then the epilogue operands
+    int nkb = (int)((kbB - kbA) < CK ? (kbB - kbA) : CK);
+    load_weights(kbA, nkb);
+    load_acts(kbA, nkb);
+    Epi ep{};
+    if (p.splits == 1) ep = load_epi<INT8>(p, wfmt, m, n, false);
+
+    // 1. amax of the whole token: the first chunk from registers, the rest from memory
+    float amax = 0.f;
+#pragma unroll
+    for (int r = 0; r < QPT; ++r) amax = fmaxf(amax, fabsf(h2f(av[r])));
+    const int64_t j0 = kbA * GPB, j1 = j0 + (int64_t)nkb * GPB;
+    for (int64_t j = tid; j < p.J; j += NT)
+        if (j < j0 || j >= j1) amax = fmaxf(amax, absmax4(a4[j]));
+    amax = wave_max(amax);
+    if (lane == 63) wmax[wave] = amax;
+    lds_barrier();
+    amax = wmax[0];
+#pragma unroll
+    for (int v = 1; v < NW; ++v) amax = fmaxf(amax, wmax[v]);
+    float scale, tok;
+    if (INT8) {
+        scale = amax == 0.f ? 0.f : __fdiv_rn(127.0f, amax);
+        tok = amax == 0.f ? 0.f : __fdiv_rn(amax, 127.0f);
+    } else if (amax == 0.f) {
+        scale = 1.f;
+        tok = 1.f;
+    } else {
+        int e;
+        (void)frexpf(amax, &e);
+        scale = ldexpf(1.f, -e);
+        tok = ldexpf(1.f, e);
+    }
+    ep.tok = tok;
+    if (p.tok_out && blockIdx.x == 0 && split == 0 && tid == 0) p.tok_out[m] = tok;
+
+    float yf = 0.f;
+    int yi = 0;
+    for (int64_t kc = kbA; kc < kbB; kc += CK) {
+        nkb = (int)((kbB - kc) < CK ? (kbB - kc) : CK);
+        if (kc != kbA) {
+            load_weights(kc, nkb);
+            load_acts(kc, nkb);
+            lds_barrier();  // the previous chunk's tables and sums are no longer read
+        }
+        // 2-3. signed tables of this chunk and the activation sums
+        int s_acc = 0;
+#pragma unroll
+        for (int r = 0; r < QPT; ++r) {
+            const int e = tid + NT * r, g = e >> 2, qr = e & 3;
+            const float xs = act_value<INT8>(av[r], scale);
+            int4 q;
+            if (INT8) {
+                const int qs = (int)xs;
+                s_acc += qs;
+                q = quarter_entries_int(quad_bcast<0>(qs), quad_bcast<1>(qs), quad_bcast<2>(qs), quad_bcast<3>(qs), qr);
+            } else {
+                const int xb = __float_as_int(xs);
+                q = quarter_entries<false>(__int_as_float(quad_bcast<0>(xb)), __int_as_float(quad_bcast<1>(xb)),
+                                           __int_as_float(quad_bcast<2>(xb)), __int_as_float(quad_bcast<3>(xb)), qr);
+                if (need_s) {  // sum of the 64 activations of this wave and round: half a 128-block
+                    const float hs = wave_sum_f(xs);
+                    if (lane == 63) hsf[r * NW + wave] = hs;
+                }
+            }
+            if (g < nkb * GPB) *(int4 *)(F + (g / GPB) * KSTRIDE + (g % GPB) * 64 + qr * 16) = q;
+        }
+        if (INT8 && need_s) {
+            const int hs = wave_sum_i(s_acc);
+            if (lane == 63) hsi[wave] = hs;
+        }
+        // epilogue operands of this lane's 128-blocks (vector loads, issued before the lookups)
+        float esc[TW], ezp[TW];
+#pragma unroll
+        for (int t = 0; t < TW; ++t) {
+            esc[t] = 0.f;
+            ezp[t] = 0.f;
+            const int kbl = sigma + t * S;
+            if (!INT8 && kbl < nkb) {
+                const int64_t kb = kc + kbl;
+                const int q = (int)(((float)kb + 0.5f) * p.inv_kpg);
+                const SZ sz = load_sz(p, q, lane_value(n));
+                esc[t] = sz.sp * (1.0f / (float)(1 << FIX_SHIFT));
+                ezp[t] = sz.sp * sz.zp;
+            }
+        }
+        lds_barrier();
+#pragma unroll
+        for (int t = 0; t < TW; ++t) {
+            const int kbl = sigma + t * S;
+            if (kbl < nkb) {
+                const uint32_t base = (uint32_t)(kbl * KSTRIDE);
+                int tot = 0;
+#pragma unroll
+                for (int i = 0; i < NPL; ++i)  // exact in INT32, see lookup_word
+                    tot += lookup_word(F, base, w[t][i]) << (pl * NPL + i);
+                if (INT8) {
+                    yi += tot;
+                } else {
+                    yf = fmaf(esc[t], (float)tot, yf);
+                    // activation sum of this 128-block: the two half-block sums of its round
+                    const int hb = (kbl / BPR) * NW + 2 * (kbl % BPR);
+                    if (need_s && pl == 0) yf -= ezp[t] * (hsf[hb] + hsf[hb + 1]);
+                }
+            }
+        }
+        if (INT8 && need_s && sigma == 0 && pl == 0) {  // the chunk's activation sum, once per column
+#pragma unroll
+            for (int v = 0; v < NW; ++v) yi += hsi[v];
+        }
+    }
+
+    // combine the lanes of each column (fixed butterfly), then the wavefronts in order
+#pragma unroll
+    for (int off = CW; off < 64; off <<= 1) {
+        if (INT8)
+            yi += __shfl_xor(yi, off, 64);
+        else
+            yf += __shfl_xor(yf, off, 64);
+    }
+    if (lane < CW) {
+        redf[wave][lane] = yf;
+        redi[wave][lane] = yi;
+    }
+    lds_barrier();
+    if (wave == 0 && lane < CW) {
+        float sf = redf[0][lane];
+        int si = redi[0][lane];
+#pragma unroll
+        for (int v = 1; v < NW; ++v) {
+            sf += redf[v][lane];
+            si += redi[v][lane];
+        }
+        if (p.splits == 1)
+            store_out<INT8>(p, wfmt, m, n, sf, si, ep);
+        else
+            p.part[((int64_t)split * p.M + m) * p.N_pad + n] = INT8 ? __int_as_float(si) : sf;
+    }
+}
+
+// Same lane decompositions as the table-fed GEMV (see lut_gemv.hip).
+template <int BITS, int PW, int SW, int TW, bool INT8>
+static void launch_fused_cfg(const LutParams &p, const Layout &L, const LutPlan &plan, hipStream_t s) {
+    constexpr int CW = 64 / (PW * SW);
+    const dim3 grid((unsigned)((L.N + CW - 1) / CW), (unsigned)plan.splits, (unsigned)p.M);
+    if (plan.gemv_nw == 16 && TW % 4 == 0)
+        hipLaunchKernelGGL((lut_fused_gemv_kernel<BITS, PW, SW, (TW + 3) / 4, 16, INT8>), grid, dim3(1024), 0, s, p, L.wfmt);
+    else if (plan.gemv_nw >= 8 && TW % 2 == 0)
+        hipLaunchKernelGGL((lut_fused_gemv_kernel<BITS, PW, SW, (TW + 1) / 2, 8, INT8>), grid, dim3(512), 0, s, p, L.wfmt);
+    else
+        hipLaunchKernelGGL((lut_fused_gemv_kernel<BITS, PW, SW, TW, 4, INT8>), grid, dim3(256), 0, s, p, L.wfmt);
+}
+
+template <bool INT8>
+static void launch_fused_bits(const LutParams &p, const Layout &L, const LutPlan &plan, hipStream_t s) {
+    if (L.bits == 1) {
+        if (plan.gemv_cfg == 0) launch_fused_cfg<1, 1, 1, 4, INT8>(p, L, plan, s);
+        else launch_fused_cfg<1, 1, 2, 4, INT8>(p, L, plan, s);
+    } else if (L.bits == 2) {
+        if (plan.gemv_cfg == 0) launch_fused_cfg<2, 1, 1, 2, INT8>(p, L, plan, s);
+        else if (plan.gemv_cfg == 1) launch_fused_cfg<2, 2, 1, 4, INT8>(p, L, plan, s);
+        else launch_fused_cfg<2, 2, 2, 4, INT8>(p, L, plan, s);
+    } else {
+        if constexpr (!INT8) {
+            if (plan.gemv_cfg == 0) launch_fused_cfg<4, 2, 1, 2, false>(p, L, plan, s);
+            else launch_fused_cfg<4, 4, 1, 4, false>(p, L, plan, s);
+        }
+    }
+}
+
+int launch_fused_gemv(const LutParams &p, const Layout &L, const LutPlan &plan, void *stream) {
+    hipStream_t s = (hipStream_t)stream;
+    if (L.act == LUTGEMM_ACT_INT8)
+        launch_fused_bits<true>(p, L, plan, s);
+    else
+        launch_fused_bits<false>(p, L, plan, s);
+    return (int)hipGetLastError();
+}
+
+}  // namespace lutgemm

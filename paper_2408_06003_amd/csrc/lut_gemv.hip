@@ -31,27 +31,6 @@
 
 namespace lutgemm {
 
-constexpr int KSTRIDE = GPB * 64 + 64;  // LDS bytes per 128-block: 32 tables x 16 INT32, + 64 B pad
-
-// base + (byte B of x), one VALU op (SDWA byte select).
-template <int B>
-__device__ __forceinline__ uint32_t add_byte(uint32_t base, uint32_t x) {
-    uint32_t r;
-    if constexpr (B == 0)
-        asm("v_add_u32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_0"
-            : "=v"(r) : "v"(base), "v"(x));
-    else if constexpr (B == 1)
-        asm("v_add_u32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_1"
-            : "=v"(r) : "v"(base), "v"(x));
-    else if constexpr (B == 2)
-        asm("v_add_u32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_2"
-            : "=v"(r) : "v"(base), "v"(x));
-    else
-        asm("v_add_u32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_3"
-            : "=v"(r) : "v"(base), "v"(x));
-    return r;
-}
-
 // One quarter (4 entries) of a 16-entry signed table from half (qr & 1) of an
 // 8-entry half table: quarters 0, 1 are T[0..3], T[4..7]; quarters 2, 3 negated.
 template <bool INT8>
@@ -163,21 +142,8 @@ __global__ __launch_bounds__(64 * NW) void lut_gemv2_kernel(LutParams p, int wfm
                 const uint32_t base = (uint32_t)(kbl * KSTRIDE);
                 int tot = 0;
 #pragma unroll
-                for (int i = 0; i < NPL; ++i) {
-                    const uint32_t wd[4] = {w[t][i].x, w[t][i].y, w[t][i].z, w[t][i].w};
-                    int acc = 0;
-#pragma unroll
-                    for (int d = 0; d < 4; ++d) {
-                        const uint32_t lo = (wd[d] << 2) & 0x3C3C3C3Cu, hi = (wd[d] >> 2) & 0x3C3C3C3Cu;
-                        const char *Fg = F + d * 8 * 64;
-                        acc += lds_i32(Fg + 0 * 64, add_byte<0>(base, lo)) + lds_i32(Fg + 1 * 64, add_byte<0>(base, hi));
-                        acc += lds_i32(Fg + 2 * 64, add_byte<1>(base, lo)) + lds_i32(Fg + 3 * 64, add_byte<1>(base, hi));
-                        acc += lds_i32(Fg + 4 * 64, add_byte<2>(base, lo)) + lds_i32(Fg + 5 * 64, add_byte<2>(base, hi));
-                        acc += lds_i32(Fg + 6 * 64, add_byte<3>(base, lo)) + lds_i32(Fg + 7 * 64, add_byte<3>(base, hi));
-                    }
-                    // |sum_t 2^t acc_t| <= 15 * 32 * 2^22 < 2^31 on the FP path: exact in INT32
-                    tot += acc << (pl * NPL + i);
-                }
+                for (int i = 0; i < NPL; ++i)  // exact in INT32, see lookup_word
+                    tot += lookup_word(F, base, w[t][i]) << (pl * NPL + i);
                 if (INT8)
                     yi += tot;
                 else

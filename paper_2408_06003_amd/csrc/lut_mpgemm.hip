@@ -200,6 +200,12 @@ int launch_lut(const LutParams &p, const Layout &L, const LutPlan &plan, void *s
     }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || plan.splits == 1) return (int)e;
+    return launch_finalize(p, L, plan, stream);
+}
+
+// Sums the K-split partials of the LUT kernel (after it, on the same stream).
+int launch_finalize(const LutParams &p, const Layout &L, const LutPlan &plan, void *stream) {
+    hipStream_t s = (hipStream_t)stream;
     const int64_t m_alloc = plan.kind == 1 ? plan.m_tiles * plan.mt : p.M;
     const dim3 grid((unsigned)(L.N_pad / 64), (unsigned)p.M);  // one lane per padded column
     const int pt = L.per_tensor ? 1 : 0;

@@ -106,7 +106,9 @@ struct PrecomputeParams {
 struct LutParams {
     const uint4 *T;        // half tables
     const void *S;         // group sums
-    const float *tok;      // per-token factor
+    const float *tok;      // per-token factor (NULL in the fused kernel, which computes it)
+    const uint16_t *act;   // FP16 [M][K]: activations of the fused kernel
+    float *tok_out;        // fused kernel with K split: per-token factor for the finalize kernel
     const uint4 *planes;
     const void *meta;
     void *out;
@@ -134,6 +136,8 @@ int launch_pack(const PackParams &p, void *stream);
 int launch_precompute(const PrecomputeParams &p, int act_int8, void *stream);
 int launch_lut(const LutParams &p, const Layout &L, const LutPlan &plan, void *stream);
 int launch_gemv(const LutParams &p, const Layout &L, const LutPlan &plan, void *stream);
+int launch_fused_gemv(const LutParams &p, const Layout &L, const LutPlan &plan, void *stream);
+int launch_finalize(const LutParams &p, const Layout &L, const LutPlan &plan, void *stream);
 int launch_dequant(const DequantParams &p, const Layout &L, void *stream);
 
 }  // namespace lutgemm

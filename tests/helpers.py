@@ -44,6 +44,14 @@ class GpuProblem:
         torch.cuda.synchronize()
         return y
 
+    def fused(self, out_dtype=None, accumulate=False, out=None, act=None):
+        import torch
+        a = self.act if act is None else act
+        od = out_dtype or (torch.int32 if self.inp.act_kind == W.ACT_INT8 else torch.float16)
+        y = self.g.fused(a, out=out, out_dtype=od, accumulate=accumulate)
+        torch.cuda.synchronize()
+        return y
+
     def dequant(self, out_dtype=None, accumulate=False, out=None):
         import torch
         y = self.g.dequant(self.act, out=out, out_dtype=out_dtype or torch.float16, accumulate=accumulate)

@@ -127,3 +127,28 @@ def test_entry_points_reject_before_launch():
     assert need > 0
     assert f.lutgemm_mpgemm(ctypes.byref(pw), 1, ok, ok, ok, L.OUT_INT32, 0, None, need, None) == L.ERROR_INVALID_VALUE
     assert f.lutgemm_mpgemm(ctypes.byref(pw), 1, ok, ok, ok, L.OUT_INT32, 0, ok, need - 1, None) == L.ERROR_INSUFFICIENT_SIZE
+
+
+def test_fused_entry_point_rejects_before_launch():
+    f = L.lib
+    ok, big = 1 << 20, 1 << 40
+    p = L.problem(4096, 4096, 2, L.WFMT_TERNARY, 0, L.ACT_INT8, True)
+    bp = ctypes.byref(p)
+    assert L.fused_workspace_size(p, 1) == 0           # one token, whole K per workgroup: no scratch
+    assert f.lutgemm_mpgemm_fused(bp, 1, None, ok, ok, L.OUT_INT32, 0, None, 0, None) == L.ERROR_INVALID_VALUE
+    assert f.lutgemm_mpgemm_fused(bp, 1, ok + 4, ok, ok, L.OUT_INT32, 0, None, 0, None) == L.ERROR_INVALID_VALUE
+    assert f.lutgemm_mpgemm_fused(bp, 1, ok, ok, ok, 7, 0, None, 0, None) == L.ERROR_INVALID_VALUE
+    assert f.lutgemm_mpgemm_fused(bp, 1, ok, ok, ok, L.OUT_INT32, 3, None, 0, None) == L.ERROR_INVALID_VALUE
+    assert f.lutgemm_mpgemm_fused(bp, 0, ok, ok, ok, L.OUT_INT32, 0, None, 0, None) == L.ERROR_INVALID_VALUE
+    pf = L.problem(1024, 256, 2, L.WFMT_UINT, 128)
+    assert f.lutgemm_mpgemm_fused(ctypes.byref(pf), 1, ok, ok, ok, L.OUT_INT32, 0, None, 0, None) == L.ERROR_NOT_SUPPORTED
+    # K split across workgroups: partial sums and per-token factors
+    ps = L.problem(8192, 1000, 2, L.WFMT_TERNARY, 0, L.ACT_INT8, True)
+    need = L.fused_workspace_size(ps, 1)
+    assert need >= 2 * 1024 * 4 + 4
+    assert f.lutgemm_mpgemm_fused(ctypes.byref(ps), 1, ok, ok, ok, L.OUT_FP32, 0, None, need, None) == L.ERROR_INVALID_VALUE
+    assert f.lutgemm_mpgemm_fused(ctypes.byref(ps), 1, ok, ok, ok, L.OUT_FP32, 0, ok, need - 1, None) == L.ERROR_INSUFFICIENT_SIZE
+    # several tokens: tables (lutgemm_table_size) plus the table-fed kernel's workspace
+    M = 8
+    assert L.fused_workspace_size(p, M) >= L.table_size(p, M) + L.workspace_size(p, M)
+    assert L.fused_workspace_size(L.problem(1000, 64, 2, L.WFMT_UINT, 0), 1) == 0  # invalid problem

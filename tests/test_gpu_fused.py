@@ -1,0 +1,127 @@
+"""GPU parity of lutgemm_mpgemm_fused (table precompute fused into the LUT kernel).
+
+The fused path is compared with the CPU oracle (INT8 activations bit-exactly, FP16
+activations within the FP tolerance) and, for INT8 activations, with the two-call
+path (lutgemm_precompute + lutgemm_mpgemm) bitwise.  Cases cover one and two
+tokens, a single K chunk, several K chunks (K = 11008), K split across
+workgroups (few columns), ragged column tails, every weight format, accumulate,
+determinism, the zero token, and the fallback to the two-call path (M > 2, large
+weights).
+"""
+import numpy as np
+import pytest
+
+import oracle
+import workloads as W
+from helpers import GpuProblem, assert_fp_close, sample_indices
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+if not torch.cuda.is_available():
+    pytest.skip("no GPU", allow_module_level=True)
+
+import paper_2408_06003_amd as L  # noqa: E402
+
+
+def banner(msg):
+    print(f"\n[case] {msg}", flush=True)
+
+
+def check_fused(gp, rows=None, cols=None, what=""):
+    inp = gp.inp
+    if inp.act_kind == W.ACT_INT8:
+        acc_ref, y_ref = oracle.reference_output(inp, rows=rows, cols=cols)
+        yi = gp.fused(out_dtype=torch.int32).cpu().numpy()
+        yf = gp.fused(out_dtype=torch.float32).cpu().numpy()
+        # the two-call path gives the same bits
+        assert np.array_equal(yi, gp.lut(out_dtype=torch.int32).cpu().numpy()), f"{what}: fused INT32 != two-call"
+        assert np.array_equal(yf, gp.lut(out_dtype=torch.float32).cpu().numpy()), f"{what}: fused FP32 != two-call"
+        if rows is not None:
+            yi, yf = yi[np.ix_(rows, cols)], yf[np.ix_(rows, cols)]
+        assert np.array_equal(yi.astype(np.int64), acc_ref), f"{what}: INT32 accumulator differs from the oracle"
+        assert np.array_equal(yf, y_ref), f"{what}: FP32 output differs from the oracle"
+        return
+    ref = oracle.reference_output(inp, rows=rows, cols=cols)
+    for od in (torch.float16, torch.float32):
+        y = gp.fused(out_dtype=od).float().cpu().numpy()
+        if rows is not None:
+            y = y[np.ix_(rows, cols)]
+        fro, mx = assert_fp_close(y, ref, f"{what} fused {od}")
+        print(f"[err] {what} fused {od}: relFro {fro:.3e} max/rms {mx:.3e}", flush=True)
+
+
+CASES = [
+    # (family, M, K, N): single chunk, several chunks, K split (few columns), ragged tails
+    (1, 1, 1024, 1000),
+    (1, 2, 1024, 300),
+    (2, 1, 4096, 4096),
+    (2, 2, 2048, 777),
+    (2, 1, 8192, 1000),
+    (3, 1, 4096, 1000),
+    (3, 1, 11008, 520),
+    (3, 1, 11008, 1000),
+    (3, 2, 2048, 33),
+    (5, 1, 2048, 1000),
+    (5, 2, 4096, 130),
+]
+
+
+@pytest.mark.parametrize("cid,M,K,N", CASES)
+def test_fused_parity(cid, M, K, N):
+    banner(f"fused parity config={cid} M={M} K={K} N={N}")
+    gp = GpuProblem(W.make_inputs(cid, 0, M=M, K=K, N=N))
+    print(f"[ws] fused workspace {L.fused_workspace_size(gp.p, M)} B", flush=True)
+    check_fused(gp, what=f"config {cid} M={M} K={K} N={N}")
+
+
+@pytest.mark.parametrize("wfmt,bits,G,act", [(W.WFMT_UINT, 1, 128, W.ACT_FP16), (W.WFMT_UINT, 2, 256, W.ACT_FP16),
+                                             (W.WFMT_UINT, 4, 1024, W.ACT_FP16), (W.WFMT_TERNARY, 2, 128, W.ACT_FP16),
+                                             (W.WFMT_BINARY, 1, 2048, W.ACT_INT8), (W.WFMT_TERNARY, 2, 0, W.ACT_INT8)])
+def test_fused_formats_and_groups(wfmt, bits, G, act):
+    banner(f"fused formats wfmt={wfmt} b={bits} G={G} act={act}")
+    inp = W.make_custom(wfmt, bits, G, act, M=1, K=2048, N=640, seed=91, scale_fp32=(G == 0))
+    check_fused(GpuProblem(inp), what=f"wfmt={wfmt} b={bits} G={G}")
+
+
+def test_fused_fallback_paths():
+    banner("fused entry point on shapes it does not fuse (M > 2, large weights)")
+    gp = GpuProblem(W.make_inputs(3, 0, M=5, K=2048, N=700))
+    check_fused(gp, what="M=5")
+    gpi = GpuProblem(W.make_custom(W.WFMT_TERNARY, 2, 0, W.ACT_INT8, M=6, K=2048, N=300, seed=93, scale_fp32=True))
+    check_fused(gpi, what="INT8 M=6")
+
+
+@pytest.mark.parametrize("cid,sid", [(2, 0), (3, 0), (3, 1), (3, 3), (5, 0), (5, 1)])
+def test_fused_full_size(cid, sid):
+    inp = W.make_inputs(cid, sid, M=1)
+    banner(f"fused full size config={cid} shape={sid} K={inp.K} N={inp.N}")
+    gp = GpuProblem(inp)
+    if inp.act_kind == W.ACT_INT8:
+        check_fused(gp, what=f"config {cid}/{sid}")
+        return
+    rows, cols = sample_indices(1, inp.N, seed=cid * 100 + sid)
+    check_fused(gp, rows=rows, cols=cols, what=f"config {cid}/{sid}")
+
+
+def test_fused_zero_token_accumulate_determinism():
+    banner("fused: zero token, accumulate, determinism")
+    inp = W.make_inputs(2, 0, M=2, K=4096, N=1000)
+    inp.act[1] = 0
+    gp = GpuProblem(inp)
+    check_fused(gp, what="zero second token")
+    y1 = gp.fused(out_dtype=torch.float32)
+    y2 = gp.fused(out_dtype=torch.float32)
+    assert torch.equal(y1, y2)
+    bi = torch.randint(-1000, 1000, (2, 1000), device="cuda", dtype=torch.int32)
+    acc = bi.clone()
+    gp.fused(out=acc, accumulate=True)
+    assert torch.equal(acc, bi + gp.fused(out_dtype=torch.int32))
+    inpf = W.make_inputs(3, 0, M=1, K=4096, N=1000)
+    gpf = GpuProblem(inpf)
+    f1 = gpf.fused(out_dtype=torch.float32)
+    assert torch.equal(f1, gpf.fused(out_dtype=torch.float32)), "fused FP path not deterministic"
+    base = torch.randn(1, 1000, device="cuda")
+    accf = base.clone()
+    gpf.fused(out=accf, accumulate=True)
+    assert torch.equal(accf, base + f1)
