@@ -46,7 +46,46 @@ __device__ __forceinline__ int lds_i32(const char *base, uint32_t off) {
     return *(const int *)(base + off);
 }
 
-constexpr int KSTRIDE = GPB * 64 + 64;  // LDS bytes per 128-block: 32 tables x 16 INT32, + 64 B pad
+// Signed 16-entry tables staged in LDS (entry s i = (s ? -1 : 1) T[i], Eq. 4-5)
+// for the 32 four-activation groups of a 128-block: INT16 entries on the INT8 path
+// (exact, |entry| <= 508), INT32 fixed point (FP16 entry x 2^20) on the FP path.
+// Blocks are padded by one group table, so the tables of two consecutive blocks
+// at the same group sit in different LDS banks.
+template <bool INT8>
+struct Tab {
+    static constexpr int E = INT8 ? 2 : 4;       // bytes per entry
+    static constexpr int G = 16 * E;             // bytes per group table
+    static constexpr int BLK = (GPB + 1) * G;    // bytes per 128-block
+};
+
+// (byte B of w) & MASK, one VALU op (SDWA byte select); with w pre-shifted so a
+// 4-bit index lands at bit 1 (INT16 tables, MASK 30) or bit 2 (INT32, MASK 60)
+// this is the byte offset of the entry.
+template <int B, bool INT8>
+__device__ __forceinline__ uint32_t idx_off(uint32_t w) {
+    if constexpr (!INT8) return idx4<B>(w);
+    uint32_t r;
+    if constexpr (B == 0)
+        asm("v_and_b32_sdwa %0, 30, %1 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_0"
+            : "=v"(r) : "v"(w));
+    else if constexpr (B == 1)
+        asm("v_and_b32_sdwa %0, 30, %1 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_1"
+            : "=v"(r) : "v"(w));
+    else if constexpr (B == 2)
+        asm("v_and_b32_sdwa %0, 30, %1 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_2"
+            : "=v"(r) : "v"(w));
+    else
+        asm("v_and_b32_sdwa %0, 30, %1 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_3"
+            : "=v"(r) : "v"(w));
+    return r;
+}
+
+// One table entry: ds_read_i16 (sign-extended) or ds_read_b32.
+template <bool INT8>
+__device__ __forceinline__ int lds_entry(const char *base, uint32_t off) {
+    if constexpr (INT8) return (int)*(const int16_t *)(base + off);
+    return *(const int *)(base + off);
+}
 
 // base + (byte B of x), one VALU op (SDWA byte select).
 template <int B>
@@ -69,23 +108,51 @@ __device__ __forceinline__ uint32_t add_byte(uint32_t base, uint32_t x) {
 
 // Sum of the 32 entries addressed by one 16-byte plane word (the 4-bit indices of
 // one 128-block, index i at bits 4 (i % 8) of 32-bit word i / 8) in the signed
-// 16-entry INT32 tables of that block, which start at byte `base` of F with a
-// stride of 64 bytes per 4-activation group.  A lookup is one SDWA byte-add, one
-// ds_read_b32 and half a v_add3_u32.  On the FP path entries are below 2^22 in
-// magnitude, so sum_t 2^t (word sum of plane t) stays below 15 * 32 * 2^22 < 2^31.
+// tables of that block (layout Tab<INT8>), which start at byte `base` of F.  A
+// lookup is one SDWA byte-add, one LDS read and half a v_add3_u32.  On the FP path
+// entries are below 2^22 in magnitude, so sum_t 2^t (word sum of plane t) stays
+// below 15 * 32 * 2^22 < 2^31.
+template <bool INT8>
 __device__ __forceinline__ int lookup_word(const char *F, uint32_t base, uint4 w) {
+    constexpr int GS = Tab<INT8>::G;
+    constexpr uint32_t MASK = INT8 ? 0x1E1E1E1Eu : 0x3C3C3C3Cu;
     const uint32_t wd[4] = {w.x, w.y, w.z, w.w};
     int acc = 0;
 #pragma unroll
     for (int d = 0; d < 4; ++d) {
-        const uint32_t lo = (wd[d] << 2) & 0x3C3C3C3Cu, hi = (wd[d] >> 2) & 0x3C3C3C3Cu;
-        const char *Fg = F + d * 8 * 64;
-        acc += lds_i32(Fg + 0 * 64, add_byte<0>(base, lo)) + lds_i32(Fg + 1 * 64, add_byte<0>(base, hi));
-        acc += lds_i32(Fg + 2 * 64, add_byte<1>(base, lo)) + lds_i32(Fg + 3 * 64, add_byte<1>(base, hi));
-        acc += lds_i32(Fg + 4 * 64, add_byte<2>(base, lo)) + lds_i32(Fg + 5 * 64, add_byte<2>(base, hi));
-        acc += lds_i32(Fg + 6 * 64, add_byte<3>(base, lo)) + lds_i32(Fg + 7 * 64, add_byte<3>(base, hi));
+        const uint32_t lo = (INT8 ? wd[d] << 1 : wd[d] << 2) & MASK, hi = (INT8 ? wd[d] >> 3 : wd[d] >> 2) & MASK;
+        const char *Fg = F + d * 8 * GS;
+        acc += lds_entry<INT8>(Fg + 0 * GS, add_byte<0>(base, lo)) + lds_entry<INT8>(Fg + 1 * GS, add_byte<0>(base, hi));
+        acc += lds_entry<INT8>(Fg + 2 * GS, add_byte<1>(base, lo)) + lds_entry<INT8>(Fg + 3 * GS, add_byte<1>(base, hi));
+        acc += lds_entry<INT8>(Fg + 4 * GS, add_byte<2>(base, lo)) + lds_entry<INT8>(Fg + 5 * GS, add_byte<2>(base, hi));
+        acc += lds_entry<INT8>(Fg + 6 * GS, add_byte<3>(base, lo)) + lds_entry<INT8>(Fg + 7 * GS, add_byte<3>(base, hi));
     }
     return acc;
+}
+
+typedef short short2_v __attribute__((ext_vector_type(2)));
+
+// Negation of two packed INT16 values (one v_pk_sub_i16).
+__device__ __forceinline__ uint32_t neg_i16x2(uint32_t x) {
+    short2_v v = __builtin_bit_cast(short2_v, x);
+    v = -v;
+    return __builtin_bit_cast(uint32_t, v);
+}
+
+// Stores quarter qr (entries 4 qr .. 4 qr + 3) of the signed table of group g of
+// the staged block `blk`, from half (qr & 1) of its 8-entry half table (4 FP16 or
+// INT16 values): quarters 0, 1 are T[0..3], T[4..7]; quarters 2, 3 their negation.
+template <bool INT8>
+__device__ __forceinline__ void store_quarter(char *F, int blk, int g, int qr, uint2 h) {
+    char *dst = F + blk * Tab<INT8>::BLK + g * Tab<INT8>::G + qr * 4 * Tab<INT8>::E;
+    if constexpr (INT8) {
+        if (qr >= 2) h = make_uint2(neg_i16x2(h.x), neg_i16x2(h.y));
+        *(uint2 *)dst = h;
+    } else {
+        const float f = qr >= 2 ? -(float)(1 << FIX_SHIFT) : (float)(1 << FIX_SHIFT);
+        *(int4 *)dst = make_int4((int)rintf(h2f(h.x & 0xFFFFu) * f), (int)rintf(h2f(h.x >> 16) * f),
+                                 (int)rintf(h2f(h.y & 0xFFFFu) * f), (int)rintf(h2f(h.y >> 16) * f));
+    }
 }
 
 // Expand one half table (8 entries, 16 bytes) into a 16-entry INT32 signed table.

@@ -12,13 +12,13 @@
 //      operator, so the tables are bitwise the ones it would produce.
 //   2. Per 4-activation group, the entries F[s i] = (s ? -1 : 1) T[i] of Eq. 4-5
 //      (T[i] = -x0 + sum_{e=1..3} (bit (3-e) of i ? x_e : -x_e), rounded to FP16
-//      on the FP path as in the stored tables), one quarter (4 entries) per lane.
+//      on the FP path as in the stored tables): on the INT8 path one lane builds a
+//      group's INT16 table from its 4 quantized activations; on the FP path the 4
+//      lanes of a DPP quad hold the group's 4 activations, exchange them by quad
+//      broadcasts and build one quarter (4 INT32 entries) each.
 //   3. The activation sums: per 128-block S_kb on the FP path (zero-point term of
 //      Eq. 3), per chunk on the INT8 path (ternary integer offset), by fixed-order
 //      DPP sums over the lanes that built the tables.
-// Lane e of a round quantizes (or scales) activation e of the chunk once; the four
-// lanes of a DPP quad hold the four activations of one group and exchange them by
-// quad broadcasts, each then building one quarter of the group's table.
 // The weights of the chunk are loaded before any of this, so their memory latency
 // overlaps the table build; lookups and epilogue are those of lut_gemv.hip.  The
 // zero-point term is applied per 128-block: s'_q z'_q S_q = sum over the blocks
@@ -65,12 +65,19 @@ __device__ __forceinline__ int quad_bcast(int v) {
     return __builtin_amdgcn_mov_dpp(v, I * 0x55, 0xF, 0xF, false);
 }
 
-// Integer form of quarter_entries for the INT8 path (exact: |entry| <= 508).
-__device__ __forceinline__ int4 quarter_entries_int(int q0, int q1, int q2, int q3, int qr) {
-    const int sg = qr >= 2 ? -1 : 1;
-    const int b = sg * (((qr & 1) ? q1 : -q1) - q0);
-    const int p2 = sg * q2, p3 = sg * q3;
-    return make_int4(b - p2 - p3, b - p2 + p3, b + p2 - p3, b + p2 + p3);
+// The signed INT16 table of one group of quantized activations q0..q3 (INT8
+// path): entries 0..7 are T[i] = -q0 + (+-q1) + (+-q2) + (+-q3) (bit 2 of i
+// selects the sign of q1, bit 1 of q2, bit 0 of q3), entries 8..15 are -T[i];
+// exact integers (|T| <= 508).  Written as two 16-byte LDS stores.
+__device__ __forceinline__ void build_group_i16(char *dst, int q0, int q1, int q2, int q3) {
+    const int b0 = -q0 - q1, b1 = -q0 + q1;
+    const int c0 = b0 - q2, c1 = b0 + q2, c2 = b1 - q2, c3 = b1 + q2;
+    const int t[8] = {c0 - q3, c0 + q3, c1 - q3, c1 + q3, c2 - q3, c2 + q3, c3 - q3, c3 + q3};
+    uint32_t pw[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) pw[i] = ((uint32_t)t[2 * i] & 0xFFFFu) | ((uint32_t)t[2 * i + 1] << 16);
+    *(uint4 *)dst = make_uint4(pw[0], pw[1], pw[2], pw[3]);
+    *(uint4 *)(dst + 16) = make_uint4(neg_i16x2(pw[0]), neg_i16x2(pw[1]), neg_i16x2(pw[2]), neg_i16x2(pw[3]));
 }
 
 template <int CTRL, int ROW_MASK>
@@ -120,11 +127,14 @@ __global__ __launch_bounds__(64 * NW) void lut_fused_gemv_kernel(LutParams p, in
     constexpr int S = NW * SW;             // K slices per workgroup
     constexpr int CK = S * TW;             // 128-blocks per chunk
     constexpr int NPL = BITS / PW;         // bit-planes per lane
-    constexpr int QPT = CK * GPB * 4 / NT; // table quarters built per thread and chunk
+    // FP path: table quarters built per thread and chunk (one activation per lane
+    // and round); INT8 path: whole group tables built per thread and chunk
+    constexpr int QPT = CK * GPB * 4 / NT;
+    constexpr int GPT = (CK * GPB + NT - 1) / NT;
     constexpr int BPR = NT / 128;          // 128-blocks covered by one round of quarters
     static_assert(QPT * NT == CK * GPB * 4 && NT % 128 == 0, "quarters divide evenly over the threads");
     static_assert(TW * NPL <= 4, "at most four prefetched weight words per lane");
-    __shared__ __attribute__((aligned(16))) char F[CK * KSTRIDE];
+    __shared__ __attribute__((aligned(16))) char F[CK * Tab<INT8>::BLK];
     __shared__ float redf[NW][CW];
     __shared__ int redi[NW][CW];
     __shared__ float hsf[QPT * NW];  // FP path: half-block activation sums, [round][wave]
@@ -157,14 +167,24 @@ __global__ __launch_bounds__(64 * NW) void lut_fused_gemv_kernel(LutParams p, in
             }
         }
     };
-    // lane e of a round holds activation e of the chunk: the 4 lanes of a quad are the
-    // 4 activations of one table group, and build the group's 4 table quarters
-    uint32_t av[QPT];
+    // FP path: lane e of a round holds activation e of the chunk, so the 4 lanes of a
+    // quad hold the 4 activations of one group and build its 4 table quarters.
+    // INT8 path: lane g of a round holds the 4 activations of group g.
+    uint32_t av[INT8 ? 1 : QPT];
+    uint2 ag[INT8 ? GPT : 1];
     auto load_acts = [&](int64_t kc, int nkb) {
+        if constexpr (INT8) {
 #pragma unroll
-        for (int r = 0; r < QPT; ++r) {
-            const int e = tid + NT * r;
-            av[r] = e < nkb * KBLK ? (uint32_t)a1[kc * KBLK + e] : 0u;
+            for (int r = 0; r < GPT; ++r) {
+                const int g = tid + NT * r;
+                ag[r] = g < nkb * GPB ? a4[kc * GPB + g] : make_uint2(0u, 0u);
+            }
+        } else {
+#pragma unroll
+            for (int r = 0; r < QPT; ++r) {
+                const int e = tid + NT * r;
+                av[r] = e < nkb * KBLK ? (uint32_t)a1[kc * KBLK + e] : 0u;
+            }
         }
     };
 
@@ -177,8 +197,13 @@ __global__ __launch_bounds__(64 * NW) void lut_fused_gemv_kernel(LutParams p, in
 
     // 1. amax of the whole token: the first chunk from registers, the rest from memory
     float amax = 0.f;
+    if constexpr (INT8) {
 #pragma unroll
-    for (int r = 0; r < QPT; ++r) amax = fmaxf(amax, fabsf(h2f(av[r])));
+        for (int r = 0; r < GPT; ++r) amax = fmaxf(amax, absmax4(ag[r]));
+    } else {
+#pragma unroll
+        for (int r = 0; r < QPT; ++r) amax = fmaxf(amax, fabsf(h2f(av[r])));
+    }
     const int64_t j0 = kbA * GPB, j1 = j0 + (int64_t)nkb * GPB;
     for (int64_t j = tid; j < p.J; j += NT)
         if (j < j0 || j >= j1) amax = fmaxf(amax, absmax4(a4[j]));
@@ -214,30 +239,36 @@ __global__ __launch_bounds__(64 * NW) void lut_fused_gemv_kernel(LutParams p, in
             lds_barrier();  // the previous chunk's tables and sums are no longer read
         }
         // 2-3. signed tables of this chunk and the activation sums
-        int s_acc = 0;
+        if constexpr (INT8) {
+            int s_acc = 0;
 #pragma unroll
-        for (int r = 0; r < QPT; ++r) {
-            const int e = tid + NT * r, g = e >> 2, qr = e & 3;
-            const float xs = act_value<INT8>(av[r], scale);
-            int4 q;
-            if (INT8) {
-                const int qs = (int)xs;
-                s_acc += qs;
-                q = quarter_entries_int(quad_bcast<0>(qs), quad_bcast<1>(qs), quad_bcast<2>(qs), quad_bcast<3>(qs), qr);
-            } else {
+            for (int r = 0; r < GPT; ++r) {
+                const int g = tid + NT * r;
+                const int q0 = (int)act_value<true>(ag[r].x & 0xFFFFu, scale);
+                const int q1 = (int)act_value<true>(ag[r].x >> 16, scale);
+                const int q2 = (int)act_value<true>(ag[r].y & 0xFFFFu, scale);
+                const int q3 = (int)act_value<true>(ag[r].y >> 16, scale);
+                s_acc += (q0 + q1) + (q2 + q3);
+                if (g < nkb * GPB) build_group_i16(F + (g / GPB) * Tab<true>::BLK + (g % GPB) * Tab<true>::G, q0, q1, q2, q3);
+            }
+            if (need_s) {
+                const int hs = wave_sum_i(s_acc);
+                if (lane == 63) hsi[wave] = hs;
+            }
+        } else {
+#pragma unroll
+            for (int r = 0; r < QPT; ++r) {
+                const int e = tid + NT * r, g = e >> 2, qr = e & 3;
+                const float xs = act_value<false>(av[r], scale);
                 const int xb = __float_as_int(xs);
-                q = quarter_entries<false>(__int_as_float(quad_bcast<0>(xb)), __int_as_float(quad_bcast<1>(xb)),
-                                           __int_as_float(quad_bcast<2>(xb)), __int_as_float(quad_bcast<3>(xb)), qr);
+                const int4 q = quarter_entries<false>(__int_as_float(quad_bcast<0>(xb)), __int_as_float(quad_bcast<1>(xb)),
+                                                      __int_as_float(quad_bcast<2>(xb)), __int_as_float(quad_bcast<3>(xb)), qr);
                 if (need_s) {  // sum of the 64 activations of this wave and round: half a 128-block
                     const float hs = wave_sum_f(xs);
                     if (lane == 63) hsf[r * NW + wave] = hs;
                 }
+                if (g < nkb * GPB) *(int4 *)(F + (g / GPB) * Tab<false>::BLK + (g % GPB) * Tab<false>::G + qr * 16) = q;
             }
-            if (g < nkb * GPB) *(int4 *)(F + (g / GPB) * KSTRIDE + (g % GPB) * 64 + qr * 16) = q;
-        }
-        if (INT8 && need_s) {
-            const int hs = wave_sum_i(s_acc);
-            if (lane == 63) hsi[wave] = hs;
         }
         // epilogue operands of this lane's 128-blocks (vector loads, issued before the lookups)
         float esc[TW], ezp[TW];
@@ -259,11 +290,11 @@ __global__ __launch_bounds__(64 * NW) void lut_fused_gemv_kernel(LutParams p, in
         for (int t = 0; t < TW; ++t) {
             const int kbl = sigma + t * S;
             if (kbl < nkb) {
-                const uint32_t base = (uint32_t)(kbl * KSTRIDE);
+                const uint32_t base = (uint32_t)(kbl * Tab<INT8>::BLK);
                 int tot = 0;
 #pragma unroll
                 for (int i = 0; i < NPL; ++i)  // exact in INT32, see lookup_word
-                    tot += lookup_word(F, base, w[t][i]) << (pl * NPL + i);
+                    tot += lookup_word<INT8>(F, base, w[t][i]) << (pl * NPL + i);
                 if (INT8) {
                     yi += tot;
                 } else {

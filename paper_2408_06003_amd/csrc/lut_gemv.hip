@@ -1,59 +1,35 @@
 // Single-token bit-serial LUT mpGEMM (LUT Tensor Core, Section 3.1 bit-serial
 // tables with Eq. 3, 5 and 6; LMMA semantics O = A x W^T + Acc, Section 3.3.1).
 //
-// gfx950 mapping.  A workgroup (4 wavefronts) owns CW output columns over its
+// gfx950 mapping.  A workgroup (NW wavefronts) owns CW output columns over its
 // whole K range, so no other workgroup has to combine its results.  The 64 lanes
 // of a wavefront are (column, bit-plane group, K slice): CW = 64 / (PW * SW)
-// columns, PW lanes per column splitting the b bit-planes, SW K slices.  The
-// four wavefronts add four more K slices.  At any LDS read every lane of a
+// columns, PW lanes per column splitting the b bit-planes, SW K slices; the
+// wavefronts add NW times more K slices.  At any LDS read every lane of a
 // wavefront addresses the table of the same 4-activation group in at most SW = 2
-// different 128-blocks of K, whose tables sit in opposite halves of the LDS
-// banks (padded block stride), so reads are conflict-free; each table entry is
-// reused by the CW x (b / PW) lookups of that group (table reuse across columns,
-// the "elongated N" idea of Section 3.2.2, here across lanes and planes).
+// different 128-blocks of K, whose tables sit in different LDS banks (padded
+// block stride), so reads are conflict-free; each table entry is reused by the
+// CW x (b / PW) lookups of that group (table reuse across columns, the
+// "elongated N" idea of Section 3.2.2, here across lanes and planes).
 //
 // K is processed in chunks of CK 128-blocks.  For every chunk the half tables of
 // Eq. 5 (8 entries per 4 activations, the HBM format) are expanded into full
 // signed 16-entry tables in LDS, F[s i] = (s ? -T[i] : T[i]), so the stored Eq. 6
 // index addresses its entry directly (the inversion of Eq. 6 was done by the
 // packer and the negation here, once per workgroup, instead of per lookup).
-// Entries are INT32: exact integers on the INT8 path, and the FP16 entries times
-// 2^20 on the FP path (exact for |T| >= 2^-10, otherwise within 2^-21; tables
-// are normalized to |T| < 4 by the precompute).  Each chunk's half tables are
-// loaded before its weight words, so the expansion overlaps the weight stream.
+// Entries are INT16 on the INT8 path (exact) and INT32 on the FP path (the FP16
+// entries times 2^20: exact for |T| >= 2^-10, otherwise within 2^-21; tables are
+// normalized to |T| < 4 by the precompute).  Each chunk's half tables are loaded
+// before its weight words, so the expansion overlaps the weight stream.
 //
-// A lookup is one SDWA byte-add (table base + 4 * index), one ds_read_b32 and
+// A lookup is one SDWA byte-add (table base + entry offset), one LDS read and
 // half of a v_add3_u32.  Per 128-block the plane sums are combined as
 // sum_t 2^t acc_t (exact in INT32) and the Eq. 3 epilogue s' (A - z' S) is
 // applied in FP32; lanes of one column are then combined by a fixed butterfly
-// and the four wavefronts in order, so results are bitwise reproducible.
+// and the wavefronts in order, so results are bitwise reproducible.
 #include "lut_common.h"
 
 namespace lutgemm {
-
-// One quarter (4 entries) of a 16-entry signed table from half (qr & 1) of an
-// 8-entry half table: quarters 0, 1 are T[0..3], T[4..7]; quarters 2, 3 negated.
-template <bool INT8>
-__device__ __forceinline__ int4 table_quarter(uint2 h, int qr) {
-    int v[4];
-    const uint32_t w[2] = {h.x, h.y};
-    if (INT8) {
-        const int sg = qr >= 2 ? -1 : 1;
-#pragma unroll
-        for (int i = 0; i < 2; ++i) {
-            v[2 * i] = sg * (int)(int16_t)(uint16_t)(w[i] & 0xFFFFu);
-            v[2 * i + 1] = sg * (int)(int16_t)(uint16_t)(w[i] >> 16);
-        }
-    } else {
-        const float f = qr >= 2 ? -(float)(1 << FIX_SHIFT) : (float)(1 << FIX_SHIFT);
-#pragma unroll
-        for (int i = 0; i < 2; ++i) {
-            v[2 * i] = (int)rintf(h2f(w[i] & 0xFFFFu) * f);
-            v[2 * i + 1] = (int)rintf(h2f(w[i] >> 16) * f);
-        }
-    }
-    return make_int4(v[0], v[1], v[2], v[3]);
-}
 
 template <int BITS, int PW, int SW, int TW, int NW, bool INT8>
 __global__ __launch_bounds__(64 * NW) void lut_gemv2_kernel(LutParams p, int wfmt) {
@@ -65,7 +41,7 @@ __global__ __launch_bounds__(64 * NW) void lut_gemv2_kernel(LutParams p, int wfm
     constexpr int QPT = CK * GPB * 4 / NT; // table quarters staged per thread and chunk
     static_assert(QPT * NT == CK * GPB * 4, "table quarters divide evenly over the threads");
     static_assert(TW * NPL <= 4, "at most four prefetched weight words per lane");
-    __shared__ __attribute__((aligned(16))) char F[CK * KSTRIDE];
+    __shared__ __attribute__((aligned(16))) char F[CK * Tab<INT8>::BLK];
     __shared__ float redf[NW][CW];
     __shared__ int redi[NW][CW];
 
@@ -114,9 +90,7 @@ __global__ __launch_bounds__(64 * NW) void lut_gemv2_kernel(LutParams p, int wfm
 #pragma unroll
         for (int r = 0; r < QPT; ++r) {
             const int e = tid + NT * r, g = e >> 2;
-            if (g < nkb * GPB)
-                *(int4 *)(F + (g / GPB) * KSTRIDE + (g % GPB) * 64 + (e & 3) * 16) =
-                    table_quarter<INT8>(tq[r], e & 3);
+            if (g < nkb * GPB) store_quarter<INT8>(F, g / GPB, g % GPB, e & 3, tq[r]);
         }
         // epilogue operands of this lane's 128-blocks (vector loads, issued before the lookups)
         float esc[TW], ezr[TW];
@@ -139,11 +113,11 @@ __global__ __launch_bounds__(64 * NW) void lut_gemv2_kernel(LutParams p, int wfm
         for (int t = 0; t < TW; ++t) {
             const int kbl = sigma + t * S;
             if (kbl < nkb) {
-                const uint32_t base = (uint32_t)(kbl * KSTRIDE);
+                const uint32_t base = (uint32_t)(kbl * Tab<INT8>::BLK);
                 int tot = 0;
 #pragma unroll
                 for (int i = 0; i < NPL; ++i)  // exact in INT32, see lookup_word
-                    tot += lookup_word(F, base, w[t][i]) << (pl * NPL + i);
+                    tot += lookup_word<INT8>(F, base, w[t][i]) << (pl * NPL + i);
                 if (INT8)
                     yi += tot;
                 else
@@ -193,7 +167,7 @@ __global__ __launch_bounds__(64 * NW) void lut_gemv2_kernel(LutParams p, int wfm
 template <int BITS, int KBS, bool INT8>
 __global__ __launch_bounds__(256) void lut_gemv_split_kernel(LutParams p, int wfmt) {
     constexpr int QPT = (KBS * GPB * 4 + 255) / 256;  // table quarters per thread
-    __shared__ __attribute__((aligned(16))) char F[KBS * KSTRIDE];
+    __shared__ __attribute__((aligned(16))) char F[KBS * Tab<INT8>::BLK];
     const int tid = threadIdx.x;
     const int64_t n = (int64_t)blockIdx.x * NTILE + tid;
     const int split = blockIdx.y;
@@ -239,7 +213,7 @@ __global__ __launch_bounds__(256) void lut_gemv_split_kernel(LutParams p, int wf
     for (int r = 0; r < QPT; ++r) {
         const int e = tid + 256 * r, g = e >> 2;
         if (g < nkb * GPB)
-            *(int4 *)(F + (g / GPB) * KSTRIDE + (g % GPB) * 64 + (e & 3) * 16) = table_quarter<INT8>(tq[r], e & 3);
+            store_quarter<INT8>(F, g / GPB, g % GPB, e & 3, tq[r]);
     }
     lds_barrier();
 
@@ -255,12 +229,13 @@ __global__ __launch_bounds__(256) void lut_gemv_split_kernel(LutParams p, int wf
                 int acc = 0;
 #pragma unroll
                 for (int d = 0; d < 4; ++d) {
-                    const uint32_t lo = wd[d] << 2, hi = wd[d] >> 2;
-                    const char *Fg = F + kbl * KSTRIDE + d * 8 * 64;
-                    acc += lds_i32(Fg + 0 * 64, idx4<0>(lo)) + lds_i32(Fg + 1 * 64, idx4<0>(hi));
-                    acc += lds_i32(Fg + 2 * 64, idx4<1>(lo)) + lds_i32(Fg + 3 * 64, idx4<1>(hi));
-                    acc += lds_i32(Fg + 4 * 64, idx4<2>(lo)) + lds_i32(Fg + 5 * 64, idx4<2>(hi));
-                    acc += lds_i32(Fg + 6 * 64, idx4<3>(lo)) + lds_i32(Fg + 7 * 64, idx4<3>(hi));
+                    constexpr int GS = Tab<INT8>::G;
+                    const uint32_t lo = INT8 ? wd[d] << 1 : wd[d] << 2, hi = INT8 ? wd[d] >> 3 : wd[d] >> 2;
+                    const char *Fg = F + kbl * Tab<INT8>::BLK + d * 8 * GS;
+                    acc += lds_entry<INT8>(Fg + 0 * GS, idx_off<0, INT8>(lo)) + lds_entry<INT8>(Fg + 1 * GS, idx_off<0, INT8>(hi));
+                    acc += lds_entry<INT8>(Fg + 2 * GS, idx_off<1, INT8>(lo)) + lds_entry<INT8>(Fg + 3 * GS, idx_off<1, INT8>(hi));
+                    acc += lds_entry<INT8>(Fg + 4 * GS, idx_off<2, INT8>(lo)) + lds_entry<INT8>(Fg + 5 * GS, idx_off<2, INT8>(hi));
+                    acc += lds_entry<INT8>(Fg + 6 * GS, idx_off<3, INT8>(lo)) + lds_entry<INT8>(Fg + 7 * GS, idx_off<3, INT8>(hi));
                 }
                 tot += acc << t;  // exact in INT32, see the kernel above
             }
