@@ -81,7 +81,7 @@ LutPlan plan_lut(const Layout &L, int64_t M) {
     LutPlan P{};
     const int64_t target = env_int("LUTGEMM_TARGET_BLOCKS", 256);
     const int64_t weight_bytes = L.KB * L.bits * L.N * 16;
-    int kind = M > 2 ? 1 : (weight_bytes <= (int64_t)env_int("LUTGEMM_WHOLEK_MAX_KB", 6000) * 1000 ? 0 : 2);
+    int kind = M > 2 ? 1 : (weight_bytes <= (int64_t)env_int("LUTGEMM_WHOLEK_MAX_KB", 10000) * 1000 ? 0 : 2);
     const int forced_kind = env_int("LUTGEMM_GEMV_KIND", -1);
     if (M <= 2 && (forced_kind == 0 || forced_kind == 2)) kind = forced_kind;
     if (kind == 0) {

@@ -19,8 +19,9 @@
 //   3. The activation sums: per 128-block S_kb on the FP path (zero-point term of
 //      Eq. 3), per chunk on the INT8 path (ternary integer offset), by fixed-order
 //      DPP sums over the lanes that built the tables.
-// The weights of the chunk are loaded before any of this, so their memory latency
-// overlaps the table build; lookups and epilogue are those of lut_gemv.hip.  The
+// The weights of the chunk are requested right after the activations, so their
+// memory latency overlaps the table build; lookups and epilogue are those of
+// lut_gemv.hip.  The
 // zero-point term is applied per 128-block: s'_q z'_q S_q = sum over the blocks
 // of group q of s'_q z'_q S_kb.
 #include "lut_common.h"
@@ -188,10 +189,12 @@ __global__ __launch_bounds__(64 * NW) void lut_fused_gemv_kernel(LutParams p, in
         }
     };
 
-    // weights and activations of the first chunk, then the epilogue operands
+    // activations, then weights of the first chunk, then the epilogue operands.
+    // Vector loads retire in issue order: the activation-max reduction waits only
+    // for the activations, and the weights keep streaming in during the table build.
     int nkb = (int)((kbB - kbA) < CK ? (kbB - kbA) : CK);
-    load_weights(kbA, nkb);
     load_acts(kbA, nkb);
+    load_weights(kbA, nkb);
     Epi ep{};
     if (p.splits == 1) ep = load_epi<INT8>(p, wfmt, m, n, false);
 
@@ -234,8 +237,8 @@ __global__ __launch_bounds__(64 * NW) void lut_fused_gemv_kernel(LutParams p, in
     for (int64_t kc = kbA; kc < kbB; kc += CK) {
         nkb = (int)((kbB - kc) < CK ? (kbB - kc) : CK);
         if (kc != kbA) {
-            load_weights(kc, nkb);
             load_acts(kc, nkb);
+            load_weights(kc, nkb);
             lds_barrier();  // the previous chunk's tables and sums are no longer read
         }
         // 2-3. signed tables of this chunk and the activation sums
