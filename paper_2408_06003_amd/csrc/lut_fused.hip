@@ -139,7 +139,7 @@ __global__ __launch_bounds__(64 * NW) void lut_fused_gemv_kernel(LutParams p, in
     __shared__ float redf[NW][CW];
     __shared__ int redi[NW][CW];
     __shared__ float hsf[QPT * NW];  // FP path: half-block activation sums, [round][wave]
-    __shared__ int hsi[NW];          // INT8 path: activation sum of the chunk, per wave
+    __shared__ int hsi[NW];          // INT8 path: activation sum of the K range, per wave
     __shared__ float wmax[NW];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -216,24 +216,21 @@ __global__ __launch_bounds__(64 * NW) void lut_fused_gemv_kernel(LutParams p, in
     amax = wmax[0];
 #pragma unroll
     for (int v = 1; v < NW; ++v) amax = fmaxf(amax, wmax[v]);
-    float scale, tok;
+    // the table scale now; the output factor t[m] (needed only by the epilogue) later
+    float scale;
+    int e2 = 0;
     if (INT8) {
         scale = amax == 0.f ? 0.f : __fdiv_rn(127.0f, amax);
-        tok = amax == 0.f ? 0.f : __fdiv_rn(amax, 127.0f);
     } else if (amax == 0.f) {
         scale = 1.f;
-        tok = 1.f;
     } else {
-        int e;
-        (void)frexpf(amax, &e);
-        scale = ldexpf(1.f, -e);
-        tok = ldexpf(1.f, e);
+        (void)frexpf(amax, &e2);
+        scale = ldexpf(1.f, -e2);
     }
-    ep.tok = tok;
-    if (p.tok_out && blockIdx.x == 0 && split == 0 && tid == 0) p.tok_out[m] = tok;
 
     float yf = 0.f;
     int yi = 0;
+    int s_tot = 0;  // INT8 path: this lane's share of the activation sum
     for (int64_t kc = kbA; kc < kbB; kc += CK) {
         nkb = (int)((kbB - kc) < CK ? (kbB - kc) : CK);
         if (kc != kbA) {
@@ -243,7 +240,6 @@ __global__ __launch_bounds__(64 * NW) void lut_fused_gemv_kernel(LutParams p, in
         }
         // 2-3. signed tables of this chunk and the activation sums
         if constexpr (INT8) {
-            int s_acc = 0;
 #pragma unroll
             for (int r = 0; r < GPT; ++r) {
                 const int g = tid + NT * r;
@@ -251,12 +247,8 @@ __global__ __launch_bounds__(64 * NW) void lut_fused_gemv_kernel(LutParams p, in
                 const int q1 = (int)act_value<true>(ag[r].x >> 16, scale);
                 const int q2 = (int)act_value<true>(ag[r].y & 0xFFFFu, scale);
                 const int q3 = (int)act_value<true>(ag[r].y >> 16, scale);
-                s_acc += (q0 + q1) + (q2 + q3);
+                s_tot += (q0 + q1) + (q2 + q3);
                 if (g < nkb * GPB) build_group_i16(F + (g / GPB) * Tab<true>::BLK + (g % GPB) * Tab<true>::G, q0, q1, q2, q3);
-            }
-            if (need_s) {
-                const int hs = wave_sum_i(s_acc);
-                if (lane == 63) hsi[wave] = hs;
             }
         } else {
 #pragma unroll
@@ -308,10 +300,17 @@ __global__ __launch_bounds__(64 * NW) void lut_fused_gemv_kernel(LutParams p, in
                 }
             }
         }
-        if (INT8 && need_s && sigma == 0 && pl == 0) {  // the chunk's activation sum, once per column
-#pragma unroll
-            for (int v = 0; v < NW; ++v) yi += hsi[v];
-        }
+    }
+    float tok;
+    if (INT8)
+        tok = amax == 0.f ? 0.f : __fdiv_rn(amax, 127.0f);
+    else
+        tok = amax == 0.f ? 1.f : ldexpf(1.f, e2);
+    ep.tok = tok;
+    if (p.tok_out && blockIdx.x == 0 && split == 0 && tid == 0) p.tok_out[m] = tok;
+    if (INT8 && need_s) {  // the activation sum of this workgroup's K range, per wavefront
+        const int hs = wave_sum_i(s_tot);
+        if (lane == 63) hsi[wave] = hs;
     }
 
     // combine the lanes of each column (fixed butterfly), then the wavefronts in order
@@ -334,6 +333,10 @@ __global__ __launch_bounds__(64 * NW) void lut_fused_gemv_kernel(LutParams p, in
         for (int v = 1; v < NW; ++v) {
             sf += redf[v][lane];
             si += redi[v][lane];
+        }
+        if (INT8 && need_s) {  // ternary offset S, once per column
+#pragma unroll
+            for (int v = 0; v < NW; ++v) si += hsi[v];
         }
         if (p.splits == 1)
             store_out<INT8>(p, wfmt, m, n, sf, si, ep);
