@@ -90,10 +90,10 @@ LutPlan plan_lut(const Layout &L, int64_t M) {
         P.m_tiles = M;
         // (columns per workgroup, 128-blocks per chunk) of each decomposition, widest first
         static const int b1[2][2] = {{64, 16}, {32, 32}};
-        static const int b2[3][2] = {{64, 8}, {32, 16}, {16, 32}};
-        static const int b4[2][2] = {{32, 8}, {16, 16}};
+        static const int b2[3][2] = {{64, 16}, {32, 16}, {16, 32}};
+        static const int b4[3][2] = {{64, 16}, {32, 16}, {16, 16}};
         const int(*cfg)[2] = L.bits == 1 ? b1 : (L.bits == 2 ? b2 : b4);
-        const int ncfg = L.bits == 2 ? 3 : 2;
+        const int ncfg = L.bits == 1 ? 2 : 3;
         int pick = ncfg - 1;
         for (int i = 0; i < ncfg; ++i)
             if ((L.N + cfg[i][0] - 1) / cfg[i][0] * M >= target) {
@@ -103,7 +103,6 @@ LutPlan plan_lut(const Layout &L, int64_t M) {
         const int forced = env_int("LUTGEMM_GEMV_CFG", -1);
         if (forced >= 0 && forced < ncfg) pick = forced;
         P.gemv_cfg = pick;
-        P.gemv_nw = env_int("LUTGEMM_GEMV_NW", 16);  // the most the decomposition allows (see lut_gemv.hip)
         const int cw = cfg[pick][0], ck = cfg[pick][1];
         P.n_tiles = (L.N + cw - 1) / cw;
         const int64_t blocks = P.n_tiles * M;
@@ -203,8 +202,8 @@ static LutParams lut_params(const Layout &L, const LutPlan &plan, int64_t M, con
 }
 
 static void log_plan(const char *who, const Layout &L, const LutPlan &plan, int64_t M) {
-    std::fprintf(stderr, "%s: M=%lld K=%lld N=%lld b=%d kind=%d cfg=%d nw=%d kbs=%d splits=%d mt=%d grid=%lldx%dx%lld\n",
-                 who, (long long)M, (long long)L.K, (long long)L.N, L.bits, plan.kind, plan.gemv_cfg, plan.gemv_nw,
+    std::fprintf(stderr, "%s: M=%lld K=%lld N=%lld b=%d kind=%d cfg=%d kbs=%d splits=%d mt=%d grid=%lldx%dx%lld\n",
+                 who, (long long)M, (long long)L.K, (long long)L.N, L.bits, plan.kind, plan.gemv_cfg,
                  plan.kbs, plan.splits, plan.mt, (long long)plan.n_tiles, plan.splits, (long long)plan.m_tiles);
 }
 

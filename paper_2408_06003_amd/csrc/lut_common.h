@@ -18,6 +18,13 @@ __device__ __forceinline__ void lds_barrier() {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
 
+// Keeps a value in a VGPR so that loads indexed by it stay vector loads (scalar
+// loads share the LDS completion counter and would serialize the lookups).
+__device__ __forceinline__ int64_t lane_value(int64_t x) {
+    asm volatile("" : "+v"(x));
+    return x;
+}
+
 __device__ __forceinline__ float h2f(uint32_t bits16) {
     return __half2float(__ushort_as_half((unsigned short)bits16));
 }
@@ -182,63 +189,89 @@ struct SZ {
     float sp, zp;
 };
 
-// Reinterpreted scale and zero (Eq. 2) of quantization group q, column n.
-// Branch-free, and every load is a vector load (the index is kept in a VGPR):
-// scalar loads share the completion counter of LDS reads and would serialize them.
-__device__ __forceinline__ SZ load_sz(const LutParams &p, int q, int64_t n) {
+// Raw metadata words of quantization group q, column n (FP16 s and z, or the two
+// FP32 per-tensor values).  Branch-free, and every load is a vector load (the
+// index is kept in a VGPR): scalar loads share the completion counter of LDS
+// reads and would serialize them.
+__device__ __forceinline__ uint2 load_meta_words(const LutParams &p, int q, int64_t n) {
     int64_t idx = p.per_tensor ? 0 : (int64_t)q * p.N_pad + n;
     asm volatile("" : "+v"(idx));
     const uint32_t *mw = (const uint32_t *)p.meta;
-    const uint32_t m0 = mw[idx];
-    const uint32_t m1 = mw[idx + (p.per_tensor ? 1 : 0)];
-    const float s = p.per_tensor ? __uint_as_float(m0) : h2f(m0 & 0xFFFFu);
-    const float z = p.per_tensor ? __uint_as_float(m1) : h2f(m0 >> 16);
+    return make_uint2(mw[idx], mw[idx + (p.per_tensor ? 1 : 0)]);
+}
+
+// Reinterpreted scale and zero (Eq. 2) from the raw metadata words.
+__device__ __forceinline__ SZ decode_sz(const LutParams &p, uint2 mw) {
+    const float s = p.per_tensor ? __uint_as_float(mw.x) : h2f(mw.x & 0xFFFFu);
+    const float z = p.per_tensor ? __uint_as_float(mw.y) : h2f(mw.x >> 16);
     SZ r;
     r.sp = p.cs * s;
     r.zp = fmaf(p.cz, z, p.c0);
     return r;
 }
 
-// Per-column weight scale of the INT8 path (per-tensor or per-channel).
-__device__ __forceinline__ float int_weight_scale(const LutParams &p, bool per_tensor, int64_t n) {
-    if (per_tensor) return ((const float *)p.meta)[n];  // n = 0: the one FP32 scale
-    return h2f(((const uint32_t *)p.meta)[n] & 0xFFFFu);
+__device__ __forceinline__ SZ load_sz(const LutParams &p, int q, int64_t n) {
+    return decode_sz(p, load_meta_words(p, q, n));
 }
 
-// Keeps a value in a VGPR so that loads indexed by it stay vector loads (scalar
-// loads share the LDS completion counter and would serialize the lookups).
-__device__ __forceinline__ int64_t lane_value(int64_t x) {
-    asm volatile("" : "+v"(x));
-    return x;
+// Epilogue operands of one 128-block kb and column n, as raw loads that can be
+// issued long before they are used: the metadata word(s) of the block's
+// quantization group and the group's activation sum S[m][q] (the zero-point term
+// is applied by the group's first block only, see blk_epilogue).  Nothing here
+// uses a loaded value, so no wait is placed until blk_epilogue.
+struct BlkMeta {
+    uint32_t m0, m1;
+    float s;
+};
+
+__device__ __forceinline__ BlkMeta load_blk_meta(const LutParams &p, int64_t kb, int64_t m, int64_t n) {
+    const int q = (int)(((float)kb + 0.5f) * p.inv_kpg);
+    int64_t idx = p.per_tensor ? 0 : (int64_t)q * p.N_pad + n;
+    asm volatile("" : "+v"(idx));
+    const uint32_t *mw = (const uint32_t *)p.meta;
+    BlkMeta b;
+    b.m0 = mw[idx];
+    b.m1 = mw[idx + (p.per_tensor ? 1 : 0)];
+    b.s = ((const float *)p.S)[lane_value(m * p.Q + q)];
+    return b;
+}
+
+// (s'/2^FIX_SHIFT, s' z' S or 0) of block kb from its raw operands (Eq. 2-3).
+__device__ __forceinline__ float2 blk_epilogue(const LutParams &p, const BlkMeta &b, int64_t kb) {
+    const int q = (int)(((float)kb + 0.5f) * p.inv_kpg);
+    const float s = p.per_tensor ? __uint_as_float(b.m0) : h2f(b.m0 & 0xFFFFu);
+    const float z = p.per_tensor ? __uint_as_float(b.m1) : h2f(b.m0 >> 16);
+    const float sp = p.cs * s, zp = fmaf(p.cz, z, p.c0);
+    return make_float2(sp * (1.0f / (float)(1 << FIX_SHIFT)), kb == (int64_t)q * p.kpg ? sp * zp * b.s : 0.f);
 }
 
 // Operands of the output epilogue of (m, n): the per-token factor t[m], the INT8
 // path's weight scale, the previous output when accumulating, and the ternary
 // group sum S[m][0] (added by the first K split only).  Loaded ahead of the main
-// loop, so that their memory latency overlaps the lookups instead of following
-// them; every load is a vector load.
+// loop as raw words, so that their memory latency overlaps the lookups instead of
+// following them, and decoded by store_out; every load is a vector load.
 struct Epi {
-    float tok, sw, prev;
+    float tok;
+    uint32_t sw;    // weight scale word: FP32 bits (per tensor) or FP16 s in the low half (per channel)
+    uint32_t prev;  // previous output bits (INT32, FP32, or FP16 in the low half)
     int s0;
 };
 
 template <bool INT8>
 __device__ __forceinline__ Epi load_epi(const LutParams &p, int wfmt, int64_t m, int64_t n, bool first_split) {
-    Epi e{1.f, 1.f, 0.f, 0};
+    Epi e{1.f, 0x3F800000u, 0u, 0};
     if (n >= p.N) return e;
     const int64_t mv = lane_value(m), nv = lane_value(n), o = mv * p.N + nv;
     if (p.tok) e.tok = p.tok[mv];
     if (INT8) {
-        e.sw = int_weight_scale(p, p.per_tensor != 0, p.per_tensor ? lane_value(0) : nv);
+        e.sw = ((const uint32_t *)p.meta)[p.per_tensor ? lane_value(0) : nv];
         if (first_split && wfmt == LUTGEMM_WFMT_TERNARY) e.s0 = ((const int *)p.S)[mv * p.Q];
     }
     if (p.accumulate) {
-        if (INT8 && p.out_dtype == LUTGEMM_OUT_INT32)
-            e.prev = __int_as_float(((const int *)p.out)[o]);
-        else if (p.out_dtype == LUTGEMM_OUT_FP32)
-            e.prev = ((const float *)p.out)[o];
+        if (p.out_dtype == LUTGEMM_OUT_FP16)
+            e.prev = ((const uint16_t *)p.out)[o];
         else
-            e.prev = __half2float(((const __half *)p.out)[o]);
+            e.prev = ((const uint32_t *)p.out)[o];
     }
     return e;
 }
@@ -254,14 +287,15 @@ __device__ __forceinline__ void store_out(const LutParams &p, int wfmt, int64_t 
     if (INT8) {
         const int y = (wfmt == LUTGEMM_WFMT_TERNARY) ? (yi >> 1) : yi;  // (A + S) / 2 is exact
         if (p.out_dtype == LUTGEMM_OUT_INT32) {
-            ((int *)p.out)[o] = p.accumulate ? y + __float_as_int(e.prev) : y;
+            ((int *)p.out)[o] = p.accumulate ? y + (int)e.prev : y;
             return;
         }
-        v = ((float)y * e.tok) * e.sw;
+        const float sw = p.per_tensor ? __uint_as_float(e.sw) : h2f(e.sw & 0xFFFFu);
+        v = ((float)y * e.tok) * sw;
     } else {
         v = e.tok * yf;
     }
-    if (p.accumulate) v += e.prev;
+    if (p.accumulate) v += p.out_dtype == LUTGEMM_OUT_FP16 ? h2f(e.prev) : __uint_as_float(e.prev);
     if (p.out_dtype == LUTGEMM_OUT_FP32)
         ((float *)p.out)[o] = v;
     else

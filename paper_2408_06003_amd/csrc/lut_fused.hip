@@ -156,16 +156,16 @@ __global__ __launch_bounds__(64 * NW) void lut_fused_gemv_kernel(LutParams p, in
     const uint2 *a4 = (const uint2 *)a1;  // one 4-activation group per element
     const bool need_s = wfmt != LUTGEMM_WFMT_BINARY;   // binary weights have z' = 0
 
+    // Chunk loads are unconditional (clamped indices, values past the chunk
+    // ignored) and conditional loads are issued before them, so every wait the
+    // compiler places counts exactly the loads after the one it waits for.
     uint4 w[TW][NPL];
     auto load_weights = [&](int64_t kc, int nkb) {
 #pragma unroll
         for (int t = 0; t < TW; ++t) {
-            const int kbl = sigma + t * S;
-            if (kbl < nkb) {
+            const int kbl = sigma + t * S, kbc = kbl < nkb ? kbl : nkb - 1;
 #pragma unroll
-                for (int i = 0; i < NPL; ++i)
-                    w[t][i] = p.planes[((kc + kbl) * BITS + pl * NPL + i) * p.N_pad + n];
-            }
+            for (int i = 0; i < NPL; ++i) w[t][i] = p.planes[((kc + kbc) * BITS + pl * NPL + i) * p.N_pad + n];
         }
     };
     // FP path: lane e of a round holds activation e of the chunk, so the 4 lanes of a
@@ -177,14 +177,16 @@ __global__ __launch_bounds__(64 * NW) void lut_fused_gemv_kernel(LutParams p, in
         if constexpr (INT8) {
 #pragma unroll
             for (int r = 0; r < GPT; ++r) {
-                const int g = tid + NT * r;
-                ag[r] = g < nkb * GPB ? a4[kc * GPB + g] : make_uint2(0u, 0u);
+                const int g = tid + NT * r, gc = g < nkb * GPB ? g : nkb * GPB - 1;
+                const uint2 v = a4[kc * GPB + gc];
+                ag[r] = g < nkb * GPB ? v : make_uint2(0u, 0u);
             }
         } else {
 #pragma unroll
             for (int r = 0; r < QPT; ++r) {
-                const int e = tid + NT * r;
-                av[r] = e < nkb * KBLK ? (uint32_t)a1[kc * KBLK + e] : 0u;
+                const int e = tid + NT * r, ec = e < nkb * KBLK ? e : nkb * KBLK - 1;
+                const uint32_t v = a1[kc * KBLK + ec];
+                av[r] = e < nkb * KBLK ? v : 0u;
             }
         }
     };
@@ -192,11 +194,11 @@ __global__ __launch_bounds__(64 * NW) void lut_fused_gemv_kernel(LutParams p, in
     // activations, then weights of the first chunk, then the epilogue operands.
     // Vector loads retire in issue order: the activation-max reduction waits only
     // for the activations, and the weights keep streaming in during the table build.
+    Epi ep{};
+    if (p.splits == 1) ep = load_epi<INT8>(p, wfmt, m, n, false);
     int nkb = (int)((kbB - kbA) < CK ? (kbB - kbA) : CK);
     load_acts(kbA, nkb);
     load_weights(kbA, nkb);
-    Epi ep{};
-    if (p.splits == 1) ep = load_epi<INT8>(p, wfmt, m, n, false);
 
     // 1. amax of the whole token: the first chunk from registers, the rest from memory
     float amax = 0.f;
@@ -208,8 +210,10 @@ __global__ __launch_bounds__(64 * NW) void lut_fused_gemv_kernel(LutParams p, in
         for (int r = 0; r < QPT; ++r) amax = fmaxf(amax, fabsf(h2f(av[r])));
     }
     const int64_t j0 = kbA * GPB, j1 = j0 + (int64_t)nkb * GPB;
-    for (int64_t j = tid; j < p.J; j += NT)
-        if (j < j0 || j >= j1) amax = fmaxf(amax, absmax4(a4[j]));
+    if (j1 - j0 < p.J) {  // the token extends past the first chunk (several chunks or a K split)
+        for (int64_t j = tid; j < p.J; j += NT)
+            if (j < j0 || j >= j1) amax = fmaxf(amax, absmax4(a4[j]));
+    }
     amax = wave_max(amax);
     if (lane == 63) wmax[wave] = amax;
     lds_barrier();
@@ -265,19 +269,15 @@ __global__ __launch_bounds__(64 * NW) void lut_fused_gemv_kernel(LutParams p, in
                 if (g < nkb * GPB) *(int4 *)(F + (g / GPB) * Tab<false>::BLK + (g % GPB) * Tab<false>::G + qr * 16) = q;
             }
         }
-        // epilogue operands of this lane's 128-blocks (vector loads, issued before the lookups)
-        float esc[TW], ezp[TW];
+        // epilogue operands of this lane's 128-blocks (unconditional vector loads,
+        // decoded after the barrier)
+        uint2 mwd[TW];
+        if constexpr (!INT8) {
 #pragma unroll
-        for (int t = 0; t < TW; ++t) {
-            esc[t] = 0.f;
-            ezp[t] = 0.f;
-            const int kbl = sigma + t * S;
-            if (!INT8 && kbl < nkb) {
-                const int64_t kb = kc + kbl;
-                const int q = (int)(((float)kb + 0.5f) * p.inv_kpg);
-                const SZ sz = load_sz(p, q, lane_value(n));
-                esc[t] = sz.sp * (1.0f / (float)(1 << FIX_SHIFT));
-                ezp[t] = sz.sp * sz.zp;
+            for (int t = 0; t < TW; ++t) {
+                const int kbl = sigma + t * S, kbc = kbl < nkb ? kbl : nkb - 1;
+                const int q = (int)(((float)(kc + kbc) + 0.5f) * p.inv_kpg);
+                mwd[t] = load_meta_words(p, q, lane_value(n));
             }
         }
         lds_barrier();
@@ -290,13 +290,14 @@ __global__ __launch_bounds__(64 * NW) void lut_fused_gemv_kernel(LutParams p, in
 #pragma unroll
                 for (int i = 0; i < NPL; ++i)  // exact in INT32, see lookup_word
                     tot += lookup_word<INT8>(F, base, w[t][i]) << (pl * NPL + i);
-                if (INT8) {
+                if constexpr (INT8) {
                     yi += tot;
                 } else {
-                    yf = fmaf(esc[t], (float)tot, yf);
+                    const SZ sz = decode_sz(p, mwd[t]);
+                    yf = fmaf(sz.sp * (1.0f / (float)(1 << FIX_SHIFT)), (float)tot, yf);
                     // activation sum of this 128-block: the two half-block sums of its round
                     const int hb = (kbl / BPR) * NW + 2 * (kbl % BPR);
-                    if (need_s && pl == 0) yf -= ezp[t] * (hsf[hb] + hsf[hb + 1]);
+                    if (need_s && pl == 0) yf -= (sz.sp * sz.zp) * (hsf[hb] + hsf[hb + 1]);
                 }
             }
         }
@@ -345,32 +346,29 @@ __global__ __launch_bounds__(64 * NW) void lut_fused_gemv_kernel(LutParams p, in
     }
 }
 
-// Same lane decompositions as the table-fed GEMV (see lut_gemv.hip).
-template <int BITS, int PW, int SW, int TW, bool INT8>
+// Same lane decompositions as the table-fed GEMV (see lut_gemv.hip): 16 wavefronts,
+// one 128-block per K slice and chunk.
+template <int BITS, int PW, int SW, bool INT8>
 static void launch_fused_cfg(const LutParams &p, const Layout &L, const LutPlan &plan, hipStream_t s) {
     constexpr int CW = 64 / (PW * SW);
     const dim3 grid((unsigned)((L.N + CW - 1) / CW), (unsigned)plan.splits, (unsigned)p.M);
-    if (plan.gemv_nw == 16 && TW % 4 == 0)
-        hipLaunchKernelGGL((lut_fused_gemv_kernel<BITS, PW, SW, (TW + 3) / 4, 16, INT8>), grid, dim3(1024), 0, s, p, L.wfmt);
-    else if (plan.gemv_nw >= 8 && TW % 2 == 0)
-        hipLaunchKernelGGL((lut_fused_gemv_kernel<BITS, PW, SW, (TW + 1) / 2, 8, INT8>), grid, dim3(512), 0, s, p, L.wfmt);
-    else
-        hipLaunchKernelGGL((lut_fused_gemv_kernel<BITS, PW, SW, TW, 4, INT8>), grid, dim3(256), 0, s, p, L.wfmt);
+    hipLaunchKernelGGL((lut_fused_gemv_kernel<BITS, PW, SW, 1, 16, INT8>), grid, dim3(1024), 0, s, p, L.wfmt);
 }
 
 template <bool INT8>
 static void launch_fused_bits(const LutParams &p, const Layout &L, const LutPlan &plan, hipStream_t s) {
     if (L.bits == 1) {
-        if (plan.gemv_cfg == 0) launch_fused_cfg<1, 1, 1, 4, INT8>(p, L, plan, s);
-        else launch_fused_cfg<1, 1, 2, 4, INT8>(p, L, plan, s);
+        if (plan.gemv_cfg == 0) launch_fused_cfg<1, 1, 1, INT8>(p, L, plan, s);
+        else launch_fused_cfg<1, 1, 2, INT8>(p, L, plan, s);
     } else if (L.bits == 2) {
-        if (plan.gemv_cfg == 0) launch_fused_cfg<2, 1, 1, 2, INT8>(p, L, plan, s);
-        else if (plan.gemv_cfg == 1) launch_fused_cfg<2, 2, 1, 4, INT8>(p, L, plan, s);
-        else launch_fused_cfg<2, 2, 2, 4, INT8>(p, L, plan, s);
+        if (plan.gemv_cfg == 0) launch_fused_cfg<2, 1, 1, INT8>(p, L, plan, s);
+        else if (plan.gemv_cfg == 1) launch_fused_cfg<2, 2, 1, INT8>(p, L, plan, s);
+        else launch_fused_cfg<2, 2, 2, INT8>(p, L, plan, s);
     } else {
         if constexpr (!INT8) {
-            if (plan.gemv_cfg == 0) launch_fused_cfg<4, 2, 1, 2, false>(p, L, plan, s);
-            else launch_fused_cfg<4, 4, 1, 4, false>(p, L, plan, s);
+            if (plan.gemv_cfg == 0) launch_fused_cfg<4, 1, 1, false>(p, L, plan, s);
+            else if (plan.gemv_cfg == 1) launch_fused_cfg<4, 2, 1, false>(p, L, plan, s);
+            else launch_fused_cfg<4, 4, 1, false>(p, L, plan, s);
         }
     }
 }

@@ -56,58 +56,57 @@ __global__ __launch_bounds__(64 * NW) void lut_gemv2_kernel(LutParams p, int wfm
     const int64_t kbA = (int64_t)split * p.kbs;
     const int64_t kbB = (kbA + p.kbs < p.KB) ? kbA + p.kbs : p.KB;
 
-    // Prefetch of one chunk: table quarters first, then the lane's weight words.
+    // Loads of one chunk: table quarters first, then the lane's weight words.
     // Loads retire in issue order, so waiting for the tables never waits for the
-    // weights, which keep streaming in while the tables are expanded.
-    uint2 tq[QPT];
-    uint4 w[TW][NPL];
-    auto load_chunk = [&](int64_t kc) {
+    // weights, which keep streaming in while the tables are expanded.  The next
+    // chunk's loads are issued before this chunk's lookups (software pipeline), so
+    // with several chunks per workgroup only the first one waits a full latency.
+    // Every chunk load is unconditional (indices past the chunk are clamped to its
+    // last group / block and the values ignored), so the waits the compiler
+    // places count exactly the loads issued after the ones they wait for;
+    // conditional loads (the epilogue operands) are issued before them.
+    uint2 tq[QPT], tqn[QPT];
+    uint4 w[TW][NPL], wn[TW][NPL];
+    auto load_chunk = [&](int64_t kc, uint2(&tq_)[QPT], uint4(&w_)[TW][NPL]) {
         const int nkb = (int)((kbB - kc) < CK ? (kbB - kc) : CK);
 #pragma unroll
         for (int r = 0; r < QPT; ++r) {
-            const int e = tid + NT * r, g = e >> 2;
-            if (g < nkb * GPB) tq[r] = ((const uint2 *)(p.T + m * p.J + kc * GPB + g))[e & 1];
+            const int e = tid + NT * r, g = e >> 2, gc = g < nkb * GPB ? g : nkb * GPB - 1;
+            tq_[r] = ((const uint2 *)(p.T + m * p.J + kc * GPB + gc))[e & 1];
         }
 #pragma unroll
         for (int t = 0; t < TW; ++t) {
-            const int kbl = sigma + t * S;
-            if (kbl < nkb) {
+            const int kbl = sigma + t * S, kbc = kbl < nkb ? kbl : nkb - 1;
 #pragma unroll
-                for (int i = 0; i < NPL; ++i)
-                    w[t][i] = p.planes[((kc + kbl) * BITS + pl * NPL + i) * p.N_pad + n];
-            }
+            for (int i = 0; i < NPL; ++i) w_[t][i] = p.planes[((kc + kbc) * BITS + pl * NPL + i) * p.N_pad + n];
         }
     };
 
     float yf = 0.f;
     int yi = 0;
     Epi ep{};
+    if (p.splits == 1) ep = load_epi<INT8>(p, wfmt, m, n, true);
+    load_chunk(kbA, tq, w);
     for (int64_t kc = kbA; kc < kbB; kc += CK) {
         const int nkb = (int)((kbB - kc) < CK ? (kbB - kc) : CK);
-        load_chunk(kc);
-        if (kc == kbA && p.splits == 1) ep = load_epi<INT8>(p, wfmt, m, n, true);
         lds_barrier();  // the previous chunk's tables are no longer read
 #pragma unroll
         for (int r = 0; r < QPT; ++r) {
             const int e = tid + NT * r, g = e >> 2;
             if (g < nkb * GPB) store_quarter<INT8>(F, g / GPB, g % GPB, e & 3, tq[r]);
         }
-        // epilogue operands of this lane's 128-blocks (vector loads, issued before the lookups)
-        float esc[TW], ezr[TW];
+        // epilogue operands of this lane's 128-blocks (unconditional vector loads,
+        // issued before the lookups)
+        BlkMeta bm[TW];
+        if constexpr (!INT8) {
 #pragma unroll
-        for (int t = 0; t < TW; ++t) {
-            esc[t] = 0.f;
-            ezr[t] = 0.f;
-            const int kbl = sigma + t * S;
-            if (!INT8 && kbl < nkb) {
-                const int64_t kb = kc + kbl;
-                const int q = (int)(((float)kb + 0.5f) * p.inv_kpg);
-                const SZ sz = load_sz(p, q, lane_value(n));
-                esc[t] = sz.sp * (1.0f / (float)(1 << FIX_SHIFT));
-                if (pl == 0 && kb == (int64_t)q * p.kpg)  // zero-point term once per group
-                    ezr[t] = sz.sp * sz.zp * ((const float *)p.S)[lane_value(m * p.Q + q)];
+            for (int t = 0; t < TW; ++t) {
+                const int kbl = sigma + t * S, kbc = kbl < nkb ? kbl : nkb - 1;
+                bm[t] = load_blk_meta(p, kc + kbc, m, lane_value(n));
             }
         }
+        const bool more = kc + CK < kbB;
+        if (more) load_chunk(kc + CK, tqn, wn);
         lds_barrier();
 #pragma unroll
         for (int t = 0; t < TW; ++t) {
@@ -118,11 +117,21 @@ __global__ __launch_bounds__(64 * NW) void lut_gemv2_kernel(LutParams p, int wfm
 #pragma unroll
                 for (int i = 0; i < NPL; ++i)  // exact in INT32, see lookup_word
                     tot += lookup_word<INT8>(F, base, w[t][i]) << (pl * NPL + i);
-                if (INT8)
+                if constexpr (INT8) {
                     yi += tot;
-                else
-                    yf = fmaf(esc[t], (float)tot, yf) - ezr[t];
+                } else {
+                    const float2 e = blk_epilogue(p, bm[t], kc + kbl);
+                    yf = fmaf(e.x, (float)tot, yf) - (pl == 0 ? e.y : 0.f);
+                }
             }
+        }
+        if (more) {
+#pragma unroll
+            for (int r = 0; r < QPT; ++r) tq[r] = tqn[r];
+#pragma unroll
+            for (int t = 0; t < TW; ++t)
+#pragma unroll
+                for (int i = 0; i < NPL; ++i) w[t][i] = wn[t][i];
         }
     }
 
@@ -175,40 +184,35 @@ __global__ __launch_bounds__(256) void lut_gemv_split_kernel(LutParams p, int wf
     const int64_t kb0 = (int64_t)split * KBS;
     const int nkb = (int)((p.KB - kb0) < KBS ? (p.KB - kb0) : KBS);
 
-    uint2 tq[QPT];
-#pragma unroll
-    for (int r = 0; r < QPT; ++r) {
-        const int e = tid + 256 * r, g = e >> 2;
-        if (g < nkb * GPB) tq[r] = ((const uint2 *)(p.T + m * p.J + kb0 * GPB + g))[e & 1];
-    }
-    uint4 w[KBS][BITS];
-#pragma unroll
-    for (int kbl = 0; kbl < KBS; ++kbl) {
-        if (kbl < nkb) {
-#pragma unroll
-            for (int t = 0; t < BITS; ++t) w[kbl][t] = p.planes[((kb0 + kbl) * BITS + t) * p.N_pad + n];
-        }
-    }
-    float esc[KBS], ezr[KBS];
-#pragma unroll
-    for (int kbl = 0; kbl < KBS; ++kbl) {
-        esc[kbl] = 0.f;
-        ezr[kbl] = 0.f;
-        if (!INT8 && kbl < nkb) {
-            const int64_t kb = kb0 + kbl;
-            const int q = (int)(((float)kb + 0.5f) * p.inv_kpg);
-            const SZ sz = load_sz(p, q, lane_value(n));
-            esc[kbl] = sz.sp * (1.0f / (float)(1 << FIX_SHIFT));
-            if (kb == (int64_t)q * p.kpg)  // zero-point term once per group
-                ezr[kbl] = sz.sp * sz.zp * ((const float *)p.S)[lane_value(m * p.Q + q)];
-        }
-    }
+    // conditional loads (epilogue operands) first, then the unconditional chunk
+    // loads with clamped indices (see lut_gemv2_kernel)
     Epi ep{};
     if (p.splits == 1)
         ep = load_epi<INT8>(p, wfmt, m, n, true);
     else if (INT8 && split == 0 && wfmt == LUTGEMM_WFMT_TERNARY)
         ep.s0 = ((const int *)p.S)[lane_value(m * p.Q)];
     const int s_total = ep.s0;
+    uint2 tq[QPT];
+#pragma unroll
+    for (int r = 0; r < QPT; ++r) {
+        const int e = tid + 256 * r, g = e >> 2, gc = g < nkb * GPB ? g : nkb * GPB - 1;
+        tq[r] = ((const uint2 *)(p.T + m * p.J + kb0 * GPB + gc))[e & 1];
+    }
+    uint4 w[KBS][BITS];
+#pragma unroll
+    for (int kbl = 0; kbl < KBS; ++kbl) {
+        const int kbc = kbl < nkb ? kbl : nkb - 1;
+#pragma unroll
+        for (int t = 0; t < BITS; ++t) w[kbl][t] = p.planes[((kb0 + kbc) * BITS + t) * p.N_pad + n];
+    }
+    BlkMeta bm[KBS];
+    if constexpr (!INT8) {
+#pragma unroll
+        for (int kbl = 0; kbl < KBS; ++kbl) {
+            const int kbc = kbl < nkb ? kbl : nkb - 1;
+            bm[kbl] = load_blk_meta(p, kb0 + kbc, m, lane_value(n));
+        }
+    }
 #pragma unroll
     for (int r = 0; r < QPT; ++r) {
         const int e = tid + 256 * r, g = e >> 2;
@@ -239,10 +243,12 @@ __global__ __launch_bounds__(256) void lut_gemv_split_kernel(LutParams p, int wf
                 }
                 tot += acc << t;  // exact in INT32, see the kernel above
             }
-            if (INT8)
+            if constexpr (INT8) {
                 yi += tot;
-            else
-                yf = fmaf(esc[kbl], (float)tot, yf) - ezr[kbl];
+            } else {
+                const float2 e = blk_epilogue(p, bm[kbl], kb0 + kbl);
+                yf = fmaf(e.x, (float)tot, yf) - e.y;
+            }
         }
     }
     if (p.splits == 1)
@@ -268,37 +274,33 @@ static void launch_split(const LutParams &p, const Layout &L, const LutPlan &pla
     }
 }
 
-// NW wavefronts per workgroup with TW * NW fixed, so the chunk (and the LDS
-// footprint) is the same for every NW; more wavefronts hide more latency.
-template <int BITS, int PW, int SW, int TW, bool INT8>
+// 16 wavefronts per workgroup, one 128-block per K slice and chunk.
+template <int BITS, int PW, int SW, bool INT8>
 static void launch_cfg(const LutParams &p, const Layout &L, const LutPlan &plan, hipStream_t s) {
     constexpr int CW = 64 / (PW * SW);
     const dim3 grid((unsigned)((L.N + CW - 1) / CW), (unsigned)plan.splits, (unsigned)p.M);
-    if (plan.gemv_nw == 16 && TW % 4 == 0)
-        hipLaunchKernelGGL((lut_gemv2_kernel<BITS, PW, SW, (TW + 3) / 4, 16, INT8>), grid, dim3(1024), 0, s, p, L.wfmt);
-    else if (plan.gemv_nw >= 8 && TW % 2 == 0)
-        hipLaunchKernelGGL((lut_gemv2_kernel<BITS, PW, SW, (TW + 1) / 2, 8, INT8>), grid, dim3(512), 0, s, p, L.wfmt);
-    else
-        hipLaunchKernelGGL((lut_gemv2_kernel<BITS, PW, SW, TW, 4, INT8>), grid, dim3(256), 0, s, p, L.wfmt);
+    hipLaunchKernelGGL((lut_gemv2_kernel<BITS, PW, SW, 1, 16, INT8>), grid, dim3(1024), 0, s, p, L.wfmt);
 }
 
-// Lane decompositions (PW, SW, TW) offered per bit width, indexed by LutPlan::gemv_cfg:
-//   b = 1: 0 -> (1,1,4) CW=64 CK=16   1 -> (1,2,4) CW=32 CK=32
-//   b = 2: 0 -> (1,1,2) CW=64 CK=8    1 -> (2,1,4) CW=32 CK=16   2 -> (2,2,4) CW=16 CK=32
-//   b = 4: 0 -> (2,1,2) CW=32 CK=8    1 -> (4,1,4) CW=16 CK=16
+// Lane decompositions (PW, SW) offered per bit width, indexed by LutPlan::gemv_cfg
+// (columns per workgroup CW = 64 / (PW SW), 128-blocks per chunk CK = 16 SW):
+//   b = 1: 0 -> (1,1) CW=64 CK=16   1 -> (1,2) CW=32 CK=32
+//   b = 2: 0 -> (1,1) CW=64 CK=16   1 -> (2,1) CW=32 CK=16   2 -> (2,2) CW=16 CK=32
+//   b = 4: 0 -> (1,1) CW=64 CK=16   1 -> (2,1) CW=32 CK=16   2 -> (4,1) CW=16 CK=16
 template <bool INT8>
 static int launch_gemv_bits(const LutParams &p, const Layout &L, const LutPlan &plan, hipStream_t s) {
     if (L.bits == 1) {
-        if (plan.gemv_cfg == 0) launch_cfg<1, 1, 1, 4, INT8>(p, L, plan, s);
-        else launch_cfg<1, 1, 2, 4, INT8>(p, L, plan, s);
+        if (plan.gemv_cfg == 0) launch_cfg<1, 1, 1, INT8>(p, L, plan, s);
+        else launch_cfg<1, 1, 2, INT8>(p, L, plan, s);
     } else if (L.bits == 2) {
-        if (plan.gemv_cfg == 0) launch_cfg<2, 1, 1, 2, INT8>(p, L, plan, s);
-        else if (plan.gemv_cfg == 1) launch_cfg<2, 2, 1, 4, INT8>(p, L, plan, s);
-        else launch_cfg<2, 2, 2, 4, INT8>(p, L, plan, s);
+        if (plan.gemv_cfg == 0) launch_cfg<2, 1, 1, INT8>(p, L, plan, s);
+        else if (plan.gemv_cfg == 1) launch_cfg<2, 2, 1, INT8>(p, L, plan, s);
+        else launch_cfg<2, 2, 2, INT8>(p, L, plan, s);
     } else {
         if constexpr (!INT8) {
-            if (plan.gemv_cfg == 0) launch_cfg<4, 2, 1, 2, false>(p, L, plan, s);
-            else launch_cfg<4, 4, 1, 4, false>(p, L, plan, s);
+            if (plan.gemv_cfg == 0) launch_cfg<4, 1, 1, false>(p, L, plan, s);
+            else if (plan.gemv_cfg == 1) launch_cfg<4, 2, 1, false>(p, L, plan, s);
+            else launch_cfg<4, 4, 1, false>(p, L, plan, s);
         }
     }
     return (int)hipGetLastError();

@@ -175,9 +175,9 @@ template <int BITS, bool INT8>
 static void launch_gemm_mt(const LutParams &p, const Layout &L, const LutPlan &plan, hipStream_t s) {
     dim3 grid((unsigned)plan.n_tiles, (unsigned)plan.splits, (unsigned)plan.m_tiles);
     const int pt = L.per_tensor ? 1 : 0;
-    if (plan.mt == 4)
+    if (plan.mt == 4 || BITS == 4)  // the planner uses 4 tokens per workgroup for 4-bit weights
         hipLaunchKernelGGL((lut_gemm_kernel<BITS, 4, INT8>), grid, dim3(256), 0, s, p, L.wfmt, pt);
-    else
+    else if constexpr (BITS != 4)
         hipLaunchKernelGGL((lut_gemm_kernel<BITS, 8, INT8>), grid, dim3(256), 0, s, p, L.wfmt, pt);
 }
 

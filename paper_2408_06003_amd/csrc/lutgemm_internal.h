@@ -73,7 +73,6 @@ inline TableLayout make_table_layout(const Layout &L, int64_t M) {
 struct LutPlan {
     int kind;        // 0: single-token whole-K GEMV, 1: multi-token kernel, 2: single-token split-K GEMV
     int gemv_cfg;    // single-token kernel: lane decomposition (see lut_gemv.hip)
-    int gemv_nw;     // single-token kernel: wavefronts per workgroup (4, 8 or 16)
     int kbs;         // 128-blocks of K per split
     int splits;      // K splits (1 = no workspace)
     int mt;          // tokens per workgroup (multi-token kernel)
