@@ -75,8 +75,8 @@ namespace lutgemm {
 // lut_gemv.hip; pick the widest lane decomposition (most columns per workgroup,
 // i.e. most table reuse) that still gives at least `target` workgroups, and
 // split K across workgroups only when even the narrowest one does not.
-// Several tokens: MT tokens per workgroup of 256 columns, K split only when the
-// token x column grid is smaller than `target`.
+// Several tokens: 8 tokens per workgroup of 256 columns, K split only when the
+// token x column grid is smaller than 4 x `target`.
 LutPlan plan_lut(const Layout &L, int64_t M) {
     LutPlan P{};
     const int64_t target = env_int("LUTGEMM_TARGET_BLOCKS", 256);
@@ -134,7 +134,7 @@ LutPlan plan_lut(const Layout &L, int64_t M) {
         P.splits = (int)((L.KB + kbs - 1) / kbs);
     } else {
         P.kind = 1;
-        P.mt = (M <= 4 || L.bits == 4) ? 4 : 8;
+        P.mt = 8;  // tokens per workgroup of the multi-token kernel (lut_mtok.hip)
         P.m_tiles = (M + P.mt - 1) / P.mt;
         P.n_tiles = L.N_pad / NTILE;
         const int64_t base = P.n_tiles * P.m_tiles;

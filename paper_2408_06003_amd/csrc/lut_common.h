@@ -49,9 +49,6 @@ __device__ __forceinline__ uint32_t idx4(uint32_t w) {
     return r;
 }
 
-__device__ __forceinline__ int lds_i32(const char *base, uint32_t off) {
-    return *(const int *)(base + off);
-}
 
 // Signed 16-entry tables staged in LDS (entry s i = (s ? -1 : 1) T[i], Eq. 4-5)
 // for the 32 four-activation groups of a 128-block: INT16 entries on the INT8 path
@@ -160,28 +157,6 @@ __device__ __forceinline__ void store_quarter(char *F, int blk, int g, int qr, u
         *(int4 *)dst = make_int4((int)rintf(h2f(h.x & 0xFFFFu) * f), (int)rintf(h2f(h.x >> 16) * f),
                                  (int)rintf(h2f(h.y & 0xFFFFu) * f), (int)rintf(h2f(h.y >> 16) * f));
     }
-}
-
-// Expand one half table (8 entries, 16 bytes) into a 16-entry INT32 signed table.
-template <bool INT8>
-__device__ __forceinline__ void expand_table(const uint4 h, int *dst) {
-    const uint32_t w[4] = {h.x, h.y, h.z, h.w};
-    int v[8];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        if (INT8) {
-            v[2 * i] = (int)(int16_t)(uint16_t)(w[i] & 0xFFFFu);
-            v[2 * i + 1] = (int)(int16_t)(uint16_t)(w[i] >> 16);
-        } else {
-            v[2 * i] = (int)rintf(h2f(w[i] & 0xFFFFu) * (float)(1 << FIX_SHIFT));
-            v[2 * i + 1] = (int)rintf(h2f(w[i] >> 16) * (float)(1 << FIX_SHIFT));
-        }
-    }
-    int4 *d4 = (int4 *)dst;
-    d4[0] = make_int4(v[0], v[1], v[2], v[3]);
-    d4[1] = make_int4(v[4], v[5], v[6], v[7]);
-    d4[2] = make_int4(-v[0], -v[1], -v[2], -v[3]);
-    d4[3] = make_int4(-v[4], -v[5], -v[6], -v[7]);
 }
 
 // Reinterpreted scale and zero (Eq. 2) of quantization group q, column n.

@@ -1,0 +1,265 @@
+// Multi-token bit-serial LUT mpGEMM with token-interleaved tables (LUT Tensor
+// Core, Section 3.1 with Eq. 3, 5-6; the elongated M dimension of the LUT tile
+// of Section 3.2.2, where one index selects an entry from the tables of several
+// tokens at once).
+//
+// gfx950 mapping.  A workgroup of 256 lanes owns 256 columns (one per lane) and
+// 8 tokens.  For each 4-activation group the signed 16-entry tables of the 8
+// tokens are stored interleaved in LDS, entry i of tokens 0..7 in one 16-byte
+// row, as 16-bit values: the exact INT16 entries on the INT8 path, the FP16
+// entries of the precompute on the FP path.  One lookup is then one SDWA byte
+// extract (the Eq. 6 index times 16) and one ds_read_b128 that returns the 8
+// tokens' entries: 2 LDS bytes per lookup instead of 4.  INT8 path: the entries
+// of one 128-block and bit-plane are summed in packed INT16 pairs (|sum| <= 32 x
+// 508 < 2^15, exact), then widened to INT32 with the plane weight 2^t.  FP path:
+// each entry is added into an FP32 accumulator per token, scaled by 2^t (exact).
+//
+// K is walked in chunks of CH 128-blocks.  Everything a chunk needs from memory
+// (the 8 tokens' half-table words it stages, the weight words, the blocks'
+// metadata and zero-point sums) is loaded one chunk ahead into one of two
+// register buffers (used alternately, no copies, every load unconditional with
+// clamped indices so that waits count exactly), and the LDS tables are
+// double-buffered, so each chunk costs one barrier.  When the grid would not
+// fill the GPU, K is split and lut_finalize_kernel sums the partials.
+#include "lut_common.h"
+
+namespace lutgemm {
+
+constexpr int MTK = 8;  // tokens per workgroup
+
+// The 16-bit lanes of x selected by SEL (v_perm_b32 byte selector) from {hi, lo}.
+__device__ __forceinline__ uint32_t perm(uint32_t hi, uint32_t lo, uint32_t sel) {
+    return __builtin_amdgcn_perm(hi, lo, sel);
+}
+
+template <bool INT8>
+__device__ __forceinline__ uint32_t neg16x2(uint32_t x) {
+    if constexpr (INT8) return neg_i16x2(x);
+    return x ^ 0x80008000u;  // FP16: flip both sign bits (exact)
+}
+
+// af[t] += sc * (FP16 entry of token t in e), t = 0..7: eight v_fma_mix_f32 in one
+// statement, so each LDS read is consumed as a whole (the compiler would otherwise
+// regroup the accumulations by token and keep every read of a block live).
+__device__ __forceinline__ void fma_mix8(float (&af)[MTK], uint4 e, float sc) {
+    asm("v_fma_mix_f32 %0, %8, %12, %0 op_sel_hi:[1,0,0]\n\t"
+        "v_fma_mix_f32 %1, %8, %12, %1 op_sel:[1,0,0] op_sel_hi:[1,0,0]\n\t"
+        "v_fma_mix_f32 %2, %9, %12, %2 op_sel_hi:[1,0,0]\n\t"
+        "v_fma_mix_f32 %3, %9, %12, %3 op_sel:[1,0,0] op_sel_hi:[1,0,0]\n\t"
+        "v_fma_mix_f32 %4, %10, %12, %4 op_sel_hi:[1,0,0]\n\t"
+        "v_fma_mix_f32 %5, %10, %12, %5 op_sel:[1,0,0] op_sel_hi:[1,0,0]\n\t"
+        "v_fma_mix_f32 %6, %11, %12, %6 op_sel_hi:[1,0,0]\n\t"
+        "v_fma_mix_f32 %7, %11, %12, %7 op_sel:[1,0,0] op_sel_hi:[1,0,0]"
+        : "+v"(af[0]), "+v"(af[1]), "+v"(af[2]), "+v"(af[3]), "+v"(af[4]), "+v"(af[5]), "+v"(af[6]), "+v"(af[7])
+        : "v"(e.x), "v"(e.y), "v"(e.z), "v"(e.w), "v"(sc));
+}
+
+template <int BITS, bool INT8>
+__global__ __launch_bounds__(256) void lut_mtok_kernel(LutParams p, int wfmt) {
+    constexpr int CH = 4 / BITS;                  // 128-blocks per chunk
+    constexpr int TASKS = CH * GPB * 4;           // staging tasks per chunk: (block, group, index pair)
+    constexpr int TPL = (TASKS + 255) / 256;      // staging tasks per lane
+    constexpr int BUF = CH * GPB * 256;           // LDS bytes of one table buffer (16 entries x 8 tokens x 2 B per group)
+    __shared__ __attribute__((aligned(16))) char F[2 * BUF];
+    __shared__ float Ssh[2][CH][MTK];             // FP path: activation sum of each block's group (first block only)
+
+    const int tid = threadIdx.x;
+    const int64_t n = (int64_t)blockIdx.x * NTILE + tid;
+    const int split = blockIdx.y;
+    const int64_t m0 = (int64_t)blockIdx.z * MTK;
+    const int64_t kbA = (int64_t)split * p.kbs;
+    const int64_t kbB = (kbA + p.kbs < p.KB) ? kbA + p.kbs : p.KB;
+    const bool need_s = !INT8 && wfmt != LUTGEMM_WFMT_BINARY;
+
+    typedef uint32_t SD[TPL][MTK];
+    typedef uint4 WW[CH][BITS];
+    typedef uint2 MW[CH];
+    typedef float SV[1];
+    auto load = [&](int64_t kc, SD &sd, WW &w, MW &mw, SV &sv) {
+        const int nkb = (int)((kbB - kc) < CH ? (kbB - kc) : CH);
+#pragma unroll
+        for (int r = 0; r < TPL; ++r) {
+            const int task = tid + 256 * r;
+            const int tk = task < TASKS ? task : TASKS - 1;
+            const int kbl = tk >> 7, g = (tk >> 2) & 31, ip = tk & 3;
+            const int kbc = kbl < nkb ? kbl : nkb - 1;
+#pragma unroll
+            for (int t = 0; t < MTK; ++t) {
+                const int64_t row = (m0 + t < p.M) ? m0 + t : p.M - 1;
+                sd[r][t] = ((const uint32_t *)(p.T + row * p.J + (kc + kbc) * GPB + g))[ip];
+            }
+        }
+#pragma unroll
+        for (int kbl = 0; kbl < CH; ++kbl) {
+            const int kbc = kbl < nkb ? kbl : nkb - 1;
+#pragma unroll
+            for (int t = 0; t < BITS; ++t) w[kbl][t] = p.planes[((kc + kbc) * BITS + t) * p.N_pad + n];
+        }
+        if constexpr (!INT8) {
+#pragma unroll
+            for (int kbl = 0; kbl < CH; ++kbl) {
+                const int kbc = kbl < nkb ? kbl : nkb - 1;
+                const int q = (int)(((float)(kc + kbc) + 0.5f) * p.inv_kpg);
+                mw[kbl] = load_meta_words(p, q, lane_value(n));
+            }
+            // one activation sum per (block, token): lanes 0 .. 8 CH - 1
+            const int kbl = (tid >> 3) < CH ? (tid >> 3) : CH - 1, t = tid & 7;
+            const int kbc = kbl < nkb ? kbl : nkb - 1;
+            const int q = (int)(((float)(kc + kbc) + 0.5f) * p.inv_kpg);
+            const int64_t row = (m0 + t < p.M) ? m0 + t : p.M - 1;
+            sv[0] = ((const float *)p.S)[lane_value(row * p.Q + q)];
+        }
+    };
+
+    float yf[MTK];
+    int yi[MTK];
+#pragma unroll
+    for (int t = 0; t < MTK; ++t) {
+        yf[t] = 0.f;
+        yi[t] = 0;
+    }
+
+    auto process = [&](int64_t kc, const SD &sd, const WW &w, const MW &mw, const SV &sv, int b) {
+        const int nkb = (int)((kbB - kc) < CH ? (kbB - kc) : CH);
+        char *Fb = F + b * BUF;
+        // stage: for each task, entries 2ip, 2ip + 1 and their negations for the 8 tokens
+#pragma unroll
+        for (int r = 0; r < TPL; ++r) {
+            const int task = tid + 256 * r;
+            const int kbl = task >> 7, g = (task >> 2) & 31, ip = task & 3;
+            if (task < TASKS && kbl < nkb) {
+                uint32_t v[MTK];
+#pragma unroll
+                for (int t = 0; t < MTK; ++t) v[t] = (m0 + t < p.M) ? sd[r][t] : 0u;
+                uint4 e0, e1;  // entries 2ip (low halves) and 2ip + 1 (high halves), tokens 0..7
+                e0.x = perm(v[1], v[0], 0x05040100u);
+                e0.y = perm(v[3], v[2], 0x05040100u);
+                e0.z = perm(v[5], v[4], 0x05040100u);
+                e0.w = perm(v[7], v[6], 0x05040100u);
+                e1.x = perm(v[1], v[0], 0x07060302u);
+                e1.y = perm(v[3], v[2], 0x07060302u);
+                e1.z = perm(v[5], v[4], 0x07060302u);
+                e1.w = perm(v[7], v[6], 0x07060302u);
+                char *row = Fb + (kbl * GPB + g) * 256;
+                *(uint4 *)(row + (2 * ip) * 16) = e0;
+                *(uint4 *)(row + (2 * ip + 1) * 16) = e1;
+                *(uint4 *)(row + (2 * ip + 8) * 16) =
+                    make_uint4(neg16x2<INT8>(e0.x), neg16x2<INT8>(e0.y), neg16x2<INT8>(e0.z), neg16x2<INT8>(e0.w));
+                *(uint4 *)(row + (2 * ip + 9) * 16) =
+                    make_uint4(neg16x2<INT8>(e1.x), neg16x2<INT8>(e1.y), neg16x2<INT8>(e1.z), neg16x2<INT8>(e1.w));
+            }
+        }
+        if (need_s && tid < CH * MTK) {
+            const int kbl = tid >> 3, kb = (int)(kc + kbl);
+            const int q = (int)(((float)kb + 0.5f) * p.inv_kpg);
+            Ssh[b][kbl][tid & 7] = (kbl < nkb && kb == q * p.kpg) ? sv[0] : 0.f;
+        }
+        lds_barrier();
+#pragma unroll
+        for (int kbl = 0; kbl < CH; ++kbl) {
+            if (kbl < nkb) {
+                int ai[MTK];
+                float af[MTK];
+#pragma unroll
+                for (int t = 0; t < MTK; ++t) {
+                    ai[t] = 0;
+                    af[t] = 0.f;
+                }
+#pragma unroll
+                for (int pl = 0; pl < BITS; ++pl) {
+                    short2_v a16[4] = {short2_v{0, 0}, short2_v{0, 0}, short2_v{0, 0}, short2_v{0, 0}};
+                    const uint32_t wd[4] = {w[kbl][pl].x, w[kbl][pl].y, w[kbl][pl].z, w[kbl][pl].w};
+#pragma unroll
+                    for (int d = 0; d < 4; ++d) {
+                        const uint32_t lo = (wd[d] << 4) & 0xF0F0F0F0u, hi = wd[d] & 0xF0F0F0F0u;
+#pragma unroll
+                        for (int k = 0; k < 8; ++k) {
+                            const uint32_t src = (k & 1) ? hi : lo;
+                            const uint32_t off = (src >> (8 * (k >> 1))) & 0xFFu;
+                            const int g = d * 8 + k;  // groups 2j (low nibble) and 2j + 1 (high nibble) of byte j
+                            const uint4 e = *(const uint4 *)(Fb + (kbl * GPB + g) * 256 + off);
+                            if constexpr (INT8) {
+                                a16[0] += __builtin_bit_cast(short2_v, e.x);
+                                a16[1] += __builtin_bit_cast(short2_v, e.y);
+                                a16[2] += __builtin_bit_cast(short2_v, e.z);
+                                a16[3] += __builtin_bit_cast(short2_v, e.w);
+                            } else {
+                                fma_mix8(af, e, (float)(1 << pl));  // af += 2^pl * entry (exact scaling)
+                            }
+                        }
+                    }
+                    if constexpr (INT8) {
+#pragma unroll
+                        for (int j = 0; j < 4; ++j) {
+                            ai[2 * j] += (int)a16[j].x << pl;
+                            ai[2 * j + 1] += (int)a16[j].y << pl;
+                        }
+                    }
+                }
+                if constexpr (INT8) {
+#pragma unroll
+                    for (int t = 0; t < MTK; ++t) yi[t] += ai[t];
+                } else {
+                    const SZ sz = decode_sz(p, mw[kbl]);
+#pragma unroll
+                    for (int t = 0; t < MTK; ++t) {
+                        yf[t] = fmaf(sz.sp, af[t], yf[t]);
+                        if (need_s) yf[t] -= (sz.sp * sz.zp) * Ssh[b][kbl][t];
+                    }
+                }
+            }
+        }
+    };
+
+    // INT8 ternary: the activation sums S[m][0], added once (first K split)
+    if (INT8 && split == 0 && wfmt == LUTGEMM_WFMT_TERNARY) {
+#pragma unroll
+        for (int t = 0; t < MTK; ++t) {
+            const int64_t row = (m0 + t < p.M) ? m0 + t : p.M - 1;
+            yi[t] = ((const int *)p.S)[lane_value(row * p.Q)];
+        }
+    }
+    const int64_t last = kbA + (kbB - 1 - kbA) / CH * CH;
+    SD sdA, sdB;
+    WW wA, wB;
+    MW mwA, mwB;
+    SV svA, svB;
+    load(kbA, sdA, wA, mwA, svA);
+    for (int64_t kc = kbA; kc < kbB; kc += 2 * CH) {
+        load(kc + CH < last ? kc + CH : last, sdB, wB, mwB, svB);
+        process(kc, sdA, wA, mwA, svA, 0);
+        if (kc + CH >= kbB) break;
+        load(kc + 2 * CH < last ? kc + 2 * CH : last, sdA, wA, mwA, svA);
+        process(kc + CH, sdB, wB, mwB, svB, 1);
+    }
+
+    const int rows = (int)((p.M - m0) < MTK ? (p.M - m0) : MTK);
+    if (p.splits == 1) {
+#pragma unroll
+        for (int t = 0; t < MTK; ++t)
+            if (t < rows) store_out<INT8>(p, wfmt, m0 + t, n, yf[t], yi[t], load_epi<INT8>(p, wfmt, m0 + t, n, false));
+        return;
+    }
+    const int64_t m_alloc = (int64_t)gridDim.z * MTK;
+#pragma unroll
+    for (int t = 0; t < MTK; ++t)
+        p.part[((int64_t)split * m_alloc + m0 + t) * p.N_pad + n] = INT8 ? __int_as_float(yi[t]) : yf[t];
+}
+
+int launch_mtok(const LutParams &p, const Layout &L, const LutPlan &plan, void *stream) {
+    hipStream_t s = (hipStream_t)stream;
+    const dim3 grid((unsigned)plan.n_tiles, (unsigned)plan.splits, (unsigned)plan.m_tiles);
+    const bool i8 = L.act == LUTGEMM_ACT_INT8;
+    if (L.bits == 1) {
+        if (i8) hipLaunchKernelGGL((lut_mtok_kernel<1, true>), grid, dim3(256), 0, s, p, L.wfmt);
+        else hipLaunchKernelGGL((lut_mtok_kernel<1, false>), grid, dim3(256), 0, s, p, L.wfmt);
+    } else if (L.bits == 2) {
+        if (i8) hipLaunchKernelGGL((lut_mtok_kernel<2, true>), grid, dim3(256), 0, s, p, L.wfmt);
+        else hipLaunchKernelGGL((lut_mtok_kernel<2, false>), grid, dim3(256), 0, s, p, L.wfmt);
+    } else {
+        hipLaunchKernelGGL((lut_mtok_kernel<4, false>), grid, dim3(256), 0, s, p, L.wfmt);
+    }
+    return (int)hipGetLastError();
+}
+
+}  // namespace lutgemm

@@ -137,6 +137,7 @@ int launch_lut(const LutParams &p, const Layout &L, const LutPlan &plan, void *s
 int launch_gemv(const LutParams &p, const Layout &L, const LutPlan &plan, void *stream);
 int launch_fused_gemv(const LutParams &p, const Layout &L, const LutPlan &plan, void *stream);
 int launch_finalize(const LutParams &p, const Layout &L, const LutPlan &plan, void *stream);
+int launch_mtok(const LutParams &p, const Layout &L, const LutPlan &plan, void *stream);
 int launch_dequant(const DequantParams &p, const Layout &L, void *stream);
 
 }  // namespace lutgemm
