@@ -138,13 +138,18 @@ LutPlan plan_lut(const Layout &L, int64_t M) {
         P.m_tiles = (M + P.mt - 1) / P.mt;
         P.n_tiles = L.N_pad / NTILE;
         const int64_t base = P.n_tiles * P.m_tiles;
+        const int64_t ch = L.bits == 1 ? 2 : 4 / L.bits;  // 128-blocks per chunk of the kernel
+        const int64_t mt_target = env_int("LUTGEMM_MT_TARGET", 4) * target;
         int64_t splits = 1;
-        if (base < 4 * target) splits = (4 * target + base - 1) / base;
-        const int64_t max_splits = (L.KB + 1) / 2;  // at least two 128-blocks per split
+        if (base < mt_target) splits = (mt_target + base - 1) / base;
+        const int64_t max_splits = (L.KB + ch - 1) / ch;  // at least one chunk per split
         if (splits > max_splits) splits = max_splits;
+        const int fs = env_int("LUTGEMM_MT_SPLITS", 0);
+        if (fs > 0) splits = fs;
         if (splits < 1) splits = 1;
         int64_t kbs = (L.KB + splits - 1) / splits;
-        kbs = (kbs + 1) / 2 * 2;
+        kbs = (kbs + ch - 1) / ch * ch;
+        if (kbs > L.KB) kbs = L.KB;
         P.kbs = (int)kbs;
         P.splits = (int)((L.KB + kbs - 1) / kbs);
     }

@@ -56,7 +56,7 @@ __device__ __forceinline__ void fma_mix8(float (&af)[MTK], uint4 e, float sc) {
 
 template <int BITS, bool INT8>
 __global__ __launch_bounds__(256) void lut_mtok_kernel(LutParams p, int wfmt) {
-    constexpr int CH = 4 / BITS;                  // 128-blocks per chunk
+    constexpr int CH = BITS == 1 ? 2 : 4 / BITS;  // 128-blocks per chunk (more workgroups per CU at b = 1)
     constexpr int TASKS = CH * GPB * 4;           // staging tasks per chunk: (block, group, index pair)
     constexpr int TPL = (TASKS + 255) / 256;      // staging tasks per lane
     constexpr int BUF = CH * GPB * 256;           // LDS bytes of one table buffer (16 entries x 8 tokens x 2 B per group)
