@@ -352,7 +352,13 @@ template <int BITS, int PW, int SW, bool INT8>
 static void launch_fused_cfg(const LutParams &p, const Layout &L, const LutPlan &plan, hipStream_t s) {
     constexpr int CW = 64 / (PW * SW);
     const dim3 grid((unsigned)((L.N + CW - 1) / CW), (unsigned)plan.splits, (unsigned)p.M);
-    hipLaunchKernelGGL((lut_fused_gemv_kernel<BITS, PW, SW, 1, 16, INT8>), grid, dim3(1024), 0, s, p, L.wfmt);
+    // 4 or 8 wavefronts when the whole K range fits one chunk of that many
+    if (L.KB <= 4 * SW)
+        hipLaunchKernelGGL((lut_fused_gemv_kernel<BITS, PW, SW, 1, 4, INT8>), grid, dim3(256), 0, s, p, L.wfmt);
+    else if (L.KB <= 8 * SW)
+        hipLaunchKernelGGL((lut_fused_gemv_kernel<BITS, PW, SW, 1, 8, INT8>), grid, dim3(512), 0, s, p, L.wfmt);
+    else
+        hipLaunchKernelGGL((lut_fused_gemv_kernel<BITS, PW, SW, 1, 16, INT8>), grid, dim3(1024), 0, s, p, L.wfmt);
 }
 
 template <bool INT8>

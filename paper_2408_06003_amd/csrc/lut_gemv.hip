@@ -274,12 +274,19 @@ static void launch_split(const LutParams &p, const Layout &L, const LutPlan &pla
     }
 }
 
-// 16 wavefronts per workgroup, one 128-block per K slice and chunk.
+// 16 wavefronts per workgroup, one 128-block per K slice and chunk; 4 or 8 when
+// the whole K range fits one chunk of that many (short K: no idle wavefronts and a
+// shorter cross-wavefront reduction).
 template <int BITS, int PW, int SW, bool INT8>
 static void launch_cfg(const LutParams &p, const Layout &L, const LutPlan &plan, hipStream_t s) {
     constexpr int CW = 64 / (PW * SW);
     const dim3 grid((unsigned)((L.N + CW - 1) / CW), (unsigned)plan.splits, (unsigned)p.M);
-    hipLaunchKernelGGL((lut_gemv2_kernel<BITS, PW, SW, 1, 16, INT8>), grid, dim3(1024), 0, s, p, L.wfmt);
+    if (L.KB <= 4 * SW)
+        hipLaunchKernelGGL((lut_gemv2_kernel<BITS, PW, SW, 1, 4, INT8>), grid, dim3(256), 0, s, p, L.wfmt);
+    else if (L.KB <= 8 * SW)
+        hipLaunchKernelGGL((lut_gemv2_kernel<BITS, PW, SW, 1, 8, INT8>), grid, dim3(512), 0, s, p, L.wfmt);
+    else
+        hipLaunchKernelGGL((lut_gemv2_kernel<BITS, PW, SW, 1, 16, INT8>), grid, dim3(1024), 0, s, p, L.wfmt);
 }
 
 // Lane decompositions (PW, SW) offered per bit width, indexed by LutPlan::gemv_cfg
