@@ -109,7 +109,8 @@ const char *lutgemm_last_error(void);
  * LUTGEMM_ERROR_NOT_SUPPORTED for: K % 128 != 0; group_size not 0 and not a
  * multiple of 128 dividing K; w_bits not allowed for wfmt; scale_fp32 with
  * group_size != 0 or with UINT; ACT_INT8 with UINT weights or with a group
- * smaller than K.
+ * smaller than K; K > 2^20, N > 2^24 or M > 2^19; M > 2 with
+ * ceil(M/8) * ceil(N/256) >= 2^24.
  */
 lutgemm_status_t lutgemm_validate(const lutgemm_problem_t *problem, int64_t M);
 

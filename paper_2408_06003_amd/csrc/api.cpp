@@ -17,6 +17,7 @@ namespace {
 constexpr int64_t MAX_M = int64_t(1) << 19;
 constexpr int64_t MAX_K = int64_t(1) << 20;
 constexpr int64_t MAX_N = int64_t(1) << 24;
+constexpr int64_t MAX_TILES = int64_t(1) << 24;
 
 bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
 
@@ -28,6 +29,9 @@ lutgemm_status_t check_problem(const lutgemm_problem_t *p, int64_t M) {
     if (p->scale_fp32 != 0 && p->scale_fp32 != 1) return LUTGEMM_ERROR_INVALID_VALUE;
     if (p->w_bits <= 0 || p->group_size < 0) return LUTGEMM_ERROR_INVALID_VALUE;
     if (p->K > MAX_K || p->N > MAX_N || M > MAX_M) return LUTGEMM_ERROR_NOT_SUPPORTED;
+    // the multi-token kernel runs one workgroup per (8 tokens, 256 columns) tile in a
+    // one-dimensional grid of at most 2^24 workgroups
+    if (M > 2 && ((M + 7) / 8) * ((p->N + 255) / 256) >= MAX_TILES) return LUTGEMM_ERROR_NOT_SUPPORTED;
     if (p->K % KBLK != 0) return LUTGEMM_ERROR_NOT_SUPPORTED;
     if (p->group_size != 0 && (p->group_size % KBLK != 0 || p->K % p->group_size != 0))
         return LUTGEMM_ERROR_NOT_SUPPORTED;
@@ -146,12 +150,18 @@ LutPlan plan_lut(const Layout &L, int64_t M) {
         if (splits > max_splits) splits = max_splits;
         const int fs = env_int("LUTGEMM_MT_SPLITS", 0);
         if (fs > 0) splits = fs;
+        if (splits * base >= MAX_TILES) splits = (MAX_TILES - 1) / base;
         if (splits < 1) splits = 1;
         int64_t kbs = (L.KB + splits - 1) / splits;
         kbs = (kbs + ch - 1) / ch * ch;
         if (kbs > L.KB) kbs = L.KB;
         P.kbs = (int)kbs;
         P.splits = (int)((L.KB + kbs - 1) / kbs);
+        // workgroup order: columns fastest.  The XCD-aware orders of the kernel measured
+        // no faster at M >= 256 (the kernel is bound by LDS and VALU, not L2) and 12 %
+        // slower at M = 16; kept for experiments (LUTGEMM_MT_ORDER)
+        P.order = env_int("LUTGEMM_MT_ORDER", 0);
+        if (P.order < 0) P.order = 0;
     }
     const int64_t rows = P.kind == 1 ? P.m_tiles * P.mt : M;
     P.ws_bytes = P.splits > 1 ? align256((size_t)P.splits * rows * L.N_pad * 4) : 0;

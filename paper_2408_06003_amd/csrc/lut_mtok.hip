@@ -12,7 +12,11 @@
 // tokens' entries: 2 LDS bytes per lookup instead of 4.  INT8 path: the entries
 // of one 128-block and bit-plane are summed in packed INT16 pairs (|sum| <= 32 x
 // 508 < 2^15, exact), then widened to INT32 with the plane weight 2^t.  FP path:
-// each entry is added into an FP32 accumulator per token, scaled by 2^t (exact).
+// the 8 entries selected by one weight word (8 consecutive groups of one plane)
+// are summed in packed FP16 pairs (v_pk_add_f16, two tokens per instruction; the
+// tables are normalized to |T| < 4, so these sums stay below 32), and each such
+// sum is added into an FP32 accumulator per token scaled by 2^t (exact), with one
+// v_fma_mix_f32 per token.
 //
 // K is walked in chunks of CH 128-blocks.  Everything a chunk needs from memory
 // (the 8 tokens' half-table words it stages, the weight words, the blocks'
@@ -38,6 +42,17 @@ __device__ __forceinline__ uint32_t neg16x2(uint32_t x) {
     return x ^ 0x80008000u;  // FP16: flip both sign bits (exact)
 }
 
+// h += e as four packed FP16 pairs (8 tokens), one statement per read for the same
+// reason as fma_mix8 below.
+__device__ __forceinline__ void pk_add4(uint4 &h, uint4 e) {
+    asm("v_pk_add_f16 %0, %0, %4\n\t"
+        "v_pk_add_f16 %1, %1, %5\n\t"
+        "v_pk_add_f16 %2, %2, %6\n\t"
+        "v_pk_add_f16 %3, %3, %7"
+        : "+v"(h.x), "+v"(h.y), "+v"(h.z), "+v"(h.w)
+        : "v"(e.x), "v"(e.y), "v"(e.z), "v"(e.w));
+}
+
 // af[t] += sc * (FP16 entry of token t in e), t = 0..7: eight v_fma_mix_f32 in one
 // statement, so each LDS read is consumed as a whole (the compiler would otherwise
 // regroup the accumulations by token and keep every read of a block live).
@@ -54,8 +69,48 @@ __device__ __forceinline__ void fma_mix8(float (&af)[MTK], uint4 e, float sc) {
         : "v"(e.x), "v"(e.y), "v"(e.z), "v"(e.w), "v"(sc));
 }
 
+// Tile of a workgroup from its linear index.  Workgroups are dealt round-robin to the
+// 8 XCDs, each with its own L2; with order != 0 the linear index is first turned into
+// a position in the dealing XCD's own contiguous share of the tile space, so that the
+// workgroups one XCD runs at the same time share weight tiles (same columns) and
+// table tiles (same tokens) in that XCD's L2.  Splits of K vary slowest.
+struct Tile {
+    int64_t nt, mt;
+    int split;
+};
+// (all counts below 2^24: 32-bit arithmetic)
+__device__ __forceinline__ Tile tile_of(uint32_t b, uint32_t n_tiles, uint32_t m_tiles, int order) {
+    const uint32_t per_split = n_tiles * m_tiles;
+    const uint32_t total = gridDim.x;  // per_split x splits
+    if (order != 0) {
+        const uint32_t q = total >> 3, r = total & 7, x = b & 7, i = b >> 3;
+        b = x * q + (x < r ? x : r) + i;
+    }
+    Tile t;
+    t.split = (int)(b / per_split);
+    const uint32_t w = b - (uint32_t)t.split * per_split;
+    if (order == 0) {
+        t.nt = w % n_tiles;
+        t.mt = w / n_tiles;
+    } else if (order == 1) {
+        t.mt = w % m_tiles;
+        t.nt = w / m_tiles;
+    } else {
+        // bands of `order` token tiles; inside a band tokens vary fastest, then columns
+        const uint32_t o = (uint32_t)order;
+        const uint32_t band = w / (o * n_tiles);
+        const uint32_t first = band * o;
+        const uint32_t rows = (m_tiles - first) < o ? (m_tiles - first) : o;
+        const uint32_t v = w - band * o * n_tiles;
+        t.mt = first + v % rows;
+        t.nt = v / rows;
+    }
+    return t;
+}
+
 template <int BITS, bool INT8>
-__global__ __launch_bounds__(256) void lut_mtok_kernel(LutParams p, int wfmt) {
+__global__ __launch_bounds__(256) void lut_mtok_kernel(LutParams p, int wfmt, int64_t n_tiles, int64_t m_tiles,
+                                                       int order) {
     constexpr int CH = BITS == 1 ? 2 : 4 / BITS;  // 128-blocks per chunk (more workgroups per CU at b = 1)
     constexpr int TASKS = CH * GPB * 4;           // staging tasks per chunk: (block, group, index pair)
     constexpr int TPL = (TASKS + 255) / 256;      // staging tasks per lane
@@ -64,9 +119,10 @@ __global__ __launch_bounds__(256) void lut_mtok_kernel(LutParams p, int wfmt) {
     __shared__ float Ssh[2][CH][MTK];             // FP path: activation sum of each block's group (first block only)
 
     const int tid = threadIdx.x;
-    const int64_t n = (int64_t)blockIdx.x * NTILE + tid;
-    const int split = blockIdx.y;
-    const int64_t m0 = (int64_t)blockIdx.z * MTK;
+    const Tile tl = tile_of(blockIdx.x, (uint32_t)n_tiles, (uint32_t)m_tiles, order);
+    const int64_t n = tl.nt * NTILE + tid;
+    const int split = tl.split;
+    const int64_t m0 = tl.mt * MTK;
     const int64_t kbA = (int64_t)split * p.kbs;
     const int64_t kbB = (kbA + p.kbs < p.KB) ? kbA + p.kbs : p.KB;
     const bool need_s = !INT8 && wfmt != LUTGEMM_WFMT_BINARY;
@@ -172,6 +228,7 @@ __global__ __launch_bounds__(256) void lut_mtok_kernel(LutParams p, int wfmt) {
 #pragma unroll
                     for (int d = 0; d < 4; ++d) {
                         const uint32_t lo = (wd[d] << 4) & 0xF0F0F0F0u, hi = wd[d] & 0xF0F0F0F0u;
+                        uint4 h;  // FP path: sum of this word's 8 entries per token, packed FP16
 #pragma unroll
                         for (int k = 0; k < 8; ++k) {
                             const uint32_t src = (k & 1) ? hi : lo;
@@ -183,10 +240,13 @@ __global__ __launch_bounds__(256) void lut_mtok_kernel(LutParams p, int wfmt) {
                                 a16[1] += __builtin_bit_cast(short2_v, e.y);
                                 a16[2] += __builtin_bit_cast(short2_v, e.z);
                                 a16[3] += __builtin_bit_cast(short2_v, e.w);
+                            } else if (k == 0) {
+                                h = e;
                             } else {
-                                fma_mix8(af, e, (float)(1 << pl));  // af += 2^pl * entry (exact scaling)
+                                pk_add4(h, e);
                             }
                         }
+                        if constexpr (!INT8) fma_mix8(af, h, (float)(1 << pl));  // af += 2^pl * h (exact scaling)
                     }
                     if constexpr (INT8) {
 #pragma unroll
@@ -240,7 +300,7 @@ __global__ __launch_bounds__(256) void lut_mtok_kernel(LutParams p, int wfmt) {
             if (t < rows) store_out<INT8>(p, wfmt, m0 + t, n, yf[t], yi[t], load_epi<INT8>(p, wfmt, m0 + t, n, false));
         return;
     }
-    const int64_t m_alloc = (int64_t)gridDim.z * MTK;
+    const int64_t m_alloc = m_tiles * MTK;
 #pragma unroll
     for (int t = 0; t < MTK; ++t)
         p.part[((int64_t)split * m_alloc + m0 + t) * p.N_pad + n] = INT8 ? __int_as_float(yi[t]) : yf[t];
@@ -248,16 +308,19 @@ __global__ __launch_bounds__(256) void lut_mtok_kernel(LutParams p, int wfmt) {
 
 int launch_mtok(const LutParams &p, const Layout &L, const LutPlan &plan, void *stream) {
     hipStream_t s = (hipStream_t)stream;
-    const dim3 grid((unsigned)plan.n_tiles, (unsigned)plan.splits, (unsigned)plan.m_tiles);
+    // one-dimensional grid (tile_of decodes it); the planner keeps it under 2^32 work-items
+    const dim3 grid((unsigned)(plan.n_tiles * plan.m_tiles * plan.splits), 1, 1);
     const bool i8 = L.act == LUTGEMM_ACT_INT8;
+    const int64_t nt = plan.n_tiles, mt = plan.m_tiles;
+    const int o = plan.order;
     if (L.bits == 1) {
-        if (i8) hipLaunchKernelGGL((lut_mtok_kernel<1, true>), grid, dim3(256), 0, s, p, L.wfmt);
-        else hipLaunchKernelGGL((lut_mtok_kernel<1, false>), grid, dim3(256), 0, s, p, L.wfmt);
+        if (i8) hipLaunchKernelGGL((lut_mtok_kernel<1, true>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
+        else hipLaunchKernelGGL((lut_mtok_kernel<1, false>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
     } else if (L.bits == 2) {
-        if (i8) hipLaunchKernelGGL((lut_mtok_kernel<2, true>), grid, dim3(256), 0, s, p, L.wfmt);
-        else hipLaunchKernelGGL((lut_mtok_kernel<2, false>), grid, dim3(256), 0, s, p, L.wfmt);
+        if (i8) hipLaunchKernelGGL((lut_mtok_kernel<2, true>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
+        else hipLaunchKernelGGL((lut_mtok_kernel<2, false>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
     } else {
-        hipLaunchKernelGGL((lut_mtok_kernel<4, false>), grid, dim3(256), 0, s, p, L.wfmt);
+        hipLaunchKernelGGL((lut_mtok_kernel<4, false>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
     }
     return (int)hipGetLastError();
 }

@@ -78,6 +78,8 @@ struct LutPlan {
     int mt;          // tokens per workgroup (multi-token kernel)
     int64_t m_tiles; // token tiles
     int64_t n_tiles; // column tiles
+    int order;       // multi-token kernel: workgroup order (0: columns fastest; 1: tokens fastest
+                     // per XCD; g >= 2: per XCD, bands of g token tiles, tokens fastest in a band)
     size_t ws_bytes;
 };
 

@@ -69,6 +69,7 @@ SMALL = [
     (5, 1, 2048, 1000),
     (5, 16, 2048, 600),
     (5, 37, 1024, 300),
+    (6, 45, 1024, 700),
 ]
 
 

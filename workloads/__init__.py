@@ -5,9 +5,10 @@ distributions. It holds none of the method's arithmetic (no dequantization, no
 tables, no reinterpretation), so both the CPU oracle and the HIP path can use it
 without sharing any computation.
 
-The five workload families are the synthetic stand-ins for the layer shapes the
+The workload families are the synthetic stand-ins for the layer shapes the
 paper evaluates on (LLaMA-2 7B/70B GEMV/GEMM shapes in the motivation figure of
-Section 2.3 and BitNet b1.58 ternary weights in Table 1).  No dataset or trained
+Section 2.3, BitNet b1.58 ternary weights in Table 1, and the LLaMA-2-13B shape of
+the kernel-level evaluation in Section 4.3).  No dataset or trained
 weight is used anywhere.
 
 Seeding: ``numpy.random.default_rng([2408, 6003, config_id, shape_id, M])``;
@@ -79,6 +80,11 @@ WORKLOADS: Dict[int, Workload] = {
                 ((8192, 28672), (28672, 8192)), (1, 16, 256),
                 "LLaMA-70B-shaped layers, binary {-1,+1} weights with per-channel FP16 scale "
                 "U(0.01,0.1), FP16 activations N(0,1), M in {1,16,256}"),
+    6: Workload(6, "binary_llama13b_kernel_eval", WFMT_BINARY, 1, None, False, 0.0, ACT_FP16,
+                ((5120, 27648),), (2048,),
+                "the LLaMA-2-13B mpGEMM shape of the paper's kernel-level evaluation (Section 4.3): "
+                "M=2048 N=27648 K=5120, binary {-1,+1} weights (W_INT1 A_FP16) with per-channel FP16 "
+                "scale U(0.01,0.1), FP16 activations N(0,1)"),
 }
 
 
