@@ -54,7 +54,12 @@ typedef enum {
 enum {
     LUTGEMM_WFMT_UINT = 0,    /* uint8 codes q in [0, 2^b), r = s (q - z); s, z FP16 per group   */
     LUTGEMM_WFMT_BINARY = 1,  /* uint8 codes q in {0,1} standing for {-1,+1}, r = s (2q - 1)        */
-    LUTGEMM_WFMT_TERNARY = 2  /* int8 codes w in {-1,0,+1}, stored as q = w + 1 with b = 2, r = s w  */
+    LUTGEMM_WFMT_TERNARY = 2, /* int8 codes w in {-1,0,+1}, stored as q = w + 1 with b = 2, r = s w  */
+    LUTGEMM_WFMT_TERNARY_3IN5 = 3 /* int8 codes w in {-1,0,+1}, r = s w, packed three weights per 5-bit
+                                     code (Section 5, non-integer weights): one table of the 27
+                                     patterns of 3 activations (half of it stored, by the symmetry
+                                     of Eq. 4) and one lookup per 3 weights; w_bits = 2, per-tensor
+                                     or per-channel scale (group_size 0 or K)                        */
 };
 
 /* Activation / table types. */
@@ -74,7 +79,7 @@ enum {
 /*
  * Problem description.
  *   K, N        reduction length and number of output columns (weight rows); K % 128 == 0, N >= 1
- *   w_bits      b: 1, 2 or 4 for UINT; 1 for BINARY; 2 for TERNARY
+ *   w_bits      b: 1, 2 or 4 for UINT; 1 for BINARY; 2 for TERNARY and TERNARY_3IN5
  *   wfmt        LUTGEMM_WFMT_*
  *   group_size  quantization group along K: a multiple of 128 that divides K (K = per channel),
  *               or 0 = a single scale (and zero) for the whole tensor
@@ -110,7 +115,8 @@ const char *lutgemm_last_error(void);
  * multiple of 128 dividing K; w_bits not allowed for wfmt; scale_fp32 with
  * group_size != 0 or with UINT; ACT_INT8 with UINT weights or with a group
  * smaller than K; K > 2^20, N > 2^24 or M > 2^19; M > 2 with
- * ceil(M/8) * ceil(N/256) >= 2^24.
+ * ceil(M/8) * ceil(N/256) >= 2^24; TERNARY_3IN5 with a group other than 0 or K,
+ * or with ceil(N/16) * M >= 2^24.
  */
 lutgemm_status_t lutgemm_validate(const lutgemm_problem_t *problem, int64_t M);
 
@@ -131,6 +137,15 @@ size_t lutgemm_packed_weight_size(const lutgemm_problem_t *problem);
  *                  max_k |a[m,k]| = f 2^e_m with f in [0.5, 1) (1 for an all-zero row);
  *                  the absmax scale s_a = amax / 127 for ACT_INT8
  * with s_off = align256(16 M J) and t_off = align256(s_off + 4 M Q).
+ * TERNARY_3IN5 instead: J = 32 ceil(K/96) triples and
+ *   offset 0:      T[M][J][16]  triple tables, FP16 or INT16, entries 14 and 15 zero;
+ *                  T[m][j][i] = sum_{e<3} x_{3j+e} w_e(13 + i) for i < 14, where
+ *                  w_e(v) is digit e of v in base 3 (most significant first) minus 1
+ *                  and x_k = 0 for k >= K (entry i is the triple pattern 13 + i; its
+ *                  negation is pattern 13 - i, Eq. 4)
+ *   offset s_off:  unused (no zero point)
+ *   offset t_off:  t[M] as above
+ * with s_off = align256(32 M J).
  * 0 for an invalid problem.
  */
 size_t lutgemm_table_size(const lutgemm_problem_t *problem, int64_t M);
@@ -159,6 +174,8 @@ size_t lutgemm_workspace_size(const lutgemm_problem_t *problem, int64_t M);
  * consecutive weights (the first weight is the MSB) with the low 3 bits inverted
  * when the MSB is set (Eq. 6); scale and zero are stored as given and
  * reinterpreted (s' = s/2, z' = 2z + 1 - 2^b, Eq. 2) in FP32 where they are used.
+ * TERNARY_3IN5: every 3 consecutive weights (padded with 0 past K) become a sign
+ * bit and a 4-bit index into the triple table (5 bits per 3 weights).
  */
 lutgemm_status_t lutgemm_pack_weights(const lutgemm_problem_t *problem, const void *codes,
                                       const void *scales, const void *zeros, void *packed,
@@ -187,6 +204,7 @@ lutgemm_status_t lutgemm_precompute(const lutgemm_problem_t *problem, int64_t M,
  *              may be NULL when that size is 0
  * FP path: O = t_m sum_q s'_q (sum_b 2^b sum_j L_{b,j} - z'_q S_q), FP32.
  * INT8 path: acc = sum_k q_a w exactly; O = acc (INT32) or (float(acc) s_a) s_w.
+ * TERNARY_3IN5: O = t_m s (sum_j L_j) (FP path, FP32) with one lookup per triple.
  * The result is bitwise reproducible run to run.
  */
 lutgemm_status_t lutgemm_mpgemm(const lutgemm_problem_t *problem, int64_t M, const void *tables,
@@ -210,8 +228,9 @@ size_t lutgemm_fused_workspace_size(const lutgemm_problem_t *problem, int64_t M)
  * lutgemm_precompute + lutgemm_mpgemm.  For single tokens with weights the
  * whole-K lookup kernel takes (at most a few MB), every workgroup builds its
  * tables in LDS from the activations: one kernel (plus a split-K sum when K is
- * split), no table buffer.  Otherwise it runs lutgemm_precompute into the
- * workspace followed by lutgemm_mpgemm.
+ * split), no table buffer.  TERNARY_3IN5: the same for every M (one kernel,
+ * tables built per workgroup for its token).  Otherwise it runs
+ * lutgemm_precompute into the workspace followed by lutgemm_mpgemm.
  *   act        device FP16 [M][K]
  *   packed, out, out_dtype, accumulate   as for lutgemm_mpgemm
  *   workspace  device, workspace_bytes >= lutgemm_fused_workspace_size(problem, M);
@@ -219,7 +238,7 @@ size_t lutgemm_fused_workspace_size(const lutgemm_problem_t *problem, int64_t M)
  * INT8 activations: results are bitwise those of lutgemm_precompute +
  * lutgemm_mpgemm.  FP16 activations: the zero-point term is summed per 128-block
  * instead of per quantization group, so results agree with the two-call path to
- * FP32 rounding.  Bitwise reproducible run to run.
+ * FP32 rounding (TERNARY_3IN5: bitwise).  Bitwise reproducible run to run.
  */
 lutgemm_status_t lutgemm_mpgemm_fused(const lutgemm_problem_t *problem, int64_t M, const void *act,
                                       const void *packed, void *out, int32_t out_dtype,
@@ -230,7 +249,8 @@ lutgemm_status_t lutgemm_mpgemm_fused(const lutgemm_problem_t *problem, int64_t 
  * Comparison path (Section 2.2, dequantization-based mpGEMM): rebuilds FP16
  * weights s (q - z) from the same packed buffer and multiplies them with FP16
  * activations act [M][K] on the matrix cores (FP32 accumulation).  ACT_FP16
- * problems only; out_dtype FP16 or FP32; accumulate as for lutgemm_mpgemm.
+ * problems only, not TERNARY_3IN5 (LUTGEMM_ERROR_NOT_SUPPORTED); out_dtype FP16
+ * or FP32; accumulate as for lutgemm_mpgemm.
  */
 lutgemm_status_t lutgemm_mpgemm_dequant(const lutgemm_problem_t *problem, int64_t M,
                                         const void *act, const void *packed, void *out,

@@ -24,14 +24,19 @@ bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
 lutgemm_status_t check_problem(const lutgemm_problem_t *p, int64_t M) {
     if (!p) return LUTGEMM_ERROR_INVALID_VALUE;
     if (p->K <= 0 || p->N <= 0 || M <= 0 || p->reserved != 0) return LUTGEMM_ERROR_INVALID_VALUE;
-    if (p->wfmt < LUTGEMM_WFMT_UINT || p->wfmt > LUTGEMM_WFMT_TERNARY) return LUTGEMM_ERROR_INVALID_VALUE;
+    if (p->wfmt < LUTGEMM_WFMT_UINT || p->wfmt > LUTGEMM_WFMT_TERNARY_3IN5) return LUTGEMM_ERROR_INVALID_VALUE;
     if (p->act != LUTGEMM_ACT_FP16 && p->act != LUTGEMM_ACT_INT8) return LUTGEMM_ERROR_INVALID_VALUE;
     if (p->scale_fp32 != 0 && p->scale_fp32 != 1) return LUTGEMM_ERROR_INVALID_VALUE;
     if (p->w_bits <= 0 || p->group_size < 0) return LUTGEMM_ERROR_INVALID_VALUE;
     if (p->K > MAX_K || p->N > MAX_N || M > MAX_M) return LUTGEMM_ERROR_NOT_SUPPORTED;
-    // the multi-token kernel runs one workgroup per (8 tokens, 256 columns) tile in a
-    // one-dimensional grid of at most 2^24 workgroups
-    if (M > 2 && ((M + 7) / 8) * ((p->N + 255) / 256) >= MAX_TILES) return LUTGEMM_ERROR_NOT_SUPPORTED;
+    // the multi-token kernel runs one workgroup per (8 tokens, 256 columns) tile, the
+    // 3-in-5 kernel one per (token, 16 columns), in one-dimensional grids of at most
+    // 2^24 workgroups
+    if (p->wfmt == LUTGEMM_WFMT_TERNARY_3IN5) {
+        if (((p->N + 15) / 16) * M >= MAX_TILES) return LUTGEMM_ERROR_NOT_SUPPORTED;
+    } else if (M > 2 && ((M + 7) / 8) * ((p->N + 255) / 256) >= MAX_TILES) {
+        return LUTGEMM_ERROR_NOT_SUPPORTED;
+    }
     if (p->K % KBLK != 0) return LUTGEMM_ERROR_NOT_SUPPORTED;
     if (p->group_size != 0 && (p->group_size % KBLK != 0 || p->K % p->group_size != 0))
         return LUTGEMM_ERROR_NOT_SUPPORTED;
@@ -42,6 +47,10 @@ lutgemm_status_t check_problem(const lutgemm_problem_t *p, int64_t M) {
         break;
     case LUTGEMM_WFMT_BINARY:
         if (p->w_bits != 1) return LUTGEMM_ERROR_NOT_SUPPORTED;
+        break;
+    case LUTGEMM_WFMT_TERNARY_3IN5:  // triples never straddle a scale: per tensor or per channel only
+        if (p->w_bits != 2) return LUTGEMM_ERROR_NOT_SUPPORTED;
+        if (p->group_size != 0 && p->group_size != p->K) return LUTGEMM_ERROR_NOT_SUPPORTED;
         break;
     default:
         if (p->w_bits != 2) return LUTGEMM_ERROR_NOT_SUPPORTED;
@@ -85,6 +94,16 @@ LutPlan plan_lut(const Layout &L, int64_t M) {
     LutPlan P{};
     const int64_t target = env_int("LUTGEMM_TARGET_BLOCKS", 256);
     const int64_t weight_bytes = L.KB * L.bits * L.N * 16;
+    if (L.tri) {  // one token per grid layer, whole K, 16 columns per workgroup (lut_tri.hip)
+        P.kind = 3;
+        P.mt = 1;
+        P.m_tiles = M;
+        P.n_tiles = (L.N + 15) / 16;
+        P.kbs = (int)L.KB;
+        P.splits = 1;
+        P.ws_bytes = 0;
+        return P;
+    }
     int kind = M > 2 ? 1 : (weight_bytes <= (int64_t)env_int("LUTGEMM_WHOLEK_MAX_KB", 10000) * 1000 ? 0 : 2);
     const int forced_kind = env_int("LUTGEMM_GEMV_KIND", -1);
     if (M <= 2 && (forced_kind == 0 || forced_kind == 2)) kind = forced_kind;
@@ -182,6 +201,7 @@ static LutParams lut_params(const Layout &L, const LutPlan &plan, int64_t M, con
     lp.S = tables ? (const char *)tables + T.s_off : nullptr;
     lp.tok = tables ? (const float *)((const char *)tables + T.tok_off) : nullptr;
     lp.planes = (const uint4 *)packed;
+    lp.sgn = L.tri ? (const uint32_t *)((const char *)packed + L.sgn_off) : nullptr;
     lp.meta = (const char *)packed + L.meta_off;
     lp.out = out;
     lp.part = plan.splits > 1 ? (float *)partials : nullptr;
@@ -231,7 +251,7 @@ struct FusedScratch {
 
 static FusedScratch fused_scratch(const Layout &L, const LutPlan &plan, int64_t M) {
     FusedScratch f{};
-    f.fused = plan.kind == 0;
+    f.fused = plan.kind == 0 || plan.kind == 3;
     if (f.fused) {
         f.part_off = 0;
         f.tok_off = plan.ws_bytes;
@@ -310,6 +330,7 @@ lutgemm_status_t lutgemm_pack_weights(const lutgemm_problem_t *problem, const vo
     pp.scales = scales;
     pp.zeros = problem->wfmt == LUTGEMM_WFMT_UINT ? zeros : nullptr;
     pp.planes = (uint4 *)packed;
+    pp.sgn = L.tri ? (uint32_t *)((char *)packed + L.sgn_off) : nullptr;
     pp.meta = (char *)packed + L.meta_off;
     pp.K = L.K;
     pp.N = L.N;
@@ -342,6 +363,7 @@ lutgemm_status_t lutgemm_precompute(const lutgemm_problem_t *problem, int64_t M,
     pp.J = L.J;
     pp.Q = L.Q;
     pp.G = L.G;
+    pp.tri = L.tri ? 1 : 0;
     return hip_status(launch_precompute(pp, L.act == LUTGEMM_ACT_INT8, stream));
 }
 
@@ -401,6 +423,7 @@ lutgemm_status_t lutgemm_mpgemm_fused(const lutgemm_problem_t *problem, int64_t 
     }
     LutParams lp = lut_params(L, plan, M, nullptr, packed, out, out_dtype, accumulate, ws + fs.part_off);
     lp.act = (const uint16_t *)act;
+    if (plan.kind == 3) return hip_status(launch_tri(lp, L, true, stream));
     lp.tok_out = plan.splits > 1 ? (float *)(ws + fs.tok_off) : nullptr;
     int e = launch_fused_gemv(lp, L, plan, stream);
     if (e == 0 && plan.splits > 1) {
@@ -415,7 +438,8 @@ lutgemm_status_t lutgemm_mpgemm_dequant(const lutgemm_problem_t *problem, int64_
                                         int32_t accumulate, void *stream) {
     lutgemm_status_t st = check_problem(problem, M);
     if (st != LUTGEMM_SUCCESS) return st;
-    if (problem->act != LUTGEMM_ACT_FP16) return LUTGEMM_ERROR_NOT_SUPPORTED;
+    if (problem->act != LUTGEMM_ACT_FP16 || problem->wfmt == LUTGEMM_WFMT_TERNARY_3IN5)
+        return LUTGEMM_ERROR_NOT_SUPPORTED;
     if (!act || !packed || !out) return LUTGEMM_ERROR_INVALID_VALUE;
     if (!aligned16(act) || !aligned16(packed) || !aligned16(out)) return LUTGEMM_ERROR_INVALID_VALUE;
     if (out_dtype != LUTGEMM_OUT_FP16 && out_dtype != LUTGEMM_OUT_FP32) return LUTGEMM_ERROR_INVALID_VALUE;

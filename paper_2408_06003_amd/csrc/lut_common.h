@@ -29,6 +29,60 @@ __device__ __forceinline__ float h2f(uint32_t bits16) {
     return __half2float(__ushort_as_half((unsigned short)bits16));
 }
 
+// Activation value entering a table: the INT8 quantization of the activation
+// quantizer, or the exact power-of-two token scaling of the FP path.
+template <bool INT8>
+__device__ __forceinline__ float act_value(uint32_t bits16, float scale) {
+    const float a = h2f(bits16);
+    if (INT8) return fminf(fmaxf(rintf(a * scale), -127.f), 127.f);
+    return a * scale;  // exact: scale is a power of two
+}
+
+__device__ __forceinline__ float absmax4(uint2 v) {
+    return fmaxf(fmaxf(fabsf(h2f(v.x & 0xFFFFu)), fabsf(h2f(v.x >> 16))),
+                 fmaxf(fabsf(h2f(v.y & 0xFFFFu)), fabsf(h2f(v.y >> 16))));
+}
+
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ float dpp_f(float v) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, ROW_MASK, 0xF, true));
+}
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ int dpp_i(int v) {
+    return __builtin_amdgcn_update_dpp(0, v, CTRL, ROW_MASK, 0xF, true);
+}
+
+// Sum over the 64 lanes of a wavefront in a fixed order (row shifts 1, 2, 4, 8,
+// then row broadcasts 15 and 31); the total is in lane 63.
+__device__ __forceinline__ float wave_sum_f(float v) {
+    v += dpp_f<0x111, 0xF>(v);
+    v += dpp_f<0x112, 0xF>(v);
+    v += dpp_f<0x114, 0xF>(v);
+    v += dpp_f<0x118, 0xF>(v);
+    v += dpp_f<0x142, 0xA>(v);
+    v += dpp_f<0x143, 0xC>(v);
+    return v;
+}
+__device__ __forceinline__ int wave_sum_i(int v) {
+    v += dpp_i<0x111, 0xF>(v);
+    v += dpp_i<0x112, 0xF>(v);
+    v += dpp_i<0x114, 0xF>(v);
+    v += dpp_i<0x118, 0xF>(v);
+    v += dpp_i<0x142, 0xA>(v);
+    v += dpp_i<0x143, 0xC>(v);
+    return v;
+}
+// Maximum over the 64 lanes (any order gives the same result); in lane 63.
+__device__ __forceinline__ float wave_max(float v) {
+    v = fmaxf(v, dpp_f<0x111, 0xF>(v));
+    v = fmaxf(v, dpp_f<0x112, 0xF>(v));
+    v = fmaxf(v, dpp_f<0x114, 0xF>(v));
+    v = fmaxf(v, dpp_f<0x118, 0xF>(v));
+    v = fmaxf(v, dpp_f<0x142, 0xA>(v));
+    v = fmaxf(v, dpp_f<0x143, 0xC>(v));
+    return v;
+}
+
 // (byte B of w) & 0x3C: a 4-bit index pre-shifted left by 2 becomes an INT32
 // table offset in one VALU op (SDWA byte select).
 template <int B>

@@ -28,18 +28,6 @@
 
 namespace lutgemm {
 
-template <bool INT8>
-__device__ __forceinline__ float act_value(uint32_t bits16, float scale) {
-    const float a = h2f(bits16);
-    if (INT8) return fminf(fmaxf(rintf(a * scale), -127.f), 127.f);
-    return a * scale;  // exact: scale is a power of two
-}
-
-__device__ __forceinline__ float absmax4(uint2 v) {
-    return fmaxf(fmaxf(fabsf(h2f(v.x & 0xFFFFu)), fabsf(h2f(v.x >> 16))),
-                 fmaxf(fabsf(h2f(v.y & 0xFFFFu)), fabsf(h2f(v.y >> 16))));
-}
-
 // Entries 4 qr .. 4 qr + 3 of the signed 16-entry table of x0..x3: quarter qr
 // holds rows 4 (qr & 1) .. + 3 of the half table, negated when qr >= 2 (Eq. 4).
 // Sums are formed in the order ((-x0 + (+-x1)) + (+-x2)) + (+-x3).
@@ -79,46 +67,6 @@ __device__ __forceinline__ void build_group_i16(char *dst, int q0, int q1, int q
     for (int i = 0; i < 4; ++i) pw[i] = ((uint32_t)t[2 * i] & 0xFFFFu) | ((uint32_t)t[2 * i + 1] << 16);
     *(uint4 *)dst = make_uint4(pw[0], pw[1], pw[2], pw[3]);
     *(uint4 *)(dst + 16) = make_uint4(neg_i16x2(pw[0]), neg_i16x2(pw[1]), neg_i16x2(pw[2]), neg_i16x2(pw[3]));
-}
-
-template <int CTRL, int ROW_MASK>
-__device__ __forceinline__ float dpp_f(float v) {
-    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, ROW_MASK, 0xF, true));
-}
-template <int CTRL, int ROW_MASK>
-__device__ __forceinline__ int dpp_i(int v) {
-    return __builtin_amdgcn_update_dpp(0, v, CTRL, ROW_MASK, 0xF, true);
-}
-
-// Sum over the 64 lanes of a wavefront in a fixed order (row shifts 1, 2, 4, 8,
-// then row broadcasts 15 and 31); the total is in lane 63.
-__device__ __forceinline__ float wave_sum_f(float v) {
-    v += dpp_f<0x111, 0xF>(v);
-    v += dpp_f<0x112, 0xF>(v);
-    v += dpp_f<0x114, 0xF>(v);
-    v += dpp_f<0x118, 0xF>(v);
-    v += dpp_f<0x142, 0xA>(v);
-    v += dpp_f<0x143, 0xC>(v);
-    return v;
-}
-__device__ __forceinline__ int wave_sum_i(int v) {
-    v += dpp_i<0x111, 0xF>(v);
-    v += dpp_i<0x112, 0xF>(v);
-    v += dpp_i<0x114, 0xF>(v);
-    v += dpp_i<0x118, 0xF>(v);
-    v += dpp_i<0x142, 0xA>(v);
-    v += dpp_i<0x143, 0xC>(v);
-    return v;
-}
-// Maximum over the 64 lanes (any order gives the same result); in lane 63.
-__device__ __forceinline__ float wave_max(float v) {
-    v = fmaxf(v, dpp_f<0x111, 0xF>(v));
-    v = fmaxf(v, dpp_f<0x112, 0xF>(v));
-    v = fmaxf(v, dpp_f<0x114, 0xF>(v));
-    v = fmaxf(v, dpp_f<0x118, 0xF>(v));
-    v = fmaxf(v, dpp_f<0x142, 0xA>(v));
-    v = fmaxf(v, dpp_f<0x143, 0xC>(v));
-    return v;
 }
 
 template <int BITS, int PW, int SW, int TW, int NW, bool INT8>

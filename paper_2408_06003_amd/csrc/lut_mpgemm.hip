@@ -1,7 +1,8 @@
 // The split-K finalize kernel and the dispatch of lutgemm_mpgemm (LUT Tensor
 // Core, Section 3.1 with Eq. 3, 5 and 6; LMMA semantics O = A x W^T + Acc,
 // Section 3.3.1): single tokens go to the GEMV kernels of lut_gemv.hip, several
-// tokens to the multi-token kernel of lut_mtok.hip.  When the grid would not fill
+// tokens to the multi-token kernel of lut_mtok.hip, ternary 3-in-5 weights to
+// lut_tri.hip.  When the grid would not fill
 // the GPU, K is split across workgroups and lut_finalize_kernel sums the partials
 // in split order after the LUT kernel ends.
 #include <hip/hip_runtime.h>
@@ -32,6 +33,7 @@ __global__ __launch_bounds__(64) void lut_finalize_kernel(LutParams p, int wfmt,
 
 int launch_lut(const LutParams &p, const Layout &L, const LutPlan &plan, void *stream) {
     hipStream_t s = (hipStream_t)stream;
+    if (plan.kind == 3) return launch_tri(p, L, false, stream);
     if (plan.kind != 1) {
         const int e0 = launch_gemv(p, L, plan, stream);
         if (e0 != 0) return e0;

@@ -13,6 +13,20 @@
 //           reinterpretation of Eq. 2 is applied in FP32 where they are used.
 // Consecutive columns are adjacent in memory so that a wavefront whose lanes are
 // 64 consecutive columns reads 1 KiB contiguous with 128-bit loads.
+//
+// Ternary 3-in-5 layout (LUTGEMM_WFMT_TERNARY_3IN5): K is covered by KB3 =
+// ceil(K/96) blocks of 32 triples of consecutive weights (weights past K are 0).
+// A triple (w0, w1, w2) is the base-3 value v = 9(w0+1) + 3(w1+1) + (w2+1) in
+// [0, 27); negation maps v to 26 - v and v = 13 is the zero triple, so the code
+// is sign = (v < 13) and index i = |v - 13| in [0, 14): the entry of pattern
+// 13 + i, negated when sign is set (the symmetry of Eq. 4 for three-valued
+// weights: 5 bits per 3 weights).
+//   index words: [KB3][N_pad] x 16 bytes, index of triple t at bits 4(t % 8) of
+//                32-bit word t / 8 (the plane-word arrangement above);
+//   sign words:  [KB3][N_pad] x 4 bytes, sign of triple t = 8d + 2k + h (d = word,
+//                k = byte, h = nibble) at bit 8k + 2d + h;
+//   meta:        as above, with G = K (per-channel) or per-tensor.
+// 20 bytes per 96 weights of a column: 1.67 bits per weight.
 #pragma once
 
 #include <stddef.h>
@@ -26,12 +40,16 @@ constexpr int KBLK = 128;       // activations covered by one packed plane word
 constexpr int GPB = 32;         // 4-activation table groups per plane word
 constexpr int NTILE = 256;      // columns per workgroup (one column per lane)
 constexpr int FIX_SHIFT = 20;   // fixed-point fraction bits of FP table entries staged in LDS
+constexpr int TBLK = 96;        // activations per 3-in-5 block (32 triples)
+constexpr int TPB = 32;         // triples per 3-in-5 block
+constexpr int TENT = 16;        // stored entries per triple table (14 used, 2 zero)
 
 struct Layout {
     int64_t K, N, N_pad, KB, J, Q, G;  // G = group size (K when per-tensor)
     int bits, wfmt, act;
     bool per_tensor;
-    size_t planes_bytes, meta_off, meta_bytes, packed_bytes;
+    bool tri;                          // ternary 3-in-5: KB counts 96-blocks, J triples
+    size_t planes_bytes, sgn_off, meta_off, meta_bytes, packed_bytes;
 };
 
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -49,8 +67,18 @@ inline Layout make_layout(const lutgemm_problem_t &p) {
     L.bits = p.w_bits;
     L.wfmt = p.wfmt;
     L.act = p.act;
-    L.planes_bytes = (size_t)L.KB * L.bits * L.N_pad * 16;
-    L.meta_off = align256(L.planes_bytes);
+    L.tri = p.wfmt == LUTGEMM_WFMT_TERNARY_3IN5;
+    if (L.tri) {
+        L.KB = (p.K + TBLK - 1) / TBLK;
+        L.J = L.KB * TPB;
+        L.planes_bytes = (size_t)L.KB * L.N_pad * 16;
+        L.sgn_off = align256(L.planes_bytes);
+        L.meta_off = align256(L.sgn_off + (size_t)L.KB * L.N_pad * 4);
+    } else {
+        L.planes_bytes = (size_t)L.KB * L.bits * L.N_pad * 16;
+        L.sgn_off = 0;
+        L.meta_off = align256(L.planes_bytes);
+    }
     L.meta_bytes = L.per_tensor ? 256 : (size_t)L.Q * L.N_pad * 4;
     L.packed_bytes = L.meta_off + align256(L.meta_bytes);
     return L;
@@ -62,7 +90,7 @@ struct TableLayout {
 
 inline TableLayout make_table_layout(const Layout &L, int64_t M) {
     TableLayout T{};
-    T.t_bytes = (size_t)M * L.J * 16;
+    T.t_bytes = (size_t)M * L.J * (L.tri ? 2 * TENT : 16);
     T.s_off = align256(T.t_bytes);
     T.tok_off = align256(T.s_off + (size_t)M * L.Q * 4);
     T.total = align256(T.tok_off + (size_t)M * 4);
@@ -71,7 +99,8 @@ inline TableLayout make_table_layout(const Layout &L, int64_t M) {
 
 // Launch plan of the LUT mpGEMM for (problem, M).
 struct LutPlan {
-    int kind;        // 0: single-token whole-K GEMV, 1: multi-token kernel, 2: single-token split-K GEMV
+    int kind;        // 0: single-token whole-K GEMV, 1: multi-token kernel, 2: single-token split-K GEMV,
+                     // 3: ternary 3-in-5 kernel (whole K, any M)
     int gemv_cfg;    // single-token kernel: lane decomposition (see lut_gemv.hip)
     int kbs;         // 128-blocks of K per split
     int splits;      // K splits (1 = no workspace)
@@ -91,6 +120,7 @@ struct PackParams {
     const void *scales;
     const void *zeros;
     uint4 *planes;
+    uint32_t *sgn;         // 3-in-5 sign words
     void *meta;
     int64_t K, N, N_pad, KB, Q, G;
     int bits, wfmt, per_tensor, scale_fp32;
@@ -102,6 +132,7 @@ struct PrecomputeParams {
     void *S;               // [M][Q]
     float *tok;            // [M]
     int64_t M, K, J, Q, G;
+    int tri;               // ternary 3-in-5 tables: [M][J triples] x 16 entries, no S
 };
 
 struct LutParams {
@@ -111,6 +142,7 @@ struct LutParams {
     const uint16_t *act;   // FP16 [M][K]: activations of the fused kernel
     float *tok_out;        // fused kernel with K split: per-token factor for the finalize kernel
     const uint4 *planes;
+    const uint32_t *sgn;   // 3-in-5 sign words
     const void *meta;
     void *out;
     float *part;           // split partial sums [splits][rows][N_pad] (float or int bits)
@@ -140,6 +172,7 @@ int launch_gemv(const LutParams &p, const Layout &L, const LutPlan &plan, void *
 int launch_fused_gemv(const LutParams &p, const Layout &L, const LutPlan &plan, void *stream);
 int launch_finalize(const LutParams &p, const Layout &L, const LutPlan &plan, void *stream);
 int launch_mtok(const LutParams &p, const Layout &L, const LutPlan &plan, void *stream);
+int launch_tri(const LutParams &p, const Layout &L, bool fused, void *stream);
 int launch_dequant(const DequantParams &p, const Layout &L, void *stream);
 
 }  // namespace lutgemm

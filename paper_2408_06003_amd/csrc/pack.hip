@@ -69,6 +69,48 @@ __global__ __launch_bounds__(256) void pack_planes_kernel(PackParams p) {
     }
 }
 
+// Ternary 3-in-5 (Section 5, three ternary weights in 5 bits): one thread per
+// (column n, 96-block kb), kb fastest.  Triple t of the block holds weights
+// 96 kb + 3t .. + 2 (0 past K); its base-3 value v = 9(w0+1) + 3(w1+1) + (w2+1)
+// becomes sign = (v < 13) and index |v - 13|: the index addresses the stored
+// half of the 27-pattern table and the sign selects its negation (Eq. 4), the
+// ternary counterpart of the offline negation of Eq. 6.
+__global__ __launch_bounds__(256) void pack_tri_kernel(PackParams p) {
+    const int64_t total = p.N_pad * p.KB;
+    for (int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; idx < total;
+         idx += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t kb = idx % p.KB;
+        const int64_t n = idx / p.KB;
+        uint32_t word[4] = {0u, 0u, 0u, 0u}, sgn = 0u;
+        if (n < p.N) {
+            const int64_t k0 = kb * TBLK;
+            const int nwords = (int)((p.K - k0) < TBLK ? (p.K - k0) : TBLK) / 4;  // K % 32 == 0
+            const uint32_t *row = (const uint32_t *)((const int8_t *)p.codes + n * p.K + k0);
+            uint32_t c[TBLK / 4];
+#pragma unroll
+            for (int i = 0; i < TBLK / 4; ++i) c[i] = i < nwords ? row[i] : 0u;
+#pragma unroll
+            for (int t = 0; t < TPB; ++t) {
+                int v = 0;
+#pragma unroll
+                for (int e = 0; e < 3; ++e) {
+                    const int k = 3 * t + e;
+                    int w = (int)(int8_t)((c[k >> 2] >> (8 * (k & 3))) & 0xFFu);
+                    w = w < -1 ? -1 : (w > 1 ? 1 : w);
+                    v = 3 * v + (w + 1);
+                }
+                const uint32_t s = v < 13 ? 1u : 0u;
+                const uint32_t i4 = (uint32_t)(v < 13 ? 13 - v : v - 13);
+                const int d = t >> 3, k = (t & 7) >> 1, h = t & 1;
+                word[d] |= i4 << (4 * (t & 7));
+                sgn |= s << (8 * k + 2 * d + h);
+            }
+        }
+        p.planes[kb * p.N_pad + n] = make_uint4(word[0], word[1], word[2], word[3]);
+        p.sgn[kb * p.N_pad + n] = sgn;
+    }
+}
+
 // Per-group metadata: (s, z) FP16 pairs [Q][N_pad]; per-tensor: FP32 (s, z).
 __global__ __launch_bounds__(256) void pack_meta_kernel(PackParams p) {
     if (p.per_tensor) {
@@ -105,7 +147,10 @@ int launch_pack(const PackParams &p, void *stream) {
     int64_t total = p.N_pad * p.KB;
     int64_t blocks = (total + 255) / 256;
     if (blocks > 65535 * 16) blocks = 65535 * 16;
-    hipLaunchKernelGGL(pack_planes_kernel, dim3((unsigned)blocks), dim3(256), 0, s, p);
+    if (p.wfmt == LUTGEMM_WFMT_TERNARY_3IN5)
+        hipLaunchKernelGGL(pack_tri_kernel, dim3((unsigned)blocks), dim3(256), 0, s, p);
+    else
+        hipLaunchKernelGGL(pack_planes_kernel, dim3((unsigned)blocks), dim3(256), 0, s, p);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return (int)e;
     int64_t mt = p.per_tensor ? 1 : p.Q * p.N_pad;

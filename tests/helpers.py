@@ -11,9 +11,11 @@ REL_FRO_TOL = 2e-3
 MAX_ABS_OVER_RMS_TOL = 1e-2
 
 
-def problem_of(inp):
+def problem_of(inp, wfmt=None):
+    """The C-ABI problem of ``inp``; ``wfmt`` overrides the weight format (the
+    ternary 3-in-5 packing of the same ternary codes)."""
     import paper_2408_06003_amd as L
-    return L.problem(inp.K, inp.N, inp.bits, inp.wfmt, inp.group,
+    return L.problem(inp.K, inp.N, inp.bits, inp.wfmt if wfmt is None else wfmt, inp.group,
                      act=inp.act_kind, scale_fp32=(inp.scales.dtype == np.float32))
 
 
@@ -25,10 +27,10 @@ def to_dev(x):
 class GpuProblem:
     """Device copies of one workload plus its packed weights."""
 
-    def __init__(self, inp):
+    def __init__(self, inp, wfmt=None):
         import paper_2408_06003_amd as L
         self.inp = inp
-        self.p = problem_of(inp)
+        self.p = problem_of(inp, wfmt)
         assert L.validate(self.p, inp.M) == L.SUCCESS, L.status_string(L.validate(self.p, inp.M))
         self.codes = to_dev(inp.codes)
         self.scales = to_dev(inp.scales)

@@ -55,6 +55,11 @@ def test_problem_struct_layout():
     (1024, 64, 2, L.WFMT_TERNARY, 128, L.ACT_FP16, True, L.ERROR_NOT_SUPPORTED),  # fp32 scale per-tensor only
     (1024, 64, 2, L.WFMT_UINT, 128, L.ACT_INT8, False, L.ERROR_NOT_SUPPORTED),    # INT8 act needs int weights
     (1024, 64, 2, L.WFMT_TERNARY, 128, L.ACT_INT8, False, L.ERROR_NOT_SUPPORTED), # INT8 act: per-channel at most
+    (4096, 4096, 2, L.WFMT_TERNARY_3IN5, 0, L.ACT_INT8, True, L.SUCCESS),
+    (4096, 4096, 2, L.WFMT_TERNARY_3IN5, 0, L.ACT_FP16, False, L.SUCCESS),
+    (11008, 300, 2, L.WFMT_TERNARY_3IN5, 11008, L.ACT_FP16, False, L.SUCCESS),
+    (1024, 64, 2, L.WFMT_TERNARY_3IN5, 128, L.ACT_FP16, False, L.ERROR_NOT_SUPPORTED),  # 3-in-5: G = 0 or K
+    (1024, 64, 1, L.WFMT_TERNARY_3IN5, 0, L.ACT_FP16, False, L.ERROR_NOT_SUPPORTED),    # 3-in-5 is ternary
     (0, 64, 2, L.WFMT_UINT, 0, L.ACT_FP16, False, L.ERROR_INVALID_VALUE),
     (1024, 0, 2, L.WFMT_UINT, 0, L.ACT_FP16, False, L.ERROR_INVALID_VALUE),
     (1024, 64, 2, 7, 0, L.ACT_FP16, False, L.ERROR_INVALID_VALUE),
@@ -93,6 +98,25 @@ def test_size_formulas():
     n_pad = 1024
     planes = K * n_pad * 4 // 8
     assert planes <= L.packed_weight_size(p) <= planes + (K // 128) * n_pad * 4 + 512
+
+
+def test_size_formulas_ternary_3in5():
+    """3-in-5 ternary: 5 bits per 3 weights (16 index bytes + 4 sign bytes per 96 weights of a
+    column, K padded to 96); tables of 16 two-byte entries per triple and token."""
+    M, K, N = 2, 4096, 1000
+    p = L.problem(K, N, 2, L.WFMT_TERNARY_3IN5, 0, L.ACT_INT8, True)
+    kb3, n_pad = -(-K // 96), 1024
+    body = kb3 * n_pad * 20
+    assert body <= L.packed_weight_size(p) <= body + 3 * 256
+    assert L.packed_weight_size(p) < K * n_pad * 2 // 8  # smaller than the 2-bit planes
+    s_off, t_off = L.table_offsets(p, M)
+    assert s_off >= M * kb3 * 32 * 16 * 2 and s_off % 256 == 0
+    assert L.table_size(p, M) >= t_off + 4 * M
+    assert L.workspace_size(p, M) == 0 and L.fused_workspace_size(p, M) == 0
+    # grid limit: ceil(N / 16) * M workgroups below 2^24
+    big = L.problem(1024, 1 << 16, 2, L.WFMT_TERNARY_3IN5, 0, L.ACT_FP16)
+    assert L.validate(big, 4095) == L.SUCCESS
+    assert L.validate(big, 4096) == L.ERROR_NOT_SUPPORTED
 
 
 def test_entry_points_reject_before_launch():
