@@ -62,20 +62,24 @@ def parse():
     return ap.parse_args()
 
 
-def algorithmic_bytes(inp, out_bytes, fused=False):
+def algorithmic_bytes(inp, out_bytes, fused=False, tri=False):
     """Bytes the method must move for one mpGEMM call: weights N K b / 8, metadata
     (FP16 scale + zero per group: 4 B; per-channel scale: 2 B; per-tensor: 4 B),
     tables 4 M K (8 two-byte entries per 4 activations) -- or, for the fused
-    kernel, the FP16 activations 2 M K instead -- and the output M N out_bytes."""
+    kernel, the FP16 activations 2 M K instead -- and the output M N out_bytes.
+    Ternary 3-in-5 (``tri``): weights 5 bits per 3 weights, N K 5 / 24 (K padded to
+    whole 96-weight blocks), and tables of 16 two-byte entries per 3 activations."""
     M, K, N, b = inp.M, inp.K, inp.N, inp.bits
     weights = N * K * b // 8
+    if tri:
+        weights = N * (-(-K // 96)) * 20
     if inp.group == 0:
         meta = 4
     elif inp.zeros is None:
         meta = 2 * N * (K // inp.group)
     else:
         meta = 4 * N * (K // inp.group)
-    tables = (2 if fused else 4) * M * K
+    tables = 2 * M * K if fused else (M * (-(-K // 96)) * 32 * 32 if tri else 4 * M * K)
     out = M * N * out_bytes
     return {"weights": weights, "meta": meta, "tables": tables, "out": out,
             "total": weights + meta + tables + out}
@@ -111,18 +115,22 @@ def load_traffic(workload, kernel):
 class Case:
     """One workload shape on the device, with a rotation set of packed weights."""
 
-    def __init__(self, cid, sid, M, rotate=True):
+    def __init__(self, cid, sid, M, rotate=True, wfmt=None):
+        """``wfmt`` overrides the packing of the same codes (the ternary 3-in-5 format)."""
         import torch
         import paper_2408_06003_amd as L
         import workloads as W
         self.torch, self.L, self.W = torch, L, W
         w = W.WORKLOADS[cid]
         self.name = w.name if len(w.kn) == 1 and len(w.ms) == 1 else f"{w.name}_M{M}_K{w.kn[sid][0]}_N{w.kn[sid][1]}"
+        self.tri = wfmt == L.WFMT_TERNARY_3IN5
+        if self.tri:
+            self.name += "_3in5"
         self.inp = W.make_inputs(cid, sid, M=M)
         inp = self.inp
         self.M, self.K, self.N = inp.M, inp.K, inp.N
-        self.p = L.problem(inp.K, inp.N, inp.bits, inp.wfmt, inp.group, act=inp.act_kind,
-                           scale_fp32=(inp.scales.dtype.itemsize == 4))
+        self.p = L.problem(inp.K, inp.N, inp.bits, inp.wfmt if wfmt is None else wfmt, inp.group,
+                           act=inp.act_kind, scale_fp32=(inp.scales.dtype.itemsize == 4))
         dev = torch.device("cuda")
         codes = torch.from_numpy(inp.codes).to(dev)
         scales = torch.from_numpy(inp.scales).to(dev)
@@ -219,7 +227,7 @@ class Case:
         self.precompute()
         ms_mp = self.timed(self.mpgemm, n_kernel, check=lambda: self.out)
         ms_pre = self.timed(lambda i: self.precompute(), n_kernel)
-        b = algorithmic_bytes(self.inp, self.out_bytes)
+        b = algorithmic_bytes(self.inp, self.out_bytes, tri=self.tri)
         gbps = b["total"] / (ms_mp * 1e-3) / 1e9
         # achievable streaming read of the same byte count, same rotation and timing
         sink = self.torch.zeros(4096, dtype=self.torch.int32, device="cuda")
@@ -237,7 +245,7 @@ class Case:
                "precompute_over_mpgemm": round(ms_pre / ms_mp, 4),
                "fused_us": round(ms_fu * 1e3, 3), "fused_tops": round(self.effective_tops(ms_fu), 3),
                "algorithmic_bytes": b["total"], "rotation_copies": len(self.packed)}
-        if self.M >= 16 and not self.int8:
+        if self.M >= 16 and not self.int8 and not self.tri:
             out = self.torch.empty((self.M, self.N), dtype=self.torch.float16, device="cuda")
             for i in range(3):
                 self.dequant(i, out)
@@ -303,7 +311,7 @@ def main():
               "one GPU (how it would shard across GPUs is described in DESIGN.md)", file=sys.stderr)
         sys.exit(2)
     import torch
-    import paper_2408_06003_amd  # noqa: F401  (fails loudly if the HIP library is not built)
+    import paper_2408_06003_amd as L  # fails loudly if the HIP library is not built
     import workloads as W
     torch.cuda.set_device(0)
 
@@ -362,7 +370,7 @@ def main():
                           "tops": round(head.effective_tops(ms_two), 4), "mpgemm_roofline": mp_roof},
         "headline_kernels": kern,
     }
-    head_inp = head.inp
+    head_inp, head_name = head.inp, head.name
     head.release()
     del head
 
@@ -372,6 +380,13 @@ def main():
     # ---------------- the other workload shapes
     if not args.quick:
         recs = []
+        # the headline shape with its ternary weights packed three per 5 bits
+        if not args.only or args.only == head_name + "_3in5":
+            c = Case(2, 0, 1, wfmt=L.WFMT_TERNARY_3IN5)
+            recs.append(c.measure(200, 3))
+            log(f"{c.name}: mpgemm {recs[-1]['mpgemm_us']} us, fused {recs[-1]['fused_us']} us")
+            c.release()
+            del c
         for cid, w in W.WORKLOADS.items():
             for (sid, M, Kd, N) in w.shapes():
                 if cid == 2:

@@ -19,21 +19,26 @@
 // the whole K; the 64 lanes of a wavefront are (column, K slice): 16 columns x 4
 // slices, and K slice sigma of the workgroup takes 96-blocks sigma, sigma + S, ...
 // (S = 4 NW slices).  Per chunk of S blocks every lane builds (fused) or expands
-// (from precomputed tables) the signed tables of 2 triples; the tables of one
-// block are padded by one table so the 4 slices of a wavefront read 4 different
-// 64-byte bank groups.  Slices are summed by a fixed butterfly, wavefronts in
+// (from precomputed tables) the signed tables of 2 triples, consecutive lanes
+// taking consecutive triples.  Triple tables sit 80 bytes apart, so the 16-byte
+// stores of 8 consecutive lanes cover all 8 16-byte bank groups of a 128-byte bank
+// row (conflict-free), and blocks are 64 mod 128 bytes apart, so the 4 slices of a
+// wavefront read their tables from two (32 banks) or four (64 banks) disjoint
+// halves or quarters of the banks.  Slices are summed by a fixed butterfly, wavefronts in
 // order, so results are bitwise reproducible.  Every workgroup of the fused
 // variant reads its token (8 KiB at K = 4096, from L2) and performs the same FP32
 // quantization / scaling as the precompute kernel, so both variants produce the
 // same tables and the same result bits.
 #include "lut_common.h"
+#include "tri_table.h"
 
 namespace lutgemm {
 
 constexpr int TRI_SW = 4;                          // K slices per wavefront
 constexpr int TRI_CW = 64 / TRI_SW;                // columns per workgroup
 constexpr int TRI_TAB = 64;                        // bytes of one signed triple table (32 x 2 B)
-constexpr int TRI_BLK = TPB * TRI_TAB + TRI_TAB;   // bytes per 96-block in LDS (one table of padding)
+constexpr int TRI_TS = 80;                         // LDS stride of the triple tables of a block
+constexpr int TRI_BLK = TPB * TRI_TS + 64;         // LDS bytes per 96-block (= 64 mod 128)
 
 template <bool INT8>
 __device__ __forceinline__ uint32_t neg2(uint32_t x) {
@@ -57,29 +62,27 @@ __device__ __forceinline__ void store_tri(char *dst, uint4 lo, uint4 hi) {
     *(uint4 *)(dst + 48) = make_uint4(neg2<INT8>(hi.x), neg2<INT8>(hi.y), neg2<INT8>(hi.z), neg2<INT8>(hi.w));
 }
 
-// The 16 stored entries of the triple x0..x2 (14 patterns and two zeros), as
-// 16-bit words: sums (w0 x0 + w1 x1) + w2 x2 in FP32, exact INT16 or FP16 (RNE).
+// The 16 stored entries of the triple x0..x2 (14 patterns and two zeros, formed
+// by tri_table14), as 16-bit words: exact INT16 from the quantized integers, or
+// FP16 (round to nearest even) from the FP32 sums.
 template <bool INT8>
 __device__ __forceinline__ void tri_entries(float x0, float x1, float x2, uint4 &lo, uint4 &hi) {
+    uint32_t h[16];
+    if constexpr (INT8) {
+        int e[14];
+        tri_table14<int>((int)x0, (int)x1, (int)x2, e);
+#pragma unroll
+        for (int i = 0; i < 14; ++i) h[i] = (uint32_t)e[i] & 0xFFFFu;
+    } else {
+        float e[14];
+        tri_table14<float>(x0, x1, x2, e);
+#pragma unroll
+        for (int i = 0; i < 14; ++i) h[i] = (uint32_t)__half_as_ushort(__float2half_rn(e[i]));
+    }
+    h[14] = h[15] = 0u;
     uint32_t w[8];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-        uint32_t h2[2];
-#pragma unroll
-        for (int u = 0; u < 2; ++u) {
-            const int e = 2 * i + u, v = 13 + e;
-            const int w0 = v / 9 - 1, w1 = (v / 3) % 3 - 1, w2 = v % 3 - 1;
-            const float p0 = w0 > 0 ? x0 : (w0 < 0 ? -x0 : 0.f);
-            const float p1 = w1 > 0 ? x1 : (w1 < 0 ? -x1 : 0.f);
-            const float p2 = w2 > 0 ? x2 : (w2 < 0 ? -x2 : 0.f);
-            const float t = e < 14 ? (p0 + p1) + p2 : 0.f;
-            if (INT8)
-                h2[u] = (uint32_t)(uint16_t)(int16_t)(int)t;
-            else
-                h2[u] = (uint32_t)__half_as_ushort(__float2half_rn(t));
-        }
-        w[i] = h2[0] | (h2[1] << 16);
-    }
+    for (int i = 0; i < 8; ++i) w[i] = h[2 * i] | (h[2 * i + 1] << 16);
     lo = make_uint4(w[0], w[1], w[2], w[3]);
     hi = make_uint4(w[4], w[5], w[6], w[7]);
 }
@@ -105,14 +108,14 @@ template <bool INT8>
 __device__ __forceinline__ void tri_lookup8(uint32_t &ai, float &af, const char *Fd, uint32_t base, uint32_t lo,
                                             uint32_t hi) {
     uint16_t h[8];
-    h[0] = *(const uint16_t *)(Fd + 0 * TRI_TAB + add_byte<0>(base, lo));
-    h[1] = *(const uint16_t *)(Fd + 1 * TRI_TAB + add_byte<0>(base, hi));
-    h[2] = *(const uint16_t *)(Fd + 2 * TRI_TAB + add_byte<1>(base, lo));
-    h[3] = *(const uint16_t *)(Fd + 3 * TRI_TAB + add_byte<1>(base, hi));
-    h[4] = *(const uint16_t *)(Fd + 4 * TRI_TAB + add_byte<2>(base, lo));
-    h[5] = *(const uint16_t *)(Fd + 5 * TRI_TAB + add_byte<2>(base, hi));
-    h[6] = *(const uint16_t *)(Fd + 6 * TRI_TAB + add_byte<3>(base, lo));
-    h[7] = *(const uint16_t *)(Fd + 7 * TRI_TAB + add_byte<3>(base, hi));
+    h[0] = *(const uint16_t *)(Fd + 0 * TRI_TS + add_byte<0>(base, lo));
+    h[1] = *(const uint16_t *)(Fd + 1 * TRI_TS + add_byte<0>(base, hi));
+    h[2] = *(const uint16_t *)(Fd + 2 * TRI_TS + add_byte<1>(base, lo));
+    h[3] = *(const uint16_t *)(Fd + 3 * TRI_TS + add_byte<1>(base, hi));
+    h[4] = *(const uint16_t *)(Fd + 4 * TRI_TS + add_byte<2>(base, lo));
+    h[5] = *(const uint16_t *)(Fd + 5 * TRI_TS + add_byte<2>(base, hi));
+    h[6] = *(const uint16_t *)(Fd + 6 * TRI_TS + add_byte<3>(base, lo));
+    h[7] = *(const uint16_t *)(Fd + 7 * TRI_TS + add_byte<3>(base, hi));
     if constexpr (INT8) {
         uint32_t pr[4];
 #pragma unroll
@@ -148,8 +151,13 @@ __global__ __launch_bounds__(64 * NW) void lut_tri_kernel(LutParams p, int wfmt,
     const int sigma = wave * TRI_SW + sl;
     const int64_t m = blockIdx.x / n_tiles;
     const int64_t n = (int64_t)(blockIdx.x % n_tiles) * TRI_CW + c;  // < N_pad
-    // this thread's two triples of every chunk: block tb, triples tj and tj + 1
-    const int tb = (2 * tid) / TPB, tj = (2 * tid) % TPB;
+    // this thread's two triples of every chunk: g = tid and tid + NT, in block g / 32
+    int tb[2], tj[2];
+#pragma unroll
+    for (int r = 0; r < 2; ++r) {
+        tb[r] = (tid + NT * r) / TPB;
+        tj[r] = (tid + NT * r) % TPB;
+    }
 
     // epilogue operands first (their latency overlaps everything below)
     const Epi ep = load_epi<INT8>(p, wfmt, m, n, false);
@@ -165,26 +173,40 @@ __global__ __launch_bounds__(64 * NW) void lut_tri_kernel(LutParams p, int wfmt,
     const uint16_t *arow = FUSED ? p.act + m * p.K : nullptr;
     const uint32_t *a32 = (const uint32_t *)arow;
     const int64_t kw = p.K / 2;  // activation words of the token
-    // the 3 activation words of this thread's triples in chunk kc (0 past K)
-    auto load_a = [&](int64_t kc, uint32_t (&aw)[3]) {
+    // the 2 activation words holding triple g of chunk kc (halves 3g .. 3g + 2 start
+    // in the low half of the first word when g is even, in its high half when odd;
+    // words past the token are 0)
+    auto load_a = [&](int64_t kc, uint32_t (&aw)[2][2]) {
 #pragma unroll
-        for (int i = 0; i < 3; ++i) {
-            const int64_t q = kc * (TBLK / 2) + 3 * tid + i;
-            const uint32_t v = a32[q < kw ? q : kw - 1];
-            aw[i] = q < kw ? v : 0u;
+        for (int r = 0; r < 2; ++r) {
+#pragma unroll
+            for (int i = 0; i < 2; ++i) {
+                const int64_t q = kc * (TBLK / 2) + ((3 * (tid + NT * r)) >> 1) + i;
+                const uint32_t v = a32[q < kw ? q : kw - 1];
+                aw[r][i] = q < kw ? v : 0u;
+            }
         }
     };
-    // the 4 table words of this thread's triples in chunk kc (table-fed)
-    auto load_t = [&](int64_t kc, int nkb, uint4 (&tw)[4]) {
-        const int64_t j = (kc + (tb < nkb ? tb : nkb - 1)) * TPB + tj;
-        const uint4 *src = p.T + 2 * (m * p.J + j);
+    // the table words of this thread's triples in chunk kc (table-fed)
+    auto load_t = [&](int64_t kc, int nkb, uint4 (&tw)[2][2]) {
 #pragma unroll
-        for (int i = 0; i < 4; ++i) tw[i] = src[i];
+        for (int r = 0; r < 2; ++r) {
+            const int64_t j = (kc + (tb[r] < nkb ? tb[r] : nkb - 1)) * TPB + tj[r];
+            const uint4 *src = p.T + 2 * (m * p.J + j);
+            tw[r][0] = src[0];
+            tw[r][1] = src[1];
+        }
+    };
+    // activations e = 0..2 of triple r from its two words (tid odd shifts by a half)
+    auto act3 = [&](const uint32_t (&aw)[2][2], int r, int e) -> uint32_t {
+        const uint64_t v = ((uint64_t)aw[r][1] << 32) | aw[r][0];
+        const int sh = 16 * (((tid + NT * r) & 1) + e);
+        return (uint32_t)(v >> sh) & 0xFFFFu;
     };
 
     float scale = 0.f;
-    uint32_t aw[3] = {0u, 0u, 0u};
-    uint4 tw[4];
+    uint32_t aw[2][2] = {{0u, 0u}, {0u, 0u}};
+    uint4 tw[2][2];
     uint4 w;
     uint32_t sg;
     int nkb = (int)(p.KB < S ? p.KB : S);
@@ -194,8 +216,10 @@ __global__ __launch_bounds__(64 * NW) void lut_tri_kernel(LutParams p, int wfmt,
         // amax of the whole token: the first chunk from registers, the rest from memory
         float amax = 0.f;
 #pragma unroll
-        for (int i = 0; i < 3; ++i)
-            amax = fmaxf(amax, fmaxf(fabsf(h2f(aw[i] & 0xFFFFu)), fabsf(h2f(aw[i] >> 16))));
+        for (int r = 0; r < 2; ++r)
+#pragma unroll
+            for (int i = 0; i < 2; ++i)
+                amax = fmaxf(amax, fmaxf(fabsf(h2f(aw[r][i] & 0xFFFFu)), fabsf(h2f(aw[r][i] >> 16))));
         for (int64_t q = (int64_t)S * (TBLK / 2) + tid; q < kw; q += NT)
             amax = fmaxf(amax, fmaxf(fabsf(h2f(a32[q] & 0xFFFFu)), fabsf(h2f(a32[q] >> 16))));
         amax = wave_max(amax);
@@ -233,23 +257,18 @@ __global__ __launch_bounds__(64 * NW) void lut_tri_kernel(LutParams p, int wfmt,
             load_w(kc, nkb, w, sg);
         }
         // build or expand this thread's two triple tables
-        if (tb < nkb) {
-            char *dst = F + tb * TRI_BLK + tj * TRI_TAB;
-            if constexpr (FUSED) {
-                float x[6];
 #pragma unroll
-                for (int i = 0; i < 3; ++i) {
-                    x[2 * i] = act_value<INT8>(aw[i] & 0xFFFFu, scale);
-                    x[2 * i + 1] = act_value<INT8>(aw[i] >> 16, scale);
+        for (int r = 0; r < 2; ++r) {
+            if (tb[r] < nkb) {
+                char *dst = F + tb[r] * TRI_BLK + tj[r] * TRI_TS;
+                if constexpr (FUSED) {
+                    uint4 lo, hi;
+                    tri_entries<INT8>(act_value<INT8>(act3(aw, r, 0), scale), act_value<INT8>(act3(aw, r, 1), scale),
+                                      act_value<INT8>(act3(aw, r, 2), scale), lo, hi);
+                    store_tri<INT8>(dst, lo, hi);
+                } else {
+                    store_tri<INT8>(dst, tw[r][0], tw[r][1]);
                 }
-                uint4 lo, hi;
-                tri_entries<INT8>(x[0], x[1], x[2], lo, hi);
-                store_tri<INT8>(dst, lo, hi);
-                tri_entries<INT8>(x[3], x[4], x[5], lo, hi);
-                store_tri<INT8>(dst + TRI_TAB, lo, hi);
-            } else {
-                store_tri<INT8>(dst, tw[0], tw[1]);
-                store_tri<INT8>(dst + TRI_TAB, tw[2], tw[3]);
             }
         }
         lds_barrier();
@@ -264,7 +283,7 @@ __global__ __launch_bounds__(64 * NW) void lut_tri_kernel(LutParams p, int wfmt,
                 if (d == 1) slot_offsets<1>(wd[1], sg, lo, hi);
                 if (d == 2) slot_offsets<2>(wd[2], sg, lo, hi);
                 if (d == 3) slot_offsets<3>(wd[3], sg, lo, hi);
-                tri_lookup8<INT8>(ai, af, F + (8 * d) * TRI_TAB, base, lo, hi);
+                tri_lookup8<INT8>(ai, af, F + (8 * d) * TRI_TS, base, lo, hi);
             }
         }
     }

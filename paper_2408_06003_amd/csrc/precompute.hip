@@ -20,13 +20,13 @@
 //      activation.  All reductions have a fixed order.
 // Ternary 3-in-5 weights (TRI): step 2 builds, per triple j of activations
 // x_{3j..3j+2} (0 past K), the 14 entries T[i] = sum_e w_e(13 + i) x_{3j+e} of
-// the stored half of the 27-pattern table (w_e(v): base-3 digit e of v, most
-// significant first, minus 1), summed as (w0 x0 + w1 x1) + w2 x2; there is no
-// zero point, so step 3 is skipped.
+// the stored half of the 27-pattern table (tri_table.h); there is no zero point,
+// so step 3 is skipped.
 #include <hip/hip_runtime.h>
 #include <hip/hip_fp16.h>
 
 #include "lutgemm_internal.h"
+#include "tri_table.h"
 
 namespace lutgemm {
 
@@ -77,16 +77,6 @@ __device__ __forceinline__ int block_sum_i(int v, int *red) {
 }
 
 constexpr int64_t ROW_LDS_MAX_K = 32768;  // tokens up to this length are staged in LDS once
-
-// Entry i < 14 of the triple table of x0..x2 (pattern 13 + i), in FP32.
-__device__ __forceinline__ float tri_entry(int i, float x0, float x1, float x2) {
-    const int v = 13 + i;
-    const int w0 = v / 9 - 1, w1 = (v / 3) % 3 - 1, w2 = v % 3 - 1;
-    const float p0 = w0 > 0 ? x0 : (w0 < 0 ? -x0 : 0.f);
-    const float p1 = w1 > 0 ? x1 : (w1 < 0 ? -x1 : 0.f);
-    const float p2 = w2 > 0 ? x2 : (w2 < 0 ? -x2 : 0.f);
-    return (p0 + p1) + p2;
-}
 
 template <bool INT8, bool ROW_LDS, bool TRI>
 __global__ __launch_bounds__(256) void precompute_kernel(PrecomputeParams p) {
@@ -146,21 +136,22 @@ __global__ __launch_bounds__(256) void precompute_kernel(PrecomputeParams p) {
                 const int64_t k = 3 * j + e;
                 x[e] = k < p.K ? token_value<INT8>(h2f(a[k]), scale) : 0.f;
             }
+            uint32_t h[16];
+            if (INT8) {
+                int e[14];  // |e| <= 381, exact
+                tri_table14<int>((int)x[0], (int)x[1], (int)x[2], e);
+#pragma unroll
+                for (int i = 0; i < 14; ++i) h[i] = (uint32_t)e[i] & 0xFFFFu;
+            } else {
+                float e[14];
+                tri_table14<float>(x[0], x[1], x[2], e);
+#pragma unroll
+                for (int i = 0; i < 14; ++i) h[i] = (uint32_t)__half_as_ushort(__float2half_rn(e[i]));
+            }
+            h[14] = h[15] = 0u;
             uint32_t w[8];
 #pragma unroll
-            for (int i = 0; i < 8; ++i) {
-                uint32_t h2[2];
-#pragma unroll
-                for (int u = 0; u < 2; ++u) {
-                    const int e = 2 * i + u;
-                    const float t = e < 14 ? tri_entry(e, x[0], x[1], x[2]) : 0.f;
-                    if (INT8)
-                        h2[u] = (uint32_t)(uint16_t)(int16_t)(int)t;  // |t| <= 381, exact
-                    else
-                        h2[u] = (uint32_t)__half_as_ushort(__float2half_rn(t));
-                }
-                w[i] = h2[0] | (h2[1] << 16);
-            }
+            for (int i = 0; i < 8; ++i) w[i] = h[2 * i] | (h[2 * i + 1] << 16);
             uint4 *dst = p.T + 2 * (m * p.J + j);
             dst[0] = make_uint4(w[0], w[1], w[2], w[3]);
             dst[1] = make_uint4(w[4], w[5], w[6], w[7]);
