@@ -65,8 +65,12 @@ enum {
 /* Activation / table types. */
 enum {
     LUTGEMM_ACT_FP16 = 0,     /* FP16 activations -> FP16 tables, FP32 accumulation              */
-    LUTGEMM_ACT_INT8 = 1      /* FP16 activations quantized per token to INT8 (absmax) -> INT16
+    LUTGEMM_ACT_INT8 = 1,     /* FP16 activations quantized per token to INT8 (absmax) -> INT16
                                  tables, exact INT32 accumulation (BINARY / TERNARY weights)     */
+    LUTGEMM_ACT_FP16_LUT8 = 2 /* FP16 activations, tables quantized to INT8 with one FP32 scale
+                                 per table (Section 3.1.4): an approximation (relative error of
+                                 the output about 3e-3), half the table bytes of ACT_FP16; not
+                                 with TERNARY_3IN5                                               */
 };
 
 /* Output types. */
@@ -116,7 +120,7 @@ const char *lutgemm_last_error(void);
  * group_size != 0 or with UINT; ACT_INT8 with UINT weights or with a group
  * smaller than K; K > 2^20, N > 2^24 or M > 2^19; M > 2 with
  * ceil(M/8) * ceil(N/256) >= 2^24; TERNARY_3IN5 with a group other than 0 or K,
- * or with ceil(N/16) * M >= 2^24.
+ * with ceil(N/16) * M >= 2^24, or with ACT_FP16_LUT8.
  */
 lutgemm_status_t lutgemm_validate(const lutgemm_problem_t *problem, int64_t M);
 
@@ -137,6 +141,11 @@ size_t lutgemm_packed_weight_size(const lutgemm_problem_t *problem);
  *                  max_k |a[m,k]| = f 2^e_m with f in [0.5, 1) (1 for an all-zero row);
  *                  the absmax scale s_a = amax / 127 for ACT_INT8
  * with s_off = align256(16 M J) and t_off = align256(s_off + 4 M Q).
+ * ACT_FP16_LUT8 instead of the FP16 T:
+ *   offset 0:      T8[M][J][8]  INT8 codes of each half table: amax = max_i |T[i]| (T as
+ *                  for ACT_FP16, FP32), T8[i] = clamp(rint(T[i] * (127 / amax)), -127, 127)
+ *   offset sc_off: sc[M][J]     FP32 amax / 127 (0 for an all-zero table)
+ * with sc_off = align256(8 M J), s_off = align256(sc_off + 4 M J); S and t as for ACT_FP16.
  * TERNARY_3IN5 instead: J = 32 ceil(K/96) triples and
  *   offset 0:      T[M][J][16]  triple tables, FP16 or INT16, entries 14 and 15 zero;
  *                  T[m][j][i] = sum_{e<3} x_{3j+e} w_e(13 + i) for i < 14, where
@@ -186,7 +195,8 @@ lutgemm_status_t lutgemm_pack_weights(const lutgemm_problem_t *problem, const vo
  * that reads act [M][K] FP16 (device) and writes the table buffer described at
  * lutgemm_table_size.  For ACT_INT8 it first quantizes each token:
  * amax = max |a|, q_a = clamp(rint(a * (127 / amax)), -127, 127) in FP32
- * (q_a = 0 when amax == 0).
+ * (q_a = 0 when amax == 0).  For ACT_FP16_LUT8 it quantizes each finished table
+ * (Section 3.1.4).
  */
 lutgemm_status_t lutgemm_precompute(const lutgemm_problem_t *problem, int64_t M, const void *act,
                                     void *tables, size_t table_bytes, void *stream);
@@ -236,7 +246,8 @@ size_t lutgemm_fused_workspace_size(const lutgemm_problem_t *problem, int64_t M)
  *   workspace  device, workspace_bytes >= lutgemm_fused_workspace_size(problem, M);
  *              may be NULL when that size is 0
  * INT8 activations: results are bitwise those of lutgemm_precompute +
- * lutgemm_mpgemm.  FP16 activations: the zero-point term is summed per 128-block
+ * lutgemm_mpgemm (ACT_FP16_LUT8: always the two calls, the quantized tables
+ * going through the workspace).  FP16 activations: the zero-point term is summed per 128-block
  * instead of per quantization group, so results agree with the two-call path to
  * FP32 rounding (TERNARY_3IN5: bitwise).  Bitwise reproducible run to run.
  */
@@ -248,9 +259,10 @@ lutgemm_status_t lutgemm_mpgemm_fused(const lutgemm_problem_t *problem, int64_t 
 /*
  * Comparison path (Section 2.2, dequantization-based mpGEMM): rebuilds FP16
  * weights s (q - z) from the same packed buffer and multiplies them with FP16
- * activations act [M][K] on the matrix cores (FP32 accumulation).  ACT_FP16
- * problems only, not TERNARY_3IN5 (LUTGEMM_ERROR_NOT_SUPPORTED); out_dtype FP16
- * or FP32; accumulate as for lutgemm_mpgemm.
+ * activations act [M][K] on the matrix cores (FP32 accumulation).  ACT_FP16 and
+ * ACT_FP16_LUT8 problems (the activations are used as they are), not
+ * TERNARY_3IN5 (LUTGEMM_ERROR_NOT_SUPPORTED); out_dtype FP16 or FP32; accumulate
+ * as for lutgemm_mpgemm.
  */
 lutgemm_status_t lutgemm_mpgemm_dequant(const lutgemm_problem_t *problem, int64_t M,
                                         const void *act, const void *packed, void *out,

@@ -19,6 +19,10 @@ Functions and the passage each follows:
 * ``half_tables``      -- precompute output: symmetric half tables (Eq. 4-5)
 * ``group_sums``       -- activation sums per quantization group (zero-point term of Eq. 3)
 * ``token_pow2``       -- per-token power-of-two normalizer of the FP16 tables
+* ``lut8_tables``      -- INT8 table quantization, per table (Section 3.1.4): codes, scales
+* ``mpgemm_lut8``      -- FP mpGEMM through the INT8-quantized tables: the approximation
+                          follows the method's steps (Section 3.1.4, Eq. 2-6, bit-serial
+                          planes of Section 3.2.1); no closed form exists for it
 """
 from __future__ import annotations
 
@@ -77,6 +81,11 @@ def lib():
         L.oracle_group_sums_i64.argtypes = [_I64, _I64, _I64, _P, _P]
         L.oracle_token_pow2.restype = None
         L.oracle_token_pow2.argtypes = [_I64, _I64, _P, _P]
+        L.oracle_lut8_tables.restype = None
+        L.oracle_lut8_tables.argtypes = [_I64, _I64, _P, _P, _P, _P]
+        L.oracle_mpgemm_lut8.restype = ctypes.c_int
+        L.oracle_mpgemm_lut8.argtypes = [_I64, _I64, _I64, _P, _P, ctypes.c_int, ctypes.c_int, _I64, _P, _P,
+                                         _P, _I64, _P, _I64, _P]
         _lib = L
     return _lib
 
@@ -207,11 +216,16 @@ def reference_output(inp, rows=None, cols=None, acc=None):
     """Oracle output for a ``workloads.Inputs`` problem.
 
     FP16 activations: float64 y.  INT8 activations: (int64 accumulator, float32 y) where
-    y = (float(acc) * s_a) * s_w.
+    y = (float(acc) * s_a) * s_w.  FP16 activations with INT8 table quantization
+    (act_kind 2): float64 y through the quantized tables (``mpgemm_lut8``).
     """
     if inp.act_kind == 0:
         return mpgemm_fp(inp.act, inp.codes, inp.wfmt, inp.group, inp.scales, inp.zeros,
                          rows=rows, cols=cols, acc=acc)
+    if inp.act_kind == 2:  # FP16 activations through INT8-quantized tables
+        y = mpgemm_lut8(inp.act, inp.codes, inp.wfmt, inp.bits, inp.group, inp.scales, inp.zeros,
+                        rows=rows, cols=cols)
+        return y if acc is None else y + np.asarray(acc, dtype=np.float64)
     qa, sa = quantize_int8(inp.act)
     iacc = mpgemm_int(qa, inp.codes, inp.wfmt, rows=rows, cols=cols)
     r = np.arange(inp.M) if rows is None else np.asarray(rows)
@@ -224,3 +238,33 @@ def reference_output(inp, rows=None, cols=None, acc=None):
         sw = np.asarray(inp.scales, dtype=np.float32).reshape(inp.N)[c]
     y = int_output_f32(iacc, sa[r], sw)
     return iacc, y
+
+
+def lut8_tables(act: np.ndarray):
+    """INT8-quantized half tables: (q int8 [M, K/4, 8], scale float32 [M, K/4], mult float64 [M])."""
+    a = np.ascontiguousarray(np.asarray(act).astype(np.float32))
+    M, K = a.shape
+    q = np.empty((M, K // 4, 8), dtype=np.int8)
+    sc = np.empty((M, K // 4), dtype=np.float32)
+    mult = np.empty((M,), dtype=np.float64)
+    lib().oracle_lut8_tables(M, K, _ptr(a), _ptr(q), _ptr(sc), _ptr(mult))
+    return q, sc, mult
+
+
+def mpgemm_lut8(act: np.ndarray, codes: np.ndarray, wfmt: int, bits: int, group: int, scales: np.ndarray,
+                zeros: Optional[np.ndarray], rows=None, cols=None) -> np.ndarray:
+    """float64 y[rows][cols] through INT8-quantized tables (the approximation's own reference)."""
+    a = np.ascontiguousarray(np.asarray(act).astype(np.float32))
+    M, K = a.shape
+    N = codes.shape[0]
+    c = np.ascontiguousarray(codes)
+    s = _f64(scales).reshape(-1)
+    z = None if zeros is None else _f64(zeros).reshape(-1)
+    r_arr, nr = _subset(rows)
+    c_arr, nc = _subset(cols)
+    y = np.empty((nr if rows is not None else M, nc if cols is not None else N), dtype=np.float64)
+    rc = lib().oracle_mpgemm_lut8(M, N, K, _ptr(a), _ptr(c), wfmt, bits, group, _ptr(s), _ptr(z),
+                                  _ptr(r_arr), nr, _ptr(c_arr), nc, _ptr(y))
+    if rc != 0:
+        raise ValueError("oracle_mpgemm_lut8 rejected its arguments")
+    return y

@@ -297,3 +297,149 @@ void oracle_token_pow2(int64_t M, int64_t K, const double *a, double *mult)
         mult[m] = ldexp(1.0, e);
     }
 }
+
+/*
+ * INT8 table quantization (Section 3.1.4): an approximation of the FP16-activation
+ * path, so this follows the method's steps in order instead of a closed form.
+ *   1. per token, the power-of-two normalization of the FP16 table path:
+ *      x = a * 2^-e with max |a| = f 2^e, f in [0.5, 1)  (exact);
+ *   2. per group j of 4 activations, the 8-entry half table of Eq. 5 in FP32,
+ *      T[idx] = ((-x0 + (+-x1)) + (+-x2)) + (+-x3)  (bit 2 of idx selects the sign
+ *      of x1, bit 1 of x2, bit 0 of x3: the first activation is the MSB of a
+ *      pattern, and the half table keeps the patterns whose MSB is 0);
+ *   3. each table quantized on its own to INT8: amax = max_idx |T[idx]|,
+ *      q = clamp(rint(T * (127 / amax)), -127, 127), scale = amax / 127 (FP32,
+ *      ties to even; q = 0 and scale = 0 for an all-zero table).  The reading of
+ *      "a unified INT8 precision per table" (the paper fixes neither rounding nor
+ *      scale format).
+ * Outputs q[m][j][8] (int8), scale[m][j] (float32), mult[m] = 2^e (float64).
+ */
+void oracle_lut8_tables(int64_t M, int64_t K, const float *a, int8_t *q, float *scale, double *mult)
+{
+    int64_t J = K / 4;
+    for (int64_t m = 0; m < M; ++m) {
+        float amax = 0.0f;
+        for (int64_t k = 0; k < K; ++k) {
+            float v = fabsf(a[m * K + k]);
+            if (v > amax)
+                amax = v;
+        }
+        int e = 0;
+        if (amax != 0.0f)
+            (void)frexpf(amax, &e);
+        const float down = ldexpf(1.0f, -e);
+        mult[m] = ldexp(1.0, e);
+        for (int64_t j = 0; j < J; ++j) {
+            float x[4], t[8], tmax = 0.0f;
+            for (int i = 0; i < 4; ++i)
+                x[i] = a[m * K + 4 * j + i] * down;
+            for (int idx = 0; idx < 8; ++idx) {
+                float s = -x[0];
+                s = s + ((idx & 4) ? x[1] : -x[1]);
+                s = s + ((idx & 2) ? x[2] : -x[2]);
+                s = s + ((idx & 1) ? x[3] : -x[3]);
+                t[idx] = s;
+                if (fabsf(s) > tmax)
+                    tmax = fabsf(s);
+            }
+            const float inv = tmax == 0.0f ? 0.0f : 127.0f / tmax;
+            for (int idx = 0; idx < 8; ++idx) {
+                float r = rintf(t[idx] * inv);
+                if (r > 127.0f) r = 127.0f;
+                if (r < -127.0f) r = -127.0f;
+                q[(m * J + j) * 8 + idx] = (int8_t)r;
+            }
+            scale[m * J + j] = tmax == 0.0f ? 0.0f : tmax / 127.0f;
+        }
+    }
+}
+
+/*
+ * FP mpGEMM with INT8-quantized tables (Section 3.1.4 on top of Section 3.1):
+ * continues from oracle_lut8_tables with
+ *   4. the lookup of Eq. 4-6: the full table entry of a 4-bit pattern p is
+ *      L(p) = scale * q[p & 7] when its MSB is 0 and -scale * q[~p & 7] when it is 1
+ *      (the negated row of the inverted low bits);
+ *   5. bit-serial weights (Section 3.2.1) with the reinterpretation of Eq. 2: plane b
+ *      of 4 consecutive codes forms the pattern (first code = MSB), every plane uses
+ *      the same table, and y = 2^e sum_q s'_q (sum_{j in q} sum_b 2^b L(p_b) - z'_q S_q)
+ *      (Eq. 3) with s' = s/2, z' = 2z + 1 - 2^b (UINT), s' = s/2, z' = -1 with codes
+ *      q = w + 1 (TERNARY), s' = s, z' = 0 (BINARY), and S_q the sum of x over
+ *      quantization group q; float64 from step 4 on.
+ * Arguments as oracle_mpgemm_f64 plus the bit width `bits`; a is float32 here.
+ */
+int oracle_mpgemm_lut8(int64_t M, int64_t N, int64_t K, const float *a, const void *codes, int wfmt,
+                       int bits, int64_t group, const double *scales, const double *zeros,
+                       const int64_t *rows, int64_t n_rows, const int64_t *cols, int64_t n_cols,
+                       double *y)
+{
+    if (K % 4 != 0 || bits < 1 || bits > 4)
+        return -1;
+    const int64_t G = group ? group : K;
+    if (K % G != 0 || G % 4 != 0)
+        return -1;
+    const int64_t J = K / 4, Q = K / G;
+    const int64_t R = rows ? n_rows : M, C = cols ? n_cols : N;
+    int8_t *q = (int8_t *)malloc((size_t)(M * J * 8));
+    float *sc = (float *)malloc((size_t)(M * J) * sizeof(float));
+    double *mult = (double *)malloc((size_t)M * sizeof(double));
+    double *S = (double *)malloc((size_t)(M * Q) * sizeof(double));
+    if (!q || !sc || !mult || !S) {
+        free(q); free(sc); free(mult); free(S);
+        return -1;
+    }
+    oracle_lut8_tables(M, K, a, q, sc, mult);
+    for (int64_t m = 0; m < M; ++m)
+        for (int64_t g = 0; g < Q; ++g) {
+            double s = 0.0;
+            for (int64_t k = g * G; k < (g + 1) * G; ++k)
+                s += (double)a[m * K + k] / mult[m];
+            S[m * Q + g] = s;
+        }
+#pragma omp parallel for schedule(dynamic, 4)
+    for (int64_t ci = 0; ci < C; ++ci) {
+        const int64_t n = cols ? cols[ci] : ci;
+        for (int64_t ri = 0; ri < R; ++ri) {
+            const int64_t m = rows ? rows[ri] : ri;
+            double total = 0.0;
+            for (int64_t g = 0; g < Q; ++g) {
+                const double s = scales[group ? n * Q + g : 0];
+                double sp, zp;
+                if (wfmt == WFMT_BINARY) {
+                    sp = s;
+                    zp = 0.0;
+                } else if (wfmt == WFMT_TERNARY) {
+                    sp = 0.5 * s;
+                    zp = -1.0;
+                } else {
+                    sp = 0.5 * s;
+                    zp = 2.0 * zeros[group ? n * Q + g : 0] + 1.0 - (double)(1 << bits);
+                }
+                double acc = 0.0;
+                for (int64_t j = g * G / 4; j < (g + 1) * G / 4; ++j) {
+                    int code[4];
+                    for (int i = 0; i < 4; ++i) {
+                        const int64_t idx = n * K + 4 * j + i;
+                        if (wfmt == WFMT_TERNARY)
+                            code[i] = (int)((const int8_t *)codes)[idx] + 1;
+                        else
+                            code[i] = (int)((const uint8_t *)codes)[idx] & ((1 << bits) - 1);
+                    }
+                    const int8_t *qt = q + (m * J + j) * 8;
+                    const double scale = (double)sc[m * J + j];
+                    for (int b = 0; b < bits; ++b) {
+                        int p = 0;
+                        for (int i = 0; i < 4; ++i)
+                            p = (p << 1) | ((code[i] >> b) & 1);
+                        const double L = (p & 8) ? -scale * (double)qt[~p & 7] : scale * (double)qt[p & 7];
+                        acc += (double)(1 << b) * L;
+                    }
+                }
+                total += sp * (acc - zp * S[m * Q + g]);
+            }
+            y[ri * C + ci] = mult[m] * total;
+        }
+    }
+    free(q); free(sc); free(mult); free(S);
+    return 0;
+}

@@ -27,7 +27,7 @@ LIB_PATH = os.path.join(_HERE, "liblutgemm.so")
 # enums of include/lutgemm.h
 SUCCESS, ERROR_INVALID_VALUE, ERROR_NOT_SUPPORTED, ERROR_INSUFFICIENT_SIZE, ERROR_HIP = 0, 1, 2, 3, 4
 WFMT_UINT, WFMT_BINARY, WFMT_TERNARY, WFMT_TERNARY_3IN5 = 0, 1, 2, 3
-ACT_FP16, ACT_INT8 = 0, 1
+ACT_FP16, ACT_INT8, ACT_FP16_LUT8 = 0, 1, 2
 OUT_FP16, OUT_FP32, OUT_INT32 = 0, 1, 2
 
 EXPORTS = [

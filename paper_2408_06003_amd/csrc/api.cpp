@@ -25,7 +25,8 @@ lutgemm_status_t check_problem(const lutgemm_problem_t *p, int64_t M) {
     if (!p) return LUTGEMM_ERROR_INVALID_VALUE;
     if (p->K <= 0 || p->N <= 0 || M <= 0 || p->reserved != 0) return LUTGEMM_ERROR_INVALID_VALUE;
     if (p->wfmt < LUTGEMM_WFMT_UINT || p->wfmt > LUTGEMM_WFMT_TERNARY_3IN5) return LUTGEMM_ERROR_INVALID_VALUE;
-    if (p->act != LUTGEMM_ACT_FP16 && p->act != LUTGEMM_ACT_INT8) return LUTGEMM_ERROR_INVALID_VALUE;
+    if (p->act != LUTGEMM_ACT_FP16 && p->act != LUTGEMM_ACT_INT8 && p->act != LUTGEMM_ACT_FP16_LUT8)
+        return LUTGEMM_ERROR_INVALID_VALUE;
     if (p->scale_fp32 != 0 && p->scale_fp32 != 1) return LUTGEMM_ERROR_INVALID_VALUE;
     if (p->w_bits <= 0 || p->group_size < 0) return LUTGEMM_ERROR_INVALID_VALUE;
     if (p->K > MAX_K || p->N > MAX_N || M > MAX_M) return LUTGEMM_ERROR_NOT_SUPPORTED;
@@ -57,6 +58,7 @@ lutgemm_status_t check_problem(const lutgemm_problem_t *p, int64_t M) {
         break;
     }
     if (p->scale_fp32 && p->group_size != 0) return LUTGEMM_ERROR_NOT_SUPPORTED;
+    if (p->act == LUTGEMM_ACT_FP16_LUT8 && p->wfmt == LUTGEMM_WFMT_TERNARY_3IN5) return LUTGEMM_ERROR_NOT_SUPPORTED;
     if (p->act == LUTGEMM_ACT_INT8) {
         if (p->wfmt == LUTGEMM_WFMT_UINT) return LUTGEMM_ERROR_NOT_SUPPORTED;
         if (p->group_size != 0 && p->group_size != p->K) return LUTGEMM_ERROR_NOT_SUPPORTED;
@@ -198,6 +200,7 @@ static LutParams lut_params(const Layout &L, const LutPlan &plan, int64_t M, con
     TableLayout T = make_table_layout(L, M);
     LutParams lp{};
     lp.T = (const uint4 *)tables;
+    lp.tsc = tables && L.act == LUTGEMM_ACT_FP16_LUT8 ? (const float *)((const char *)tables + T.sc_off) : nullptr;
     lp.S = tables ? (const char *)tables + T.s_off : nullptr;
     lp.tok = tables ? (const float *)((const char *)tables + T.tok_off) : nullptr;
     lp.planes = (const uint4 *)packed;
@@ -251,7 +254,9 @@ struct FusedScratch {
 
 static FusedScratch fused_scratch(const Layout &L, const LutPlan &plan, int64_t M) {
     FusedScratch f{};
-    f.fused = plan.kind == 0 || plan.kind == 3;
+    // INT8 table quantization exists to shrink the tables that travel through HBM, so
+    // that mode always takes the two-call path
+    f.fused = (plan.kind == 0 || plan.kind == 3) && L.act != LUTGEMM_ACT_FP16_LUT8;
     if (f.fused) {
         f.part_off = 0;
         f.tok_off = plan.ws_bytes;
@@ -364,6 +369,7 @@ lutgemm_status_t lutgemm_precompute(const lutgemm_problem_t *problem, int64_t M,
     pp.Q = L.Q;
     pp.G = L.G;
     pp.tri = L.tri ? 1 : 0;
+    pp.tsc = L.act == LUTGEMM_ACT_FP16_LUT8 ? (float *)((char *)tables + T.sc_off) : nullptr;
     return hip_status(launch_precompute(pp, L.act == LUTGEMM_ACT_INT8, stream));
 }
 
@@ -438,7 +444,7 @@ lutgemm_status_t lutgemm_mpgemm_dequant(const lutgemm_problem_t *problem, int64_
                                         int32_t accumulate, void *stream) {
     lutgemm_status_t st = check_problem(problem, M);
     if (st != LUTGEMM_SUCCESS) return st;
-    if (problem->act != LUTGEMM_ACT_FP16 || problem->wfmt == LUTGEMM_WFMT_TERNARY_3IN5)
+    if (problem->act == LUTGEMM_ACT_INT8 || problem->wfmt == LUTGEMM_WFMT_TERNARY_3IN5)
         return LUTGEMM_ERROR_NOT_SUPPORTED;
     if (!act || !packed || !out) return LUTGEMM_ERROR_INVALID_VALUE;
     if (!aligned16(act) || !aligned16(packed) || !aligned16(out)) return LUTGEMM_ERROR_INVALID_VALUE;

@@ -200,17 +200,33 @@ __device__ __forceinline__ uint32_t neg_i16x2(uint32_t x) {
 // Stores quarter qr (entries 4 qr .. 4 qr + 3) of the signed table of group g of
 // the staged block `blk`, from half (qr & 1) of its 8-entry half table (4 FP16 or
 // INT16 values): quarters 0, 1 are T[0..3], T[4..7]; quarters 2, 3 their negation.
-template <bool INT8>
+// INT8-quantized tables (TQ, FP path): h holds the 4 INT8 codes of that half and the
+// table's FP32 scale; the staged entry is round(code x scale x 2^20).
+template <bool INT8, bool TQ = false>
 __device__ __forceinline__ void store_quarter(char *F, int blk, int g, int qr, uint2 h) {
     char *dst = F + blk * Tab<INT8>::BLK + g * Tab<INT8>::G + qr * 4 * Tab<INT8>::E;
     if constexpr (INT8) {
         if (qr >= 2) h = make_uint2(neg_i16x2(h.x), neg_i16x2(h.y));
         *(uint2 *)dst = h;
+    } else if constexpr (TQ) {
+        const float f = __uint_as_float(h.y) * (qr >= 2 ? -(float)(1 << FIX_SHIFT) : (float)(1 << FIX_SHIFT));
+        *(int4 *)dst = make_int4((int)rintf((float)(int8_t)(h.x & 0xFFu) * f),
+                                 (int)rintf((float)(int8_t)((h.x >> 8) & 0xFFu) * f),
+                                 (int)rintf((float)(int8_t)((h.x >> 16) & 0xFFu) * f),
+                                 (int)rintf((float)(int8_t)(h.x >> 24) * f));
     } else {
         const float f = qr >= 2 ? -(float)(1 << FIX_SHIFT) : (float)(1 << FIX_SHIFT);
         *(int4 *)dst = make_int4((int)rintf(h2f(h.x & 0xFFFFu) * f), (int)rintf(h2f(h.x >> 16) * f),
                                  (int)rintf(h2f(h.y & 0xFFFFu) * f), (int)rintf(h2f(h.y >> 16) * f));
     }
+}
+
+// Half `half` (entries 4 half .. + 3) of the half table of table group rg = m J + j:
+// 4 FP16 / INT16 entries, or (TQ) the 4 INT8 codes and the table's scale bits.
+template <bool TQ>
+__device__ __forceinline__ uint2 load_quarter(const LutParams &p, int64_t rg, int half) {
+    if constexpr (TQ) return make_uint2(((const uint32_t *)p.T)[2 * rg + half], __float_as_uint(p.tsc[rg]));
+    return ((const uint2 *)(p.T + rg))[half];
 }
 
 // Reinterpreted scale and zero (Eq. 2) of quantization group q, column n.

@@ -31,7 +31,7 @@
 
 namespace lutgemm {
 
-template <int BITS, int PW, int SW, int TW, int NW, bool INT8>
+template <int BITS, int PW, int SW, int TW, int NW, bool INT8, bool TQ>
 __global__ __launch_bounds__(64 * NW) void lut_gemv2_kernel(LutParams p, int wfmt) {
     constexpr int NT = 64 * NW;            // threads per workgroup
     constexpr int CW = 64 / (PW * SW);    // columns per workgroup
@@ -72,7 +72,7 @@ __global__ __launch_bounds__(64 * NW) void lut_gemv2_kernel(LutParams p, int wfm
 #pragma unroll
         for (int r = 0; r < QPT; ++r) {
             const int e = tid + NT * r, g = e >> 2, gc = g < nkb * GPB ? g : nkb * GPB - 1;
-            tq_[r] = ((const uint2 *)(p.T + m * p.J + kc * GPB + gc))[e & 1];
+            tq_[r] = load_quarter<TQ>(p, m * p.J + kc * GPB + gc, e & 1);
         }
 #pragma unroll
         for (int t = 0; t < TW; ++t) {
@@ -93,7 +93,7 @@ __global__ __launch_bounds__(64 * NW) void lut_gemv2_kernel(LutParams p, int wfm
 #pragma unroll
         for (int r = 0; r < QPT; ++r) {
             const int e = tid + NT * r, g = e >> 2;
-            if (g < nkb * GPB) store_quarter<INT8>(F, g / GPB, g % GPB, e & 3, tq[r]);
+            if (g < nkb * GPB) store_quarter<INT8, TQ>(F, g / GPB, g % GPB, e & 3, tq[r]);
         }
         // epilogue operands of this lane's 128-blocks (unconditional vector loads,
         // issued before the lookups)
@@ -173,7 +173,7 @@ __global__ __launch_bounds__(64 * NW) void lut_gemv2_kernel(LutParams p, int wfm
 // conflicts) and the compile-time table offsets leave one SDWA AND per lookup.
 // With more than one K split the partial sums go to the workspace and
 // lut_finalize_kernel adds them in split order.
-template <int BITS, int KBS, bool INT8>
+template <int BITS, int KBS, bool INT8, bool TQ>
 __global__ __launch_bounds__(256) void lut_gemv_split_kernel(LutParams p, int wfmt) {
     constexpr int QPT = (KBS * GPB * 4 + 255) / 256;  // table quarters per thread
     __shared__ __attribute__((aligned(16))) char F[KBS * Tab<INT8>::BLK];
@@ -196,7 +196,7 @@ __global__ __launch_bounds__(256) void lut_gemv_split_kernel(LutParams p, int wf
 #pragma unroll
     for (int r = 0; r < QPT; ++r) {
         const int e = tid + 256 * r, g = e >> 2, gc = g < nkb * GPB ? g : nkb * GPB - 1;
-        tq[r] = ((const uint2 *)(p.T + m * p.J + kb0 * GPB + gc))[e & 1];
+        tq[r] = load_quarter<TQ>(p, m * p.J + kb0 * GPB + gc, e & 1);
     }
     uint4 w[KBS][BITS];
 #pragma unroll
@@ -217,7 +217,7 @@ __global__ __launch_bounds__(256) void lut_gemv_split_kernel(LutParams p, int wf
     for (int r = 0; r < QPT; ++r) {
         const int e = tid + 256 * r, g = e >> 2;
         if (g < nkb * GPB)
-            store_quarter<INT8>(F, g / GPB, g % GPB, e & 3, tq[r]);
+            store_quarter<INT8, TQ>(F, g / GPB, g % GPB, e & 3, tq[r]);
     }
     lds_barrier();
 
@@ -257,19 +257,19 @@ __global__ __launch_bounds__(256) void lut_gemv_split_kernel(LutParams p, int wf
         p.part[((int64_t)split * p.M + m) * p.N_pad + n] = INT8 ? __int_as_float(yi) : yf;
 }
 
-template <int BITS, bool INT8>
+template <int BITS, bool INT8, bool TQ>
 static void launch_split(const LutParams &p, const Layout &L, const LutPlan &plan, hipStream_t s) {
     const dim3 grid((unsigned)(L.N_pad / NTILE), (unsigned)plan.splits, (unsigned)p.M);
     switch (plan.kbs) {
-    case 1: hipLaunchKernelGGL((lut_gemv_split_kernel<BITS, 1, INT8>), grid, dim3(256), 0, s, p, L.wfmt); break;
-    case 2: hipLaunchKernelGGL((lut_gemv_split_kernel<BITS, 2, INT8>), grid, dim3(256), 0, s, p, L.wfmt); break;
+    case 1: hipLaunchKernelGGL((lut_gemv_split_kernel<BITS, 1, INT8, TQ>), grid, dim3(256), 0, s, p, L.wfmt); break;
+    case 2: hipLaunchKernelGGL((lut_gemv_split_kernel<BITS, 2, INT8, TQ>), grid, dim3(256), 0, s, p, L.wfmt); break;
     case 4:
         if constexpr (BITS <= 2)
-            hipLaunchKernelGGL((lut_gemv_split_kernel<BITS, 4, INT8>), grid, dim3(256), 0, s, p, L.wfmt);
+            hipLaunchKernelGGL((lut_gemv_split_kernel<BITS, 4, INT8, TQ>), grid, dim3(256), 0, s, p, L.wfmt);
         break;
     default:
         if constexpr (BITS == 1)
-            hipLaunchKernelGGL((lut_gemv_split_kernel<BITS, 8, INT8>), grid, dim3(256), 0, s, p, L.wfmt);
+            hipLaunchKernelGGL((lut_gemv_split_kernel<BITS, 8, INT8, TQ>), grid, dim3(256), 0, s, p, L.wfmt);
         break;
     }
 }
@@ -277,16 +277,16 @@ static void launch_split(const LutParams &p, const Layout &L, const LutPlan &pla
 // 16 wavefronts per workgroup, one 128-block per K slice and chunk; 4 or 8 when
 // the whole K range fits one chunk of that many (short K: no idle wavefronts and a
 // shorter cross-wavefront reduction).
-template <int BITS, int PW, int SW, bool INT8>
+template <int BITS, int PW, int SW, bool INT8, bool TQ>
 static void launch_cfg(const LutParams &p, const Layout &L, const LutPlan &plan, hipStream_t s) {
     constexpr int CW = 64 / (PW * SW);
     const dim3 grid((unsigned)((L.N + CW - 1) / CW), (unsigned)plan.splits, (unsigned)p.M);
     if (L.KB <= 4 * SW)
-        hipLaunchKernelGGL((lut_gemv2_kernel<BITS, PW, SW, 1, 4, INT8>), grid, dim3(256), 0, s, p, L.wfmt);
+        hipLaunchKernelGGL((lut_gemv2_kernel<BITS, PW, SW, 1, 4, INT8, TQ>), grid, dim3(256), 0, s, p, L.wfmt);
     else if (L.KB <= 8 * SW)
-        hipLaunchKernelGGL((lut_gemv2_kernel<BITS, PW, SW, 1, 8, INT8>), grid, dim3(512), 0, s, p, L.wfmt);
+        hipLaunchKernelGGL((lut_gemv2_kernel<BITS, PW, SW, 1, 8, INT8, TQ>), grid, dim3(512), 0, s, p, L.wfmt);
     else
-        hipLaunchKernelGGL((lut_gemv2_kernel<BITS, PW, SW, 1, 16, INT8>), grid, dim3(1024), 0, s, p, L.wfmt);
+        hipLaunchKernelGGL((lut_gemv2_kernel<BITS, PW, SW, 1, 16, INT8, TQ>), grid, dim3(1024), 0, s, p, L.wfmt);
 }
 
 // Lane decompositions (PW, SW) offered per bit width, indexed by LutPlan::gemv_cfg
@@ -294,20 +294,20 @@ static void launch_cfg(const LutParams &p, const Layout &L, const LutPlan &plan,
 //   b = 1: 0 -> (1,1) CW=64 CK=16   1 -> (1,2) CW=32 CK=32
 //   b = 2: 0 -> (1,1) CW=64 CK=16   1 -> (2,1) CW=32 CK=16   2 -> (2,2) CW=16 CK=32
 //   b = 4: 0 -> (1,1) CW=64 CK=16   1 -> (2,1) CW=32 CK=16   2 -> (4,1) CW=16 CK=16
-template <bool INT8>
+template <bool INT8, bool TQ>
 static int launch_gemv_bits(const LutParams &p, const Layout &L, const LutPlan &plan, hipStream_t s) {
     if (L.bits == 1) {
-        if (plan.gemv_cfg == 0) launch_cfg<1, 1, 1, INT8>(p, L, plan, s);
-        else launch_cfg<1, 1, 2, INT8>(p, L, plan, s);
+        if (plan.gemv_cfg == 0) launch_cfg<1, 1, 1, INT8, TQ>(p, L, plan, s);
+        else launch_cfg<1, 1, 2, INT8, TQ>(p, L, plan, s);
     } else if (L.bits == 2) {
-        if (plan.gemv_cfg == 0) launch_cfg<2, 1, 1, INT8>(p, L, plan, s);
-        else if (plan.gemv_cfg == 1) launch_cfg<2, 2, 1, INT8>(p, L, plan, s);
-        else launch_cfg<2, 2, 2, INT8>(p, L, plan, s);
+        if (plan.gemv_cfg == 0) launch_cfg<2, 1, 1, INT8, TQ>(p, L, plan, s);
+        else if (plan.gemv_cfg == 1) launch_cfg<2, 2, 1, INT8, TQ>(p, L, plan, s);
+        else launch_cfg<2, 2, 2, INT8, TQ>(p, L, plan, s);
     } else {
         if constexpr (!INT8) {
-            if (plan.gemv_cfg == 0) launch_cfg<4, 1, 1, false>(p, L, plan, s);
-            else if (plan.gemv_cfg == 1) launch_cfg<4, 2, 1, false>(p, L, plan, s);
-            else launch_cfg<4, 4, 1, false>(p, L, plan, s);
+            if (plan.gemv_cfg == 0) launch_cfg<4, 1, 1, false, TQ>(p, L, plan, s);
+            else if (plan.gemv_cfg == 1) launch_cfg<4, 2, 1, false, TQ>(p, L, plan, s);
+            else launch_cfg<4, 4, 1, false, TQ>(p, L, plan, s);
         }
     }
     return (int)hipGetLastError();
@@ -315,15 +315,24 @@ static int launch_gemv_bits(const LutParams &p, const Layout &L, const LutPlan &
 
 int launch_gemv(const LutParams &p, const Layout &L, const LutPlan &plan, void *stream) {
     hipStream_t s = (hipStream_t)stream;
+    const bool i8 = L.act == LUTGEMM_ACT_INT8, tq = L.act == LUTGEMM_ACT_FP16_LUT8;
     if (plan.kind == 2) {
-        const bool i8 = L.act == LUTGEMM_ACT_INT8;
-        if (L.bits == 1) i8 ? launch_split<1, true>(p, L, plan, s) : launch_split<1, false>(p, L, plan, s);
-        else if (L.bits == 2) i8 ? launch_split<2, true>(p, L, plan, s) : launch_split<2, false>(p, L, plan, s);
-        else launch_split<4, false>(p, L, plan, s);
+        if (L.bits == 1) {
+            if (i8) launch_split<1, true, false>(p, L, plan, s);
+            else if (tq) launch_split<1, false, true>(p, L, plan, s);
+            else launch_split<1, false, false>(p, L, plan, s);
+        } else if (L.bits == 2) {
+            if (i8) launch_split<2, true, false>(p, L, plan, s);
+            else if (tq) launch_split<2, false, true>(p, L, plan, s);
+            else launch_split<2, false, false>(p, L, plan, s);
+        } else {
+            if (tq) launch_split<4, false, true>(p, L, plan, s);
+            else launch_split<4, false, false>(p, L, plan, s);
+        }
         return (int)hipGetLastError();
     }
-    return L.act == LUTGEMM_ACT_INT8 ? launch_gemv_bits<true>(p, L, plan, s)
-                                      : launch_gemv_bits<false>(p, L, plan, s);
+    if (i8) return launch_gemv_bits<true, false>(p, L, plan, s);
+    return tq ? launch_gemv_bits<false, true>(p, L, plan, s) : launch_gemv_bits<false, false>(p, L, plan, s);
 }
 
 }  // namespace lutgemm

@@ -25,6 +25,8 @@
 // clamped indices so that waits count exactly), and the LDS tables are
 // double-buffered, so each chunk costs one barrier.  When the grid would not
 // fill the GPU, K is split and lut_finalize_kernel sums the partials.
+#include <type_traits>
+
 #include "lut_common.h"
 
 namespace lutgemm {
@@ -108,7 +110,7 @@ __device__ __forceinline__ Tile tile_of(uint32_t b, uint32_t n_tiles, uint32_t m
     return t;
 }
 
-template <int BITS, bool INT8>
+template <int BITS, bool INT8, bool TQ>
 __global__ __launch_bounds__(256) void lut_mtok_kernel(LutParams p, int wfmt, int64_t n_tiles, int64_t m_tiles,
                                                        int order) {
     constexpr int CH = BITS == 1 ? 2 : 4 / BITS;  // 128-blocks per chunk (more workgroups per CU at b = 1)
@@ -127,7 +129,10 @@ __global__ __launch_bounds__(256) void lut_mtok_kernel(LutParams p, int wfmt, in
     const int64_t kbB = (kbA + p.kbs < p.KB) ? kbA + p.kbs : p.KB;
     const bool need_s = !INT8 && wfmt != LUTGEMM_WFMT_BINARY;
 
-    typedef uint32_t SD[TPL][MTK];
+    // staged table words: entries 2ip, 2ip + 1 of a token's half table (FP16 / INT16
+    // pair), or with INT8-quantized tables (TQ) their two codes and the table's scale
+    typedef std::conditional_t<TQ, uint2, uint32_t> SDE;
+    typedef SDE SD[TPL][MTK];
     typedef uint4 WW[CH][BITS];
     typedef uint2 MW[CH];
     typedef float SV[1];
@@ -142,7 +147,11 @@ __global__ __launch_bounds__(256) void lut_mtok_kernel(LutParams p, int wfmt, in
 #pragma unroll
             for (int t = 0; t < MTK; ++t) {
                 const int64_t row = (m0 + t < p.M) ? m0 + t : p.M - 1;
-                sd[r][t] = ((const uint32_t *)(p.T + row * p.J + (kc + kbc) * GPB + g))[ip];
+                const int64_t rg = row * p.J + (kc + kbc) * GPB + g;
+                if constexpr (TQ)
+                    sd[r][t] = make_uint2(((const uint16_t *)p.T)[4 * rg + ip], __float_as_uint(p.tsc[rg]));
+                else
+                    sd[r][t] = ((const uint32_t *)(p.T + rg))[ip];
             }
         }
 #pragma unroll
@@ -186,7 +195,18 @@ __global__ __launch_bounds__(256) void lut_mtok_kernel(LutParams p, int wfmt, in
             if (task < TASKS && kbl < nkb) {
                 uint32_t v[MTK];
 #pragma unroll
-                for (int t = 0; t < MTK; ++t) v[t] = (m0 + t < p.M) ? sd[r][t] : 0u;
+                for (int t = 0; t < MTK; ++t) {
+                    if constexpr (TQ) {  // code x scale, rounded to FP16
+                        const float sc = __uint_as_float(sd[r][t].y);
+                        const float f0 = (float)(int8_t)(sd[r][t].x & 0xFFu) * sc;
+                        const float f1 = (float)(int8_t)((sd[r][t].x >> 8) & 0xFFu) * sc;
+                        const uint32_t h = (uint32_t)__half_as_ushort(__float2half_rn(f0)) |
+                                           ((uint32_t)__half_as_ushort(__float2half_rn(f1)) << 16);
+                        v[t] = (m0 + t < p.M) ? h : 0u;
+                    } else {
+                        v[t] = (m0 + t < p.M) ? sd[r][t] : 0u;
+                    }
+                }
                 uint4 e0, e1;  // entries 2ip (low halves) and 2ip + 1 (high halves), tokens 0..7
                 e0.x = perm(v[1], v[0], 0x05040100u);
                 e0.y = perm(v[3], v[2], 0x05040100u);
@@ -313,14 +333,18 @@ int launch_mtok(const LutParams &p, const Layout &L, const LutPlan &plan, void *
     const bool i8 = L.act == LUTGEMM_ACT_INT8;
     const int64_t nt = plan.n_tiles, mt = plan.m_tiles;
     const int o = plan.order;
+    const bool tq = L.act == LUTGEMM_ACT_FP16_LUT8;
     if (L.bits == 1) {
-        if (i8) hipLaunchKernelGGL((lut_mtok_kernel<1, true>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
-        else hipLaunchKernelGGL((lut_mtok_kernel<1, false>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
+        if (i8) hipLaunchKernelGGL((lut_mtok_kernel<1, true, false>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
+        else if (tq) hipLaunchKernelGGL((lut_mtok_kernel<1, false, true>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
+        else hipLaunchKernelGGL((lut_mtok_kernel<1, false, false>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
     } else if (L.bits == 2) {
-        if (i8) hipLaunchKernelGGL((lut_mtok_kernel<2, true>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
-        else hipLaunchKernelGGL((lut_mtok_kernel<2, false>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
+        if (i8) hipLaunchKernelGGL((lut_mtok_kernel<2, true, false>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
+        else if (tq) hipLaunchKernelGGL((lut_mtok_kernel<2, false, true>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
+        else hipLaunchKernelGGL((lut_mtok_kernel<2, false, false>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
     } else {
-        hipLaunchKernelGGL((lut_mtok_kernel<4, false>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
+        if (tq) hipLaunchKernelGGL((lut_mtok_kernel<4, false, true>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
+        else hipLaunchKernelGGL((lut_mtok_kernel<4, false, false>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
     }
     return (int)hipGetLastError();
 }

@@ -85,13 +85,20 @@ inline Layout make_layout(const lutgemm_problem_t &p) {
 }
 
 struct TableLayout {
-    size_t t_bytes, s_off, tok_off, total;
+    size_t t_bytes, sc_off, s_off, tok_off, total;  // sc_off: INT8-quantized tables' scales
 };
 
 inline TableLayout make_table_layout(const Layout &L, int64_t M) {
     TableLayout T{};
-    T.t_bytes = (size_t)M * L.J * (L.tri ? 2 * TENT : 16);
-    T.s_off = align256(T.t_bytes);
+    if (L.act == LUTGEMM_ACT_FP16_LUT8) {  // [M][J] x 8 INT8 codes, then [M][J] FP32 scales
+        T.t_bytes = (size_t)M * L.J * 8;
+        T.sc_off = align256(T.t_bytes);
+        T.s_off = align256(T.sc_off + (size_t)M * L.J * 4);
+    } else {
+        T.t_bytes = (size_t)M * L.J * (L.tri ? 2 * TENT : 16);
+        T.sc_off = 0;
+        T.s_off = align256(T.t_bytes);
+    }
     T.tok_off = align256(T.s_off + (size_t)M * L.Q * 4);
     T.total = align256(T.tok_off + (size_t)M * 4);
     return T;
@@ -133,10 +140,12 @@ struct PrecomputeParams {
     float *tok;            // [M]
     int64_t M, K, J, Q, G;
     int tri;               // ternary 3-in-5 tables: [M][J triples] x 16 entries, no S
+    float *tsc;            // INT8 table quantization: per-table scales [M][J] (T holds [M][J] x 8 INT8)
 };
 
 struct LutParams {
-    const uint4 *T;        // half tables
+    const uint4 *T;        // half tables (INT8 table quantization: [M][J] x 8 INT8 codes)
+    const float *tsc;      // INT8 table quantization: per-table scales [M][J], else NULL
     const void *S;         // group sums
     const float *tok;      // per-token factor (NULL in the fused kernel, which computes it)
     const uint16_t *act;   // FP16 [M][K]: activations of the fused kernel

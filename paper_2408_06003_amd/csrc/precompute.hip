@@ -14,6 +14,10 @@
 //      T[m][j][i] = -x_0 + sum_{e=1..3} (bit (3-e) of i ? x_e : -x_e), the entry of
 //      pattern 0 i of the full 16-entry table (Eq. 5); the other half is its
 //      negation (Eq. 4) and is never stored.
+//      INT8 table quantization (Section 3.1.4, `tsc` set): each half table is
+//      stored as 8 INT8 codes clamp(rint(T * (127 / amax)), -127, 127) with
+//      amax = max |T| (FP32, the entries as computed above) and its scale
+//      amax / 127 in FP32.
 //   3. S[m][q] = sum of x over quantization group q (zero-point term of Eq. 3):
 //      groups of 128..1024 activations are reduced across the lanes that built
 //      them; larger ones are summed by the workgroup that holds their first
@@ -169,16 +173,34 @@ __global__ __launch_bounds__(256) void precompute_kernel(PrecomputeParams p) {
         const float x2 = token_value<INT8>(h2f(v.y & 0xFFFFu), scale);
         const float x3 = token_value<INT8>(h2f(v.y >> 16), scale);
         uint32_t e[8];
+        float tf[8];
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
             const float t = ((-x0 + ((i & 4) ? x1 : -x1)) + ((i & 2) ? x2 : -x2)) + ((i & 1) ? x3 : -x3);
+            tf[i] = t;
             if (INT8)
                 e[i] = (uint32_t)(uint16_t)(int16_t)(int)t;  // |t| <= 508, exact
             else
                 e[i] = (uint32_t)__half_as_ushort(__float2half_rn(t));
         }
-        p.T[m * p.J + j] = make_uint4(e[0] | (e[1] << 16), e[2] | (e[3] << 16), e[4] | (e[5] << 16),
-                                      e[6] | (e[7] << 16));
+        if (!INT8 && p.tsc) {
+            // INT8 table quantization (Section 3.1.4), one scale per table, FP32
+            float tmax = 0.f;
+#pragma unroll
+            for (int i = 0; i < 8; ++i) tmax = fmaxf(tmax, fabsf(tf[i]));
+            const float inv = tmax == 0.f ? 0.f : __fdiv_rn(127.0f, tmax);
+            uint32_t c[2] = {0u, 0u};
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                const float r = fminf(fmaxf(rintf(tf[i] * inv), -127.f), 127.f);
+                c[i >> 2] |= ((uint32_t)(int)r & 0xFFu) << (8 * (i & 3));
+            }
+            ((uint2 *)p.T)[m * p.J + j] = make_uint2(c[0], c[1]);
+            p.tsc[m * p.J + j] = tmax == 0.f ? 0.f : __fdiv_rn(tmax, 127.0f);
+        } else {
+            p.T[m * p.J + j] = make_uint4(e[0] | (e[1] << 16), e[2] | (e[3] << 16), e[4] | (e[5] << 16),
+                                          e[6] | (e[7] << 16));
+        }
         g4f = ((x0 + x1) + x2) + x3;
         g4i = (int)x0 + (int)x1 + (int)x2 + (int)x3;
     }

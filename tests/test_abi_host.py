@@ -59,6 +59,10 @@ def test_problem_struct_layout():
     (4096, 4096, 2, L.WFMT_TERNARY_3IN5, 0, L.ACT_FP16, False, L.SUCCESS),
     (11008, 300, 2, L.WFMT_TERNARY_3IN5, 11008, L.ACT_FP16, False, L.SUCCESS),
     (1024, 64, 2, L.WFMT_TERNARY_3IN5, 128, L.ACT_FP16, False, L.ERROR_NOT_SUPPORTED),  # 3-in-5: G = 0 or K
+    (4096, 4096, 4, L.WFMT_UINT, 128, L.ACT_FP16_LUT8, False, L.SUCCESS),
+    (8192, 1000, 1, L.WFMT_BINARY, 8192, L.ACT_FP16_LUT8, False, L.SUCCESS),
+    (4096, 64, 2, L.WFMT_TERNARY, 0, L.ACT_FP16_LUT8, True, L.SUCCESS),
+    (4096, 64, 2, L.WFMT_TERNARY_3IN5, 0, L.ACT_FP16_LUT8, True, L.ERROR_NOT_SUPPORTED),  # no 3-in-5 LUT8
     (1024, 64, 1, L.WFMT_TERNARY_3IN5, 0, L.ACT_FP16, False, L.ERROR_NOT_SUPPORTED),    # 3-in-5 is ternary
     (0, 64, 2, L.WFMT_UINT, 0, L.ACT_FP16, False, L.ERROR_INVALID_VALUE),
     (1024, 0, 2, L.WFMT_UINT, 0, L.ACT_FP16, False, L.ERROR_INVALID_VALUE),
@@ -117,6 +121,20 @@ def test_size_formulas_ternary_3in5():
     big = L.problem(1024, 1 << 16, 2, L.WFMT_TERNARY_3IN5, 0, L.ACT_FP16)
     assert L.validate(big, 4095) == L.SUCCESS
     assert L.validate(big, 4096) == L.ERROR_NOT_SUPPORTED
+
+
+def test_size_formulas_int8_table_quantization():
+    """INT8 table quantization (Section 3.1.4): 8 one-byte codes and one FP32 scale per 4
+    activations and token, i.e. 12 bytes against 16 for FP16 tables."""
+    M, K, N = 5, 4096, 300
+    p = L.problem(K, N, 2, L.WFMT_UINT, 128, L.ACT_FP16_LUT8)
+    q = L.problem(K, N, 2, L.WFMT_UINT, 128, L.ACT_FP16)
+    s_off, t_off = L.table_offsets(p, M)
+    assert s_off >= M * (K // 4) * 12 and s_off % 256 == 0
+    assert s_off < L.table_offsets(q, M)[0]
+    assert t_off >= s_off + M * (K // 128) * 4
+    assert L.table_size(p, M) < L.table_size(q, M)
+    assert L.packed_weight_size(p) == L.packed_weight_size(q)
 
 
 def test_entry_points_reject_before_launch():

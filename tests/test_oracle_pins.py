@@ -344,3 +344,76 @@ def test_reference_output_int8_path():
     assert np.array_equal(acc, ref)
     yy = (acc.astype(np.float32) * sa[0]) * inp.scales.astype(np.float32)[0]
     assert np.array_equal(y, yy.astype(np.float32))
+
+
+# ----------------------------------------------------------------- INT8 table quantization (Section 3.1.4)
+
+def _exact_table_activations(M, K, rng):
+    """Integer activations whose groups of 4 have |a0| + |a1| + |a2| + |a3| = 127: the
+    largest half-table entry of every group is then 127 times the token's power-of-two
+    unit, so INT8 table quantization is lossless."""
+    a = np.zeros((M, K))
+    for m in range(M):
+        for j in range(K // 4):
+            cut = np.sort(rng.integers(0, 128, size=3))
+            parts = np.diff(np.concatenate([[0], cut, [127]]))
+            a[m, 4 * j:4 * j + 4] = parts * rng.choice([-1.0, 1.0], size=4)
+    return a.astype(np.float16)
+
+
+@pytest.mark.parametrize("wfmt,bits,group", [(W.WFMT_UINT, 2, 128), (W.WFMT_UINT, 4, 256),
+                                             (W.WFMT_BINARY, 1, 512), (W.WFMT_TERNARY, 2, 0)])
+def test_lut8_lossless_tables_reduce_to_the_exact_product(wfmt, bits, group):
+    """When every table is exactly representable in INT8 the table-quantized oracle must
+    give the dense result: this pins its lookup (Eq. 4-6 sign handling), bit-serial
+    planes, reinterpretation and zero-point term against the plain definition."""
+    rng = np.random.default_rng(31)
+    inp = W.make_custom(wfmt, bits, group, W.ACT_FP16, 3, 512, 40, seed=5)
+    inp.act = _exact_table_activations(3, 512, rng)
+    y = oracle.reference_output(inp)
+    y8 = oracle.mpgemm_lut8(inp.act, inp.codes, wfmt, bits, group, inp.scales, inp.zeros)
+    assert np.allclose(y8, y, rtol=1e-12, atol=1e-9 * np.abs(y).max())
+    q, sc, mult = oracle.lut8_tables(inp.act)
+    assert np.all(np.abs(q).max(axis=2) == 127)  # every table uses the full INT8 range
+
+
+def test_lut8_table_codes_within_half_a_step():
+    """Each quantized entry is within half a quantization step of the table it
+    approximates (the half tables of the precompute, Eq. 5, of the normalized token)."""
+    inp = W.make_custom(W.WFMT_UINT, 2, 128, W.ACT_FP16, 4, 1024, 8, seed=6)
+    q, sc, mult = oracle.lut8_tables(inp.act)
+    x = inp.act.astype(np.float64) / mult[:, None]
+    T = oracle.half_tables(x)
+    err = np.abs(q.astype(np.float64) * sc[:, :, None] - T)
+    assert np.all(err <= sc[:, :, None] * (0.5 + 1e-5) + 1e-6)
+    assert np.all((np.abs(q) <= 127))
+    assert np.all(np.abs(q).max(axis=2) == 127)
+
+
+@pytest.mark.parametrize("wfmt,bits,group", [(W.WFMT_UINT, 2, 128), (W.WFMT_UINT, 4, 128),
+                                             (W.WFMT_BINARY, 1, 2048), (W.WFMT_TERNARY, 2, 0)])
+def test_lut8_error_bound_and_symmetry(wfmt, bits, group):
+    """Against the exact product: within the bound implied by half a step per entry
+    (|T| < 4 for the normalized token, so each table step is below 4/127), and a real
+    approximation (not exact).  Negating the activations negates the result exactly."""
+    inp = W.make_custom(wfmt, bits, group, W.ACT_FP16, 3, 2048, 96, seed=7)
+    y = oracle.reference_output(inp)
+    y8 = oracle.reference_output(_as_lut8(inp))
+    G = group or 2048
+    s = np.asarray(inp.scales, dtype=np.float64).reshape(-1)
+    smax = np.abs(s).max() * (1.0 if wfmt == W.WFMT_BINARY else 0.5)
+    mult = oracle.token_pow2(inp.act)
+    bound = mult[:, None] * (2048 // G) * smax * (G // 4) * ((1 << bits) - 1) * (2.0 / 127.0)
+    assert np.all(np.abs(y8 - y) <= bound)
+    rel = np.linalg.norm(y8 - y) / np.linalg.norm(y)
+    assert 1e-4 < rel < 1e-2
+    neg = _as_lut8(inp)
+    neg.act = (-inp.act.astype(np.float32)).astype(np.float16)
+    assert np.array_equal(oracle.reference_output(neg), -y8)
+
+
+def _as_lut8(inp):
+    import copy
+    out = copy.copy(inp)
+    out.act_kind = W.ACT_FP16_LUT8
+    return out

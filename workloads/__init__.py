@@ -29,6 +29,7 @@ WFMT_TERNARY = 2   # int8 w in {-1, 0, +1}, real weight r = s * w
 
 ACT_FP16 = 0
 ACT_INT8 = 1
+ACT_FP16_LUT8 = 2   # FP16 activations, tables quantized to INT8 per table (same draws as ACT_FP16)
 
 
 @dataclass(frozen=True)
