@@ -62,13 +62,15 @@ def parse():
     return ap.parse_args()
 
 
-def algorithmic_bytes(inp, out_bytes, fused=False, tri=False):
+def algorithmic_bytes(inp, out_bytes, fused=False, tri=False, lut8=False):
     """Bytes the method must move for one mpGEMM call: weights N K b / 8, metadata
     (FP16 scale + zero per group: 4 B; per-channel scale: 2 B; per-tensor: 4 B),
     tables 4 M K (8 two-byte entries per 4 activations) -- or, for the fused
     kernel, the FP16 activations 2 M K instead -- and the output M N out_bytes.
     Ternary 3-in-5 (``tri``): weights 5 bits per 3 weights, N K 5 / 24 (K padded to
-    whole 96-weight blocks), and tables of 16 two-byte entries per 3 activations."""
+    whole 96-weight blocks), and tables of 16 two-byte entries per 3 activations.
+    INT8 table quantization (``lut8``): tables of 8 one-byte codes and one FP32 scale
+    per 4 activations, 3 M K."""
     M, K, N, b = inp.M, inp.K, inp.N, inp.bits
     weights = N * K * b // 8
     if tri:
@@ -79,7 +81,7 @@ def algorithmic_bytes(inp, out_bytes, fused=False, tri=False):
         meta = 2 * N * (K // inp.group)
     else:
         meta = 4 * N * (K // inp.group)
-    tables = 2 * M * K if fused else (M * (-(-K // 96)) * 32 * 32 if tri else 4 * M * K)
+    tables = 2 * M * K if fused else (M * (-(-K // 96)) * 32 * 32 if tri else (3 if lut8 else 4) * M * K)
     out = M * N * out_bytes
     return {"weights": weights, "meta": meta, "tables": tables, "out": out,
             "total": weights + meta + tables + out}
@@ -115,8 +117,9 @@ def load_traffic(workload, kernel):
 class Case:
     """One workload shape on the device, with a rotation set of packed weights."""
 
-    def __init__(self, cid, sid, M, rotate=True, wfmt=None):
-        """``wfmt`` overrides the packing of the same codes (the ternary 3-in-5 format)."""
+    def __init__(self, cid, sid, M, rotate=True, wfmt=None, act=None):
+        """``wfmt`` overrides the packing of the same codes (the ternary 3-in-5 format),
+        ``act`` the table precision of the same FP16 activations (INT8 table quantization)."""
         import torch
         import paper_2408_06003_amd as L
         import workloads as W
@@ -127,6 +130,10 @@ class Case:
         if self.tri:
             self.name += "_3in5"
         self.inp = W.make_inputs(cid, sid, M=M)
+        self.lut8 = act == W.ACT_FP16_LUT8
+        if self.lut8:
+            self.inp.act_kind = act
+            self.name += "_lut8"
         inp = self.inp
         self.M, self.K, self.N = inp.M, inp.K, inp.N
         self.p = L.problem(inp.K, inp.N, inp.bits, inp.wfmt if wfmt is None else wfmt, inp.group,
@@ -227,7 +234,7 @@ class Case:
         self.precompute()
         ms_mp = self.timed(self.mpgemm, n_kernel, check=lambda: self.out)
         ms_pre = self.timed(lambda i: self.precompute(), n_kernel)
-        b = algorithmic_bytes(self.inp, self.out_bytes, tri=self.tri)
+        b = algorithmic_bytes(self.inp, self.out_bytes, tri=self.tri, lut8=self.lut8)
         gbps = b["total"] / (ms_mp * 1e-3) / 1e9
         # achievable streaming read of the same byte count, same rotation and timing
         sink = self.torch.zeros(4096, dtype=self.torch.int32, device="cuda")
@@ -245,7 +252,7 @@ class Case:
                "precompute_over_mpgemm": round(ms_pre / ms_mp, 4),
                "fused_us": round(ms_fu * 1e3, 3), "fused_tops": round(self.effective_tops(ms_fu), 3),
                "algorithmic_bytes": b["total"], "rotation_copies": len(self.packed)}
-        if self.M >= 16 and not self.int8 and not self.tri:
+        if self.M >= 16 and not self.int8 and not self.tri and not self.lut8:
             out = self.torch.empty((self.M, self.N), dtype=self.torch.float16, device="cuda")
             for i in range(3):
                 self.dequant(i, out)
@@ -385,6 +392,16 @@ def main():
             c = Case(2, 0, 1, wfmt=L.WFMT_TERNARY_3IN5)
             recs.append(c.measure(200, 3))
             log(f"{c.name}: mpgemm {recs[-1]['mpgemm_us']} us, fused {recs[-1]['fused_us']} us")
+            c.release()
+            del c
+        # INT8 table quantization on a decode shape and on the prefill shape
+        for cid, sid, M in ((3, 1, 1), (4, 0, 4096)):
+            c = Case(cid, sid, M, act=W.ACT_FP16_LUT8)
+            if args.only and c.name != args.only:
+                c.release()
+                continue
+            recs.append(c.measure(200 if M == 1 else 5, 3))
+            log(f"{c.name}: mpgemm {recs[-1]['mpgemm_us']} us, precompute {recs[-1]['precompute_us']} us")
             c.release()
             del c
         for cid, w in W.WORKLOADS.items():
