@@ -314,8 +314,8 @@ def calibrate_copy():
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py: --gpus {args.gpus} is not supported: this build runs the LUT mpGEMM hot path on "
-              "one GPU (how it would shard across GPUs is described in DESIGN.md)", file=sys.stderr)
+        print(f"bench.py: --gpus {args.gpus} is not supported: the LUT mpGEMM hot path runs on one GPU "
+              "(sharding along N across GPUs is designed, not implemented)", file=sys.stderr)
         sys.exit(2)
     import torch
     import paper_2408_06003_amd as L  # fails loudly if the HIP library is not built
