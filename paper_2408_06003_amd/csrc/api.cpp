@@ -143,18 +143,28 @@ LutPlan plan_lut(const Layout &L, int64_t M) {
         P.kbs = (int)kbs;
         P.splits = (int)((L.KB + kbs - 1) / kbs);
     } else if (kind == 2) {
-        // split-K GEMV: 256 columns per workgroup, KBS 128-blocks each: four weight words
-        // per lane, halved while the grid has fewer than `2 * target` workgroups
+        // split-K GEMV: 256 columns per workgroup, KBS 128-blocks each.  Start from four
+        // weight words per lane; double KBS while there are more splits than the
+        // finalize kernel sums in one batch of loads; then halve it while the grid stays
+        // within 16 x `target` workgroups and the splits within that batch (measured on
+        // the LLaMA-shaped decode layers: 1-bit 8192 x 28672 takes KBS 2, 28672 x 8192
+        // KBS 4, 4-bit 11008 x 4096 KBS 2)
         P.kind = 2;
         P.mt = 1;
         P.m_tiles = M;
         P.n_tiles = L.N_pad / NTILE;
+        const int kmax = 8 / L.bits;
+        auto n_splits = [&](int k) { return (L.KB + k - 1) / k; };
         int kbs = L.bits == 4 ? 1 : 4 / L.bits;
         const int forced = env_int("LUTGEMM_KBS", 0);
-        if (forced == 1 || forced == 2 || forced == 4 || forced == 8)
-            kbs = forced > 8 / L.bits ? 8 / L.bits : forced;
-        else
-            while (kbs > 1 && P.n_tiles * M * ((L.KB + kbs - 1) / kbs) < 2 * target) kbs >>= 1;
+        if (forced == 1 || forced == 2 || forced == 4 || forced == 8) {
+            kbs = forced > kmax ? kmax : forced;
+        } else {
+            while (kbs < kmax && n_splits(kbs) > FIN_BATCH) kbs <<= 1;
+            while (kbs > 1 && n_splits(kbs / 2) <= FIN_BATCH &&
+                   P.n_tiles * M * n_splits(kbs / 2) <= 16 * target)
+                kbs >>= 1;
+        }
         P.kbs = kbs;
         P.splits = (int)((L.KB + kbs - 1) / kbs);
     } else {

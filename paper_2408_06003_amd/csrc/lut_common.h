@@ -347,26 +347,32 @@ __device__ __forceinline__ void store_out(const LutParams &p, int wfmt, int64_t 
         ((__half *)p.out)[o] = __float2half_rn(v);
 }
 
-// Sum of the partials of row m, column n over all splits, in split order.  Loads
-// are issued 32 at a time so that one memory latency covers up to 32 splits.
-template <bool INT8>
-__device__ __forceinline__ void sum_partials(const LutParams &p, int64_t m_alloc, int64_t m, int64_t n,
-                                             float &sf, int &si) {
-    sf = 0.f;
-    si = 0;
+// Partial sums of row m, column n for splits s0 .. s0 + PB - 1 (indices past the
+// last split clamped to it).  Unconditional loads, so all PB are in flight before
+// the first is used (a load under a condition makes the compiler wait for it
+// before issuing the next one).
+constexpr int PB = FIN_BATCH;
+__device__ __forceinline__ void load_partials(const LutParams &p, int64_t m_alloc, int64_t m, int64_t n, int s0,
+                                              float (&v)[PB]) {
     const float *src = p.part + m * p.N_pad + n;
     const int64_t stride = m_alloc * p.N_pad;
-    for (int s0 = 0; s0 < p.splits; s0 += 32) {
-        float v[32];
 #pragma unroll
-        for (int j = 0; j < 32; ++j) v[j] = (s0 + j < p.splits) ? src[(int64_t)(s0 + j) * stride] : 0.f;
+    for (int j = 0; j < PB; ++j) {
+        const int sp = (s0 + j < p.splits) ? s0 + j : p.splits - 1;
+        v[j] = src[(int64_t)sp * stride];
+    }
+}
+
+// Adds the loaded partials of splits s0 .. in split order.
+template <bool INT8>
+__device__ __forceinline__ void add_partials(const LutParams &p, int s0, const float (&v)[PB], float &sf, int &si) {
 #pragma unroll
-        for (int j = 0; j < 32; ++j) {
-            if (INT8)
-                si += __float_as_int(v[j]);
-            else
-                sf += v[j];
-        }
+    for (int j = 0; j < PB; ++j) {
+        const bool in = s0 + j < p.splits;
+        if (INT8)
+            si += in ? __float_as_int(v[j]) : 0;
+        else
+            sf += in ? v[j] : 0.f;
     }
 }
 

@@ -16,16 +16,27 @@ namespace lutgemm {
 
 // Sums the split partials of output (m, n) in split order and applies the output
 // epilogue.  Runs after the LUT kernel on the same stream, so the kernel boundary
-// makes every partial visible without fences inside the LUT kernel.
+// makes every partial visible without fences inside the LUT kernel.  (Completing
+// the sum inside the LUT kernel instead, by its last workgroup per column tile,
+// needs a device-scope release per workgroup, i.e. an L2 write-back; measured on
+// MI355X that costs far more than this launch.)  The first PB partials are
+// requested before the epilogue operands, so the kernel waits about one memory
+// latency for up to PB splits.
 template <bool INT8>
 __global__ __launch_bounds__(64) void lut_finalize_kernel(LutParams p, int wfmt, int per_tensor_i,
                                                           int64_t m_alloc) {
     const int64_t n = (int64_t)blockIdx.x * 64 + threadIdx.x;
     const int64_t m = blockIdx.y;
+    float v[PB];
+    load_partials(p, m_alloc, m, n, 0, v);
     const Epi ep = load_epi<INT8>(p, wfmt, m, n, false);
-    float sf;
-    int si;
-    sum_partials<INT8>(p, m_alloc, m, n, sf, si);
+    float sf = 0.f;
+    int si = 0;
+    add_partials<INT8>(p, 0, v, sf, si);
+    for (int s0 = PB; s0 < p.splits; s0 += PB) {
+        load_partials(p, m_alloc, m, n, s0, v);
+        add_partials<INT8>(p, s0, v, sf, si);
+    }
     store_out<INT8>(p, wfmt, m, n, sf, si, ep);
 }
 

@@ -40,6 +40,7 @@ constexpr int KBLK = 128;       // activations covered by one packed plane word
 constexpr int GPB = 32;         // 4-activation table groups per plane word
 constexpr int NTILE = 256;      // columns per workgroup (one column per lane)
 constexpr int FIX_SHIFT = 20;   // fixed-point fraction bits of FP table entries staged in LDS
+constexpr int FIN_BATCH = 64;   // split partial sums the finalize kernel requests at once per output
 constexpr int TBLK = 96;        // activations per 3-in-5 block (32 triples)
 constexpr int TPB = 32;         // triples per 3-in-5 block
 constexpr int TENT = 16;        // stored entries per triple table (14 used, 2 zero)
