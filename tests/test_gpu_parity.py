@@ -226,3 +226,17 @@ def test_extreme_scales():
     ref = oracle.reference_output(inp)
     y = GpuProblem(inp).lut(out_dtype=torch.float32).cpu().numpy()
     assert_fp_close(y, ref, "extreme scales")
+
+
+# ----------------------------------------------------------------- large-M comparison kernel
+
+@pytest.mark.parametrize("cid,M,K,N", [(4, 300, 1024, 520), (3, 257, 2048, 300), (5, 280, 1024, 600),
+                                       (6, 512, 1024, 256)])
+def test_dequant_big_tile_parity(cid, M, K, N, monkeypatch):
+    """The 256 x 256 pipelined dequantization + MFMA kernel (chosen for large M) on
+    small shapes with ragged M and N tails, every output against the oracle."""
+    monkeypatch.setenv("LUTGEMM_DEQUANT_BIG", "1")
+    banner(f"dequant 256x256 tile config={cid} M={M} K={K} N={N}")
+    gp = GpuProblem(W.make_inputs(cid, 0, M=M, K=K, N=N))
+    check_fp_path(gp, dequant=True, what=f"dequant big config {cid}")
+    check_fp_path(gp, dequant=True, out_dtype=torch.float32, what=f"dequant big config {cid} fp32 out")
