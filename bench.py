@@ -59,6 +59,15 @@ def parse():
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a plain 256 MiB device copy (counter calibration)")
+    ap.add_argument("--summarize-trace", metavar="DIR", default=None,
+                    help="print the summary of a rocprofv3 --kernel-trace --stats output directory (no GPU)")
+    ap.add_argument("--summarize-traffic", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"), default=None,
+                    help="print HBM traffic records from two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE; no GPU)")
+    ap.add_argument("--summarize-counters", metavar="DIR", nargs="+", default=None,
+                    help="print per-kernel utilization from rocprofv3 --pmc runs (no GPU)")
+    ap.add_argument("--command", default="", help="the profiling command, recorded in a summary")
+    ap.add_argument("--bench-logs", nargs="*", default=[],
+                    help="bench.py outputs (JSON line last) whose headline launch times a trace summary quotes")
     return ap.parse_args()
 
 
@@ -114,6 +123,14 @@ def load_traffic(workload, kernel):
     return None
 
 
+def case_name(cid, sid, M, tri=False, lut8=False):
+    """Name of one workload shape in the bench output."""
+    import workloads as W
+    w = W.WORKLOADS[cid]
+    name = w.name if len(w.kn) == 1 and len(w.ms) == 1 else f"{w.name}_M{M}_K{w.kn[sid][0]}_N{w.kn[sid][1]}"
+    return name + ("_3in5" if tri else "") + ("_lut8" if lut8 else "")
+
+
 class Case:
     """One workload shape on the device, with a rotation set of packed weights."""
 
@@ -124,16 +141,12 @@ class Case:
         import paper_2408_06003_amd as L
         import workloads as W
         self.torch, self.L, self.W = torch, L, W
-        w = W.WORKLOADS[cid]
-        self.name = w.name if len(w.kn) == 1 and len(w.ms) == 1 else f"{w.name}_M{M}_K{w.kn[sid][0]}_N{w.kn[sid][1]}"
         self.tri = wfmt == L.WFMT_TERNARY_3IN5
-        if self.tri:
-            self.name += "_3in5"
-        self.inp = W.make_inputs(cid, sid, M=M)
         self.lut8 = act == W.ACT_FP16_LUT8
+        self.name = case_name(cid, sid, M, self.tri, self.lut8)
+        self.inp = W.make_inputs(cid, sid, M=M)
         if self.lut8:
             self.inp.act_kind = act
-            self.name += "_lut8"
         inp = self.inp
         self.M, self.K, self.N = inp.M, inp.K, inp.N
         self.p = L.problem(inp.K, inp.N, inp.bits, inp.wfmt if wfmt is None else wfmt, inp.group,
@@ -311,8 +324,190 @@ def calibrate_copy():
             "gbps": round(2 * n / (ms * 1e-3) / 1e9, 1)}
 
 
+# ---------------------------------------------------------------- rocprofv3 summaries (CPU only)
+
+HEADLINE_KERNELS = {
+    # kind in KERNEL_SOURCES -> name prefix of the kernel the headline step launches
+    "fused": "void lutgemm::lut_fused_gemv_kernel<2, 2, 2, 1, 16, true>",
+    "mpgemm": "void lutgemm::lut_gemv2_kernel<2, 2, 2, 1, 16, true, false>",
+}
+COPY_KERNEL = "__amd_rocclr_copyBuffer"
+
+
+def _csv_rows(directory, suffix):
+    import csv
+    import glob
+    rows = []
+    for path in sorted(glob.glob(os.path.join(directory, "**", "*" + suffix), recursive=True)):
+        with open(path, newline="") as f:
+            rows.extend(csv.DictReader(f))
+    return rows
+
+
+def _short(name, n=78):
+    return name if len(name) <= n else name[:n - 3] + "..."
+
+
+def summarize_trace(directory, command="", bench_logs=()):
+    """Per-kernel durations of a rocprofv3 kernel-trace run, and the headline kernels'
+    durations over their back-to-back runs (the bench's graph replays)."""
+    import statistics
+    stats = _csv_rows(directory, "kernel_stats.csv")
+    trace = _csv_rows(directory, "kernel_trace.csv")
+    out = ["# rocprofv3 kernel-trace summary", "", "command (on the MI355X, from /tmp with TMPDIR=/tmp):",
+           f"  {command}", "",
+           "Average/min/max kernel durations in microseconds over all dispatches of the run",
+           "(kernel start to end; the bench's per-launch times, measured with HIP events over",
+           "graph replays, also include the gap between back-to-back kernels).", "",
+           f"{'kernel':78s} {'calls':>7s} {'avg_us':>9s} {'min_us':>9s} {'max_us':>9s} {'%time':>6s}"]
+    stats.sort(key=lambda r: -float(r["TotalDurationNs"]))
+    for r in stats:
+        out.append(f"{_short(r['Name']):78s} {int(r['Calls']):7d} {float(r['AverageNs']) / 1e3:9.2f} "
+                   f"{float(r['MinNs']) / 1e3:9.2f} {float(r['MaxNs']) / 1e3:9.2f} {float(r['Percentage']):6.2f}")
+    trace.sort(key=lambda r: int(r["Start_Timestamp"]))
+    out += ["", "Headline kernels in runs of >= 100 back-to-back dispatches (the timed graph replays):"]
+    for kind, prefix in HEADLINE_KERNELS.items():
+        runs, cur = [], []
+        for r in trace:
+            if r["Kernel_Name"].startswith(prefix):
+                cur.append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
+            elif cur:
+                runs.append(cur)
+                cur = []
+        if cur:
+            runs.append(cur)
+        runs = [x for x in runs if len(x) >= 100]
+        d = [v for x in runs for v in x]
+        if d:
+            d.sort()
+            out.append(f"  {prefix[5:]}: {len(runs)} runs, {len(d)} dispatches, duration median "
+                       f"{statistics.median(d):.3f} us, mean {statistics.mean(d):.3f} us, "
+                       f"p10 {d[len(d) // 10]:.3f} us")
+    for path in bench_logs:
+        with open(path) as f:
+            res = json.loads([line for line in f if line.startswith("{")][-1])
+        out.append(f"bench.py's own per-launch times (HIP events over graph replays), {os.path.basename(path)}: "
+                   f"fused {res['roofline']['avg_launch_us']} us, table-fed mpGEMM "
+                   f"{res['two_call_step']['mpgemm_roofline']['avg_launch_us']} us")
+    return "\n".join(out)
+
+
+def _per_dispatch(rows, counter):
+    """{kernel name: [value per dispatch]} for one counter (instances summed per dispatch)."""
+    per = {}
+    for r in rows:
+        if r["Counter_Name"] != counter:
+            continue
+        key = (r["Kernel_Name"], r["Dispatch_Id"])
+        per[key] = per.get(key, 0.0) + float(r["Counter_Value"])
+    out = {}
+    for (name, _), v in per.items():
+        out.setdefault(name, []).append(v)
+    return out
+
+
+def summarize_traffic(fetch_dir, write_dir, command=""):
+    """HBM bytes per launch of the headline kernels from FETCH_SIZE and WRITE_SIZE runs
+    (KiB per dispatch), scaled by what the counters read for a 256 MiB device copy."""
+    import workloads as W
+    fetch = _per_dispatch(_csv_rows(fetch_dir, "counter_collection.csv"), "FETCH_SIZE")
+    write = _per_dispatch(_csv_rows(write_dir, "counter_collection.csv"), "WRITE_SIZE")
+    kib = 256 * 1024  # the calibration copy reads and writes 256 MiB
+    f_copy = max(fetch.get(COPY_KERNEL, [0.0]))
+    w_copy = max(write.get(COPY_KERNEL, [0.0]))
+    if f_copy <= 0 or w_copy <= 0:
+        raise SystemExit("no 256 MiB copy in the runs: profile bench.py with --calibrate-copy")
+    fs, ws = kib / f_copy, kib / w_copy
+    out = ["# HBM traffic of the headline kernels from rocprofv3 PMC counters", "",
+           "commands (each counter in its own run, from /tmp with TMPDIR=/tmp):", f"  {command}", "",
+           f"Calibration: the 256 MiB device copy (torch copy, {COPY_KERNEL}) reads FETCH_SIZE = "
+           f"{f_copy:.0f} KiB and WRITE_SIZE = {w_copy:.0f} KiB for {kib} KiB read and written,",
+           f"so FETCH_SIZE is scaled by {fs:.4f} and WRITE_SIZE by {ws:.4f}.", ""]
+    inp = W.make_inputs(2, 0, M=1)
+    recs = []
+    for kind, prefix in HEADLINE_KERNELS.items():
+        names = [n for n in fetch if n.startswith(prefix)]
+        if not names or names[0] not in write:
+            continue
+        name = names[0]
+        f_raw = sum(fetch[name]) / len(fetch[name])
+        w_raw = sum(write[name]) / len(write[name])
+        traffic = round((f_raw * fs + w_raw * ws) * 1024)
+        alg = algorithmic_bytes(inp, 4, fused=(kind == "fused"))["total"]
+        out += [name, f"  dispatches: {len(fetch[name])}",
+                f"  FETCH_SIZE raw {f_raw:.1f} KiB/dispatch -> {f_raw * fs:.1f} KiB",
+                f"  WRITE_SIZE raw {w_raw:.1f} KiB/dispatch -> {w_raw * ws:.1f} KiB",
+                f"  HBM traffic {traffic} B/launch vs algorithmic {alg} B ({traffic / alg:.3f}x)", ""]
+        recs.append({"workload": "ternary_int8_gemv_4k", "timed_kernel": kind, "kernel": name,
+                     "fetch_kib_raw": round(f_raw, 1), "write_kib_raw": round(w_raw, 1),
+                     "fetch_scale": round(fs, 4), "write_scale": round(ws, 4), "bytes_per_launch": traffic,
+                     "algorithmic_bytes": alg, "kernel_source_sha256_16": kernel_source_hash(kind)})
+    out.append("Per-kernel raw averages (KiB per dispatch):")
+    for name in sorted(fetch):
+        if name in write:
+            out.append(f"  {_short(name, 76):76s} fetch {sum(fetch[name]) / len(fetch[name]):10.1f}  "
+                       f"write {sum(write[name]) / len(write[name]):10.1f}")
+    out += ["", "machine-readable records (bench.py uses one only while the kernel sources hash the same):"]
+    out += [json.dumps(r) for r in recs]
+    return "\n".join(out)
+
+
+def summarize_counters(dirs, command=""):
+    """Per-kernel utilization from rocprofv3 --pmc runs: MFMA busy per SIMD, LDS active
+    and bank-conflict cycles per CU, VALU active per CU, each as a fraction of the
+    kernel's GRBM_GUI_ACTIVE cycles (256 CUs, 1024 SIMDs)."""
+    per = {}
+    for d in dirs:  # one run per directory: dispatch ids repeat across runs
+        rows = _csv_rows(d, "counter_collection.csv")
+        for c in sorted({r["Counter_Name"] for r in rows}):
+            for name, vals in _per_dispatch(rows, c).items():
+                per.setdefault(c, {}).setdefault(name, []).extend(vals)
+    counters = sorted(per)
+    names = sorted({n for c in counters for n in per[c]})
+    out = ["# Utilization counters of the large-M kernels (rocprofv3 --pmc)", "",
+           "commands (from /tmp with TMPDIR=/tmp):", f"  {command}", "",
+           "Per dispatch, averaged over dispatches; cycles are shader-clock cycles summed over",
+           "the instances the counter has (GRBM_GUI_ACTIVE is summed over the 8 XCDs, so the",
+           "kernel's own cycles are GRBM_GUI_ACTIVE / 8).", ""]
+
+    def avg(c, n):
+        v = per.get(c, {}).get(n)
+        return sum(v) / len(v) if v else None
+
+    for n in names:
+        if not n.startswith("void lutgemm::") and not n.startswith("lutgemm::"):
+            continue
+        g = avg("GRBM_GUI_ACTIVE", n)
+        vals = {c: avg(c, n) for c in counters if avg(c, n) is not None}
+        out.append(_short(n, 100))
+        out.append("  " + ", ".join(f"{c} {v:.0f}" for c, v in vals.items()))
+        if g:
+            cyc = g / 8
+            parts = []
+            if "SQ_VALU_MFMA_BUSY_CYCLES" in vals:
+                parts.append(f"MFMA busy {100 * vals['SQ_VALU_MFMA_BUSY_CYCLES'] / (1024 * cyc):.1f} % of SIMD cycles")
+            if "SQ_LDS_IDX_ACTIVE" in vals:
+                parts.append(f"LDS active {100 * vals['SQ_LDS_IDX_ACTIVE'] / (256 * cyc):.1f} % of CU cycles")
+            if "SQ_LDS_BANK_CONFLICT" in vals and "SQ_LDS_IDX_ACTIVE" in vals:
+                parts.append(f"bank conflicts {100 * vals['SQ_LDS_BANK_CONFLICT'] / max(1.0, vals['SQ_LDS_IDX_ACTIVE']):.1f} % of LDS active")
+            if "SQ_ACTIVE_INST_VALU" in vals:
+                parts.append(f"VALU issuing {100 * vals['SQ_ACTIVE_INST_VALU'] / (256 * cyc):.1f} % of CU cycles")
+            if parts:
+                out.append("  " + "; ".join(parts))
+        out.append("")
+    return "\n".join(out)
+
+
 def main():
     args = parse()
+    if args.summarize_trace or args.summarize_traffic or args.summarize_counters:
+        if args.summarize_trace:
+            print(summarize_trace(args.summarize_trace, args.command, args.bench_logs))
+        elif args.summarize_traffic:
+            print(summarize_traffic(*args.summarize_traffic, args.command))
+        else:
+            print(summarize_counters(args.summarize_counters, args.command))
+        return
     if args.gpus != 1:
         print(f"bench.py: --gpus {args.gpus} is not supported: the LUT mpGEMM hot path runs on one GPU "
               "(sharding along N across GPUs is designed, not implemented)", file=sys.stderr)
@@ -396,22 +591,18 @@ def main():
             del c
         # INT8 table quantization on a decode shape and on the prefill shape
         for cid, sid, M in ((3, 1, 1), (4, 0, 4096)):
-            c = Case(cid, sid, M, act=W.ACT_FP16_LUT8)
-            if args.only and c.name != args.only:
-                c.release()
+            if args.only and case_name(cid, sid, M, lut8=True) != args.only:
                 continue
+            c = Case(cid, sid, M, act=W.ACT_FP16_LUT8)
             recs.append(c.measure(200 if M == 1 else 5, 3))
             log(f"{c.name}: mpgemm {recs[-1]['mpgemm_us']} us, precompute {recs[-1]['precompute_us']} us")
             c.release()
             del c
         for cid, w in W.WORKLOADS.items():
             for (sid, M, Kd, N) in w.shapes():
-                if cid == 2:
+                if cid == 2 or (args.only and case_name(cid, sid, M) != args.only):
                     continue
                 c = Case(cid, sid, M)
-                if args.only and c.name != args.only:
-                    c.release()
-                    continue
                 n = 200 if M == 1 else (20 if M <= 256 else 5)
                 recs.append(c.measure(n, 3))
                 log(f"{c.name}: mpgemm {recs[-1]['mpgemm_us']} us, {recs[-1]['mpgemm_gbps']} GB/s")
