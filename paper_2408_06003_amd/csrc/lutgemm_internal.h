@@ -142,6 +142,7 @@ struct PrecomputeParams {
     int64_t M, K, J, Q, G;
     int tri;               // ternary 3-in-5 tables: [M][J triples] x 16 entries, no S
     float *tsc;            // INT8 table quantization: per-table scales [M][J] (T holds [M][J] x 8 INT8)
+    int vbs;               // blocks of 256 table groups per workgroup (set by the launcher)
 };
 
 struct LutParams {

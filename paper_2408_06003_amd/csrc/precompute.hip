@@ -1,8 +1,9 @@
 // Table precompute as an independent operator (LUT Tensor Core, Section 3.1.1),
 // building the symmetric half tables of Eq. 4-5.
 //
-// Grid (ceil(J / 256), M): workgroup b of token m owns table groups
-// [256 b, 256 b + 256), one group of 4 activations per lane.
+// Grid (ceil(J / (256 R)), M): workgroup b of token m owns table groups
+// [256 R b, 256 R (b + 1)), one group of 4 activations per lane and step of R
+// (R = 1, 2, 4 or 8: the largest that keeps the grid at >= 256 workgroups).
 //   1. amax = max_k |a[m,k]| over the whole token (every workgroup reads the
 //      token once, into LDS when K <= 32768, so steps 2-3 read no global memory;
 //      the token is at most a few tens of KiB and stays in L2).  FP16 tables: the
@@ -82,6 +83,10 @@ __device__ __forceinline__ int block_sum_i(int v, int *red) {
 
 constexpr int64_t ROW_LDS_MAX_K = 32768;  // tokens up to this length are staged in LDS once
 
+template <bool INT8, bool TRI>
+__device__ __forceinline__ void build_block(const PrecomputeParams &p, const uint16_t *a, int64_t vb, int64_t m,
+                                            float scale, float *redf, int *redi, float *segf, int *segi);
+
 template <bool INT8, bool ROW_LDS, bool TRI>
 __global__ __launch_bounds__(256) void precompute_kernel(PrecomputeParams p) {
     extern __shared__ __attribute__((aligned(16))) uint16_t row[];  // K halves when ROW_LDS
@@ -92,11 +97,12 @@ __global__ __launch_bounds__(256) void precompute_kernel(PrecomputeParams p) {
     const int64_t m = blockIdx.y;
     const uint16_t *ag = p.act + m * p.K;
     const uint16_t *a = ROW_LDS ? row : ag;  // reads after step 1 come from the staged row
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int64_t j = (int64_t)blockIdx.x * 256 + tid;
+    const int tid = threadIdx.x;
 
-    // 1. absmax of the token, 8 activations per load
+    // 1. absmax of the token, 8 activations per load (unrolled: long tokens keep
+    // several loads in flight per lane)
     float amax = 0.f;
+#pragma unroll 8
     for (int64_t c = tid; c < p.K / 8; c += 256) {
         const uint4 v = ((const uint4 *)ag)[c];
         if (ROW_LDS) ((uint4 *)row)[c] = v;
@@ -131,6 +137,24 @@ __global__ __launch_bounds__(256) void precompute_kernel(PrecomputeParams p) {
     }
     if (blockIdx.x == 0 && tid == 0) p.tok[m] = tok;
 
+    // steps 2-3 for the R virtual blocks of 256 table groups this workgroup owns
+    if (p.vbs == 1) {
+        build_block<INT8, TRI>(p, a, blockIdx.x, m, scale, redf, redi, segf, segi);
+        return;
+    }
+    for (int r = 0; r < p.vbs; ++r) {
+        const int64_t vb = (int64_t)blockIdx.x * p.vbs + r;
+        if (vb * 256 >= p.J) break;  // uniform
+        build_block<INT8, TRI>(p, a, vb, m, scale, redf, redi, segf, segi);
+    }
+}
+
+// Steps 2-3 for virtual block vb (table groups [256 vb, 256 vb + 256)).
+template <bool INT8, bool TRI>
+__device__ __forceinline__ void build_block(const PrecomputeParams &p, const uint16_t *a, int64_t vb, int64_t m,
+                                            float scale, float *redf, int *redi, float *segf, int *segi) {
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int64_t j = vb * 256 + tid;
     if constexpr (TRI) {
         // 2'. triple table of this lane's triple
         if (j < p.J) {
@@ -241,8 +265,8 @@ __global__ __launch_bounds__(256) void precompute_kernel(PrecomputeParams p) {
                 ((float *)p.S)[m * p.Q + q] = sf;
         }
     } else {
-        // quantization groups starting in this workgroup's range, summed by the whole workgroup
-        const int64_t k_lo = (int64_t)blockIdx.x * 1024;
+        // quantization groups starting in this block's range, summed by the whole workgroup
+        const int64_t k_lo = vb * 1024;
         const int64_t k_hi = (k_lo + 1024 < p.K) ? k_lo + 1024 : p.K;
         for (int64_t q = (k_lo + p.G - 1) / p.G; q * p.G < k_hi; ++q) {
             const uint16_t *aq = a + q * p.G;
@@ -273,10 +297,20 @@ __global__ __launch_bounds__(256) void precompute_kernel(PrecomputeParams p) {
     }
 }
 
-int launch_precompute(const PrecomputeParams &p, int act_int8, void *stream) {
+int launch_precompute(const PrecomputeParams &p_in, int act_int8, void *stream) {
     hipStream_t s = (hipStream_t)stream;
-    if (p.M <= 0) return 0;
-    const dim3 grid((unsigned)((p.J + 255) / 256), (unsigned)p.M);
+    if (p_in.M <= 0) return 0;
+    // virtual blocks of 256 table groups per workgroup: more when the grid stays at
+    // >= 256 workgroups, so fewer workgroups each read the whole token for its absmax
+    PrecomputeParams p = p_in;
+    const int64_t nvb = (p.J + 255) / 256;
+    p.vbs = 1;
+    for (int r = 8; r > 1; r /= 2)
+        if ((nvb + r - 1) / r * p.M >= 256) {
+            p.vbs = r;
+            break;
+        }
+    const dim3 grid((unsigned)((nvb + p.vbs - 1) / p.vbs), (unsigned)p.M);
     const bool lds = p.K <= ROW_LDS_MAX_K;
     const size_t shm = lds ? (size_t)p.K * 2 : 0;
     if (p.tri) {
