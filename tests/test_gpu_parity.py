@@ -114,11 +114,14 @@ def test_full_size_sampled(cid, sid, M, K, N):
 
 # ----------------------------------------------------------------- precompute
 
-@pytest.mark.parametrize("act_kind", [W.ACT_FP16, W.ACT_INT8])
-def test_precompute_matches_table_definition(act_kind):
-    banner(f"precompute act={act_kind}")
-    M, K = 3, 1024
-    wfmt, bits, G = (W.WFMT_UINT, 2, 128) if act_kind == W.ACT_FP16 else (W.WFMT_TERNARY, 2, 0)
+@pytest.mark.parametrize("act_kind,M,K,G", [(W.ACT_FP16, 3, 1024, 128), (W.ACT_INT8, 3, 1024, 0),
+                                             # several 1024-activation blocks per workgroup (large M),
+                                             # group sums by lane butterflies and by whole workgroups
+                                             (W.ACT_FP16, 300, 4096, 128), (W.ACT_FP16, 260, 8192, 2048),
+                                             (W.ACT_INT8, 300, 4096, 0)])
+def test_precompute_matches_table_definition(act_kind, M, K, G):
+    banner(f"precompute act={act_kind} M={M} K={K} G={G}")
+    wfmt, bits = (W.WFMT_UINT, 2) if act_kind == W.ACT_FP16 else (W.WFMT_TERNARY, 2)
     inp = W.make_custom(wfmt, bits, G, act_kind, M=M, K=K, N=256, seed=21, scale_fp32=(G == 0))
     inp.act[1] *= np.float16(300)            # a large-magnitude token
     inp.act[2, :] = 0                        # an all-zero token
