@@ -69,7 +69,8 @@ enum {
                                  tables, exact INT32 accumulation (BINARY / TERNARY weights)     */
     LUTGEMM_ACT_FP16_LUT8 = 2 /* FP16 activations, tables quantized to INT8 with one FP32 scale
                                  per table (Section 3.1.4): an approximation (relative error of
-                                 the output about 3e-3), half the table bytes of ACT_FP16; not
+                                 the output about 3e-3), 12 instead of 16 table bytes per 4
+                                 activations (8 INT8 codes + FP32 scale); not
                                  with TERNARY_3IN5                                               */
 };
 
@@ -233,23 +234,25 @@ size_t lutgemm_fused_workspace_size(const lutgemm_problem_t *problem, int64_t M)
  * Table precompute fused into the LUT mpGEMM (Section 3.1.1 splits the
  * precompute out of the lookup so that it can be fused; this fuses it on the
  * consumer side): O = A x W^T (+ O) from act [M][K] FP16 (device) and the packed
- * weights, with the same activation quantization (ACT_INT8) or power-of-two
- * token scaling (ACT_FP16) and the same FP16 / INT16 table entries as
- * lutgemm_precompute + lutgemm_mpgemm.  For single tokens with weights the
- * whole-K lookup kernel takes (at most a few MB), every workgroup builds its
- * tables in LDS from the activations: one kernel (plus a split-K sum when K is
- * split), no table buffer.  TERNARY_3IN5: the same for every M (one kernel,
- * tables built per workgroup for its token).  Otherwise it runs
- * lutgemm_precompute into the workspace followed by lutgemm_mpgemm.
+ * weights.  Single tokens (M <= 2): every workgroup builds the tables of its K
+ * range in LDS from the activations -- with the weights the whole-K lookup kernel
+ * takes (at most a few MB) the same activation quantization (ACT_INT8) or
+ * power-of-two token scaling (ACT_FP16) and the same FP16 / INT16 table entries as
+ * lutgemm_precompute + lutgemm_mpgemm, one kernel; with larger weights and
+ * ACT_FP16 the split-K kernel, whose tables are exact FP32 sums of the
+ * activations as given (no token scaling, no FP16 rounding of entries), plus the
+ * split sum.  TERNARY_3IN5: one kernel for every M, tables built per workgroup
+ * for its token.  Otherwise (M > 2, ACT_INT8 with larger weights, ACT_FP16_LUT8)
+ * it runs lutgemm_precompute into the workspace followed by lutgemm_mpgemm.
  *   act        device FP16 [M][K]
  *   packed, out, out_dtype, accumulate   as for lutgemm_mpgemm
  *   workspace  device, workspace_bytes >= lutgemm_fused_workspace_size(problem, M);
  *              may be NULL when that size is 0
  * INT8 activations: results are bitwise those of lutgemm_precompute +
- * lutgemm_mpgemm (ACT_FP16_LUT8: always the two calls, the quantized tables
- * going through the workspace).  FP16 activations: the zero-point term is summed per 128-block
- * instead of per quantization group, so results agree with the two-call path to
- * FP32 rounding (TERNARY_3IN5: bitwise).  Bitwise reproducible run to run.
+ * lutgemm_mpgemm.  FP16 activations: the zero-point term is summed per 128-block
+ * instead of per quantization group, and the split-K kernel's entries are not
+ * rounded to FP16, so results agree with the two-call path to within that
+ * rounding (TERNARY_3IN5: bitwise).  Bitwise reproducible run to run.
  */
 lutgemm_status_t lutgemm_mpgemm_fused(const lutgemm_problem_t *problem, int64_t M, const void *act,
                                       const void *packed, void *out, int32_t out_dtype,

@@ -265,8 +265,10 @@ struct FusedScratch {
 static FusedScratch fused_scratch(const Layout &L, const LutPlan &plan, int64_t M) {
     FusedScratch f{};
     // INT8 table quantization exists to shrink the tables that travel through HBM, so
-    // that mode always takes the two-call path
-    f.fused = (plan.kind == 0 || plan.kind == 3) && L.act != LUTGEMM_ACT_FP16_LUT8;
+    // that mode always takes the two-call path; the split-K GEMV builds its tables only
+    // on the FP path (INT8 quantization needs the whole token's absmax)
+    f.fused = ((plan.kind == 0 || plan.kind == 3) && L.act != LUTGEMM_ACT_FP16_LUT8) ||
+              (plan.kind == 2 && L.act == LUTGEMM_ACT_FP16);
     if (f.fused) {
         f.part_off = 0;
         f.tok_off = plan.ws_bytes;
@@ -440,6 +442,11 @@ lutgemm_status_t lutgemm_mpgemm_fused(const lutgemm_problem_t *problem, int64_t 
     LutParams lp = lut_params(L, plan, M, nullptr, packed, out, out_dtype, accumulate, ws + fs.part_off);
     lp.act = (const uint16_t *)act;
     if (plan.kind == 3) return hip_status(launch_tri(lp, L, true, stream));
+    if (plan.kind == 2) {  // FP activations: tables from the activations, then the split sum
+        int e = launch_fused_split(lp, L, plan, stream);
+        if (e == 0 && plan.splits > 1) e = launch_finalize(lp, L, plan, stream);
+        return hip_status(e);
+    }
     lp.tok_out = plan.splits > 1 ? (float *)(ws + fs.tok_off) : nullptr;
     int e = launch_fused_gemv(lp, L, plan, stream);
     if (e == 0 && plan.splits > 1) {

@@ -327,6 +327,130 @@ static void launch_fused_bits(const LutParams &p, const Layout &L, const LutPlan
     }
 }
 
+// ---------------------------------------------------------------- split-K, FP activations
+//
+// The split-K GEMV of lut_gemv.hip (256 columns per workgroup, one per lane, KBS
+// 128-blocks of K per workgroup, partial sums summed by the finalize kernel) with
+// its tables built from the FP16 activations of its own K range instead of read
+// from the precompute.  The FP path's power-of-two token scaling only keeps FP16
+// table entries in range, so it is not needed here: each lane builds the signed
+// 16-entry table of one 4-activation group in FP32 (entries
+// ((-x0 + (+-x1)) + (+-x2)) + (+-x3) of the activations as given, the negated half
+// by Eq. 4), without the FP16 rounding of stored tables, and a lookup adds the
+// FP32 entry.  The zero-point term of Eq. 3 is applied per 128-block (the sum over
+// a group's blocks of s'_q z'_q S_kb is s'_q z'_q S_q), with S_kb summed in a fixed
+// order over the 32 lanes that built the block's tables.
+template <int BITS, int KBS>
+__global__ __launch_bounds__(256) void lut_fused_split_kernel(LutParams p, int wfmt) {
+    constexpr int GS = 16;                 // entries per signed table
+    constexpr int BLKF = (GPB + 1) * GS;   // floats per 128-block (padded by one table)
+    __shared__ __attribute__((aligned(16))) float F[KBS * BLKF];
+    __shared__ float Sblk[KBS];
+    const int tid = threadIdx.x;
+    const int64_t n = (int64_t)blockIdx.x * NTILE + tid;
+    const int split = blockIdx.y;
+    const int64_t m = blockIdx.z;
+    const int64_t kb0 = (int64_t)split * KBS;
+    const int nkb = (int)((p.KB - kb0) < KBS ? (p.KB - kb0) : KBS);
+    const bool need_s = wfmt != LUTGEMM_WFMT_BINARY;
+
+    // conditional loads first, then unconditional clamped ones (see lut_gemv_kernel)
+    Epi ep{};
+    if (p.splits == 1) ep = load_epi<false>(p, wfmt, m, n, true);
+    // activations: lane g holds group g of the workgroup's range (KBS x 32 <= 256 groups)
+    const int g = tid, gc = g < nkb * GPB ? g : nkb * GPB - 1;
+    const uint2 av = ((const uint2 *)(p.act + m * p.K))[kb0 * GPB + gc];
+    uint4 w[KBS][BITS];
+#pragma unroll
+    for (int kbl = 0; kbl < KBS; ++kbl) {
+        const int kbc = kbl < nkb ? kbl : nkb - 1;
+#pragma unroll
+        for (int t = 0; t < BITS; ++t) w[kbl][t] = p.planes[((kb0 + kbc) * BITS + t) * p.N_pad + n];
+    }
+    uint2 mw[KBS];
+#pragma unroll
+    for (int kbl = 0; kbl < KBS; ++kbl) {
+        const int kbc = kbl < nkb ? kbl : nkb - 1;
+        const int q = (int)(((float)(kb0 + kbc) + 0.5f) * p.inv_kpg);
+        mw[kbl] = load_meta_words(p, q, lane_value(n));
+    }
+
+    // signed FP32 table of group g and the block sums
+    const float x0 = h2f(av.x & 0xFFFFu), x1 = h2f(av.x >> 16), x2 = h2f(av.y & 0xFFFFu), x3 = h2f(av.y >> 16);
+    if (g < nkb * GPB) {
+        float t[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) t[i] = ((-x0 + ((i & 4) ? x1 : -x1)) + ((i & 2) ? x2 : -x2)) + ((i & 1) ? x3 : -x3);
+        float *dst = F + (g / GPB) * BLKF + (g % GPB) * GS;
+        *(float4 *)(dst + 0) = make_float4(t[0], t[1], t[2], t[3]);
+        *(float4 *)(dst + 4) = make_float4(t[4], t[5], t[6], t[7]);
+        *(float4 *)(dst + 8) = make_float4(-t[0], -t[1], -t[2], -t[3]);
+        *(float4 *)(dst + 12) = make_float4(-t[4], -t[5], -t[6], -t[7]);
+    }
+    if (need_s) {  // S of block g / 32: fixed butterfly over its 32 lanes
+        float sg = g < nkb * GPB ? ((x0 + x1) + x2) + x3 : 0.f;
+#pragma unroll
+        for (int off = 1; off < 32; off <<= 1) sg += __shfl_xor(sg, off, 64);
+        if ((tid & 31) == 0 && (tid >> 5) < KBS) Sblk[tid >> 5] = sg;
+    }
+    lds_barrier();
+
+    float yf = 0.f;
+#pragma unroll
+    for (int kbl = 0; kbl < KBS; ++kbl) {
+        if (kbl < nkb) {
+            float tot = 0.f;
+#pragma unroll
+            for (int t = 0; t < BITS; ++t) {
+                const uint32_t wd[4] = {w[kbl][t].x, w[kbl][t].y, w[kbl][t].z, w[kbl][t].w};
+                float acc = 0.f;
+#pragma unroll
+                for (int d = 0; d < 4; ++d) {
+                    const char *Fg = (const char *)(F + kbl * BLKF + d * 8 * GS);
+                    const uint32_t lo = wd[d] << 2, hi = wd[d] >> 2;
+                    acc += *(const float *)(Fg + 0 * GS * 4 + idx4<0>(lo)) + *(const float *)(Fg + 1 * GS * 4 + idx4<0>(hi));
+                    acc += *(const float *)(Fg + 2 * GS * 4 + idx4<1>(lo)) + *(const float *)(Fg + 3 * GS * 4 + idx4<1>(hi));
+                    acc += *(const float *)(Fg + 4 * GS * 4 + idx4<2>(lo)) + *(const float *)(Fg + 5 * GS * 4 + idx4<2>(hi));
+                    acc += *(const float *)(Fg + 6 * GS * 4 + idx4<3>(lo)) + *(const float *)(Fg + 7 * GS * 4 + idx4<3>(hi));
+                }
+                tot += acc * (float)(1 << t);  // exact scaling by the plane weight
+            }
+            const SZ sz = decode_sz(p, mw[kbl]);
+            yf = fmaf(sz.sp, tot, yf);
+            if (need_s) yf -= (sz.sp * sz.zp) * Sblk[kbl];
+        }
+    }
+    if (p.splits == 1)
+        store_out<false>(p, wfmt, m, n, yf, 0, ep);
+    else
+        p.part[((int64_t)split * p.M + m) * p.N_pad + n] = yf;
+}
+
+template <int BITS>
+static void launch_fused_split_bits(const LutParams &p, const Layout &L, const LutPlan &plan, hipStream_t s) {
+    const dim3 grid((unsigned)(L.N_pad / NTILE), (unsigned)plan.splits, (unsigned)p.M);
+    switch (plan.kbs) {
+    case 1: hipLaunchKernelGGL((lut_fused_split_kernel<BITS, 1>), grid, dim3(256), 0, s, p, L.wfmt); break;
+    case 2: hipLaunchKernelGGL((lut_fused_split_kernel<BITS, 2>), grid, dim3(256), 0, s, p, L.wfmt); break;
+    case 4:
+        if constexpr (BITS <= 2)
+            hipLaunchKernelGGL((lut_fused_split_kernel<BITS, 4>), grid, dim3(256), 0, s, p, L.wfmt);
+        break;
+    default:
+        if constexpr (BITS == 1)
+            hipLaunchKernelGGL((lut_fused_split_kernel<BITS, 8>), grid, dim3(256), 0, s, p, L.wfmt);
+        break;
+    }
+}
+
+int launch_fused_split(const LutParams &p, const Layout &L, const LutPlan &plan, void *stream) {
+    hipStream_t s = (hipStream_t)stream;
+    if (L.bits == 1) launch_fused_split_bits<1>(p, L, plan, s);
+    else if (L.bits == 2) launch_fused_split_bits<2>(p, L, plan, s);
+    else launch_fused_split_bits<4>(p, L, plan, s);
+    return (int)hipGetLastError();
+}
+
 int launch_fused_gemv(const LutParams &p, const Layout &L, const LutPlan &plan, void *stream) {
     hipStream_t s = (hipStream_t)stream;
     if (L.act == LUTGEMM_ACT_INT8)

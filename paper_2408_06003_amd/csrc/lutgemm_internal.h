@@ -181,6 +181,7 @@ int launch_precompute(const PrecomputeParams &p, int act_int8, void *stream);
 int launch_lut(const LutParams &p, const Layout &L, const LutPlan &plan, void *stream);
 int launch_gemv(const LutParams &p, const Layout &L, const LutPlan &plan, void *stream);
 int launch_fused_gemv(const LutParams &p, const Layout &L, const LutPlan &plan, void *stream);
+int launch_fused_split(const LutParams &p, const Layout &L, const LutPlan &plan, void *stream);
 int launch_finalize(const LutParams &p, const Layout &L, const LutPlan &plan, void *stream);
 int launch_mtok(const LutParams &p, const Layout &L, const LutPlan &plan, void *stream);
 int launch_tri(const LutParams &p, const Layout &L, bool fused, void *stream);
