@@ -194,12 +194,13 @@ class Case:
         self.L.mpgemm_fused(self.p, self.M, self.act, self.packed[i % len(self.packed)], self.out,
                             self.out_code, False, workspace=self.fws)
 
-    def timed(self, fn, n, graph=True, check=None):
+    def timed(self, fn, n, graph=True, check=None, reps=1):
         """Average milliseconds per call over n back-to-back calls, timed with HIP events
         on the stream they run on.  With graph=True the n calls are captured once into a
         HIP graph and replayed, so host launch overhead is not counted (the way a decode
         loop runs); ``check`` (a function returning a tensor) compares two replays,
-        separated by eager work, with the eager result."""
+        separated by eager work, with the eager result.  With reps > 1 the replay is
+        timed reps times and the median batch is returned."""
         torch = self.torch
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         if not graph:
@@ -231,11 +232,27 @@ class Case:
         g.replay()  # warm replay
         torch.cuda.synchronize()
         s = torch.cuda.current_stream()
+        batches = []
+        for _ in range(reps):
+            e0.record(s)
+            g.replay()
+            e1.record(s)
+            torch.cuda.synchronize()
+            batches.append(e0.elapsed_time(e1) / n)
+        return sorted(batches)[len(batches) // 2]
+
+    def cold_call_us(self, fn, i):
+        """One call on its own (device idle before it, HBM-cold weight copy i), timed with
+        HIP events on its stream: the latency a single decode step sees."""
+        torch = self.torch
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s = torch.cuda.current_stream()
+        torch.cuda.synchronize()
         e0.record(s)
-        g.replay()
+        fn(i)
         e1.record(s)
         torch.cuda.synchronize()
-        return e0.elapsed_time(e1) / n
+        return e0.elapsed_time(e1) * 1e3
 
     def effective_tops(self, ms):
         return 2.0 * self.M * self.N * self.K / (ms * 1e-3) / 1e12
@@ -245,16 +262,16 @@ class Case:
         for i in range(warmup):
             self.step(i)
         self.precompute()
-        ms_mp = self.timed(self.mpgemm, n_kernel, check=lambda: self.out)
-        ms_pre = self.timed(lambda i: self.precompute(), n_kernel)
+        ms_mp = self.timed(self.mpgemm, n_kernel, check=lambda: self.out, reps=5)
+        ms_pre = self.timed(lambda i: self.precompute(), n_kernel, reps=5)
         b = algorithmic_bytes(self.inp, self.out_bytes, tri=self.tri, lut8=self.lut8)
         gbps = b["total"] / (ms_mp * 1e-3) / 1e9
         # achievable streaming read of the same byte count, same rotation and timing
         sink = self.torch.zeros(4096, dtype=self.torch.int32, device="cuda")
         wb = self.L.packed_weight_size(self.p)
         ms_rd = self.timed(lambda i: self.L.calibrate_stream_read(self.packed[i % len(self.packed)], wb, sink, 1024),
-                           n_kernel)
-        ms_fu = self.timed(self.fused, n_kernel, check=lambda: self.out)
+                           n_kernel, reps=5)
+        ms_fu = self.timed(self.fused, n_kernel, check=lambda: self.out, reps=5)
         rec = {"workload": self.name, "M": self.M, "K": self.K, "N": self.N, "bits": self.inp.bits,
                "mpgemm_us": round(ms_mp * 1e3, 3), "mpgemm_tops": round(self.effective_tops(ms_mp), 3),
                "mpgemm_gbps": round(gbps, 1), "hbm_frac": round(gbps / HBM_PEAK_GBPS, 4),
@@ -531,6 +548,7 @@ def main():
     ms_two = head.timed(head.step, K, check=lambda: head.out)
     ms_two_eager = head.timed(head.step, K, graph=False)
     kern = head.measure(max(K, 50), 5)
+    cold_us = round(head.cold_call_us(head.fused, len(head.packed) // 2), 3)
     log(f"headline: fused {ms_step * 1e3:.2f} us/step, two-call {ms_two * 1e3:.2f} us/step, "
         f"mpgemm {kern['mpgemm_us']} us")
     fb = algorithmic_bytes(head.inp, head.out_bytes, fused=True)["total"]
@@ -565,6 +583,7 @@ def main():
         "timing": "HIP graph of the K steps replayed once between HIP events (host launch overhead "
                   "excluded); ms_per_step_eager launches the same steps one by one from Python",
         "ms_per_step_eager": round(ms_step_eager, 6),
+        "single_call_cold_us": cold_us,
         "hbm_gbps_step": achieved,
         "roofline": roofline,
         "two_call_step": {"entries": "lutgemm_precompute + lutgemm_mpgemm (tables through HBM)",
