@@ -473,30 +473,36 @@ def summarize_counters(dirs, command=""):
     """Per-kernel utilization from rocprofv3 --pmc runs: MFMA busy per SIMD, LDS active
     and bank-conflict cycles per CU, VALU active per CU, each as a fraction of the
     kernel's GRBM_GUI_ACTIVE cycles (256 CUs, 1024 SIMDs)."""
+    import re
+    # runs of one workload (directories named <tag>_<letter>_<workload>) are grouped,
+    # so that a kernel that serves several workloads is reported per workload
     per = {}
     for d in dirs:  # one run per directory: dispatch ids repeat across runs
+        base = os.path.basename(os.path.normpath(d))
+        m = re.match(r"^[^_]+_[a-z]_(.+)$", base)
+        wl = m.group(1) if m else base
         rows = _csv_rows(d, "counter_collection.csv")
         for c in sorted({r["Counter_Name"] for r in rows}):
             for name, vals in _per_dispatch(rows, c).items():
-                per.setdefault(c, {}).setdefault(name, []).extend(vals)
+                per.setdefault(c, {}).setdefault((wl, name), []).extend(vals)
     counters = sorted(per)
-    names = sorted({n for c in counters for n in per[c]})
+    keys = sorted({k for c in counters for k in per[c]})
     out = ["# Utilization counters of the large-M kernels (rocprofv3 --pmc)", "",
            "commands (from /tmp with TMPDIR=/tmp):", f"  {command}", "",
-           "Per dispatch, averaged over dispatches; cycles are shader-clock cycles summed over",
-           "the instances the counter has (GRBM_GUI_ACTIVE is summed over the 8 XCDs, so the",
-           "kernel's own cycles are GRBM_GUI_ACTIVE / 8).", ""]
+           "Per dispatch, averaged over the dispatches of one workload's runs; cycles are",
+           "shader-clock cycles summed over the instances the counter has (GRBM_GUI_ACTIVE is",
+           "summed over the 8 XCDs, so the kernel's own cycles are GRBM_GUI_ACTIVE / 8).", ""]
 
     def avg(c, n):
         v = per.get(c, {}).get(n)
         return sum(v) / len(v) if v else None
 
-    for n in names:
-        if not n.startswith("void lutgemm::") and not n.startswith("lutgemm::"):
+    for n in keys:
+        if not n[1].startswith("void lutgemm::") and not n[1].startswith("lutgemm::"):
             continue
         g = avg("GRBM_GUI_ACTIVE", n)
         vals = {c: avg(c, n) for c in counters if avg(c, n) is not None}
-        out.append(_short(n, 100))
+        out.append(f"{n[0]}: {_short(n[1], 100)}")
         out.append("  " + ", ".join(f"{c} {v:.0f}" for c, v in vals.items()))
         if g:
             cyc = g / 8
