@@ -44,6 +44,47 @@ __device__ __forceinline__ uint32_t neg16x2(uint32_t x) {
     return x ^ 0x80008000u;  // FP16: flip both sign bits (exact)
 }
 
+// (x >> 8 j) & 0xF0 for a compile-time byte j (after unrolling) in one SDWA
+// instruction: the high nibble of byte j of x, times 16, i.e. the byte offset of
+// that Eq. 6 index's row in a token-interleaved table.  (The compiler emits a
+// shift and a mask for bytes 1 and 2.)
+__device__ __forceinline__ uint32_t nib_off(uint32_t x, int j) {
+    uint32_t r;
+    const uint32_t m = 0xF0u;
+    switch (j) {
+        case 0:
+            asm("v_and_b32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:BYTE_0 src1_sel:DWORD"
+                : "=v"(r) : "v"(x), "s"(m));
+            break;
+        case 1:
+            asm("v_and_b32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:BYTE_1 src1_sel:DWORD"
+                : "=v"(r) : "v"(x), "s"(m));
+            break;
+        case 2:
+            asm("v_and_b32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:BYTE_2 src1_sel:DWORD"
+                : "=v"(r) : "v"(x), "s"(m));
+            break;
+        default:
+            asm("v_and_b32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:BYTE_3 src1_sel:DWORD"
+                : "=v"(r) : "v"(x), "s"(m));
+            break;
+    }
+    return r;
+}
+
+// h = a + b as four packed FP16 pairs (8 tokens): the first two entries of a word
+// are summed without copying either into the accumulator.
+__device__ __forceinline__ uint4 pk_sum4(uint4 a, uint4 b) {
+    uint4 h;
+    asm("v_pk_add_f16 %0, %4, %8\n\t"
+        "v_pk_add_f16 %1, %5, %9\n\t"
+        "v_pk_add_f16 %2, %6, %10\n\t"
+        "v_pk_add_f16 %3, %7, %11"
+        : "=&v"(h.x), "=&v"(h.y), "=&v"(h.z), "=&v"(h.w)
+        : "v"(a.x), "v"(a.y), "v"(a.z), "v"(a.w), "v"(b.x), "v"(b.y), "v"(b.z), "v"(b.w));
+    return h;
+}
+
 // h += e as four packed FP16 pairs (8 tokens), one statement per read for the same
 // reason as fma_mix8 below.
 __device__ __forceinline__ void pk_add4(uint4 &h, uint4 e) {
@@ -111,68 +152,87 @@ __device__ __forceinline__ Tile tile_of(uint32_t b, uint32_t n_tiles, uint32_t m
 }
 
 template <int BITS, bool INT8, bool TQ>
-__global__ __launch_bounds__(256) void lut_mtok_kernel(LutParams p, int wfmt, int64_t n_tiles, int64_t m_tiles,
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(TQ ? 1 : 5))) void lut_mtok_kernel(LutParams p, int wfmt, int64_t n_tiles, int64_t m_tiles,
                                                        int order) {
     constexpr int CH = BITS == 1 ? 2 : 4 / BITS;  // 128-blocks per chunk (more workgroups per CU at b = 1)
     constexpr int TASKS = CH * GPB * 4;           // staging tasks per chunk: (block, group, index pair)
     constexpr int TPL = (TASKS + 255) / 256;      // staging tasks per lane
     constexpr int BUF = CH * GPB * 256;           // LDS bytes of one table buffer (16 entries x 8 tokens x 2 B per group)
+    // exactly 32 KB for b <= 2, so that five workgroups fit in the 160 KB of a CU
     __shared__ __attribute__((aligned(16))) char F[2 * BUF];
-    __shared__ float Ssh[2][CH][MTK];             // FP path: activation sum of each block's group (first block only)
 
     const int tid = threadIdx.x;
     const Tile tl = tile_of(blockIdx.x, (uint32_t)n_tiles, (uint32_t)m_tiles, order);
-    const int64_t n = tl.nt * NTILE + tid;
+    const uint32_t n = (uint32_t)(tl.nt * NTILE + tid);
     const int split = tl.split;
     const int64_t m0 = tl.mt * MTK;
-    const int64_t kbA = (int64_t)split * p.kbs;
-    const int64_t kbB = (kbA + p.kbs < p.KB) ? kbA + p.kbs : p.KB;
+    // 128-block indices fit in 32 bits (K < 2^38)
+    const int kbA = split * p.kbs;
+    const int kbB = (kbA + p.kbs < (int)p.KB) ? kbA + p.kbs : (int)p.KB;
     const bool need_s = !INT8 && wfmt != LUTGEMM_WFMT_BINARY;
+    // Token rows past M repeat row M - 1: their sums are computed but never stored.
+    auto row_of = [&](int t) { return (m0 + t < p.M) ? m0 + t : p.M - 1; };
+    // Addresses: the workgroup-uniform part (token row, chunk, block, quantization
+    // group) stays in scalar registers; lanes add 32-bit offsets that do not change
+    // from chunk to chunk, so the loads cost almost no vector instructions.
+    const uint32_t n_meta = p.per_tensor ? 0u : n;  // metadata column (0: one pair per tensor)
+    // quantization group of a 128-block (workgroup-uniform: moved to a scalar register,
+    // so that what depends on it is scalar arithmetic)
+    auto group_of = [&](int kb) {
+        return __builtin_amdgcn_readfirstlane((int)(((float)kb + 0.5f) * p.inv_kpg));
+    };
 
     // staged table words: entries 2ip, 2ip + 1 of a token's half table (FP16 / INT16
     // pair), or with INT8-quantized tables (TQ) their two codes and the table's scale
     typedef std::conditional_t<TQ, uint2, uint32_t> SDE;
     typedef SDE SD[TPL][MTK];
     typedef uint4 WW[CH][BITS];
-    typedef uint2 MW[CH];
+    struct MW {
+        uint2 w[CH];  // metadata words of each block's group
+        int q[CH];    // each block's group
+    };
     typedef float SV[1];
-    auto load = [&](int64_t kc, SD &sd, WW &w, MW &mw, SV &sv) {
-        const int nkb = (int)((kbB - kc) < CH ? (kbB - kc) : CH);
+    auto load = [&](int kc, SD &sd, WW &w, MW &mw, SV &sv) {
+        const int nkb = (kbB - kc) < CH ? (kbB - kc) : CH;
 #pragma unroll
         for (int r = 0; r < TPL; ++r) {
             const int task = tid + 256 * r;
             const int tk = task < TASKS ? task : TASKS - 1;
             const int kbl = tk >> 7, g = (tk >> 2) & 31, ip = tk & 3;
             const int kbc = kbl < nkb ? kbl : nkb - 1;
+            const uint32_t tab = (uint32_t)(kbc * GPB + g);  // the lane's table within the chunk
 #pragma unroll
             for (int t = 0; t < MTK; ++t) {
-                const int64_t row = (m0 + t < p.M) ? m0 + t : p.M - 1;
-                const int64_t rg = row * p.J + (kc + kbc) * GPB + g;
+                const int64_t base = row_of(t) * p.J + (int64_t)kc * GPB;
                 if constexpr (TQ)
-                    sd[r][t] = make_uint2(((const uint16_t *)p.T)[4 * rg + ip], __float_as_uint(p.tsc[rg]));
+                    sd[r][t] = make_uint2(((const uint16_t *)p.T + 4 * base)[4 * tab + ip],  // 8 codes per table
+                                          __float_as_uint((p.tsc + base)[tab]));
                 else
-                    sd[r][t] = ((const uint32_t *)(p.T + rg))[ip];
+                    sd[r][t] = ((const uint32_t *)(p.T + base))[4 * tab + ip];
             }
         }
 #pragma unroll
         for (int kbl = 0; kbl < CH; ++kbl) {
             const int kbc = kbl < nkb ? kbl : nkb - 1;
 #pragma unroll
-            for (int t = 0; t < BITS; ++t) w[kbl][t] = p.planes[((kc + kbc) * BITS + t) * p.N_pad + n];
+            for (int t = 0; t < BITS; ++t) w[kbl][t] = (p.planes + ((int64_t)(kc + kbc) * BITS + t) * p.N_pad)[n];
         }
         if constexpr (!INT8) {
 #pragma unroll
             for (int kbl = 0; kbl < CH; ++kbl) {
                 const int kbc = kbl < nkb ? kbl : nkb - 1;
-                const int q = (int)(((float)(kc + kbc) + 0.5f) * p.inv_kpg);
-                mw[kbl] = load_meta_words(p, q, lane_value(n));
+                const int q = group_of(kc + kbc);
+                const uint32_t *mb = (const uint32_t *)p.meta + (p.per_tensor ? 0 : (int64_t)q * p.N_pad);
+                mw.w[kbl] = make_uint2(mb[n_meta], (mb + p.per_tensor)[n_meta]);
+                mw.q[kbl] = q;
             }
-            // one activation sum per (block, token): lanes 0 .. 8 CH - 1
-            const int kbl = (tid >> 3) < CH ? (tid >> 3) : CH - 1, t = tid & 7;
-            const int kbc = kbl < nkb ? kbl : nkb - 1;
-            const int q = (int)(((float)(kc + kbc) + 0.5f) * p.inv_kpg);
-            const int64_t row = (m0 + t < p.M) ? m0 + t : p.M - 1;
-            sv[0] = ((const float *)p.S)[lane_value(row * p.Q + q)];
+            // one activation sum per (block, token): lanes 0 .. 8 CH - 1 of every wavefront,
+            // broadcast to the others by readlane
+            const int ln = tid & 63;
+            const int t = ln & 7;
+            const int q = (CH == 1 || ln < 8) ? mw.q[0] : mw.q[CH - 1];
+            const uint32_t rt = (uint32_t)((m0 + t < p.M) ? t : p.M - 1 - m0);
+            sv[0] = ((const float *)p.S + m0 * p.Q)[rt * (uint32_t)p.Q + (uint32_t)q];
         }
     };
 
@@ -184,8 +244,8 @@ __global__ __launch_bounds__(256) void lut_mtok_kernel(LutParams p, int wfmt, in
         yi[t] = 0;
     }
 
-    auto process = [&](int64_t kc, const SD &sd, const WW &w, const MW &mw, const SV &sv, int b) {
-        const int nkb = (int)((kbB - kc) < CH ? (kbB - kc) : CH);
+    auto process = [&](int kc, const SD &sd, const WW &w, const MW &mw, const SV &sv, int b) {
+        const int nkb = (kbB - kc) < CH ? (kbB - kc) : CH;
         char *Fb = F + b * BUF;
         // stage: for each task, entries 2ip, 2ip + 1 and their negations for the 8 tokens
 #pragma unroll
@@ -200,11 +260,10 @@ __global__ __launch_bounds__(256) void lut_mtok_kernel(LutParams p, int wfmt, in
                         const float sc = __uint_as_float(sd[r][t].y);
                         const float f0 = (float)(int8_t)(sd[r][t].x & 0xFFu) * sc;
                         const float f1 = (float)(int8_t)((sd[r][t].x >> 8) & 0xFFu) * sc;
-                        const uint32_t h = (uint32_t)__half_as_ushort(__float2half_rn(f0)) |
-                                           ((uint32_t)__half_as_ushort(__float2half_rn(f1)) << 16);
-                        v[t] = (m0 + t < p.M) ? h : 0u;
+                        v[t] = (uint32_t)__half_as_ushort(__float2half_rn(f0)) |
+                               ((uint32_t)__half_as_ushort(__float2half_rn(f1)) << 16);
                     } else {
-                        v[t] = (m0 + t < p.M) ? sd[r][t] : 0u;
+                        v[t] = sd[r][t];
                     }
                 }
                 uint4 e0, e1;  // entries 2ip (low halves) and 2ip + 1 (high halves), tokens 0..7
@@ -225,34 +284,29 @@ __global__ __launch_bounds__(256) void lut_mtok_kernel(LutParams p, int wfmt, in
                     make_uint4(neg16x2<INT8>(e1.x), neg16x2<INT8>(e1.y), neg16x2<INT8>(e1.z), neg16x2<INT8>(e1.w));
             }
         }
-        if (need_s && tid < CH * MTK) {
-            const int kbl = tid >> 3, kb = (int)(kc + kbl);
-            const int q = (int)(((float)kb + 0.5f) * p.inv_kpg);
-            Ssh[b][kbl][tid & 7] = (kbl < nkb && kb == q * p.kpg) ? sv[0] : 0.f;
-        }
         lds_barrier();
 #pragma unroll
         for (int kbl = 0; kbl < CH; ++kbl) {
             if (kbl < nkb) {
                 int ai[MTK];
-                float af[MTK];
 #pragma unroll
-                for (int t = 0; t < MTK; ++t) {
-                    ai[t] = 0;
-                    af[t] = 0.f;
-                }
+                for (int t = 0; t < MTK; ++t) ai[t] = 0;
+                // FP path: the block's scale s' enters each word's FP16 sums directly
+                // (y += 2^pl s' h, one v_fma_mix_f32 per token)
+                SZ sz{};
+                if constexpr (!INT8) sz = decode_sz(p, mw.w[kbl]);
 #pragma unroll
                 for (int pl = 0; pl < BITS; ++pl) {
                     short2_v a16[4] = {short2_v{0, 0}, short2_v{0, 0}, short2_v{0, 0}, short2_v{0, 0}};
                     const uint32_t wd[4] = {w[kbl][pl].x, w[kbl][pl].y, w[kbl][pl].z, w[kbl][pl].w};
+                    const float sc = INT8 ? 0.f : sz.sp * (float)(1 << pl);  // exact scaling by 2^pl
 #pragma unroll
                     for (int d = 0; d < 4; ++d) {
-                        const uint32_t lo = (wd[d] << 4) & 0xF0F0F0F0u, hi = wd[d] & 0xF0F0F0F0u;
-                        uint4 h;  // FP path: sum of this word's 8 entries per token, packed FP16
+                        const uint32_t lo = wd[d] << 4, hi = wd[d];
+                        uint4 h, e0;  // FP path: sum of this word's 8 entries per token, packed FP16
 #pragma unroll
                         for (int k = 0; k < 8; ++k) {
-                            const uint32_t src = (k & 1) ? hi : lo;
-                            const uint32_t off = (src >> (8 * (k >> 1))) & 0xFFu;
+                            const uint32_t off = nib_off((k & 1) ? hi : lo, k >> 1);
                             const int g = d * 8 + k;  // groups 2j (low nibble) and 2j + 1 (high nibble) of byte j
                             const uint4 e = *(const uint4 *)(Fb + (kbl * GPB + g) * 256 + off);
                             if constexpr (INT8) {
@@ -261,12 +315,14 @@ __global__ __launch_bounds__(256) void lut_mtok_kernel(LutParams p, int wfmt, in
                                 a16[2] += __builtin_bit_cast(short2_v, e.z);
                                 a16[3] += __builtin_bit_cast(short2_v, e.w);
                             } else if (k == 0) {
-                                h = e;
+                                e0 = e;
+                            } else if (k == 1) {
+                                h = pk_sum4(e0, e);
                             } else {
                                 pk_add4(h, e);
                             }
                         }
-                        if constexpr (!INT8) fma_mix8(af, h, (float)(1 << pl));  // af += 2^pl * h (exact scaling)
+                        if constexpr (!INT8) fma_mix8(yf, h, sc);
                     }
                     if constexpr (INT8) {
 #pragma unroll
@@ -279,12 +335,15 @@ __global__ __launch_bounds__(256) void lut_mtok_kernel(LutParams p, int wfmt, in
                 if constexpr (INT8) {
 #pragma unroll
                     for (int t = 0; t < MTK; ++t) yi[t] += ai[t];
-                } else {
-                    const SZ sz = decode_sz(p, mw[kbl]);
+                } else if (need_s) {
+                    // the zero-point term enters with the first block of each group only
+                    if (kc + kbl == mw.q[kbl] * p.kpg) {
+                        const float nspz = -(sz.sp * sz.zp);
 #pragma unroll
-                    for (int t = 0; t < MTK; ++t) {
-                        yf[t] = fmaf(sz.sp, af[t], yf[t]);
-                        if (need_s) yf[t] -= (sz.sp * sz.zp) * Ssh[b][kbl][t];
+                        for (int t = 0; t < MTK; ++t) {
+                            const float st = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(sv[0]), kbl * MTK + t));
+                            yf[t] = fmaf(nspz, st, yf[t]);
+                        }
                     }
                 }
             }
@@ -294,18 +353,15 @@ __global__ __launch_bounds__(256) void lut_mtok_kernel(LutParams p, int wfmt, in
     // INT8 ternary: the activation sums S[m][0], added once (first K split)
     if (INT8 && split == 0 && wfmt == LUTGEMM_WFMT_TERNARY) {
 #pragma unroll
-        for (int t = 0; t < MTK; ++t) {
-            const int64_t row = (m0 + t < p.M) ? m0 + t : p.M - 1;
-            yi[t] = ((const int *)p.S)[lane_value(row * p.Q)];
-        }
+        for (int t = 0; t < MTK; ++t) yi[t] = ((const int *)p.S)[lane_value(row_of(t) * p.Q)];
     }
-    const int64_t last = kbA + (kbB - 1 - kbA) / CH * CH;
+    const int last = kbA + (kbB - 1 - kbA) / CH * CH;
     SD sdA, sdB;
     WW wA, wB;
     MW mwA, mwB;
     SV svA, svB;
     load(kbA, sdA, wA, mwA, svA);
-    for (int64_t kc = kbA; kc < kbB; kc += 2 * CH) {
+    for (int kc = kbA; kc < kbB; kc += 2 * CH) {
         load(kc + CH < last ? kc + CH : last, sdB, wB, mwB, svB);
         process(kc, sdA, wA, mwA, svA, 0);
         if (kc + CH >= kbB) break;
