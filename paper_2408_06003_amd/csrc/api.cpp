@@ -91,7 +91,8 @@ namespace lutgemm {
 // i.e. most table reuse) that still gives at least `target` workgroups, and
 // split K across workgroups only when even the narrowest one does not.
 // Several tokens: 8 tokens per workgroup of 256 columns, K split only when the
-// token x column grid is smaller than 4 x `target`.
+// token x column grid is smaller than 8 x `target` (five workgroups fit on a CU;
+// at M = 16 the K-split partials cost less than the shorter K ranges save).
 LutPlan plan_lut(const Layout &L, int64_t M) {
     LutPlan P{};
     const int64_t target = env_int("LUTGEMM_TARGET_BLOCKS", 256);
@@ -174,7 +175,7 @@ LutPlan plan_lut(const Layout &L, int64_t M) {
         P.n_tiles = L.N_pad / NTILE;
         const int64_t base = P.n_tiles * P.m_tiles;
         const int64_t ch = L.bits == 1 ? 2 : 4 / L.bits;  // 128-blocks per chunk of the kernel
-        const int64_t mt_target = env_int("LUTGEMM_MT_TARGET", 4) * target;
+        const int64_t mt_target = env_int("LUTGEMM_MT_TARGET", 8) * target;
         int64_t splits = 1;
         if (base < mt_target) splits = (mt_target + base - 1) / base;
         const int64_t max_splits = (L.KB + ch - 1) / ch;  // at least one chunk per split
