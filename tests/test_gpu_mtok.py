@@ -1,0 +1,75 @@
+"""Multi-token LUT kernel (M >= 3) across metadata layouts, group sizes, ragged chunks
+and forced K splits: every output against the oracle (FP paths within the FP bar,
+INT8 path bit-exact), FP16 and FP32 outputs, and run-to-run bitwise determinism.
+
+The cases are chosen for the kernel's bookkeeping: the zero-point term of Eq. 3
+enters once per quantization group (groups of 4 blocks split mid-group, per-tensor
+groups that only the first split sees), chunks of two 128-blocks with an odd block
+count, token tiles of 8 with 3 and 5 live rows, and K splits that leave a short last
+range.
+"""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+
+import oracle
+import workloads as W
+from helpers import GpuProblem, assert_fp_close
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+if not torch.cuda.is_available():
+    pytest.skip("no GPU", allow_module_level=True)
+
+import paper_2408_06003_amd as L  # noqa: E402,F401  (fails loudly when the HIP library is missing)
+
+FP_CASES = [
+    # (weight format, bits, group, FP32 per-tensor scale, M, K, N, forced K splits)
+    (W.WFMT_TERNARY, 2, 0, True, 11, 2048, 300, 0),     # per-tensor FP32 s, z' = -1
+    (W.WFMT_TERNARY, 2, 0, True, 11, 2048, 300, 3),     # ... zero-point term in the first split only
+    (W.WFMT_UINT, 2, 512, False, 9, 2048, 520, 3),      # groups of 4 blocks, splits of 6 blocks
+    (W.WFMT_UINT, 4, 1024, False, 20, 1024, 257, 2),    # per-channel, one block per chunk
+    (W.WFMT_BINARY, 1, 256, False, 13, 1536, 300, 5),   # binary group scales (z' = 0)
+    (W.WFMT_UINT, 1, 128, False, 8, 1152, 300, 0),      # 9 blocks: the last chunk holds one
+    (W.WFMT_UINT, 2, 128, False, 3, 1152, 64, 2),       # 3 live rows of 8, a single column tile
+    (W.WFMT_UINT, 4, 256, False, 45, 2048, 700, 0),     # 5 live rows in the last token tile
+]
+
+
+@pytest.mark.parametrize("wfmt,bits,G,fp32,M,K,N,splits", FP_CASES)
+def test_multi_token_fp_layouts(wfmt, bits, G, fp32, M, K, N, splits, monkeypatch):
+    if splits:
+        monkeypatch.setenv("LUTGEMM_MT_SPLITS", str(splits))
+    what = f"wfmt={wfmt} b={bits} G={G} M={M} K={K} N={N} splits={splits}"
+    print(f"\n[case] multi-token FP {what}", flush=True)
+    inp = W.make_custom(wfmt, bits, G, W.ACT_FP16, M=M, K=K, N=N, seed=M + K + N + splits, scale_fp32=fp32)
+    gp = GpuProblem(inp)
+    ref = oracle.reference_output(inp)
+    y32 = gp.lut(out_dtype=torch.float32)
+    fro, mx = assert_fp_close(y32.cpu().numpy(), ref, what)
+    print(f"[err] {what}: relFro {fro:.3e} max/rms {mx:.3e}", flush=True)
+    assert_fp_close(gp.lut(out_dtype=torch.float16).float().cpu().numpy(), ref, what + " fp16 out")
+    assert torch.equal(gp.lut(out_dtype=torch.float32), y32), f"{what}: two runs differ bitwise"
+
+
+INT_CASES = [
+    # (weight format, bits, group, FP32 per-tensor scale, M, K, N, forced K splits)
+    (W.WFMT_TERNARY, 2, 0, True, 10, 1152, 300, 3),
+    (W.WFMT_TERNARY, 2, 0, True, 21, 2048, 513, 0),
+    (W.WFMT_BINARY, 1, 1536, False, 9, 1536, 300, 2),
+]
+
+
+@pytest.mark.parametrize("wfmt,bits,G,fp32,M,K,N,splits", INT_CASES)
+def test_multi_token_int8_layouts(wfmt, bits, G, fp32, M, K, N, splits, monkeypatch):
+    if splits:
+        monkeypatch.setenv("LUTGEMM_MT_SPLITS", str(splits))
+    print(f"\n[case] multi-token INT8 wfmt={wfmt} b={bits} G={G} M={M} K={K} N={N} splits={splits}", flush=True)
+    inp = W.make_custom(wfmt, bits, G, W.ACT_INT8, M=M, K=K, N=N, seed=M + K + N + splits, scale_fp32=fp32)
+    gp = GpuProblem(inp)
+    acc_ref, y_ref = oracle.reference_output(inp)
+    yi = gp.lut(out_dtype=torch.int32).cpu().numpy()
+    yf = gp.lut(out_dtype=torch.float32).cpu().numpy()
+    assert np.array_equal(yi.astype(np.int64), acc_ref), "INT32 accumulator differs from the oracle"
+    assert np.array_equal(yf, y_ref), "FP32 scaled output differs from the oracle"
