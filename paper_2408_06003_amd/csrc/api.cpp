@@ -174,7 +174,7 @@ LutPlan plan_lut(const Layout &L, int64_t M) {
         P.m_tiles = (M + P.mt - 1) / P.mt;
         P.n_tiles = L.N_pad / NTILE;
         const int64_t base = P.n_tiles * P.m_tiles;
-        const int64_t ch = L.bits == 1 ? 2 : 4 / L.bits;  // 128-blocks per chunk of the kernel
+        const int64_t ch = L.bits == 1 ? 1 : 4 / L.bits;  // 128-blocks per chunk of the kernel
         const int64_t mt_target = env_int("LUTGEMM_MT_TARGET", 8) * target;
         int64_t splits = 1;
         if (base < mt_target) splits = (mt_target + base - 1) / base;
