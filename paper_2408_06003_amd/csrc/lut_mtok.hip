@@ -44,6 +44,24 @@ __device__ __forceinline__ uint32_t neg16x2(uint32_t x) {
     return x ^ 0x80008000u;  // FP16: flip both sign bits (exact)
 }
 
+// Raw buffer resource over `bytes` bytes at `base` (stride 0; a load at or past the
+// extent returns 0).  Loads through it take a 32-bit lane offset and a
+// workgroup-uniform scalar offset, so they need no 64-bit address arithmetic.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buf_rsrc(const void *base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)bytes, 0x00020000);
+}
+__device__ __forceinline__ uint32_t buf_u32(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+    return __builtin_amdgcn_raw_buffer_load_b32(r, (int)voff, (int)soff, 0);
+}
+__device__ __forceinline__ uint32_t buf_u16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+    return __builtin_amdgcn_raw_buffer_load_b16(r, (int)voff, (int)soff, 0);
+}
+__device__ __forceinline__ uint4 buf_u128(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+    typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+    const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, (int)voff, (int)soff, 0);
+    return make_uint4(v.x, v.y, v.z, v.w);
+}
+
 // (x >> 8 j) & 0xF0 for a compile-time byte j (after unrolling) in one SDWA
 // instruction: the high nibble of byte j of x, times 16, i.e. the byte offset of
 // that Eq. 6 index's row in a token-interleaved table.  (The compiler emits a
@@ -172,16 +190,23 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(TQ ? 1 : (B
     const bool need_s = !INT8 && wfmt != LUTGEMM_WFMT_BINARY;
     // Token rows past M repeat row M - 1: their sums are computed but never stored.
     auto row_of = [&](int t) { return (m0 + t < p.M) ? m0 + t : p.M - 1; };
-    // Addresses: the workgroup-uniform part (token row, chunk, block, quantization
-    // group) stays in scalar registers; lanes add 32-bit offsets that do not change
-    // from chunk to chunk, so the loads cost almost no vector instructions.
+    // Loads go through buffer resources: the workgroup-uniform part of each address
+    // (token row, chunk, block, quantization group) is a scalar offset, lanes add
+    // 32-bit offsets, so the loads cost almost no vector instructions.  Extents: the
+    // tile's live token rows (K < 2^20: under 2^25 bytes), one chunk of planes.
+    const int64_t J = p.J;
+    const uint32_t rows_live = (uint32_t)((p.M - m0) < MTK ? (p.M - m0) : MTK);
+    constexpr uint32_t TB = TQ ? 8 : 16;  // bytes per stored half table
+    const __amdgpu_buffer_rsrc_t rT = buf_rsrc((const char *)p.T + m0 * J * TB, rows_live * (uint32_t)J * TB);
+    const __amdgpu_buffer_rsrc_t rTs = buf_rsrc(TQ ? (const void *)(p.tsc + m0 * J) : (const void *)p.T,
+                                                TQ ? rows_live * (uint32_t)J * 4u : 0u);
+    const __amdgpu_buffer_rsrc_t rS = buf_rsrc((const float *)p.S + m0 * p.Q, rows_live * (uint32_t)p.Q * 4u);
     const uint32_t n_meta = p.per_tensor ? 0u : n;  // metadata column (0: one pair per tensor)
     // quantization group of a 128-block (workgroup-uniform: moved to a scalar register,
     // so that what depends on it is scalar arithmetic)
     auto group_of = [&](int kb) {
         return __builtin_amdgcn_readfirstlane((int)(((float)kb + 0.5f) * p.inv_kpg));
     };
-
     // staged table words: entries 2ip, 2ip + 1 of a token's half table (FP16 / INT16
     // pair), or with INT8-quantized tables (TQ) their two codes and the table's scale
     typedef std::conditional_t<TQ, uint2, uint32_t> SDE;
@@ -203,27 +228,30 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(TQ ? 1 : (B
             const uint32_t tab = (uint32_t)(kbc * GPB + g);  // the lane's table within the chunk
 #pragma unroll
             for (int t = 0; t < MTK; ++t) {
-                const int64_t base = row_of(t) * p.J + (int64_t)kc * GPB;
+                const uint32_t so = ((uint32_t)(row_of(t) - m0) * (uint32_t)J + (uint32_t)kc * GPB) * TB;
                 if constexpr (TQ)
-                    sd[r][t] = make_uint2(((const uint16_t *)p.T + 4 * base)[4 * tab + ip],  // 8 codes per table
-                                          __float_as_uint((p.tsc + base)[tab]));
+                    sd[r][t] = make_uint2(buf_u16(rT, tab * 8 + ip * 2, so), buf_u32(rTs, tab * 4, so / 2));
                 else
-                    sd[r][t] = ((const uint32_t *)(p.T + base))[4 * tab + ip];
+                    sd[r][t] = buf_u32(rT, tab * 16 + ip * 4, so);
             }
         }
+        const __amdgpu_buffer_rsrc_t rW =
+            buf_rsrc(p.planes + (int64_t)kc * BITS * p.N_pad, (uint32_t)(CH * BITS) * (uint32_t)p.N_pad * 16u);
 #pragma unroll
         for (int kbl = 0; kbl < CH; ++kbl) {
             const int kbc = kbl < nkb ? kbl : nkb - 1;
 #pragma unroll
-            for (int t = 0; t < BITS; ++t) w[kbl][t] = (p.planes + ((int64_t)(kc + kbc) * BITS + t) * p.N_pad)[n];
+            for (int t = 0; t < BITS; ++t)
+                w[kbl][t] = buf_u128(rW, n * 16u, (uint32_t)(kbc * BITS + t) * (uint32_t)p.N_pad * 16u);
         }
         if constexpr (!INT8) {
 #pragma unroll
             for (int kbl = 0; kbl < CH; ++kbl) {
                 const int kbc = kbl < nkb ? kbl : nkb - 1;
                 const int q = group_of(kc + kbc);
-                const uint32_t *mb = (const uint32_t *)p.meta + (p.per_tensor ? 0 : (int64_t)q * p.N_pad);
-                mw.w[kbl] = make_uint2(mb[n_meta], (mb + p.per_tensor)[n_meta]);
+                const __amdgpu_buffer_rsrc_t rM =
+                    buf_rsrc((const uint32_t *)p.meta + (p.per_tensor ? 0 : (int64_t)q * p.N_pad), (uint32_t)p.N_pad * 4u);
+                mw.w[kbl] = make_uint2(buf_u32(rM, n_meta * 4u, 0), buf_u32(rM, n_meta * 4u, p.per_tensor ? 4u : 0u));
                 mw.q[kbl] = q;
             }
             // one activation sum per (block, token): lanes 0 .. 8 CH - 1 of every wavefront,
@@ -231,8 +259,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(TQ ? 1 : (B
             const int ln = tid & 63;
             const int t = ln & 7;
             const int q = (CH == 1 || ln < 8) ? mw.q[0] : mw.q[CH - 1];
-            const uint32_t rt = (uint32_t)((m0 + t < p.M) ? t : p.M - 1 - m0);
-            sv[0] = ((const float *)p.S + m0 * p.Q)[rt * (uint32_t)p.Q + (uint32_t)q];
+            const uint32_t rt = (uint32_t)(row_of(t) - m0);
+            sv[0] = __uint_as_float(buf_u32(rS, (rt * (uint32_t)p.Q + (uint32_t)q) * 4u, 0));
         }
     };
 
