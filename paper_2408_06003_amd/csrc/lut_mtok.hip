@@ -103,6 +103,19 @@ __device__ __forceinline__ uint4 pk_sum4(uint4 a, uint4 b) {
     return h;
 }
 
+// 2 a + b as four packed FP16 pairs (8 tokens): two bit-planes' word sums combined.
+__device__ __forceinline__ uint4 pk_fma2x4(uint4 a, uint4 b) {
+    uint4 h;
+    const uint32_t two = 0x40004000u;  // FP16 2.0 in both halves
+    asm("v_pk_fma_f16 %0, %4, %12, %8\n\t"
+        "v_pk_fma_f16 %1, %5, %12, %9\n\t"
+        "v_pk_fma_f16 %2, %6, %12, %10\n\t"
+        "v_pk_fma_f16 %3, %7, %12, %11"
+        : "=&v"(h.x), "=&v"(h.y), "=&v"(h.z), "=&v"(h.w)
+        : "v"(a.x), "v"(a.y), "v"(a.z), "v"(a.w), "v"(b.x), "v"(b.y), "v"(b.z), "v"(b.w), "s"(two));
+    return h;
+}
+
 // h += e as four packed FP16 pairs (8 tokens), one statement per read for the same
 // reason as fma_mix8 below.
 __device__ __forceinline__ void pk_add4(uint4 &h, uint4 e) {
@@ -315,63 +328,76 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(TQ ? 1 : (B
         lds_barrier();
 #pragma unroll
         for (int kbl = 0; kbl < CH; ++kbl) {
-            if (kbl < nkb) {
-                int ai[MTK];
-#pragma unroll
-                for (int t = 0; t < MTK; ++t) ai[t] = 0;
-                // FP path: the block's scale s' enters each word's FP16 sums directly
-                // (y += 2^pl s' h, one v_fma_mix_f32 per token)
-                SZ sz{};
-                if constexpr (!INT8) sz = decode_sz(p, mw.w[kbl]);
+            if (kbl >= nkb) continue;
+            if constexpr (INT8) {
+                // INT8 path: per plane, the 32 entries of the block summed exactly in packed
+                // INT16 (|sum| <= 32 x 508 < 2^15), then widened with the plane weight 2^pl
 #pragma unroll
                 for (int pl = 0; pl < BITS; ++pl) {
                     short2_v a16[4] = {short2_v{0, 0}, short2_v{0, 0}, short2_v{0, 0}, short2_v{0, 0}};
                     const uint32_t wd[4] = {w[kbl][pl].x, w[kbl][pl].y, w[kbl][pl].z, w[kbl][pl].w};
-                    const float sc = INT8 ? 0.f : sz.sp * (float)(1 << pl);  // exact scaling by 2^pl
 #pragma unroll
                     for (int d = 0; d < 4; ++d) {
                         const uint32_t lo = wd[d] << 4, hi = wd[d];
-                        uint4 h, e0;  // FP path: sum of this word's 8 entries per token, packed FP16
 #pragma unroll
                         for (int k = 0; k < 8; ++k) {
                             const uint32_t off = nib_off((k & 1) ? hi : lo, k >> 1);
                             const int g = d * 8 + k;  // groups 2j (low nibble) and 2j + 1 (high nibble) of byte j
                             const uint4 e = *(const uint4 *)(Fb + (kbl * GPB + g) * 256 + off);
-                            if constexpr (INT8) {
-                                a16[0] += __builtin_bit_cast(short2_v, e.x);
-                                a16[1] += __builtin_bit_cast(short2_v, e.y);
-                                a16[2] += __builtin_bit_cast(short2_v, e.z);
-                                a16[3] += __builtin_bit_cast(short2_v, e.w);
-                            } else if (k == 0) {
-                                e0 = e;
-                            } else if (k == 1) {
-                                h = pk_sum4(e0, e);
-                            } else {
-                                pk_add4(h, e);
-                            }
+                            a16[0] += __builtin_bit_cast(short2_v, e.x);
+                            a16[1] += __builtin_bit_cast(short2_v, e.y);
+                            a16[2] += __builtin_bit_cast(short2_v, e.z);
+                            a16[3] += __builtin_bit_cast(short2_v, e.w);
                         }
-                        if constexpr (!INT8) fma_mix8(yf, h, sc);
                     }
-                    if constexpr (INT8) {
 #pragma unroll
-                        for (int j = 0; j < 4; ++j) {
-                            ai[2 * j] += (int)a16[j].x << pl;
-                            ai[2 * j + 1] += (int)a16[j].y << pl;
-                        }
+                    for (int j = 0; j < 4; ++j) {
+                        yi[2 * j] += (int)a16[j].x << pl;
+                        yi[2 * j + 1] += (int)a16[j].y << pl;
                     }
                 }
-                if constexpr (INT8) {
+            } else {
+                // FP path, per weight word: the 8 entries one plane's word selects summed in
+                // packed FP16, pairs of planes combined as h_2i + 2 h_2i+1 (v_pk_fma_f16),
+                // and each result added into the FP32 outputs with factor 4^i s' (one
+                // v_fma_mix_f32 per token)
+                const SZ sz = decode_sz(p, mw.w[kbl]);
 #pragma unroll
-                    for (int t = 0; t < MTK; ++t) yi[t] += ai[t];
-                } else if (need_s) {
-                    // the zero-point term enters with the first block of each group only
-                    if (kc + kbl == mw.q[kbl] * p.kpg) {
-                        const float nspz = -(sz.sp * sz.zp);
+                for (int d = 0; d < 4; ++d) {
+                    uint4 hp[BITS];
 #pragma unroll
-                        for (int t = 0; t < MTK; ++t) {
-                            const float st = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(sv[0]), kbl * MTK + t));
-                            yf[t] = fmaf(nspz, st, yf[t]);
+                    for (int pl = 0; pl < BITS; ++pl) {
+                        const uint32_t wv = d == 0 ? w[kbl][pl].x : d == 1 ? w[kbl][pl].y : d == 2 ? w[kbl][pl].z : w[kbl][pl].w;
+                        const uint32_t lo = wv << 4, hi = wv;
+                        uint4 e0;
+#pragma unroll
+                        for (int k = 0; k < 8; ++k) {
+                            const uint32_t off = nib_off((k & 1) ? hi : lo, k >> 1);
+                            const int g = d * 8 + k;  // groups 2j (low nibble) and 2j + 1 (high nibble) of byte j
+                            const uint4 e = *(const uint4 *)(Fb + (kbl * GPB + g) * 256 + off);
+                            if (k == 0)
+                                e0 = e;
+                            else if (k == 1)
+                                hp[pl] = pk_sum4(e0, e);
+                            else
+                                pk_add4(hp[pl], e);
                         }
+                    }
+                    if constexpr (BITS == 1) {
+                        fma_mix8(yf, hp[0], sz.sp);
+                    } else {
+#pragma unroll
+                        for (int i = 0; i < BITS / 2; ++i)
+                            fma_mix8(yf, pk_fma2x4(hp[2 * i + 1], hp[2 * i]), sz.sp * (float)(1 << (2 * i)));
+                    }
+                }
+                // the zero-point term enters with the first block of each group only
+                if (need_s && kc + kbl == mw.q[kbl] * p.kpg) {
+                    const float nspz = -(sz.sp * sz.zp);
+#pragma unroll
+                    for (int t = 0; t < MTK; ++t) {
+                        const float st = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(sv[0]), kbl * MTK + t));
+                        yf[t] = fmaf(nspz, st, yf[t]);
                     }
                 }
             }
