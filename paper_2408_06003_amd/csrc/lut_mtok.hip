@@ -183,13 +183,15 @@ __device__ __forceinline__ Tile tile_of(uint32_t b, uint32_t n_tiles, uint32_t m
 }
 
 template <int BITS, bool INT8, bool TQ>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(TQ ? 1 : (BITS == 1 ? 6 : 5)))) void lut_mtok_kernel(LutParams p, int wfmt, int64_t n_tiles, int64_t m_tiles,
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(TQ ? 1 : (BITS == 1 ? 6 : 4)))) void lut_mtok_kernel(LutParams p, int wfmt, int64_t n_tiles, int64_t m_tiles,
                                                        int order) {
     constexpr int CH = BITS == 1 ? 1 : 4 / BITS;  // 128-blocks per chunk (b = 1: 16 KB of LDS, more workgroups per CU)
     constexpr int TASKS = CH * GPB * 4;           // staging tasks per chunk: (block, group, index pair)
     constexpr int TPL = (TASKS + 255) / 256;      // staging tasks per lane
     constexpr int BUF = CH * GPB * 256;           // LDS bytes of one table buffer (16 entries x 8 tokens x 2 B per group)
-    // 16 KB (b = 1, 4) or exactly 32 KB (b = 2, five workgroups in the 160 KB of a CU)
+    // 16 KB (b = 1, 4) or 32 KB (b = 2).  Occupancy hints: b = 1 keeps six workgroups per
+    // CU; b >= 2 measured faster at four, where the scheduler keeps more LDS reads in
+    // flight per wavefront
     __shared__ __attribute__((aligned(16))) char F[2 * BUF];
 
     const int tid = threadIdx.x;
