@@ -14,16 +14,21 @@
 // 508 < 2^15, exact), then widened to INT32 with the plane weight 2^t.  FP path:
 // the 8 entries selected by one weight word (8 consecutive groups of one plane)
 // are summed in packed FP16 pairs (v_pk_add_f16, two tokens per instruction; the
-// tables are normalized to |T| < 4, so these sums stay below 32), and each such
-// sum is added into an FP32 accumulator per token scaled by 2^t (exact), with one
-// v_fma_mix_f32 per token.
+// tables are normalized to |T| < 4, so these sums stay below 32), the sums of
+// planes 2i and 2i + 1 are combined as h_2i + 2 h_2i+1 (v_pk_fma_f16), and each
+// result is added into the per-token FP32 outputs with factor 4^i s' (one
+// v_fma_mix_f32 per token).  The zero-point term s' z' S of Eq. 3 is applied by
+// the first block of each quantization group, the 8 tokens' sums S broadcast
+// from 8 lanes by readlane.
 //
 // K is walked in chunks of CH 128-blocks.  Everything a chunk needs from memory
 // (the 8 tokens' half-table words it stages, the weight words, the blocks'
 // metadata and zero-point sums) is loaded one chunk ahead into one of two
 // register buffers (used alternately, no copies, every load unconditional with
 // clamped indices so that waits count exactly), and the LDS tables are
-// double-buffered, so each chunk costs one barrier.  When the grid would not
+// double-buffered, so each chunk costs one barrier.  The loads go through buffer
+// resources: workgroup-uniform offsets in scalar registers, fixed 32-bit lane
+// offsets, no 64-bit address arithmetic in the loop.  When the grid would not
 // fill the GPU, K is split and lut_finalize_kernel sums the partials.
 #include <type_traits>
 
