@@ -351,7 +351,7 @@ __device__ __forceinline__ void store_out(const LutParams &p, int wfmt, int64_t 
 // last split clamped to it).  Unconditional loads, so all PB are in flight before
 // the first is used (a load under a condition makes the compiler wait for it
 // before issuing the next one).
-constexpr int PB = FIN_BATCH;
+template <int PB>
 __device__ __forceinline__ void load_partials(const LutParams &p, int64_t m_alloc, int64_t m, int64_t n, int s0,
                                               float (&v)[PB]) {
     const float *src = p.part + m * p.N_pad + n;
@@ -364,7 +364,7 @@ __device__ __forceinline__ void load_partials(const LutParams &p, int64_t m_allo
 }
 
 // Adds the loaded partials of splits s0 .. in split order.
-template <bool INT8>
+template <bool INT8, int PB>
 __device__ __forceinline__ void add_partials(const LutParams &p, int s0, const float (&v)[PB], float &sf, int &si) {
 #pragma unroll
     for (int j = 0; j < PB; ++j) {
@@ -375,6 +375,5 @@ __device__ __forceinline__ void add_partials(const LutParams &p, int s0, const f
             sf += in ? v[j] : 0.f;
     }
 }
-
 
 }  // namespace lutgemm

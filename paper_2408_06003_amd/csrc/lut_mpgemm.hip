@@ -21,23 +21,41 @@ namespace lutgemm {
 // needs a device-scope release per workgroup, i.e. an L2 write-back; measured on
 // MI355X that costs far more than this launch.)  The first PB partials are
 // requested before the epilogue operands, so the kernel waits about one memory
-// latency for up to PB splits.
-template <bool INT8>
-__global__ __launch_bounds__(64) void lut_finalize_kernel(LutParams p, int wfmt, int per_tensor_i,
+// latency for up to PB splits; PB is the smallest power of two covering the
+// splits (at most FIN_BATCH), so few splits issue few loads.  NT lanes per
+// workgroup, one per padded column.
+template <bool INT8, int PB, int NT>
+__global__ __launch_bounds__(NT) void lut_finalize_kernel(LutParams p, int wfmt, int per_tensor_i,
                                                           int64_t m_alloc) {
-    const int64_t n = (int64_t)blockIdx.x * 64 + threadIdx.x;
+    const int64_t n = (int64_t)blockIdx.x * NT + threadIdx.x;
     const int64_t m = blockIdx.y;
     float v[PB];
-    load_partials(p, m_alloc, m, n, 0, v);
+    load_partials<PB>(p, m_alloc, m, n, 0, v);
     const Epi ep = load_epi<INT8>(p, wfmt, m, n, false);
     float sf = 0.f;
     int si = 0;
-    add_partials<INT8>(p, 0, v, sf, si);
+    add_partials<INT8, PB>(p, 0, v, sf, si);
     for (int s0 = PB; s0 < p.splits; s0 += PB) {
-        load_partials(p, m_alloc, m, n, s0, v);
-        add_partials<INT8>(p, s0, v, sf, si);
+        load_partials<PB>(p, m_alloc, m, n, s0, v);
+        add_partials<INT8, PB>(p, s0, v, sf, si);
     }
     store_out<INT8>(p, wfmt, m, n, sf, si, ep);
+}
+
+template <bool INT8, int NT>
+static void launch_finalize_pb(const LutParams &p, const Layout &L, int pt, int64_t m_alloc, hipStream_t s) {
+    const dim3 grid((unsigned)(L.N_pad / NT), (unsigned)p.M);
+    const int sp = p.splits;
+    if (sp <= 4)
+        hipLaunchKernelGGL((lut_finalize_kernel<INT8, 4, NT>), grid, dim3(NT), 0, s, p, L.wfmt, pt, m_alloc);
+    else if (sp <= 8)
+        hipLaunchKernelGGL((lut_finalize_kernel<INT8, 8, NT>), grid, dim3(NT), 0, s, p, L.wfmt, pt, m_alloc);
+    else if (sp <= 16)
+        hipLaunchKernelGGL((lut_finalize_kernel<INT8, 16, NT>), grid, dim3(NT), 0, s, p, L.wfmt, pt, m_alloc);
+    else if (sp <= 32)
+        hipLaunchKernelGGL((lut_finalize_kernel<INT8, 32, NT>), grid, dim3(NT), 0, s, p, L.wfmt, pt, m_alloc);
+    else
+        hipLaunchKernelGGL((lut_finalize_kernel<INT8, FIN_BATCH, NT>), grid, dim3(NT), 0, s, p, L.wfmt, pt, m_alloc);
 }
 
 // ------------------------------------------------------------------ dispatch
@@ -61,12 +79,17 @@ int launch_lut(const LutParams &p, const Layout &L, const LutPlan &plan, void *s
 int launch_finalize(const LutParams &p, const Layout &L, const LutPlan &plan, void *stream) {
     hipStream_t s = (hipStream_t)stream;
     const int64_t m_alloc = plan.kind == 1 ? plan.m_tiles * plan.mt : p.M;
-    const dim3 grid((unsigned)(L.N_pad / 64), (unsigned)p.M);  // one lane per padded column
     const int pt = L.per_tensor ? 1 : 0;
-    if (L.act == LUTGEMM_ACT_INT8)
-        hipLaunchKernelGGL(lut_finalize_kernel<true>, grid, dim3(64), 0, s, p, L.wfmt, pt, m_alloc);
-    else
-        hipLaunchKernelGGL(lut_finalize_kernel<false>, grid, dim3(64), 0, s, p, L.wfmt, pt, m_alloc);
+    // single tokens: 64-lane workgroups spread the few columns over many CUs; several
+    // tokens: 256 lanes, a quarter of the workgroups
+    const bool wide = p.M > 2;
+    if (L.act == LUTGEMM_ACT_INT8) {
+        if (wide) launch_finalize_pb<true, 256>(p, L, pt, m_alloc, s);
+        else launch_finalize_pb<true, 64>(p, L, pt, m_alloc, s);
+    } else {
+        if (wide) launch_finalize_pb<false, 256>(p, L, pt, m_alloc, s);
+        else launch_finalize_pb<false, 64>(p, L, pt, m_alloc, s);
+    }
     return (int)hipGetLastError();
 }
 
