@@ -91,8 +91,8 @@ namespace lutgemm {
 // i.e. most table reuse) that still gives at least `target` workgroups, and
 // split K across workgroups only when even the narrowest one does not.
 // Several tokens: 8 tokens per workgroup of 256 columns, K split only when the
-// token x column grid is smaller than 8 x `target` (five workgroups fit on a CU;
-// at M = 16 the K-split partials cost less than the shorter K ranges save).
+// token x column grid is smaller than 8 x `target` workgroups (to twice that when the
+// K ranges stay at least 32 blocks long).
 LutPlan plan_lut(const Layout &L, int64_t M) {
     LutPlan P{};
     const int64_t target = env_int("LUTGEMM_TARGET_BLOCKS", 256);
@@ -177,7 +177,13 @@ LutPlan plan_lut(const Layout &L, int64_t M) {
         const int64_t ch = L.bits == 1 ? 1 : 4 / L.bits;  // 128-blocks per chunk of the kernel
         const int64_t mt_target = env_int("LUTGEMM_MT_TARGET", 8) * target;
         int64_t splits = 1;
-        if (base < mt_target) splits = (mt_target + base - 1) / base;
+        if (base < mt_target) {
+            splits = (mt_target + base - 1) / base;
+            // long K ranges stay long enough at twice the grid: take it (1-bit
+            // 256 x 28672 x 8192: 2 -> 4 splits, 383 -> 367 us); short ones (M = 16) do not
+            const int64_t s2 = (2 * mt_target + base - 1) / base;
+            if (L.KB / s2 >= 32) splits = s2;
+        }
         const int64_t max_splits = (L.KB + ch - 1) / ch;  // at least one chunk per split
         if (splits > max_splits) splits = max_splits;
         const int fs = env_int("LUTGEMM_MT_SPLITS", 0);
