@@ -73,3 +73,23 @@ def test_multi_token_int8_layouts(wfmt, bits, G, fp32, M, K, N, splits, monkeypa
     yf = gp.lut(out_dtype=torch.float32).cpu().numpy()
     assert np.array_equal(yi.astype(np.int64), acc_ref), "INT32 accumulator differs from the oracle"
     assert np.array_equal(yf, y_ref), "FP32 scaled output differs from the oracle"
+
+
+@pytest.mark.parametrize("splits", [5, 9, 17, 33, 65, 128])
+def test_multi_token_many_splits(splits, monkeypatch):
+    """K split into 5 .. 128 ranges: the finalize kernel's load batch (4 .. 64 partials,
+    looping when there are more) at every size it takes, FP and INT8 paths."""
+    monkeypatch.setenv("LUTGEMM_MT_SPLITS", str(splits))
+    print(f"\n[case] multi-token K splits={splits} (M=5, K=16384, N=200)", flush=True)
+    inp = W.make_custom(W.WFMT_BINARY, 1, 16384, W.ACT_FP16, M=5, K=16384, N=200, seed=300 + splits)
+    gp = GpuProblem(inp)
+    ref = oracle.reference_output(inp)
+    y32 = gp.lut(out_dtype=torch.float32)
+    assert_fp_close(y32.cpu().numpy(), ref, f"splits={splits}")
+    assert torch.equal(gp.lut(out_dtype=torch.float32), y32), f"splits={splits}: two runs differ bitwise"
+    inpi = W.make_custom(W.WFMT_TERNARY, 2, 0, W.ACT_INT8, M=5, K=16384, N=200, seed=400 + splits,
+                         scale_fp32=True)
+    gpi = GpuProblem(inpi)
+    acc_ref, y_ref = oracle.reference_output(inpi)
+    assert np.array_equal(gpi.lut(out_dtype=torch.int32).cpu().numpy().astype(np.int64), acc_ref)
+    assert np.array_equal(gpi.lut(out_dtype=torch.float32).cpu().numpy(), y_ref)
