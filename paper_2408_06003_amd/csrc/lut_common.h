@@ -255,10 +255,6 @@ __device__ __forceinline__ SZ decode_sz(const LutParams &p, uint2 mw) {
     return r;
 }
 
-__device__ __forceinline__ SZ load_sz(const LutParams &p, int q, int64_t n) {
-    return decode_sz(p, load_meta_words(p, q, n));
-}
-
 // Epilogue operands of one 128-block kb and column n, as raw loads that can be
 // issued long before they are used: the metadata word(s) of the block's
 // quantization group and the group's activation sum S[m][q] (the zero-point term
