@@ -183,6 +183,11 @@ LutPlan plan_lut(const Layout &L, int64_t M) {
             // 256 x 28672 x 8192: 2 -> 4 splits, 383 -> 367 us); short ones (M = 16) do not
             const int64_t s2 = (2 * mt_target + base - 1) / base;
             if (L.KB / s2 >= 32) splits = s2;
+            // but each split keeps about 6 or more block-planes of lookups: shorter K
+            // ranges spend more on pipeline fill and partial sums than the extra
+            // workgroups gain (M = 3-8 decode shapes: 8-15 % faster than 19-64 splits)
+            const int64_t cap = L.KB * L.bits / 6 > 1 ? L.KB * L.bits / 6 : 1;
+            if (splits > cap) splits = cap;
         }
         const int64_t max_splits = (L.KB + ch - 1) / ch;  // at least one chunk per split
         if (splits > max_splits) splits = max_splits;

@@ -439,8 +439,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(TQ ? 1 : (B
     }
     const int64_t m_alloc = m_tiles * MTK;
 #pragma unroll
-    for (int t = 0; t < MTK; ++t)
-        p.part[((int64_t)split * m_alloc + m0 + t) * p.N_pad + n] = INT8 ? __int_as_float(yi[t]) : yf[t];
+    for (int t = 0; t < MTK; ++t)  // the finalize kernel reads rows below M only
+        if (t < rows) p.part[((int64_t)split * m_alloc + m0 + t) * p.N_pad + n] = INT8 ? __int_as_float(yi[t]) : yf[t];
 }
 
 int launch_mtok(const LutParams &p, const Layout &L, const LutPlan &plan, void *stream) {
