@@ -170,7 +170,10 @@ LutPlan plan_lut(const Layout &L, int64_t M) {
         P.splits = (int)((L.KB + kbs - 1) / kbs);
     } else {
         P.kind = 1;
-        P.mt = 8;  // tokens per workgroup of the multi-token kernel (lut_mtok.hip)
+        // tokens per workgroup of the multi-token kernel (lut_mtok.hip): 16 from M = 16 on
+        // (one decoded index serves two token halves), except with INT8-quantized tables
+        const int mt16 = env_int("LUTGEMM_MT16", 1);
+        P.mt = (M >= 16 && L.act != LUTGEMM_ACT_FP16_LUT8 && mt16) ? 16 : 8;
         P.m_tiles = (M + P.mt - 1) / P.mt;
         P.n_tiles = L.N_pad / NTILE;
         const int64_t base = P.n_tiles * P.m_tiles;

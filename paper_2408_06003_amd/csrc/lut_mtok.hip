@@ -121,6 +121,20 @@ __device__ __forceinline__ uint4 pk_fma2x4(uint4 a, uint4 b) {
     return h;
 }
 
+// ha += ea and hb += eb (two token halves), one statement for both reads of an index
+__device__ __forceinline__ void pk_add4x2(uint4 &ha, uint4 ea, uint4 &hb, uint4 eb) {
+    asm("v_pk_add_f16 %0, %0, %8\n\t"
+        "v_pk_add_f16 %1, %1, %9\n\t"
+        "v_pk_add_f16 %2, %2, %10\n\t"
+        "v_pk_add_f16 %3, %3, %11\n\t"
+        "v_pk_add_f16 %4, %4, %12\n\t"
+        "v_pk_add_f16 %5, %5, %13\n\t"
+        "v_pk_add_f16 %6, %6, %14\n\t"
+        "v_pk_add_f16 %7, %7, %15"
+        : "+v"(ha.x), "+v"(ha.y), "+v"(ha.z), "+v"(ha.w), "+v"(hb.x), "+v"(hb.y), "+v"(hb.z), "+v"(hb.w)
+        : "v"(ea.x), "v"(ea.y), "v"(ea.z), "v"(ea.w), "v"(eb.x), "v"(eb.y), "v"(eb.z), "v"(eb.w));
+}
+
 // h += e as four packed FP16 pairs (8 tokens), one statement per read for the same
 // reason as fma_mix8 below.
 __device__ __forceinline__ void pk_add4(uint4 &h, uint4 e) {
@@ -135,7 +149,7 @@ __device__ __forceinline__ void pk_add4(uint4 &h, uint4 e) {
 // af[t] += sc * (FP16 entry of token t in e), t = 0..7: eight v_fma_mix_f32 in one
 // statement, so each LDS read is consumed as a whole (the compiler would otherwise
 // regroup the accumulations by token and keep every read of a block live).
-__device__ __forceinline__ void fma_mix8(float (&af)[MTK], uint4 e, float sc) {
+__device__ __forceinline__ void fma_mix8(float *af, uint4 e, float sc) {
     asm("v_fma_mix_f32 %0, %8, %12, %0 op_sel_hi:[1,0,0]\n\t"
         "v_fma_mix_f32 %1, %8, %12, %1 op_sel:[1,0,0] op_sel_hi:[1,0,0]\n\t"
         "v_fma_mix_f32 %2, %9, %12, %2 op_sel_hi:[1,0,0]\n\t"
@@ -187,23 +201,29 @@ __device__ __forceinline__ Tile tile_of(uint32_t b, uint32_t n_tiles, uint32_t m
     return t;
 }
 
-template <int BITS, bool INT8, bool TQ>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(TQ ? 1 : (BITS == 1 ? 6 : 4)))) void lut_mtok_kernel(LutParams p, int wfmt, int64_t n_tiles, int64_t m_tiles,
+// NH halves of 8 tokens per workgroup (NH = 2: one decoded index serves two 16-byte
+// reads, the second at a fixed +256-byte offset, so index decoding, weight loads and
+// metadata are shared by 16 tokens).
+template <int BITS, bool INT8, bool TQ, int NH>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(TQ ? 1 : (BITS == 1 && NH == 1 ? 6 : 4)))) void lut_mtok_kernel(LutParams p, int wfmt, int64_t n_tiles, int64_t m_tiles,
                                                        int order) {
-    constexpr int CH = BITS == 1 ? 1 : 4 / BITS;  // 128-blocks per chunk (b = 1: 16 KB of LDS, more workgroups per CU)
+    constexpr int MT = MTK * NH;                  // tokens per workgroup
+    // 128-blocks per chunk (b = 1 and 16 tokens: 16 KB of LDS per buffer, more workgroups per CU)
+    constexpr int CH = (BITS == 1 || NH == 2) ? 1 : 4 / BITS;
     constexpr int TASKS = CH * GPB * 4;           // staging tasks per chunk: (block, group, index pair)
     constexpr int TPL = (TASKS + 255) / 256;      // staging tasks per lane
-    constexpr int BUF = CH * GPB * 256;           // LDS bytes of one table buffer (16 entries x 8 tokens x 2 B per group)
-    // 16 KB (b = 1, 4) or 32 KB (b = 2).  Occupancy hints: b = 1 keeps six workgroups per
-    // CU; b >= 2 measured faster at four, where the scheduler keeps more LDS reads in
-    // flight per wavefront
+    constexpr int GST = 256 * NH;                 // LDS bytes of one group (16 entries x 8 tokens x 2 B per half)
+    constexpr int BUF = CH * GPB * GST;           // LDS bytes of one table buffer
+    // 16 KB (b = 1, 4, 8 tokens) or 32 KB.  Occupancy hints: b = 1 with 8 tokens keeps six
+    // workgroups per CU; the others measured faster at four, where the scheduler keeps
+    // more LDS reads in flight per wavefront
     __shared__ __attribute__((aligned(16))) char F[2 * BUF];
 
     const int tid = threadIdx.x;
     const Tile tl = tile_of(blockIdx.x, (uint32_t)n_tiles, (uint32_t)m_tiles, order);
     const uint32_t n = (uint32_t)(tl.nt * NTILE + tid);
     const int split = tl.split;
-    const int64_t m0 = tl.mt * MTK;
+    const int64_t m0 = tl.mt * MT;
     // 128-block indices fit in 32 bits (K < 2^38)
     const int kbA = split * p.kbs;
     const int kbB = (kbA + p.kbs < (int)p.KB) ? kbA + p.kbs : (int)p.KB;
@@ -215,7 +235,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(TQ ? 1 : (B
     // 32-bit offsets, so the loads cost almost no vector instructions.  Extents: the
     // tile's live token rows (K < 2^20: under 2^25 bytes), one chunk of planes.
     const int64_t J = p.J;
-    const uint32_t rows_live = (uint32_t)((p.M - m0) < MTK ? (p.M - m0) : MTK);
+    const uint32_t rows_live = (uint32_t)((p.M - m0) < MT ? (p.M - m0) : MT);
     constexpr uint32_t TB = TQ ? 8 : 16;  // bytes per stored half table
     const __amdgpu_buffer_rsrc_t rT = buf_rsrc((const char *)p.T + m0 * J * TB, rows_live * (uint32_t)J * TB);
     const __amdgpu_buffer_rsrc_t rTs = buf_rsrc(TQ ? (const void *)(p.tsc + m0 * J) : (const void *)p.T,
@@ -230,7 +250,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(TQ ? 1 : (B
     // staged table words: entries 2ip, 2ip + 1 of a token's half table (FP16 / INT16
     // pair), or with INT8-quantized tables (TQ) their two codes and the table's scale
     typedef std::conditional_t<TQ, uint2, uint32_t> SDE;
-    typedef SDE SD[TPL][MTK];
+    typedef SDE SD[TPL][MT];
     typedef uint4 WW[CH][BITS];
     struct MW {
         uint2 w[CH];  // metadata words of each block's group
@@ -247,7 +267,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(TQ ? 1 : (B
             const int kbc = kbl < nkb ? kbl : nkb - 1;
             const uint32_t tab = (uint32_t)(kbc * GPB + g);  // the lane's table within the chunk
 #pragma unroll
-            for (int t = 0; t < MTK; ++t) {
+            for (int t = 0; t < MT; ++t) {
                 const uint32_t so = ((uint32_t)(row_of(t) - m0) * (uint32_t)J + (uint32_t)kc * GPB) * TB;
                 if constexpr (TQ)
                     sd[r][t] = make_uint2(buf_u16(rT, tab * 8 + ip * 2, so), buf_u32(rTs, tab * 4, so / 2));
@@ -274,20 +294,20 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(TQ ? 1 : (B
                 mw.w[kbl] = make_uint2(buf_u32(rM, n_meta * 4u, 0), buf_u32(rM, n_meta * 4u, p.per_tensor ? 4u : 0u));
                 mw.q[kbl] = q;
             }
-            // one activation sum per (block, token): lanes 0 .. 8 CH - 1 of every wavefront,
+            // one activation sum per (block, token): lanes 0 .. MT CH - 1 of every wavefront,
             // broadcast to the others by readlane
             const int ln = tid & 63;
-            const int t = ln & 7;
-            const int q = (CH == 1 || ln < 8) ? mw.q[0] : mw.q[CH - 1];
+            const int t = ln % MT;
+            const int q = (CH == 1 || ln < MT) ? mw.q[0] : mw.q[CH - 1];
             const uint32_t rt = (uint32_t)(row_of(t) - m0);
             sv[0] = __uint_as_float(buf_u32(rS, (rt * (uint32_t)p.Q + (uint32_t)q) * 4u, 0));
         }
     };
 
-    float yf[MTK];
-    int yi[MTK];
+    float yf[MT];
+    int yi[MT];
 #pragma unroll
-    for (int t = 0; t < MTK; ++t) {
+    for (int t = 0; t < MT; ++t) {
         yf[t] = 0.f;
         yi[t] = 0;
     }
@@ -301,35 +321,38 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(TQ ? 1 : (B
             const int task = tid + 256 * r;
             const int kbl = task >> 7, g = (task >> 2) & 31, ip = task & 3;
             if (task < TASKS && kbl < nkb) {
-                uint32_t v[MTK];
 #pragma unroll
-                for (int t = 0; t < MTK; ++t) {
-                    if constexpr (TQ) {  // code x scale, rounded to FP16
-                        const float sc = __uint_as_float(sd[r][t].y);
-                        const float f0 = (float)(int8_t)(sd[r][t].x & 0xFFu) * sc;
-                        const float f1 = (float)(int8_t)((sd[r][t].x >> 8) & 0xFFu) * sc;
-                        v[t] = (uint32_t)__half_as_ushort(__float2half_rn(f0)) |
-                               ((uint32_t)__half_as_ushort(__float2half_rn(f1)) << 16);
-                    } else {
-                        v[t] = sd[r][t];
+                for (int h = 0; h < NH; ++h) {
+                    uint32_t v[MTK];
+#pragma unroll
+                    for (int t = 0; t < MTK; ++t) {
+                        if constexpr (TQ) {  // code x scale, rounded to FP16
+                            const float sc = __uint_as_float(sd[r][MTK * h + t].y);
+                            const float f0 = (float)(int8_t)(sd[r][MTK * h + t].x & 0xFFu) * sc;
+                            const float f1 = (float)(int8_t)((sd[r][MTK * h + t].x >> 8) & 0xFFu) * sc;
+                            v[t] = (uint32_t)__half_as_ushort(__float2half_rn(f0)) |
+                                   ((uint32_t)__half_as_ushort(__float2half_rn(f1)) << 16);
+                        } else {
+                            v[t] = sd[r][MTK * h + t];
+                        }
                     }
+                    uint4 e0, e1;  // entries 2ip (low halves) and 2ip + 1 (high halves), tokens 8h .. 8h + 7
+                    e0.x = perm(v[1], v[0], 0x05040100u);
+                    e0.y = perm(v[3], v[2], 0x05040100u);
+                    e0.z = perm(v[5], v[4], 0x05040100u);
+                    e0.w = perm(v[7], v[6], 0x05040100u);
+                    e1.x = perm(v[1], v[0], 0x07060302u);
+                    e1.y = perm(v[3], v[2], 0x07060302u);
+                    e1.z = perm(v[5], v[4], 0x07060302u);
+                    e1.w = perm(v[7], v[6], 0x07060302u);
+                    char *row = Fb + (kbl * GPB + g) * GST + 256 * h;
+                    *(uint4 *)(row + (2 * ip) * 16) = e0;
+                    *(uint4 *)(row + (2 * ip + 1) * 16) = e1;
+                    *(uint4 *)(row + (2 * ip + 8) * 16) =
+                        make_uint4(neg16x2<INT8>(e0.x), neg16x2<INT8>(e0.y), neg16x2<INT8>(e0.z), neg16x2<INT8>(e0.w));
+                    *(uint4 *)(row + (2 * ip + 9) * 16) =
+                        make_uint4(neg16x2<INT8>(e1.x), neg16x2<INT8>(e1.y), neg16x2<INT8>(e1.z), neg16x2<INT8>(e1.w));
                 }
-                uint4 e0, e1;  // entries 2ip (low halves) and 2ip + 1 (high halves), tokens 0..7
-                e0.x = perm(v[1], v[0], 0x05040100u);
-                e0.y = perm(v[3], v[2], 0x05040100u);
-                e0.z = perm(v[5], v[4], 0x05040100u);
-                e0.w = perm(v[7], v[6], 0x05040100u);
-                e1.x = perm(v[1], v[0], 0x07060302u);
-                e1.y = perm(v[3], v[2], 0x07060302u);
-                e1.z = perm(v[5], v[4], 0x07060302u);
-                e1.w = perm(v[7], v[6], 0x07060302u);
-                char *row = Fb + (kbl * GPB + g) * 256;
-                *(uint4 *)(row + (2 * ip) * 16) = e0;
-                *(uint4 *)(row + (2 * ip + 1) * 16) = e1;
-                *(uint4 *)(row + (2 * ip + 8) * 16) =
-                    make_uint4(neg16x2<INT8>(e0.x), neg16x2<INT8>(e0.y), neg16x2<INT8>(e0.z), neg16x2<INT8>(e0.w));
-                *(uint4 *)(row + (2 * ip + 9) * 16) =
-                    make_uint4(neg16x2<INT8>(e1.x), neg16x2<INT8>(e1.y), neg16x2<INT8>(e1.z), neg16x2<INT8>(e1.w));
             }
         }
         lds_barrier();
@@ -341,7 +364,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(TQ ? 1 : (B
                 // INT16 (|sum| <= 32 x 508 < 2^15), then widened with the plane weight 2^pl
 #pragma unroll
                 for (int pl = 0; pl < BITS; ++pl) {
-                    short2_v a16[4] = {short2_v{0, 0}, short2_v{0, 0}, short2_v{0, 0}, short2_v{0, 0}};
+                    short2_v a16[NH][4];
+#pragma unroll
+                    for (int h = 0; h < NH; ++h)
+#pragma unroll
+                        for (int j = 0; j < 4; ++j) a16[h][j] = short2_v{0, 0};
                     const uint32_t wd[4] = {w[kbl][pl].x, w[kbl][pl].y, w[kbl][pl].z, w[kbl][pl].w};
 #pragma unroll
                     for (int d = 0; d < 4; ++d) {
@@ -350,18 +377,23 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(TQ ? 1 : (B
                         for (int k = 0; k < 8; ++k) {
                             const uint32_t off = nib_off((k & 1) ? hi : lo, k >> 1);
                             const int g = d * 8 + k;  // groups 2j (low nibble) and 2j + 1 (high nibble) of byte j
-                            const uint4 e = *(const uint4 *)(Fb + (kbl * GPB + g) * 256 + off);
-                            a16[0] += __builtin_bit_cast(short2_v, e.x);
-                            a16[1] += __builtin_bit_cast(short2_v, e.y);
-                            a16[2] += __builtin_bit_cast(short2_v, e.z);
-                            a16[3] += __builtin_bit_cast(short2_v, e.w);
+#pragma unroll
+                            for (int h = 0; h < NH; ++h) {
+                                const uint4 e = *(const uint4 *)(Fb + (kbl * GPB + g) * GST + 256 * h + off);
+                                a16[h][0] += __builtin_bit_cast(short2_v, e.x);
+                                a16[h][1] += __builtin_bit_cast(short2_v, e.y);
+                                a16[h][2] += __builtin_bit_cast(short2_v, e.z);
+                                a16[h][3] += __builtin_bit_cast(short2_v, e.w);
+                            }
                         }
                     }
 #pragma unroll
-                    for (int j = 0; j < 4; ++j) {
-                        yi[2 * j] += (int)a16[j].x << pl;
-                        yi[2 * j + 1] += (int)a16[j].y << pl;
-                    }
+                    for (int h = 0; h < NH; ++h)
+#pragma unroll
+                        for (int j = 0; j < 4; ++j) {
+                            yi[MTK * h + 2 * j] += (int)a16[h][j].x << pl;
+                            yi[MTK * h + 2 * j + 1] += (int)a16[h][j].y << pl;
+                        }
                 }
             } else {
                 // FP path, per weight word: the 8 entries one plane's word selects summed in
@@ -371,39 +403,52 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(TQ ? 1 : (B
                 const SZ sz = decode_sz(p, mw.w[kbl]);
 #pragma unroll
                 for (int d = 0; d < 4; ++d) {
-                    uint4 hp[BITS];
+                    uint4 hp[NH][BITS];
 #pragma unroll
                     for (int pl = 0; pl < BITS; ++pl) {
                         const uint32_t wv = d == 0 ? w[kbl][pl].x : d == 1 ? w[kbl][pl].y : d == 2 ? w[kbl][pl].z : w[kbl][pl].w;
                         const uint32_t lo = wv << 4, hi = wv;
-                        uint4 e0;
+                        uint4 e0[NH];
 #pragma unroll
                         for (int k = 0; k < 8; ++k) {
                             const uint32_t off = nib_off((k & 1) ? hi : lo, k >> 1);
                             const int g = d * 8 + k;  // groups 2j (low nibble) and 2j + 1 (high nibble) of byte j
-                            const uint4 e = *(const uint4 *)(Fb + (kbl * GPB + g) * 256 + off);
-                            if (k == 0)
-                                e0 = e;
-                            else if (k == 1)
-                                hp[pl] = pk_sum4(e0, e);
-                            else
-                                pk_add4(hp[pl], e);
+                            uint4 e[NH];
+#pragma unroll
+                            for (int h = 0; h < NH; ++h) e[h] = *(const uint4 *)(Fb + (kbl * GPB + g) * GST + 256 * h + off);
+                            if (k == 0) {
+#pragma unroll
+                                for (int h = 0; h < NH; ++h) e0[h] = e[h];
+                            } else if (k == 1) {
+#pragma unroll
+                                for (int h = 0; h < NH; ++h) hp[h][pl] = pk_sum4(e0[h], e[h]);
+                            } else if constexpr (NH == 2 && BITS > 1) {
+                                pk_add4x2(hp[0][pl], e[0], hp[1][pl], e[1]);  // both reads in flight together
+                            } else if constexpr (NH == 2) {
+                                pk_add4(hp[0][pl], e[0]);
+                                pk_add4(hp[1][pl], e[1]);
+                            } else {
+                                pk_add4(hp[0][pl], e[0]);
+                            }
                         }
                     }
-                    if constexpr (BITS == 1) {
-                        fma_mix8(yf, hp[0], sz.sp);
-                    } else {
 #pragma unroll
-                        for (int i = 0; i < BITS / 2; ++i)
-                            fma_mix8(yf, pk_fma2x4(hp[2 * i + 1], hp[2 * i]), sz.sp * (float)(1 << (2 * i)));
+                    for (int h = 0; h < NH; ++h) {
+                        if constexpr (BITS == 1) {
+                            fma_mix8(yf + MTK * h, hp[h][0], sz.sp);
+                        } else {
+#pragma unroll
+                            for (int i = 0; i < BITS / 2; ++i)
+                                fma_mix8(yf + MTK * h, pk_fma2x4(hp[h][2 * i + 1], hp[h][2 * i]), sz.sp * (float)(1 << (2 * i)));
+                        }
                     }
                 }
                 // the zero-point term enters with the first block of each group only
                 if (need_s && kc + kbl == mw.q[kbl] * p.kpg) {
                     const float nspz = -(sz.sp * sz.zp);
 #pragma unroll
-                    for (int t = 0; t < MTK; ++t) {
-                        const float st = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(sv[0]), kbl * MTK + t));
+                    for (int t = 0; t < MT; ++t) {
+                        const float st = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(sv[0]), kbl * MT + t));
                         yf[t] = fmaf(nspz, st, yf[t]);
                     }
                 }
@@ -414,7 +459,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(TQ ? 1 : (B
     // INT8 ternary: the activation sums S[m][0], added once (first K split)
     if (INT8 && split == 0 && wfmt == LUTGEMM_WFMT_TERNARY) {
 #pragma unroll
-        for (int t = 0; t < MTK; ++t) yi[t] = ((const int *)p.S)[lane_value(row_of(t) * p.Q)];
+        for (int t = 0; t < MT; ++t) yi[t] = ((const int *)p.S)[lane_value(row_of(t) * p.Q)];
     }
     const int last = kbA + (kbB - 1 - kbA) / CH * CH;
     SD sdA, sdB;
@@ -430,38 +475,50 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(TQ ? 1 : (B
         process(kc + CH, sdB, wB, mwB, svB, 1);
     }
 
-    const int rows = (int)((p.M - m0) < MTK ? (p.M - m0) : MTK);
+    const int rows = (int)((p.M - m0) < MT ? (p.M - m0) : MT);
     if (p.splits == 1) {
 #pragma unroll
-        for (int t = 0; t < MTK; ++t)
+        for (int t = 0; t < MT; ++t)
             if (t < rows) store_out<INT8>(p, wfmt, m0 + t, n, yf[t], yi[t], load_epi<INT8>(p, wfmt, m0 + t, n, false));
         return;
     }
-    const int64_t m_alloc = m_tiles * MTK;
+    const int64_t m_alloc = m_tiles * MT;
 #pragma unroll
-    for (int t = 0; t < MTK; ++t)  // the finalize kernel reads rows below M only
+    for (int t = 0; t < MT; ++t)  // the finalize kernel reads rows below M only
         if (t < rows) p.part[((int64_t)split * m_alloc + m0 + t) * p.N_pad + n] = INT8 ? __int_as_float(yi[t]) : yf[t];
 }
 
-int launch_mtok(const LutParams &p, const Layout &L, const LutPlan &plan, void *stream) {
-    hipStream_t s = (hipStream_t)stream;
+template <int NH>
+static void launch_mtok_nh(const LutParams &p, const Layout &L, const LutPlan &plan, hipStream_t s) {
     // one-dimensional grid (tile_of decodes it); the planner keeps it under 2^32 work-items
     const dim3 grid((unsigned)(plan.n_tiles * plan.m_tiles * plan.splits), 1, 1);
     const bool i8 = L.act == LUTGEMM_ACT_INT8;
     const int64_t nt = plan.n_tiles, mt = plan.m_tiles;
     const int o = plan.order;
-    const bool tq = L.act == LUTGEMM_ACT_FP16_LUT8;
     if (L.bits == 1) {
-        if (i8) hipLaunchKernelGGL((lut_mtok_kernel<1, true, false>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
-        else if (tq) hipLaunchKernelGGL((lut_mtok_kernel<1, false, true>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
-        else hipLaunchKernelGGL((lut_mtok_kernel<1, false, false>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
+        if (i8) hipLaunchKernelGGL((lut_mtok_kernel<1, true, false, NH>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
+        else hipLaunchKernelGGL((lut_mtok_kernel<1, false, false, NH>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
     } else if (L.bits == 2) {
-        if (i8) hipLaunchKernelGGL((lut_mtok_kernel<2, true, false>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
-        else if (tq) hipLaunchKernelGGL((lut_mtok_kernel<2, false, true>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
-        else hipLaunchKernelGGL((lut_mtok_kernel<2, false, false>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
+        if (i8) hipLaunchKernelGGL((lut_mtok_kernel<2, true, false, NH>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
+        else hipLaunchKernelGGL((lut_mtok_kernel<2, false, false, NH>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
     } else {
-        if (tq) hipLaunchKernelGGL((lut_mtok_kernel<4, false, true>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
-        else hipLaunchKernelGGL((lut_mtok_kernel<4, false, false>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
+        hipLaunchKernelGGL((lut_mtok_kernel<4, false, false, NH>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
+    }
+}
+
+int launch_mtok(const LutParams &p, const Layout &L, const LutPlan &plan, void *stream) {
+    hipStream_t s = (hipStream_t)stream;
+    if (L.act == LUTGEMM_ACT_FP16_LUT8) {  // INT8-quantized tables: 8 tokens per workgroup
+        const dim3 grid((unsigned)(plan.n_tiles * plan.m_tiles * plan.splits), 1, 1);
+        const int64_t nt = plan.n_tiles, mt = plan.m_tiles;
+        const int o = plan.order;
+        if (L.bits == 1) hipLaunchKernelGGL((lut_mtok_kernel<1, false, true, 1>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
+        else if (L.bits == 2) hipLaunchKernelGGL((lut_mtok_kernel<2, false, true, 1>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
+        else hipLaunchKernelGGL((lut_mtok_kernel<4, false, true, 1>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
+    } else if (plan.mt == 16) {
+        launch_mtok_nh<2>(p, L, plan, s);
+    } else {
+        launch_mtok_nh<1>(p, L, plan, s);
     }
     return (int)hipGetLastError();
 }
