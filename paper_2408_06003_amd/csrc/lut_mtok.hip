@@ -408,27 +408,26 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(TQ ? 1 : (B
                     for (int pl = 0; pl < BITS; ++pl) {
                         const uint32_t wv = d == 0 ? w[kbl][pl].x : d == 1 ? w[kbl][pl].y : d == 2 ? w[kbl][pl].z : w[kbl][pl].w;
                         const uint32_t lo = wv << 4, hi = wv;
-                        uint4 e0[NH];
+                        uint4 e[8][NH];
 #pragma unroll
                         for (int k = 0; k < 8; ++k) {
                             const uint32_t off = nib_off((k & 1) ? hi : lo, k >> 1);
                             const int g = d * 8 + k;  // groups 2j (low nibble) and 2j + 1 (high nibble) of byte j
-                            uint4 e[NH];
 #pragma unroll
-                            for (int h = 0; h < NH; ++h) e[h] = *(const uint4 *)(Fb + (kbl * GPB + g) * GST + 256 * h + off);
-                            if (k == 0) {
+                            for (int h = 0; h < NH; ++h) e[k][h] = *(const uint4 *)(Fb + (kbl * GPB + g) * GST + 256 * h + off);
+                            if (k == 1) {
 #pragma unroll
-                                for (int h = 0; h < NH; ++h) e0[h] = e[h];
-                            } else if (k == 1) {
+                                for (int h = 0; h < NH; ++h) hp[h][pl] = pk_sum4(e[0][h], e[1][h]);
+                            } else if (k >= 2) {
+                                if constexpr (NH == 2 && BITS > 1) {
+                                    if (k & 1) {  // two indices, four reads in flight together
+                                        pk_add4x2(hp[0][pl], e[k - 1][0], hp[1][pl], e[k - 1][1]);
+                                        pk_add4x2(hp[0][pl], e[k][0], hp[1][pl], e[k][1]);
+                                    }
+                                } else {
 #pragma unroll
-                                for (int h = 0; h < NH; ++h) hp[h][pl] = pk_sum4(e0[h], e[h]);
-                            } else if constexpr (NH == 2 && BITS > 1) {
-                                pk_add4x2(hp[0][pl], e[0], hp[1][pl], e[1]);  // both reads in flight together
-                            } else if constexpr (NH == 2) {
-                                pk_add4(hp[0][pl], e[0]);
-                                pk_add4(hp[1][pl], e[1]);
-                            } else {
-                                pk_add4(hp[0][pl], e[0]);
+                                    for (int h = 0; h < NH; ++h) pk_add4(hp[h][pl], e[k][h]);
+                                }
                             }
                         }
                     }
