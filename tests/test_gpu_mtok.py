@@ -37,10 +37,13 @@ FP_CASES = [
 ]
 
 
+@pytest.mark.parametrize("mt16", [1, 0])
 @pytest.mark.parametrize("wfmt,bits,G,fp32,M,K,N,splits", FP_CASES)
-def test_multi_token_fp_layouts(wfmt, bits, G, fp32, M, K, N, splits, monkeypatch):
+def test_multi_token_fp_layouts(wfmt, bits, G, fp32, M, K, N, splits, mt16, monkeypatch):
+    """mt16 = 0 keeps 8-token workgroups where 16-token ones would be used (M >= 16)."""
     if splits:
         monkeypatch.setenv("LUTGEMM_MT_SPLITS", str(splits))
+    monkeypatch.setenv("LUTGEMM_MT16", str(mt16))
     what = f"wfmt={wfmt} b={bits} G={G} M={M} K={K} N={N} splits={splits}"
     print(f"\n[case] multi-token FP {what}", flush=True)
     inp = W.make_custom(wfmt, bits, G, W.ACT_FP16, M=M, K=K, N=N, seed=M + K + N + splits, scale_fp32=fp32)
@@ -75,19 +78,21 @@ def test_multi_token_int8_layouts(wfmt, bits, G, fp32, M, K, N, splits, monkeypa
     assert np.array_equal(yf, y_ref), "FP32 scaled output differs from the oracle"
 
 
+@pytest.mark.parametrize("M", [5, 17])
 @pytest.mark.parametrize("splits", [5, 9, 17, 33, 65, 128])
-def test_multi_token_many_splits(splits, monkeypatch):
+def test_multi_token_many_splits(splits, M, monkeypatch):
     """K split into 5 .. 128 ranges: the finalize kernel's load batch (4 .. 64 partials,
-    looping when there are more) at every size it takes, FP and INT8 paths."""
+    looping when there are more) at every size it takes, FP and INT8 paths, with 8-token
+    (M = 5) and 16-token (M = 17: one full tile and one with a single live row) workgroups."""
     monkeypatch.setenv("LUTGEMM_MT_SPLITS", str(splits))
-    print(f"\n[case] multi-token K splits={splits} (M=5, K=16384, N=200)", flush=True)
-    inp = W.make_custom(W.WFMT_BINARY, 1, 16384, W.ACT_FP16, M=5, K=16384, N=200, seed=300 + splits)
+    print(f"\n[case] multi-token K splits={splits} (M={M}, K=16384, N=200)", flush=True)
+    inp = W.make_custom(W.WFMT_BINARY, 1, 16384, W.ACT_FP16, M=M, K=16384, N=200, seed=300 + splits)
     gp = GpuProblem(inp)
     ref = oracle.reference_output(inp)
     y32 = gp.lut(out_dtype=torch.float32)
     assert_fp_close(y32.cpu().numpy(), ref, f"splits={splits}")
     assert torch.equal(gp.lut(out_dtype=torch.float32), y32), f"splits={splits}: two runs differ bitwise"
-    inpi = W.make_custom(W.WFMT_TERNARY, 2, 0, W.ACT_INT8, M=5, K=16384, N=200, seed=400 + splits,
+    inpi = W.make_custom(W.WFMT_TERNARY, 2, 0, W.ACT_INT8, M=M, K=16384, N=200, seed=400 + splits,
                          scale_fp32=True)
     gpi = GpuProblem(inpi)
     acc_ref, y_ref = oracle.reference_output(inpi)
