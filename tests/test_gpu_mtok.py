@@ -98,3 +98,15 @@ def test_multi_token_many_splits(splits, M, monkeypatch):
     acc_ref, y_ref = oracle.reference_output(inpi)
     assert np.array_equal(gpi.lut(out_dtype=torch.int32).cpu().numpy().astype(np.int64), acc_ref)
     assert np.array_equal(gpi.lut(out_dtype=torch.float32).cpu().numpy(), y_ref)
+
+
+@pytest.mark.parametrize("order", [1, 8, 16])
+def test_multi_token_tile_orders(order, monkeypatch):
+    """XCD-aware workgroup orders (token-fastest, bands of 8 or 16 token tiles) over a
+    grid whose token tiles do not fill the last band, every output against the oracle."""
+    monkeypatch.setenv("LUTGEMM_MT_ORDER", str(order))
+    monkeypatch.setenv("LUTGEMM_MT_SPLITS", "1")
+    print(f"\n[case] multi-token tile order {order} (M=300, K=1024, N=520)", flush=True)
+    inp = W.make_custom(W.WFMT_UINT, 2, 128, W.ACT_FP16, M=300, K=1024, N=520, seed=500 + order)
+    gp = GpuProblem(inp)
+    assert_fp_close(gp.lut(out_dtype=torch.float32).cpu().numpy(), oracle.reference_output(inp), f"order {order}")
