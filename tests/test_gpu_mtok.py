@@ -110,3 +110,30 @@ def test_multi_token_tile_orders(order, monkeypatch):
     inp = W.make_custom(W.WFMT_UINT, 2, 128, W.ACT_FP16, M=300, K=1024, N=520, seed=500 + order)
     gp = GpuProblem(inp)
     assert_fp_close(gp.lut(out_dtype=torch.float32).cpu().numpy(), oracle.reference_output(inp), f"order {order}")
+
+
+@pytest.mark.parametrize("splits", [1, 3])
+@pytest.mark.parametrize("M", [10, 20])
+def test_multi_token_accumulate(M, splits, monkeypatch):
+    """O += A W^T through the multi-token kernel's own epilogue (one split) and through the
+    finalize kernel (three splits), FP32 and FP16 outputs, and the INT8 path's INT32 output."""
+    monkeypatch.setenv("LUTGEMM_MT_SPLITS", str(splits))
+    print(f"\n[case] multi-token accumulate M={M} splits={splits}", flush=True)
+    inp = W.make_custom(W.WFMT_UINT, 2, 128, W.ACT_FP16, M=M, K=1024, N=300, seed=600 + M + splits)
+    gp = GpuProblem(inp)
+    y1 = gp.lut(out_dtype=torch.float32)
+    base = torch.randn(M, 300, device="cuda", dtype=torch.float32)
+    acc = base.clone()
+    gp.lut(out=acc, accumulate=True)
+    assert torch.equal(acc, base + y1), "FP32 accumulate is not O + A W^T"
+    base16 = torch.randn(M, 300, device="cuda", dtype=torch.float32).half()
+    acc16 = base16.clone()
+    gp.lut(out=acc16, accumulate=True)
+    assert torch.equal(acc16, (base16.float() + y1).half()), "FP16 accumulate is not round(O + A W^T)"
+    inpi = W.make_custom(W.WFMT_TERNARY, 2, 0, W.ACT_INT8, M=M, K=1024, N=300, seed=700 + M + splits,
+                         scale_fp32=True)
+    gpi = GpuProblem(inpi)
+    bi = torch.randint(-1000, 1000, (M, 300), device="cuda", dtype=torch.int32)
+    acci = bi.clone()
+    gpi.lut(out=acci, accumulate=True)
+    assert torch.equal(acci, bi + gpi.lut(out_dtype=torch.int32)), "INT32 accumulate is not O + acc"
