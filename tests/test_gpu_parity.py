@@ -243,3 +243,24 @@ def test_dequant_big_tile_parity(cid, M, K, N, monkeypatch):
     gp = GpuProblem(W.make_inputs(cid, 0, M=M, K=K, N=N))
     check_fp_path(gp, dequant=True, what=f"dequant big config {cid}")
     check_fp_path(gp, dequant=True, out_dtype=torch.float32, what=f"dequant big config {cid} fp32 out")
+
+
+@pytest.mark.parametrize("kbs", [0, 1, 4])
+def test_split_k_gemv_two_tokens(kbs, monkeypatch):
+    """The table-fed split-K GEMV (forced) with two tokens and a ragged column tail, K
+    split into 8-64 ranges summed by the finalize kernel: FP (all outputs within the FP
+    bar) and INT8 (bit-exact) paths, and accumulation through the finalize epilogue."""
+    monkeypatch.setenv("LUTGEMM_GEMV_KIND", "2")
+    if kbs:
+        monkeypatch.setenv("LUTGEMM_KBS", str(kbs))
+    banner(f"split-K GEMV M=2 kbs={kbs or 'planned'}")
+    inp = W.make_custom(W.WFMT_UINT, 2, 128, W.ACT_FP16, M=2, K=8192, N=777, seed=800 + kbs)
+    gp = GpuProblem(inp)
+    y = check_fp_path(gp, out_dtype=torch.float32, what=f"split-K M=2 kbs={kbs}")
+    y32 = gp.lut(out_dtype=torch.float32)
+    base = torch.randn(2, 777, device="cuda", dtype=torch.float32)
+    acc = base.clone()
+    gp.lut(out=acc, accumulate=True)
+    assert torch.equal(acc, base + y32), "accumulate through the finalize kernel"
+    inpi = W.make_custom(W.WFMT_TERNARY, 2, 0, W.ACT_INT8, M=2, K=8192, N=777, seed=900 + kbs, scale_fp32=True)
+    check_int_path(GpuProblem(inpi))
