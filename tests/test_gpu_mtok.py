@@ -137,3 +137,18 @@ def test_multi_token_accumulate(M, splits, monkeypatch):
     acci = bi.clone()
     gpi.lut(out=acci, accumulate=True)
     assert torch.equal(acci, bi + gpi.lut(out_dtype=torch.int32)), "INT32 accumulate is not O + acc"
+
+
+@pytest.mark.parametrize("M,K,N", [(33, 256, 1), (17, 128, 255), (16, 128, 1), (3, 128, 1), (40, 384, 257)])
+def test_multi_token_tiny_shapes(M, K, N):
+    """Degenerate multi-token shapes: a single output column, a single 128-block of K, a
+    ragged column tile, token counts at and just past the 8/16-token tile sizes."""
+    print(f"\n[case] multi-token tiny M={M} K={K} N={N}", flush=True)
+    inp = W.make_custom(W.WFMT_UINT, 2, 128, W.ACT_FP16, M=M, K=K, N=N, seed=1000 + M + K + N)
+    gp = GpuProblem(inp)
+    assert_fp_close(gp.lut(out_dtype=torch.float32).cpu().numpy(), oracle.reference_output(inp), "tiny FP")
+    inpi = W.make_custom(W.WFMT_TERNARY, 2, 0, W.ACT_INT8, M=M, K=K, N=N, seed=1100 + M + K + N, scale_fp32=True)
+    gpi = GpuProblem(inpi)
+    acc_ref, y_ref = oracle.reference_output(inpi)
+    assert np.array_equal(gpi.lut(out_dtype=torch.int32).cpu().numpy().astype(np.int64), acc_ref)
+    assert np.array_equal(gpi.lut(out_dtype=torch.float32).cpu().numpy(), y_ref)
