@@ -305,7 +305,7 @@ int launch_precompute(const PrecomputeParams &p_in, int act_int8, void *stream) 
     PrecomputeParams p = p_in;
     const int64_t nvb = (p.J + 255) / 256;
     p.vbs = 1;
-    for (int r = 8; r > 1; r /= 2)
+    for (int r = 32; r > 1; r /= 2)
         if ((nvb + r - 1) / r * p.M >= 256) {
             p.vbs = r;
             break;
