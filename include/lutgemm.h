@@ -68,7 +68,7 @@ enum {
     LUTGEMM_ACT_INT8 = 1,     /* FP16 activations quantized per token to INT8 (absmax) -> INT16
                                  tables, exact INT32 accumulation (BINARY / TERNARY weights)     */
     LUTGEMM_ACT_FP16_LUT8 = 2 /* FP16 activations, tables quantized to INT8 with one FP32 scale
-                                 per table (Section 3.1.4): an approximation (relative error of
+                                 per table (Section 3.1.3): an approximation (relative error of
                                  the output about 3e-3), 12 instead of 16 table bytes per 4
                                  activations (8 INT8 codes + FP32 scale); not
                                  with TERNARY_3IN5                                               */
@@ -197,7 +197,7 @@ lutgemm_status_t lutgemm_pack_weights(const lutgemm_problem_t *problem, const vo
  * lutgemm_table_size.  For ACT_INT8 it first quantizes each token:
  * amax = max |a|, q_a = clamp(rint(a * (127 / amax)), -127, 127) in FP32
  * (q_a = 0 when amax == 0).  For ACT_FP16_LUT8 it quantizes each finished table
- * (Section 3.1.4).
+ * (Section 3.1.3).
  */
 lutgemm_status_t lutgemm_precompute(const lutgemm_problem_t *problem, int64_t M, const void *act,
                                     void *tables, size_t table_bytes, void *stream);
@@ -282,6 +282,19 @@ lutgemm_status_t lutgemm_mpgemm_dequant(const lutgemm_problem_t *problem, int64_
  */
 lutgemm_status_t lutgemm_calibrate_stream_read(const void *src, size_t bytes, void *sink,
                                                int32_t blocks, void *stream);
+
+/*
+ * The same measurement with the read pattern chosen by the caller, to search for
+ * the fastest single-launch read of a byte count: each of the `blocks` x 256
+ * lanes keeps `unroll` (1, 2, 4, 8 or 16) 16-byte loads in flight; flags bit 0
+ * marks the loads nontemporal, bit 1 gives each workgroup one contiguous range
+ * (else tiles of 256 x unroll words are dealt to the workgroups in turn).
+ * lutgemm_calibrate_stream_read is unroll 4, flags 0.  Returns
+ * LUTGEMM_ERROR_INVALID_VALUE as above and for any other unroll or flags value.
+ */
+lutgemm_status_t lutgemm_calibrate_stream_read_ex(const void *src, size_t bytes, void *sink,
+                                                  int32_t blocks, int32_t unroll, int32_t flags,
+                                                  void *stream);
 
 #ifdef __cplusplus
 }

@@ -19,9 +19,9 @@ Functions and the passage each follows:
 * ``half_tables``      -- precompute output: symmetric half tables (Eq. 4-5)
 * ``group_sums``       -- activation sums per quantization group (zero-point term of Eq. 3)
 * ``token_pow2``       -- per-token power-of-two normalizer of the FP16 tables
-* ``lut8_tables``      -- INT8 table quantization, per table (Section 3.1.4): codes, scales
+* ``lut8_tables``      -- INT8 table quantization, per table (Section 3.1.3): codes, scales
 * ``mpgemm_lut8``      -- FP mpGEMM through the INT8-quantized tables: the approximation
-                          follows the method's steps (Section 3.1.4, Eq. 2-6, bit-serial
+                          follows the method's steps (Section 3.1.3, Eq. 2-6, bit-serial
                           planes of Section 3.2.1); no closed form exists for it
 """
 from __future__ import annotations

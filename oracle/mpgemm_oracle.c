@@ -299,19 +299,30 @@ void oracle_token_pow2(int64_t M, int64_t K, const double *a, double *mult)
 }
 
 /*
- * INT8 table quantization (Section 3.1.4): an approximation of the FP16-activation
+ * INT8 table quantization (Section 3.1.3): an approximation of the FP16-activation
  * path, so this follows the method's steps in order instead of a closed form.
  *   1. per token, the power-of-two normalization of the FP16 table path:
- *      x = a * 2^-e with max |a| = f 2^e, f in [0.5, 1)  (exact);
- *   2. per group j of 4 activations, the 8-entry half table of Eq. 5 in FP32,
- *      T[idx] = ((-x0 + (+-x1)) + (+-x2)) + (+-x3)  (bit 2 of idx selects the sign
- *      of x1, bit 1 of x2, bit 0 of x3: the first activation is the MSB of a
+ *      x = a * 2^-e with max |a| = f 2^e, f in [0.5, 1)  (exact; it changes no code,
+ *      only the unit of the scale);
+ *   2. per group j of 4 activations, the 8-entry half table of Eq. 5 as exact real
+ *      numbers, T[idx] = -x0 + (+-x1) + (+-x2) + (+-x3) (bit 2 of idx selects the
+ *      sign of x1, bit 1 of x2, bit 0 of x3: the first activation is the MSB of a
  *      pattern, and the half table keeps the patterns whose MSB is 0);
- *   3. each table quantized on its own to INT8: amax = max_idx |T[idx]|,
- *      q = clamp(rint(T * (127 / amax)), -127, 127), scale = amax / 127 (FP32,
- *      ties to even; q = 0 and scale = 0 for an all-zero table).  The reading of
- *      "a unified INT8 precision per table" (the paper fixes neither rounding nor
- *      scale format).
+ *   3. each table quantized on its own to INT8 with a symmetric scale: with
+ *      amax = max_idx |T[idx]|, q = round(127 T / amax), ties to even (|q| <= 127
+ *      by construction), and scale = amax / 127 rounded to the nearest FP32 value;
+ *      q = 0 and scale = 0 for an all-zero table.  The paper asks for one INT8
+ *      precision per table and fixes neither rounding nor scale format; this is the
+ *      reading.
+ * Exactness of this float64 evaluation: every x is an integer multiple of
+ * u = 2^(-24-e) (FP16 values are multiples of 2^-24) below 1 in magnitude, so every
+ * T is n u with |n| < 2^42 and its sums are exact in float64, in any order, and so
+ * is 127 T (|127 n| < 2^49).  When 127 T / amax = 127 n / n_max is not a half-integer
+ * it lies at least 1 / (2 n_max) > 2^-43 away from every half-integer, more than the
+ * float64 division's rounding error (at most 2^-47 below 128), so rint of the
+ * rounded quotient is the exact round-half-to-even.  The FP32 scale is the float64
+ * quotient rounded to FP32; amax / 127 has a binary expansion of period 7 (or
+ * terminates), so that second rounding never meets a tie the first one created.
  * Outputs q[m][j][8] (int8), scale[m][j] (float32), mult[m] = 2^e (float64).
  */
 void oracle_lut8_tables(int64_t M, int64_t K, const float *a, int8_t *q, float *scale, double *mult)
@@ -327,35 +338,30 @@ void oracle_lut8_tables(int64_t M, int64_t K, const float *a, int8_t *q, float *
         int e = 0;
         if (amax != 0.0f)
             (void)frexpf(amax, &e);
-        const float down = ldexpf(1.0f, -e);
+        const double down = ldexp(1.0, -e);
         mult[m] = ldexp(1.0, e);
         for (int64_t j = 0; j < J; ++j) {
-            float x[4], t[8], tmax = 0.0f;
+            double x[4], t[8], tmax = 0.0;
             for (int i = 0; i < 4; ++i)
-                x[i] = a[m * K + 4 * j + i] * down;
+                x[i] = (double)a[m * K + 4 * j + i] * down;
             for (int idx = 0; idx < 8; ++idx) {
-                float s = -x[0];
-                s = s + ((idx & 4) ? x[1] : -x[1]);
-                s = s + ((idx & 2) ? x[2] : -x[2]);
-                s = s + ((idx & 1) ? x[3] : -x[3]);
+                double s = -x[0];
+                s += (idx & 4) ? x[1] : -x[1];
+                s += (idx & 2) ? x[2] : -x[2];
+                s += (idx & 1) ? x[3] : -x[3];
                 t[idx] = s;
-                if (fabsf(s) > tmax)
-                    tmax = fabsf(s);
+                if (fabs(s) > tmax)
+                    tmax = fabs(s);
             }
-            const float inv = tmax == 0.0f ? 0.0f : 127.0f / tmax;
-            for (int idx = 0; idx < 8; ++idx) {
-                float r = rintf(t[idx] * inv);
-                if (r > 127.0f) r = 127.0f;
-                if (r < -127.0f) r = -127.0f;
-                q[(m * J + j) * 8 + idx] = (int8_t)r;
-            }
-            scale[m * J + j] = tmax == 0.0f ? 0.0f : tmax / 127.0f;
+            for (int idx = 0; idx < 8; ++idx)
+                q[(m * J + j) * 8 + idx] = tmax == 0.0 ? 0 : (int8_t)rint((127.0 * t[idx]) / tmax);
+            scale[m * J + j] = tmax == 0.0 ? 0.0f : (float)(tmax / 127.0);
         }
     }
 }
 
 /*
- * FP mpGEMM with INT8-quantized tables (Section 3.1.4 on top of Section 3.1):
+ * FP mpGEMM with INT8-quantized tables (Section 3.1.3 on top of Section 3.1):
  * continues from oracle_lut8_tables with
  *   4. the lookup of Eq. 4-6: the full table entry of a 4-bit pattern p is
  *      L(p) = scale * q[p & 7] when its MSB is 0 and -scale * q[~p & 7] when it is 1

@@ -34,7 +34,7 @@ EXPORTS = [
     "lutgemm_status_string", "lutgemm_version", "lutgemm_last_error", "lutgemm_validate", "lutgemm_packed_weight_size",
     "lutgemm_table_size", "lutgemm_table_offsets", "lutgemm_workspace_size", "lutgemm_pack_weights",
     "lutgemm_precompute", "lutgemm_mpgemm", "lutgemm_mpgemm_dequant", "lutgemm_calibrate_stream_read",
-    "lutgemm_fused_workspace_size", "lutgemm_mpgemm_fused",
+    "lutgemm_fused_workspace_size", "lutgemm_mpgemm_fused", "lutgemm_calibrate_stream_read_ex",
 ]
 
 
@@ -95,6 +95,8 @@ def _load():
     L.lutgemm_mpgemm_fused.argtypes = [PP, I64, P, P, P, I32, I32, P, SZ, P]
     L.lutgemm_calibrate_stream_read.restype = ctypes.c_int
     L.lutgemm_calibrate_stream_read.argtypes = [P, SZ, P, I32, P]
+    L.lutgemm_calibrate_stream_read_ex.restype = ctypes.c_int
+    L.lutgemm_calibrate_stream_read_ex.argtypes = [P, SZ, P, I32, I32, I32, P]
     return L
 
 
@@ -203,6 +205,13 @@ def calibrate_stream_read(src, nbytes: int, sink, blocks: int, stream=None):
     """Launch the streaming-read calibration kernel over ``nbytes`` of ``src``."""
     _check(lib.lutgemm_calibrate_stream_read(_ptr(src), nbytes, _ptr(sink), blocks, _stream(stream)),
            "lutgemm_calibrate_stream_read")
+
+
+def calibrate_stream_read_ex(src, nbytes: int, sink, blocks: int, unroll: int = 4, flags: int = 0,
+                             stream=None):
+    """Streaming-read calibration with a chosen read pattern (unroll, nontemporal / contiguous flags)."""
+    _check(lib.lutgemm_calibrate_stream_read_ex(_ptr(src), nbytes, _ptr(sink), blocks, unroll, flags,
+                                                _stream(stream)), "lutgemm_calibrate_stream_read_ex")
 
 
 class LutGemm:

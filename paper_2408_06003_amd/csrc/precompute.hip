@@ -15,10 +15,10 @@
 //      T[m][j][i] = -x_0 + sum_{e=1..3} (bit (3-e) of i ? x_e : -x_e), the entry of
 //      pattern 0 i of the full 16-entry table (Eq. 5); the other half is its
 //      negation (Eq. 4) and is never stored.
-//      INT8 table quantization (Section 3.1.4, `tsc` set): each half table is
-//      stored as 8 INT8 codes clamp(rint(T * (127 / amax)), -127, 127) with
-//      amax = max |T| (FP32, the entries as computed above) and its scale
-//      amax / 127 in FP32.
+//      INT8 table quantization (Section 3.1.3, `tsc` set): each half table is
+//      stored as 8 INT8 codes round(127 T / amax), ties to even, with amax = max |T|
+//      of the exact entries (formed in FP64, where they are exact), and its scale
+//      amax / 127 rounded to FP32.
 //   3. S[m][q] = sum of x over quantization group q (zero-point term of Eq. 3):
 //      groups of 128..1024 activations are reduced across the lanes that built
 //      them; larger ones are summed by the workgroup that holds their first
@@ -197,30 +197,38 @@ __device__ __forceinline__ void build_block(const PrecomputeParams &p, const uin
         const float x2 = token_value<INT8>(h2f(v.y & 0xFFFFu), scale);
         const float x3 = token_value<INT8>(h2f(v.y >> 16), scale);
         uint32_t e[8];
-        float tf[8];
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
             const float t = ((-x0 + ((i & 4) ? x1 : -x1)) + ((i & 2) ? x2 : -x2)) + ((i & 1) ? x3 : -x3);
-            tf[i] = t;
             if (INT8)
                 e[i] = (uint32_t)(uint16_t)(int16_t)(int)t;  // |t| <= 508, exact
             else
                 e[i] = (uint32_t)__half_as_ushort(__float2half_rn(t));
         }
         if (!INT8 && p.tsc) {
-            // INT8 table quantization (Section 3.1.4), one scale per table, FP32
-            float tmax = 0.f;
-#pragma unroll
-            for (int i = 0; i < 8; ++i) tmax = fmaxf(tmax, fabsf(tf[i]));
-            const float inv = tmax == 0.f ? 0.f : __fdiv_rn(127.0f, tmax);
-            uint32_t c[2] = {0u, 0u};
+            // INT8 table quantization (Section 3.1.3), one scale per table.  The table
+            // is formed in FP64, where it is exact (the x are FP16 values times a power
+            // of two: integer multiples of 2^(-24-e) below 1, so every sum is exact);
+            // 127 T is exact too, and the rounding of the FP64 quotient cannot reach or
+            // cross a half-integer the exact 127 T / amax does not lie on, so rint gives
+            // round-half-to-even of the exact value.  Scale: amax / 127 to FP32.
+            const double d0 = x0, d1 = x1, d2 = x2, d3 = x3;
+            double td[8], tmax = 0.0;
 #pragma unroll
             for (int i = 0; i < 8; ++i) {
-                const float r = fminf(fmaxf(rintf(tf[i] * inv), -127.f), 127.f);
-                c[i >> 2] |= ((uint32_t)(int)r & 0xFFu) << (8 * (i & 3));
+                td[i] = ((-d0 + ((i & 4) ? d1 : -d1)) + ((i & 2) ? d2 : -d2)) + ((i & 1) ? d3 : -d3);
+                tmax = fmax(tmax, fabs(td[i]));
+            }
+            uint32_t c[2] = {0u, 0u};
+            if (tmax != 0.0) {
+#pragma unroll
+                for (int i = 0; i < 8; ++i) {
+                    const int r = (int)rint((127.0 * td[i]) / tmax);  // |r| <= 127
+                    c[i >> 2] |= ((uint32_t)r & 0xFFu) << (8 * (i & 3));
+                }
             }
             ((uint2 *)p.T)[m * p.J + j] = make_uint2(c[0], c[1]);
-            p.tsc[m * p.J + j] = tmax == 0.f ? 0.f : __fdiv_rn(tmax, 127.0f);
+            p.tsc[m * p.J + j] = tmax == 0.0 ? 0.f : __double2float_rn(tmax / 127.0);
         } else {
             p.T[m * p.J + j] = make_uint4(e[0] | (e[1] << 16), e[2] | (e[3] << 16), e[4] | (e[5] << 16),
                                           e[6] | (e[7] << 16));

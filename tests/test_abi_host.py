@@ -124,7 +124,7 @@ def test_size_formulas_ternary_3in5():
 
 
 def test_size_formulas_int8_table_quantization():
-    """INT8 table quantization (Section 3.1.4): 8 one-byte codes and one FP32 scale per 4
+    """INT8 table quantization (Section 3.1.3): 8 one-byte codes and one FP32 scale per 4
     activations and token, i.e. 12 bytes against 16 for FP16 tables."""
     M, K, N = 5, 4096, 300
     p = L.problem(K, N, 2, L.WFMT_UINT, 128, L.ACT_FP16_LUT8)

@@ -1,4 +1,4 @@
-"""GPU parity of INT8 table quantization (Section 3.1.4; LUTGEMM_ACT_FP16_LUT8).
+"""GPU parity of INT8 table quantization (Section 3.1.3; LUTGEMM_ACT_FP16_LUT8).
 
 The approximation has its own reference, the table-quantized oracle
 (``oracle.mpgemm_lut8``, pinned in test_oracle_pins.py):
@@ -65,6 +65,12 @@ def test_lut8_precompute_matches_oracle_tables(wfmt, bits, group):
     banner(f"lut8 precompute wfmt={wfmt} b={bits} G={group}")
     M, K = 3, 2048
     inp = lut8(W.make_custom(wfmt, bits, group, W.ACT_FP16, M, K, 64, seed=11))
+    # token 2: magnitudes from FP16 subnormals to 6e4 in one group (an FP32 sum of the
+    # four terms would round) and groups whose 127 T / amax are half-integers (ties)
+    rng = np.random.default_rng(44)
+    mags = 2.0 ** rng.integers(-24, 15, size=K)
+    inp.act[2] = np.clip(rng.standard_normal(K) * mags, -6e4, 6e4).astype(np.float16)
+    inp.act[2, :8] = [-31.25, 31.25, 31.25, 33.25, 31.25, -31.25, -31.25, -33.25]
     gp = GpuProblem(inp)
     gp.lut()
     buf = gp.g.tables(M).cpu().numpy()

@@ -265,11 +265,88 @@ def test_quantizer_reduces_to_rint_and_bounds():
         assert err.max() <= s[m] * 0.5 * (1 + 1e-5)
 
 
-def test_int_output_rounding_order():
-    acc = np.array([[3, -7, 1 << 23]], dtype=np.int64)
-    y = oracle.int_output_f32(acc, np.array([np.float32(0.1)]), np.array([0.3, 0.07, 0.001], np.float32))
-    ref = (acc.astype(np.float32) * np.float32(0.1)) * np.array([0.3, 0.07, 0.001], np.float32)
-    assert np.array_equal(y, ref.astype(np.float32))
+def rne_binary32(x: Fraction) -> Fraction:
+    """Exact rational x rounded to the nearest IEEE binary32 value, ties to even
+    (24-bit significand, subnormals below 2^-126): the rounding IEEE 754 defines,
+    computed with integers only, independently of any hardware FP arithmetic."""
+    if x == 0:
+        return Fraction(0)
+    sign = -1 if x < 0 else 1
+    a = abs(x)
+    e = a.numerator.bit_length() - a.denominator.bit_length()
+    if Fraction(2) ** e > a:
+        e -= 1                                   # now 2^e <= a < 2^(e+1)
+    ulp = Fraction(2) ** (max(e, -126) - 23)
+    q = a / ulp
+    n = q.numerator // q.denominator
+    r = q - n
+    if r > Fraction(1, 2) or (r == Fraction(1, 2) and n % 2 == 1):
+        n += 1
+    return sign * n * ulp
+
+
+def test_rne_binary32_helper_matches_numpy_casts():
+    """The helper above is itself checked against numpy's float64 -> float32 cast on
+    values exactly representable in float64 (a single rounding there)."""
+    rng = np.random.default_rng(40)
+    vals = np.concatenate([rng.standard_normal(2000) * 10.0 ** rng.integers(-40, 30, 2000),
+                           [1 + 2.0 ** -24, 1 + 3 * 2.0 ** -24, -(1 + 2.0 ** -24), 2.0 ** -149 * 1.5]])
+    for v in vals:
+        assert rne_binary32(Fraction(float(v))) == Fraction(float(np.float32(v)))
+
+
+def test_int_output_exact_with_power_of_two_scales():
+    """Power-of-two scales and |acc| < 2^24: both FP32 multiplies are exact, so
+    y[i][c] must equal acc[i][c] * s_a[i] * s_w[c] exactly.  Distinct scales per row
+    and per column pin the indexing (a row/column mix-up changes every value)."""
+    rng = np.random.default_rng(41)
+    acc = rng.integers(-(1 << 23), 1 << 23, size=(3, 5)).astype(np.int64)
+    s_a = np.array([2.0 ** -3, 2.0 ** -7, 4.0], np.float32)
+    s_w = np.array([2.0 ** -5, 0.5, 1.0, 8.0, 2.0 ** -10], np.float32)
+    y = oracle.int_output_f32(acc, s_a, s_w)
+    assert y.shape == (3, 5) and y.dtype == np.float32
+    for i in range(3):
+        for c in range(5):
+            assert Fraction(float(y[i, c])) == int(acc[i, c]) * Fraction(float(s_a[i])) * Fraction(float(s_w[c]))
+    # transposing the scale roles would give other values
+    assert not np.array_equal(y, oracle.int_output_f32(acc, s_a[::-1].copy(), s_w[::-1].copy()))
+
+
+def test_int_output_large_accumulators_round_on_conversion():
+    """|acc| >= 2^24 is not exact in FP32: the conversion rounds to nearest, ties to
+    even (2^24 + 1 -> 2^24, 2^24 + 3 -> 2^24 + 4, -(2^25 + 2) -> -2^25, and
+    2^25 + 6 -> 2^25 + 8); with unit scales y is that rounded value."""
+    acc = np.array([[(1 << 24) + 1, (1 << 24) + 3, -((1 << 25) + 2), (1 << 25) + 6,
+                     (1 << 31) - 1]], dtype=np.int64)
+    y = oracle.int_output_f32(acc, np.array([1.0], np.float32), np.ones(5, np.float32))
+    expect = [1 << 24, (1 << 24) + 4, -(1 << 25), (1 << 25) + 8, 1 << 31]
+    assert [int(v) for v in y[0]] == expect
+
+
+def test_int_output_two_roundings_in_order():
+    """Random accumulators and scales: y equals RNE32(RNE32(RNE32(acc) s_a) s_w)
+    evaluated with exact rationals (the definition: two FP32 multiplies, the token
+    scale first); the result lies within two binary32 roundings of the exact product;
+    and the sample contains cases where the other association would differ, so the
+    order is really pinned."""
+    rng = np.random.default_rng(42)
+    R, C = 6, 40
+    acc = rng.integers(-(1 << 30), 1 << 30, size=(R, C)).astype(np.int64)
+    acc[:, :10] = rng.integers(-5000, 5000, size=(R, 10))
+    s_a = (rng.uniform(0.5, 1.0, R) * 2.0 ** rng.integers(-12, 2, R)).astype(np.float32)
+    s_w = rng.uniform(0.01, 0.1, C).astype(np.float32)
+    y = oracle.int_output_f32(acc, s_a, s_w)
+    other_order = 0
+    for i in range(R):
+        for c in range(C):
+            a, sa, sw = int(acc[i, c]), Fraction(float(s_a[i])), Fraction(float(s_w[c]))
+            want = rne_binary32(rne_binary32(rne_binary32(Fraction(a)) * sa) * sw)
+            assert Fraction(float(y[i, c])) == want
+            exact = a * sa * sw
+            assert abs(Fraction(float(y[i, c])) - exact) <= abs(exact) * Fraction(3, 1 << 24)
+            if rne_binary32(rne_binary32(Fraction(a)) * rne_binary32(sa * sw)) != want:
+                other_order += 1
+    assert other_order > 0
 
 
 # --------------------------------------------------------------------------- precompute definitions
@@ -346,7 +423,7 @@ def test_reference_output_int8_path():
     assert np.array_equal(y, yy.astype(np.float32))
 
 
-# ----------------------------------------------------------------- INT8 table quantization (Section 3.1.4)
+# ----------------------------------------------------------------- INT8 table quantization (Section 3.1.3)
 
 def _exact_table_activations(M, K, rng):
     """Integer activations whose groups of 4 have |a0| + |a1| + |a2| + |a3| = 127: the
@@ -417,3 +494,48 @@ def _as_lut8(inp):
     out = copy.copy(inp)
     out.act_kind = W.ACT_FP16_LUT8
     return out
+
+
+def _exact_codes(act_row_f16):
+    """Codes and FP32 scales of the INT8-quantized half tables of one token, from the
+    definition in exact rational arithmetic: T exact, q = round(127 T / amax) with
+    ties to even (Python's round on a Fraction), scale = amax / 127 rounded to binary32,
+    in the unit of the token normalized by its power of two."""
+    x = [Fraction(float(v)) for v in act_row_f16.astype(np.float32)]
+    amax_a = max(abs(v) for v in x)
+    unit = Fraction(1)
+    if amax_a != 0:
+        _, e = np.frexp(float(amax_a))
+        unit = Fraction(2) ** int(e)
+    codes, scales = [], []
+    for j in range(len(x) // 4):
+        h = L.half_table([v / unit for v in x[4 * j:4 * j + 4]])
+        tmax = max(abs(t) for t in h)
+        if tmax == 0:
+            codes.append([0] * 8)
+            scales.append(Fraction(0))
+            continue
+        codes.append([round(127 * t / tmax) for t in h])
+        scales.append(rne_binary32(tmax / 127))
+    return codes, scales
+
+
+def test_lut8_codes_round_half_even_exactly():
+    """The table-quantized oracle's codes and scales equal the exact-rational definition
+    on activations that mix magnitudes from FP16 subnormals to 6e4 (where an FP32 sum of
+    the four terms would round), and on groups built so that 127 T / amax is a
+    half-integer: (-31.25, 31.25, 31.25, 33.25) gives T = (-64.5, 2, -2, 64.5, -2, 64.5,
+    60.5, 127), so ties to even give (-64, 2, -2, 64, -2, 64, 60, 127) where rounding
+    half away from zero would give -65, 65, 61."""
+    rng = np.random.default_rng(43)
+    mags = 2.0 ** rng.integers(-24, 15, size=(3, 64))
+    act = np.clip(rng.standard_normal((3, 64)) * mags, -6e4, 6e4).astype(np.float16)
+    act[2, :8] = [-31.25, 31.25, 31.25, 33.25, 31.25, -31.25, -31.25, -33.25]
+    act[2, 8:12] = [2.0 ** -24, 1024.0, -3.0 * 2.0 ** -20, 7.0]
+    q, sc, mult = oracle.lut8_tables(act)
+    for m in range(3):
+        codes, scales = _exact_codes(act[m])
+        assert q[m].tolist() == codes
+        assert [Fraction(float(v)) for v in sc[m]] == scales
+    assert q[2, 0].tolist() == [-64, 2, -2, 64, -2, 64, 60, 127]
+    assert q[2, 1].tolist() == [64, -2, 2, -64, 2, -64, -60, -127]  # negated group: negated codes
