@@ -272,6 +272,46 @@ lutgemm_status_t lutgemm_mpgemm_dequant(const lutgemm_problem_t *problem, int64_
                                         int32_t out_dtype, int32_t accumulate, void *stream);
 
 /*
+ * Overrides of the launch planner, for tests and experiments only (normal use needs
+ * none).  Each key holds one integer, set when the library is loaded from the
+ * environment variable named beside it (if that is set) or else to its default;
+ * no entry point reads the environment after that.  Setting -1 restores the
+ * default.  The values are process-wide and apply to calls made after the setter
+ * returns; changing them while other threads call the library gives those calls
+ * either the old or the new value.  Kernel choices forced this way must still
+ * suit the problem (the planner clamps splits and block counts to the problem).
+ */
+enum {
+    LUTGEMM_TUNE_TARGET_BLOCKS = 0, /* LUTGEMM_TARGET_BLOCKS: workgroups a launch aims for (256)      */
+    LUTGEMM_TUNE_WHOLEK_MAX_KB = 1, /* LUTGEMM_WHOLEK_MAX_KB: largest packed weights, in kB, that the
+                                       single-token whole-K kernel takes (10000)                     */
+    LUTGEMM_TUNE_GEMV_KIND = 2,     /* LUTGEMM_GEMV_KIND: single-token kernel, 0 whole-K, 2 split-K
+                                       (default -1: by weight size)                                  */
+    LUTGEMM_TUNE_GEMV_CFG = 3,      /* LUTGEMM_GEMV_CFG: lane decomposition of the whole-K kernel (-1) */
+    LUTGEMM_TUNE_SPLITS = 4,        /* LUTGEMM_SPLITS: K splits of the whole-K kernel (0: planned)     */
+    LUTGEMM_TUNE_KBS = 5,           /* LUTGEMM_KBS: 128-blocks per workgroup of the split-K kernel
+                                       (0: planned)                                                  */
+    LUTGEMM_TUNE_MT16 = 6,          /* LUTGEMM_MT16: 0 keeps 8-token tiles from M = 16 on (1)         */
+    LUTGEMM_TUNE_MT_TARGET = 7,     /* LUTGEMM_MT_TARGET: multi-token grid target, in units of
+                                       TARGET_BLOCKS (8)                                              */
+    LUTGEMM_TUNE_MT_SPLITS = 8,     /* LUTGEMM_MT_SPLITS: K splits of the multi-token kernel
+                                       (0: planned)                                                  */
+    LUTGEMM_TUNE_MT_ORDER = 9,      /* LUTGEMM_MT_ORDER: multi-token workgroup order (-1: planned)    */
+    LUTGEMM_TUNE_DEQUANT_BIG = 10,  /* LUTGEMM_DEQUANT_BIG: 1 / 0 forces the 256x256 / 128x128
+                                       comparison kernel (-1: by grid size)                          */
+    LUTGEMM_TUNE_LOG = 11,          /* LUTGEMM_LOG: 1 prints each launch plan to stderr (0)           */
+    LUTGEMM_TUNE_COUNT = 12
+};
+
+/* Sets planner override `key` (LUTGEMM_TUNE_*) to `value` (-1: its default).
+ * LUTGEMM_ERROR_INVALID_VALUE for an unknown key or a value outside [-1, 2^24]
+ * (TARGET_BLOCKS: 0 is rejected too). */
+lutgemm_status_t lutgemm_set_tuning(int32_t key, int32_t value);
+
+/* Current value of planner override `key`; -2 for an unknown key. */
+int32_t lutgemm_get_tuning(int32_t key);
+
+/*
  * Measurement utility (not part of the method): reads `bytes` (rounded down to a
  * multiple of 16) of device memory at `src` with 128-bit loads from `blocks`
  * workgroups of 256 lanes and writes one 32-bit word per workgroup to `sink`

@@ -35,7 +35,12 @@ EXPORTS = [
     "lutgemm_table_size", "lutgemm_table_offsets", "lutgemm_workspace_size", "lutgemm_pack_weights",
     "lutgemm_precompute", "lutgemm_mpgemm", "lutgemm_mpgemm_dequant", "lutgemm_calibrate_stream_read",
     "lutgemm_fused_workspace_size", "lutgemm_mpgemm_fused", "lutgemm_calibrate_stream_read_ex",
+    "lutgemm_set_tuning", "lutgemm_get_tuning",
 ]
+
+# planner overrides (LUTGEMM_TUNE_*), for tests and experiments
+TUNE = {"TARGET_BLOCKS": 0, "WHOLEK_MAX_KB": 1, "GEMV_KIND": 2, "GEMV_CFG": 3, "SPLITS": 4, "KBS": 5,
+        "MT16": 6, "MT_TARGET": 7, "MT_SPLITS": 8, "MT_ORDER": 9, "DEQUANT_BIG": 10, "LOG": 11}
 
 
 class Problem(ctypes.Structure):
@@ -95,6 +100,10 @@ def _load():
     L.lutgemm_mpgemm_fused.argtypes = [PP, I64, P, P, P, I32, I32, P, SZ, P]
     L.lutgemm_calibrate_stream_read.restype = ctypes.c_int
     L.lutgemm_calibrate_stream_read.argtypes = [P, SZ, P, I32, P]
+    L.lutgemm_set_tuning.restype = ctypes.c_int
+    L.lutgemm_set_tuning.argtypes = [I32, I32]
+    L.lutgemm_get_tuning.restype = ctypes.c_int32
+    L.lutgemm_get_tuning.argtypes = [I32]
     L.lutgemm_calibrate_stream_read_ex.restype = ctypes.c_int
     L.lutgemm_calibrate_stream_read_ex.argtypes = [P, SZ, P, I32, I32, I32, P]
     return L
@@ -205,6 +214,15 @@ def calibrate_stream_read(src, nbytes: int, sink, blocks: int, stream=None):
     """Launch the streaming-read calibration kernel over ``nbytes`` of ``src``."""
     _check(lib.lutgemm_calibrate_stream_read(_ptr(src), nbytes, _ptr(sink), blocks, _stream(stream)),
            "lutgemm_calibrate_stream_read")
+
+
+def set_tuning(name: str, value: int):
+    """Planner override ``name`` (a key of ``TUNE``) to ``value`` (-1 restores its default)."""
+    _check(lib.lutgemm_set_tuning(TUNE[name], int(value)), "lutgemm_set_tuning")
+
+
+def get_tuning(name: str) -> int:
+    return int(lib.lutgemm_get_tuning(TUNE[name]))
 
 
 def calibrate_stream_read_ex(src, nbytes: int, sink, blocks: int, unroll: int = 4, flags: int = 0,

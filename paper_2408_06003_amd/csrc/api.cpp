@@ -4,6 +4,7 @@
 // lut_mpgemm.hip, lut_fused.hip and dequant_mfma.hip.
 #include <hip/hip_runtime.h>
 
+#include <atomic>
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
@@ -66,11 +67,35 @@ lutgemm_status_t check_problem(const lutgemm_problem_t *p, int64_t M) {
     return LUTGEMM_SUCCESS;
 }
 
-int env_int(const char *name, int dflt) {
-    const char *v = std::getenv(name);
-    if (!v || !*v) return dflt;
-    return std::atoi(v);
+// Planner overrides: environment variables read once, when the library is loaded
+// (a static initializer), then only changed through lutgemm_set_tuning.
+const char *const kTuneEnv[LUTGEMM_TUNE_COUNT] = {
+    "LUTGEMM_TARGET_BLOCKS", "LUTGEMM_WHOLEK_MAX_KB", "LUTGEMM_GEMV_KIND", "LUTGEMM_GEMV_CFG",
+    "LUTGEMM_SPLITS",        "LUTGEMM_KBS",           "LUTGEMM_MT16",      "LUTGEMM_MT_TARGET",
+    "LUTGEMM_MT_SPLITS",     "LUTGEMM_MT_ORDER",      "LUTGEMM_DEQUANT_BIG", "LUTGEMM_LOG"};
+const int kTuneDefault[LUTGEMM_TUNE_COUNT] = {256, 10000, -1, -1, 0, 0, 1, 8, 0, -1, -1, 0};
+std::atomic<int> g_tune[LUTGEMM_TUNE_COUNT];
+
+bool tune_value_ok(int key, int value) {
+    if (value < -1 || value > (1 << 24)) return false;
+    if (key == LUTGEMM_TUNE_TARGET_BLOCKS && value == 0) return false;
+    return true;
 }
+
+struct TuneInit {
+    TuneInit() {
+        for (int k = 0; k < LUTGEMM_TUNE_COUNT; ++k) {
+            int v = kTuneDefault[k];
+            const char *e = std::getenv(kTuneEnv[k]);
+            if (e && *e) {
+                const int x = std::atoi(e);
+                if (tune_value_ok(k, x) && x != -1) v = x;
+            }
+            g_tune[k].store(v, std::memory_order_relaxed);
+        }
+    }
+};
+const TuneInit g_tune_init;
 
 thread_local char g_last_error[256] = "";
 
@@ -85,6 +110,12 @@ lutgemm_status_t hip_status(int e) {
 
 namespace lutgemm {
 
+int tuning(int key) { return g_tune[key].load(std::memory_order_relaxed); }
+
+void set_last_error(const char *msg) { std::snprintf(g_last_error, sizeof(g_last_error), "%s", msg); }
+
+lutgemm_status_t hip_error(int e) { return e == 0 ? LUTGEMM_SUCCESS : hip_status(e); }
+
 // Work decomposition.
 // Single token (M <= 2, one grid layer per token): the GEMV kernel of
 // lut_gemv.hip; pick the widest lane decomposition (most columns per workgroup,
@@ -95,7 +126,7 @@ namespace lutgemm {
 // K ranges stay at least 32 blocks long).
 LutPlan plan_lut(const Layout &L, int64_t M) {
     LutPlan P{};
-    const int64_t target = env_int("LUTGEMM_TARGET_BLOCKS", 256);
+    const int64_t target = tuning(LUTGEMM_TUNE_TARGET_BLOCKS);
     const int64_t weight_bytes = L.KB * L.bits * L.N * 16;
     if (L.tri) {  // one token per grid layer, whole K, 16 columns per workgroup (lut_tri.hip)
         P.kind = 3;
@@ -107,8 +138,8 @@ LutPlan plan_lut(const Layout &L, int64_t M) {
         P.ws_bytes = 0;
         return P;
     }
-    int kind = M > 2 ? 1 : (weight_bytes <= (int64_t)env_int("LUTGEMM_WHOLEK_MAX_KB", 10000) * 1000 ? 0 : 2);
-    const int forced_kind = env_int("LUTGEMM_GEMV_KIND", -1);
+    int kind = M > 2 ? 1 : (weight_bytes <= (int64_t)tuning(LUTGEMM_TUNE_WHOLEK_MAX_KB) * 1000 ? 0 : 2);
+    const int forced_kind = tuning(LUTGEMM_TUNE_GEMV_KIND);
     if (M <= 2 && (forced_kind == 0 || forced_kind == 2)) kind = forced_kind;
     if (kind == 0) {
         P.kind = 0;
@@ -126,7 +157,7 @@ LutPlan plan_lut(const Layout &L, int64_t M) {
                 pick = i;
                 break;
             }
-        const int forced = env_int("LUTGEMM_GEMV_CFG", -1);
+        const int forced = tuning(LUTGEMM_TUNE_GEMV_CFG);
         if (forced >= 0 && forced < ncfg) pick = forced;
         P.gemv_cfg = pick;
         const int cw = cfg[pick][0], ck = cfg[pick][1];
@@ -136,7 +167,7 @@ LutPlan plan_lut(const Layout &L, int64_t M) {
         if (blocks < target) splits = (target + blocks - 1) / blocks;
         const int64_t max_splits = (L.KB + ck - 1) / ck;  // at least one chunk per split
         if (splits > max_splits) splits = max_splits;
-        const int fs = env_int("LUTGEMM_SPLITS", 0);
+        const int fs = tuning(LUTGEMM_TUNE_SPLITS);
         if (fs > 0) splits = fs;
         int64_t kbs = (L.KB + splits - 1) / splits;
         kbs = (kbs + ck - 1) / ck * ck;
@@ -157,7 +188,7 @@ LutPlan plan_lut(const Layout &L, int64_t M) {
         const int kmax = 8 / L.bits;
         auto n_splits = [&](int k) { return (L.KB + k - 1) / k; };
         int kbs = L.bits == 4 ? 1 : 4 / L.bits;
-        const int forced = env_int("LUTGEMM_KBS", 0);
+        const int forced = tuning(LUTGEMM_TUNE_KBS);
         if (forced == 1 || forced == 2 || forced == 4 || forced == 8) {
             kbs = forced > kmax ? kmax : forced;
         } else {
@@ -172,13 +203,13 @@ LutPlan plan_lut(const Layout &L, int64_t M) {
         P.kind = 1;
         // tokens per workgroup of the multi-token kernel (lut_mtok.hip): 16 from M = 16 on
         // (one decoded index serves two token halves), except with INT8-quantized tables
-        const int mt16 = env_int("LUTGEMM_MT16", 1);
+        const int mt16 = tuning(LUTGEMM_TUNE_MT16);
         P.mt = (M >= 16 && L.act != LUTGEMM_ACT_FP16_LUT8 && mt16) ? 16 : 8;
         P.m_tiles = (M + P.mt - 1) / P.mt;
         P.n_tiles = L.N_pad / NTILE;
         const int64_t base = P.n_tiles * P.m_tiles;
         const int64_t ch = L.bits == 1 ? 1 : 4 / L.bits;  // 128-blocks per chunk of the kernel
-        const int64_t mt_target = env_int("LUTGEMM_MT_TARGET", 8) * target;
+        const int64_t mt_target = tuning(LUTGEMM_TUNE_MT_TARGET) * target;
         int64_t splits = 1;
         if (base < mt_target) {
             splits = (mt_target + base - 1) / base;
@@ -194,7 +225,7 @@ LutPlan plan_lut(const Layout &L, int64_t M) {
         }
         const int64_t max_splits = (L.KB + ch - 1) / ch;  // at least one chunk per split
         if (splits > max_splits) splits = max_splits;
-        const int fs = env_int("LUTGEMM_MT_SPLITS", 0);
+        const int fs = tuning(LUTGEMM_TUNE_MT_SPLITS);
         if (fs > 0) splits = fs;
         if (splits * base >= MAX_TILES) splits = (MAX_TILES - 1) / base;
         if (splits < 1) splits = 1;
@@ -207,8 +238,8 @@ LutPlan plan_lut(const Layout &L, int64_t M) {
         // own contiguous share of the tiles in bands of 8 token tiles, tokens fastest
         // (the LLaMA-2-13B shape 1616 -> 1579 us, the 4096^3 prefill 704 -> 701 us); else
         // columns fastest (the XCD-aware orders measured up to 18 % slower at M = 16)
-        P.order = env_int("LUTGEMM_MT_ORDER", (P.m_tiles >= 16 && P.splits == 1) ? 8 : 0);
-        if (P.order < 0) P.order = 0;
+        P.order = tuning(LUTGEMM_TUNE_MT_ORDER);
+        if (P.order < 0) P.order = (P.m_tiles >= 16 && P.splits == 1) ? 8 : 0;
     }
     const int64_t rows = P.kind == 1 ? P.m_tiles * P.mt : M;
     P.ws_bytes = P.splits > 1 ? align256((size_t)P.splits * rows * L.N_pad * 4) : 0;
@@ -316,6 +347,17 @@ const char *lutgemm_version(void) { return "lutgemm-gfx950 0.1.0"; }
 
 const char *lutgemm_last_error(void) { return g_last_error; }
 
+lutgemm_status_t lutgemm_set_tuning(int32_t key, int32_t value) {
+    if (key < 0 || key >= LUTGEMM_TUNE_COUNT || !tune_value_ok(key, value)) return LUTGEMM_ERROR_INVALID_VALUE;
+    g_tune[key].store(value == -1 ? kTuneDefault[key] : value, std::memory_order_relaxed);
+    return LUTGEMM_SUCCESS;
+}
+
+int32_t lutgemm_get_tuning(int32_t key) {
+    if (key < 0 || key >= LUTGEMM_TUNE_COUNT) return -2;
+    return g_tune[key].load(std::memory_order_relaxed);
+}
+
 lutgemm_status_t lutgemm_validate(const lutgemm_problem_t *problem, int64_t M) {
     return check_problem(problem, M);
 }
@@ -419,7 +461,7 @@ lutgemm_status_t lutgemm_mpgemm(const lutgemm_problem_t *problem, int64_t M, con
         if (workspace_bytes < plan.ws_bytes) return LUTGEMM_ERROR_INSUFFICIENT_SIZE;
     }
     LutParams lp = lut_params(L, plan, M, tables, packed, out, out_dtype, accumulate, workspace);
-    if (env_int("LUTGEMM_LOG", 0)) log_plan("lutgemm_mpgemm", L, plan, M);
+    if (tuning(LUTGEMM_TUNE_LOG)) log_plan("lutgemm_mpgemm", L, plan, M);
     return hip_status(launch_lut(lp, L, plan, stream));
 }
 
@@ -448,7 +490,7 @@ lutgemm_status_t lutgemm_mpgemm_fused(const lutgemm_problem_t *problem, int64_t 
         if (workspace_bytes < fs.total) return LUTGEMM_ERROR_INSUFFICIENT_SIZE;
     }
     char *ws = (char *)workspace;
-    if (env_int("LUTGEMM_LOG", 0)) log_plan(fs.fused ? "lutgemm_mpgemm_fused" : "lutgemm_mpgemm_fused(unfused)", L, plan, M);
+    if (tuning(LUTGEMM_TUNE_LOG)) log_plan(fs.fused ? "lutgemm_mpgemm_fused" : "lutgemm_mpgemm_fused(unfused)", L, plan, M);
     if (!fs.fused) {  // precompute into the workspace, then the table-fed kernels
         st = lutgemm_precompute(problem, M, act, ws, fs.tables, stream);
         if (st != LUTGEMM_SUCCESS) return st;

@@ -390,11 +390,11 @@ void dequant_mfma_big_kernel(DequantParams p, int wfmt, int per_tensor) {
 int launch_dequant(const DequantParams &p, const Layout &L, void *stream) {
     hipStream_t s = (hipStream_t)stream;
     const int pt = L.per_tensor ? 1 : 0;
-    // 256 x 256 tiles when they alone fill the GPU (one workgroup per CU);
-    // LUTGEMM_DEQUANT_BIG=1 / 0 forces one kernel (tests, experiments)
+    // 256 x 256 tiles when they alone fill the GPU (one workgroup per CU); the
+    // LUTGEMM_TUNE_DEQUANT_BIG override forces one kernel (tests, experiments)
     const dim3 big((unsigned)(L.N_pad / QBN), (unsigned)((p.M + QBM - 1) / QBM));
-    const char *force = std::getenv("LUTGEMM_DEQUANT_BIG");
-    const bool use_big = force && *force ? std::atoi(force) != 0 : (int64_t)big.x * big.y >= 256;
+    const int force = tuning(LUTGEMM_TUNE_DEQUANT_BIG);
+    const bool use_big = force >= 0 ? force != 0 : (int64_t)big.x * big.y >= 256;
     if (use_big) {
         if (L.bits == 1)
             hipLaunchKernelGGL(dequant_mfma_big_kernel<1>, big, dim3(256), 0, s, p, L.wfmt, pt);

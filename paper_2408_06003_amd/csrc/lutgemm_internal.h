@@ -122,6 +122,14 @@ struct LutPlan {
 
 LutPlan plan_lut(const Layout &L, int64_t M);
 
+// Current value of planner override `key` (LUTGEMM_TUNE_*, see lutgemm_set_tuning).
+int tuning(int key);
+
+// Text returned by lutgemm_last_error for the calling thread.
+void set_last_error(const char *msg);
+// LUTGEMM_ERROR_HIP with the HIP error's text recorded for lutgemm_last_error.
+lutgemm_status_t hip_error(int e);
+
 // Kernel parameter blocks.
 struct PackParams {
     const void *codes;

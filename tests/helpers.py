@@ -63,6 +63,27 @@ class GpuProblem:
         return y
 
 
+class tuning:
+    """Context manager: planner overrides (``paper_2408_06003_amd.TUNE`` names) for the
+    duration of a block, restored to their previous values afterwards."""
+
+    def __init__(self, **kw):
+        self.kw = kw
+
+    def __enter__(self):
+        import paper_2408_06003_amd as L
+        self.old = {k: L.get_tuning(k) for k in self.kw}
+        for k, v in self.kw.items():
+            L.set_tuning(k, v)
+        return self
+
+    def __exit__(self, *exc):
+        import paper_2408_06003_amd as L
+        for k, v in self.old.items():
+            L.set_tuning(k, v)
+        return False
+
+
 def fp_errors(y, ref):
     y = np.asarray(y, dtype=np.float64)
     ref = np.asarray(ref, dtype=np.float64)

@@ -194,3 +194,25 @@ def test_fused_entry_point_rejects_before_launch():
     M = 8
     assert L.fused_workspace_size(p, M) >= L.table_size(p, M) + L.workspace_size(p, M)
     assert L.fused_workspace_size(L.problem(1000, 64, 2, L.WFMT_UINT, 0), 1) == 0  # invalid problem
+
+
+def test_tuning_overrides():
+    """Planner overrides go through lutgemm_set_tuning (no entry point reads the
+    environment per call): unknown keys and out-of-range values are rejected, -1
+    restores the default, and a forced value changes the planned workspace."""
+    assert L.lib.lutgemm_get_tuning(-1) == -2 and L.lib.lutgemm_get_tuning(99) == -2
+    assert L.lib.lutgemm_set_tuning(99, 1) == L.ERROR_INVALID_VALUE
+    assert L.lib.lutgemm_set_tuning(L.TUNE["KBS"], -2) == L.ERROR_INVALID_VALUE
+    assert L.lib.lutgemm_set_tuning(L.TUNE["TARGET_BLOCKS"], 0) == L.ERROR_INVALID_VALUE
+    old = L.get_tuning("GEMV_KIND")
+    p = L.problem(4096, 4096, 2, L.WFMT_UINT, 128)
+    ws = L.workspace_size(p, 1)
+    try:
+        L.set_tuning("GEMV_KIND", 2)   # the split-K kernel: partial sums need a workspace
+        assert L.get_tuning("GEMV_KIND") == 2
+        assert L.workspace_size(p, 1) > ws
+        L.set_tuning("GEMV_KIND", -1)
+        assert L.get_tuning("GEMV_KIND") == -1
+        assert L.workspace_size(p, 1) == ws
+    finally:
+        L.set_tuning("GEMV_KIND", old)

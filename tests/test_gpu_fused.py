@@ -130,11 +130,11 @@ def test_fused_zero_token_accumulate_determinism():
 
 @pytest.mark.parametrize("cid,M,K,N", [(3, 1, 4096, 1000), (3, 2, 11008, 300), (5, 1, 8192, 700),
                                        (1, 1, 1024, 1000), (1, 2, 2048, 257)])
-def test_fused_split_k_parity(cid, M, K, N, monkeypatch):
+def test_fused_split_k_parity(cid, M, K, N, tune):
     """The split-K GEMV with its tables built from the activations (FP path: FP32 entries,
     no token scaling), forced at reduced sizes: ragged column tails, one and two tokens,
     K split into many workgroups, zero points per 128-block."""
-    monkeypatch.setenv("LUTGEMM_GEMV_KIND", "2")
+    tune(GEMV_KIND=2)
     banner(f"fused split-K config={cid} M={M} K={K} N={N}")
     gp = GpuProblem(W.make_inputs(cid, 0, M=M, K=K, N=N))
     check_fused(gp, what=f"split-K config {cid} M={M} K={K} N={N}")
@@ -142,8 +142,8 @@ def test_fused_split_k_parity(cid, M, K, N, monkeypatch):
 
 @pytest.mark.parametrize("wfmt,bits,G", [(W.WFMT_UINT, 1, 128), (W.WFMT_UINT, 2, 1024), (W.WFMT_UINT, 4, 512),
                                          (W.WFMT_TERNARY, 2, 128), (W.WFMT_BINARY, 1, 2048)])
-def test_fused_split_k_formats(wfmt, bits, G, monkeypatch):
-    monkeypatch.setenv("LUTGEMM_GEMV_KIND", "2")
+def test_fused_split_k_formats(wfmt, bits, G, tune):
+    tune(GEMV_KIND=2)
     banner(f"fused split-K formats wfmt={wfmt} b={bits} G={G}")
     inp = W.make_custom(wfmt, bits, G, W.ACT_FP16, M=1, K=2048, N=640, seed=97)
     inp.act[0] *= np.float16(300)  # large activations: the FP32 tables need no token scaling

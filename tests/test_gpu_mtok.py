@@ -39,11 +39,11 @@ FP_CASES = [
 
 @pytest.mark.parametrize("mt16", [1, 0])
 @pytest.mark.parametrize("wfmt,bits,G,fp32,M,K,N,splits", FP_CASES)
-def test_multi_token_fp_layouts(wfmt, bits, G, fp32, M, K, N, splits, mt16, monkeypatch):
+def test_multi_token_fp_layouts(wfmt, bits, G, fp32, M, K, N, splits, mt16, tune):
     """mt16 = 0 keeps 8-token workgroups where 16-token ones would be used (M >= 16)."""
     if splits:
-        monkeypatch.setenv("LUTGEMM_MT_SPLITS", str(splits))
-    monkeypatch.setenv("LUTGEMM_MT16", str(mt16))
+        tune(MT_SPLITS=splits)
+    tune(MT16=mt16)
     what = f"wfmt={wfmt} b={bits} G={G} M={M} K={K} N={N} splits={splits}"
     print(f"\n[case] multi-token FP {what}", flush=True)
     inp = W.make_custom(wfmt, bits, G, W.ACT_FP16, M=M, K=K, N=N, seed=M + K + N + splits, scale_fp32=fp32)
@@ -65,9 +65,9 @@ INT_CASES = [
 
 
 @pytest.mark.parametrize("wfmt,bits,G,fp32,M,K,N,splits", INT_CASES)
-def test_multi_token_int8_layouts(wfmt, bits, G, fp32, M, K, N, splits, monkeypatch):
+def test_multi_token_int8_layouts(wfmt, bits, G, fp32, M, K, N, splits, tune):
     if splits:
-        monkeypatch.setenv("LUTGEMM_MT_SPLITS", str(splits))
+        tune(MT_SPLITS=splits)
     print(f"\n[case] multi-token INT8 wfmt={wfmt} b={bits} G={G} M={M} K={K} N={N} splits={splits}", flush=True)
     inp = W.make_custom(wfmt, bits, G, W.ACT_INT8, M=M, K=K, N=N, seed=M + K + N + splits, scale_fp32=fp32)
     gp = GpuProblem(inp)
@@ -80,11 +80,11 @@ def test_multi_token_int8_layouts(wfmt, bits, G, fp32, M, K, N, splits, monkeypa
 
 @pytest.mark.parametrize("M", [5, 17])
 @pytest.mark.parametrize("splits", [5, 9, 17, 33, 65, 128])
-def test_multi_token_many_splits(splits, M, monkeypatch):
+def test_multi_token_many_splits(splits, M, tune):
     """K split into 5 .. 128 ranges: the finalize kernel's load batch (4 .. 64 partials,
     looping when there are more) at every size it takes, FP and INT8 paths, with 8-token
     (M = 5) and 16-token (M = 17: one full tile and one with a single live row) workgroups."""
-    monkeypatch.setenv("LUTGEMM_MT_SPLITS", str(splits))
+    tune(MT_SPLITS=splits)
     print(f"\n[case] multi-token K splits={splits} (M={M}, K=16384, N=200)", flush=True)
     inp = W.make_custom(W.WFMT_BINARY, 1, 16384, W.ACT_FP16, M=M, K=16384, N=200, seed=300 + splits)
     gp = GpuProblem(inp)
@@ -101,11 +101,11 @@ def test_multi_token_many_splits(splits, M, monkeypatch):
 
 
 @pytest.mark.parametrize("order", [1, 8, 16])
-def test_multi_token_tile_orders(order, monkeypatch):
+def test_multi_token_tile_orders(order, tune):
     """XCD-aware workgroup orders (token-fastest, bands of 8 or 16 token tiles) over a
     grid whose token tiles do not fill the last band, every output against the oracle."""
-    monkeypatch.setenv("LUTGEMM_MT_ORDER", str(order))
-    monkeypatch.setenv("LUTGEMM_MT_SPLITS", "1")
+    tune(MT_ORDER=order)
+    tune(MT_SPLITS=1)
     print(f"\n[case] multi-token tile order {order} (M=300, K=1024, N=520)", flush=True)
     inp = W.make_custom(W.WFMT_UINT, 2, 128, W.ACT_FP16, M=300, K=1024, N=520, seed=500 + order)
     gp = GpuProblem(inp)
@@ -114,10 +114,10 @@ def test_multi_token_tile_orders(order, monkeypatch):
 
 @pytest.mark.parametrize("splits", [1, 3])
 @pytest.mark.parametrize("M", [10, 20])
-def test_multi_token_accumulate(M, splits, monkeypatch):
+def test_multi_token_accumulate(M, splits, tune):
     """O += A W^T through the multi-token kernel's own epilogue (one split) and through the
     finalize kernel (three splits), FP32 and FP16 outputs, and the INT8 path's INT32 output."""
-    monkeypatch.setenv("LUTGEMM_MT_SPLITS", str(splits))
+    tune(MT_SPLITS=splits)
     print(f"\n[case] multi-token accumulate M={M} splits={splits}", flush=True)
     inp = W.make_custom(W.WFMT_UINT, 2, 128, W.ACT_FP16, M=M, K=1024, N=300, seed=600 + M + splits)
     gp = GpuProblem(inp)

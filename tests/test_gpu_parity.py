@@ -235,10 +235,10 @@ def test_extreme_scales():
 
 @pytest.mark.parametrize("cid,M,K,N", [(4, 300, 1024, 520), (3, 257, 2048, 300), (5, 280, 1024, 600),
                                        (6, 512, 1024, 256)])
-def test_dequant_big_tile_parity(cid, M, K, N, monkeypatch):
+def test_dequant_big_tile_parity(cid, M, K, N, tune):
     """The 256 x 256 pipelined dequantization + MFMA kernel (chosen for large M) on
     small shapes with ragged M and N tails, every output against the oracle."""
-    monkeypatch.setenv("LUTGEMM_DEQUANT_BIG", "1")
+    tune(DEQUANT_BIG=1)
     banner(f"dequant 256x256 tile config={cid} M={M} K={K} N={N}")
     gp = GpuProblem(W.make_inputs(cid, 0, M=M, K=K, N=N))
     check_fp_path(gp, dequant=True, what=f"dequant big config {cid}")
@@ -246,13 +246,13 @@ def test_dequant_big_tile_parity(cid, M, K, N, monkeypatch):
 
 
 @pytest.mark.parametrize("kbs", [0, 1, 4])
-def test_split_k_gemv_two_tokens(kbs, monkeypatch):
+def test_split_k_gemv_two_tokens(kbs, tune):
     """The table-fed split-K GEMV (forced) with two tokens and a ragged column tail, K
     split into 8-64 ranges summed by the finalize kernel: FP (all outputs within the FP
     bar) and INT8 (bit-exact) paths, and accumulation through the finalize epilogue."""
-    monkeypatch.setenv("LUTGEMM_GEMV_KIND", "2")
+    tune(GEMV_KIND=2)
     if kbs:
-        monkeypatch.setenv("LUTGEMM_KBS", str(kbs))
+        tune(KBS=kbs)
     banner(f"split-K GEMV M=2 kbs={kbs or 'planned'}")
     inp = W.make_custom(W.WFMT_UINT, 2, 128, W.ACT_FP16, M=2, K=8192, N=777, seed=800 + kbs)
     gp = GpuProblem(inp)
