@@ -223,6 +223,26 @@ lutgemm_status_t lutgemm_mpgemm(const lutgemm_problem_t *problem, int64_t M, con
                                 int32_t accumulate, void *workspace, size_t workspace_bytes,
                                 void *stream);
 
+/* Size of the static scratch array behind lutgemm_mpgemm_noalloc, per GPU. */
+#define LUTGEMM_NOALLOC_SCRATCH_BYTES ((size_t)16 << 20)
+
+/*
+ * lutgemm_mpgemm without a workspace argument, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid allocation).  Same arguments, kernels and results as lutgemm_mpgemm; the
+ * K-split partial sums go to a static device array of
+ * LUTGEMM_NOALLOC_SCRATCH_BYTES per GPU that the library holds until the process
+ * ends (its address is looked up on the first call with each device current).
+ * Calls needing more scratch than that (lutgemm_workspace_size) return
+ * LUTGEMM_ERROR_NOT_SUPPORTED and launch nothing, with the sizes in
+ * lutgemm_last_error().  No call allocates or frees memory.  All calls on one GPU
+ * share its array: calls that overlap on one GPU (other streams, other threads)
+ * race on it and must be serialized by the caller.
+ */
+lutgemm_status_t lutgemm_mpgemm_noalloc(const lutgemm_problem_t *problem, int64_t M, const void *tables,
+                                        const void *packed, void *out, int32_t out_dtype,
+                                        int32_t accumulate, void *stream);
+
 /*
  * Bytes of scratch memory lutgemm_mpgemm_fused needs for M tokens; may be 0.  No
  * initialization is required; a workspace must not be shared by calls that run

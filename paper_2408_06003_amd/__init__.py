@@ -35,7 +35,7 @@ EXPORTS = [
     "lutgemm_table_size", "lutgemm_table_offsets", "lutgemm_workspace_size", "lutgemm_pack_weights",
     "lutgemm_precompute", "lutgemm_mpgemm", "lutgemm_mpgemm_dequant", "lutgemm_calibrate_stream_read",
     "lutgemm_fused_workspace_size", "lutgemm_mpgemm_fused", "lutgemm_calibrate_stream_read_ex",
-    "lutgemm_set_tuning", "lutgemm_get_tuning",
+    "lutgemm_set_tuning", "lutgemm_get_tuning", "lutgemm_mpgemm_noalloc",
 ]
 
 # planner overrides (LUTGEMM_TUNE_*), for tests and experiments
@@ -100,6 +100,8 @@ def _load():
     L.lutgemm_mpgemm_fused.argtypes = [PP, I64, P, P, P, I32, I32, P, SZ, P]
     L.lutgemm_calibrate_stream_read.restype = ctypes.c_int
     L.lutgemm_calibrate_stream_read.argtypes = [P, SZ, P, I32, P]
+    L.lutgemm_mpgemm_noalloc.restype = ctypes.c_int
+    L.lutgemm_mpgemm_noalloc.argtypes = [PP, I64, P, P, P, I32, I32, P]
     L.lutgemm_set_tuning.restype = ctypes.c_int
     L.lutgemm_set_tuning.argtypes = [I32, I32]
     L.lutgemm_get_tuning.restype = ctypes.c_int32
@@ -189,6 +191,13 @@ def mpgemm(p: Problem, M: int, tables, packed, out, out_dtype: int, accumulate: 
     _check(lib.lutgemm_mpgemm(ctypes.byref(p), M, _ptr(tables), _ptr(packed), _ptr(out), out_dtype,
                               1 if accumulate else 0, _ptr(workspace), workspace_bytes, _stream(stream)),
            "lutgemm_mpgemm")
+
+
+def mpgemm_noalloc(p: Problem, M: int, tables, packed, out, out_dtype: int, accumulate: bool = False,
+                   stream=None):
+    """lutgemm_mpgemm with the library's static scratch array instead of a workspace."""
+    _check(lib.lutgemm_mpgemm_noalloc(ctypes.byref(p), M, _ptr(tables), _ptr(packed), _ptr(out), out_dtype,
+                                      1 if accumulate else 0, _stream(stream)), "lutgemm_mpgemm_noalloc")
 
 
 def fused_workspace_size(p: Problem, M: int) -> int:

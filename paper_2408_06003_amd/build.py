@@ -19,7 +19,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "liblutgemm.so")
-SOURCES = ["api.cpp", "pack.hip", "precompute.hip", "lut_gemv.hip", "lut_mpgemm.hip", "lut_fused.hip", "lut_mtok.hip", "lut_tri.hip", "dequant_mfma.hip", "calib.hip"]
+SOURCES = ["api.cpp", "pack.hip", "precompute.hip", "lut_gemv.hip", "lut_mpgemm.hip", "lut_fused.hip", "lut_mtok.hip", "lut_tri.hip", "dequant_mfma.hip", "calib.hip", "noalloc.hip"]
 ARCH = "gfx950"
 
 COMMON = [
