@@ -36,6 +36,10 @@ METRIC = "effective TOPS + HBM GB/s (% of peak) for LUT mpGEMM, M=1 and M=4096"
 HBM_PEAK_GBPS = 8000.0
 MFMA_FP16_PEAK_TFLOPS = 2500.0
 ROTATION_BYTES = 1 << 30
+# read patterns of the streaming-read ceiling (workgroups, 16-byte loads per lane):
+# the best single-launch reads of 4-48 MB and of 1 GiB in a sweep over grid size,
+# loads in flight, nontemporal hints and workgroup ranges (profiles/stream_read_ceiling.txt)
+STREAM_READ_CONFIGS = ((1024, 2), (512, 4), (512, 8))
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "pmc_traffic.txt")
 # sources that define each timed kernel and its launch (a PMC traffic record is used
 # only while they hash as when the counters were taken)
@@ -207,19 +211,26 @@ class Case:
         """The same step through lutgemm_mpgemm_fused (tables built inside the LUT kernel)."""
         if not hasattr(self, "fws"):
             n = self.L.fused_workspace_size(self.p, self.M)
-            self.fws = self.torch.empty(n, dtype=self.torch.uint8, device="cuda") if n else None
+            self.fws = self.torch.zeros(n, dtype=self.torch.uint8, device="cuda") if n else None
         self.L.mpgemm_fused(self.p, self.M, self.act, self.packed[i % len(self.packed)], self.out,
                             self.out_code, False, workspace=self.fws)
 
-    def timed(self, fn, n, graph=True, check=None, reps=1):
-        """Average milliseconds per call over n back-to-back calls, timed with HIP events
-        on the stream they run on.  With graph=True the n calls are captured once into a
-        HIP graph and replayed, so host launch overhead is not counted (the way a decode
-        loop runs); ``check`` (a function returning a tensor) compares two replays,
-        separated by eager work, with the eager result.  With reps > 1 the replay is
-        timed reps times and the median batch is returned."""
+    def timed(self, fn, n, graph=True, check=None, reps=5):
+        """Milliseconds per call of n back-to-back calls, timed with HIP events on the
+        stream they run on.  With graph=True the calls are captured into HIP graphs and
+        replayed, so host launch overhead is not counted (the way a decode loop runs).
+        Every graph holds n calls on its own slice of the rotation set, and enough graphs
+        are captured to cover the whole set (>= 1 GiB of distinct weight copies); the
+        graphs are replayed in turn and each replay is timed on its own, so between two
+        replays of one graph at least 1 GiB of other weights has been read and every
+        timed call reads its weights from HBM, whatever n is.  At least ``reps`` replays
+        are timed (every graph at least once) and the median is returned;
+        ``self.last_distinct_bytes`` records the distinct weight bytes they read.
+        ``check`` (a function returning a tensor) compares a replay, after eager work,
+        with the eager result."""
         torch = self.torch
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        R = len(self.packed)
         if not graph:
             s = torch.cuda.current_stream()
             torch.cuda.synchronize()
@@ -229,12 +240,16 @@ class Case:
             e1.record(s)
             torch.cuda.synchronize()
             return e0.elapsed_time(e1) / n
+        n_graphs = max(1, -(-R // n))
         side = torch.cuda.Stream()
         side.wait_stream(torch.cuda.current_stream())
-        g = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(g, stream=side):
-            for i in range(n):
-                fn(i)
+        graphs = []
+        for gi in range(n_graphs):
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g, stream=side):
+                for j in range(n):
+                    fn(gi * n + j)
+            graphs.append(g)
         torch.cuda.synchronize()
         if check is not None:
             for _ in range(2):
@@ -242,20 +257,26 @@ class Case:
                 torch.cuda.synchronize()
                 ref = check().clone()
                 check().zero_()
-                g.replay()
+                graphs[0].replay()
                 torch.cuda.synchronize()
                 if not torch.equal(check(), ref):
                     raise RuntimeError(f"{self.name}: graph replay differs from the eager result")
-        g.replay()  # warm replay
+        for g in graphs:  # warm replays of every slice
+            g.replay()
         torch.cuda.synchronize()
         s = torch.cuda.current_stream()
-        batches = []
-        for _ in range(reps):
+        batches, touched = [], set()
+        for r in range(max(reps, n_graphs)):
+            gi = r % n_graphs
+            torch.cuda.synchronize()
             e0.record(s)
-            g.replay()
+            graphs[gi].replay()
             e1.record(s)
             torch.cuda.synchronize()
             batches.append(e0.elapsed_time(e1) / n)
+            touched.update((gi * n + j) % R for j in range(n))
+        self.last_distinct_bytes = len(touched) * self.packed[0].numel()
+        self.last_replays = len(batches)
         return sorted(batches)[len(batches) // 2]
 
     def cold_call_us(self, fn, i):
@@ -280,19 +301,28 @@ class Case:
             self.step(i)
         self.precompute()
         ms_mp = self.timed(self.mpgemm, n_kernel, check=lambda: self.out, reps=5)
+        distinct = self.last_distinct_bytes
         ms_pre = self.timed(lambda i: self.precompute(), n_kernel, reps=5)
         b = algorithmic_bytes(self.inp, self.out_bytes, tri=self.tri, lut8=self.lut8)
         gbps = b["total"] / (ms_mp * 1e-3) / 1e9
-        # achievable streaming read of the same byte count, same rotation and timing
+        # the achievable single-launch read of the same byte count, same rotation and
+        # timing: the fastest of the read patterns the calibration sweep found best
+        # (nontemporal 16-byte loads; grid and loads in flight per lane vary with size)
         sink = self.torch.zeros(4096, dtype=self.torch.int32, device="cuda")
         wb = self.L.packed_weight_size(self.p)
-        ms_rd = self.timed(lambda i: self.L.calibrate_stream_read(self.packed[i % len(self.packed)], wb, sink, 1024),
-                           n_kernel, reps=5)
+        R = len(self.packed)
+        ms_rd, rd_cfg = None, None
+        for blocks, unroll in STREAM_READ_CONFIGS:
+            ms = self.timed(lambda i: self.L.calibrate_stream_read_ex(self.packed[i % R], wb, sink, blocks, unroll, 1),
+                            n_kernel, reps=5)
+            if ms_rd is None or ms < ms_rd:
+                ms_rd, rd_cfg = ms, f"{blocks} workgroups x 256 lanes, {unroll} nontemporal 16-B loads in flight per lane"
         ms_fu = self.timed(self.fused, n_kernel, check=lambda: self.out, reps=5)
         rec = {"workload": self.name, "M": self.M, "K": self.K, "N": self.N, "bits": self.inp.bits,
                "mpgemm_us": round(ms_mp * 1e3, 3), "mpgemm_tops": round(self.effective_tops(ms_mp), 3),
                "mpgemm_gbps": round(gbps, 1), "hbm_frac": round(gbps / HBM_PEAK_GBPS, 4),
-               "stream_read_us": round(ms_rd * 1e3, 3),
+               "distinct_weight_bytes_timed": distinct,
+               "stream_read_us": round(ms_rd * 1e3, 3), "stream_read_cfg": rd_cfg,
                "stream_read_gbps": round(wb / (ms_rd * 1e-3) / 1e9, 1),
                "frac_of_stream_read": round(ms_rd / ms_mp, 4),
                "precompute_us": round(ms_pre * 1e3, 3),
@@ -574,6 +604,7 @@ def main():
     torch.cuda.synchronize()
     # the step as one kernel (headline) and as two calls (tables through HBM)
     ms_step = head.timed(head.fused, K, check=lambda: head.out)
+    step_distinct, step_replays = head.last_distinct_bytes, head.last_replays
     ms_step_eager = head.timed(head.fused, K, graph=False)
     ms_two = head.timed(head.step, K, check=lambda: head.out)
     ms_two_eager = head.timed(head.step, K, graph=False)
@@ -610,8 +641,12 @@ def main():
                    "output": "FP32 (float(acc) s_a) s_w",
                    "step": "lutgemm_mpgemm_fused: INT8 quantization + table build in LDS + bit-serial "
                            "lookup + epilogue, one kernel"},
-        "timing": "HIP graph of the K steps replayed once between HIP events (host launch overhead "
-                  "excluded); ms_per_step_eager launches the same steps one by one from Python",
+        "timing": "HIP graphs of K steps, one per slice of a >= 1 GiB rotation set of packed-weight copies, "
+                  "replayed in turn; each replay of K steps is timed on its own between HIP events (host launch "
+                  "overhead excluded) and ms_per_step is the median replay / K, so every timed step reads its "
+                  "weights from HBM whatever K is; ms_per_step_eager launches the same steps one by one from Python",
+        "timed_replays": step_replays,
+        "distinct_weight_bytes_timed": step_distinct,
         "ms_per_step_eager": round(ms_step_eager, 6),
         "single_call_cold_us": cold_us,
         "hbm_gbps_step": achieved,

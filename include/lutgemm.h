@@ -165,9 +165,14 @@ lutgemm_status_t lutgemm_table_offsets(const lutgemm_problem_t *problem, int64_t
                                        size_t *s_offset, size_t *t_offset);
 
 /*
- * Bytes of scratch memory lutgemm_mpgemm needs for M tokens (partial sums when
- * K is split across workgroups); may be 0.  No initialization is required; a
- * workspace must not be shared by calls that run concurrently.
+ * Bytes of scratch memory lutgemm_mpgemm needs for M tokens (partial sums when K
+ * is split across workgroups, and the arrival counters with which the single-token
+ * split-K kernel completes the split itself); may be 0.  The workspace must be
+ * zero-filled before its first use.  Its first 64 KiB hold the arrival counters:
+ * every call leaves them zero again (the kernel re-arms them) and nothing else is
+ * ever stored there, so one zero fill per allocation suffices even when the
+ * workspace is shared by calls on different problems.  A workspace must not be
+ * shared by calls that run concurrently.
  */
 size_t lutgemm_workspace_size(const lutgemm_problem_t *problem, int64_t M);
 
@@ -232,7 +237,8 @@ lutgemm_status_t lutgemm_mpgemm(const lutgemm_problem_t *problem, int64_t M, con
  * forbid allocation).  Same arguments, kernels and results as lutgemm_mpgemm; the
  * K-split partial sums go to a static device array of
  * LUTGEMM_NOALLOC_SCRATCH_BYTES per GPU that the library holds until the process
- * ends (its address is looked up on the first call with each device current).
+ * ends (its address is looked up on the first call with each device current; it
+ * is zero when the library is loaded and every call leaves it zeroed).
  * Calls needing more scratch than that (lutgemm_workspace_size) return
  * LUTGEMM_ERROR_NOT_SUPPORTED and launch nothing, with the sizes in
  * lutgemm_last_error().  No call allocates or frees memory.  All calls on one GPU
@@ -244,9 +250,9 @@ lutgemm_status_t lutgemm_mpgemm_noalloc(const lutgemm_problem_t *problem, int64_
                                         int32_t accumulate, void *stream);
 
 /*
- * Bytes of scratch memory lutgemm_mpgemm_fused needs for M tokens; may be 0.  No
- * initialization is required; a workspace must not be shared by calls that run
- * concurrently.
+ * Bytes of scratch memory lutgemm_mpgemm_fused needs for M tokens; may be 0.  As
+ * for lutgemm_workspace_size: zero-filled before its first use, left zero-filled by
+ * every call, not shared by calls that run concurrently.
  */
 size_t lutgemm_fused_workspace_size(const lutgemm_problem_t *problem, int64_t M);
 

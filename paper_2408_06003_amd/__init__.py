@@ -297,7 +297,7 @@ class LutGemm:
             return None
         key = ("fused", M)
         if key not in self._ws:
-            self._ws[key] = torch.empty(n, dtype=torch.uint8, device=self.device)
+            self._ws[key] = torch.zeros(n, dtype=torch.uint8, device=self.device)
         return self._ws[key]
 
     def fused(self, act, out=None, out_dtype=None, accumulate=False, stream=None):

@@ -141,6 +141,9 @@ LutPlan plan_lut(const Layout &L, int64_t M) {
     int kind = M > 2 ? 1 : (weight_bytes <= (int64_t)tuning(LUTGEMM_TUNE_WHOLEK_MAX_KB) * 1000 ? 0 : 2);
     const int forced_kind = tuning(LUTGEMM_TUNE_GEMV_KIND);
     if (M <= 2 && (forced_kind == 0 || forced_kind == 2)) kind = forced_kind;
+    // the split-K GEMV keeps one arrival counter per (token, 256-column tile); layers with
+    // more tiles than the counter area holds fill the GPU without a K split anyway
+    if (kind == 2 && M * (L.N_pad / NTILE) > CNT_MAX) kind = 0;
     if (kind == 0) {
         P.kind = 0;
         P.mt = 1;
@@ -175,27 +178,23 @@ LutPlan plan_lut(const Layout &L, int64_t M) {
         P.kbs = (int)kbs;
         P.splits = (int)((L.KB + kbs - 1) / kbs);
     } else if (kind == 2) {
-        // split-K GEMV: 256 columns per workgroup, KBS 128-blocks each.  Start from four
-        // weight words per lane; double KBS while there are more splits than the
-        // finalize kernel sums in one batch of loads; then halve it while the grid stays
-        // within 16 x `target` workgroups and the splits within that batch (measured on
-        // the LLaMA-shaped decode layers: 1-bit 8192 x 28672 takes KBS 2, 28672 x 8192
-        // KBS 4, 4-bit 11008 x 4096 KBS 2)
+        // split-K GEMV: 256 columns per workgroup (one per lane), KBS 128-blocks each, the
+        // K split completed inside the kernel.  About eight weight words per lane (KBS =
+        // 8 / b): few, long-lived workgroups that the GPU holds all at once, so the
+        // end-of-workgroup arrival protocol never delays a waiting workgroup; KBS is
+        // halved only while the grid would have fewer than 2 x `target` workgroups
         P.kind = 2;
         P.mt = 1;
         P.m_tiles = M;
         P.n_tiles = L.N_pad / NTILE;
         const int kmax = 8 / L.bits;
         auto n_splits = [&](int k) { return (L.KB + k - 1) / k; };
-        int kbs = L.bits == 4 ? 1 : 4 / L.bits;
+        int kbs = kmax;
         const int forced = tuning(LUTGEMM_TUNE_KBS);
         if (forced == 1 || forced == 2 || forced == 4 || forced == 8) {
             kbs = forced > kmax ? kmax : forced;
         } else {
-            while (kbs < kmax && n_splits(kbs) > FIN_BATCH) kbs <<= 1;
-            while (kbs > 1 && n_splits(kbs / 2) <= FIN_BATCH &&
-                   P.n_tiles * M * n_splits(kbs / 2) <= 16 * target)
-                kbs >>= 1;
+            while (kbs > 1 && P.n_tiles * M * n_splits(kbs) < 2 * target) kbs >>= 1;
         }
         P.kbs = kbs;
         P.splits = (int)((L.KB + kbs - 1) / kbs);
@@ -242,7 +241,9 @@ LutPlan plan_lut(const Layout &L, int64_t M) {
         if (P.order < 0) P.order = (P.m_tiles >= 16 && P.splits == 1) ? 8 : 0;
     }
     const int64_t rows = P.kind == 1 ? P.m_tiles * P.mt : M;
-    P.ws_bytes = P.splits > 1 ? align256((size_t)P.splits * rows * L.N_pad * 4) : 0;
+    // [arrival counters: CNT_AREA][partial sums]
+    P.part_off = CNT_AREA;
+    P.ws_bytes = P.splits > 1 ? CNT_AREA + align256((size_t)P.splits * rows * L.N_pad * 4) : 0;
     return P;
 }
 
@@ -253,7 +254,7 @@ namespace lutgemm {
 // Kernel parameters of one LUT mpGEMM call (tables in the layout of lutgemm_table_size).
 static LutParams lut_params(const Layout &L, const LutPlan &plan, int64_t M, const void *tables,
                             const void *packed, void *out, int32_t out_dtype, int32_t accumulate,
-                            void *partials) {
+                            void *workspace) {
     TableLayout T = make_table_layout(L, M);
     LutParams lp{};
     lp.T = (const uint4 *)tables;
@@ -264,7 +265,8 @@ static LutParams lut_params(const Layout &L, const LutPlan &plan, int64_t M, con
     lp.sgn = L.tri ? (const uint32_t *)((const char *)packed + L.sgn_off) : nullptr;
     lp.meta = (const char *)packed + L.meta_off;
     lp.out = out;
-    lp.part = plan.splits > 1 ? (float *)partials : nullptr;
+    lp.part = plan.splits > 1 ? (float *)((char *)workspace + plan.part_off) : nullptr;
+    lp.cnt = plan.kind == 2 && plan.splits > 1 ? (uint32_t *)workspace : nullptr;
     lp.M = M;
     lp.N = L.N;
     lp.N_pad = L.N_pad;
@@ -302,11 +304,12 @@ static void log_plan(const char *who, const Layout &L, const LutPlan &plan, int6
                  plan.kbs, plan.splits, plan.mt, (long long)plan.n_tiles, plan.splits, (long long)plan.m_tiles);
 }
 
-// Scratch of lutgemm_mpgemm_fused: the fused GEMV needs partial sums and the
-// per-token factors only when it splits K; otherwise tables, then the partials.
+// Scratch of lutgemm_mpgemm_fused: the plan's workspace (counters, partial sums) at
+// offset 0 as for lutgemm_mpgemm, then the per-token factors when the fused GEMV
+// splits K, or the staged tables when the call runs precompute + mpGEMM.
 struct FusedScratch {
     bool fused;
-    size_t tables, part_off, tok_off, total;
+    size_t tables, tables_off, tok_off, total;
 };
 
 static FusedScratch fused_scratch(const Layout &L, const LutPlan &plan, int64_t M) {
@@ -317,13 +320,12 @@ static FusedScratch fused_scratch(const Layout &L, const LutPlan &plan, int64_t 
     f.fused = ((plan.kind == 0 || plan.kind == 3) && L.act != LUTGEMM_ACT_FP16_LUT8) ||
               (plan.kind == 2 && L.act == LUTGEMM_ACT_FP16);
     if (f.fused) {
-        f.part_off = 0;
         f.tok_off = plan.ws_bytes;
         f.total = plan.splits > 1 ? plan.ws_bytes + align256((size_t)M * 4) : 0;
     } else {
         f.tables = make_table_layout(L, M).total;
-        f.part_off = align256(f.tables);
-        f.total = f.part_off + plan.ws_bytes;
+        f.tables_off = align256(plan.ws_bytes);
+        f.total = f.tables_off + f.tables;
     }
     return f;
 }
@@ -492,19 +494,16 @@ lutgemm_status_t lutgemm_mpgemm_fused(const lutgemm_problem_t *problem, int64_t 
     char *ws = (char *)workspace;
     if (tuning(LUTGEMM_TUNE_LOG)) log_plan(fs.fused ? "lutgemm_mpgemm_fused" : "lutgemm_mpgemm_fused(unfused)", L, plan, M);
     if (!fs.fused) {  // precompute into the workspace, then the table-fed kernels
-        st = lutgemm_precompute(problem, M, act, ws, fs.tables, stream);
+        st = lutgemm_precompute(problem, M, act, ws + fs.tables_off, fs.tables, stream);
         if (st != LUTGEMM_SUCCESS) return st;
-        LutParams lp = lut_params(L, plan, M, ws, packed, out, out_dtype, accumulate, ws + fs.part_off);
+        LutParams lp = lut_params(L, plan, M, ws + fs.tables_off, packed, out, out_dtype, accumulate, ws);
         return hip_status(launch_lut(lp, L, plan, stream));
     }
-    LutParams lp = lut_params(L, plan, M, nullptr, packed, out, out_dtype, accumulate, ws + fs.part_off);
+    LutParams lp = lut_params(L, plan, M, nullptr, packed, out, out_dtype, accumulate, ws);
     lp.act = (const uint16_t *)act;
     if (plan.kind == 3) return hip_status(launch_tri(lp, L, true, stream));
-    if (plan.kind == 2) {  // FP activations: tables from the activations, then the split sum
-        int e = launch_fused_split(lp, L, plan, stream);
-        if (e == 0 && plan.splits > 1) e = launch_finalize(lp, L, plan, stream);
-        return hip_status(e);
-    }
+    if (plan.kind == 2)  // FP activations: tables from the activations, split sum in the kernel
+        return hip_status(launch_fused_split(lp, L, plan, stream));
     lp.tok_out = plan.splits > 1 ? (float *)(ws + fs.tok_off) : nullptr;
     int e = launch_fused_gemv(lp, L, plan, stream);
     if (e == 0 && plan.splits > 1) {

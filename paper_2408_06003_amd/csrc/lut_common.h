@@ -372,4 +372,62 @@ __device__ __forceinline__ void add_partials(const LutParams &p, int s0, const f
     }
 }
 
+// Nontemporal 16-byte load (a streaming read that should not displace cached data):
+// used for the packed weights, which every call reads exactly once.
+__device__ __forceinline__ uint4 ld_nt(const uint4 *p) {
+    typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+    const u32x4 v = __builtin_nontemporal_load((const u32x4 *)p);
+    return make_uint4(v.x, v.y, v.z, v.w);
+}
+
+// Completes a K split inside the LUT kernel itself, with no second launch.  Every
+// workgroup publishes its partial sum of (m, n) with an agent-coherent store (written
+// through to memory), waits until all of its stores are acknowledged, and one lane
+// counts the workgroup on the arrival counter of its column tile.  The workgroup
+// that arrives last reads the partial sums of all splits back with agent-coherent
+// loads, adds them in split order (so the result does not depend on the order of
+// arrival), applies the output epilogue and re-arms the counter to 0 for the next
+// call.  No fence instruction is needed: the partial stores are complete before the
+// counter is touched, and the last workgroup's loads are issued after it has seen
+// the count.  Returns only after the output is stored (or at once for the others).
+// Partials of split s, row m at part[(s M + m) N_pad + n]; split 0 includes the
+// ternary group sum.
+template <bool INT8>
+__device__ __forceinline__ void split_complete(const LutParams &p, int wfmt, int64_t m, int64_t n, int split,
+                                               float yf, int yi, uint32_t *counter) {
+    __shared__ int is_last;
+    float *part = p.part + m * p.N_pad + n;
+    const int64_t stride = p.M * p.N_pad;
+    __hip_atomic_store(part + split * stride, INT8 ? __int_as_float(yi) : yf, __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_AGENT);
+    __builtin_amdgcn_s_waitcnt(0);  // every outstanding memory operation of this wave acknowledged
+    __syncthreads();
+    if (threadIdx.x == 0)
+        is_last = __hip_atomic_fetch_add(counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
+                  (uint32_t)(p.splits - 1);
+    __syncthreads();
+    if (!is_last) return;
+    const Epi ep = load_epi<INT8>(p, wfmt, m, n, false);
+    constexpr int PB = 16;
+    float sf = 0.f;
+    int si = 0;
+    for (int s0 = 0; s0 < p.splits; s0 += PB) {
+        float v[PB];
+#pragma unroll
+        for (int j = 0; j < PB; ++j) {
+            const int sp = s0 + j < p.splits ? s0 + j : p.splits - 1;
+            v[j] = __hip_atomic_load(part + sp * stride, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+#pragma unroll
+        for (int j = 0; j < PB; ++j) {
+            if (INT8)
+                si += s0 + j < p.splits ? __float_as_int(v[j]) : 0;
+            else
+                sf += s0 + j < p.splits ? v[j] : 0.f;
+        }
+    }
+    if (threadIdx.x == 0) __hip_atomic_store(counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    store_out<INT8>(p, wfmt, m, n, sf, si, ep);
+}
+
 }  // namespace lutgemm

@@ -113,7 +113,7 @@ __global__ __launch_bounds__(64 * NW) void lut_fused_gemv_kernel(LutParams p, in
         for (int t = 0; t < TW; ++t) {
             const int kbl = sigma + t * S, kbc = kbl < nkb ? kbl : nkb - 1;
 #pragma unroll
-            for (int i = 0; i < NPL; ++i) w[t][i] = p.planes[((kc + kbc) * BITS + pl * NPL + i) * p.N_pad + n];
+            for (int i = 0; i < NPL; ++i) w[t][i] = ld_nt(p.planes + ((kc + kbc) * BITS + pl * NPL + i) * p.N_pad + n);
         }
     };
     // FP path: lane e of a round holds activation e of the chunk, so the 4 lanes of a
@@ -365,7 +365,7 @@ __global__ __launch_bounds__(256) void lut_fused_split_kernel(LutParams p, int w
     for (int kbl = 0; kbl < KBS; ++kbl) {
         const int kbc = kbl < nkb ? kbl : nkb - 1;
 #pragma unroll
-        for (int t = 0; t < BITS; ++t) w[kbl][t] = p.planes[((kb0 + kbc) * BITS + t) * p.N_pad + n];
+        for (int t = 0; t < BITS; ++t) w[kbl][t] = ld_nt(p.planes + ((kb0 + kbc) * BITS + t) * p.N_pad + n);
     }
     uint2 mw[KBS];
 #pragma unroll
@@ -423,13 +423,13 @@ __global__ __launch_bounds__(256) void lut_fused_split_kernel(LutParams p, int w
     if (p.splits == 1)
         store_out<false>(p, wfmt, m, n, yf, 0, ep);
     else
-        p.part[((int64_t)split * p.M + m) * p.N_pad + n] = yf;
+        split_complete<false>(p, wfmt, m, n, split, yf, 0, p.cnt + m * gridDim.x + blockIdx.x);
 }
 
 template <int BITS>
 static void launch_fused_split_bits(const LutParams &p, const Layout &L, const LutPlan &plan, hipStream_t s) {
     const dim3 grid((unsigned)(L.N_pad / NTILE), (unsigned)plan.splits, (unsigned)p.M);
-    switch (plan.kbs) {
+    switch (plan.kbs) {  // the planner keeps KBS <= 8 / b (and KBS x 32 groups <= 256 lanes)
     case 1: hipLaunchKernelGGL((lut_fused_split_kernel<BITS, 1>), grid, dim3(256), 0, s, p, L.wfmt); break;
     case 2: hipLaunchKernelGGL((lut_fused_split_kernel<BITS, 2>), grid, dim3(256), 0, s, p, L.wfmt); break;
     case 4:

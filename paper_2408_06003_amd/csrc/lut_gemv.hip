@@ -78,7 +78,7 @@ __global__ __launch_bounds__(64 * NW) void lut_gemv2_kernel(LutParams p, int wfm
         for (int t = 0; t < TW; ++t) {
             const int kbl = sigma + t * S, kbc = kbl < nkb ? kbl : nkb - 1;
 #pragma unroll
-            for (int i = 0; i < NPL; ++i) w_[t][i] = p.planes[((kc + kbc) * BITS + pl * NPL + i) * p.N_pad + n];
+            for (int i = 0; i < NPL; ++i) w_[t][i] = ld_nt(p.planes + ((kc + kbc) * BITS + pl * NPL + i) * p.N_pad + n);
         }
     };
 
@@ -165,14 +165,15 @@ __global__ __launch_bounds__(64 * NW) void lut_gemv2_kernel(LutParams p, int wfm
     }
 }
 
-// Split-K variant for large N.  One lane per column and 256 columns per
+// Split-K variant for large weights.  One lane per column and 256 columns per
 // workgroup, so each staged table serves 256 columns (the widest reuse); each
 // workgroup covers KBS 128-blocks of K and every load of the workgroup (its half
-// tables first, then all KBS x b weight words of each lane) is issued before
-// anything waits.  The 4 wavefronts read the same table at a time (no bank
+// tables first, then all KBS x b weight words of each lane, nontemporal) is issued
+// before anything waits.  The 4 wavefronts read the same table at a time (no bank
 // conflicts) and the compile-time table offsets leave one SDWA AND per lookup.
-// With more than one K split the partial sums go to the workspace and
-// lut_finalize_kernel adds them in split order.
+// With more than one K split the workgroups of a column tile complete the sum
+// themselves (split_complete: the last one to finish adds the partials in split
+// order), so the call is one launch.
 template <int BITS, int KBS, bool INT8, bool TQ>
 __global__ __launch_bounds__(256) void lut_gemv_split_kernel(LutParams p, int wfmt) {
     constexpr int QPT = (KBS * GPB * 4 + 255) / 256;  // table quarters per thread
@@ -203,7 +204,7 @@ __global__ __launch_bounds__(256) void lut_gemv_split_kernel(LutParams p, int wf
     for (int kbl = 0; kbl < KBS; ++kbl) {
         const int kbc = kbl < nkb ? kbl : nkb - 1;
 #pragma unroll
-        for (int t = 0; t < BITS; ++t) w[kbl][t] = p.planes[((kb0 + kbc) * BITS + t) * p.N_pad + n];
+        for (int t = 0; t < BITS; ++t) w[kbl][t] = ld_nt(p.planes + ((kb0 + kbc) * BITS + t) * p.N_pad + n);
     }
     BlkMeta bm[KBS];
     if constexpr (!INT8) {
@@ -254,13 +255,13 @@ __global__ __launch_bounds__(256) void lut_gemv_split_kernel(LutParams p, int wf
     if (p.splits == 1)
         store_out<INT8>(p, wfmt, m, n, yf, yi, ep);
     else
-        p.part[((int64_t)split * p.M + m) * p.N_pad + n] = INT8 ? __int_as_float(yi) : yf;
+        split_complete<INT8>(p, wfmt, m, n, split, yf, yi, p.cnt + m * gridDim.x + blockIdx.x);
 }
 
 template <int BITS, bool INT8, bool TQ>
 static void launch_split(const LutParams &p, const Layout &L, const LutPlan &plan, hipStream_t s) {
     const dim3 grid((unsigned)(L.N_pad / NTILE), (unsigned)plan.splits, (unsigned)p.M);
-    switch (plan.kbs) {
+    switch (plan.kbs) {  // at most 8 weight words per lane (the planner keeps KBS <= 8 / b)
     case 1: hipLaunchKernelGGL((lut_gemv_split_kernel<BITS, 1, INT8, TQ>), grid, dim3(256), 0, s, p, L.wfmt); break;
     case 2: hipLaunchKernelGGL((lut_gemv_split_kernel<BITS, 2, INT8, TQ>), grid, dim3(256), 0, s, p, L.wfmt); break;
     case 4:

@@ -44,6 +44,12 @@ constexpr int FIN_BATCH = 64;   // split partial sums the finalize kernel reques
 constexpr int TBLK = 96;        // activations per 3-in-5 block (32 triples)
 constexpr int TPB = 32;         // triples per 3-in-5 block
 constexpr int TENT = 16;        // stored entries per triple table (14 used, 2 zero)
+// Every workspace that is needed at all starts with this many bytes of arrival
+// counters (zero between calls, touched only by the split-K GEMV, which re-arms
+// them); partial sums and staged tables always come after it, so no call can leave
+// a nonzero value where a later call, of any problem, expects a zero counter.
+constexpr size_t CNT_AREA = 65536;
+constexpr int64_t CNT_MAX = (int64_t)(CNT_AREA / 4);
 
 struct Layout {
     int64_t K, N, N_pad, KB, J, Q, G;  // G = group size (K when per-tensor)
@@ -118,6 +124,7 @@ struct LutPlan {
     int order;       // multi-token kernel: workgroup order (0: columns fastest; 1: tokens fastest
                      // per XCD; g >= 2: per XCD, bands of g token tiles, tokens fastest in a band)
     size_t ws_bytes;
+    size_t part_off;  // byte offset of the split partial sums in the workspace (counters at 0)
 };
 
 LutPlan plan_lut(const Layout &L, int64_t M);
@@ -165,6 +172,7 @@ struct LutParams {
     const void *meta;
     void *out;
     float *part;           // split partial sums [splits][rows][N_pad] (float or int bits)
+    uint32_t *cnt;         // split-K GEMV: arrival counters [M][n_tiles], zero between calls
     int64_t M, N, N_pad, K, KB, J, Q, G;
     int splits, kbs, out_dtype, accumulate;
     int kpg;               // 128-blocks of K per quantization group (G / 128)

@@ -10,7 +10,9 @@
 // that address is ever handed to kernels.  Every call on one GPU shares its
 // array, so calls that overlap on one GPU (different streams, or different host
 // threads) race on it.  The partial sums are written completely before they are
-// read within a call, so nothing in the array needs to start at zero.
+// read within a call; the arrival counters of the split-K GEMV must start at
+// zero: a static device array is zero when the code object is loaded, and every
+// call re-arms the counters it used, so the array stays a valid workspace.
 #include <hip/hip_runtime.h>
 
 #include <cstdio>

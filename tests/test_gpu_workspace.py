@@ -1,0 +1,134 @@
+"""Workspace sharing and buffer bounds of the GPU path.
+
+* One zero-filled workspace, sized for the largest call, is used in turn by calls on
+  different problems: the multi-token kernel with a K split (partial sums summed by
+  the finalize kernel), the single-token split-K GEMV (its K split completed inside
+  the kernel by arrival counters that must be zero when a call starts), the fused
+  entry point on both its fused and its precompute + mpGEMM path.  Every output must
+  equal, bit for bit, the same call made with a fresh workspace of its own.
+* Guard bands (canaries) of 4 KiB filled with a byte pattern around the output, the
+  workspace and the tables of each entry point must be unchanged after the call.
+"""
+import ctypes
+
+import numpy as np
+import pytest
+
+import workloads as W
+from helpers import problem_of, to_dev
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+if not torch.cuda.is_available():
+    pytest.skip("no GPU", allow_module_level=True)
+
+import paper_2408_06003_amd as L  # noqa: E402
+
+GUARD = 4096
+PATTERN = 0xA5
+
+
+class Guarded:
+    """A byte buffer of n bytes with a GUARD-byte band of PATTERN on each side."""
+
+    def __init__(self, n, fill=0):
+        self.n = n
+        self.full = torch.full((n + 2 * GUARD,), PATTERN, dtype=torch.uint8, device="cuda")
+        self.full[GUARD:GUARD + n] = fill
+        self.ptr = self.full.data_ptr() + GUARD
+
+    def view(self, dtype, shape):
+        return self.full[GUARD:GUARD + self.n].view(dtype).view(shape)
+
+    def check(self, what):
+        torch.cuda.synchronize()
+        lo, hi = self.full[:GUARD], self.full[GUARD + self.n:]
+        assert bool((lo == PATTERN).all()) and bool((hi == PATTERN).all()), f"{what}: write outside the buffer"
+
+
+def setup(inp, wfmt=None):
+    p = problem_of(inp, wfmt)
+    codes = to_dev(inp.codes)
+    scales = to_dev(inp.scales)
+    zeros = None if inp.zeros is None else to_dev(inp.zeros)
+    packed = Guarded(L.packed_weight_size(p))
+    L.pack_weights(p, codes, scales, zeros, packed.ptr, packed_bytes=packed.n)
+    packed.check("packed weights")
+    return p, packed, to_dev(inp.act)
+
+
+def out_dtype_of(inp):
+    return (torch.int32, L.OUT_INT32) if inp.act_kind == W.ACT_INT8 else (torch.float16, L.OUT_FP16)
+
+
+def run_mpgemm(p, M, act, packed, ws_ptr, ws_bytes, N, inp):
+    dt, code = out_dtype_of(inp)
+    tables = Guarded(L.table_size(p, M))
+    L.precompute(p, M, act, tables.ptr, table_bytes=tables.n)
+    out = Guarded(M * N * torch.tensor([], dtype=dt).element_size())
+    L.mpgemm(p, M, tables.ptr, packed.ptr, out.ptr, code, False, workspace=ws_ptr, workspace_bytes=ws_bytes)
+    tables.check("tables")
+    out.check("mpgemm output")
+    return out.view(dt, (M, N)).clone()
+
+
+def run_fused(p, M, act, packed, ws_ptr, ws_bytes, N, inp):
+    dt, code = out_dtype_of(inp)
+    out = Guarded(M * N * torch.tensor([], dtype=dt).element_size())
+    L.mpgemm_fused(p, M, act, packed.ptr, out.ptr, code, False, workspace=ws_ptr, workspace_bytes=ws_bytes)
+    out.check("fused output")
+    return out.view(dt, (M, N)).clone()
+
+
+CALLS = [
+    # (name, inputs, entry, forced split-K GEMV)
+    ("multi-token 16x8192x2048 binary (K split, finalize)", lambda: W.make_inputs(5, 0, M=16, N=2048), "mpgemm", False),
+    ("split-K 1x8192x3000 binary", lambda: W.make_inputs(5, 0, M=1, N=3000), "mpgemm", True),
+    ("split-K 2x4096x1000 INT4 g128", lambda: W.make_inputs(3, 1, M=2, N=1000), "mpgemm", True),
+    ("fused split-K 1x4096x2000 INT4", lambda: W.make_inputs(3, 1, M=1, N=2000), "fused", True),
+    ("fused two-call 1x4096x777 ternary INT8 (large-weight path)", lambda: W.make_inputs(2, 0, M=1, N=777), "fused", True),
+    ("split-K 1x8192x3000 binary again", lambda: W.make_inputs(5, 0, M=1, N=3000), "mpgemm", True),
+]
+
+
+def test_shared_workspace_across_problems(tune):
+    prepared = []
+    need = 0
+    for name, make, entry, split in CALLS:
+        inp = make()
+        tune(GEMV_KIND=2 if split else -1)
+        p, packed, act = setup(inp)
+        size = (L.workspace_size if entry == "mpgemm" else L.fused_workspace_size)(p, inp.M)
+        need = max(need, size)
+        prepared.append((name, inp, entry, split, p, packed, act, size))
+    shared = Guarded(need)
+    for name, inp, entry, split, p, packed, act, size in prepared:
+        print(f"\n[case] shared workspace: {name} (needs {size} B)", flush=True)
+        tune(GEMV_KIND=2 if split else -1)
+        run = run_mpgemm if entry == "mpgemm" else run_fused
+        own = Guarded(max(size, 16))
+        ref = run(p, inp.M, act, packed, own.ptr if size else None, size, inp.N, inp)
+        own.check(f"{name}: own workspace")
+        y = run(p, inp.M, act, packed, shared.ptr if need else None, need, inp.N, inp)
+        shared.check(f"{name}: shared workspace")
+        assert torch.equal(y, ref), f"{name}: shared workspace changed the result"
+        # the arrival counters are left zero for the next call
+        assert not shared.view(torch.uint8, (need,))[:65536].any(), f"{name}: counters not re-armed"
+
+
+def test_guard_bands_dequant_and_noalloc():
+    print("\n[case] guard bands: dequant comparison path and no-alloc entry", flush=True)
+    inp = W.make_inputs(5, 0, M=16, N=1000)
+    p, packed, act = setup(inp)
+    out = Guarded(16 * 1000 * 2)
+    L.mpgemm_dequant(p, 16, act, packed.ptr, out.ptr, L.OUT_FP16, False)
+    out.check("dequant output")
+    inp = W.make_inputs(3, 1, M=1, N=1000)
+    p, packed, act = setup(inp)
+    tables = Guarded(L.table_size(p, 1))
+    L.precompute(p, 1, act, tables.ptr, table_bytes=tables.n)
+    out = Guarded(1000 * 2)
+    L.mpgemm_noalloc(p, 1, tables.ptr, packed.ptr, out.ptr, L.OUT_FP16, False)
+    out.check("no-alloc output")
+    tables.check("tables")
