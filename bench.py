@@ -69,6 +69,11 @@ def parse():
                     help="print HBM traffic records from two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE; no GPU)")
     ap.add_argument("--summarize-counters", metavar="DIR", nargs="+", default=None,
                     help="print per-kernel utilization from rocprofv3 --pmc runs (no GPU)")
+    ap.add_argument("--timeline", metavar="WORKLOAD", default=None,
+                    help="per-wavefront phase timeline of one workload's single-token kernel, from the "
+                         "instrumented library (paper_2408_06003_amd/build.py --timeline)")
+    ap.add_argument("--timeline-entry", default="mpgemm", choices=("mpgemm", "fused"),
+                    help="entry point whose kernel the timeline records")
     ap.add_argument("--command", default="", help="the profiling command, recorded in a summary")
     ap.add_argument("--bench-logs", nargs="*", default=[],
                     help="bench.py outputs (JSON line last) whose headline launch times a trace summary quotes")
@@ -575,8 +580,88 @@ def summarize_counters(dirs, command=""):
     return "\n".join(out)
 
 
+TIMELINE_SLOTS = {
+    # kernel family -> names of the stamp slots it writes (see tl_stamp in csrc/lut_common.h)
+    "split": ("start", "tables in LDS", "lookups done", "partial stored+acked", "arrival counted",
+              "partials summed (last workgroup)", "end"),
+    "fused_gemv": ("start", "amax known", "tables built", "lookups done", "cross-wave barrier", "end"),
+    "gemv2": ("start", "first chunk's tables", None, "lookups done", "cross-wave barrier"),
+}
+
+
+def timeline(name, entry, n_calls=200):
+    """Phase timeline of the kernel of one workload (M <= 2), recorded by the instrumented
+    library: lane 0 of every wavefront stamps the 100 MHz real-time clock at each phase
+    boundary.  A graph of back-to-back calls on HBM-cold weight copies is replayed; the
+    stamps are those of its last call.  Prints per phase the distribution over wavefronts
+    (microseconds after the first wavefront started)."""
+    import ctypes
+    import numpy as np
+    import torch
+    import paper_2408_06003_amd as L
+    import workloads as W
+    torch.cuda.set_device(0)
+    tl_path = os.path.join(ROOT, "paper_2408_06003_amd", "liblutgemm_timeline.so")
+    L.lib = L._load(tl_path)
+    L.lib.lutgemm_timeline_set.argtypes = [ctypes.c_void_p]
+    found = None
+    for cid, w in W.WORKLOADS.items():
+        for (sid, M, _, _) in w.shapes():
+            if case_name(cid, sid, M) == name and M <= 2:
+                found = (cid, sid, M)
+    if not found:
+        raise SystemExit(f"no single-token workload named {name}")
+    c = Case(*found)
+    buf = torch.zeros(8 << 20, dtype=torch.int64, device="cuda")
+    L.lib.lutgemm_timeline_set(buf.data_ptr())
+    fn = c.fused if entry == "fused" else c.mpgemm
+    c.precompute()
+    for i in range(3):
+        fn(i)
+    ms = c.timed(fn, n_calls, reps=5)
+    torch.cuda.synchronize()
+    L.lib.lutgemm_timeline_set(None)
+    rec = buf.view(-1, 8).cpu().numpy()
+    rec = rec[rec[:, 0] != 0]
+    t0 = rec[:, 0].min()
+    us = (rec.astype(np.float64) - t0) / 100.0  # 100 MHz clock
+    us[rec == 0] = np.nan
+    if np.isfinite(us[:, 6]).any():  # only the split-K kernels stamp slot 6
+        fam = "split"
+    else:
+        fam = "fused_gemv" if entry == "fused" else "gemv2"
+    names = TIMELINE_SLOTS[fam]
+    lines = [f"# Phase timeline: {name}, lutgemm_{entry} ({fam} kernel)", "",
+             f"graph-timed {ms * 1e3:.3f} us per call (HBM-cold weights, back-to-back); stamps of the last call of "
+             f"a {n_calls}-call replay, {rec.shape[0]} wavefronts; microseconds after the first wavefront started", "",
+             f"{'phase':36s} {'waves':>6s} {'p10':>7s} {'p50':>7s} {'p90':>7s} {'max':>7s}"]
+    for k, nm in enumerate(names):
+        if nm is None:
+            continue
+        v = us[:, k]
+        v = v[np.isfinite(v)]
+        if v.size == 0:
+            continue
+        q = np.percentile(v, [10, 50, 90])
+        lines.append(f"{nm:36s} {v.size:6d} {q[0]:7.2f} {q[1]:7.2f} {q[2]:7.2f} {v.max():7.2f}")
+    # per-wavefront phase durations
+    lines += ["", "per-wavefront durations (median over wavefronts, us):"]
+    for a, b in zip(range(len(names)), range(1, len(names))):
+        if names[a] is None or names[b] is None:
+            continue
+        d = us[:, b] - us[:, a]
+        d = d[np.isfinite(d)]
+        if d.size:
+            lines.append(f"  {names[a]} -> {names[b]}: {np.median(d):.2f} (p90 {np.percentile(d, 90):.2f})")
+    c.release()
+    return "\n".join(lines)
+
+
 def main():
     args = parse()
+    if args.timeline:
+        print(timeline(args.timeline, args.timeline_entry))
+        return
     if args.summarize_trace or args.summarize_traffic or args.summarize_counters:
         if args.summarize_trace:
             print(summarize_trace(args.summarize_trace, args.command, args.bench_logs))

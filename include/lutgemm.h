@@ -326,7 +326,9 @@ enum {
     LUTGEMM_TUNE_DEQUANT_BIG = 10,  /* LUTGEMM_DEQUANT_BIG: 1 / 0 forces the 256x256 / 128x128
                                        comparison kernel (-1: by grid size)                          */
     LUTGEMM_TUNE_LOG = 11,          /* LUTGEMM_LOG: 1 prints each launch plan to stderr (0)           */
-    LUTGEMM_TUNE_COUNT = 12
+    LUTGEMM_TUNE_SPLIT_PRE = 12,    /* LUTGEMM_SPLIT_PRE: weight words per lane the split-K kernel
+                                       requests before its tables arrive, 0, 2, 4 or 8 = all (4)    */
+    LUTGEMM_TUNE_COUNT = 13
 };
 
 /* Sets planner override `key` (LUTGEMM_TUNE_*) to `value` (-1: its default).

@@ -40,7 +40,8 @@ EXPORTS = [
 
 # planner overrides (LUTGEMM_TUNE_*), for tests and experiments
 TUNE = {"TARGET_BLOCKS": 0, "WHOLEK_MAX_KB": 1, "GEMV_KIND": 2, "GEMV_CFG": 3, "SPLITS": 4, "KBS": 5,
-        "MT16": 6, "MT_TARGET": 7, "MT_SPLITS": 8, "MT_ORDER": 9, "DEQUANT_BIG": 10, "LOG": 11}
+        "MT16": 6, "MT_TARGET": 7, "MT_SPLITS": 8, "MT_ORDER": 9, "DEQUANT_BIG": 10, "LOG": 11,
+        "SPLIT_PRE": 12}
 
 
 class Problem(ctypes.Structure):
@@ -63,11 +64,11 @@ class LutGemmError(RuntimeError):
         self.status = status
 
 
-def _load():
-    if not os.path.exists(LIB_PATH):
-        raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build() "
+def _load(path: str = LIB_PATH):
+    if not os.path.exists(path):
+        raise ImportError(f"{path} is not built; run __graft_entry__.build() "
                           "(or python paper_2408_06003_amd/build.py) first")
-    L = ctypes.CDLL(LIB_PATH)
+    L = ctypes.CDLL(path)
     P, I64, I32, SZ = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_size_t
     PP = ctypes.POINTER(Problem)
     L.lutgemm_status_string.restype = ctypes.c_char_p

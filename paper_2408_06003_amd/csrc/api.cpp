@@ -72,8 +72,9 @@ lutgemm_status_t check_problem(const lutgemm_problem_t *p, int64_t M) {
 const char *const kTuneEnv[LUTGEMM_TUNE_COUNT] = {
     "LUTGEMM_TARGET_BLOCKS", "LUTGEMM_WHOLEK_MAX_KB", "LUTGEMM_GEMV_KIND", "LUTGEMM_GEMV_CFG",
     "LUTGEMM_SPLITS",        "LUTGEMM_KBS",           "LUTGEMM_MT16",      "LUTGEMM_MT_TARGET",
-    "LUTGEMM_MT_SPLITS",     "LUTGEMM_MT_ORDER",      "LUTGEMM_DEQUANT_BIG", "LUTGEMM_LOG"};
-const int kTuneDefault[LUTGEMM_TUNE_COUNT] = {256, 10000, -1, -1, 0, 0, 1, 8, 0, -1, -1, 0};
+    "LUTGEMM_MT_SPLITS",     "LUTGEMM_MT_ORDER",      "LUTGEMM_DEQUANT_BIG", "LUTGEMM_LOG",
+    "LUTGEMM_SPLIT_PRE"};
+const int kTuneDefault[LUTGEMM_TUNE_COUNT] = {256, 10000, -1, -1, 0, 0, 1, 8, 0, -1, -1, 0, 4};
 std::atomic<int> g_tune[LUTGEMM_TUNE_COUNT];
 
 bool tune_value_ok(int key, int value) {
@@ -98,6 +99,10 @@ struct TuneInit {
 const TuneInit g_tune_init;
 
 thread_local char g_last_error[256] = "";
+
+#ifdef LUTGEMM_TIMELINE
+unsigned long long *g_timeline = nullptr;  // instrumented builds: phase-stamp buffer
+#endif
 
 lutgemm_status_t hip_status(int e) {
     if (e == 0) return LUTGEMM_SUCCESS;
@@ -195,9 +200,18 @@ LutPlan plan_lut(const Layout &L, int64_t M) {
             kbs = forced > kmax ? kmax : forced;
         } else {
             while (kbs > 1 && P.n_tiles * M * n_splits(kbs) < 2 * target) kbs >>= 1;
+            // 1-bit weights: four words per lane (twice the workgroups) while the split
+            // stays short enough to complete in the kernel (1 x 8192 x 28672: 11.7 -> 10.9 us)
+            if (L.bits == 1 && kbs == 8 && n_splits(4) <= INKERNEL_MAX_SPLITS) kbs = 4;
         }
         P.kbs = kbs;
         P.splits = (int)((L.KB + kbs - 1) / kbs);
+        P.pre = tuning(LUTGEMM_TUNE_SPLIT_PRE);
+        // the last workgroup of a tile loads every split's partial sum in one batch: up to
+        // INKERNEL_MAX_SPLITS; beyond that the finalize kernel's wide batches are faster
+        // (measured: 1 x 11008 x 4096 INT4, 43 splits: 15.5 us in the kernel, 11.8 us with
+        // the finalize launch)
+        P.inkernel = P.splits > 1 && P.splits <= INKERNEL_MAX_SPLITS;
     } else {
         P.kind = 1;
         // tokens per workgroup of the multi-token kernel (lut_mtok.hip): 16 from M = 16 on
@@ -266,7 +280,7 @@ static LutParams lut_params(const Layout &L, const LutPlan &plan, int64_t M, con
     lp.meta = (const char *)packed + L.meta_off;
     lp.out = out;
     lp.part = plan.splits > 1 ? (float *)((char *)workspace + plan.part_off) : nullptr;
-    lp.cnt = plan.kind == 2 && plan.splits > 1 ? (uint32_t *)workspace : nullptr;
+    lp.cnt = plan.kind == 2 && plan.inkernel ? (uint32_t *)workspace : nullptr;
     lp.M = M;
     lp.N = L.N;
     lp.N_pad = L.N_pad;
@@ -295,6 +309,9 @@ static LutParams lut_params(const Layout &L, const LutPlan &plan, int64_t M, con
     }
     lp.out_dtype = out_dtype;
     lp.accumulate = accumulate;
+#ifdef LUTGEMM_TIMELINE
+    lp.tl = g_timeline;
+#endif
     return lp;
 }
 
@@ -348,6 +365,12 @@ const char *lutgemm_status_string(lutgemm_status_t s) {
 const char *lutgemm_version(void) { return "lutgemm-gfx950 0.1.0"; }
 
 const char *lutgemm_last_error(void) { return g_last_error; }
+
+#ifdef LUTGEMM_TIMELINE
+// Instrumented builds only (not declared in lutgemm.h): the device buffer that the
+// single-token kernels write their per-wavefront phase stamps to (NULL: none).
+void lutgemm_timeline_set(void *buf) { g_timeline = (unsigned long long *)buf; }
+#endif
 
 lutgemm_status_t lutgemm_set_tuning(int32_t key, int32_t value) {
     if (key < 0 || key >= LUTGEMM_TUNE_COUNT || !tune_value_ok(key, value)) return LUTGEMM_ERROR_INVALID_VALUE;
@@ -502,8 +525,11 @@ lutgemm_status_t lutgemm_mpgemm_fused(const lutgemm_problem_t *problem, int64_t 
     LutParams lp = lut_params(L, plan, M, nullptr, packed, out, out_dtype, accumulate, ws);
     lp.act = (const uint16_t *)act;
     if (plan.kind == 3) return hip_status(launch_tri(lp, L, true, stream));
-    if (plan.kind == 2)  // FP activations: tables from the activations, split sum in the kernel
-        return hip_status(launch_fused_split(lp, L, plan, stream));
+    if (plan.kind == 2) {  // FP activations: tables from the activations, then the split sum
+        int e = launch_fused_split(lp, L, plan, stream);
+        if (e == 0 && plan.splits > 1 && !plan.inkernel) e = launch_finalize(lp, L, plan, stream);
+        return hip_status(e);
+    }
     lp.tok_out = plan.splits > 1 ? (float *)(ws + fs.tok_off) : nullptr;
     int e = launch_fused_gemv(lp, L, plan, stream);
     if (e == 0 && plan.splits > 1) {

@@ -10,6 +10,37 @@
 
 namespace lutgemm {
 
+// Phase timestamps of instrumented builds (-DLUTGEMM_TIMELINE, never the product
+// library): lane 0 of each wavefront stores the 100 MHz real-time clock at a phase
+// boundary into slot `slot` of its record, p.tl[(linear workgroup id x waves per
+// workgroup + wave) x TL_SLOTS + slot].  Every use is a no-op in normal builds.
+constexpr int TL_SLOTS = 8;
+template <typename P>
+__device__ __forceinline__ void tl_stamp(const P &p, int slot) {
+#ifdef LUTGEMM_TIMELINE
+    if (p.tl && (threadIdx.x & 63) == 0) {
+        const uint64_t wg = ((uint64_t)blockIdx.z * gridDim.y + blockIdx.y) * gridDim.x + blockIdx.x;
+        p.tl[(wg * (blockDim.x >> 6) + (threadIdx.x >> 6)) * TL_SLOTS + slot] = wall_clock64();
+    }
+#else
+    (void)p;
+    (void)slot;
+#endif
+}
+
+template <typename P>
+__device__ __forceinline__ void tl_clear(const P &p, int slot) {
+#ifdef LUTGEMM_TIMELINE
+    if (p.tl && (threadIdx.x & 63) == 0) {
+        const uint64_t wg = ((uint64_t)blockIdx.z * gridDim.y + blockIdx.y) * gridDim.x + blockIdx.x;
+        p.tl[(wg * (blockDim.x >> 6) + (threadIdx.x >> 6)) * TL_SLOTS + slot] = 0;
+    }
+#else
+    (void)p;
+    (void)slot;
+#endif
+}
+
 // LDS-only barrier: waits for this wave's LDS writes (lgkmcnt) but not for its
 // global loads, so prefetches issued before it stay in flight.
 __device__ __forceinline__ void lds_barrier() {
@@ -401,31 +432,36 @@ __device__ __forceinline__ void split_complete(const LutParams &p, int wfmt, int
     __hip_atomic_store(part + split * stride, INT8 ? __int_as_float(yi) : yf, __ATOMIC_RELAXED,
                        __HIP_MEMORY_SCOPE_AGENT);
     __builtin_amdgcn_s_waitcnt(0);  // every outstanding memory operation of this wave acknowledged
+    tl_stamp(p, 3);
     __syncthreads();
     if (threadIdx.x == 0)
         is_last = __hip_atomic_fetch_add(counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
                   (uint32_t)(p.splits - 1);
     __syncthreads();
-    if (!is_last) return;
+    tl_stamp(p, 4);
+    if (!is_last) {
+        tl_clear(p, 5);
+        return;
+    }
+    // every split's partial in one batch of loads (splits <= INKERNEL_MAX_SPLITS, indices
+    // past the last split clamped to it), then the fixed-order sum
+    float v[INKERNEL_MAX_SPLITS];
+#pragma unroll
+    for (int j = 0; j < INKERNEL_MAX_SPLITS; ++j) {
+        const int sp = j < p.splits ? j : p.splits - 1;
+        v[j] = __hip_atomic_load(part + sp * stride, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
     const Epi ep = load_epi<INT8>(p, wfmt, m, n, false);
-    constexpr int PB = 16;
     float sf = 0.f;
     int si = 0;
-    for (int s0 = 0; s0 < p.splits; s0 += PB) {
-        float v[PB];
 #pragma unroll
-        for (int j = 0; j < PB; ++j) {
-            const int sp = s0 + j < p.splits ? s0 + j : p.splits - 1;
-            v[j] = __hip_atomic_load(part + sp * stride, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        }
-#pragma unroll
-        for (int j = 0; j < PB; ++j) {
-            if (INT8)
-                si += s0 + j < p.splits ? __float_as_int(v[j]) : 0;
-            else
-                sf += s0 + j < p.splits ? v[j] : 0.f;
-        }
+    for (int j = 0; j < INKERNEL_MAX_SPLITS; ++j) {
+        if (INT8)
+            si += j < p.splits ? __float_as_int(v[j]) : 0;
+        else
+            sf += j < p.splits ? v[j] : 0.f;
     }
+    tl_stamp(p, 5);
     if (threadIdx.x == 0) __hip_atomic_store(counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     store_out<INT8>(p, wfmt, m, n, sf, si, ep);
 }

@@ -90,6 +90,7 @@ __global__ __launch_bounds__(64 * NW) void lut_fused_gemv_kernel(LutParams p, in
     __shared__ int hsi[NW];          // INT8 path: activation sum of the K range, per wave
     __shared__ float wmax[NW];
 
+    tl_stamp(p, 0);
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int c = lane % CW;
     const int pl = (lane / CW) % PW;
@@ -165,6 +166,7 @@ __global__ __launch_bounds__(64 * NW) void lut_fused_gemv_kernel(LutParams p, in
     amax = wave_max(amax);
     if (lane == 63) wmax[wave] = amax;
     lds_barrier();
+    tl_stamp(p, 1);
     amax = wmax[0];
 #pragma unroll
     for (int v = 1; v < NW; ++v) amax = fmaxf(amax, wmax[v]);
@@ -229,6 +231,7 @@ __global__ __launch_bounds__(64 * NW) void lut_fused_gemv_kernel(LutParams p, in
             }
         }
         lds_barrier();
+        tl_stamp(p, 2);
 #pragma unroll
         for (int t = 0; t < TW; ++t) {
             const int kbl = sigma + t * S;
@@ -250,6 +253,7 @@ __global__ __launch_bounds__(64 * NW) void lut_fused_gemv_kernel(LutParams p, in
             }
         }
     }
+    tl_stamp(p, 3);
     float tok;
     if (INT8)
         tok = amax == 0.f ? 0.f : __fdiv_rn(amax, 127.0f);
@@ -275,6 +279,7 @@ __global__ __launch_bounds__(64 * NW) void lut_fused_gemv_kernel(LutParams p, in
         redi[wave][lane] = yi;
     }
     lds_barrier();
+    tl_stamp(p, 4);
     if (wave == 0 && lane < CW) {
         float sf = redf[0][lane];
         int si = redi[0][lane];
@@ -292,6 +297,7 @@ __global__ __launch_bounds__(64 * NW) void lut_fused_gemv_kernel(LutParams p, in
         else
             p.part[((int64_t)split * p.M + m) * p.N_pad + n] = INT8 ? __int_as_float(si) : sf;
     }
+    tl_stamp(p, 5);
 }
 
 // Same lane decompositions as the table-fed GEMV (see lut_gemv.hip): 16 wavefronts,
@@ -340,12 +346,15 @@ static void launch_fused_bits(const LutParams &p, const Layout &L, const LutPlan
 // FP32 entry.  The zero-point term of Eq. 3 is applied per 128-block (the sum over
 // a group's blocks of s'_q z'_q S_kb is s'_q z'_q S_q), with S_kb summed in a fixed
 // order over the 32 lanes that built the block's tables.
-template <int BITS, int KBS>
+template <int BITS, int KBS, int PRE>
 __global__ __launch_bounds__(256) void lut_fused_split_kernel(LutParams p, int wfmt) {
+    constexpr int NWD = KBS * BITS;              // weight words per lane
+    constexpr int NPRE = PRE < NWD ? PRE : NWD;  // of which issued before the table build
     constexpr int GS = 16;                 // entries per signed table
     constexpr int BLKF = (GPB + 1) * GS;   // floats per 128-block (padded by one table)
     __shared__ __attribute__((aligned(16))) float F[KBS * BLKF];
     __shared__ float Sblk[KBS];
+    tl_stamp(p, 0);
     const int tid = threadIdx.x;
     const int64_t n = (int64_t)blockIdx.x * NTILE + tid;
     const int split = blockIdx.y;
@@ -360,13 +369,6 @@ __global__ __launch_bounds__(256) void lut_fused_split_kernel(LutParams p, int w
     // activations: lane g holds group g of the workgroup's range (KBS x 32 <= 256 groups)
     const int g = tid, gc = g < nkb * GPB ? g : nkb * GPB - 1;
     const uint2 av = ((const uint2 *)(p.act + m * p.K))[kb0 * GPB + gc];
-    uint4 w[KBS][BITS];
-#pragma unroll
-    for (int kbl = 0; kbl < KBS; ++kbl) {
-        const int kbc = kbl < nkb ? kbl : nkb - 1;
-#pragma unroll
-        for (int t = 0; t < BITS; ++t) w[kbl][t] = ld_nt(p.planes + ((kb0 + kbc) * BITS + t) * p.N_pad + n);
-    }
     uint2 mw[KBS];
 #pragma unroll
     for (int kbl = 0; kbl < KBS; ++kbl) {
@@ -374,6 +376,15 @@ __global__ __launch_bounds__(256) void lut_fused_split_kernel(LutParams p, int w
         const int q = (int)(((float)(kb0 + kbc) + 0.5f) * p.inv_kpg);
         mw[kbl] = load_meta_words(p, q, lane_value(n));
     }
+    // the first NPRE weight words now, the rest once the tables are built (as in the
+    // table-fed split kernel: the activations are not queued behind the weight stream)
+    uint4 w[KBS][BITS];
+    auto load_word = [&](int i) {
+        const int kbl = i / BITS, t = i % BITS, kbc = kbl < nkb ? kbl : nkb - 1;
+        w[kbl][t] = ld_nt(p.planes + ((kb0 + kbc) * BITS + t) * p.N_pad + n);
+    };
+#pragma unroll
+    for (int i = 0; i < NPRE; ++i) load_word(i);
 
     // signed FP32 table of group g and the block sums
     const float x0 = h2f(av.x & 0xFFFFu), x1 = h2f(av.x >> 16), x2 = h2f(av.y & 0xFFFFu), x3 = h2f(av.y >> 16);
@@ -394,6 +405,10 @@ __global__ __launch_bounds__(256) void lut_fused_split_kernel(LutParams p, int w
         if ((tid & 31) == 0 && (tid >> 5) < KBS) Sblk[tid >> 5] = sg;
     }
     lds_barrier();
+    asm volatile("" ::: "memory");  // the remaining weight loads stay after the table build
+    tl_stamp(p, 1);
+#pragma unroll
+    for (int i = NPRE; i < NWD; ++i) load_word(i);
 
     float yf = 0.f;
 #pragma unroll
@@ -420,27 +435,39 @@ __global__ __launch_bounds__(256) void lut_fused_split_kernel(LutParams p, int w
             if (need_s) yf -= (sz.sp * sz.zp) * Sblk[kbl];
         }
     }
+    tl_stamp(p, 2);
     if (p.splits == 1)
         store_out<false>(p, wfmt, m, n, yf, 0, ep);
-    else
+    else if (p.cnt)
         split_complete<false>(p, wfmt, m, n, split, yf, 0, p.cnt + m * gridDim.x + blockIdx.x);
+    else  // long K splits: lut_finalize_kernel adds the partials after this kernel
+        p.part[((int64_t)split * p.M + m) * p.N_pad + n] = yf;
+    tl_stamp(p, 6);
+}
+
+template <int BITS, int PRE>
+static void launch_fused_split_pre(const LutParams &p, const Layout &L, const LutPlan &plan, hipStream_t s) {
+    const dim3 grid((unsigned)(L.N_pad / NTILE), (unsigned)plan.splits, (unsigned)p.M);
+    switch (plan.kbs) {  // the planner keeps KBS <= 8 / b (and KBS x 32 groups <= 256 lanes)
+    case 1: hipLaunchKernelGGL((lut_fused_split_kernel<BITS, 1, PRE>), grid, dim3(256), 0, s, p, L.wfmt); break;
+    case 2: hipLaunchKernelGGL((lut_fused_split_kernel<BITS, 2, PRE>), grid, dim3(256), 0, s, p, L.wfmt); break;
+    case 4:
+        if constexpr (BITS <= 2)
+            hipLaunchKernelGGL((lut_fused_split_kernel<BITS, 4, PRE>), grid, dim3(256), 0, s, p, L.wfmt);
+        break;
+    default:
+        if constexpr (BITS == 1)
+            hipLaunchKernelGGL((lut_fused_split_kernel<BITS, 8, PRE>), grid, dim3(256), 0, s, p, L.wfmt);
+        break;
+    }
 }
 
 template <int BITS>
 static void launch_fused_split_bits(const LutParams &p, const Layout &L, const LutPlan &plan, hipStream_t s) {
-    const dim3 grid((unsigned)(L.N_pad / NTILE), (unsigned)plan.splits, (unsigned)p.M);
-    switch (plan.kbs) {  // the planner keeps KBS <= 8 / b (and KBS x 32 groups <= 256 lanes)
-    case 1: hipLaunchKernelGGL((lut_fused_split_kernel<BITS, 1>), grid, dim3(256), 0, s, p, L.wfmt); break;
-    case 2: hipLaunchKernelGGL((lut_fused_split_kernel<BITS, 2>), grid, dim3(256), 0, s, p, L.wfmt); break;
-    case 4:
-        if constexpr (BITS <= 2)
-            hipLaunchKernelGGL((lut_fused_split_kernel<BITS, 4>), grid, dim3(256), 0, s, p, L.wfmt);
-        break;
-    default:
-        if constexpr (BITS == 1)
-            hipLaunchKernelGGL((lut_fused_split_kernel<BITS, 8>), grid, dim3(256), 0, s, p, L.wfmt);
-        break;
-    }
+    if (plan.pre == 0) launch_fused_split_pre<BITS, 0>(p, L, plan, s);
+    else if (plan.pre == 4) launch_fused_split_pre<BITS, 4>(p, L, plan, s);
+    else if (plan.pre >= 8) launch_fused_split_pre<BITS, 8>(p, L, plan, s);
+    else launch_fused_split_pre<BITS, 2>(p, L, plan, s);
 }
 
 int launch_fused_split(const LutParams &p, const Layout &L, const LutPlan &plan, void *stream) {

@@ -45,6 +45,7 @@ __global__ __launch_bounds__(64 * NW) void lut_gemv2_kernel(LutParams p, int wfm
     __shared__ float redf[NW][CW];
     __shared__ int redi[NW][CW];
 
+    tl_stamp(p, 0);
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int c = lane % CW;
     const int pl = (lane / CW) % PW;       // plane group of this lane
@@ -108,6 +109,7 @@ __global__ __launch_bounds__(64 * NW) void lut_gemv2_kernel(LutParams p, int wfm
         const bool more = kc + CK < kbB;
         if (more) load_chunk(kc + CK, tqn, wn);
         lds_barrier();
+        if (kc == kbA) tl_stamp(p, 1);
 #pragma unroll
         for (int t = 0; t < TW; ++t) {
             const int kbl = sigma + t * S;
@@ -135,6 +137,7 @@ __global__ __launch_bounds__(64 * NW) void lut_gemv2_kernel(LutParams p, int wfm
         }
     }
 
+    tl_stamp(p, 3);
     // combine the lanes of each column (fixed butterfly), then the wavefronts in order
 #pragma unroll
     for (int off = CW; off < 64; off <<= 1) {
@@ -148,6 +151,7 @@ __global__ __launch_bounds__(64 * NW) void lut_gemv2_kernel(LutParams p, int wfm
         redi[wave][lane] = yi;
     }
     lds_barrier();
+    tl_stamp(p, 4);
     if (wave == 0 && lane < CW) {
         float sf = redf[0][lane];
         int si = redi[0][lane];
@@ -167,17 +171,25 @@ __global__ __launch_bounds__(64 * NW) void lut_gemv2_kernel(LutParams p, int wfm
 
 // Split-K variant for large weights.  One lane per column and 256 columns per
 // workgroup, so each staged table serves 256 columns (the widest reuse); each
-// workgroup covers KBS 128-blocks of K and every load of the workgroup (its half
-// tables first, then all KBS x b weight words of each lane, nontemporal) is issued
-// before anything waits.  The 4 wavefronts read the same table at a time (no bank
-// conflicts) and the compile-time table offsets leave one SDWA AND per lookup.
-// With more than one K split the workgroups of a column tile complete the sum
-// themselves (split_complete: the last one to finish adds the partials in split
-// order), so the call is one launch.
-template <int BITS, int KBS, bool INT8, bool TQ>
+// workgroup covers KBS 128-blocks of K.  Load order: the half tables and the
+// epilogue operands, then the first PRE of the lane's KBS x b weight words
+// (nontemporal), then -- once the tables are in LDS -- the remaining words.  The
+// tables are tiny L2 hits, but requested behind a full load of weight misses they
+// would wait about one loaded HBM latency and hold every lookup back until the
+// weight stream is over; staged first, the lookups follow the weight words as they
+// arrive, while the PRE early words keep HBM busy during the table latency.  The 4
+// wavefronts read the same table at a time (no bank conflicts) and the
+// compile-time table offsets leave one SDWA AND per lookup.  With more than one K
+// split the workgroups of a column tile complete the sum themselves
+// (split_complete: the last one to finish adds the partials in split order), so the
+// call is one launch.
+template <int BITS, int KBS, bool INT8, bool TQ, int PRE>
 __global__ __launch_bounds__(256) void lut_gemv_split_kernel(LutParams p, int wfmt) {
-    constexpr int QPT = (KBS * GPB * 4 + 255) / 256;  // table quarters per thread
+    constexpr int QPT = (KBS * GPB * 4 + 255) / 256;  // table quantities per thread
+    constexpr int NWD = KBS * BITS;                  // weight words per lane
+    constexpr int NPRE = PRE < NWD ? PRE : NWD;      // of which issued before the table wait
     __shared__ __attribute__((aligned(16))) char F[KBS * Tab<INT8>::BLK];
+    tl_stamp(p, 0);
     const int tid = threadIdx.x;
     const int64_t n = (int64_t)blockIdx.x * NTILE + tid;
     const int split = blockIdx.y;
@@ -185,8 +197,8 @@ __global__ __launch_bounds__(256) void lut_gemv_split_kernel(LutParams p, int wf
     const int64_t kb0 = (int64_t)split * KBS;
     const int nkb = (int)((p.KB - kb0) < KBS ? (p.KB - kb0) : KBS);
 
-    // conditional loads (epilogue operands) first, then the unconditional chunk
-    // loads with clamped indices (see lut_gemv2_kernel)
+    // conditional loads (epilogue operands) first, then the unconditional loads with
+    // clamped indices (see lut_gemv2_kernel)
     Epi ep{};
     if (p.splits == 1)
         ep = load_epi<INT8>(p, wfmt, m, n, true);
@@ -199,13 +211,6 @@ __global__ __launch_bounds__(256) void lut_gemv_split_kernel(LutParams p, int wf
         const int e = tid + 256 * r, g = e >> 2, gc = g < nkb * GPB ? g : nkb * GPB - 1;
         tq[r] = load_quarter<TQ>(p, m * p.J + kb0 * GPB + gc, e & 1);
     }
-    uint4 w[KBS][BITS];
-#pragma unroll
-    for (int kbl = 0; kbl < KBS; ++kbl) {
-        const int kbc = kbl < nkb ? kbl : nkb - 1;
-#pragma unroll
-        for (int t = 0; t < BITS; ++t) w[kbl][t] = ld_nt(p.planes + ((kb0 + kbc) * BITS + t) * p.N_pad + n);
-    }
     BlkMeta bm[KBS];
     if constexpr (!INT8) {
 #pragma unroll
@@ -214,6 +219,13 @@ __global__ __launch_bounds__(256) void lut_gemv_split_kernel(LutParams p, int wf
             bm[kbl] = load_blk_meta(p, kb0 + kbc, m, lane_value(n));
         }
     }
+    uint4 w[KBS][BITS];
+    auto load_word = [&](int i) {
+        const int kbl = i / BITS, t = i % BITS, kbc = kbl < nkb ? kbl : nkb - 1;
+        w[kbl][t] = ld_nt(p.planes + ((kb0 + kbc) * BITS + t) * p.N_pad + n);
+    };
+#pragma unroll
+    for (int i = 0; i < NPRE; ++i) load_word(i);
 #pragma unroll
     for (int r = 0; r < QPT; ++r) {
         const int e = tid + 256 * r, g = e >> 2;
@@ -221,6 +233,10 @@ __global__ __launch_bounds__(256) void lut_gemv_split_kernel(LutParams p, int wf
             store_quarter<INT8, TQ>(F, g / GPB, g % GPB, e & 3, tq[r]);
     }
     lds_barrier();
+    asm volatile("" ::: "memory");  // the remaining weight loads stay after the table wait
+    tl_stamp(p, 1);
+#pragma unroll
+    for (int i = NPRE; i < NWD; ++i) load_word(i);
 
     float yf = 0.f;
     int yi = s_total;
@@ -252,27 +268,40 @@ __global__ __launch_bounds__(256) void lut_gemv_split_kernel(LutParams p, int wf
             }
         }
     }
+    tl_stamp(p, 2);
     if (p.splits == 1)
         store_out<INT8>(p, wfmt, m, n, yf, yi, ep);
-    else
+    else if (p.cnt)
         split_complete<INT8>(p, wfmt, m, n, split, yf, yi, p.cnt + m * gridDim.x + blockIdx.x);
+    else  // long K splits: lut_finalize_kernel adds the partials after this kernel
+        p.part[((int64_t)split * p.M + m) * p.N_pad + n] = INT8 ? __int_as_float(yi) : yf;
+    tl_stamp(p, 6);
 }
 
-template <int BITS, bool INT8, bool TQ>
-static void launch_split(const LutParams &p, const Layout &L, const LutPlan &plan, hipStream_t s) {
+template <int BITS, bool INT8, bool TQ, int PRE>
+static void launch_split_pre(const LutParams &p, const Layout &L, const LutPlan &plan, hipStream_t s) {
     const dim3 grid((unsigned)(L.N_pad / NTILE), (unsigned)plan.splits, (unsigned)p.M);
     switch (plan.kbs) {  // at most 8 weight words per lane (the planner keeps KBS <= 8 / b)
-    case 1: hipLaunchKernelGGL((lut_gemv_split_kernel<BITS, 1, INT8, TQ>), grid, dim3(256), 0, s, p, L.wfmt); break;
-    case 2: hipLaunchKernelGGL((lut_gemv_split_kernel<BITS, 2, INT8, TQ>), grid, dim3(256), 0, s, p, L.wfmt); break;
+    case 1: hipLaunchKernelGGL((lut_gemv_split_kernel<BITS, 1, INT8, TQ, PRE>), grid, dim3(256), 0, s, p, L.wfmt); break;
+    case 2: hipLaunchKernelGGL((lut_gemv_split_kernel<BITS, 2, INT8, TQ, PRE>), grid, dim3(256), 0, s, p, L.wfmt); break;
     case 4:
         if constexpr (BITS <= 2)
-            hipLaunchKernelGGL((lut_gemv_split_kernel<BITS, 4, INT8, TQ>), grid, dim3(256), 0, s, p, L.wfmt);
+            hipLaunchKernelGGL((lut_gemv_split_kernel<BITS, 4, INT8, TQ, PRE>), grid, dim3(256), 0, s, p, L.wfmt);
         break;
     default:
         if constexpr (BITS == 1)
-            hipLaunchKernelGGL((lut_gemv_split_kernel<BITS, 8, INT8, TQ>), grid, dim3(256), 0, s, p, L.wfmt);
+            hipLaunchKernelGGL((lut_gemv_split_kernel<BITS, 8, INT8, TQ, PRE>), grid, dim3(256), 0, s, p, L.wfmt);
         break;
     }
+}
+
+// weight words issued before the table wait: plan.pre (4 by default; 8 = all of them)
+template <int BITS, bool INT8, bool TQ>
+static void launch_split(const LutParams &p, const Layout &L, const LutPlan &plan, hipStream_t s) {
+    if (plan.pre == 0) launch_split_pre<BITS, INT8, TQ, 0>(p, L, plan, s);
+    else if (plan.pre == 4) launch_split_pre<BITS, INT8, TQ, 4>(p, L, plan, s);
+    else if (plan.pre >= 8) launch_split_pre<BITS, INT8, TQ, 8>(p, L, plan, s);
+    else launch_split_pre<BITS, INT8, TQ, 2>(p, L, plan, s);
 }
 
 // 16 wavefronts per workgroup, one 128-block per K slice and chunk; 4 or 8 when

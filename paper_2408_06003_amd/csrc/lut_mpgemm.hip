@@ -71,8 +71,8 @@ int launch_lut(const LutParams &p, const Layout &L, const LutPlan &plan, void *s
         if (e0 != 0) return e0;
     }
     hipError_t e = hipGetLastError();
-    // the split-K GEMV (kind 2) completes its K split itself
-    if (e != hipSuccess || plan.splits == 1 || plan.kind == 2) return (int)e;
+    // the split-K GEMV (kind 2) completes short K splits itself
+    if (e != hipSuccess || plan.splits == 1 || (plan.kind == 2 && plan.inkernel)) return (int)e;
     return launch_finalize(p, L, plan, stream);
 }
 

@@ -50,6 +50,9 @@ constexpr int TENT = 16;        // stored entries per triple table (14 used, 2 z
 // a nonzero value where a later call, of any problem, expects a zero counter.
 constexpr size_t CNT_AREA = 65536;
 constexpr int64_t CNT_MAX = (int64_t)(CNT_AREA / 4);
+// Largest K split the split-K GEMV completes inside the kernel (one batch of partial
+// loads by the last workgroup); longer splits are summed by the finalize kernel.
+constexpr int INKERNEL_MAX_SPLITS = 32;
 
 struct Layout {
     int64_t K, N, N_pad, KB, J, Q, G;  // G = group size (K when per-tensor)
@@ -117,6 +120,8 @@ struct LutPlan {
                      // 3: ternary 3-in-5 kernel (whole K, any M)
     int gemv_cfg;    // single-token kernel: lane decomposition (see lut_gemv.hip)
     int kbs;         // 128-blocks of K per split
+    int pre;         // split-K GEMV: weight words per lane requested before the tables are waited for
+    bool inkernel;   // split-K GEMV: the K split is completed in the kernel (else by the finalize kernel)
     int splits;      // K splits (1 = no workspace)
     int mt;          // tokens per workgroup (multi-token kernel)
     int64_t m_tiles; // token tiles
@@ -171,6 +176,7 @@ struct LutParams {
     const uint32_t *sgn;   // 3-in-5 sign words
     const void *meta;
     void *out;
+    unsigned long long *tl; // instrumented builds: per-wavefront phase stamps (see lut_common.h), else NULL
     float *part;           // split partial sums [splits][rows][N_pad] (float or int bits)
     uint32_t *cnt;         // split-K GEMV: arrival counters [M][n_tiles], zero between calls
     int64_t M, N, N_pad, K, KB, J, Q, G;
