@@ -65,7 +65,7 @@ __device__ __forceinline__ float h2f(uint32_t bits16) {
 template <bool INT8>
 __device__ __forceinline__ float act_value(uint32_t bits16, float scale) {
     const float a = h2f(bits16);
-    if (INT8) return fminf(fmaxf(rintf(a * scale), -127.f), 127.f);
+    if (INT8) return __builtin_amdgcn_fmed3f(rintf(a * scale), -127.f, 127.f);  // clamp to [-127, 127]
     return a * scale;  // exact: scale is a power of two
 }
 
@@ -143,7 +143,9 @@ __device__ __forceinline__ uint32_t idx4(uint32_t w) {
 template <bool INT8>
 struct Tab {
     static constexpr int E = INT8 ? 2 : 4;       // bytes per entry
-    static constexpr int G = 16 * E;             // bytes per group table
+    // bytes per group table: the INT16 tables (32 bytes) are padded to 48 so that one
+    // 16-byte store per lane of 16 consecutive groups covers 64 different LDS banks
+    static constexpr int G = INT8 ? 48 : 16 * E;
     static constexpr int BLK = (GPB + 1) * G;    // bytes per 128-block
 };
 

@@ -167,19 +167,22 @@ __global__ __launch_bounds__(64 * NW) void lut_fused_gemv_kernel(LutParams p, in
     if (lane == 63) wmax[wave] = amax;
     lds_barrier();
     tl_stamp(p, 1);
-    amax = wmax[0];
-#pragma unroll
-    for (int v = 1; v < NW; ++v) amax = fmaxf(amax, wmax[v]);
-    // the table scale now; the output factor t[m] (needed only by the epilogue) later
-    float scale;
-    int e2 = 0;
+    // the wavefront maxima, one per lane, reduced by DPP and broadcast from lane 63
+    amax = wave_max(lane < NW ? wmax[lane] : 0.f);
+    amax = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(amax), 63));
+    // the table scale and the output factor t[m] now (off the tail of the kernel)
+    float scale, tok;
     if (INT8) {
         scale = amax == 0.f ? 0.f : __fdiv_rn(127.0f, amax);
+        tok = amax == 0.f ? 0.f : __fdiv_rn(amax, 127.0f);
     } else if (amax == 0.f) {
         scale = 1.f;
+        tok = 1.f;
     } else {
+        int e2;
         (void)frexpf(amax, &e2);
         scale = ldexpf(1.f, -e2);
+        tok = ldexpf(1.f, e2);
     }
 
     float yf = 0.f;
@@ -254,11 +257,6 @@ __global__ __launch_bounds__(64 * NW) void lut_fused_gemv_kernel(LutParams p, in
         }
     }
     tl_stamp(p, 3);
-    float tok;
-    if (INT8)
-        tok = amax == 0.f ? 0.f : __fdiv_rn(amax, 127.0f);
-    else
-        tok = amax == 0.f ? 1.f : ldexpf(1.f, e2);
     ep.tok = tok;
     if (p.tok_out && blockIdx.x == 0 && split == 0 && tid == 0) p.tok_out[m] = tok;
     if (INT8 && need_s) {  // the activation sum of this workgroup's K range, per wavefront
