@@ -380,6 +380,41 @@ def cpu_baseline(inp, budget_s=10.0):
                       f"N={inp.N}, repeated {reps}x in {el:.1f} s; {per * 1e3:.2f} ms per step"}
 
 
+SINGLE_CORE_CODE = r"""
+import json, sys, time
+sys.path.insert(0, sys.argv[1])
+import oracle, workloads as W
+oracle.lib()
+out = []
+for cid, sid in ((1, 0), (2, 0), (3, 0), (3, 1), (3, 2), (3, 3)):
+    inp = W.make_inputs(cid, sid, M=1)
+    reps, t0 = 0, time.perf_counter()
+    while True:
+        oracle.reference_output(inp)
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= float(sys.argv[2]):
+            break
+    per = el / reps
+    out.append({"workload": f"{W.WORKLOADS[cid].name}/{inp.K}x{inp.N}", "value": round(2.0 * inp.M * inp.N * inp.K / per / 1e9, 3),
+                "unit": "GOPS", "seconds_per_call": round(per, 6), "calls": reps})
+print(json.dumps(out))
+"""
+
+
+def cpu_baseline_single_core(budget_s=2.0):
+    """The CPU oracle on ONE host core (OpenMP limited to one thread in a child process
+    that never touches the GPU) for the M = 1 workloads of configs 1-3, each repeated
+    for about ``budget_s`` seconds."""
+    import subprocess
+    env = dict(os.environ, OMP_NUM_THREADS="1")
+    r = subprocess.run([sys.executable, "-c", SINGLE_CORE_CODE, ROOT, str(budget_s)], env=env,
+                       capture_output=True, text=True, timeout=300)
+    if r.returncode != 0:
+        return {"error": r.stderr[-500:]}
+    return {"cores": 1, "kind": "oracle", "per_workload": json.loads(r.stdout.strip().splitlines()[-1])}
+
+
 def calibrate_copy():
     """A plain device copy of known size, for scaling rocprofv3 FETCH_SIZE / WRITE_SIZE."""
     import torch
@@ -782,6 +817,8 @@ def main():
     if not args.no_cpu:
         log("CPU oracle baseline")
         result["cpu_baseline"] = cpu_baseline(head_inp)
+        log("CPU oracle on one core, configs 1-3")
+        result["cpu_baseline_1core"] = cpu_baseline_single_core()
     result["paper_context"] = PAPER_CONTEXT
     print(json.dumps(result), flush=True)
 

@@ -93,7 +93,7 @@ def test_fused_fallback_paths():
     check_fused(gpi, what="INT8 M=6")
 
 
-@pytest.mark.parametrize("cid,sid", [(2, 0), (3, 0), (3, 1), (3, 3), (5, 0), (5, 1)])
+@pytest.mark.parametrize("cid,sid", [(1, 0), (2, 0), (3, 0), (3, 1), (3, 2), (3, 3), (5, 0), (5, 1)])
 def test_fused_full_size(cid, sid):
     inp = W.make_inputs(cid, sid, M=1)
     banner(f"fused full size config={cid} shape={sid} K={inp.K} N={inp.N}")

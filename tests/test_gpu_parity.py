@@ -118,7 +118,12 @@ def test_full_size_sampled(cid, sid, M, K, N):
                                              # several 1024-activation blocks per workgroup (large M),
                                              # group sums by lane butterflies and by whole workgroups
                                              (W.ACT_FP16, 300, 4096, 128), (W.ACT_FP16, 260, 8192, 2048),
-                                             (W.ACT_INT8, 300, 4096, 0)])
+                                             (W.ACT_INT8, 300, 4096, 0),
+                                             # the longest tokens staged in LDS (K = 32768) and the
+                                             # global-memory branch for longer ones
+                                             (W.ACT_FP16, 3, 32768, 128), (W.ACT_INT8, 3, 32768, 0),
+                                             (W.ACT_FP16, 3, 36864, 1024), (W.ACT_INT8, 3, 36864, 0),
+                                             (W.ACT_FP16, 4, 65536, 128), (W.ACT_INT8, 4, 65536, 0)])
 def test_precompute_matches_table_definition(act_kind, M, K, G):
     banner(f"precompute act={act_kind} M={M} K={K} G={G}")
     wfmt, bits = (W.WFMT_UINT, 2) if act_kind == W.ACT_FP16 else (W.WFMT_TERNARY, 2)
@@ -264,3 +269,43 @@ def test_split_k_gemv_two_tokens(kbs, tune):
     assert torch.equal(acc, base + y32), "accumulate through the finalize kernel"
     inpi = W.make_custom(W.WFMT_TERNARY, 2, 0, W.ACT_INT8, M=2, K=8192, N=777, seed=900 + kbs, scale_fp32=True)
     check_int_path(GpuProblem(inpi))
+
+
+# ----------------------------------------------------------------- long tokens (K > 32768)
+
+@pytest.mark.parametrize("wfmt,bits,G,act,K,N,M", [
+    (W.WFMT_UINT, 4, 128, W.ACT_FP16, 36864, 300, 1),
+    (W.WFMT_UINT, 2, 1024, W.ACT_FP16, 65536, 260, 2),
+    (W.WFMT_TERNARY, 2, 0, W.ACT_INT8, 36864, 300, 1),
+    (W.WFMT_BINARY, 1, 65536, W.ACT_INT8, 65536, 200, 1),
+    (W.WFMT_UINT, 2, 128, W.ACT_FP16, 36864, 300, 5),      # multi-token kernel
+    (W.WFMT_TERNARY, 2, 0, W.ACT_INT8, 65536, 130, 9),
+])
+def test_long_k_parity(wfmt, bits, G, act, K, N, M, tune):
+    """Tokens longer than the 32768 activations the precompute stages in LDS (its
+    global-memory branch), through the two-call path, the fused entry point and the
+    split-K GEMV (long K splits: finalize kernel), against the oracle, all outputs."""
+    banner(f"long K wfmt={wfmt} b={bits} G={G} act={act} K={K} N={N} M={M}")
+    inp = W.make_custom(wfmt, bits, G, act, M=M, K=K, N=N, seed=71, scale_fp32=(G == 0))
+    gp = GpuProblem(inp)
+    paths = [("two-call", gp.lut), ("fused", gp.fused)]
+    for name, run in paths:
+        if act == W.ACT_INT8:
+            acc_ref, y_ref = oracle.reference_output(inp)
+            assert np.array_equal(run(out_dtype=torch.int32).cpu().numpy().astype(np.int64), acc_ref), name
+            assert np.array_equal(run(out_dtype=torch.float32).cpu().numpy(), y_ref), name
+        else:
+            ref = oracle.reference_output(inp)
+            fro, mx = assert_fp_close(run(out_dtype=torch.float32).cpu().numpy(), ref, f"long K {name}")
+            print(f"[err] long K {name}: relFro {fro:.3e} max/rms {mx:.3e}", flush=True)
+    if M <= 2:  # the split-K GEMV on the same problem
+        tune(GEMV_KIND=2)
+        gs = GpuProblem(inp)
+        if act == W.ACT_INT8:
+            acc_ref, _ = oracle.reference_output(inp)
+            assert np.array_equal(gs.lut(out_dtype=torch.int32).cpu().numpy().astype(np.int64), acc_ref)
+        else:
+            assert_fp_close(gs.lut(out_dtype=torch.float32).cpu().numpy(), oracle.reference_output(inp),
+                            "long K split-K")
+            assert_fp_close(gs.fused(out_dtype=torch.float32).cpu().numpy(), oracle.reference_output(inp),
+                            "long K fused split-K")
