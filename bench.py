@@ -191,6 +191,8 @@ class Case:
         self.tables = torch.empty(L.table_size(self.p, M), dtype=torch.uint8, device=dev)
         ws = L.workspace_size(self.p, M)
         self.ws = torch.zeros(ws, dtype=torch.uint8, device=dev) if ws else None
+        dq = L.dequant_workspace_size(self.p, M)
+        self.dq_ws = torch.empty(dq, dtype=torch.uint8, device=dev) if dq else None
         self.int8 = inp.act_kind == W.ACT_INT8
         self.out_code = L.OUT_FP32 if self.int8 else L.OUT_FP16
         self.out = torch.empty((M, inp.N), dtype=torch.float32 if self.int8 else torch.float16, device=dev)
@@ -206,7 +208,7 @@ class Case:
 
     def dequant(self, i, out):
         self.L.mpgemm_dequant(self.p, self.M, self.act, self.packed[i % len(self.packed)], out,
-                              self.L.OUT_FP16, False)
+                              self.L.OUT_FP16, False, workspace=self.dq_ws)
 
     def step(self, i):
         self.precompute()
@@ -341,15 +343,14 @@ class Case:
             n = max(5, min(n_kernel, 50))
             ms_dq = self.timed(lambda i: self.dequant(i, out), n, check=lambda: out)
             tflops = self.effective_tops(ms_dq)
-            # the library takes the pipelined 256 x 256 kernel when its tiles alone fill the
-            # GPU; the 128 x 128 kernel of smaller grids is not tuned (no K split, no
-            # pipelining), so no LUT / dequantization ratio is quoted against it
-            big = (-(-self.N // 256)) * (-(-self.M // 256)) >= 256
+            kind, splits = self.L.dequant_plan(self.p, self.M)
+            name = {0: "dequant_mfma_kernel (128x128 tiles; not tuned)",
+                    1: "dequant_mfma_big_kernel (256x256 tiles, 8 wavefronts, pipelined)",
+                    2: "dequant_skinny_kernel (16-token slabs, 1-bit weights decoded in registers)"}[kind]
             rec.update({"dequant_mfma_us": round(ms_dq * 1e3, 3), "dequant_mfma_tops": round(tflops, 2),
                         "dequant_mfma_frac_of_fp16_peak": round(tflops / MFMA_FP16_PEAK_TFLOPS, 4),
-                        "dequant_kernel": ("dequant_mfma_big_kernel (256x256, pipelined)" if big else
-                                           "dequant_mfma_kernel (128x128, small grids, untuned: not a fair baseline)")})
-            if big:
+                        "dequant_kernel": name, "dequant_k_splits": splits})
+            if kind != 0:
                 rec["lut_over_dequant_time"] = round(ms_mp / ms_dq, 2)
         return rec
 

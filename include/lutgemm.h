@@ -292,10 +292,32 @@ lutgemm_status_t lutgemm_mpgemm_fused(const lutgemm_problem_t *problem, int64_t 
  * ACT_FP16_LUT8 problems (the activations are used as they are), not
  * TERNARY_3IN5 (LUTGEMM_ERROR_NOT_SUPPORTED); out_dtype FP16 or FP32; accumulate
  * as for lutgemm_mpgemm.
+ *   workspace  device, 16-byte aligned, workspace_bytes >=
+ *              lutgemm_dequant_workspace_size(problem, M); may be NULL when that is 0
+ * With a K split the partial sums are added in split order by a second kernel, so
+ * results are bitwise reproducible run to run.
  */
 lutgemm_status_t lutgemm_mpgemm_dequant(const lutgemm_problem_t *problem, int64_t M,
                                         const void *act, const void *packed, void *out,
-                                        int32_t out_dtype, int32_t accumulate, void *stream);
+                                        int32_t out_dtype, int32_t accumulate, void *workspace,
+                                        size_t workspace_bytes, void *stream);
+
+/*
+ * Bytes of scratch memory lutgemm_mpgemm_dequant needs for M tokens: FP32 partial
+ * sums [splits][M][N_pad] when its kernel splits K across workgroups (small grids),
+ * else 0 (also for problems the comparison path does not support).  Any contents
+ * on entry; not shared by calls that run concurrently.
+ */
+size_t lutgemm_dequant_workspace_size(const lutgemm_problem_t *problem, int64_t M);
+
+/*
+ * The launch plan lutgemm_mpgemm_dequant uses for M tokens (host only, launches
+ * nothing): *kernel = 0 for 128 x 128 tiles, 1 for the pipelined 256 x 256 tiles, 2
+ * for 16-token slabs (1-bit weights); *splits = K ranges (1: no split).  Errors as
+ * for lutgemm_mpgemm_dequant.
+ */
+lutgemm_status_t lutgemm_dequant_plan(const lutgemm_problem_t *problem, int64_t M, int32_t *kernel,
+                                      int32_t *splits);
 
 /*
  * Overrides of the launch planner, for tests and experiments only (normal use needs
@@ -323,12 +345,16 @@ enum {
     LUTGEMM_TUNE_MT_SPLITS = 8,     /* LUTGEMM_MT_SPLITS: K splits of the multi-token kernel
                                        (0: planned)                                                  */
     LUTGEMM_TUNE_MT_ORDER = 9,      /* LUTGEMM_MT_ORDER: multi-token workgroup order (-1: planned)    */
-    LUTGEMM_TUNE_DEQUANT_BIG = 10,  /* LUTGEMM_DEQUANT_BIG: 1 / 0 forces the 256x256 / 128x128
-                                       comparison kernel (-1: by grid size)                          */
+    LUTGEMM_TUNE_DEQUANT_KIND = 10, /* LUTGEMM_DEQUANT_KIND: comparison kernel, 0 128x128 tiles,
+                                       1 pipelined 256x256 tiles, 2 16-token slabs (1-bit weights
+                                       with one scale per column or tensor only; ignored for
+                                       others) (-1: planned)                                         */
     LUTGEMM_TUNE_LOG = 11,          /* LUTGEMM_LOG: 1 prints each launch plan to stderr (0)           */
     LUTGEMM_TUNE_SPLIT_PRE = 12,    /* LUTGEMM_SPLIT_PRE: weight words per lane the split-K kernel
                                        requests before its tables arrive, 0, 2, 4 or 8 = all (4)    */
-    LUTGEMM_TUNE_COUNT = 13
+    LUTGEMM_TUNE_DEQUANT_SPLITS = 13, /* LUTGEMM_DEQUANT_SPLITS: K splits of the comparison kernel
+                                       (0: planned)                                                  */
+    LUTGEMM_TUNE_COUNT = 14
 };
 
 /* Sets planner override `key` (LUTGEMM_TUNE_*) to `value` (-1: its default).

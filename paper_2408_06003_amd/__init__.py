@@ -7,7 +7,7 @@ package raises ``ImportError`` -- there is no CPU fallback.
 
 Low-level functions mirror the C entry points (``validate``, ``packed_weight_size``,
 ``table_size``, ``table_offsets``, ``workspace_size``, ``pack_weights``,
-``precompute``, ``mpgemm``, ``fused_workspace_size``, ``mpgemm_fused``, ``mpgemm_dequant``); ``LutGemm`` is a small holder that
+``precompute``, ``mpgemm``, ``fused_workspace_size``, ``mpgemm_fused``, ``dequant_workspace_size``, ``mpgemm_dequant``); ``LutGemm`` is a small holder that
 allocates the packed weights, tables and workspace with torch and calls them.
 """
 from __future__ import annotations
@@ -33,15 +33,16 @@ OUT_FP16, OUT_FP32, OUT_INT32 = 0, 1, 2
 EXPORTS = [
     "lutgemm_status_string", "lutgemm_version", "lutgemm_last_error", "lutgemm_validate", "lutgemm_packed_weight_size",
     "lutgemm_table_size", "lutgemm_table_offsets", "lutgemm_workspace_size", "lutgemm_pack_weights",
-    "lutgemm_precompute", "lutgemm_mpgemm", "lutgemm_mpgemm_dequant", "lutgemm_calibrate_stream_read",
+    "lutgemm_precompute", "lutgemm_mpgemm", "lutgemm_mpgemm_dequant", "lutgemm_dequant_workspace_size", "lutgemm_dequant_plan",
+    "lutgemm_calibrate_stream_read",
     "lutgemm_fused_workspace_size", "lutgemm_mpgemm_fused", "lutgemm_calibrate_stream_read_ex",
     "lutgemm_set_tuning", "lutgemm_get_tuning", "lutgemm_mpgemm_noalloc",
 ]
 
 # planner overrides (LUTGEMM_TUNE_*), for tests and experiments
 TUNE = {"TARGET_BLOCKS": 0, "WHOLEK_MAX_KB": 1, "GEMV_KIND": 2, "GEMV_CFG": 3, "SPLITS": 4, "KBS": 5,
-        "MT16": 6, "MT_TARGET": 7, "MT_SPLITS": 8, "MT_ORDER": 9, "DEQUANT_BIG": 10, "LOG": 11,
-        "SPLIT_PRE": 12}
+        "MT16": 6, "MT_TARGET": 7, "MT_SPLITS": 8, "MT_ORDER": 9, "DEQUANT_KIND": 10, "LOG": 11,
+        "SPLIT_PRE": 12, "DEQUANT_SPLITS": 13}
 
 
 class Problem(ctypes.Structure):
@@ -94,7 +95,11 @@ def _load(path: str = LIB_PATH):
     L.lutgemm_mpgemm.restype = ctypes.c_int
     L.lutgemm_mpgemm.argtypes = [PP, I64, P, P, P, I32, I32, P, SZ, P]
     L.lutgemm_mpgemm_dequant.restype = ctypes.c_int
-    L.lutgemm_mpgemm_dequant.argtypes = [PP, I64, P, P, P, I32, I32, P]
+    L.lutgemm_mpgemm_dequant.argtypes = [PP, I64, P, P, P, I32, I32, P, SZ, P]
+    L.lutgemm_dequant_workspace_size.restype = ctypes.c_size_t
+    L.lutgemm_dequant_workspace_size.argtypes = [PP, I64]
+    L.lutgemm_dequant_plan.restype = ctypes.c_int
+    L.lutgemm_dequant_plan.argtypes = [PP, I64, ctypes.POINTER(I32), ctypes.POINTER(I32)]
     L.lutgemm_fused_workspace_size.restype = SZ
     L.lutgemm_fused_workspace_size.argtypes = [PP, I64]
     L.lutgemm_mpgemm_fused.restype = ctypes.c_int
@@ -214,10 +219,25 @@ def mpgemm_fused(p: Problem, M: int, act, packed, out, out_dtype: int, accumulat
            "lutgemm_mpgemm_fused")
 
 
+def dequant_workspace_size(p: Problem, M: int) -> int:
+    return lib.lutgemm_dequant_workspace_size(ctypes.byref(p), M)
+
+
+def dequant_plan(p: Problem, M: int):
+    """(kernel, splits) of the comparison path for M tokens: kernel 0 = 128x128 tiles,
+    1 = pipelined 256x256 tiles, 2 = 16-token slabs."""
+    k, s = ctypes.c_int32(), ctypes.c_int32()
+    _check(lib.lutgemm_dequant_plan(ctypes.byref(p), M, ctypes.byref(k), ctypes.byref(s)), "lutgemm_dequant_plan")
+    return k.value, s.value
+
+
 def mpgemm_dequant(p: Problem, M: int, act, packed, out, out_dtype: int, accumulate: bool = False,
-                   stream=None):
+                   workspace=None, stream=None, workspace_bytes=None):
+    if workspace_bytes is None:
+        workspace_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     _check(lib.lutgemm_mpgemm_dequant(ctypes.byref(p), M, _ptr(act), _ptr(packed), _ptr(out), out_dtype,
-                                      1 if accumulate else 0, _stream(stream)), "lutgemm_mpgemm_dequant")
+                                      1 if accumulate else 0, _ptr(workspace), workspace_bytes,
+                                      _stream(stream)), "lutgemm_mpgemm_dequant")
 
 
 def calibrate_stream_read(src, nbytes: int, sink, blocks: int, stream=None):
@@ -318,5 +338,15 @@ class LutGemm:
         if out is None:
             out = torch.empty((M, self.p.N), dtype=out_dtype or torch.float16, device=self.device)
         mpgemm_dequant(self.p, M, act, self.packed, out, self.out_dtype_code(out.dtype), accumulate,
-                       stream=stream)
+                       workspace=self.dequant_workspace(M), stream=stream)
         return out
+
+    def dequant_workspace(self, M: int):
+        import torch
+        n = dequant_workspace_size(self.p, M)
+        if n == 0:
+            return None
+        key = ("dequant", M)
+        if key not in self._ws:
+            self._ws[key] = torch.empty(n, dtype=torch.uint8, device=self.device)
+        return self._ws[key]

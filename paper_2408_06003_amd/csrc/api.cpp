@@ -72,9 +72,9 @@ lutgemm_status_t check_problem(const lutgemm_problem_t *p, int64_t M) {
 const char *const kTuneEnv[LUTGEMM_TUNE_COUNT] = {
     "LUTGEMM_TARGET_BLOCKS", "LUTGEMM_WHOLEK_MAX_KB", "LUTGEMM_GEMV_KIND", "LUTGEMM_GEMV_CFG",
     "LUTGEMM_SPLITS",        "LUTGEMM_KBS",           "LUTGEMM_MT16",      "LUTGEMM_MT_TARGET",
-    "LUTGEMM_MT_SPLITS",     "LUTGEMM_MT_ORDER",      "LUTGEMM_DEQUANT_BIG", "LUTGEMM_LOG",
-    "LUTGEMM_SPLIT_PRE"};
-const int kTuneDefault[LUTGEMM_TUNE_COUNT] = {256, 10000, -1, -1, 0, 0, 1, 8, 0, -1, -1, 0, 4};
+    "LUTGEMM_MT_SPLITS",     "LUTGEMM_MT_ORDER",      "LUTGEMM_DEQUANT_KIND", "LUTGEMM_LOG",
+    "LUTGEMM_SPLIT_PRE",     "LUTGEMM_DEQUANT_SPLITS"};
+const int kTuneDefault[LUTGEMM_TUNE_COUNT] = {256, 10000, -1, -1, 0, 0, 1, 8, 0, -1, -1, 0, 4, 0};
 std::atomic<int> g_tune[LUTGEMM_TUNE_COUNT];
 
 bool tune_value_ok(int key, int value) {
@@ -539,9 +539,29 @@ lutgemm_status_t lutgemm_mpgemm_fused(const lutgemm_problem_t *problem, int64_t 
     return hip_status(e);
 }
 
+size_t lutgemm_dequant_workspace_size(const lutgemm_problem_t *problem, int64_t M) {
+    if (check_problem(problem, M) != LUTGEMM_SUCCESS) return 0;
+    if (problem->act == LUTGEMM_ACT_INT8 || problem->wfmt == LUTGEMM_WFMT_TERNARY_3IN5) return 0;
+    return plan_dequant(make_layout(*problem), M).ws_bytes;
+}
+
+lutgemm_status_t lutgemm_dequant_plan(const lutgemm_problem_t *problem, int64_t M, int32_t *kernel,
+                                      int32_t *splits) {
+    lutgemm_status_t st = check_problem(problem, M);
+    if (st != LUTGEMM_SUCCESS) return st;
+    if (problem->act == LUTGEMM_ACT_INT8 || problem->wfmt == LUTGEMM_WFMT_TERNARY_3IN5)
+        return LUTGEMM_ERROR_NOT_SUPPORTED;
+    if (!kernel || !splits) return LUTGEMM_ERROR_INVALID_VALUE;
+    const DequantPlan plan = plan_dequant(make_layout(*problem), M);
+    *kernel = plan.kind;
+    *splits = plan.splits;
+    return LUTGEMM_SUCCESS;
+}
+
 lutgemm_status_t lutgemm_mpgemm_dequant(const lutgemm_problem_t *problem, int64_t M, const void *act,
                                         const void *packed, void *out, int32_t out_dtype,
-                                        int32_t accumulate, void *stream) {
+                                        int32_t accumulate, void *workspace, size_t workspace_bytes,
+                                        void *stream) {
     lutgemm_status_t st = check_problem(problem, M);
     if (st != LUTGEMM_SUCCESS) return st;
     if (problem->act == LUTGEMM_ACT_INT8 || problem->wfmt == LUTGEMM_WFMT_TERNARY_3IN5)
@@ -565,7 +585,18 @@ lutgemm_status_t lutgemm_mpgemm_dequant(const lutgemm_problem_t *problem, int64_
     dp.G = L.G;
     dp.out_dtype = out_dtype;
     dp.accumulate = accumulate;
-    return hip_status(launch_dequant(dp, L, stream));
+    const DequantPlan plan = plan_dequant(L, M);
+    if (plan.ws_bytes) {
+        if (!workspace || !aligned16(workspace)) return LUTGEMM_ERROR_INVALID_VALUE;
+        if (workspace_bytes < plan.ws_bytes) return LUTGEMM_ERROR_INSUFFICIENT_SIZE;
+        dp.part = (float *)workspace;
+    }
+    dp.splits = plan.splits;
+    dp.kbs = plan.kbs;
+    if (tuning(LUTGEMM_TUNE_LOG) > 0)
+        std::fprintf(stderr, "lutgemm_mpgemm_dequant: M=%lld K=%lld N=%lld kind=%d splits=%d kbs=%d ws=%zu\n",
+                (long long)M, (long long)L.K, (long long)L.N, plan.kind, plan.splits, plan.kbs, plan.ws_bytes);
+    return hip_status(launch_dequant(dp, L, plan, stream));
 }
 
 }  // extern "C"

@@ -17,6 +17,12 @@
 namespace lutgemm {
 
 typedef _Float16 half8_t __attribute__((ext_vector_type(8)));
+
+// Keeps an index in a VGPR, so that the load it addresses stays a vector load.
+__device__ __forceinline__ int64_t lane_value_dq(int64_t x) {
+    asm volatile("" : "+v"(x));
+    return x;
+}
 typedef float floatx16_t __attribute__((ext_vector_type(16)));
 
 constexpr int DBM = 128, DBN = 128, DBK = 128;
@@ -24,6 +30,26 @@ constexpr int LDS_STRIDE = DBK + 8;  // halves per LDS row (padding against bank
 
 __device__ __forceinline__ float dq_h2f(uint32_t bits16) {
     return __half2float(__ushort_as_half((unsigned short)bits16));
+}
+
+// Result y of output (row, col): with a K split the FP32 partial of this workgroup's
+// split (blockIdx.z), summed later by dequant_reduce_kernel; else the output itself
+// (optional accumulate, dtype conversion).  Rows and columns past the problem are
+// skipped.
+__device__ __forceinline__ void dq_store(const DequantParams &p, int64_t row, int64_t col, float y) {
+    if (row >= p.M || col >= p.N) return;
+    if (p.part) {
+        p.part[((int64_t)blockIdx.z * p.M + row) * p.N_pad + col] = y;
+        return;
+    }
+    const int64_t o = row * p.N + col;
+    if (p.out_dtype == LUTGEMM_OUT_FP32) {
+        if (p.accumulate) y += ((const float *)p.out)[o];
+        ((float *)p.out)[o] = y;
+    } else {
+        if (p.accumulate) y += __half2float(((const __half *)p.out)[o]);
+        ((__half *)p.out)[o] = __float2half_rn(y);
+    }
 }
 
 template <int BITS>
@@ -49,7 +75,9 @@ __global__ __launch_bounds__(256) void dequant_mfma_kernel(DequantParams p, int 
     const int h = tid >> 7;
     const int64_t n = n0 + c;
 
-    for (int64_t kb = 0; kb < p.KB; ++kb) {
+    const int64_t kbA = (int64_t)blockIdx.z * p.kbs;
+    const int64_t kbB = kbA + p.kbs < p.KB ? kbA + p.kbs : p.KB;
+    for (int64_t kb = kbA; kb < kbB; ++kb) {
         // ---- A tile: 128 rows x 128 halves, 16-byte chunks
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
@@ -140,40 +168,34 @@ __global__ __launch_bounds__(256) void dequant_mfma_kernel(DequantParams p, int 
 #pragma unroll
         for (int j = 0; j < 2; ++j) {
             const int64_t col = n0 + wn + 32 * j + (lane & 31);
-            if (col >= p.N) continue;
 #pragma unroll
             for (int v = 0; v < 16; ++v) {
                 const int64_t row = m0 + wm + 32 * i + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
-                if (row >= p.M) continue;
-                const int64_t o = row * p.N + col;
-                float y = acc[i][j][v];
-                if (p.out_dtype == LUTGEMM_OUT_FP32) {
-                    if (p.accumulate) y += ((const float *)p.out)[o];
-                    ((float *)p.out)[o] = y;
-                } else {
-                    if (p.accumulate) y += __half2float(((const __half *)p.out)[o]);
-                    ((__half *)p.out)[o] = __float2half_rn(y);
-                }
+                dq_store(p, row, col, acc[i][j][v]);
             }
         }
 }
 
 // ---------------------------------------------------------------- large M
 //
-// Workgroup tile 256 (M) x 256 (N), K step 64; 4 wavefronts, each owning a
-// 128 x 128 sub-tile as 4 x 4 MFMA 32x32 blocks (256 FP32 accumulators per lane,
-// one wavefront per SIMD).  LDS holds two K steps of activations and dequantized
-// weights (2 x 68 KiB): while the matrix cores work on one, the next step's
-// activations stream straight into the other buffer (global_load_lds_dwordx4, no
-// registers) and the next step's packed weights are dequantized into it, so each
-// K step costs one barrier.  Activation rows are 128 bytes with their 16-byte
-// chunks XOR-swizzled by the row (chunk c of row r at slot c ^ (r & 7)), which
-// keeps both the lane-contiguous direct loads and the 128-bit MFMA operand reads
-// free of bank conflicts.  Each thread dequantizes one column's 64 weights of a
-// step: the Eq. 6 inversion is undone on whole 32-bit words, the 4 weights of a
-// 4-bit index are spread into the 4 bytes of a register (one multiply), the planes
-// are combined there, and each byte is converted (v_cvt_f32_ubyte) and scaled as
-// r = s q - s z in FP32 (exact) before rounding to FP16.
+// Workgroup tile 256 (M) x 256 (N), K step 64, 8 wavefronts: two per SIMD, so that
+// one can dequantize or wait while the other drives the matrix cores.  Wavefront w
+// owns the 128 x 64 sub-tile at rows 128 (w / 4), columns 64 (w % 4) as 4 x 2 MFMA
+// 32x32 blocks (128 FP32 accumulators per lane).  LDS holds two K steps of
+// activations (2 x 32 KiB) and of dequantized weights (2 x 36 KiB): while the matrix
+// cores work on one, the next step's activations stream straight into the other
+// buffer (global_load_lds_dwordx4, no registers) and the next step's packed weights
+// are dequantized into it, so each K step costs one barrier.  Activation rows are
+// 128 bytes with their 16-byte chunks XOR-swizzled (chunk c of row r at slot
+// c ^ ((r / 2) % 8)): the lane-contiguous direct loads and the 128-bit operand reads
+// of 16 consecutive rows then touch distinct banks.  Dequantized-weight rows (one
+// per column) are padded to 144 bytes, which spreads 16 consecutive columns over all
+// banks.  Each thread dequantizes 32 weights of one column per step: the Eq. 6
+// inversion is undone on whole 32-bit words, the 4 weights of a 4-bit index are
+// spread into the 4 bytes of a register (one multiply), the planes are combined
+// there, and each byte is converted (v_cvt_f32_ubyte) and scaled as r = s q - s z in
+// FP32 (exact) before rounding to FP16.  The packed words are loaded two K steps
+// ahead.
 constexpr int QBM = 256, QBN = 256, QBK = 64;
 constexpr int QST = QBK + 8;  // halves per dequantized-weight LDS row (16-byte padding)
 
@@ -193,12 +215,29 @@ __device__ __forceinline__ float ubyte_f(uint32_t v, int b) {
     return (float)((v >> (8 * b)) & 0xFFu);
 }
 
+// r = A q + B for a b-bit index q, with A = 2 s', B = s' (-(2^b - 1) - z') (Eq. 2):
+// s q - s z for UINT, s (2 q - 1) for BINARY, s (q - 1) for TERNARY codes.
+template <int BITS>
+__device__ __forceinline__ float2 dq_affine(int wfmt, float s, float z) {
+    float sp, zp;
+    if (wfmt == LUTGEMM_WFMT_BINARY) {
+        sp = s;
+        zp = 0.f;
+    } else if (wfmt == LUTGEMM_WFMT_TERNARY) {
+        sp = 0.5f * s;
+        zp = -1.f;
+    } else {
+        sp = 0.5f * s;
+        zp = 2.f * z + 1.f - (float)(1 << BITS);
+    }
+    return make_float2(2.f * sp, sp * (-(float)((1 << BITS) - 1) - zp));
+}
+
 typedef __attribute__((address_space(3))) void lds_void;
 typedef const __attribute__((address_space(1))) void glb_void;
 
-template <int BITS>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
-void dequant_mfma_big_kernel(DequantParams p, int wfmt, int per_tensor) {
+template <int BITS, bool PT>
+__global__ __launch_bounds__(512) void dequant_mfma_big_kernel(DequantParams p, int wfmt) {
     // two buffers per operand as distinct objects, so the compiler can tell the
     // direct loads into one from the reads of the other
     __shared__ __attribute__((aligned(16))) _Float16 As0[QBM * QBK], As1[QBM * QBK];
@@ -207,118 +246,104 @@ void dequant_mfma_big_kernel(DequantParams p, int wfmt, int per_tensor) {
     const int lane = tid & 63, wave = tid >> 6;
     const int64_t m0 = (int64_t)blockIdx.y * QBM;
     const int64_t n0 = (int64_t)blockIdx.x * QBN;
-    const int wm = (wave >> 1) * 128, wn = (wave & 1) * 128;
-    const int64_t n = n0 + tid;  // column this thread dequantizes (< N_pad)
-    const int nk = (int)(p.K / QBK);
+    const int wm = (wave >> 2) * 128, wn = (wave & 3) * 64;
+    const int col = tid & (QBN - 1), hf = tid >> 8;  // dequantized column, which 32 k of a step
+    const int64_t n = n0 + col;
+    // K steps of this workgroup's split: two per 128-block
+    const int64_t kb0 = (int64_t)blockIdx.z * p.kbs;
+    const int nkb = (int)(p.KB - kb0 < p.kbs ? p.KB - kb0 : p.kbs);
+    const int nk = 2 * nkb;
+    const int64_t k00 = kb0 * KBLK;
 
-    floatx16_t acc[4][4];
+    floatx16_t acc[4][2];
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
+        for (int j = 0; j < 2; ++j)
 #pragma unroll
             for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
-    // Activations of step ks into buffer `buf`: 8 direct loads per wavefront, each
-    // writing 1 KiB of LDS (8 rows); lane L of load i fills slot L % 8 of row
-    // 64 wave + 8 i + L / 8 with the chunk that belongs there under the swizzle.
+    float2 ab_pt = make_float2(0.f, 0.f);  // per-tensor scale and zero: FP32 s, z
+    if constexpr (PT) ab_pt = dq_affine<BITS>(wfmt, ((const float *)p.meta)[0], ((const float *)p.meta)[1]);
+
+    // Activations of step ks into dst: 4 direct loads per wavefront, each writing
+    // 1 KiB of LDS (8 rows); lane L of load i fills slot L % 8 of row
+    // 32 wave + 8 i + L / 8 with the chunk that belongs there under the swizzle.
     auto load_act = [&](int ks, _Float16 *dst) {
-        const int64_t k0 = (int64_t)ks * QBK;
+        const int64_t k0 = k00 + (int64_t)ks * QBK;
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            const int row = 64 * wave + 8 * i + (lane >> 3), slot = lane & 7;
-            const int c = slot ^ (row & 7);
+        for (int i = 0; i < 4; ++i) {
+            const int row = 32 * wave + 8 * i + (lane >> 3), slot = lane & 7;
+            const int c = slot ^ ((row >> 1) & 7);
             const int64_t r = (m0 + row < p.M) ? m0 + row : p.M - 1;  // rows past M: clamped, never stored
             __builtin_amdgcn_global_load_lds((glb_void *)(p.act + r * p.K + k0 + 8 * c),
-                                             (lds_void *)(dst + (64 * wave + 8 * i) * QBK), 16, 0, 0);
+                                             (lds_void *)(dst + (32 * wave + 8 * i) * QBK), 16, 0, 0);
         }
     };
-    // packed weights of a step: the 64 indices of each plane (two 32-bit words) and
-    // the column's metadata word(s); two register sets, loaded two steps ahead
+    // packed weights of step ks for this thread: 32 indices of each plane (one 32-bit
+    // word, the thread's half of the step) and the group's metadata word
     struct WReg {
-        uint2 br[BITS];
-        uint2 mr;
+        uint32_t b[BITS];
+        uint32_t m;
     };
     auto load_w = [&](int ks, WReg &w) {
-        const int64_t k0 = (int64_t)ks * QBK;
+        const int64_t k0 = k00 + (int64_t)ks * QBK;
         const int64_t kb = k0 / KBLK;
-        const int hw = (int)((k0 % KBLK) / QBK);  // which half of the 128-k plane word
+        const int dw = 2 * (ks & 1) + hf;  // word of the 128-k plane word (k00 is a multiple of 128)
 #pragma unroll
-        for (int t = 0; t < BITS; ++t) w.br[t] = ((const uint2 *)(p.planes + (kb * BITS + t) * p.N_pad + n))[hw];
-        // branch-free (a load under a condition makes the compiler wait for every
-        // load in flight, the direct activation loads included)
-        const int64_t idx = per_tensor ? 0 : (k0 / p.G) * p.N_pad + n;
-        const uint32_t *mw = (const uint32_t *)p.meta;
-        w.mr = make_uint2(mw[idx], mw[idx + per_tensor]);
+        for (int t = 0; t < BITS; ++t) w.b[t] = ((const uint32_t *)(p.planes + (kb * BITS + t) * p.N_pad + n))[dw];
+        if constexpr (!PT) w.m = ((const uint32_t *)p.meta)[(int64_t)((uint32_t)k0 / (uint32_t)p.G) * p.N_pad + n];
+        else w.m = 0u;
     };
-    // r = A q + B with A = 2 s', B = s' (-(2^b - 1) - z') (Eq. 2): s q - s z for UINT
-    auto affine = [&](const WReg &w) {
-        float s, z;
-        if (per_tensor) {
-            s = __uint_as_float(w.mr.x);
-            z = __uint_as_float(w.mr.y);
-        } else {
-            s = dq_h2f(w.mr.x & 0xFFFFu);
-            z = dq_h2f(w.mr.x >> 16);
-        }
-        float sp, zp;
-        if (wfmt == LUTGEMM_WFMT_BINARY) {
-            sp = s;
-            zp = 0.f;
-        } else if (wfmt == LUTGEMM_WFMT_TERNARY) {
-            sp = 0.5f * s;
-            zp = -1.f;
-        } else {
-            sp = 0.5f * s;
-            zp = 2.f * z + 1.f - (float)(1 << BITS);
-        }
-        return make_float2(2.f * sp, sp * (-(float)((1 << BITS) - 1) - zp));
-    };
-    // weights it*8 .. it*8 + 7 of the column (it in [0, 8)): one 16-byte LDS store
-    auto dequant8 = [&](const WReg &w, float2 ab, _Float16 *dst, int it) {
-        const int d = it >> 2, jj = 2 * (it & 3);
+    // weights 32 hf .. 32 hf + 31 of the step for column col: four 16-byte LDS stores
+    auto dequant = [&](const WReg &w, _Float16 *dst) {
+        float2 ab;
+        if constexpr (PT) ab = ab_pt;
+        else ab = dq_affine<BITS>(wfmt, dq_h2f(w.m & 0xFFFFu), dq_h2f(w.m >> 16));
         uint32_t raw[BITS];
 #pragma unroll
-        for (int t = 0; t < BITS; ++t) raw[t] = undo_eq6(d ? w.br[t].y : w.br[t].x);
-        uint32_t packed[4];
+        for (int t = 0; t < BITS; ++t) raw[t] = undo_eq6(w.b[t]);
 #pragma unroll
-        for (int u = 0; u < 2; ++u) {
-            uint32_t qb = 0;  // byte e: bit e of each plane's index, i.e. weight 3 - e
+        for (int it = 0; it < 4; ++it) {
+            uint32_t packed[4];
 #pragma unroll
-            for (int t = 0; t < BITS; ++t) qb |= spread_nibble(raw[t], jj + u) << t;
-            const float r3 = fmaf(ab.x, ubyte_f(qb, 0), ab.y), r2 = fmaf(ab.x, ubyte_f(qb, 1), ab.y);
-            const float r1 = fmaf(ab.x, ubyte_f(qb, 2), ab.y), r0 = fmaf(ab.x, ubyte_f(qb, 3), ab.y);
-            packed[2 * u] = (uint32_t)__half_as_ushort(__float2half_rn(r0)) |
-                            ((uint32_t)__half_as_ushort(__float2half_rn(r1)) << 16);
-            packed[2 * u + 1] = (uint32_t)__half_as_ushort(__float2half_rn(r2)) |
-                                ((uint32_t)__half_as_ushort(__float2half_rn(r3)) << 16);
+            for (int u = 0; u < 2; ++u) {
+                uint32_t qb = 0;  // byte e: bit e of each plane's index, i.e. weight 3 - e
+#pragma unroll
+                for (int t = 0; t < BITS; ++t) qb |= spread_nibble(raw[t], 2 * it + u) << t;
+                const float r3 = fmaf(ab.x, ubyte_f(qb, 0), ab.y), r2 = fmaf(ab.x, ubyte_f(qb, 1), ab.y);
+                const float r1 = fmaf(ab.x, ubyte_f(qb, 2), ab.y), r0 = fmaf(ab.x, ubyte_f(qb, 3), ab.y);
+                packed[2 * u] = (uint32_t)__half_as_ushort(__float2half_rn(r0)) |
+                                ((uint32_t)__half_as_ushort(__float2half_rn(r1)) << 16);
+                packed[2 * u + 1] = (uint32_t)__half_as_ushort(__float2half_rn(r2)) |
+                                    ((uint32_t)__half_as_ushort(__float2half_rn(r3)) << 16);
+            }
+            *(uint4 *)(dst + col * QST + 32 * hf + 8 * it) = make_uint4(packed[0], packed[1], packed[2], packed[3]);
         }
-        *(uint4 *)(dst + tid * QST + 32 * d + 4 * jj) = make_uint4(packed[0], packed[1], packed[2], packed[3]);
     };
 
     // one K step: MFMAs on (as, bs) while the next step's activations stream into
     // as_n; then the next step's weights (wn_, requested one step earlier) are
     // dequantized into bs_n; the weights two steps ahead are requested into wl_
+    // (the index clamped to the last step: the load is unconditional)
     auto step = [&](int ks, const _Float16 *as, const _Float16 *bs, _Float16 *as_n, _Float16 *bs_n,
                     const WReg &wn_, WReg &wl_) {
         const bool more = ks + 1 < nk;
         if (more) load_act(ks + 1, as_n);
-        if (ks + 2 < nk) load_w(ks + 2, wl_);
-        const float2 ab = affine(wn_);
+        load_w(ks + 2 < nk ? ks + 2 : nk - 1, wl_);
         // operand fragments double-buffered across the four 16-deep sub-steps
-        half8_t a[2][4], b[2][4];
+        half8_t a[2][4], b[2][2];
         auto read_frags = [&](int kk, int f) {
             const int c = 2 * kk + (lane >> 5);  // 16-byte chunk of the K step this lane supplies
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 const int row = wm + 32 * i + (lane & 31);
-                a[f][i] = *(const half8_t *)(as + row * QBK + 8 * (c ^ (row & 7)));
+                a[f][i] = *(const half8_t *)(as + row * QBK + 8 * (c ^ ((row >> 1) & 7)));
             }
 #pragma unroll
-            for (int j = 0; j < 4; ++j) b[f][j] = *(const half8_t *)(bs + (wn + 32 * j + (lane & 31)) * QST + 8 * c);
+            for (int j = 0; j < 2; ++j) b[f][j] = *(const half8_t *)(bs + (wn + 32 * j + (lane & 31)) * QST + 8 * c);
         };
         read_frags(0, 0);
-        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int kk = 0; kk < QBK / 16; ++kk) {
             const int f = kk & 1;
@@ -326,39 +351,22 @@ void dequant_mfma_big_kernel(DequantParams p, int wfmt, int per_tensor) {
 #pragma unroll
             for (int i = 0; i < 4; ++i)
 #pragma unroll
-                for (int j = 0; j < 4; ++j)
+                for (int j = 0; j < 2; ++j)
                     acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a[f][i], b[f][j], acc[i][j], 0, 0, 0);
-            // issue order: the next sub-step's 8 LDS reads between the first 8 MFMAs
-            if (kk + 1 < QBK / 16) {
-#pragma unroll
-                for (int t = 0; t < 8; ++t) {
-                    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
-                    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read
-                }
-                __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
-            }
-            __builtin_amdgcn_sched_barrier(0);
         }
-        if (more) {
-#pragma unroll
-            for (int it = 0; it < 8; ++it) dequant8(wn_, ab, bs_n, it);
-            __builtin_amdgcn_s_waitcnt(0);  // this wavefront's direct LDS loads have landed
-        }
+        if (more) dequant(wn_, bs_n);
+        __builtin_amdgcn_s_waitcnt(0);  // this wavefront's loads (direct LDS ones included) have landed
         __syncthreads();
     };
 
     WReg wA, wB;
     load_act(0, As0);
     load_w(0, wA);
-    if (nk > 1) load_w(1, wB);
-    {
-        const float2 ab = affine(wA);
-#pragma unroll
-        for (int it = 0; it < 8; ++it) dequant8(wA, ab, Bs0, it);
-    }
+    load_w(1, wB);  // nk >= 2
+    dequant(wA, Bs0);
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
-    for (int ks = 0; ks < nk; ks += 2) {  // nk is even (K is a multiple of 128)
+    for (int ks = 0; ks < nk; ks += 2) {           // nk is even
         step(ks, As0, Bs0, As1, Bs1, wB, wA);      // dequantizes step ks + 1 from wB, loads ks + 2 into wA
         step(ks + 1, As1, Bs1, As0, Bs0, wA, wB);  // dequantizes step ks + 2 from wA, loads ks + 3 into wB
     }
@@ -367,50 +375,252 @@ void dequant_mfma_big_kernel(DequantParams p, int wfmt, int per_tensor) {
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int64_t col = n0 + wn + 32 * j + (lane & 31);
-            if (col >= p.N) continue;
+        for (int j = 0; j < 2; ++j) {
+            const int64_t c = n0 + wn + 32 * j + (lane & 31);
 #pragma unroll
             for (int v = 0; v < 16; ++v) {
                 const int64_t row = m0 + wm + 32 * i + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
-                if (row >= p.M) continue;
-                const int64_t o = row * p.N + col;
-                float y = acc[i][j][v];
-                if (p.out_dtype == LUTGEMM_OUT_FP32) {
-                    if (p.accumulate) y += ((const float *)p.out)[o];
-                    ((float *)p.out)[o] = y;
-                } else {
-                    if (p.accumulate) y += __half2float(((const __half *)p.out)[o]);
-                    ((__half *)p.out)[o] = __float2half_rn(y);
-                }
+                dq_store(p, row, c, acc[i][j][v]);
             }
         }
 }
 
-int launch_dequant(const DequantParams &p, const Layout &L, void *stream) {
+// ---------------------------------------------------------------- few tokens
+//
+// 1-bit weights (BINARY, one scale per column or per tensor) and up to 16 tokens per
+// workgroup: v_mfma_f32_16x16x32_f16 on 16-token slabs.  A workgroup owns 256
+// columns (64 per wavefront, four 16-column MFMA blocks) and kbs 128-blocks of K.
+//
+// The order of k inside an MFMA is free as long as both operands follow it, so it is
+// chosen to make the weight decode cheap.  Lane (r, g) = (lane % 16, lane / 16) of a
+// 16-column block takes the 32-bit word g (weights 32 g .. 32 g + 31 of the 128-block)
+// of column r and undoes the Eq. 6 inversion on the whole word (a set bit marks a +1).
+// Shifted left by h (0 .. 15), the word holds its bits 15 - h and 31 - h at the sign
+// positions of an FP16 pair, so one shift and one three-input bit operation (the
+// inverted sign bits over 0x3C003C00) give two FP16 weights +-1; MFMA step st uses
+// h = 4 st .. 4 st + 3.
+// Bit b of a word is weight 4 (b / 4) + 3 - b % 4 (the first weight of a 4-group in
+// its bit 3), so pair h = 4 st + t holds weights 4 (3 - st) + t (low half) and
+// 4 (7 - st) + t (high half).  The activations are staged in LDS in exactly that
+// order, in chunks of at most 16 128-blocks (64 KiB); 16-byte slot j of a block's
+// 256 bytes in row r is stored at slot j ^ r, so the operand reads of the 16 rows
+// hit distinct banks.  The packed words are requested
+// nontemporally eight 128-blocks ahead (a ring of registers); the column scale
+// multiplies the FP32 result.  At a few tokens the decode, not the matrix cores, is
+// the work: no decoded weight is reused beyond the slab's 16 tokens.
+constexpr int SK_CHUNK = 16;  // 128-blocks of activations staged in LDS at once
+constexpr int SK_RING = 8;    // 128-blocks of weight words in flight per lane
+typedef float floatx4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+
+inline size_t skinny_lds_bytes(int kbs) {
+    const int ch = kbs < SK_CHUNK ? kbs : SK_CHUNK;
+    return (size_t)16 * ch * KBLK * 2;
+}
+
+// undo_eq6 with the multiply by 7 done on 16-bit halves (full rate; each half of
+// (w >> 3) & 0x11111111 times 7 stays below 2^16).
+__device__ __forceinline__ uint32_t undo_eq6_pk(uint32_t w) {
+    typedef unsigned short u16x2_t __attribute__((ext_vector_type(2)));
+    const u16x2_t t = __builtin_bit_cast(u16x2_t, (w >> 3) & 0x11111111u);
+    return w ^ __builtin_bit_cast(uint32_t, t * (u16x2_t){7, 7});
+}
+
+// A workgroup barrier that orders LDS only (global loads in flight stay in flight).
+__device__ __forceinline__ void dq_lds_barrier() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+__global__ __launch_bounds__(256) void dequant_skinny_kernel(DequantParams p, int per_tensor) {
+    extern __shared__ __attribute__((aligned(16))) _Float16 As[];  // [16][row_h] halves
+    const int ch = p.kbs < SK_CHUNK ? p.kbs : SK_CHUNK;
+    const int row_h = ch * KBLK;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int r = lane & 15, g = lane >> 4;
+    const int64_t ncol0 = (int64_t)blockIdx.x * NTILE + wave * 64;
+    const int64_t kb0 = (int64_t)blockIdx.z * p.kbs;
+    const int nkb = (int)(p.KB - kb0 < p.kbs ? p.KB - kb0 : p.kbs);
+    const int64_t m0 = (int64_t)blockIdx.y * 16;
+
+    // word g of column ncol0 + 16 cb + r in 128-block kbl of the range (clamped to the
+    // last block: loads past the range repeat it and are never used)
+    uint32_t w[SK_RING][4];
+    const uint32_t *wbase = (const uint32_t *)(p.planes + kb0 * p.N_pad + ncol0 + r) + g;
+    auto load_w = [&](int kbl, uint32_t(&d)[4]) {
+        const int64_t kb = kbl < nkb ? kbl : nkb - 1;
+#pragma unroll
+        for (int cb = 0; cb < 4; ++cb) d[cb] = __builtin_nontemporal_load(wbase + (kb * p.N_pad + 16 * cb) * 4);
+    };
+#pragma unroll
+    for (int u = 0; u < SK_RING; ++u) load_w(u, w[u]);
+
+    floatx4_t acc[4];
+#pragma unroll
+    for (int cb = 0; cb < 4; ++cb) acc[cb] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+
+    // the MFMAs of 128-block kb_l (LDS column blk) with the weight words d
+    auto block = [&](int blk, const uint32_t(&d)[4]) {
+        const _Float16 *arow = As + r * row_h + blk * KBLK;
+        uint32_t y[4];
+#pragma unroll
+        for (int cb = 0; cb < 4; ++cb) y[cb] = undo_eq6_pk(d[cb]);
+#pragma unroll
+        for (int st = 0; st < 4; ++st) {
+            const half8_t a = *(const half8_t *)(arow + 8 * ((4 * g + st) ^ r));
+#pragma unroll
+            for (int cb = 0; cb < 4; ++cb) {
+                u32x4_t bw;
+#pragma unroll
+                for (int t = 0; t < 4; ++t) bw[t] = (~(y[cb] << (4 * st + t)) & 0x80008000u) | 0x3C003C00u;
+                acc[cb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, __builtin_bit_cast(half8_t, bw), acc[cb], 0, 0, 0);
+            }
+        }
+    };
+
+    for (int c0 = 0; c0 < nkb; c0 += ch) {
+        const int nc = nkb - c0 < ch ? nkb - c0 : ch;
+        if (c0) dq_lds_barrier();  // every wavefront is done with the previous chunk
+        // stage: one 16-byte operand chunk (row, block, word g2, step st) per item, the 4
+        // activations of the low half (from 4 (3 - st)) and of the high half (from
+        // 4 (7 - st)) of word g2 interleaved; rows past M are zero
+        const int items = 16 * nc * 16;
+        for (int i = tid; i < items; i += 256) {
+            const int row = i / (nc * 16), rest = i % (nc * 16);
+            const int blk = rest >> 4, g2 = (rest >> 2) & 3, st = rest & 3;
+            const int64_t mr = m0 + row < p.M ? m0 + row : p.M - 1;
+            const uint16_t *src = p.act + mr * p.K + (kb0 + c0 + blk) * KBLK + 32 * g2;
+            uint2 lo = *(const uint2 *)(src + 4 * (3 - st));
+            uint2 hi = *(const uint2 *)(src + 4 * (7 - st));
+            if (m0 + row >= p.M) lo = hi = make_uint2(0u, 0u);
+            const uint4 v = make_uint4(__builtin_amdgcn_perm(hi.x, lo.x, 0x05040100u),
+                                       __builtin_amdgcn_perm(hi.x, lo.x, 0x07060302u),
+                                       __builtin_amdgcn_perm(hi.y, lo.y, 0x05040100u),
+                                       __builtin_amdgcn_perm(hi.y, lo.y, 0x07060302u));
+            *(uint4 *)(As + row * row_h + blk * KBLK + 8 * ((4 * g2 + st) ^ row)) = v;
+        }
+        dq_lds_barrier();
+
+        // whole groups of SK_RING blocks: no condition in the body, so the waits for the
+        // ring's loads stay exact
+        int kk = 0;
+        for (; kk + SK_RING <= nc; kk += SK_RING) {
+#pragma unroll
+            for (int u = 0; u < SK_RING; ++u) {
+                block(kk + u, w[u]);
+                load_w(c0 + kk + u + SK_RING, w[u]);
+                // keep the blocks in order (hoisting every decode to the top of the group
+                // would wait for all of the ring's loads at once)
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        }
+        // the rest of the last chunk (its words are already in the ring)
+#pragma unroll
+        for (int u = 0; u < SK_RING; ++u)
+            if (kk + u < nc) block(kk + u, w[u]);
+    }
+
+    // epilogue: acc[cb][j] is token 4 (lane / 16) + j, column 16 cb + lane % 16
+#pragma unroll
+    for (int cb = 0; cb < 4; ++cb) {
+        const int64_t col = ncol0 + 16 * cb + r;
+        const float sc = per_tensor ? ((const float *)p.meta)[lane_value_dq(0)]
+                                    : dq_h2f(((const uint32_t *)p.meta)[lane_value_dq(col)] & 0xFFFFu);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) dq_store(p, m0 + 4 * g + j, col, acc[cb][j] * sc);
+    }
+}
+
+// Sums the K-split partials of output (m, n) in split order, then the output
+// epilogue (accumulate, dtype).  One lane per column, 256 per workgroup.
+__global__ __launch_bounds__(256) void dequant_reduce_kernel(DequantParams p) {
+    const int64_t n = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    const int64_t m = blockIdx.y;
+    if (n >= p.N) return;
+    float y = 0.f;
+    for (int s = 0; s < p.splits; ++s) y += p.part[((int64_t)s * p.M + m) * p.N_pad + n];
+    const int64_t o = m * p.N + n;
+    if (p.out_dtype == LUTGEMM_OUT_FP32) {
+        if (p.accumulate) y += ((const float *)p.out)[o];
+        ((float *)p.out)[o] = y;
+    } else {
+        if (p.accumulate) y += __half2float(((const __half *)p.out)[o]);
+        ((__half *)p.out)[o] = __float2half_rn(y);
+    }
+}
+
+// Kernel and K split of the comparison path.  1-bit weights with one scale per column
+// (or tensor) and at most 64 tokens: the 16-token-slab kernel, K split until the grid
+// has about 2 x 256 workgroups (at least 4 blocks per split).  Otherwise the pipelined
+// 256 x 256 kernel when M >= 128 and it has at least 32 tiles, K split into as many
+// ranges as keep the grid within one workgroup per CU (256; a second, partial round
+// costs more than the split saves); else 128 x 128 tiles, K split until the grid has
+// about 256 workgroups.  A split costs FP32 partial sums of splits x M x N_pad
+// and the reduce launch.  LUTGEMM_TUNE_DEQUANT_KIND and LUTGEMM_TUNE_DEQUANT_SPLITS
+// force the kernel and the split count (clamped to the 128-blocks of K).
+DequantPlan plan_dequant(const Layout &L, int64_t M) {
+    DequantPlan P{};
+    const int force = tuning(LUTGEMM_TUNE_DEQUANT_KIND);
+    const int force_splits = tuning(LUTGEMM_TUNE_DEQUANT_SPLITS);
+    const int64_t tiles256 = (L.N_pad / QBN) * ((M + QBM - 1) / QBM);
+    // splits = ceil(target / base), or floor (at least 1) when one round of workgroups
+    // must not spill over the target (one workgroup per CU)
+    auto split_for = [&](int64_t base, int64_t target, int64_t min_kbs, bool floor_div = false) {
+        int64_t splits = base >= target ? 1 : floor_div ? target / base : (target + base - 1) / base;
+        const int64_t max_splits = L.KB / min_kbs > 1 ? L.KB / min_kbs : 1;
+        if (splits > max_splits) splits = max_splits;
+        if (force_splits > 0) splits = force_splits < L.KB ? force_splits : L.KB;
+        const int64_t kbs = (L.KB + splits - 1) / splits;
+        P.kbs = (int)kbs;
+        P.splits = (int)((L.KB + kbs - 1) / kbs);
+    };
+    const bool slab_ok = L.wfmt == LUTGEMM_WFMT_BINARY && (L.per_tensor || L.Q == 1);
+    if (slab_ok && (force == 2 || (force < 0 && M <= 64))) {
+        P.kind = 2;
+        split_for((L.N_pad / NTILE) * ((M + 15) / 16), 512, 4);
+    } else if (force == 1 || (force < 0 && M >= 128 && tiles256 * 8 >= 256)) {
+        P.kind = 1;
+        split_for(tiles256, 256, 1, true);
+    } else {
+        P.kind = 0;
+        split_for((L.N_pad / DBN) * ((M + DBM - 1) / DBM), 256, 1);
+    }
+    P.ws_bytes = P.splits > 1 ? align256((size_t)P.splits * M * L.N_pad * 4) : 0;
+    return P;
+}
+
+int launch_dequant(const DequantParams &p, const Layout &L, const DequantPlan &plan, void *stream) {
     hipStream_t s = (hipStream_t)stream;
     const int pt = L.per_tensor ? 1 : 0;
-    // 256 x 256 tiles when they alone fill the GPU (one workgroup per CU); the
-    // LUTGEMM_TUNE_DEQUANT_BIG override forces one kernel (tests, experiments)
-    const dim3 big((unsigned)(L.N_pad / QBN), (unsigned)((p.M + QBM - 1) / QBM));
-    const int force = tuning(LUTGEMM_TUNE_DEQUANT_BIG);
-    const bool use_big = force >= 0 ? force != 0 : (int64_t)big.x * big.y >= 256;
-    if (use_big) {
+    const unsigned sp = (unsigned)plan.splits;
+    if (plan.kind == 2) {
+        const dim3 grid((unsigned)(L.N_pad / NTILE), (unsigned)((p.M + 15) / 16), sp);
+        hipLaunchKernelGGL(dequant_skinny_kernel, grid, dim3(256), skinny_lds_bytes(plan.kbs), s, p, pt);
+    } else if (plan.kind == 1) {
+        const dim3 big((unsigned)(L.N_pad / QBN), (unsigned)((p.M + QBM - 1) / QBM), sp);
+        const dim3 blk(512);
+        if (pt) {
+            if (L.bits == 1) hipLaunchKernelGGL((dequant_mfma_big_kernel<1, true>), big, blk, 0, s, p, L.wfmt);
+            else if (L.bits == 2) hipLaunchKernelGGL((dequant_mfma_big_kernel<2, true>), big, blk, 0, s, p, L.wfmt);
+            else hipLaunchKernelGGL((dequant_mfma_big_kernel<4, true>), big, blk, 0, s, p, L.wfmt);
+        } else {
+            if (L.bits == 1) hipLaunchKernelGGL((dequant_mfma_big_kernel<1, false>), big, blk, 0, s, p, L.wfmt);
+            else if (L.bits == 2) hipLaunchKernelGGL((dequant_mfma_big_kernel<2, false>), big, blk, 0, s, p, L.wfmt);
+            else hipLaunchKernelGGL((dequant_mfma_big_kernel<4, false>), big, blk, 0, s, p, L.wfmt);
+        }
+    } else {
+        const dim3 grid((unsigned)(L.N_pad / DBN), (unsigned)((p.M + DBM - 1) / DBM), sp);
         if (L.bits == 1)
-            hipLaunchKernelGGL(dequant_mfma_big_kernel<1>, big, dim3(256), 0, s, p, L.wfmt, pt);
+            hipLaunchKernelGGL(dequant_mfma_kernel<1>, grid, dim3(256), 0, s, p, L.wfmt, pt);
         else if (L.bits == 2)
-            hipLaunchKernelGGL(dequant_mfma_big_kernel<2>, big, dim3(256), 0, s, p, L.wfmt, pt);
+            hipLaunchKernelGGL(dequant_mfma_kernel<2>, grid, dim3(256), 0, s, p, L.wfmt, pt);
         else
-            hipLaunchKernelGGL(dequant_mfma_big_kernel<4>, big, dim3(256), 0, s, p, L.wfmt, pt);
-        return (int)hipGetLastError();
+            hipLaunchKernelGGL(dequant_mfma_kernel<4>, grid, dim3(256), 0, s, p, L.wfmt, pt);
     }
-    dim3 grid((unsigned)(L.N_pad / DBN), (unsigned)((p.M + DBM - 1) / DBM));
-    if (L.bits == 1)
-        hipLaunchKernelGGL(dequant_mfma_kernel<1>, grid, dim3(256), 0, s, p, L.wfmt, pt);
-    else if (L.bits == 2)
-        hipLaunchKernelGGL(dequant_mfma_kernel<2>, grid, dim3(256), 0, s, p, L.wfmt, pt);
-    else
-        hipLaunchKernelGGL(dequant_mfma_kernel<4>, grid, dim3(256), 0, s, p, L.wfmt, pt);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || plan.splits == 1) return (int)e;
+    hipLaunchKernelGGL(dequant_reduce_kernel, dim3((unsigned)(L.N_pad / 256), (unsigned)p.M), dim3(256), 0, s, p);
     return (int)hipGetLastError();
 }
 

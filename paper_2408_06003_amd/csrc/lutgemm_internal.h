@@ -193,9 +193,19 @@ struct DequantParams {
     const uint4 *planes;
     const void *meta;
     void *out;
+    float *part;           // K split: FP32 partial sums [splits][M][N_pad], else NULL
     int64_t M, N, N_pad, K, KB, Q, G;
     int out_dtype, accumulate;
+    int splits, kbs;       // K splits and 128-blocks per split
 };
+
+// Launch plan of the comparison path: which kernel, and its K split.
+struct DequantPlan {
+    int kind;        // 0: 128 x 128 tiles, 1: pipelined 256 x 256 tiles, 2: 16-token slabs (binary weights)
+    int splits, kbs;
+    size_t ws_bytes; // FP32 partial sums when splits > 1
+};
+DequantPlan plan_dequant(const Layout &L, int64_t M);
 
 // Launchers (return hipError_t as int).
 int launch_pack(const PackParams &p, void *stream);
@@ -207,6 +217,6 @@ int launch_fused_split(const LutParams &p, const Layout &L, const LutPlan &plan,
 int launch_finalize(const LutParams &p, const Layout &L, const LutPlan &plan, void *stream);
 int launch_mtok(const LutParams &p, const Layout &L, const LutPlan &plan, void *stream);
 int launch_tri(const LutParams &p, const Layout &L, bool fused, void *stream);
-int launch_dequant(const DequantParams &p, const Layout &L, void *stream);
+int launch_dequant(const DequantParams &p, const Layout &L, const DequantPlan &plan, void *stream);
 
 }  // namespace lutgemm

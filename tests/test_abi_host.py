@@ -152,7 +152,7 @@ def test_entry_points_reject_before_launch():
     # misaligned pointers
     assert f.lutgemm_pack_weights(bp, ok + 4, ok, ok, ok, big, None) == L.ERROR_INVALID_VALUE
     assert f.lutgemm_precompute(bp, 1, ok, ok + 8, big, None) == L.ERROR_INVALID_VALUE
-    assert f.lutgemm_mpgemm_dequant(bp, 1, ok + 2, ok, ok, L.OUT_FP16, 0, None) == L.ERROR_INVALID_VALUE
+    assert f.lutgemm_mpgemm_dequant(bp, 1, ok + 2, ok, ok, L.OUT_FP16, 0, None, 0, None) == L.ERROR_INVALID_VALUE
     # too-small buffers
     assert f.lutgemm_pack_weights(bp, ok, ok, ok, ok, 16, None) == L.ERROR_INSUFFICIENT_SIZE
     assert f.lutgemm_precompute(bp, 1, ok, ok, 16, None) == L.ERROR_INSUFFICIENT_SIZE
@@ -160,15 +160,31 @@ def test_entry_points_reject_before_launch():
     assert f.lutgemm_mpgemm(bp, 1, ok, ok, ok, 9, 0, ok, big, None) == L.ERROR_INVALID_VALUE
     assert f.lutgemm_mpgemm(bp, 1, ok, ok, ok, L.OUT_INT32, 0, ok, big, None) == L.ERROR_NOT_SUPPORTED
     assert f.lutgemm_mpgemm(bp, 1, ok, ok, ok, L.OUT_FP16, 2, ok, big, None) == L.ERROR_INVALID_VALUE
-    assert f.lutgemm_mpgemm_dequant(bp, 1, ok, ok, ok, L.OUT_INT32, 0, None) == L.ERROR_INVALID_VALUE
+    assert f.lutgemm_mpgemm_dequant(bp, 1, ok, ok, ok, L.OUT_INT32, 0, None, 0, None) == L.ERROR_INVALID_VALUE
     pi = L.problem(1024, 256, 2, L.WFMT_TERNARY, 0, L.ACT_INT8, True)
-    assert f.lutgemm_mpgemm_dequant(ctypes.byref(pi), 1, ok, ok, ok, L.OUT_FP16, 0, None) == L.ERROR_NOT_SUPPORTED
+    assert f.lutgemm_mpgemm_dequant(ctypes.byref(pi), 1, ok, ok, ok, L.OUT_FP16, 0, None, 0, None) == L.ERROR_NOT_SUPPORTED
     # workspace required but missing / too small
     pw = L.problem(8192, 1024, 2, L.WFMT_TERNARY, 0, L.ACT_INT8, True)  # too few columns: K is split
     need = L.workspace_size(pw, 1)
     assert need > 0
     assert f.lutgemm_mpgemm(ctypes.byref(pw), 1, ok, ok, ok, L.OUT_INT32, 0, None, need, None) == L.ERROR_INVALID_VALUE
     assert f.lutgemm_mpgemm(ctypes.byref(pw), 1, ok, ok, ok, L.OUT_INT32, 0, ok, need - 1, None) == L.ERROR_INSUFFICIENT_SIZE
+    # comparison path: a few tokens on few columns split K (FP32 partials per split)
+    pd = L.problem(8192, 1024, 1, L.WFMT_BINARY, 0)
+    need = L.dequant_workspace_size(pd, 16)
+    assert need > 0 and need % (16 * 1024 * 4) == 0
+    assert f.lutgemm_mpgemm_dequant(ctypes.byref(pd), 16, ok, ok, ok, L.OUT_FP16, 0, None, need, None) == L.ERROR_INVALID_VALUE
+    assert f.lutgemm_mpgemm_dequant(ctypes.byref(pd), 16, ok, ok, ok, L.OUT_FP16, 0, ok, need - 1, None) == L.ERROR_INSUFFICIENT_SIZE
+    # large M on a wide layer: whole K per workgroup, no scratch; unsupported problems report 0
+    assert L.dequant_workspace_size(L.problem(4096, 16384, 2, L.WFMT_UINT, 128), 4096) == 0
+    assert L.dequant_workspace_size(pi, 16) == 0
+    # launch plans: 16-token slabs for few tokens of 1-bit weights, 256 x 256 tiles at
+    # large M (K split only while the grid stays within one round of 256 workgroups)
+    assert L.dequant_plan(pd, 16)[0] == 2
+    assert L.dequant_plan(L.problem(4096, 4096, 2, L.WFMT_UINT, 128), 4096) == (1, 1)
+    assert L.dequant_plan(L.problem(8192, 28672, 1, L.WFMT_BINARY, 8192), 256) == (1, 2)
+    assert L.dequant_plan(L.problem(28672, 8192, 1, L.WFMT_BINARY, 28672), 256) == (1, 8)
+    assert f.lutgemm_dequant_plan(ctypes.byref(pi), 16, None, None) == L.ERROR_NOT_SUPPORTED
 
 
 def test_fused_entry_point_rejects_before_launch():

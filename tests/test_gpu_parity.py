@@ -243,7 +243,7 @@ def test_extreme_scales():
 def test_dequant_big_tile_parity(cid, M, K, N, tune):
     """The 256 x 256 pipelined dequantization + MFMA kernel (chosen for large M) on
     small shapes with ragged M and N tails, every output against the oracle."""
-    tune(DEQUANT_BIG=1)
+    tune(DEQUANT_KIND=1)
     banner(f"dequant 256x256 tile config={cid} M={M} K={K} N={N}")
     gp = GpuProblem(W.make_inputs(cid, 0, M=M, K=K, N=N))
     check_fp_path(gp, dequant=True, what=f"dequant big config {cid}")

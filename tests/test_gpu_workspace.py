@@ -122,8 +122,11 @@ def test_guard_bands_dequant_and_noalloc():
     inp = W.make_inputs(5, 0, M=16, N=1000)
     p, packed, act = setup(inp)
     out = Guarded(16 * 1000 * 2)
-    L.mpgemm_dequant(p, 16, act, packed.ptr, out.ptr, L.OUT_FP16, False)
+    ws = Guarded(L.dequant_workspace_size(p, 16))  # K split: FP32 partials
+    assert ws.n > 0
+    L.mpgemm_dequant(p, 16, act, packed.ptr, out.ptr, L.OUT_FP16, False, workspace=ws.ptr, workspace_bytes=ws.n)
     out.check("dequant output")
+    ws.check("dequant workspace")
     inp = W.make_inputs(3, 1, M=1, N=1000)
     p, packed, act = setup(inp)
     tables = Guarded(L.table_size(p, 1))
