@@ -194,8 +194,10 @@ __global__ __launch_bounds__(256) void dequant_mfma_kernel(DequantParams p, int 
 // inversion is undone on whole 32-bit words, the 4 weights of a 4-bit index are
 // spread into the 4 bytes of a register (one multiply), the planes are combined
 // there, and each byte is converted (v_cvt_f32_ubyte) and scaled as r = s q - s z in
-// FP32 (exact) before rounding to FP16.  The packed words are loaded two K steps
-// ahead.
+// FP32 (exact) before rounding to FP16, a quarter of it between the MFMAs of each
+// 16-deep sub-step.  The packed words are loaded two K steps ahead.  Tiles are
+// assigned so that each XCD works on a contiguous band of them (shared activation
+// rows stay in that XCD's L2).
 constexpr int QBM = 256, QBN = 256, QBK = 64;
 constexpr int QST = QBK + 8;  // halves per dequantized-weight LDS row (16-byte padding)
 
@@ -244,8 +246,14 @@ __global__ __launch_bounds__(512) void dequant_mfma_big_kernel(DequantParams p, 
     __shared__ __attribute__((aligned(16))) _Float16 Bs0[QBN * QST], Bs1[QBN * QST];
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
-    const int64_t m0 = (int64_t)blockIdx.y * QBM;
-    const int64_t n0 = (int64_t)blockIdx.x * QBN;
+    // Tile of this workgroup.  Workgroups are dealt to the 8 XCDs round robin; when the
+    // tile count allows, XCD x gets tiles x T/8 .. (x + 1) T/8 - 1 in row-major order,
+    // so the workgroups sharing an XCD's L2 also share activation rows.
+    const uint32_t nx = gridDim.x, tiles = gridDim.x * gridDim.y;
+    uint32_t t = blockIdx.x + nx * blockIdx.y;
+    if (tiles % 8 == 0) t = (t % 8) * (tiles / 8) + t / 8;
+    const int64_t m0 = (int64_t)(t / nx) * QBM;
+    const int64_t n0 = (int64_t)(t % nx) * QBN;
     const int wm = (wave >> 2) * 128, wn = (wave & 3) * 64;
     const int col = tid & (QBN - 1), hf = tid >> 8;  // dequantized column, which 32 k of a step
     const int64_t n = n0 + col;
@@ -295,42 +303,48 @@ __global__ __launch_bounds__(512) void dequant_mfma_big_kernel(DequantParams p, 
         if constexpr (!PT) w.m = ((const uint32_t *)p.meta)[(int64_t)((uint32_t)k0 / (uint32_t)p.G) * p.N_pad + n];
         else w.m = 0u;
     };
-    // weights 32 hf .. 32 hf + 31 of the step for column col: four 16-byte LDS stores
-    auto dequant = [&](const WReg &w, _Float16 *dst) {
+    // weights 32 hf .. 32 hf + 31 of the step for column col, in four parts of 8 (one
+    // 16-byte LDS store each): the affine coefficients and the Eq. 6-undone words first
+    struct DqPrep {
         float2 ab;
-        if constexpr (PT) ab = ab_pt;
-        else ab = dq_affine<BITS>(wfmt, dq_h2f(w.m & 0xFFFFu), dq_h2f(w.m >> 16));
         uint32_t raw[BITS];
+    };
+    auto dq_prep = [&](const WReg &w) {
+        DqPrep d;
+        if constexpr (PT) d.ab = ab_pt;
+        else d.ab = dq_affine<BITS>(wfmt, dq_h2f(w.m & 0xFFFFu), dq_h2f(w.m >> 16));
 #pragma unroll
-        for (int t = 0; t < BITS; ++t) raw[t] = undo_eq6(w.b[t]);
+        for (int t = 0; t < BITS; ++t) d.raw[t] = undo_eq6(w.b[t]);
+        return d;
+    };
+    auto dq_part = [&](const DqPrep &d, int it, _Float16 *dst) {
+        uint32_t packed[4];
 #pragma unroll
-        for (int it = 0; it < 4; ++it) {
-            uint32_t packed[4];
+        for (int u = 0; u < 2; ++u) {
+            uint32_t qb = 0;  // byte e: bit e of each plane's index, i.e. weight 3 - e
 #pragma unroll
-            for (int u = 0; u < 2; ++u) {
-                uint32_t qb = 0;  // byte e: bit e of each plane's index, i.e. weight 3 - e
-#pragma unroll
-                for (int t = 0; t < BITS; ++t) qb |= spread_nibble(raw[t], 2 * it + u) << t;
-                const float r3 = fmaf(ab.x, ubyte_f(qb, 0), ab.y), r2 = fmaf(ab.x, ubyte_f(qb, 1), ab.y);
-                const float r1 = fmaf(ab.x, ubyte_f(qb, 2), ab.y), r0 = fmaf(ab.x, ubyte_f(qb, 3), ab.y);
-                packed[2 * u] = (uint32_t)__half_as_ushort(__float2half_rn(r0)) |
-                                ((uint32_t)__half_as_ushort(__float2half_rn(r1)) << 16);
-                packed[2 * u + 1] = (uint32_t)__half_as_ushort(__float2half_rn(r2)) |
-                                    ((uint32_t)__half_as_ushort(__float2half_rn(r3)) << 16);
-            }
-            *(uint4 *)(dst + col * QST + 32 * hf + 8 * it) = make_uint4(packed[0], packed[1], packed[2], packed[3]);
+            for (int t = 0; t < BITS; ++t) qb |= spread_nibble(d.raw[t], 2 * it + u) << t;
+            const float r3 = fmaf(d.ab.x, ubyte_f(qb, 0), d.ab.y), r2 = fmaf(d.ab.x, ubyte_f(qb, 1), d.ab.y);
+            const float r1 = fmaf(d.ab.x, ubyte_f(qb, 2), d.ab.y), r0 = fmaf(d.ab.x, ubyte_f(qb, 3), d.ab.y);
+            packed[2 * u] = (uint32_t)__half_as_ushort(__float2half_rn(r0)) |
+                            ((uint32_t)__half_as_ushort(__float2half_rn(r1)) << 16);
+            packed[2 * u + 1] = (uint32_t)__half_as_ushort(__float2half_rn(r2)) |
+                                ((uint32_t)__half_as_ushort(__float2half_rn(r3)) << 16);
         }
+        *(uint4 *)(dst + col * QST + 32 * hf + 8 * it) = make_uint4(packed[0], packed[1], packed[2], packed[3]);
     };
 
-    // one K step: MFMAs on (as, bs) while the next step's activations stream into
-    // as_n; then the next step's weights (wn_, requested one step earlier) are
-    // dequantized into bs_n; the weights two steps ahead are requested into wl_
-    // (the index clamped to the last step: the load is unconditional)
+    // One K step: MFMAs on (as, bs) while the next step's activations stream into
+    // as_n and the next step's weights (wn_, requested one step earlier) are
+    // dequantized into bs_n, a quarter per 16-deep sub-step, interleaved with the
+    // MFMAs; the weights two steps ahead are requested into wl_.  Indices past the
+    // last step are clamped to it, so every load and store is unconditional (the
+    // buffers they fill at the last step are never read).
     auto step = [&](int ks, const _Float16 *as, const _Float16 *bs, _Float16 *as_n, _Float16 *bs_n,
                     const WReg &wn_, WReg &wl_) {
-        const bool more = ks + 1 < nk;
-        if (more) load_act(ks + 1, as_n);
+        load_act(ks + 1 < nk ? ks + 1 : nk - 1, as_n);
         load_w(ks + 2 < nk ? ks + 2 : nk - 1, wl_);
+        const DqPrep dq = dq_prep(wn_);
         // operand fragments double-buffered across the four 16-deep sub-steps
         half8_t a[2][4], b[2][2];
         auto read_frags = [&](int kk, int f) {
@@ -344,6 +358,7 @@ __global__ __launch_bounds__(512) void dequant_mfma_big_kernel(DequantParams p, 
             for (int j = 0; j < 2; ++j) b[f][j] = *(const half8_t *)(bs + (wn + 32 * j + (lane & 31)) * QST + 8 * c);
         };
         read_frags(0, 0);
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int kk = 0; kk < QBK / 16; ++kk) {
             const int f = kk & 1;
@@ -353,8 +368,29 @@ __global__ __launch_bounds__(512) void dequant_mfma_big_kernel(DequantParams p, 
 #pragma unroll
                 for (int j = 0; j < 2; ++j)
                     acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a[f][i], b[f][j], acc[i][j], 0, 0, 0);
+            dq_part(dq, kk, bs_n);
+            // issue order: MFMAs spaced by the next sub-step's LDS reads and a share of
+            // the dequantization arithmetic
+            if (kk + 1 < QBK / 16) {
+#pragma unroll
+                for (int t = 0; t < 6; ++t) {
+                    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
+                    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read
+                    __builtin_amdgcn_sched_group_barrier(0x002, 5, 0);  // VALU
+                }
+                __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+                __builtin_amdgcn_sched_group_barrier(0x002, 20, 0);
+                __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);  // the LDS store
+            } else {
+#pragma unroll
+                for (int t = 0; t < 8; ++t) {
+                    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                    __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);
+                }
+                __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);
+            }
+            __builtin_amdgcn_sched_barrier(0);
         }
-        if (more) dequant(wn_, bs_n);
         __builtin_amdgcn_s_waitcnt(0);  // this wavefront's loads (direct LDS ones included) have landed
         __syncthreads();
     };
@@ -363,7 +399,11 @@ __global__ __launch_bounds__(512) void dequant_mfma_big_kernel(DequantParams p, 
     load_act(0, As0);
     load_w(0, wA);
     load_w(1, wB);  // nk >= 2
-    dequant(wA, Bs0);
+    {
+        const DqPrep dq = dq_prep(wA);
+#pragma unroll
+        for (int it = 0; it < 4; ++it) dq_part(dq, it, Bs0);
+    }
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     for (int ks = 0; ks < nk; ks += 2) {           // nk is even
