@@ -44,8 +44,9 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "pmc_traffic.txt")
 # sources that define each timed kernel and its launch (a PMC traffic record is used
 # only while they hash as when the counters were taken)
 KERNEL_SOURCES = {
-    "mpgemm": ("lut_gemv.hip", "lut_common.h", "lutgemm_internal.h", "api.cpp"),
-    "fused": ("lut_fused.hip", "lut_common.h", "lutgemm_internal.h", "api.cpp"),
+    "mpgemm": ("lut_gemv.hip", "lut_mtok.hip", "lut_mpgemm.hip", "lut_common.h", "lutgemm_internal.h", "api.cpp"),
+    "fused": ("lut_fused.hip", "lut_mpgemm.hip", "lut_common.h", "lutgemm_internal.h", "api.cpp"),
+    "dequant": ("dequant_mfma.hip", "lutgemm_internal.h", "api.cpp"),
 }
 
 
@@ -65,8 +66,9 @@ def parse():
                     help="also run a plain 256 MiB device copy (counter calibration)")
     ap.add_argument("--summarize-trace", metavar="DIR", default=None,
                     help="print the summary of a rocprofv3 --kernel-trace --stats output directory (no GPU)")
-    ap.add_argument("--summarize-traffic", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"), default=None,
-                    help="print HBM traffic records from two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE; no GPU)")
+    ap.add_argument("--summarize-traffic", nargs="+", metavar="DIR", default=None,
+                    help="print HBM traffic records from rocprofv3 --pmc runs in directories named "
+                         "fetch_<workload> / write_<workload> (FETCH_SIZE, WRITE_SIZE; no GPU)")
     ap.add_argument("--summarize-counters", metavar="DIR", nargs="+", default=None,
                     help="print per-kernel utilization from rocprofv3 --pmc runs (no GPU)")
     ap.add_argument("--timeline", metavar="WORKLOAD", default=None,
@@ -335,7 +337,11 @@ class Case:
                "precompute_us": round(ms_pre * 1e3, 3),
                "precompute_over_mpgemm": round(ms_pre / ms_mp, 4),
                "fused_us": round(ms_fu * 1e3, 3), "fused_tops": round(self.effective_tops(ms_fu), 3),
-               "algorithmic_bytes": b["total"], "rotation_copies": len(self.packed)}
+               "algorithmic_bytes": b["total"], "rotation_copies": len(self.packed),
+               # HBM bytes per call from rocprofv3 FETCH_SIZE + WRITE_SIZE (null without a record
+               # taken on the current kernel sources)
+               "mpgemm_hbm_traffic_bytes": load_traffic(self.name, "mpgemm"),
+               "fused_hbm_traffic_bytes": load_traffic(self.name, "fused")}
         if self.M >= 16 and not self.int8 and not self.tri and not self.lut8:
             out = self.torch.empty((self.M, self.N), dtype=self.torch.float16, device="cuda")
             for i in range(3):
@@ -349,7 +355,8 @@ class Case:
                     2: "dequant_skinny_kernel (16-token slabs, 1-bit weights decoded in registers)"}[kind]
             rec.update({"dequant_mfma_us": round(ms_dq * 1e3, 3), "dequant_mfma_tops": round(tflops, 2),
                         "dequant_mfma_frac_of_fp16_peak": round(tflops / MFMA_FP16_PEAK_TFLOPS, 4),
-                        "dequant_kernel": name, "dequant_k_splits": splits})
+                        "dequant_kernel": name, "dequant_k_splits": splits,
+                        "dequant_hbm_traffic_bytes": load_traffic(self.name, "dequant")})
             if kind != 0:
                 rec["lut_over_dequant_time"] = round(ms_mp / ms_dq, 2)
         return rec
@@ -518,48 +525,117 @@ def _per_dispatch(rows, counter):
     return out
 
 
-def summarize_traffic(fetch_dir, write_dir, command=""):
-    """HBM bytes per launch of the headline kernels from FETCH_SIZE and WRITE_SIZE runs
-    (KiB per dispatch), scaled by what the counters read for a 256 MiB device copy."""
-    import workloads as W
-    fetch = _per_dispatch(_csv_rows(fetch_dir, "counter_collection.csv"), "FETCH_SIZE")
-    write = _per_dispatch(_csv_rows(write_dir, "counter_collection.csv"), "WRITE_SIZE")
-    kib = 256 * 1024  # the calibration copy reads and writes 256 MiB
-    f_copy = max(fetch.get(COPY_KERNEL, [0.0]))
-    w_copy = max(write.get(COPY_KERNEL, [0.0]))
-    if f_copy <= 0 or w_copy <= 0:
-        raise SystemExit("no 256 MiB copy in the runs: profile bench.py with --calibrate-copy")
-    fs, ws = kib / f_copy, kib / w_copy
-    out = ["# HBM traffic of the headline kernels from rocprofv3 PMC counters", "",
-           "commands (each counter in its own run, from /tmp with TMPDIR=/tmp):", f"  {command}", "",
-           f"Calibration: the 256 MiB device copy (torch copy, {COPY_KERNEL}) reads FETCH_SIZE = "
-           f"{f_copy:.0f} KiB and WRITE_SIZE = {w_copy:.0f} KiB for {kib} KiB read and written,",
-           f"so FETCH_SIZE is scaled by {fs:.4f} and WRITE_SIZE by {ws:.4f}.", ""]
-    inp = W.make_inputs(2, 0, M=1)
-    recs = []
-    for kind, prefix in HEADLINE_KERNELS.items():
-        names = [n for n in fetch if n.startswith(prefix)]
-        if not names or names[0] not in write:
+def _dispatches(rows, counter):
+    """[(dispatch id, kernel name, value)] of one counter in dispatch order (instances summed)."""
+    per = {}
+    for r in rows:
+        if r["Counter_Name"] != counter:
             continue
-        name = names[0]
-        f_raw = sum(fetch[name]) / len(fetch[name])
-        w_raw = sum(write[name]) / len(write[name])
-        traffic = round((f_raw * fs + w_raw * ws) * 1024)
-        alg = algorithmic_bytes(inp, 4, fused=(kind == "fused"))["total"]
-        out += [name, f"  dispatches: {len(fetch[name])}",
-                f"  FETCH_SIZE raw {f_raw:.1f} KiB/dispatch -> {f_raw * fs:.1f} KiB",
-                f"  WRITE_SIZE raw {w_raw:.1f} KiB/dispatch -> {w_raw * ws:.1f} KiB",
-                f"  HBM traffic {traffic} B/launch vs algorithmic {alg} B ({traffic / alg:.3f}x)", ""]
-        recs.append({"workload": "ternary_int8_gemv_4k", "timed_kernel": kind, "kernel": name,
-                     "fetch_kib_raw": round(f_raw, 1), "write_kib_raw": round(w_raw, 1),
-                     "fetch_scale": round(fs, 4), "write_scale": round(ws, 4), "bytes_per_launch": traffic,
-                     "algorithmic_bytes": alg, "kernel_source_sha256_16": kernel_source_hash(kind)})
-    out.append("Per-kernel raw averages (KiB per dispatch):")
-    for name in sorted(fetch):
-        if name in write:
-            out.append(f"  {_short(name, 76):76s} fetch {sum(fetch[name]) / len(fetch[name]):10.1f}  "
-                       f"write {sum(write[name]) / len(write[name]):10.1f}")
-    out += ["", "machine-readable records (bench.py uses one only while the kernel sources hash the same):"]
+        key = (int(r["Dispatch_Id"]), r["Kernel_Name"])
+        per[key] = per.get(key, 0.0) + float(r["Counter_Value"])
+    return sorted((d, n, v) for (d, n), v in per.items())
+
+
+def _call_kind(name):
+    """Which timed call a kernel serves: 'mpgemm', 'fused' or 'dequant' for the main
+    kernels, 'attach' for the split-completion kernels (finalize, reduce) that belong to
+    the call launched just before them, None for everything else."""
+    if "lut_finalize_kernel" in name or "dequant_reduce_kernel" in name:
+        return "attach"
+    if "lut_fused_" in name:
+        return "fused"
+    if "lut_gemv" in name or "lut_mtok_kernel" in name:
+        return "mpgemm"
+    if "dequant_" in name:
+        return "dequant"
+    return None
+
+
+def _workload_inputs(name):
+    """Inputs and output element size of a workload named as in the bench output."""
+    import workloads as W
+    for cid, w in W.WORKLOADS.items():
+        for (sid, M, _, _) in w.shapes():
+            for lut8 in (False, True):
+                if case_name(cid, sid, M, lut8=lut8) == name:
+                    inp = W.make_inputs(cid, sid, M=M)
+                    return inp, (4 if inp.act_kind == W.ACT_INT8 else 2), lut8
+    return None, None, None
+
+
+def summarize_traffic(dirs, command=""):
+    """HBM bytes per call of the LUT and comparison kernels from FETCH_SIZE and
+    WRITE_SIZE runs (KiB per dispatch, each counter in its own run), scaled by what the
+    counters read for the run's 256 MiB device copy.  Directories are named
+    fetch_<workload> / write_<workload>, one bench.py --only <workload> --calibrate-copy
+    run each; in every run the dispatches before the copy belong to the headline
+    workload and those after it to <workload>.  A call's traffic is its main kernel plus
+    the split-completion kernel launched right after it (finalize, reduce)."""
+    import re
+    runs = {}
+    for d in dirs:
+        base = os.path.basename(os.path.normpath(d))
+        m = re.match(r"^(fetch|write)_(.+)$", base)
+        if not m:
+            raise SystemExit(f"{d}: expected a directory named fetch_<workload> or write_<workload>")
+        runs.setdefault(m.group(2), {})[m.group(1)] = d
+    kib = 256 * 1024  # the calibration copy reads and writes 256 MiB
+    head = case_name(2, 0, 1)
+    per_call = {}   # (workload, kind) -> {"fetch": [per call], "write": [...], "kernels": set}
+    scales = {}
+    for wl, pair in sorted(runs.items()):
+        if set(pair) != {"fetch", "write"}:
+            raise SystemExit(f"{wl}: need both a fetch_ and a write_ run")
+        for counter, key in (("FETCH_SIZE", "fetch"), ("WRITE_SIZE", "write")):
+            seq = _dispatches(_csv_rows(pair[key], "counter_collection.csv"), counter)
+            copies = [(v, d) for d, n, v in seq if n.startswith(COPY_KERNEL)]
+            if not copies:
+                raise SystemExit(f"{pair[key]}: no 256 MiB copy: profile bench.py with --calibrate-copy")
+            v_copy, d_copy = max(copies)
+            scale = kib / v_copy
+            scales[(wl, key)] = scale
+            cur = None  # (segment workload, kind, call record) of the last main kernel
+            for d, n, v in seq:
+                seg = head if d < d_copy else wl
+                kind = _call_kind(n)
+                if kind in ("mpgemm", "fused", "dequant"):
+                    rec = per_call.setdefault((seg, kind), {"fetch": [], "write": [], "kernels": set()})
+                    rec[key].append(v * scale * 1024)
+                    rec["kernels"].add(n)
+                    cur = (seg, kind)
+                elif kind == "attach" and cur is not None:
+                    rec = per_call[cur]
+                    rec[key][-1] += v * scale * 1024
+                    rec["kernels"].add(n)
+    out = ["# HBM traffic per call of the LUT mpGEMM and comparison kernels (rocprofv3 PMC counters)", "",
+           "commands (each counter in its own run, from /tmp with TMPDIR=/tmp), for each <workload> listed below:",
+           f"  {command}", "",
+           "Each run's FETCH_SIZE / WRITE_SIZE (KiB per dispatch) are scaled by what the same counter reads",
+           "for the run's 256 MiB device copy (torch copy_, __amd_rocclr_copyBuffer; 262144 KiB read and written).",
+           "A call's traffic adds the split-completion kernel (finalize / reduce) that follows its main kernel.",
+           "Algorithmic bytes: weights N K b / 8 + metadata + tables 4 M K (mpgemm) or FP16 activations 2 M K",
+           "(fused, dequant) + output; the ratio above 1 is re-read or partial-sum traffic.", ""]
+    recs = []
+    for (wl, kind), rec in sorted(per_call.items()):
+        inp, ob, lut8 = _workload_inputs(wl)
+        if inp is None or not rec["fetch"] or not rec["write"]:
+            continue
+        n = min(len(rec["fetch"]), len(rec["write"]))
+        f = sorted(rec["fetch"])[n // 2] if n else 0.0
+        w = sorted(rec["write"])[n // 2] if n else 0.0
+        out_b = 2 if kind == "dequant" else ob
+        alg = algorithmic_bytes(inp, out_b, fused=(kind != "mpgemm"), lut8=(lut8 and kind == "mpgemm"))["total"]
+        traffic = round(f + w)
+        out += [f"{wl} / {kind}: {', '.join(sorted(_short(k, 90) for k in rec['kernels']))}",
+                f"  calls {n}; median per call: read {f / 1024:.1f} KiB, written {w / 1024:.1f} KiB; "
+                f"traffic {traffic} B vs algorithmic {alg} B ({traffic / alg:.3f}x)", ""]
+        recs.append({"workload": wl, "timed_kernel": kind, "kernels": sorted(rec["kernels"]), "calls": n,
+                     "read_bytes": round(f), "write_bytes": round(w), "bytes_per_launch": traffic,
+                     "algorithmic_bytes": alg, "ratio": round(traffic / alg, 4),
+                     "fetch_scale": round(scales.get((wl, "fetch"), 0.0), 4),
+                     "write_scale": round(scales.get((wl, "write"), 0.0), 4),
+                     "kernel_source_sha256_16": kernel_source_hash(kind)})
+    out += ["machine-readable records (bench.py uses one only while the kernel sources hash the same):"]
     out += [json.dumps(r) for r in recs]
     return "\n".join(out)
 
@@ -702,7 +778,7 @@ def main():
         if args.summarize_trace:
             print(summarize_trace(args.summarize_trace, args.command, args.bench_logs))
         elif args.summarize_traffic:
-            print(summarize_traffic(*args.summarize_traffic, args.command))
+            print(summarize_traffic(args.summarize_traffic, args.command))
         else:
             print(summarize_counters(args.summarize_counters, args.command))
         return
