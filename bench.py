@@ -76,6 +76,9 @@ def parse():
                          "instrumented library (paper_2408_06003_amd/build.py --timeline)")
     ap.add_argument("--timeline-entry", default="mpgemm", choices=("mpgemm", "fused"),
                     help="entry point whose kernel the timeline records")
+    ap.add_argument("--stream-ceiling", action="store_true",
+                    help="sweep the streaming-read calibration kernel over sizes and launch shapes and print "
+                         "the best single-launch read per size (GPU)")
     ap.add_argument("--command", default="", help="the profiling command, recorded in a summary")
     ap.add_argument("--bench-logs", nargs="*", default=[],
                     help="bench.py outputs (JSON line last) whose headline launch times a trace summary quotes")
@@ -443,6 +446,78 @@ def calibrate_copy():
             "gbps": round(2 * n / (ms * 1e-3) / 1e9, 1)}
 
 
+def stream_ceiling(sizes_mb=(4.2, 8.9, 26.8, 29.5, 48.0, 1024.0)):
+    """The best single-launch streaming read of each byte count: the calibration kernel
+    over grid sizes, 16-byte loads in flight per lane, nontemporal hints and workgroup
+    ranges, each launch on its own slice of a >= 1 GiB rotation set (HBM-cold), graph
+    replays of back-to-back launches, median of 5 replays.  Prints a text summary."""
+    import itertools
+    import math
+    import torch
+    import paper_2408_06003_amd as L
+    torch.cuda.set_device(0)
+    sink = torch.zeros(65536, dtype=torch.int32, device="cuda")
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+
+    def replay_us(fn, n, reps=5):
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=side):
+            for i in range(n):
+                fn(i)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        t = []
+        for _ in range(reps):
+            e0.record()
+            g.replay()
+            e1.record()
+            torch.cuda.synchronize()
+            t.append(e0.elapsed_time(e1) * 1e3 / n)
+        return sorted(t)[len(t) // 2]
+
+    lines = ["# Single-launch streaming-read ceiling of the MI355X (HBM-cold)", "",
+             "command (on the MI355X): python3 bench.py --stream-ceiling", "",
+             "lutgemm_calibrate_stream_read_ex: every lane keeps U 16-byte loads in flight (clamped indices,",
+             "XOR-folded, one word per workgroup written); 'nt' = nontemporal loads, 'contig' = one contiguous",
+             "range per workgroup instead of round-robin tiles.  Each launch reads its own copy of the buffer",
+             "(a >= 1 GiB rotation set), launches are graph-replayed back to back, median of 5 replays.",
+             "Published HBM3E peak: 8000 GB/s.", ""]
+    summary = []
+    for mb in sizes_mb:
+        nb = (int(mb * (1 << 20)) + 255) // 256 * 256
+        R = max(2, math.ceil((1 << 30) / nb))
+        bufs = [torch.ones(nb, dtype=torch.uint8, device="cuda") for _ in range(R)]
+        torch.cuda.synchronize()
+        n = 4 if nb >= (1 << 29) else max(20, min(200, R))
+        blist = (256, 512, 1024, 2048, 4096, 8192) if nb < (1 << 29) else (1024, 2048, 4096, 8192, 16384)
+        res = []
+        for blocks, unroll, flags in itertools.product(blist, (1, 2, 4, 8, 16), (0, 1, 2, 3)):
+            if blocks * 256 * unroll * 16 > 4 * nb and blocks > 256:
+                continue  # grids far larger than the data
+            us = replay_us(lambda i: L.calibrate_stream_read_ex(bufs[i % R], nb, sink, blocks, unroll, flags), n)
+            res.append((us, blocks, unroll, flags))
+        floor = {b: round(replay_us(lambda i: L.calibrate_stream_read_ex(bufs[i % R], 16, sink, b, 1, 0), 100), 3)
+                 for b in (256, 1024, 4096)}
+        res.sort()
+        best = res[0]
+        lines.append(f"{nb / 1e6:8.1f} MB: best {best[0]:8.3f} us = {nb / (best[0] * 1e-6) / 1e9:7.1f} GB/s "
+                     f"({nb / (best[0] * 1e-6) / 8e12:.3f} of 8 TB/s) with {best[1]} workgroups, U={best[2]}, "
+                     f"nt={best[3] & 1}, contig={best[3] >> 1}; 16-byte launch floor {floor} us")
+        for us, blocks, unroll, flags in res[1:5]:
+            lines.append(f"{'':12s}next: {us:8.3f} us ({nb / (us * 1e-6) / 1e9:7.1f} GB/s) {blocks} wg, U={unroll}, "
+                         f"nt={flags & 1}, contig={flags >> 1}")
+        summary.append((nb, best[0]))
+        del bufs
+        torch.cuda.empty_cache()
+    lines += ["", "bytes, best time, best rate:"]
+    for nb, us in summary:
+        lines.append(f"  {nb:>12d} B: {us:9.3f} us, {nb / (us * 1e-6) / 1e9:7.1f} GB/s")
+    return "\n".join(lines)
+
+
 # ---------------------------------------------------------------- rocprofv3 summaries (CPU only)
 
 HEADLINE_KERNELS = {
@@ -773,6 +848,9 @@ def main():
     args = parse()
     if args.timeline:
         print(timeline(args.timeline, args.timeline_entry))
+        return
+    if args.stream_ceiling:
+        print(stream_ceiling(), flush=True)
         return
     if args.summarize_trace or args.summarize_traffic or args.summarize_counters:
         if args.summarize_trace:
