@@ -39,7 +39,7 @@ ROTATION_BYTES = 1 << 30
 # read patterns of the streaming-read ceiling (workgroups, 16-byte loads per lane):
 # the best single-launch reads of 4-48 MB and of 1 GiB in a sweep over grid size,
 # loads in flight, nontemporal hints and workgroup ranges (profiles/stream_read_ceiling.txt)
-STREAM_READ_CONFIGS = ((1024, 2), (512, 4), (512, 8))
+STREAM_READ_CONFIGS = ((1024, 2), (2048, 1), (4096, 2), (512, 4), (512, 8))
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "pmc_traffic.txt")
 # sources that define each timed kernel and its launch (a PMC traffic record is used
 # only while they hash as when the counters were taken)
@@ -198,6 +198,10 @@ class Case:
         self.ws = torch.zeros(ws, dtype=torch.uint8, device=dev) if ws else None
         dq = L.dequant_workspace_size(self.p, M)
         self.dq_ws = torch.empty(dq, dtype=torch.uint8, device=dev) if dq else None
+        # allocated and zero-filled here, not on first use: a first use inside a graph
+        # capture would capture the fill instead of running it
+        fw = L.fused_workspace_size(self.p, M)
+        self.fws = torch.zeros(fw, dtype=torch.uint8, device=dev) if fw else None
         self.int8 = inp.act_kind == W.ACT_INT8
         self.out_code = L.OUT_FP32 if self.int8 else L.OUT_FP16
         self.out = torch.empty((M, inp.N), dtype=torch.float32 if self.int8 else torch.float16, device=dev)
@@ -221,9 +225,6 @@ class Case:
 
     def fused(self, i):
         """The same step through lutgemm_mpgemm_fused (tables built inside the LUT kernel)."""
-        if not hasattr(self, "fws"):
-            n = self.L.fused_workspace_size(self.p, self.M)
-            self.fws = self.torch.zeros(n, dtype=self.torch.uint8, device="cuda") if n else None
         self.L.mpgemm_fused(self.p, self.M, self.act, self.packed[i % len(self.packed)], self.out,
                             self.out_code, False, workspace=self.fws)
 

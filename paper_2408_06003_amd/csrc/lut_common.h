@@ -422,7 +422,11 @@ __device__ __forceinline__ uint4 ld_nt(const uint4 *p) {
 // arrival), applies the output epilogue and re-arms the counter to 0 for the next
 // call.  No fence instruction is needed: the partial stores are complete before the
 // counter is touched, and the last workgroup's loads are issued after it has seen
-// the count.  Returns only after the output is stored (or at once for the others).
+// the count.  The counter is re-armed by an atomic subtraction whose returned value
+// the last workgroup waits for, so the re-arm has been performed before the kernel
+// ends: a launch that follows directly (also one with no memory fence in between, as
+// between the kernel nodes of a graph) never finds the counter still at `splits`.
+// Returns only after the output is stored (or at once for the others).
 // Partials of split s, row m at part[(s M + m) N_pad + n]; split 0 includes the
 // ternary group sum.
 template <bool INT8>
@@ -445,6 +449,11 @@ __device__ __forceinline__ void split_complete(const LutParams &p, int wfmt, int
         tl_clear(p, 5);
         return;
     }
+    // re-arm the counter (all `splits` arrivals have been counted), issued before the
+    // partial loads so that its round trip overlaps theirs
+    uint32_t rearmed = 0u;
+    if (threadIdx.x == 0)
+        rearmed = __hip_atomic_fetch_add(counter, 0u - (uint32_t)p.splits, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     // every split's partial in one batch of loads (splits <= INKERNEL_MAX_SPLITS, indices
     // past the last split clamped to it), then the fixed-order sum
     float v[INKERNEL_MAX_SPLITS];
@@ -464,8 +473,9 @@ __device__ __forceinline__ void split_complete(const LutParams &p, int wfmt, int
             sf += j < p.splits ? v[j] : 0.f;
     }
     tl_stamp(p, 5);
-    if (threadIdx.x == 0) __hip_atomic_store(counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     store_out<INT8>(p, wfmt, m, n, sf, si, ep);
+    // the re-arm's returned value is needed here: the wave waits until it is performed
+    asm volatile("; counter re-armed from %0" ::"v"(rearmed));
 }
 
 }  // namespace lutgemm
