@@ -734,7 +734,7 @@ def summarize_counters(dirs, command=""):
                 per.setdefault(c, {}).setdefault((wl, name), []).extend(vals)
     counters = sorted(per)
     keys = sorted({k for c in counters for k in per[c]})
-    out = ["# Utilization counters of the large-M kernels (rocprofv3 --pmc)", "",
+    out = ["# Utilization counters of the LUT and comparison kernels (rocprofv3 --pmc)", "",
            "commands (from /tmp with TMPDIR=/tmp):", f"  {command}", "",
            "Per dispatch, averaged over the dispatches of one workload's runs; cycles are",
            "shader-clock cycles summed over the instances the counter has (GRBM_GUI_ACTIVE is",
