@@ -115,3 +115,15 @@ def test_accumulate_and_determinism(kind, splits, tune):
     a = gp.dequant(out_dtype=torch.float32)
     b = gp.dequant(out_dtype=torch.float32)
     assert torch.equal(a, b), "comparison path not bitwise reproducible"
+
+
+@pytest.mark.parametrize("kind", [0, 1])
+@pytest.mark.parametrize("wfmt,bits", [(W.WFMT_TERNARY, 2), (W.WFMT_UINT, 4), (W.WFMT_BINARY, 1)])
+def test_tile_kernels_per_tensor_scale(kind, wfmt, bits, tune):
+    """One FP32 scale (and zero) for the whole tensor: the 256 x 256 kernel reads them
+    once per workgroup, the 128 x 128 kernel per K step."""
+    tune(DEQUANT_KIND=kind)
+    banner(f"dequant tile kernel kind={kind}, per-tensor scale, wfmt={wfmt} b={bits}, M=130 K=1024 N=300")
+    inp = W.make_custom(wfmt, bits, 0, W.ACT_FP16, M=130, K=1024, N=300, seed=950 + 10 * kind + wfmt,
+                        scale_fp32=(wfmt != W.WFMT_UINT))  # UINT: FP16 scale and zero
+    check(GpuProblem(inp), f"tile kind={kind} per-tensor wfmt={wfmt}")
