@@ -1,12 +1,16 @@
 // Comparison path: dequantization-based mpGEMM (LUT Tensor Core, Section 2.2,
-// "indirect mpGEMM with dequantization"), fused into one gfx950 matrix-core
-// kernel.  Weights are rebuilt from the same packed bit-planes as FP16
-// r = s' (q' - z') = s (q - z) (Eq. 1-2) in LDS, then multiplied with FP16
-// activations by v_mfma_f32_32x32x16_f16 with FP32 accumulation.
+// "indirect mpGEMM with dequantization"), fused into gfx950 matrix-core kernels.
+// Weights are rebuilt from the same packed bit-planes as FP16
+// r = s' (q' - z') = s (q - z) (Eq. 1-2), in LDS or in registers, then multiplied
+// with the FP16 activations on the matrix cores with FP32 accumulation.
 //
-// Small grids: workgroup tile 128 (M) x 128 (N), K step 128 (one packed plane
-// word per column and plane); 4 wavefronts, each owning a 64 x 64 sub-tile as
-// 2 x 2 MFMA 32x32 blocks.  Large M: the pipelined 256 x 256 kernel below.
+// Three kernels, chosen by plan_dequant at the end of this file: 1-bit weights at
+// a few tokens, 16-token slabs on v_mfma_f32_16x16x32_f16 with the weights decoded
+// in registers; large M, the pipelined 256 x 256 kernel; other shapes, 128 x 128
+// tiles with K step 128 (one packed plane word per column and plane), 4
+// wavefronts each owning a 64 x 64 sub-tile as 2 x 2 MFMA 32x32 blocks.  Any of them
+// can split K; the FP32 partial sums are then added in split order by
+// dequant_reduce_kernel.
 #include <hip/hip_runtime.h>
 #include <hip/hip_fp16.h>
 
