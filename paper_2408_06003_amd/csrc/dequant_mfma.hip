@@ -454,6 +454,7 @@ __global__ __launch_bounds__(512) void dequant_mfma_big_kernel(DequantParams p, 
 // the work: no decoded weight is reused beyond the slab's 16 tokens.
 constexpr int SK_CHUNK = 16;  // 128-blocks of activations staged in LDS at once
 constexpr int SK_RING = 8;    // 128-blocks of weight words in flight per lane
+constexpr int SK_STAGE = 4;   // staging items per thread: 16 rows x SK_CHUNK blocks x 4 words / 256
 typedef float floatx4_t __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
@@ -487,6 +488,54 @@ __global__ __launch_bounds__(256) void dequant_skinny_kernel(DequantParams p, in
     const int64_t kb0 = (int64_t)blockIdx.z * p.kbs;
     const int nkb = (int)(p.KB - kb0 < p.kbs ? p.KB - kb0 : p.kbs);
     const int64_t m0 = (int64_t)blockIdx.y * 16;
+
+    // Activation staging, one item per (row, block, word g2) = the 32 activations of
+    // word g2 of the block, 64 contiguous bytes (four 16-byte loads); all of a thread's
+    // loads are issued before any of its LDS stores (at most 4 items per thread: nc <=
+    // 16), and each item gives the four operand chunks of steps st = 0..3: the 4
+    // activations from 4 (3 - st) (low halves) and from 4 (7 - st) (high halves)
+    // interleaved.  Rows past M are zero; item indices past the chunk are clamped and
+    // not stored.  A wavefront's loads return in issue order, so the first chunk's are
+    // issued before the weight ring: behind it they would wait for the weight stream.
+    uint4 xv[SK_STAGE][4];
+    auto stage_load = [&](int c0, int nc) {
+        const int items = 16 * nc * 4;
+#pragma unroll
+        for (int u = 0; u < SK_STAGE; ++u) {
+            const int i = tid + 256 * u, ic = i < items ? i : items - 1;
+            const int row = ic / (nc * 4), rest = ic % (nc * 4);
+            const int64_t mr = m0 + row < p.M ? m0 + row : p.M - 1;
+            const uint4 *src = (const uint4 *)(p.act + mr * p.K + (kb0 + c0 + (rest >> 2)) * KBLK + 32 * (rest & 3));
+#pragma unroll
+            for (int j = 0; j < 4; ++j) xv[u][j] = src[j];
+        }
+    };
+    auto stage_store = [&](int nc) {
+        const int items = 16 * nc * 4;
+#pragma unroll
+        for (int u = 0; u < SK_STAGE; ++u) {
+            const int i = tid + 256 * u;
+            if (i < items) {
+                const int row = i / (nc * 4), rest = i % (nc * 4);
+                const int blk = rest >> 2, g2 = rest & 3;
+                const bool live = m0 + row < p.M;
+                const uint32_t X[16] = {xv[u][0].x, xv[u][0].y, xv[u][0].z, xv[u][0].w, xv[u][1].x, xv[u][1].y,
+                                        xv[u][1].z, xv[u][1].w, xv[u][2].x, xv[u][2].y, xv[u][2].z, xv[u][2].w,
+                                        xv[u][3].x, xv[u][3].y, xv[u][3].z, xv[u][3].w};
+#pragma unroll
+                for (int st = 0; st < 4; ++st) {
+                    const uint32_t lx = X[2 * (3 - st)], ly = X[2 * (3 - st) + 1];
+                    const uint32_t hx = X[2 * (7 - st)], hy = X[2 * (7 - st) + 1];
+                    uint4 v = make_uint4(__builtin_amdgcn_perm(hx, lx, 0x05040100u), __builtin_amdgcn_perm(hx, lx, 0x07060302u),
+                                         __builtin_amdgcn_perm(hy, ly, 0x05040100u), __builtin_amdgcn_perm(hy, ly, 0x07060302u));
+                    if (!live) v = make_uint4(0u, 0u, 0u, 0u);
+                    *(uint4 *)(As + row * row_h + blk * KBLK + 8 * ((4 * g2 + st) ^ row)) = v;
+                }
+            }
+        }
+    };
+    stage_load(0, nkb < ch ? nkb : ch);
+    __builtin_amdgcn_sched_barrier(0);  // keep the activation loads ahead of the weight ring
 
     // word g of column ncol0 + 16 cb + r in 128-block kbl of the range (clamped to the
     // last block: loads past the range repeat it and are never used)
@@ -523,28 +572,18 @@ __global__ __launch_bounds__(256) void dequant_skinny_kernel(DequantParams p, in
         }
     };
 
+    // the first chunk, loaded before the weight ring, in straight-line code (so the
+    // compiler's waits count only the activation loads ahead of the ring)
+    stage_store(nkb < ch ? nkb : ch);
+    dq_lds_barrier();
     for (int c0 = 0; c0 < nkb; c0 += ch) {
         const int nc = nkb - c0 < ch ? nkb - c0 : ch;
-        if (c0) dq_lds_barrier();  // every wavefront is done with the previous chunk
-        // stage: one 16-byte operand chunk (row, block, word g2, step st) per item, the 4
-        // activations of the low half (from 4 (3 - st)) and of the high half (from
-        // 4 (7 - st)) of word g2 interleaved; rows past M are zero
-        const int items = 16 * nc * 16;
-        for (int i = tid; i < items; i += 256) {
-            const int row = i / (nc * 16), rest = i % (nc * 16);
-            const int blk = rest >> 4, g2 = (rest >> 2) & 3, st = rest & 3;
-            const int64_t mr = m0 + row < p.M ? m0 + row : p.M - 1;
-            const uint16_t *src = p.act + mr * p.K + (kb0 + c0 + blk) * KBLK + 32 * g2;
-            uint2 lo = *(const uint2 *)(src + 4 * (3 - st));
-            uint2 hi = *(const uint2 *)(src + 4 * (7 - st));
-            if (m0 + row >= p.M) lo = hi = make_uint2(0u, 0u);
-            const uint4 v = make_uint4(__builtin_amdgcn_perm(hi.x, lo.x, 0x05040100u),
-                                       __builtin_amdgcn_perm(hi.x, lo.x, 0x07060302u),
-                                       __builtin_amdgcn_perm(hi.y, lo.y, 0x05040100u),
-                                       __builtin_amdgcn_perm(hi.y, lo.y, 0x07060302u));
-            *(uint4 *)(As + row * row_h + blk * KBLK + 8 * ((4 * g2 + st) ^ row)) = v;
+        if (c0) {
+            dq_lds_barrier();  // every wavefront is done with the previous chunk
+            stage_load(c0, nc);
+            stage_store(nc);
+            dq_lds_barrier();
         }
-        dq_lds_barrier();
 
         // whole groups of SK_RING blocks: no condition in the body, so the waits for the
         // ring's loads stay exact
