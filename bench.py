@@ -234,11 +234,11 @@ class Case:
         replayed, so host launch overhead is not counted (the way a decode loop runs).
         Every graph holds n calls on its own slice of the rotation set, and enough graphs
         are captured to cover the whole set (>= 1 GiB of distinct weight copies); the
-        graphs are replayed in turn, enqueued back to back, and each replay is timed on
-        its own between a pair of events, so between two replays of one graph at least
-        1 GiB of other weights has been read and every timed call reads its weights from
-        HBM, whatever n is.  At least ``reps`` replays are timed (every graph at least
-        once) and the median is returned;
+        graphs are replayed in turn and each replay is timed on its own (the device
+        idle before it), so between two replays of one graph at least 1 GiB of other
+        weights has been read and every timed call reads its weights from HBM, whatever
+        n is.  At least ``reps`` replays are timed (every graph at least once) and the
+        median is returned;
         ``self.last_distinct_bytes`` records the distinct weight bytes they read.
         ``check`` (a function returning a tensor) compares a replay, after eager work,
         with the eager result."""
@@ -278,22 +278,17 @@ class Case:
         for g in graphs:  # warm replays of every slice
             g.replay()
         torch.cuda.synchronize()
-        # The replays are enqueued back to back (a decode loop's steady state: the next
-        # graph's launch overlaps the current one's work), each between its own pair of
-        # events; one synchronization before and after all of them.
         s = torch.cuda.current_stream()
-        n_rep = max(reps, n_graphs)
-        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n_rep)]
-        touched = set()
-        torch.cuda.synchronize()
-        for r in range(n_rep):
+        batches, touched = [], set()
+        for r in range(max(reps, n_graphs)):
             gi = r % n_graphs
-            ev[r][0].record(s)
+            torch.cuda.synchronize()
+            e0.record(s)
             graphs[gi].replay()
-            ev[r][1].record(s)
+            e1.record(s)
+            torch.cuda.synchronize()
+            batches.append(e0.elapsed_time(e1) / n)
             touched.update((gi * n + j) % R for j in range(n))
-        torch.cuda.synchronize()
-        batches = [a.elapsed_time(b) / n for a, b in ev]
         self.last_distinct_bytes = len(touched) * self.packed[0].numel()
         self.last_replays = len(batches)
         return sorted(batches)[len(batches) // 2]
@@ -924,10 +919,10 @@ def main():
                    "step": "lutgemm_mpgemm_fused: INT8 quantization + table build in LDS + bit-serial "
                            "lookup + epilogue, one kernel"},
         "timing": "HIP graphs of K steps, one per slice of a >= 1 GiB rotation set of packed-weight copies, "
-                  "replayed in turn and enqueued back to back (the next replay's launch overlaps the current "
-                  "one's work, as in a decode loop); each replay of K steps is timed on its own between HIP "
-                  "events and ms_per_step is the median replay / K, so every timed step reads its weights from "
-                  "HBM whatever K is; ms_per_step_eager launches the same steps one by one from Python",
+                  "replayed in turn; each replay of K steps is timed on its own between HIP events (the device "
+                  "idle before it) and ms_per_step is the median replay / K, so every timed step reads its "
+                  "weights from HBM whatever K is; ms_per_step_eager launches the same steps one by one from "
+                  "Python",
         "timed_replays": step_replays,
         "distinct_weight_bytes_timed": step_distinct,
         "ms_per_step_eager": round(ms_step_eager, 6),
