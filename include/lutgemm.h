@@ -267,9 +267,17 @@ size_t lutgemm_fused_workspace_size(const lutgemm_problem_t *problem, int64_t M)
  * lutgemm_precompute + lutgemm_mpgemm, one kernel; with larger weights and
  * ACT_FP16 the split-K kernel, whose tables are exact FP32 sums of the
  * activations as given (no token scaling, no FP16 rounding of entries), plus the
- * split sum.  TERNARY_3IN5: one kernel for every M, tables built per workgroup
- * for its token.  Otherwise (M > 2, ACT_INT8 with larger weights, ACT_FP16_LUT8)
- * it runs lutgemm_precompute into the workspace followed by lutgemm_mpgemm.
+ * split sum.  Several tokens (2 < M <= 64) with ACT_FP16 on layers of at most
+ * 64 x 256 columns: the multi-token kernel reads the FP16 activations of its
+ * tokens and K range, scales each token by the power of two 2^-e with e from its
+ * absmax over that K range, and builds the same FP16 entries as
+ * lutgemm_precompute (tuning key LUTGEMM_TUNE_MT_FUSED forces it on or off; every
+ * column tile repeats the build, so beyond those sizes precompute + mpGEMM is
+ * faster).  TERNARY_3IN5: one kernel for every M, tables built per workgroup for
+ * its token.  Otherwise (larger M or N with ACT_FP16, ACT_INT8 with M > 2 or
+ * larger weights, ACT_FP16_LUT8) it runs lutgemm_precompute into the workspace
+ * followed by lutgemm_mpgemm; INT8 quantization needs the absmax of the whole
+ * token, which a workgroup owning one K range does not see.
  *   act        device FP16 [M][K]
  *   packed, out, out_dtype, accumulate   as for lutgemm_mpgemm
  *   workspace  device, workspace_bytes >= lutgemm_fused_workspace_size(problem, M);
@@ -278,7 +286,9 @@ size_t lutgemm_fused_workspace_size(const lutgemm_problem_t *problem, int64_t M)
  * lutgemm_mpgemm.  FP16 activations: the zero-point term is summed per 128-block
  * instead of per quantization group, and the split-K kernel's entries are not
  * rounded to FP16, so results agree with the two-call path to within that
- * rounding (TERNARY_3IN5: bitwise).  Bitwise reproducible run to run.
+ * rounding (TERNARY_3IN5, and the multi-token kernel on weights without zero
+ * points: bitwise, unless an entry or partial sum is subnormal).  Bitwise
+ * reproducible run to run.
  */
 lutgemm_status_t lutgemm_mpgemm_fused(const lutgemm_problem_t *problem, int64_t M, const void *act,
                                       const void *packed, void *out, int32_t out_dtype,
@@ -354,7 +364,11 @@ enum {
                                        requests before its tables arrive, 0, 2, 4 or 8 = all (4)    */
     LUTGEMM_TUNE_DEQUANT_SPLITS = 13, /* LUTGEMM_DEQUANT_SPLITS: K splits of the comparison kernel
                                        (0: planned)                                                  */
-    LUTGEMM_TUNE_COUNT = 14
+    LUTGEMM_TUNE_MT_FUSED = 14,     /* LUTGEMM_MT_FUSED: lutgemm_mpgemm_fused with FP16 activations and
+                                       M > 2: 1 builds the tables inside the multi-token kernel, 0
+                                       runs precompute + mpGEMM (-1: planned, the former for
+                                       M <= 64 on layers of at most 64 x 256 columns)              */
+    LUTGEMM_TUNE_COUNT = 15
 };
 
 /* Sets planner override `key` (LUTGEMM_TUNE_*) to `value` (-1: its default).

@@ -42,7 +42,7 @@ EXPORTS = [
 # planner overrides (LUTGEMM_TUNE_*), for tests and experiments
 TUNE = {"TARGET_BLOCKS": 0, "WHOLEK_MAX_KB": 1, "GEMV_KIND": 2, "GEMV_CFG": 3, "SPLITS": 4, "KBS": 5,
         "MT16": 6, "MT_TARGET": 7, "MT_SPLITS": 8, "MT_ORDER": 9, "DEQUANT_KIND": 10, "LOG": 11,
-        "SPLIT_PRE": 12, "DEQUANT_SPLITS": 13}
+        "SPLIT_PRE": 12, "DEQUANT_SPLITS": 13, "MT_FUSED": 14}
 
 
 class Problem(ctypes.Structure):
@@ -291,7 +291,7 @@ class LutGemm:
         n = workspace_size(self.p, M)
         if n == 0:
             return None
-        if M not in self._ws:
+        if M not in self._ws or self._ws[M].numel() < n:  # (the size follows the tuning keys)
             self._ws[M] = torch.zeros(n, dtype=torch.uint8, device=self.device)
         return self._ws[M]
 
@@ -317,7 +317,7 @@ class LutGemm:
         if n == 0:
             return None
         key = ("fused", M)
-        if key not in self._ws:
+        if key not in self._ws or self._ws[key].numel() < n:
             self._ws[key] = torch.zeros(n, dtype=torch.uint8, device=self.device)
         return self._ws[key]
 
@@ -347,6 +347,6 @@ class LutGemm:
         if n == 0:
             return None
         key = ("dequant", M)
-        if key not in self._ws:
+        if key not in self._ws or self._ws[key].numel() < n:
             self._ws[key] = torch.empty(n, dtype=torch.uint8, device=self.device)
         return self._ws[key]

@@ -73,8 +73,8 @@ const char *const kTuneEnv[LUTGEMM_TUNE_COUNT] = {
     "LUTGEMM_TARGET_BLOCKS", "LUTGEMM_WHOLEK_MAX_KB", "LUTGEMM_GEMV_KIND", "LUTGEMM_GEMV_CFG",
     "LUTGEMM_SPLITS",        "LUTGEMM_KBS",           "LUTGEMM_MT16",      "LUTGEMM_MT_TARGET",
     "LUTGEMM_MT_SPLITS",     "LUTGEMM_MT_ORDER",      "LUTGEMM_DEQUANT_KIND", "LUTGEMM_LOG",
-    "LUTGEMM_SPLIT_PRE",     "LUTGEMM_DEQUANT_SPLITS"};
-const int kTuneDefault[LUTGEMM_TUNE_COUNT] = {256, 10000, -1, -1, 0, 0, 1, 8, 0, -1, -1, 0, 4, 0};
+    "LUTGEMM_SPLIT_PRE",     "LUTGEMM_DEQUANT_SPLITS", "LUTGEMM_MT_FUSED"};
+const int kTuneDefault[LUTGEMM_TUNE_COUNT] = {256, 10000, -1, -1, 0, 0, 1, 8, 0, -1, -1, 0, 4, 0, -1};
 std::atomic<int> g_tune[LUTGEMM_TUNE_COUNT];
 
 bool tune_value_ok(int key, int value) {
@@ -129,7 +129,22 @@ lutgemm_status_t hip_error(int e) { return e == 0 ? LUTGEMM_SUCCESS : hip_status
 // Several tokens: 8 tokens per workgroup of 256 columns, K split only when the
 // token x column grid is smaller than 8 x `target` workgroups (to twice that when the
 // K ranges stay at least 32 blocks long).
-LutPlan plan_lut(const Layout &L, int64_t M) {
+// Whether lutgemm_mpgemm_fused runs the multi-token kernel with its own table build
+// (FP16 activations, M > 2).  Every 256-column tile builds the tables of its tokens and
+// K range again, work the precompute does once, and the build is vector work in a
+// kernel bound by vector issue at large M; measured on MI355X it is faster than
+// precompute + mpGEMM up to M = 64 on layers of at most 64 column tiles (INT4 4096 x
+// 12288: 22 us against 25 at M = 4 and 8; binary 28672 x 8192: 26-28 against 28-30;
+// INT2 4096^2 at M = 64: 25 against 28) and slower beyond (binary 8192 x 28672, 112
+// tiles: +1.3 us at M = 16; +17 % at M = 256, +10 % for INT2 at M = 4096).
+static bool mtok_fused(const Layout &L, int64_t M) {
+    if (L.act != LUTGEMM_ACT_FP16 || M <= 2 || L.tri) return false;
+    const int f = tuning(LUTGEMM_TUNE_MT_FUSED);
+    if (f >= 0) return f != 0;
+    return M <= 64 && L.N_pad / NTILE <= 64;
+}
+
+LutPlan plan_lut(const Layout &L, int64_t M, bool fused) {
     LutPlan P{};
     const int64_t target = tuning(LUTGEMM_TUNE_TARGET_BLOCKS);
     const int64_t weight_bytes = L.KB * L.bits * L.N * 16;
@@ -242,6 +257,9 @@ LutPlan plan_lut(const Layout &L, int64_t M) {
         if (fs > 0) splits = fs;
         if (splits * base >= MAX_TILES) splits = (MAX_TILES - 1) / base;
         if (splits < 1) splits = 1;
+        // the fused table build with zero points keeps each K range's block sums in LDS
+        const bool zp_fused = fused && mtok_fused(L, M) && L.wfmt != LUTGEMM_WFMT_BINARY;
+        if (zp_fused && (L.KB + splits - 1) / splits > MTOK_FUSED_SMAX) splits = (L.KB + MTOK_FUSED_SMAX - 1) / MTOK_FUSED_SMAX;
         int64_t kbs = (L.KB + splits - 1) / splits;
         kbs = (kbs + ch - 1) / ch * ch;
         if (kbs > L.KB) kbs = L.KB;
@@ -323,7 +341,8 @@ static void log_plan(const char *who, const Layout &L, const LutPlan &plan, int6
 
 // Scratch of lutgemm_mpgemm_fused: the plan's workspace (counters, partial sums) at
 // offset 0 as for lutgemm_mpgemm, then the per-token factors when the fused GEMV
-// splits K, or the staged tables when the call runs precompute + mpGEMM.
+// splits K, or the staged tables when the call runs precompute + mpGEMM.  (The fused
+// multi-token kernel stores its partial sums already multiplied by the token factors.)
 struct FusedScratch {
     bool fused;
     size_t tables, tables_off, tok_off, total;
@@ -335,8 +354,10 @@ static FusedScratch fused_scratch(const Layout &L, const LutPlan &plan, int64_t 
     // that mode always takes the two-call path; the split-K GEMV builds its tables only
     // on the FP path (INT8 quantization needs the whole token's absmax)
     f.fused = ((plan.kind == 0 || plan.kind == 3) && L.act != LUTGEMM_ACT_FP16_LUT8) ||
-              (plan.kind == 2 && L.act == LUTGEMM_ACT_FP16);
-    if (f.fused) {
+              ((plan.kind == 2 || (plan.kind == 1 && mtok_fused(L, M))) && L.act == LUTGEMM_ACT_FP16);
+    if (f.fused && plan.kind == 1) {
+        f.total = plan.ws_bytes;
+    } else if (f.fused) {
         f.tok_off = plan.ws_bytes;
         f.total = plan.splits > 1 ? plan.ws_bytes + align256((size_t)M * 4) : 0;
     } else {
@@ -493,7 +514,7 @@ lutgemm_status_t lutgemm_mpgemm(const lutgemm_problem_t *problem, int64_t M, con
 size_t lutgemm_fused_workspace_size(const lutgemm_problem_t *problem, int64_t M) {
     if (check_problem(problem, M) != LUTGEMM_SUCCESS) return 0;
     Layout L = make_layout(*problem);
-    return fused_scratch(L, plan_lut(L, M), M).total;
+    return fused_scratch(L, plan_lut(L, M, true), M).total;
 }
 
 lutgemm_status_t lutgemm_mpgemm_fused(const lutgemm_problem_t *problem, int64_t M, const void *act,
@@ -508,7 +529,7 @@ lutgemm_status_t lutgemm_mpgemm_fused(const lutgemm_problem_t *problem, int64_t 
     if (out_dtype == LUTGEMM_OUT_INT32 && problem->act != LUTGEMM_ACT_INT8) return LUTGEMM_ERROR_NOT_SUPPORTED;
     if (accumulate != 0 && accumulate != 1) return LUTGEMM_ERROR_INVALID_VALUE;
     Layout L = make_layout(*problem);
-    LutPlan plan = plan_lut(L, M);
+    LutPlan plan = plan_lut(L, M, true);
     FusedScratch fs = fused_scratch(L, plan, M);
     if (fs.total > 0) {
         if (!workspace || !aligned16(workspace)) return LUTGEMM_ERROR_INVALID_VALUE;
@@ -525,6 +546,11 @@ lutgemm_status_t lutgemm_mpgemm_fused(const lutgemm_problem_t *problem, int64_t 
     LutParams lp = lut_params(L, plan, M, nullptr, packed, out, out_dtype, accumulate, ws);
     lp.act = (const uint16_t *)act;
     if (plan.kind == 3) return hip_status(launch_tri(lp, L, true, stream));
+    if (plan.kind == 1) {  // tables from the FP16 activations inside the multi-token kernel
+        int e = launch_mtok_fused(lp, L, plan, stream);
+        if (e == 0 && plan.splits > 1) e = launch_finalize(lp, L, plan, stream);
+        return hip_status(e);
+    }
     if (plan.kind == 2) {  // FP activations: tables from the activations, then the split sum
         int e = launch_fused_split(lp, L, plan, stream);
         if (e == 0 && plan.splits > 1 && !plan.inkernel) e = launch_finalize(lp, L, plan, stream);

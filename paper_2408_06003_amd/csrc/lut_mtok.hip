@@ -30,17 +30,48 @@
 // resources: workgroup-uniform offsets in scalar registers, fixed 32-bit lane
 // offsets, no 64-bit address arithmetic in the loop.  When the grid would not
 // fill the GPU, K is split and lut_finalize_kernel sums the partials.
+//
+// Precompute fused into the kernel (FZ != 0, FP16 activations; Section 3.1.1 splits
+// the precompute out so that it can be fused): the workgroup reads the FP16
+// activations of its tokens instead of precomputed half tables.  A first pass over
+// its K range gives each token's absmax (and, FZ = 2, the sum of every 128-block:
+// the S of Eq. 3 per block) and the power-of-two scale 2^-e with amax = f 2^e; each
+// staging lane then forms its two table entries per token as
+// ((-x0 + (+-x1)) + (+-x2)) + (+-x3) in FP32 from the scaled activations (exact
+// products, one rounding per addition) and rounds them to FP16, the operations of
+// the precompute operator.  The scale is local to the workgroup's K range; the
+// partial sums are multiplied back by 2^e before they are stored, and power-of-two
+// scaling commutes with every rounding on the way, so the output equals that of the
+// two-launch path whenever no entry or partial sum is subnormal.
 #include <type_traits>
 
 #include "lut_common.h"
 
 namespace lutgemm {
 
-constexpr int MTK = 8;  // tokens per workgroup
+constexpr int MTK = 8;  // tokens per workgroup (per half)
+constexpr int FZ_SMAX = MTOK_FUSED_SMAX;  // fused build with zero points: most 128-blocks per K range
 
 // The 16-bit lanes of x selected by SEL (v_perm_b32 byte selector) from {hi, lo}.
 __device__ __forceinline__ uint32_t perm(uint32_t hi, uint32_t lo, uint32_t sel) {
     return __builtin_amdgcn_perm(hi, lo, sel);
+}
+
+// Lane-wise maximum of two packed unsigned 16-bit pairs (v_pk_max_u16).
+__device__ __forceinline__ uint32_t max_u16x2(uint32_t a, uint32_t b) {
+    typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
+    return __builtin_bit_cast(uint32_t,
+                              __builtin_elementwise_max(__builtin_bit_cast(u16x2, a), __builtin_bit_cast(u16x2, b)));
+}
+
+// Sum of v over each row of 16 lanes by DPP (quad_perm [1,0,3,2], [2,3,0,1], row half
+// mirror, row mirror): every lane of the row ends with the same bits.
+__device__ __forceinline__ float row_sum16(float v) {
+    v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0xB1, 0xF, 0xF, false));
+    v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x4E, 0xF, 0xF, false));
+    v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x141, 0xF, 0xF, false));
+    v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x140, 0xF, 0xF, false));
+    return v;
 }
 
 template <bool INT8>
@@ -60,6 +91,11 @@ __device__ __forceinline__ uint32_t buf_u32(__amdgpu_buffer_rsrc_t r, uint32_t v
 }
 __device__ __forceinline__ uint32_t buf_u16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
     return __builtin_amdgcn_raw_buffer_load_b16(r, (int)voff, (int)soff, 0);
+}
+__device__ __forceinline__ uint2 buf_u64(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+    typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
+    const u32x2 v = __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(r, (int)voff, (int)soff, 0));
+    return make_uint2(v.x, v.y);
 }
 __device__ __forceinline__ uint4 buf_u128(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
     typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
@@ -204,20 +240,32 @@ __device__ __forceinline__ Tile tile_of(uint32_t b, uint32_t n_tiles, uint32_t m
 // NH halves of 8 tokens per workgroup (NH = 2: one decoded index serves two 16-byte
 // reads, the second at a fixed +256-byte offset, so index decoding, weight loads and
 // metadata are shared by 16 tokens).
-template <int BITS, bool INT8, bool TQ, int NH>
+// FZ: 0 = tables from the precompute; 1 = tables built from the FP16 activations;
+// 2 = the same with the per-block activation sums of the zero-point term.
+template <int BITS, bool INT8, bool TQ, int NH, int FZ>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(TQ ? 1 : (BITS == 1 && NH == 1 ? 6 : 4)))) void lut_mtok_kernel(LutParams p, int wfmt, int64_t n_tiles, int64_t m_tiles,
                                                        int order) {
+    static_assert(FZ == 0 || (!INT8 && !TQ), "the fused table build takes FP16 activations");
     constexpr int MT = MTK * NH;                  // tokens per workgroup
     // 128-blocks per chunk (b = 1 and 16 tokens: 16 KB of LDS per buffer, more workgroups per CU)
     constexpr int CH = (BITS == 1 || NH == 2) ? 1 : 4 / BITS;
-    constexpr int TASKS = CH * GPB * 4;           // staging tasks per chunk: (block, group, index pair)
+    // staging tasks per chunk: (block, group, index pair); with FZ (token slice, block,
+    // group, index pair), a slice being the 8 tokens of a half.  1-bit weights (one plane
+    // of lookups per chunk, so the build weighs most) take slices of 4 tokens where 8
+    // would leave half the lanes idle, so every lane shares the build (measured: 1.5 us
+    // faster at 4 and 8 tokens; with 4-bit weights 2 us slower)
+    constexpr int HT = CH * GPB * 4 * NH;         // FZ: (half, block, group, index pair) tasks
+    constexpr int TOK = (FZ && BITS == 1 && HT < 256) ? MTK * HT / 256 : MTK;  // FZ: tokens per task
+    constexpr int TASKS = FZ ? HT * (MTK / TOK) : CH * GPB * 4;
     constexpr int TPL = (TASKS + 255) / 256;      // staging tasks per lane
+    static_assert(FZ == 0 || (TPL == 1 && (TOK == 4 || TOK == 8)), "one fused staging task per lane");
     constexpr int GST = 256 * NH;                 // LDS bytes of one group (16 entries x 8 tokens x 2 B per half)
     constexpr int BUF = CH * GPB * GST;           // LDS bytes of one table buffer
-    // 16 KB (b = 1, 4, 8 tokens) or 32 KB.  Occupancy hints: b = 1 with 8 tokens keeps six
+    // 16 KB (b = 1, 4, 8 tokens) or 32 KB, plus with FZ = 2 the block sums of the K range
+    // (at most FZ_SMAX blocks).  Occupancy hints: b = 1 with 8 tokens keeps six
     // workgroups per CU; the others measured faster at four, where the scheduler keeps
     // more LDS reads in flight per wavefront
-    __shared__ __attribute__((aligned(16))) char F[2 * BUF];
+    __shared__ __attribute__((aligned(16))) char F[2 * BUF + (FZ == 2 ? FZ_SMAX * MT * 4 : 0)];
 
     const int tid = threadIdx.x;
     const Tile tl = tile_of(blockIdx.x, (uint32_t)n_tiles, (uint32_t)m_tiles, order);
@@ -237,10 +285,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(TQ ? 1 : (B
     const int64_t J = p.J;
     const uint32_t rows_live = (uint32_t)((p.M - m0) < MT ? (p.M - m0) : MT);
     constexpr uint32_t TB = TQ ? 8 : 16;  // bytes per stored half table
-    const __amdgpu_buffer_rsrc_t rT = buf_rsrc((const char *)p.T + m0 * J * TB, rows_live * (uint32_t)J * TB);
+    // (FZ: the tile's activation rows instead of its tables)
+    const __amdgpu_buffer_rsrc_t rT = FZ ? buf_rsrc(p.act + m0 * p.K, rows_live * (uint32_t)p.K * 2u)
+                                         : buf_rsrc((const char *)p.T + m0 * J * TB, rows_live * (uint32_t)J * TB);
     const __amdgpu_buffer_rsrc_t rTs = buf_rsrc(TQ ? (const void *)(p.tsc + m0 * J) : (const void *)p.T,
                                                 TQ ? rows_live * (uint32_t)J * 4u : 0u);
-    const __amdgpu_buffer_rsrc_t rS = buf_rsrc((const float *)p.S + m0 * p.Q, rows_live * (uint32_t)p.Q * 4u);
+    const __amdgpu_buffer_rsrc_t rS = FZ ? buf_rsrc(nullptr, 0u)
+                                         : buf_rsrc((const float *)p.S + m0 * p.Q, rows_live * (uint32_t)p.Q * 4u);
     const uint32_t n_meta = p.per_tensor ? 0u : n;  // metadata column (0: one pair per tensor)
     // quantization group of a 128-block (workgroup-uniform: moved to a scalar register,
     // so that what depends on it is scalar arithmetic)
@@ -248,9 +299,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(TQ ? 1 : (B
         return __builtin_amdgcn_readfirstlane((int)(((float)kb + 0.5f) * p.inv_kpg));
     };
     // staged table words: entries 2ip, 2ip + 1 of a token's half table (FP16 / INT16
-    // pair), or with INT8-quantized tables (TQ) their two codes and the table's scale
-    typedef std::conditional_t<TQ, uint2, uint32_t> SDE;
-    typedef SDE SD[TPL][MT];
+    // pair), or with INT8-quantized tables (TQ) their two codes and the table's scale;
+    // FZ: the 4 FP16 activations of the task's group, for the 8 tokens of its half
+    typedef std::conditional_t<TQ || FZ, uint2, uint32_t> SDE;
+    typedef SDE SD[TPL][FZ ? TOK : MT];
     typedef uint4 WW[CH][BITS];
     struct MW {
         uint2 w[CH];  // metadata words of each block's group
@@ -259,6 +311,21 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(TQ ? 1 : (B
     typedef float SV[1];
     auto load = [&](int kc, SD &sd, WW &w, MW &mw, SV &sv) {
         const int nkb = (kbB - kc) < CH ? (kbB - kc) : CH;
+        if constexpr (FZ) {
+            // task (token slice q, block kbl, group g, index pair ip), ip fastest; q and
+            // kbl are uniform over a wavefront, so the row and block offsets are scalar
+            // (lanes past the tasks load rows past the tile: clamped, or zero from the
+            // buffer's extent, and never staged)
+            const int q = __builtin_amdgcn_readfirstlane(tid / (CH * 128));
+            const int kbl = __builtin_amdgcn_readfirstlane((tid / 128) % CH);
+            const int kbc = kbl < nkb ? kbl : nkb - 1;
+            const uint32_t g = (uint32_t)((tid >> 2) & 31);
+#pragma unroll
+            for (int t = 0; t < TOK; ++t) {
+                const uint32_t so = (uint32_t)(row_of(TOK * q + t) - m0) * (uint32_t)p.K * 2u + (uint32_t)(kc + kbc) * 256u;
+                sd[0][t] = buf_u64(rT, g * 8u, so);
+            }
+        } else {
 #pragma unroll
         for (int r = 0; r < TPL; ++r) {
             const int task = tid + 256 * r;
@@ -274,6 +341,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(TQ ? 1 : (B
                 else
                     sd[r][t] = buf_u32(rT, tab * 16 + ip * 4, so);
             }
+        }
         }
         const __amdgpu_buffer_rsrc_t rW =
             buf_rsrc(p.planes + (int64_t)kc * BITS * p.N_pad, (uint32_t)(CH * BITS) * (uint32_t)p.N_pad * 16u);
@@ -295,12 +363,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(TQ ? 1 : (B
                 mw.q[kbl] = q;
             }
             // one activation sum per (block, token): lanes 0 .. MT CH - 1 of every wavefront,
-            // broadcast to the others by readlane
-            const int ln = tid & 63;
-            const int t = ln % MT;
-            const int q = (CH == 1 || ln < MT) ? mw.q[0] : mw.q[CH - 1];
-            const uint32_t rt = (uint32_t)(row_of(t) - m0);
-            sv[0] = __uint_as_float(buf_u32(rS, (rt * (uint32_t)p.Q + (uint32_t)q) * 4u, 0));
+            // broadcast to the others by readlane (FZ: the block sums are in LDS)
+            if constexpr (!FZ) {
+                const int ln = tid & 63;
+                const int t = ln % MT;
+                const int q = (CH == 1 || ln < MT) ? mw.q[0] : mw.q[CH - 1];
+                const uint32_t rt = (uint32_t)(row_of(t) - m0);
+                sv[0] = __uint_as_float(buf_u32(rS, (rt * (uint32_t)p.Q + (uint32_t)q) * 4u, 0));
+            }
         }
     };
 
@@ -311,11 +381,62 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(TQ ? 1 : (B
         yf[t] = 0.f;
         yi[t] = 0;
     }
+    // FZ: lane l holds the scale 2^-e and the output factor 2^e of token l % MT
+    float escl = 1.f, etok = 1.f;
 
     auto process = [&](int kc, const SD &sd, const WW &w, const MW &mw, const SV &sv, int b) {
         const int nkb = (kbB - kc) < CH ? (kbB - kc) : CH;
         char *Fb = F + b * BUF;
         // stage: for each task, entries 2ip, 2ip + 1 and their negations for the 8 tokens
+        if constexpr (FZ) {
+            // the two entries formed here from the activations: T[2ip + s] =
+            // ((-x0 + (+-x1)) + (+-x2)) + (+-x3), x1 added when bit 2 of 2ip is set, x2
+            // when bit 1 is, x3 subtracted for s = 0 and added for s = 1; the signs of x1
+            // and x2 are applied by flipping the FP16 sign bits, x_e = a_e 2^-e exactly
+            const int q = __builtin_amdgcn_readfirstlane(tid / (CH * 128));
+            const int kbl = (tid / 128) % CH, g = (tid >> 2) & 31, ip = tid & 3;
+            if (tid < TASKS && kbl < nkb) {
+                const uint32_t f1 = (ip & 2) ? 0u : 0x80000000u, f2 = (ip & 1) ? 0u : 0x8000u;
+                uint32_t r0[TOK / 2], r1[TOK / 2];
+#pragma unroll
+                for (int t = 0; t < TOK; ++t) {
+                    const float sc = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(escl), TOK * q + t));
+                    const uint32_t ax = sd[0][t].x ^ f1, ay = sd[0][t].y ^ f2;
+                    const float nx0 = fmaf(h2f(ax & 0xFFFFu), -sc, -0.0f);  // -x0, exact (and -0 for +0)
+                    const float bb = fmaf(h2f(ax >> 16), sc, nx0);
+                    const float u = fmaf(h2f(ay & 0xFFFFu), sc, bb);
+                    const float x3 = h2f(ay >> 16);
+                    float t0 = fmaf(-x3, sc, u), t1 = fmaf(x3, sc, u);
+                    // rounded to FP32 first, then to FP16 (not one fused FMA-to-FP16 rounding)
+                    asm volatile("" : "+v"(t0), "+v"(t1));
+                    const uint32_t q0 = __half_as_ushort(__float2half_rn(t0));
+                    const uint32_t q1 = __half_as_ushort(__float2half_rn(t1));
+                    if (t & 1) {
+                        r0[t / 2] |= q0 << 16;
+                        r1[t / 2] |= q1 << 16;
+                    } else {
+                        r0[t / 2] = q0;
+                        r1[t / 2] = q1;
+                    }
+                }
+                // slice q: half (TOK q) / 8 of the row, at token (TOK q) % 8 within it
+                char *row = Fb + (kbl * GPB + g) * GST + 256 * (TOK * q / MTK) + 2 * (TOK * q % MTK);
+                if constexpr (TOK == MTK) {
+                    const uint4 e0 = make_uint4(r0[0], r0[1], r0[2], r0[3]), e1 = make_uint4(r1[0], r1[1], r1[2], r1[3]);
+                    *(uint4 *)(row + (2 * ip) * 16) = e0;
+                    *(uint4 *)(row + (2 * ip + 1) * 16) = e1;
+                    *(uint4 *)(row + (2 * ip + 8) * 16) =
+                        make_uint4(neg16x2<false>(e0.x), neg16x2<false>(e0.y), neg16x2<false>(e0.z), neg16x2<false>(e0.w));
+                    *(uint4 *)(row + (2 * ip + 9) * 16) =
+                        make_uint4(neg16x2<false>(e1.x), neg16x2<false>(e1.y), neg16x2<false>(e1.z), neg16x2<false>(e1.w));
+                } else {
+                    *(uint2 *)(row + (2 * ip) * 16) = make_uint2(r0[0], r0[1]);
+                    *(uint2 *)(row + (2 * ip + 1) * 16) = make_uint2(r1[0], r1[1]);
+                    *(uint2 *)(row + (2 * ip + 8) * 16) = make_uint2(neg16x2<false>(r0[0]), neg16x2<false>(r0[1]));
+                    *(uint2 *)(row + (2 * ip + 9) * 16) = make_uint2(neg16x2<false>(r1[0]), neg16x2<false>(r1[1]));
+                }
+            }
+        } else {
 #pragma unroll
         for (int r = 0; r < TPL; ++r) {
             const int task = tid + 256 * r;
@@ -354,6 +475,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(TQ ? 1 : (B
                         make_uint4(neg16x2<INT8>(e1.x), neg16x2<INT8>(e1.y), neg16x2<INT8>(e1.z), neg16x2<INT8>(e1.w));
                 }
             }
+        }
         }
         lds_barrier();
 #pragma unroll
@@ -442,8 +564,15 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(TQ ? 1 : (B
                         }
                     }
                 }
-                // the zero-point term enters with the first block of each group only
-                if (need_s && kc + kbl == mw.q[kbl] * p.kpg) {
+                if constexpr (FZ == 2) {  // the zero-point term of this block, from its sums in LDS
+                    if (need_s) {
+                        const float nspz = -(sz.sp * sz.zp);
+                        const float *sb = (const float *)(F + 2 * BUF) + (kc + kbl - kbA) * MT;
+#pragma unroll
+                        for (int t = 0; t < MT; ++t) yf[t] = fmaf(nspz, sb[t], yf[t]);
+                    }
+                } else if (need_s && kc + kbl == mw.q[kbl] * p.kpg) {
+                    // the zero-point term enters with the first block of each group only
                     const float nspz = -(sz.sp * sz.zp);
 #pragma unroll
                     for (int t = 0; t < MT; ++t) {
@@ -466,6 +595,65 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(TQ ? 1 : (B
     MW mwA, mwB;
     SV svA, svB;
     load(kbA, sdA, wA, mwA, svA);
+    if constexpr (FZ) {
+        // absmax of each token over this workgroup's K range (FZ = 2: and the sum of each
+        // 128-block), LPT lanes per token and 16 bytes per lane and block, eight loads in
+        // flight (issued after the first chunk's, whose latency they share)
+        constexpr int LPT = 256 / MT;  // 16 or 32
+        constexpr int BPS = LPT / 16;  // 128-blocks per step
+        const int t = tid / LPT, sub = tid % LPT;
+        const uint32_t rowoff = (uint32_t)(row_of(t) - m0) * (uint32_t)p.K * 2u + (uint32_t)(sub & 15) * 16u;
+        float *sl = (float *)(F + 2 * BUF);
+        uint32_t mx = 0u;  // two FP16 magnitudes (the bits of a finite |a| order like integers)
+        for (int i0 = 0; i0 < kbB - kbA; i0 += 8 * BPS) {
+            uint4 v[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+                const int kb = kbA + i0 + u * BPS + (sub >> 4);
+                v[u] = buf_u128(rT, rowoff + (uint32_t)(kb < kbB ? kb : kbB - 1) * 256u, 0);
+            }
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+                mx = max_u16x2(mx, max_u16x2(max_u16x2(v[u].x & 0x7FFF7FFFu, v[u].y & 0x7FFF7FFFu),
+                                             max_u16x2(v[u].z & 0x7FFF7FFFu, v[u].w & 0x7FFF7FFFu)));
+                if constexpr (FZ == 2) {
+                    const uint32_t d[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
+                    float sm = 0.f;
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) sm = (sm + h2f(d[i] & 0xFFFFu)) + h2f(d[i] >> 16);
+                    sm = row_sum16(sm);
+                    const int kb = kbA + i0 + u * BPS + (sub >> 4);
+                    if ((sub & 15) == 0 && kb < kbB && kb - kbA < FZ_SMAX) sl[(kb - kbA) * MT + t] = sm;
+                }
+            }
+        }
+        uint32_t m16 = (mx & 0xFFFFu) > (mx >> 16) ? (mx & 0xFFFFu) : (mx >> 16);
+#pragma unroll
+        for (int off = 1; off < LPT; off <<= 1) {
+            const uint32_t o = (uint32_t)__shfl_xor((int)m16, off, 64);
+            m16 = o > m16 ? o : m16;
+        }
+        float *xs = (float *)(F + BUF);  // scale and factor per token, in the second table buffer
+        if (sub == 0) {
+            const float amax = h2f(m16);
+            float sc = 1.f, tk = 1.f;
+            if (amax != 0.f) {
+                int e2;
+                (void)frexpf(amax, &e2);
+                sc = ldexpf(1.f, -e2);
+                tk = ldexpf(1.f, e2);
+            }
+            xs[t] = sc;
+            xs[MT + t] = tk;
+        }
+        lds_barrier();
+        if constexpr (FZ == 2) {  // the block sums of the scaled activations (exact rescaling)
+            for (int i = tid; i < (kbB - kbA) * MT && i < FZ_SMAX * MT; i += 256) sl[i] *= xs[i % MT];
+        }
+        escl = xs[tid % MT];
+        etok = xs[MT + tid % MT];
+        if constexpr (FZ == 2) lds_barrier();
+    }
     for (int kc = kbA; kc < kbB; kc += 2 * CH) {
         load(kc + CH < last ? kc + CH : last, sdB, wB, mwB, svB);
         process(kc, sdA, wA, mwA, svA, 0);
@@ -478,13 +666,20 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(TQ ? 1 : (B
     if (p.splits == 1) {
 #pragma unroll
         for (int t = 0; t < MT; ++t)
-            if (t < rows) store_out<INT8>(p, wfmt, m0 + t, n, yf[t], yi[t], load_epi<INT8>(p, wfmt, m0 + t, n, false));
+            if (t < rows) {
+                Epi ep = load_epi<INT8>(p, wfmt, m0 + t, n, false);
+                if constexpr (FZ != 0) ep.tok = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(etok), t));
+                store_out<INT8>(p, wfmt, m0 + t, n, yf[t], yi[t], ep);
+            }
         return;
     }
     const int64_t m_alloc = m_tiles * MT;
 #pragma unroll
-    for (int t = 0; t < MT; ++t)  // the finalize kernel reads rows below M only
-        if (t < rows) p.part[((int64_t)split * m_alloc + m0 + t) * p.N_pad + n] = INT8 ? __int_as_float(yi[t]) : yf[t];
+    for (int t = 0; t < MT; ++t) {  // the finalize kernel reads rows below M only
+        // FZ: the partial times this K range's 2^e (the finalize kernel applies no factor)
+        const float v = FZ ? yf[t] * __int_as_float(__builtin_amdgcn_readlane(__float_as_int(etok), t)) : yf[t];
+        if (t < rows) p.part[((int64_t)split * m_alloc + m0 + t) * p.N_pad + n] = INT8 ? __int_as_float(yi[t]) : v;
+    }
 }
 
 template <int NH>
@@ -495,14 +690,26 @@ static void launch_mtok_nh(const LutParams &p, const Layout &L, const LutPlan &p
     const int64_t nt = plan.n_tiles, mt = plan.m_tiles;
     const int o = plan.order;
     if (L.bits == 1) {
-        if (i8) hipLaunchKernelGGL((lut_mtok_kernel<1, true, false, NH>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
-        else hipLaunchKernelGGL((lut_mtok_kernel<1, false, false, NH>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
+        if (i8) hipLaunchKernelGGL((lut_mtok_kernel<1, true, false, NH, 0>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
+        else hipLaunchKernelGGL((lut_mtok_kernel<1, false, false, NH, 0>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
     } else if (L.bits == 2) {
-        if (i8) hipLaunchKernelGGL((lut_mtok_kernel<2, true, false, NH>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
-        else hipLaunchKernelGGL((lut_mtok_kernel<2, false, false, NH>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
+        if (i8) hipLaunchKernelGGL((lut_mtok_kernel<2, true, false, NH, 0>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
+        else hipLaunchKernelGGL((lut_mtok_kernel<2, false, false, NH, 0>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
     } else {
-        hipLaunchKernelGGL((lut_mtok_kernel<4, false, false, NH>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
+        hipLaunchKernelGGL((lut_mtok_kernel<4, false, false, NH, 0>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
     }
+}
+
+// Tables built in the kernel from FP16 activations: FZ = 2 when the format has zero
+// points (the per-block activation sums are kept in LDS), else 1.
+template <int NH, int FZ>
+static void launch_mtok_fz(const LutParams &p, const Layout &L, const LutPlan &plan, hipStream_t s) {
+    const dim3 grid((unsigned)(plan.n_tiles * plan.m_tiles * plan.splits), 1, 1);
+    const int64_t nt = plan.n_tiles, mt = plan.m_tiles;
+    const int o = plan.order;
+    if (L.bits == 1) hipLaunchKernelGGL((lut_mtok_kernel<1, false, false, NH, FZ>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
+    else if (L.bits == 2) hipLaunchKernelGGL((lut_mtok_kernel<2, false, false, NH, FZ>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
+    else hipLaunchKernelGGL((lut_mtok_kernel<4, false, false, NH, FZ>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
 }
 
 int launch_mtok(const LutParams &p, const Layout &L, const LutPlan &plan, void *stream) {
@@ -511,13 +718,28 @@ int launch_mtok(const LutParams &p, const Layout &L, const LutPlan &plan, void *
         const dim3 grid((unsigned)(plan.n_tiles * plan.m_tiles * plan.splits), 1, 1);
         const int64_t nt = plan.n_tiles, mt = plan.m_tiles;
         const int o = plan.order;
-        if (L.bits == 1) hipLaunchKernelGGL((lut_mtok_kernel<1, false, true, 1>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
-        else if (L.bits == 2) hipLaunchKernelGGL((lut_mtok_kernel<2, false, true, 1>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
-        else hipLaunchKernelGGL((lut_mtok_kernel<4, false, true, 1>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
+        if (L.bits == 1) hipLaunchKernelGGL((lut_mtok_kernel<1, false, true, 1, 0>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
+        else if (L.bits == 2) hipLaunchKernelGGL((lut_mtok_kernel<2, false, true, 1, 0>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
+        else hipLaunchKernelGGL((lut_mtok_kernel<4, false, true, 1, 0>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
     } else if (plan.mt == 16) {
         launch_mtok_nh<2>(p, L, plan, s);
     } else {
         launch_mtok_nh<1>(p, L, plan, s);
+    }
+    return (int)hipGetLastError();
+}
+
+int launch_mtok_fused(const LutParams &p, const Layout &L, const LutPlan &plan, void *stream) {
+    hipStream_t s = (hipStream_t)stream;
+    if (L.act != LUTGEMM_ACT_FP16 || !p.act) return (int)hipErrorInvalidValue;
+    const bool zp = L.wfmt != LUTGEMM_WFMT_BINARY;
+    if (zp && plan.kbs > MTOK_FUSED_SMAX) return (int)hipErrorInvalidValue;  // the planner caps it
+    if (plan.mt == 16) {
+        if (zp) launch_mtok_fz<2, 2>(p, L, plan, s);
+        else launch_mtok_fz<2, 1>(p, L, plan, s);
+    } else {
+        if (zp) launch_mtok_fz<1, 2>(p, L, plan, s);
+        else launch_mtok_fz<1, 1>(p, L, plan, s);
     }
     return (int)hipGetLastError();
 }

@@ -53,6 +53,10 @@ constexpr int64_t CNT_MAX = (int64_t)(CNT_AREA / 4);
 // Largest K split the split-K GEMV completes inside the kernel (one batch of partial
 // loads by the last workgroup); longer splits are summed by the finalize kernel.
 constexpr int INKERNEL_MAX_SPLITS = 32;
+// Multi-token kernel with the table build fused in, for formats with zero points: the
+// per-128-block activation sums of a workgroup's K range stay in LDS, so a K range
+// holds at most this many blocks (the planner splits K further when it would not).
+constexpr int MTOK_FUSED_SMAX = 64;
 
 struct Layout {
     int64_t K, N, N_pad, KB, J, Q, G;  // G = group size (K when per-tensor)
@@ -132,7 +136,9 @@ struct LutPlan {
     size_t part_off;  // byte offset of the split partial sums in the workspace (counters at 0)
 };
 
-LutPlan plan_lut(const Layout &L, int64_t M);
+// fused: the plan of lutgemm_mpgemm_fused (the multi-token kernel that builds its tables
+// from the activations keeps a K range within MTOK_FUSED_SMAX blocks for zero-point formats)
+LutPlan plan_lut(const Layout &L, int64_t M, bool fused = false);
 
 // Current value of planner override `key` (LUTGEMM_TUNE_*, see lutgemm_set_tuning).
 int tuning(int key);
@@ -216,6 +222,8 @@ int launch_fused_gemv(const LutParams &p, const Layout &L, const LutPlan &plan, 
 int launch_fused_split(const LutParams &p, const Layout &L, const LutPlan &plan, void *stream);
 int launch_finalize(const LutParams &p, const Layout &L, const LutPlan &plan, void *stream);
 int launch_mtok(const LutParams &p, const Layout &L, const LutPlan &plan, void *stream);
+// The multi-token kernel building its tables from the FP16 activations (p.act).
+int launch_mtok_fused(const LutParams &p, const Layout &L, const LutPlan &plan, void *stream);
 int launch_tri(const LutParams &p, const Layout &L, bool fused, void *stream);
 int launch_dequant(const DequantParams &p, const Layout &L, const DequantPlan &plan, void *stream);
 

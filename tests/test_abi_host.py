@@ -212,6 +212,37 @@ def test_fused_entry_point_rejects_before_launch():
     assert L.fused_workspace_size(L.problem(1000, 64, 2, L.WFMT_UINT, 0), 1) == 0  # invalid problem
 
 
+def test_fused_multi_token_plan():
+    """lutgemm_mpgemm_fused with FP16 activations and M > 2: the multi-token kernel
+    builds its own tables (scratch: the partial sums only) for M <= 64 on layers of at
+    most 64 x 256 columns, else precompute + mpGEMM (scratch: tables too); the tuning
+    key forces either; zero-point formats keep K ranges within 64 blocks."""
+    def tables_in_scratch(p, M):  # the two-call layout: [workspace, 256-aligned][tables]
+        ws = L.workspace_size(p, M)
+        return L.fused_workspace_size(p, M) == (ws + 255) // 256 * 256 + L.table_size(p, M)
+    small = L.problem(4096, 12288, 4, L.WFMT_UINT, 128)    # 48 column tiles
+    wide = L.problem(8192, 28672, 1, L.WFMT_BINARY, 8192)   # 112 column tiles
+    assert not tables_in_scratch(small, 8) and not tables_in_scratch(small, 64)
+    assert tables_in_scratch(small, 65) and tables_in_scratch(wide, 16)
+    assert L.fused_workspace_size(small, 8) == L.workspace_size(small, 8)
+    old = L.get_tuning("MT_FUSED")
+    try:
+        L.set_tuning("MT_FUSED", 1)
+        assert not tables_in_scratch(wide, 16) and not tables_in_scratch(small, 300)
+        L.set_tuning("MT_FUSED", 0)
+        assert tables_in_scratch(small, 8)
+        # INT4 K = 11008 (86 blocks), no split planned for the table-fed kernel at M = 2048:
+        # the fused build splits K so that every range holds at most 64 blocks
+        L.set_tuning("MT_FUSED", 1)
+        k = L.problem(11008, 4096, 4, L.WFMT_UINT, 128)
+        assert L.fused_workspace_size(k, 2048) > 0 and L.workspace_size(k, 2048) == 0
+    finally:
+        L.set_tuning("MT_FUSED", old)
+    # INT8 activations with several tokens always take the two-call path
+    pi = L.problem(4096, 4096, 2, L.WFMT_TERNARY, 0, L.ACT_INT8, True)
+    assert tables_in_scratch(pi, 8)
+
+
 def test_tuning_overrides():
     """Planner overrides go through lutgemm_set_tuning (no entry point reads the
     environment per call): unknown keys and out-of-range values are rejected, -1

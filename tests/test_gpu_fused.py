@@ -6,8 +6,8 @@ path (lutgemm_precompute + lutgemm_mpgemm) bitwise.  Cases cover one and two
 tokens, a single K chunk, several K chunks (K = 11008), K split across
 workgroups (few columns), ragged column tails, every weight format, accumulate,
 determinism, the zero token, the split-K kernel that builds FP32 tables from the
-activations (large FP16-activation layers), and the fallback to the two-call path
-(M > 2, INT8 activations with large weights).
+activations (large FP16-activation layers), and the two-call path behind the same
+entry point (INT8 activations with M > 2 or large weights).
 """
 import numpy as np
 import pytest
@@ -86,7 +86,10 @@ def test_fused_formats_and_groups(wfmt, bits, G, act):
 
 
 def test_fused_fallback_paths():
-    banner("fused entry point on shapes it does not fuse (M > 2, large weights)")
+    """M = 5 with FP16 activations takes the multi-token kernel with its own table
+    build (tests/test_gpu_fused_mtok.py covers it in depth); INT8 activations with
+    M > 2 run precompute + mpGEMM behind the same entry point."""
+    banner("fused entry point: M = 5 FP16 (multi-token build), INT8 M = 6 (two-call path)")
     gp = GpuProblem(W.make_inputs(3, 0, M=5, K=2048, N=700))
     check_fused(gp, what="M=5")
     gpi = GpuProblem(W.make_custom(W.WFMT_TERNARY, 2, 0, W.ACT_INT8, M=6, K=2048, N=300, seed=93, scale_fp32=True))
