@@ -103,6 +103,37 @@ __device__ __forceinline__ int wave_sum_i(int v) {
     v += dpp_i<0x143, 0xC>(v);
     return v;
 }
+// v(l) + v(l ^ OFF) for OFF = 16 or 32 in every lane, by the gfx950 lane-swap
+// instructions (v_permlane16_swap_b32 exchanges the odd 16-lane rows of one register
+// with the even rows of another, v_permlane32_swap_b32 the two halves): vector ALU
+// work, no LDS round trip as a shuffle through ds_bpermute has.  Both lanes of a pair
+// add the lower lane's value and the upper lane's in that order (identical bits).
+template <int OFF>
+__device__ __forceinline__ uint32_t xor_swap_pair(uint32_t v, uint32_t *hi) {
+    static_assert(OFF == 16 || OFF == 32, "lane-swap distance");
+    if constexpr (OFF == 16) {
+        const auto r = __builtin_amdgcn_permlane16_swap(v, v, false, false);
+        *hi = r[1];
+        return r[0];
+    } else {
+        const auto r = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+        *hi = r[1];
+        return r[0];
+    }
+}
+template <int OFF>
+__device__ __forceinline__ int xor_sum_i(int v) {
+    uint32_t hi;
+    const uint32_t lo = xor_swap_pair<OFF>((uint32_t)v, &hi);
+    return (int)lo + (int)hi;
+}
+template <int OFF>
+__device__ __forceinline__ float xor_sum_f(float v) {
+    uint32_t hi;
+    const uint32_t lo = xor_swap_pair<OFF>(__float_as_uint(v), &hi);
+    return __uint_as_float(lo) + __uint_as_float(hi);
+}
+
 // Maximum over the 64 lanes (any order gives the same result); in lane 63.
 __device__ __forceinline__ float wave_max(float v) {
     v = fmaxf(v, dpp_f<0x111, 0xF>(v));

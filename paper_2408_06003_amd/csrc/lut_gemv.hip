@@ -138,13 +138,16 @@ __global__ __launch_bounds__(64 * NW) void lut_gemv2_kernel(LutParams p, int wfm
     }
 
     tl_stamp(p, 3);
-    // combine the lanes of each column (fixed butterfly), then the wavefronts in order
-#pragma unroll
-    for (int off = CW; off < 64; off <<= 1) {
-        if (INT8)
-            yi += __shfl_xor(yi, off, 64);
-        else
-            yf += __shfl_xor(yf, off, 64);
+    // combine the lanes of each column (fixed butterfly by lane swaps), then the
+    // wavefronts in order
+    static_assert(CW == 16 || CW == 32 || CW == 64, "lane decompositions of 16, 32 or 64 columns");
+    if constexpr (CW <= 16) {
+        if (INT8) yi = xor_sum_i<16>(yi);
+        else yf = xor_sum_f<16>(yf);
+    }
+    if constexpr (CW <= 32) {
+        if (INT8) yi = xor_sum_i<32>(yi);
+        else yf = xor_sum_f<32>(yf);
     }
     if (lane < CW) {
         redf[wave][lane] = yf;

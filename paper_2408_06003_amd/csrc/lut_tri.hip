@@ -291,12 +291,10 @@ __global__ __launch_bounds__(64 * NW) void lut_tri_kernel(LutParams p, int wfmt,
     // slices of the wavefront (lanes c, c + 16, c + 32, c + 48), then wavefronts in order
     if (INT8) {
         int a = (int)(ai - 32768u * nlook);
-        a += __shfl_xor(a, 16, 64);
-        a += __shfl_xor(a, 32, 64);
+        a = xor_sum_i<32>(xor_sum_i<16>(a));
         if (lane < TRI_CW) redi[wave][c] = a;
     } else {
-        af += __shfl_xor(af, 16, 64);
-        af += __shfl_xor(af, 32, 64);
+        af = xor_sum_f<32>(xor_sum_f<16>(af));
         if (lane < TRI_CW) redf[wave][c] = af;
     }
     lds_barrier();
