@@ -184,6 +184,7 @@ __global__ __launch_bounds__(64 * NW) void lut_fused_gemv_kernel(LutParams p, in
         scale = ldexpf(1.f, -e2);
         tok = ldexpf(1.f, e2);
     }
+    asm volatile("" : "+v"(tok));  // formed here, not sunk by the compiler into the tail
 
     float yf = 0.f;
     int yi = 0;
@@ -233,6 +234,10 @@ __global__ __launch_bounds__(64 * NW) void lut_fused_gemv_kernel(LutParams p, in
                 mwd[t] = load_meta_words(p, q, lane_value(n));
             }
         }
+        if (INT8 && need_s && kc + CK >= kbB) {  // the activation sum of this wavefront, before the lookups
+            const int hs = wave_sum_i(s_tot);
+            if (lane == 63) hsi[wave] = hs;
+        }
         lds_barrier();
         tl_stamp(p, 2);
 #pragma unroll
@@ -259,10 +264,6 @@ __global__ __launch_bounds__(64 * NW) void lut_fused_gemv_kernel(LutParams p, in
     tl_stamp(p, 3);
     ep.tok = tok;
     if (p.tok_out && blockIdx.x == 0 && split == 0 && tid == 0) p.tok_out[m] = tok;
-    if (INT8 && need_s) {  // the activation sum of this workgroup's K range, per wavefront
-        const int hs = wave_sum_i(s_tot);
-        if (lane == 63) hsi[wave] = hs;
-    }
 
     // combine the lanes of each column (fixed butterfly by lane swaps), then the
     // wavefronts in order
