@@ -267,17 +267,19 @@ size_t lutgemm_fused_workspace_size(const lutgemm_problem_t *problem, int64_t M)
  * lutgemm_precompute + lutgemm_mpgemm, one kernel; with larger weights and
  * ACT_FP16 the split-K kernel, whose tables are exact FP32 sums of the
  * activations as given (no token scaling, no FP16 rounding of entries), plus the
- * split sum.  Several tokens (2 < M <= 64) with ACT_FP16 on layers of at most
+ * split sum; with larger weights and ACT_INT8 the same kernel, each workgroup
+ * reading the whole token for the absmax and building the exact INT16 entries of
+ * the precompute's quantization for its K range.  Several tokens (2 < M <= 64) with ACT_FP16 on layers of at most
  * 64 x 256 columns: the multi-token kernel reads the FP16 activations of its
  * tokens and K range, scales each token by the power of two 2^-e with e from its
  * absmax over that K range, and builds the same FP16 entries as
  * lutgemm_precompute (tuning key LUTGEMM_TUNE_MT_FUSED forces it on or off; every
  * column tile repeats the build, so beyond those sizes precompute + mpGEMM is
  * faster).  TERNARY_3IN5: one kernel for every M, tables built per workgroup for
- * its token.  Otherwise (larger M or N with ACT_FP16, ACT_INT8 with M > 2 or
- * larger weights, ACT_FP16_LUT8) it runs lutgemm_precompute into the workspace
- * followed by lutgemm_mpgemm; INT8 quantization needs the absmax of the whole
- * token, which a workgroup owning one K range does not see.
+ * its token.  Otherwise (larger M or N with ACT_FP16, ACT_INT8 with M > 2,
+ * ACT_FP16_LUT8) it runs lutgemm_precompute into the workspace followed by
+ * lutgemm_mpgemm: with several tokens every workgroup would have to read all of its
+ * tokens for the INT8 quantizer's absmax.
  *   act        device FP16 [M][K]
  *   packed, out, out_dtype, accumulate   as for lutgemm_mpgemm
  *   workspace  device, workspace_bytes >= lutgemm_fused_workspace_size(problem, M);

@@ -351,10 +351,11 @@ struct FusedScratch {
 static FusedScratch fused_scratch(const Layout &L, const LutPlan &plan, int64_t M) {
     FusedScratch f{};
     // INT8 table quantization exists to shrink the tables that travel through HBM, so
-    // that mode always takes the two-call path; the split-K GEMV builds its tables only
-    // on the FP path (INT8 quantization needs the whole token's absmax)
-    f.fused = ((plan.kind == 0 || plan.kind == 3) && L.act != LUTGEMM_ACT_FP16_LUT8) ||
-              ((plan.kind == 2 || (plan.kind == 1 && mtok_fused(L, M))) && L.act == LUTGEMM_ACT_FP16);
+    // that mode always takes the two-call path; with INT8 activations the split-K GEMV's
+    // workgroups read the whole token for the quantizer's absmax, while the multi-token
+    // kernel (several tokens, K split across workgroups) takes the two-call path
+    f.fused = ((plan.kind == 0 || plan.kind == 2 || plan.kind == 3) && L.act != LUTGEMM_ACT_FP16_LUT8) ||
+              (plan.kind == 1 && mtok_fused(L, M));
     if (f.fused && plan.kind == 1) {
         f.total = plan.ws_bytes;
     } else if (f.fused) {
@@ -551,9 +552,15 @@ lutgemm_status_t lutgemm_mpgemm_fused(const lutgemm_problem_t *problem, int64_t 
         if (e == 0 && plan.splits > 1) e = launch_finalize(lp, L, plan, stream);
         return hip_status(e);
     }
-    if (plan.kind == 2) {  // FP activations: tables from the activations, then the split sum
+    if (plan.kind == 2) {  // tables from the activations of each K range, then the split sum
+        // INT8: the kernel forms the token factor itself; the finalize kernel (long K
+        // splits) takes it from the workspace
+        lp.tok_out = (L.act == LUTGEMM_ACT_INT8 && plan.splits > 1) ? (float *)(ws + fs.tok_off) : nullptr;
         int e = launch_fused_split(lp, L, plan, stream);
-        if (e == 0 && plan.splits > 1 && !plan.inkernel) e = launch_finalize(lp, L, plan, stream);
+        if (e == 0 && plan.splits > 1 && !plan.inkernel) {
+            lp.tok = lp.tok_out;
+            e = launch_finalize(lp, L, plan, stream);
+        }
         return hip_status(e);
     }
     lp.tok_out = plan.splits > 1 ? (float *)(ws + fs.tok_off) : nullptr;

@@ -134,6 +134,14 @@ __device__ __forceinline__ float xor_sum_f(float v) {
     return __uint_as_float(lo) + __uint_as_float(hi);
 }
 
+// Lane-wise maximum of two packed unsigned 16-bit pairs (v_pk_max_u16); on the bits of
+// FP16 magnitudes (sign cleared) it is the maximum magnitude of finite values.
+__device__ __forceinline__ uint32_t max_u16x2(uint32_t a, uint32_t b) {
+    typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
+    return __builtin_bit_cast(uint32_t,
+                              __builtin_elementwise_max(__builtin_bit_cast(u16x2, a), __builtin_bit_cast(u16x2, b)));
+}
+
 // Maximum over the 64 lanes (any order gives the same result); in lane 63.
 __device__ __forceinline__ float wave_max(float v) {
     v = fmaxf(v, dpp_f<0x111, 0xF>(v));
@@ -462,7 +470,7 @@ __device__ __forceinline__ uint4 ld_nt(const uint4 *p) {
 // ternary group sum.
 template <bool INT8>
 __device__ __forceinline__ void split_complete(const LutParams &p, int wfmt, int64_t m, int64_t n, int split,
-                                               float yf, int yi, uint32_t *counter) {
+                                               float yf, int yi, uint32_t *counter, float tok = -1.f) {
     __shared__ int is_last;
     float *part = p.part + m * p.N_pad + n;
     const int64_t stride = p.M * p.N_pad;
@@ -493,7 +501,8 @@ __device__ __forceinline__ void split_complete(const LutParams &p, int wfmt, int
         const int sp = j < p.splits ? j : p.splits - 1;
         v[j] = __hip_atomic_load(part + sp * stride, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
-    const Epi ep = load_epi<INT8>(p, wfmt, m, n, false);
+    Epi ep = load_epi<INT8>(p, wfmt, m, n, false);
+    if (tok >= 0.f) ep.tok = tok;  // a token factor the calling kernel formed itself
     float sf = 0.f;
     int si = 0;
 #pragma unroll

@@ -335,48 +335,78 @@ static void launch_fused_bits(const LutParams &p, const Layout &L, const LutPlan
     }
 }
 
-// ---------------------------------------------------------------- split-K, FP activations
+// ---------------------------------------------------------------- split-K
 //
 // The split-K GEMV of lut_gemv.hip (256 columns per workgroup, one per lane, KBS
-// 128-blocks of K per workgroup, partial sums summed by the finalize kernel) with
-// its tables built from the FP16 activations of its own K range instead of read
-// from the precompute.  The FP path's power-of-two token scaling only keeps FP16
-// table entries in range, so it is not needed here: each lane builds the signed
-// 16-entry table of one 4-activation group in FP32 (entries
-// ((-x0 + (+-x1)) + (+-x2)) + (+-x3) of the activations as given, the negated half
-// by Eq. 4), without the FP16 rounding of stored tables, and a lookup adds the
-// FP32 entry.  The zero-point term of Eq. 3 is applied per 128-block (the sum over
-// a group's blocks of s'_q z'_q S_kb is s'_q z'_q S_q), with S_kb summed in a fixed
-// order over the 32 lanes that built the block's tables.
-template <int BITS, int KBS, int PRE>
+// 128-blocks of K per workgroup, the split completed in the kernel or by the
+// finalize kernel) with its tables built from the activations of its own K range
+// instead of read from the precompute; each lane builds the signed 16-entry table
+// of one 4-activation group (the negated half by Eq. 4).
+// FP path: the power-of-two token scaling only keeps FP16 table entries in range,
+// so it is not needed here: entries ((-x0 + (+-x1)) + (+-x2)) + (+-x3) of the
+// activations as given, in FP32, without the FP16 rounding of stored tables; a
+// lookup adds the FP32 entry; the zero-point term of Eq. 3 is applied per 128-block
+// (the sum over a group's blocks of s'_q z'_q S_kb is s'_q z'_q S_q), with S_kb
+// summed in a fixed order over the 32 lanes that built the block's tables.
+// INT8 path: the quantization needs the absmax of the whole token, so every
+// workgroup first reads the whole token (16 bytes per lane and load, four loads in
+// flight; the token stays in L2) and forms the same scale 127 / amax and factor
+// amax / 127 as the precompute operator, then the exact INT32 entries of its
+// quantized group; the ternary offset S is summed over the workgroup's K range
+// (the ranges' sums add up to the token's).  Lookups and the split sum are exact,
+// so the output equals the two-call path's bit for bit.
+template <int BITS, int KBS, int PRE, bool INT8>
 __global__ __launch_bounds__(256) void lut_fused_split_kernel(LutParams p, int wfmt) {
     constexpr int NWD = KBS * BITS;              // weight words per lane
     constexpr int NPRE = PRE < NWD ? PRE : NWD;  // of which issued before the table build
     constexpr int GS = 16;                 // entries per signed table
-    constexpr int BLKF = (GPB + 1) * GS;   // floats per 128-block (padded by one table)
-    __shared__ __attribute__((aligned(16))) float F[KBS * BLKF];
-    __shared__ float Sblk[KBS];
+    constexpr int BLKF = (GPB + 1) * GS;   // 32-bit entries per 128-block (padded by one table)
+    __shared__ __attribute__((aligned(16))) float F[KBS * BLKF];  // FP32 entries, or INT32 bits
+    __shared__ float Sblk[KBS];                                   // FP32 sums, or INT32 bits
+    __shared__ float wmx[4];                                      // INT8: the wavefronts' absmax
     tl_stamp(p, 0);
-    const int tid = threadIdx.x;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int64_t n = (int64_t)blockIdx.x * NTILE + tid;
     const int split = blockIdx.y;
     const int64_t m = blockIdx.z;
     const int64_t kb0 = (int64_t)split * KBS;
     const int nkb = (int)((p.KB - kb0) < KBS ? (p.KB - kb0) : KBS);
-    const bool need_s = wfmt != LUTGEMM_WFMT_BINARY;
+    // FP path: zero-point term of every format but binary; INT8 path: ternary offset
+    const bool need_s = INT8 ? wfmt == LUTGEMM_WFMT_TERNARY : wfmt != LUTGEMM_WFMT_BINARY;
 
     // conditional loads first, then unconditional clamped ones (see lut_gemv_kernel)
     Epi ep{};
-    if (p.splits == 1) ep = load_epi<false>(p, wfmt, m, n, true);
+    if (p.splits == 1) ep = load_epi<INT8>(p, wfmt, m, n, false);
     // activations: lane g holds group g of the workgroup's range (KBS x 32 <= 256 groups)
+    const uint16_t *arow = p.act + m * p.K;
     const int g = tid, gc = g < nkb * GPB ? g : nkb * GPB - 1;
-    const uint2 av = ((const uint2 *)(p.act + m * p.K))[kb0 * GPB + gc];
-    uint2 mw[KBS];
+    const uint2 av = ((const uint2 *)arow)[kb0 * GPB + gc];
+    // INT8 path: the whole token for its absmax (clamped duplicates do not change a max)
+    uint32_t mx = 0u;
+    if constexpr (INT8) {
+        const uint4 *a8 = (const uint4 *)arow;
+        const int64_t n8 = p.K / 8;
+        for (int64_t c = tid; c < n8; c += 4 * 256) {
+            uint4 v[4];
 #pragma unroll
-    for (int kbl = 0; kbl < KBS; ++kbl) {
-        const int kbc = kbl < nkb ? kbl : nkb - 1;
-        const int q = (int)(((float)(kb0 + kbc) + 0.5f) * p.inv_kpg);
-        mw[kbl] = load_meta_words(p, q, lane_value(n));
+            for (int u = 0; u < 4; ++u) {
+                const int64_t i = c + 256 * u;
+                v[u] = a8[i < n8 ? i : n8 - 1];
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+                mx = max_u16x2(mx, max_u16x2(max_u16x2(v[u].x & 0x7FFF7FFFu, v[u].y & 0x7FFF7FFFu),
+                                             max_u16x2(v[u].z & 0x7FFF7FFFu, v[u].w & 0x7FFF7FFFu)));
+        }
+    }
+    uint2 mw[KBS];
+    if constexpr (!INT8) {
+#pragma unroll
+        for (int kbl = 0; kbl < KBS; ++kbl) {
+            const int kbc = kbl < nkb ? kbl : nkb - 1;
+            const int q = (int)(((float)(kb0 + kbc) + 0.5f) * p.inv_kpg);
+            mw[kbl] = load_meta_words(p, q, lane_value(n));
+        }
     }
     // the first NPRE weight words now, the rest once the tables are built (as in the
     // table-fed split kernel: the activations are not queued behind the weight stream)
@@ -388,23 +418,65 @@ __global__ __launch_bounds__(256) void lut_fused_split_kernel(LutParams p, int w
 #pragma unroll
     for (int i = 0; i < NPRE; ++i) load_word(i);
 
-    // signed FP32 table of group g and the block sums
+    // INT8 path: token absmax (DPP within the wavefront, then the 4 wavefronts) and the
+    // precompute's quantizer
+    float scale = 1.f, tok = 1.f;
+    if constexpr (INT8) {
+        const uint32_t m16 = (mx & 0xFFFFu) > (mx >> 16) ? (mx & 0xFFFFu) : (mx >> 16);
+        const float wm = wave_max(h2f(m16));
+        if (lane == 63) wmx[wave] = wm;
+        lds_barrier();
+        const float amax = fmaxf(fmaxf(wmx[0], wmx[1]), fmaxf(wmx[2], wmx[3]));
+        scale = amax == 0.f ? 0.f : __fdiv_rn(127.0f, amax);
+        tok = amax == 0.f ? 0.f : __fdiv_rn(amax, 127.0f);
+        if (p.tok_out && blockIdx.x == 0 && split == 0 && tid == 0) p.tok_out[m] = tok;
+    }
+    auto qv = [&](uint32_t bits16) {  // r = clamp(rint(a * 127 / amax), -127, 127)
+        const float r = rintf(h2f(bits16) * scale);
+        return (int)fminf(fmaxf(r, -127.f), 127.f);
+    };
+
+    // signed table of group g and the block sums
     const float x0 = h2f(av.x & 0xFFFFu), x1 = h2f(av.x >> 16), x2 = h2f(av.y & 0xFFFFu), x3 = h2f(av.y >> 16);
+    int q0 = 0, q1 = 0, q2 = 0, q3 = 0;
+    if constexpr (INT8) {
+        q0 = qv(av.x & 0xFFFFu);
+        q1 = qv(av.x >> 16);
+        q2 = qv(av.y & 0xFFFFu);
+        q3 = qv(av.y >> 16);
+    }
     if (g < nkb * GPB) {
-        float t[8];
-#pragma unroll
-        for (int i = 0; i < 8; ++i) t[i] = ((-x0 + ((i & 4) ? x1 : -x1)) + ((i & 2) ? x2 : -x2)) + ((i & 1) ? x3 : -x3);
         float *dst = F + (g / GPB) * BLKF + (g % GPB) * GS;
-        *(float4 *)(dst + 0) = make_float4(t[0], t[1], t[2], t[3]);
-        *(float4 *)(dst + 4) = make_float4(t[4], t[5], t[6], t[7]);
-        *(float4 *)(dst + 8) = make_float4(-t[0], -t[1], -t[2], -t[3]);
-        *(float4 *)(dst + 12) = make_float4(-t[4], -t[5], -t[6], -t[7]);
+        if constexpr (INT8) {  // |entry| <= 508, exact
+            int t[8];
+#pragma unroll
+            for (int i = 0; i < 8; ++i) t[i] = ((-q0 + ((i & 4) ? q1 : -q1)) + ((i & 2) ? q2 : -q2)) + ((i & 1) ? q3 : -q3);
+            *(int4 *)(dst + 0) = make_int4(t[0], t[1], t[2], t[3]);
+            *(int4 *)(dst + 4) = make_int4(t[4], t[5], t[6], t[7]);
+            *(int4 *)(dst + 8) = make_int4(-t[0], -t[1], -t[2], -t[3]);
+            *(int4 *)(dst + 12) = make_int4(-t[4], -t[5], -t[6], -t[7]);
+        } else {
+            float t[8];
+#pragma unroll
+            for (int i = 0; i < 8; ++i) t[i] = ((-x0 + ((i & 4) ? x1 : -x1)) + ((i & 2) ? x2 : -x2)) + ((i & 1) ? x3 : -x3);
+            *(float4 *)(dst + 0) = make_float4(t[0], t[1], t[2], t[3]);
+            *(float4 *)(dst + 4) = make_float4(t[4], t[5], t[6], t[7]);
+            *(float4 *)(dst + 8) = make_float4(-t[0], -t[1], -t[2], -t[3]);
+            *(float4 *)(dst + 12) = make_float4(-t[4], -t[5], -t[6], -t[7]);
+        }
     }
     if (need_s) {  // S of block g / 32: fixed butterfly over its 32 lanes
-        float sg = g < nkb * GPB ? ((x0 + x1) + x2) + x3 : 0.f;
+        if constexpr (INT8) {
+            int sg = g < nkb * GPB ? (q0 + q1) + (q2 + q3) : 0;
 #pragma unroll
-        for (int off = 1; off < 32; off <<= 1) sg += __shfl_xor(sg, off, 64);
-        if ((tid & 31) == 0 && (tid >> 5) < KBS) Sblk[tid >> 5] = sg;
+            for (int off = 1; off < 32; off <<= 1) sg += __shfl_xor(sg, off, 64);
+            if ((tid & 31) == 0 && (tid >> 5) < KBS) Sblk[tid >> 5] = __int_as_float(sg);
+        } else {
+            float sg = g < nkb * GPB ? ((x0 + x1) + x2) + x3 : 0.f;
+#pragma unroll
+            for (int off = 1; off < 32; off <<= 1) sg += __shfl_xor(sg, off, 64);
+            if ((tid & 31) == 0 && (tid >> 5) < KBS) Sblk[tid >> 5] = sg;
+        }
     }
     lds_barrier();
     asm volatile("" ::: "memory");  // the remaining weight loads stay after the table build
@@ -413,70 +485,98 @@ __global__ __launch_bounds__(256) void lut_fused_split_kernel(LutParams p, int w
     for (int i = NPRE; i < NWD; ++i) load_word(i);
 
     float yf = 0.f;
+    int yi = 0;
 #pragma unroll
     for (int kbl = 0; kbl < KBS; ++kbl) {
         if (kbl < nkb) {
             float tot = 0.f;
+            int toti = 0;
 #pragma unroll
             for (int t = 0; t < BITS; ++t) {
                 const uint32_t wd[4] = {w[kbl][t].x, w[kbl][t].y, w[kbl][t].z, w[kbl][t].w};
                 float acc = 0.f;
+                int acci = 0;
 #pragma unroll
                 for (int d = 0; d < 4; ++d) {
                     const char *Fg = (const char *)(F + kbl * BLKF + d * 8 * GS);
                     const uint32_t lo = wd[d] << 2, hi = wd[d] >> 2;
-                    acc += *(const float *)(Fg + 0 * GS * 4 + idx4<0>(lo)) + *(const float *)(Fg + 1 * GS * 4 + idx4<0>(hi));
-                    acc += *(const float *)(Fg + 2 * GS * 4 + idx4<1>(lo)) + *(const float *)(Fg + 3 * GS * 4 + idx4<1>(hi));
-                    acc += *(const float *)(Fg + 4 * GS * 4 + idx4<2>(lo)) + *(const float *)(Fg + 5 * GS * 4 + idx4<2>(hi));
-                    acc += *(const float *)(Fg + 6 * GS * 4 + idx4<3>(lo)) + *(const float *)(Fg + 7 * GS * 4 + idx4<3>(hi));
+                    if constexpr (INT8) {
+                        acci += *(const int *)(Fg + 0 * GS * 4 + idx4<0>(lo)) + *(const int *)(Fg + 1 * GS * 4 + idx4<0>(hi));
+                        acci += *(const int *)(Fg + 2 * GS * 4 + idx4<1>(lo)) + *(const int *)(Fg + 3 * GS * 4 + idx4<1>(hi));
+                        acci += *(const int *)(Fg + 4 * GS * 4 + idx4<2>(lo)) + *(const int *)(Fg + 5 * GS * 4 + idx4<2>(hi));
+                        acci += *(const int *)(Fg + 6 * GS * 4 + idx4<3>(lo)) + *(const int *)(Fg + 7 * GS * 4 + idx4<3>(hi));
+                    } else {
+                        acc += *(const float *)(Fg + 0 * GS * 4 + idx4<0>(lo)) + *(const float *)(Fg + 1 * GS * 4 + idx4<0>(hi));
+                        acc += *(const float *)(Fg + 2 * GS * 4 + idx4<1>(lo)) + *(const float *)(Fg + 3 * GS * 4 + idx4<1>(hi));
+                        acc += *(const float *)(Fg + 4 * GS * 4 + idx4<2>(lo)) + *(const float *)(Fg + 5 * GS * 4 + idx4<2>(hi));
+                        acc += *(const float *)(Fg + 6 * GS * 4 + idx4<3>(lo)) + *(const float *)(Fg + 7 * GS * 4 + idx4<3>(hi));
+                    }
                 }
-                tot += acc * (float)(1 << t);  // exact scaling by the plane weight
+                if constexpr (INT8)
+                    toti += acci << t;  // exact: |sum| < 2^31
+                else
+                    tot += acc * (float)(1 << t);  // exact scaling by the plane weight
             }
-            const SZ sz = decode_sz(p, mw[kbl]);
-            yf = fmaf(sz.sp, tot, yf);
-            if (need_s) yf -= (sz.sp * sz.zp) * Sblk[kbl];
+            if constexpr (INT8) {
+                yi += toti;
+                if (need_s) yi += __float_as_int(Sblk[kbl]);  // ternary offset of this block
+            } else {
+                const SZ sz = decode_sz(p, mw[kbl]);
+                yf = fmaf(sz.sp, tot, yf);
+                if (need_s) yf -= (sz.sp * sz.zp) * Sblk[kbl];
+            }
         }
     }
     tl_stamp(p, 2);
-    if (p.splits == 1)
-        store_out<false>(p, wfmt, m, n, yf, 0, ep);
-    else if (p.cnt)
-        split_complete<false>(p, wfmt, m, n, split, yf, 0, p.cnt + m * gridDim.x + blockIdx.x);
-    else  // long K splits: lut_finalize_kernel adds the partials after this kernel
-        p.part[((int64_t)split * p.M + m) * p.N_pad + n] = yf;
+    if (p.splits == 1) {
+        ep.tok = tok;
+        store_out<INT8>(p, wfmt, m, n, yf, yi, ep);
+    } else if (p.cnt) {
+        split_complete<INT8>(p, wfmt, m, n, split, yf, yi, p.cnt + m * gridDim.x + blockIdx.x, INT8 ? tok : -1.f);
+    } else {  // long K splits: lut_finalize_kernel adds the partials after this kernel
+        p.part[((int64_t)split * p.M + m) * p.N_pad + n] = INT8 ? __int_as_float(yi) : yf;
+    }
     tl_stamp(p, 6);
 }
 
-template <int BITS, int PRE>
+template <int BITS, int PRE, bool INT8>
 static void launch_fused_split_pre(const LutParams &p, const Layout &L, const LutPlan &plan, hipStream_t s) {
     const dim3 grid((unsigned)(L.N_pad / NTILE), (unsigned)plan.splits, (unsigned)p.M);
     switch (plan.kbs) {  // the planner keeps KBS <= 8 / b (and KBS x 32 groups <= 256 lanes)
-    case 1: hipLaunchKernelGGL((lut_fused_split_kernel<BITS, 1, PRE>), grid, dim3(256), 0, s, p, L.wfmt); break;
-    case 2: hipLaunchKernelGGL((lut_fused_split_kernel<BITS, 2, PRE>), grid, dim3(256), 0, s, p, L.wfmt); break;
+    case 1: hipLaunchKernelGGL((lut_fused_split_kernel<BITS, 1, PRE, INT8>), grid, dim3(256), 0, s, p, L.wfmt); break;
+    case 2: hipLaunchKernelGGL((lut_fused_split_kernel<BITS, 2, PRE, INT8>), grid, dim3(256), 0, s, p, L.wfmt); break;
     case 4:
         if constexpr (BITS <= 2)
-            hipLaunchKernelGGL((lut_fused_split_kernel<BITS, 4, PRE>), grid, dim3(256), 0, s, p, L.wfmt);
+            hipLaunchKernelGGL((lut_fused_split_kernel<BITS, 4, PRE, INT8>), grid, dim3(256), 0, s, p, L.wfmt);
         break;
     default:
         if constexpr (BITS == 1)
-            hipLaunchKernelGGL((lut_fused_split_kernel<BITS, 8, PRE>), grid, dim3(256), 0, s, p, L.wfmt);
+            hipLaunchKernelGGL((lut_fused_split_kernel<BITS, 8, PRE, INT8>), grid, dim3(256), 0, s, p, L.wfmt);
         break;
     }
 }
 
-template <int BITS>
+template <int BITS, bool INT8>
 static void launch_fused_split_bits(const LutParams &p, const Layout &L, const LutPlan &plan, hipStream_t s) {
-    if (plan.pre == 0) launch_fused_split_pre<BITS, 0>(p, L, plan, s);
-    else if (plan.pre == 4) launch_fused_split_pre<BITS, 4>(p, L, plan, s);
-    else if (plan.pre >= 8) launch_fused_split_pre<BITS, 8>(p, L, plan, s);
-    else launch_fused_split_pre<BITS, 2>(p, L, plan, s);
+    if (plan.pre == 0) launch_fused_split_pre<BITS, 0, INT8>(p, L, plan, s);
+    else if (plan.pre == 4) launch_fused_split_pre<BITS, 4, INT8>(p, L, plan, s);
+    else if (plan.pre >= 8) launch_fused_split_pre<BITS, 8, INT8>(p, L, plan, s);
+    else launch_fused_split_pre<BITS, 2, INT8>(p, L, plan, s);
 }
 
 int launch_fused_split(const LutParams &p, const Layout &L, const LutPlan &plan, void *stream) {
     hipStream_t s = (hipStream_t)stream;
-    if (L.bits == 1) launch_fused_split_bits<1>(p, L, plan, s);
-    else if (L.bits == 2) launch_fused_split_bits<2>(p, L, plan, s);
-    else launch_fused_split_bits<4>(p, L, plan, s);
+    if (L.act == LUTGEMM_ACT_INT8) {  // binary and ternary weights only (1 or 2 planes)
+        if (L.bits == 1) launch_fused_split_bits<1, true>(p, L, plan, s);
+        else if (L.bits == 2) launch_fused_split_bits<2, true>(p, L, plan, s);
+        else return (int)hipErrorInvalidValue;
+    } else if (L.bits == 1) {
+        launch_fused_split_bits<1, false>(p, L, plan, s);
+    } else if (L.bits == 2) {
+        launch_fused_split_bits<2, false>(p, L, plan, s);
+    } else {
+        launch_fused_split_bits<4, false>(p, L, plan, s);
+    }
     return (int)hipGetLastError();
 }
 

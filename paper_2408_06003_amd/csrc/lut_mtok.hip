@@ -57,13 +57,6 @@ __device__ __forceinline__ uint32_t perm(uint32_t hi, uint32_t lo, uint32_t sel)
     return __builtin_amdgcn_perm(hi, lo, sel);
 }
 
-// Lane-wise maximum of two packed unsigned 16-bit pairs (v_pk_max_u16).
-__device__ __forceinline__ uint32_t max_u16x2(uint32_t a, uint32_t b) {
-    typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
-    return __builtin_bit_cast(uint32_t,
-                              __builtin_elementwise_max(__builtin_bit_cast(u16x2, a), __builtin_bit_cast(u16x2, b)));
-}
-
 // Sum of v over each row of 16 lanes by DPP (quad_perm [1,0,3,2], [2,3,0,1], row half
 // mirror, row mirror): every lane of the row ends with the same bits.
 __device__ __forceinline__ float row_sum16(float v) {

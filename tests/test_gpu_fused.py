@@ -6,8 +6,9 @@ path (lutgemm_precompute + lutgemm_mpgemm) bitwise.  Cases cover one and two
 tokens, a single K chunk, several K chunks (K = 11008), K split across
 workgroups (few columns), ragged column tails, every weight format, accumulate,
 determinism, the zero token, the split-K kernel that builds FP32 tables from the
-activations (large FP16-activation layers), and the two-call path behind the same
-entry point (INT8 activations with M > 2 or large weights).
+activations (large layers; INT8 activations: every workgroup reads the whole token for
+the absmax), and the two-call path behind the same entry point (INT8 activations with
+M > 2).
 """
 import numpy as np
 import pytest
@@ -96,6 +97,17 @@ def test_fused_fallback_paths():
     check_fused(gpi, what="INT8 M=6")
 
 
+def test_fused_int8_large_weights_full_size():
+    """Ternary INT8 at 1 x 8192 x 28672 (58 MB of weights: the planned split-K kernel),
+    bitwise against the two-call path, sampled columns against the oracle."""
+    inp = W.make_custom(W.WFMT_TERNARY, 2, 0, W.ACT_INT8, M=1, K=8192, N=28672, seed=141, scale_fp32=True)
+    banner("fused INT8 split-K full size 1x8192x28672")
+    gp = GpuProblem(inp)
+    assert L.fused_workspace_size(gp.p, 1) < L.table_size(gp.p, 1) + L.workspace_size(gp.p, 1)
+    rows, cols = sample_indices(1, inp.N, seed=141)
+    check_fused(gp, rows=rows, cols=cols, what="INT8 1x8192x28672")
+
+
 @pytest.mark.parametrize("cid,sid", [(1, 0), (2, 0), (3, 0), (3, 1), (3, 2), (3, 3), (5, 0), (5, 1)])
 def test_fused_full_size(cid, sid):
     inp = W.make_inputs(cid, sid, M=1)
@@ -141,6 +153,33 @@ def test_fused_split_k_parity(cid, M, K, N, tune):
     banner(f"fused split-K config={cid} M={M} K={K} N={N}")
     gp = GpuProblem(W.make_inputs(cid, 0, M=M, K=K, N=N))
     check_fused(gp, what=f"split-K config {cid} M={M} K={K} N={N}")
+
+
+@pytest.mark.parametrize("wfmt,bits,G,sf,M,K,N,kbs", [
+    (W.WFMT_TERNARY, 2, 0, True, 1, 4096, 1000, 0),     # ternary, per-tensor FP32 scale, planned K ranges
+    (W.WFMT_TERNARY, 2, 0, True, 2, 8192, 300, 0),      # two tokens, ragged columns
+    (W.WFMT_BINARY, 1, 0, True, 1, 4096, 777, 0),       # binary per-tensor
+    (W.WFMT_BINARY, 1, 2048, False, 2, 2048, 520, 0),   # binary per-channel FP16 scale
+    (W.WFMT_TERNARY, 2, 0, True, 1, 8192, 600, 1),      # 64 K ranges: the finalize kernel, token factor from the workspace
+    (W.WFMT_TERNARY, 2, 0, True, 2, 4096, 300, 2),      # 16 K ranges, completed in the kernel
+])
+def test_fused_split_k_int8(wfmt, bits, G, sf, M, K, N, kbs, tune):
+    """INT8 activations on the split-K kernel: every workgroup reads the whole token for
+    the absmax and builds the exact INT16 entries of its K range; bitwise against the
+    two-call path and the oracle (check_fused), including a zero token and a token
+    whose absmax sits in another workgroup's K range."""
+    tune(GEMV_KIND=2, KBS=kbs)
+    banner(f"fused split-K INT8 wfmt={wfmt} b={bits} G={G} M={M} K={K} N={N} kbs={kbs or 'planned'}")
+    inp = W.make_custom(wfmt, bits, G, W.ACT_INT8, M=M, K=K, N=N, seed=131 + bits + K // 1024, scale_fp32=sf)
+    a = inp.act.astype(np.float32)
+    a[0, K - 5] = 9.0  # the token's absmax in the last K range only
+    if M > 1:
+        a[1] = 0.0      # a zero token: factor 0, zero output
+    inp.act = a.astype(np.float16)
+    gp = GpuProblem(inp)
+    check_fused(gp, what=f"split-K INT8 wfmt={wfmt} M={M} K={K}")
+    if M > 1:
+        assert not gp.fused(out_dtype=torch.int32)[1].any()
 
 
 @pytest.mark.parametrize("wfmt,bits,G", [(W.WFMT_UINT, 1, 128), (W.WFMT_UINT, 2, 1024), (W.WFMT_UINT, 4, 512),
