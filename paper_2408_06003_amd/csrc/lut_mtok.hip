@@ -245,8 +245,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(TQ ? 1 : (B
     // staging tasks per chunk: (block, group, index pair); with FZ (token slice, block,
     // group, index pair), a slice being the 8 tokens of a half.  1-bit weights (one plane
     // of lookups per chunk, so the build weighs most) take slices of 4 tokens where 8
-    // would leave half the lanes idle, so every lane shares the build (measured: 1.5 us
-    // faster at 4 and 8 tokens; with 4-bit weights 2 us slower)
+    // would leave half the lanes idle, so every lane shares the build (measured at M = 4
+    // and 8: 1.5 us faster for 1-bit weights, 2 us slower for 4-bit ones)
     constexpr int HT = CH * GPB * 4 * NH;         // FZ: (half, block, group, index pair) tasks
     constexpr int TOK = (FZ && BITS == 1 && HT < 256) ? MTK * HT / 256 : MTK;  // FZ: tokens per task
     constexpr int TASKS = FZ ? HT * (MTK / TOK) : CH * GPB * 4;
