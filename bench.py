@@ -310,7 +310,8 @@ class Case:
         return 2.0 * self.M * self.N * self.K / (ms * 1e-3) / 1e12
 
     def measure(self, n_kernel, warmup):
-        """Kernel-level numbers of this shape: mpGEMM, precompute, and (M >= 16) the comparison path."""
+        """Kernel-level numbers of this shape: mpGEMM, precompute, and the comparison path
+        (M >= 16, and at any M where it takes the 16-token slab kernel: 1-bit weights)."""
         for i in range(warmup):
             self.step(i)
         self.precompute()
@@ -347,7 +348,8 @@ class Case:
                # taken on the current kernel sources)
                "mpgemm_hbm_traffic_bytes": load_traffic(self.name, "mpgemm"),
                "fused_hbm_traffic_bytes": load_traffic(self.name, "fused")}
-        if self.M >= 16 and not self.int8 and not self.tri and not self.lut8:
+        if (not self.int8 and not self.tri and not self.lut8
+                and (self.M >= 16 or self.L.dequant_plan(self.p, self.M)[0] == 2)):
             out = self.torch.empty((self.M, self.N), dtype=self.torch.float16, device="cuda")
             for i in range(3):
                 self.dequant(i, out)
