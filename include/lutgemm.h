@@ -370,7 +370,9 @@ enum {
                                        M > 2: 1 builds the tables inside the multi-token kernel, 0
                                        runs precompute + mpGEMM (-1: planned, the former for
                                        M <= 64 on layers of at most 64 x 256 columns)              */
-    LUTGEMM_TUNE_COUNT = 15
+    LUTGEMM_TUNE_MT4 = 15,          /* LUTGEMM_MT4: 0 keeps 8-token tiles for M <= 4 (1: 4-token
+                                       tiles)                                                        */
+    LUTGEMM_TUNE_COUNT = 16
 };
 
 /* Sets planner override `key` (LUTGEMM_TUNE_*) to `value` (-1: its default).

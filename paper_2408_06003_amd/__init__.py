@@ -42,7 +42,7 @@ EXPORTS = [
 # planner overrides (LUTGEMM_TUNE_*), for tests and experiments
 TUNE = {"TARGET_BLOCKS": 0, "WHOLEK_MAX_KB": 1, "GEMV_KIND": 2, "GEMV_CFG": 3, "SPLITS": 4, "KBS": 5,
         "MT16": 6, "MT_TARGET": 7, "MT_SPLITS": 8, "MT_ORDER": 9, "DEQUANT_KIND": 10, "LOG": 11,
-        "SPLIT_PRE": 12, "DEQUANT_SPLITS": 13, "MT_FUSED": 14}
+        "SPLIT_PRE": 12, "DEQUANT_SPLITS": 13, "MT_FUSED": 14, "MT4": 15}
 
 
 class Problem(ctypes.Structure):

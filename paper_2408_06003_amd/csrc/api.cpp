@@ -73,8 +73,8 @@ const char *const kTuneEnv[LUTGEMM_TUNE_COUNT] = {
     "LUTGEMM_TARGET_BLOCKS", "LUTGEMM_WHOLEK_MAX_KB", "LUTGEMM_GEMV_KIND", "LUTGEMM_GEMV_CFG",
     "LUTGEMM_SPLITS",        "LUTGEMM_KBS",           "LUTGEMM_MT16",      "LUTGEMM_MT_TARGET",
     "LUTGEMM_MT_SPLITS",     "LUTGEMM_MT_ORDER",      "LUTGEMM_DEQUANT_KIND", "LUTGEMM_LOG",
-    "LUTGEMM_SPLIT_PRE",     "LUTGEMM_DEQUANT_SPLITS", "LUTGEMM_MT_FUSED"};
-const int kTuneDefault[LUTGEMM_TUNE_COUNT] = {256, 10000, -1, -1, 0, 0, 1, 8, 0, -1, -1, 0, 4, 0, -1};
+    "LUTGEMM_SPLIT_PRE",     "LUTGEMM_DEQUANT_SPLITS", "LUTGEMM_MT_FUSED", "LUTGEMM_MT4"};
+const int kTuneDefault[LUTGEMM_TUNE_COUNT] = {256, 10000, -1, -1, 0, 0, 1, 8, 0, -1, -1, 0, 4, 0, -1, 1};
 std::atomic<int> g_tune[LUTGEMM_TUNE_COUNT];
 
 bool tune_value_ok(int key, int value) {
@@ -230,9 +230,11 @@ LutPlan plan_lut(const Layout &L, int64_t M, bool fused) {
     } else {
         P.kind = 1;
         // tokens per workgroup of the multi-token kernel (lut_mtok.hip): 16 from M = 16 on
-        // (one decoded index serves two token halves), except with INT8-quantized tables
+        // (one decoded index serves two token halves), 4 up to M = 4 (half-filled rows,
+        // half the LDS bytes and packed adds per lookup), except with INT8-quantized tables
         const int mt16 = tuning(LUTGEMM_TUNE_MT16);
-        P.mt = (M >= 16 && L.act != LUTGEMM_ACT_FP16_LUT8 && mt16) ? 16 : 8;
+        const bool lut8 = L.act == LUTGEMM_ACT_FP16_LUT8;
+        P.mt = (M >= 16 && !lut8 && mt16) ? 16 : ((M <= 4 && !lut8 && tuning(LUTGEMM_TUNE_MT4)) ? 4 : 8);
         P.m_tiles = (M + P.mt - 1) / P.mt;
         P.n_tiles = L.N_pad / NTILE;
         const int64_t base = P.n_tiles * P.m_tiles;

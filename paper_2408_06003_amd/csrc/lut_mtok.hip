@@ -49,7 +49,7 @@
 
 namespace lutgemm {
 
-constexpr int MTK = 8;  // tokens per workgroup (per half)
+constexpr int MTK = 8;  // token slots of a 16-byte table row (tokens per half)
 constexpr int FZ_SMAX = MTOK_FUSED_SMAX;  // fused build with zero points: most 128-blocks per K range
 
 // The 16-bit lanes of x selected by SEL (v_perm_b32 byte selector) from {hi, lo}.
@@ -175,6 +175,43 @@ __device__ __forceinline__ void pk_add4(uint4 &h, uint4 e) {
         : "v"(e.x), "v"(e.y), "v"(e.z), "v"(e.w));
 }
 
+// Four-token rows (two packed FP16 pairs): the same operations on uint2.
+__device__ __forceinline__ uint2 pk_sum4(uint2 a, uint2 b) {
+    uint2 h;
+    asm("v_pk_add_f16 %0, %2, %4\n\t"
+        "v_pk_add_f16 %1, %3, %5"
+        : "=&v"(h.x), "=&v"(h.y)
+        : "v"(a.x), "v"(a.y), "v"(b.x), "v"(b.y));
+    return h;
+}
+__device__ __forceinline__ void pk_add4(uint2 &h, uint2 e) {
+    asm("v_pk_add_f16 %0, %0, %2\n\t"
+        "v_pk_add_f16 %1, %1, %3"
+        : "+v"(h.x), "+v"(h.y)
+        : "v"(e.x), "v"(e.y));
+}
+__device__ __forceinline__ uint2 pk_fma2x4(uint2 a, uint2 b) {
+    uint2 h;
+    const uint32_t two = 0x40004000u;
+    asm("v_pk_fma_f16 %0, %2, %6, %4\n\t"
+        "v_pk_fma_f16 %1, %3, %6, %5"
+        : "=&v"(h.x), "=&v"(h.y)
+        : "v"(a.x), "v"(a.y), "v"(b.x), "v"(b.y), "s"(two));
+    return h;
+}
+__device__ __forceinline__ void fma_mix8(float *af, uint2 e, float sc) {
+    asm("v_fma_mix_f32 %0, %4, %6, %0 op_sel_hi:[1,0,0]\n\t"
+        "v_fma_mix_f32 %1, %4, %6, %1 op_sel:[1,0,0] op_sel_hi:[1,0,0]\n\t"
+        "v_fma_mix_f32 %2, %5, %6, %2 op_sel_hi:[1,0,0]\n\t"
+        "v_fma_mix_f32 %3, %5, %6, %3 op_sel:[1,0,0] op_sel_hi:[1,0,0]"
+        : "+v"(af[0]), "+v"(af[1]), "+v"(af[2]), "+v"(af[3])
+        : "v"(e.x), "v"(e.y), "v"(sc));
+}
+__device__ __forceinline__ uint32_t row_word(const uint4 &e, int j) {
+    return j == 0 ? e.x : j == 1 ? e.y : j == 2 ? e.z : e.w;
+}
+__device__ __forceinline__ uint32_t row_word(const uint2 &e, int j) { return j == 0 ? e.x : e.y; }
+
 // af[t] += sc * (FP16 entry of token t in e), t = 0..7: eight v_fma_mix_f32 in one
 // statement, so each LDS read is consumed as a whole (the compiler would otherwise
 // regroup the accumulations by token and keep every read of a block live).
@@ -230,16 +267,20 @@ __device__ __forceinline__ Tile tile_of(uint32_t b, uint32_t n_tiles, uint32_t m
     return t;
 }
 
-// NH halves of 8 tokens per workgroup (NH = 2: one decoded index serves two 16-byte
+// NH halves of TK tokens per workgroup (NH = 2: one decoded index serves two 16-byte
 // reads, the second at a fixed +256-byte offset, so index decoding, weight loads and
-// metadata are shared by 16 tokens).
+// metadata are shared by 16 tokens).  TK = 4 (one half, M <= 4): only the first 8
+// bytes of each table row are filled and read (ds_read_b64), so a lookup costs half
+// the LDS bytes and half the packed adds of an 8-token row.
 // FZ: 0 = tables from the precompute; 1 = tables built from the FP16 activations;
 // 2 = the same with the per-block activation sums of the zero-point term.
-template <int BITS, bool INT8, bool TQ, int NH, int FZ>
+template <int BITS, bool INT8, bool TQ, int NH, int FZ, int TK>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(TQ ? 1 : (BITS == 1 && NH == 1 ? 6 : 4)))) void lut_mtok_kernel(LutParams p, int wfmt, int64_t n_tiles, int64_t m_tiles,
                                                        int order) {
     static_assert(FZ == 0 || (!INT8 && !TQ), "the fused table build takes FP16 activations");
-    constexpr int MT = MTK * NH;                  // tokens per workgroup
+    static_assert(TK == MTK || (TK == 4 && NH == 1 && !TQ), "rows of 8 tokens, or 4 in a single half");
+    constexpr int MT = TK * NH;                   // tokens per workgroup
+    typedef std::conditional_t<TK == MTK, uint4, uint2> Row;  // the row part a lookup reads
     // 128-blocks per chunk (b = 1 and 16 tokens: 16 KB of LDS per buffer, more workgroups per CU)
     constexpr int CH = (BITS == 1 || NH == 2) ? 1 : 4 / BITS;
     // staging tasks per chunk: (block, group, index pair); with FZ (token slice, block,
@@ -248,8 +289,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(TQ ? 1 : (B
     // would leave half the lanes idle, so every lane shares the build (measured at M = 4
     // and 8: 1.5 us faster for 1-bit weights, 2 us slower for 4-bit ones)
     constexpr int HT = CH * GPB * 4 * NH;         // FZ: (half, block, group, index pair) tasks
-    constexpr int TOK = (FZ && BITS == 1 && HT < 256) ? MTK * HT / 256 : MTK;  // FZ: tokens per task
-    constexpr int TASKS = FZ ? HT * (MTK / TOK) : CH * GPB * 4;
+    constexpr int TOK = (FZ && BITS == 1 && HT < 256 && TK == MTK) ? MTK * HT / 256 : TK;  // FZ: tokens per task
+    constexpr int TASKS = FZ ? HT * (TK / TOK) : CH * GPB * 4;
     constexpr int TPL = (TASKS + 255) / 256;      // staging tasks per lane
     static_assert(FZ == 0 || (TPL == 1 && (TOK == 4 || TOK == 8)), "one fused staging task per lane");
     constexpr int GST = 256 * NH;                 // LDS bytes of one group (16 entries x 8 tokens x 2 B per half)
@@ -413,7 +454,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(TQ ? 1 : (B
                     }
                 }
                 // slice q: half (TOK q) / 8 of the row, at token (TOK q) % 8 within it
-                char *row = Fb + (kbl * GPB + g) * GST + 256 * (TOK * q / MTK) + 2 * (TOK * q % MTK);
+                char *row = Fb + (kbl * GPB + g) * GST + 256 * (TOK * q / TK) + 2 * (TOK * q % TK);
                 if constexpr (TOK == MTK) {
                     const uint4 e0 = make_uint4(r0[0], r0[1], r0[2], r0[3]), e1 = make_uint4(r1[0], r1[1], r1[2], r1[3]);
                     *(uint4 *)(row + (2 * ip) * 16) = e0;
@@ -439,7 +480,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(TQ ? 1 : (B
                 for (int h = 0; h < NH; ++h) {
                     uint32_t v[MTK];
 #pragma unroll
-                    for (int t = 0; t < MTK; ++t) {
+                    for (int t = 0; t < TK; ++t) {
                         if constexpr (TQ) {  // code x scale, rounded to FP16
                             const float sc = __uint_as_float(sd[r][MTK * h + t].y);
                             const float f0 = (float)(int8_t)(sd[r][MTK * h + t].x & 0xFFu) * sc;
@@ -447,25 +488,34 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(TQ ? 1 : (B
                             v[t] = (uint32_t)__half_as_ushort(__float2half_rn(f0)) |
                                    ((uint32_t)__half_as_ushort(__float2half_rn(f1)) << 16);
                         } else {
-                            v[t] = sd[r][MTK * h + t];
+                            v[t] = sd[r][TK * h + t];
                         }
                     }
-                    uint4 e0, e1;  // entries 2ip (low halves) and 2ip + 1 (high halves), tokens 8h .. 8h + 7
-                    e0.x = perm(v[1], v[0], 0x05040100u);
-                    e0.y = perm(v[3], v[2], 0x05040100u);
-                    e0.z = perm(v[5], v[4], 0x05040100u);
-                    e0.w = perm(v[7], v[6], 0x05040100u);
-                    e1.x = perm(v[1], v[0], 0x07060302u);
-                    e1.y = perm(v[3], v[2], 0x07060302u);
-                    e1.z = perm(v[5], v[4], 0x07060302u);
-                    e1.w = perm(v[7], v[6], 0x07060302u);
                     char *row = Fb + (kbl * GPB + g) * GST + 256 * h;
-                    *(uint4 *)(row + (2 * ip) * 16) = e0;
-                    *(uint4 *)(row + (2 * ip + 1) * 16) = e1;
-                    *(uint4 *)(row + (2 * ip + 8) * 16) =
-                        make_uint4(neg16x2<INT8>(e0.x), neg16x2<INT8>(e0.y), neg16x2<INT8>(e0.z), neg16x2<INT8>(e0.w));
-                    *(uint4 *)(row + (2 * ip + 9) * 16) =
-                        make_uint4(neg16x2<INT8>(e1.x), neg16x2<INT8>(e1.y), neg16x2<INT8>(e1.z), neg16x2<INT8>(e1.w));
+                    if constexpr (TK == MTK) {
+                        uint4 e0, e1;  // entries 2ip (low halves) and 2ip + 1 (high halves), tokens 8h .. 8h + 7
+                        e0.x = perm(v[1], v[0], 0x05040100u);
+                        e0.y = perm(v[3], v[2], 0x05040100u);
+                        e0.z = perm(v[5], v[4], 0x05040100u);
+                        e0.w = perm(v[7], v[6], 0x05040100u);
+                        e1.x = perm(v[1], v[0], 0x07060302u);
+                        e1.y = perm(v[3], v[2], 0x07060302u);
+                        e1.z = perm(v[5], v[4], 0x07060302u);
+                        e1.w = perm(v[7], v[6], 0x07060302u);
+                        *(uint4 *)(row + (2 * ip) * 16) = e0;
+                        *(uint4 *)(row + (2 * ip + 1) * 16) = e1;
+                        *(uint4 *)(row + (2 * ip + 8) * 16) =
+                            make_uint4(neg16x2<INT8>(e0.x), neg16x2<INT8>(e0.y), neg16x2<INT8>(e0.z), neg16x2<INT8>(e0.w));
+                        *(uint4 *)(row + (2 * ip + 9) * 16) =
+                            make_uint4(neg16x2<INT8>(e1.x), neg16x2<INT8>(e1.y), neg16x2<INT8>(e1.z), neg16x2<INT8>(e1.w));
+                    } else {  // tokens 0 .. 3 in the first 8 bytes of each row
+                        const uint2 e0 = make_uint2(perm(v[1], v[0], 0x05040100u), perm(v[3], v[2], 0x05040100u));
+                        const uint2 e1 = make_uint2(perm(v[1], v[0], 0x07060302u), perm(v[3], v[2], 0x07060302u));
+                        *(uint2 *)(row + (2 * ip) * 16) = e0;
+                        *(uint2 *)(row + (2 * ip + 1) * 16) = e1;
+                        *(uint2 *)(row + (2 * ip + 8) * 16) = make_uint2(neg16x2<INT8>(e0.x), neg16x2<INT8>(e0.y));
+                        *(uint2 *)(row + (2 * ip + 9) * 16) = make_uint2(neg16x2<INT8>(e1.x), neg16x2<INT8>(e1.y));
+                    }
                 }
             }
         }
@@ -479,11 +529,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(TQ ? 1 : (B
                 // INT16 (|sum| <= 32 x 508 < 2^15), then widened with the plane weight 2^pl
 #pragma unroll
                 for (int pl = 0; pl < BITS; ++pl) {
-                    short2_v a16[NH][4];
+                    short2_v a16[NH][TK / 2];
 #pragma unroll
                     for (int h = 0; h < NH; ++h)
 #pragma unroll
-                        for (int j = 0; j < 4; ++j) a16[h][j] = short2_v{0, 0};
+                        for (int j = 0; j < TK / 2; ++j) a16[h][j] = short2_v{0, 0};
                     const uint32_t wd[4] = {w[kbl][pl].x, w[kbl][pl].y, w[kbl][pl].z, w[kbl][pl].w};
 #pragma unroll
                     for (int d = 0; d < 4; ++d) {
@@ -494,20 +544,18 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(TQ ? 1 : (B
                             const int g = d * 8 + k;  // groups 2j (low nibble) and 2j + 1 (high nibble) of byte j
 #pragma unroll
                             for (int h = 0; h < NH; ++h) {
-                                const uint4 e = *(const uint4 *)(Fb + (kbl * GPB + g) * GST + 256 * h + off);
-                                a16[h][0] += __builtin_bit_cast(short2_v, e.x);
-                                a16[h][1] += __builtin_bit_cast(short2_v, e.y);
-                                a16[h][2] += __builtin_bit_cast(short2_v, e.z);
-                                a16[h][3] += __builtin_bit_cast(short2_v, e.w);
+                                const Row e = *(const Row *)(Fb + (kbl * GPB + g) * GST + 256 * h + off);
+#pragma unroll
+                                for (int j = 0; j < TK / 2; ++j) a16[h][j] += __builtin_bit_cast(short2_v, row_word(e, j));
                             }
                         }
                     }
 #pragma unroll
                     for (int h = 0; h < NH; ++h)
 #pragma unroll
-                        for (int j = 0; j < 4; ++j) {
-                            yi[MTK * h + 2 * j] += (int)a16[h][j].x << pl;
-                            yi[MTK * h + 2 * j + 1] += (int)a16[h][j].y << pl;
+                        for (int j = 0; j < TK / 2; ++j) {
+                            yi[TK * h + 2 * j] += (int)a16[h][j].x << pl;
+                            yi[TK * h + 2 * j + 1] += (int)a16[h][j].y << pl;
                         }
                 }
             } else {
@@ -518,18 +566,18 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(TQ ? 1 : (B
                 const SZ sz = decode_sz(p, mw.w[kbl]);
 #pragma unroll
                 for (int d = 0; d < 4; ++d) {
-                    uint4 hp[NH][BITS];
+                    Row hp[NH][BITS];
 #pragma unroll
                     for (int pl = 0; pl < BITS; ++pl) {
                         const uint32_t wv = d == 0 ? w[kbl][pl].x : d == 1 ? w[kbl][pl].y : d == 2 ? w[kbl][pl].z : w[kbl][pl].w;
                         const uint32_t lo = wv << 4, hi = wv;
-                        uint4 e[8][NH];
+                        Row e[8][NH];
 #pragma unroll
                         for (int k = 0; k < 8; ++k) {
                             const uint32_t off = nib_off((k & 1) ? hi : lo, k >> 1);
                             const int g = d * 8 + k;  // groups 2j (low nibble) and 2j + 1 (high nibble) of byte j
 #pragma unroll
-                            for (int h = 0; h < NH; ++h) e[k][h] = *(const uint4 *)(Fb + (kbl * GPB + g) * GST + 256 * h + off);
+                            for (int h = 0; h < NH; ++h) e[k][h] = *(const Row *)(Fb + (kbl * GPB + g) * GST + 256 * h + off);
                             if (k == 1) {
 #pragma unroll
                                 for (int h = 0; h < NH; ++h) hp[h][pl] = pk_sum4(e[0][h], e[1][h]);
@@ -549,11 +597,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(TQ ? 1 : (B
 #pragma unroll
                     for (int h = 0; h < NH; ++h) {
                         if constexpr (BITS == 1) {
-                            fma_mix8(yf + MTK * h, hp[h][0], sz.sp);
+                            fma_mix8(yf + TK * h, hp[h][0], sz.sp);
                         } else {
 #pragma unroll
                             for (int i = 0; i < BITS / 2; ++i)
-                                fma_mix8(yf + MTK * h, pk_fma2x4(hp[h][2 * i + 1], hp[h][2 * i]), sz.sp * (float)(1 << (2 * i)));
+                                fma_mix8(yf + TK * h, pk_fma2x4(hp[h][2 * i + 1], hp[h][2 * i]), sz.sp * (float)(1 << (2 * i)));
                         }
                     }
                 }
@@ -675,7 +723,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(TQ ? 1 : (B
     }
 }
 
-template <int NH>
+template <int NH, int TK>
 static void launch_mtok_nh(const LutParams &p, const Layout &L, const LutPlan &plan, hipStream_t s) {
     // one-dimensional grid (tile_of decodes it); the planner keeps it under 2^32 work-items
     const dim3 grid((unsigned)(plan.n_tiles * plan.m_tiles * plan.splits), 1, 1);
@@ -683,26 +731,26 @@ static void launch_mtok_nh(const LutParams &p, const Layout &L, const LutPlan &p
     const int64_t nt = plan.n_tiles, mt = plan.m_tiles;
     const int o = plan.order;
     if (L.bits == 1) {
-        if (i8) hipLaunchKernelGGL((lut_mtok_kernel<1, true, false, NH, 0>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
-        else hipLaunchKernelGGL((lut_mtok_kernel<1, false, false, NH, 0>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
+        if (i8) hipLaunchKernelGGL((lut_mtok_kernel<1, true, false, NH, 0, TK>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
+        else hipLaunchKernelGGL((lut_mtok_kernel<1, false, false, NH, 0, TK>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
     } else if (L.bits == 2) {
-        if (i8) hipLaunchKernelGGL((lut_mtok_kernel<2, true, false, NH, 0>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
-        else hipLaunchKernelGGL((lut_mtok_kernel<2, false, false, NH, 0>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
+        if (i8) hipLaunchKernelGGL((lut_mtok_kernel<2, true, false, NH, 0, TK>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
+        else hipLaunchKernelGGL((lut_mtok_kernel<2, false, false, NH, 0, TK>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
     } else {
-        hipLaunchKernelGGL((lut_mtok_kernel<4, false, false, NH, 0>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
+        hipLaunchKernelGGL((lut_mtok_kernel<4, false, false, NH, 0, TK>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
     }
 }
 
 // Tables built in the kernel from FP16 activations: FZ = 2 when the format has zero
 // points (the per-block activation sums are kept in LDS), else 1.
-template <int NH, int FZ>
+template <int NH, int FZ, int TK>
 static void launch_mtok_fz(const LutParams &p, const Layout &L, const LutPlan &plan, hipStream_t s) {
     const dim3 grid((unsigned)(plan.n_tiles * plan.m_tiles * plan.splits), 1, 1);
     const int64_t nt = plan.n_tiles, mt = plan.m_tiles;
     const int o = plan.order;
-    if (L.bits == 1) hipLaunchKernelGGL((lut_mtok_kernel<1, false, false, NH, FZ>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
-    else if (L.bits == 2) hipLaunchKernelGGL((lut_mtok_kernel<2, false, false, NH, FZ>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
-    else hipLaunchKernelGGL((lut_mtok_kernel<4, false, false, NH, FZ>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
+    if (L.bits == 1) hipLaunchKernelGGL((lut_mtok_kernel<1, false, false, NH, FZ, TK>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
+    else if (L.bits == 2) hipLaunchKernelGGL((lut_mtok_kernel<2, false, false, NH, FZ, TK>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
+    else hipLaunchKernelGGL((lut_mtok_kernel<4, false, false, NH, FZ, TK>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
 }
 
 int launch_mtok(const LutParams &p, const Layout &L, const LutPlan &plan, void *stream) {
@@ -711,13 +759,15 @@ int launch_mtok(const LutParams &p, const Layout &L, const LutPlan &plan, void *
         const dim3 grid((unsigned)(plan.n_tiles * plan.m_tiles * plan.splits), 1, 1);
         const int64_t nt = plan.n_tiles, mt = plan.m_tiles;
         const int o = plan.order;
-        if (L.bits == 1) hipLaunchKernelGGL((lut_mtok_kernel<1, false, true, 1, 0>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
-        else if (L.bits == 2) hipLaunchKernelGGL((lut_mtok_kernel<2, false, true, 1, 0>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
-        else hipLaunchKernelGGL((lut_mtok_kernel<4, false, true, 1, 0>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
+        if (L.bits == 1) hipLaunchKernelGGL((lut_mtok_kernel<1, false, true, 1, 0, 8>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
+        else if (L.bits == 2) hipLaunchKernelGGL((lut_mtok_kernel<2, false, true, 1, 0, 8>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
+        else hipLaunchKernelGGL((lut_mtok_kernel<4, false, true, 1, 0, 8>), grid, dim3(256), 0, s, p, L.wfmt, nt, mt, o);
     } else if (plan.mt == 16) {
-        launch_mtok_nh<2>(p, L, plan, s);
+        launch_mtok_nh<2, 8>(p, L, plan, s);
+    } else if (plan.mt == 4) {
+        launch_mtok_nh<1, 4>(p, L, plan, s);
     } else {
-        launch_mtok_nh<1>(p, L, plan, s);
+        launch_mtok_nh<1, 8>(p, L, plan, s);
     }
     return (int)hipGetLastError();
 }
@@ -728,11 +778,14 @@ int launch_mtok_fused(const LutParams &p, const Layout &L, const LutPlan &plan, 
     const bool zp = L.wfmt != LUTGEMM_WFMT_BINARY;
     if (zp && plan.kbs > MTOK_FUSED_SMAX) return (int)hipErrorInvalidValue;  // the planner caps it
     if (plan.mt == 16) {
-        if (zp) launch_mtok_fz<2, 2>(p, L, plan, s);
-        else launch_mtok_fz<2, 1>(p, L, plan, s);
+        if (zp) launch_mtok_fz<2, 2, 8>(p, L, plan, s);
+        else launch_mtok_fz<2, 1, 8>(p, L, plan, s);
+    } else if (plan.mt == 4) {
+        if (zp) launch_mtok_fz<1, 2, 4>(p, L, plan, s);
+        else launch_mtok_fz<1, 1, 4>(p, L, plan, s);
     } else {
-        if (zp) launch_mtok_fz<1, 2>(p, L, plan, s);
-        else launch_mtok_fz<1, 1>(p, L, plan, s);
+        if (zp) launch_mtok_fz<1, 2, 8>(p, L, plan, s);
+        else launch_mtok_fz<1, 1, 8>(p, L, plan, s);
     }
     return (int)hipGetLastError();
 }

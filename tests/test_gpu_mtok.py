@@ -78,6 +78,49 @@ def test_multi_token_int8_layouts(wfmt, bits, G, fp32, M, K, N, splits, tune):
     assert np.array_equal(yf, y_ref), "FP32 scaled output differs from the oracle"
 
 
+FOUR_CASES = [
+    # (weight format, bits, group, FP32 per-tensor scale, activations, M, K, N, forced K splits)
+    (W.WFMT_UINT, 2, 128, False, W.ACT_FP16, 4, 2048, 520, 0),    # INT2 g128, 4 live rows
+    (W.WFMT_UINT, 4, 512, False, W.ACT_FP16, 3, 2560, 300, 3),    # INT4, groups of 4 blocks split mid-group, 3 rows
+    (W.WFMT_UINT, 1, 0, False, W.ACT_FP16, 4, 1152, 257, 0),      # UINT1 per-channel, 9 blocks
+    (W.WFMT_BINARY, 1, 256, False, W.ACT_FP16, 3, 4096, 1000, 0),  # binary group scales
+    (W.WFMT_TERNARY, 2, 0, True, W.ACT_FP16, 4, 2048, 300, 5),    # per-tensor FP32 scale, z' = -1
+    (W.WFMT_TERNARY, 2, 0, True, W.ACT_INT8, 4, 2048, 513, 3),    # INT8: exact
+    (W.WFMT_BINARY, 1, 1536, False, W.ACT_INT8, 3, 1536, 300, 0),
+]
+
+
+@pytest.mark.parametrize("wfmt,bits,G,fp32,act,M,K,N,splits", FOUR_CASES)
+def test_multi_token_four_token_tiles(wfmt, bits, G, fp32, act, M, K, N, splits, tune):
+    """M <= 4 takes 4-token tiles (half-filled rows, 8-byte reads): against the oracle,
+    and against the 8-token tiles of the same call (bitwise on the INT8 path, within
+    the FP bar on the FP path: the same entries summed in the same order per token)."""
+    if splits:
+        tune(MT_SPLITS=splits)
+    what = f"4-token tiles wfmt={wfmt} b={bits} G={G} act={act} M={M} K={K} N={N} splits={splits}"
+    print(f"\n[case] {what}", flush=True)
+    inp = W.make_custom(wfmt, bits, G, act, M=M, K=K, N=N, seed=7 * M + K + N + splits, scale_fp32=fp32)
+    gp = GpuProblem(inp)
+    tune(MT4=1)
+    if act == W.ACT_INT8:
+        acc_ref, y_ref = oracle.reference_output(inp)
+        yi = gp.lut(out_dtype=torch.int32)
+        assert np.array_equal(yi.cpu().numpy().astype(np.int64), acc_ref), f"{what}: INT32 accumulator differs"
+        assert np.array_equal(gp.lut(out_dtype=torch.float32).cpu().numpy(), y_ref), f"{what}: FP32 output differs"
+        tune(MT4=0)
+        assert torch.equal(gp.lut(out_dtype=torch.int32), yi), f"{what}: 4- and 8-token tiles differ"
+        return
+    ref = oracle.reference_output(inp)
+    y4 = gp.lut(out_dtype=torch.float32)
+    fro, mx = assert_fp_close(y4.cpu().numpy(), ref, what)
+    print(f"[err] {what}: relFro {fro:.3e} max/rms {mx:.3e}", flush=True)
+    assert torch.equal(gp.lut(out_dtype=torch.float32), y4), f"{what}: two runs differ bitwise"
+    assert_fp_close(gp.fused(out_dtype=torch.float32).cpu().numpy(), ref, what + " fused")
+    tune(MT4=0)
+    y8 = gp.lut(out_dtype=torch.float32)
+    assert torch.equal(y8, y4), f"{what}: 4- and 8-token tiles differ"
+
+
 @pytest.mark.parametrize("M", [5, 17])
 @pytest.mark.parametrize("splits", [5, 9, 17, 33, 65, 128])
 def test_multi_token_many_splits(splits, M, tune):
