@@ -345,8 +345,8 @@ enum {
     LUTGEMM_TUNE_TARGET_BLOCKS = 0, /* LUTGEMM_TARGET_BLOCKS: workgroups a launch aims for (256)      */
     LUTGEMM_TUNE_WHOLEK_MAX_KB = 1, /* LUTGEMM_WHOLEK_MAX_KB: largest packed weights, in kB, that the
                                        single-token whole-K kernel takes (10000)                     */
-    LUTGEMM_TUNE_GEMV_KIND = 2,     /* LUTGEMM_GEMV_KIND: single-token kernel, 0 whole-K, 2 split-K
-                                       (default -1: by weight size)                                  */
+    LUTGEMM_TUNE_GEMV_KIND = 2,     /* LUTGEMM_GEMV_KIND: kernel for M <= 2, 0 whole-K, 2 split-K,
+                                       1 the multi-token kernel (default -1: planned)                */
     LUTGEMM_TUNE_GEMV_CFG = 3,      /* LUTGEMM_GEMV_CFG: lane decomposition of the whole-K kernel (-1) */
     LUTGEMM_TUNE_SPLITS = 4,        /* LUTGEMM_SPLITS: K splits of the whole-K kernel (0: planned)     */
     LUTGEMM_TUNE_KBS = 5,           /* LUTGEMM_KBS: 128-blocks per workgroup of the split-K kernel

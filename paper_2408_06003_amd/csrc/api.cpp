@@ -160,7 +160,7 @@ LutPlan plan_lut(const Layout &L, int64_t M, bool fused) {
     }
     int kind = M > 2 ? 1 : (weight_bytes <= (int64_t)tuning(LUTGEMM_TUNE_WHOLEK_MAX_KB) * 1000 ? 0 : 2);
     const int forced_kind = tuning(LUTGEMM_TUNE_GEMV_KIND);
-    if (M <= 2 && (forced_kind == 0 || forced_kind == 2)) kind = forced_kind;
+    if (M <= 2 && (forced_kind == 0 || forced_kind == 1 || forced_kind == 2)) kind = forced_kind;
     // the split-K GEMV keeps one arrival counter per (token, 256-column tile); layers with
     // more tiles than the counter area holds fill the GPU without a K split anyway
     if (kind == 2 && M * (L.N_pad / NTILE) > CNT_MAX) kind = 0;
