@@ -134,9 +134,9 @@ lutgemm_status_t hip_error(int e) { return e == 0 ? LUTGEMM_SUCCESS : hip_status
 // K range again, work the precompute does once, and the build is vector work in a
 // kernel bound by vector issue at large M; measured on MI355X it is faster than
 // precompute + mpGEMM up to M = 64 on layers of at most 64 column tiles (INT4 4096 x
-// 12288: 22 us against 25 at M = 4 and 8; binary 28672 x 8192: 26-28 against 28-30;
-// INT2 4096^2 at M = 64: 25 against 28) and slower beyond (binary 8192 x 28672, 112
-// tiles: +1.3 us at M = 16; +17 % at M = 256, +10 % for INT2 at M = 4096).
+// 12288: 18 and 22 us against 22.5 and 25 at M = 4 and 8; binary 28672 x 8192: 21-28
+// against 24-30; INT2 4096^2 at M = 64: 25 against 28) and slower beyond (binary 8192
+// x 28672, 112 tiles: +1.5 us at M = 16; +17 % at M = 256, +10 % for INT2 at M = 4096).
 static bool mtok_fused(const Layout &L, int64_t M) {
     if (L.act != LUTGEMM_ACT_FP16 || M <= 2 || L.tri) return false;
     const int f = tuning(LUTGEMM_TUNE_MT_FUSED);
