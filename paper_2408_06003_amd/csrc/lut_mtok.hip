@@ -334,7 +334,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(TQ ? 1 : (B
     };
     // staged table words: entries 2ip, 2ip + 1 of a token's half table (FP16 / INT16
     // pair), or with INT8-quantized tables (TQ) their two codes and the table's scale;
-    // FZ: the 4 FP16 activations of the task's group, for the 8 tokens of its half
+    // FZ: the 4 FP16 activations of the task's group, for the TOK tokens of its slice
     typedef std::conditional_t<TQ || FZ, uint2, uint32_t> SDE;
     typedef SDE SD[TPL][FZ ? TOK : MT];
     typedef uint4 WW[CH][BITS];
