@@ -164,15 +164,19 @@ size_t lutgemm_table_size(const lutgemm_problem_t *problem, int64_t M);
 lutgemm_status_t lutgemm_table_offsets(const lutgemm_problem_t *problem, int64_t M,
                                        size_t *s_offset, size_t *t_offset);
 
+/* Leading bytes of every nonempty workspace that are zero between calls. */
+#define LUTGEMM_WORKSPACE_ZERO_BYTES ((size_t)1 << 20)
+
 /*
  * Bytes of scratch memory lutgemm_mpgemm needs for M tokens (partial sums when K
- * is split across workgroups, and the arrival counters with which the single-token
- * split-K kernel completes the split itself); may be 0.  The workspace must be
- * zero-filled before its first use.  Its first 64 KiB hold the arrival counters:
- * every call leaves them zero again (the kernel re-arms them) and nothing else is
- * ever stored there, so one zero fill per allocation suffices even when the
- * workspace is shared by calls on different problems.  A workspace must not be
- * shared by calls that run concurrently.
+ * is split across workgroups, and the arrival counters and exact split-sum words
+ * with which the single-token split-K kernel completes the split itself); may be 0.
+ * The workspace must be zero-filled before its first use.  Its first
+ * LUTGEMM_WORKSPACE_ZERO_BYTES hold the counters and split-sum words: every call
+ * leaves them zero again (the kernel re-arms them) and nothing else is ever stored
+ * there, so one zero fill per allocation suffices even when the workspace is shared
+ * by calls on different problems.  A workspace must not be shared by calls that
+ * run concurrently.
  */
 size_t lutgemm_workspace_size(const lutgemm_problem_t *problem, int64_t M);
 
@@ -372,7 +376,12 @@ enum {
                                        M <= 64 on layers of at most 64 x 256 columns)              */
     LUTGEMM_TUNE_MT4 = 15,          /* LUTGEMM_MT4: 0 keeps 8-token tiles for M <= 4 (1: 4-token
                                        tiles)                                                        */
-    LUTGEMM_TUNE_COUNT = 16
+    LUTGEMM_TUNE_SPLIT_EXACT = 16,  /* LUTGEMM_SPLIT_EXACT: 1 completes the single-token K split by one
+                                       64-bit atomic per output where every split's partial sum is an
+                                       integer (INT8 activations, or FP16 activations on weights with
+                                       one scale per column or tensor); 0 always sums FP32 partials
+                                       in split order (1)                                            */
+    LUTGEMM_TUNE_COUNT = 17
 };
 
 /* Sets planner override `key` (LUTGEMM_TUNE_*) to `value` (-1: its default).

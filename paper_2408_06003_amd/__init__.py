@@ -29,6 +29,7 @@ SUCCESS, ERROR_INVALID_VALUE, ERROR_NOT_SUPPORTED, ERROR_INSUFFICIENT_SIZE, ERRO
 WFMT_UINT, WFMT_BINARY, WFMT_TERNARY, WFMT_TERNARY_3IN5 = 0, 1, 2, 3
 ACT_FP16, ACT_INT8, ACT_FP16_LUT8 = 0, 1, 2
 OUT_FP16, OUT_FP32, OUT_INT32 = 0, 1, 2
+WORKSPACE_ZERO_BYTES = 1 << 20  # LUTGEMM_WORKSPACE_ZERO_BYTES
 
 EXPORTS = [
     "lutgemm_status_string", "lutgemm_version", "lutgemm_last_error", "lutgemm_validate", "lutgemm_packed_weight_size",
@@ -42,7 +43,7 @@ EXPORTS = [
 # planner overrides (LUTGEMM_TUNE_*), for tests and experiments
 TUNE = {"TARGET_BLOCKS": 0, "WHOLEK_MAX_KB": 1, "GEMV_KIND": 2, "GEMV_CFG": 3, "SPLITS": 4, "KBS": 5,
         "MT16": 6, "MT_TARGET": 7, "MT_SPLITS": 8, "MT_ORDER": 9, "DEQUANT_KIND": 10, "LOG": 11,
-        "SPLIT_PRE": 12, "DEQUANT_SPLITS": 13, "MT_FUSED": 14, "MT4": 15}
+        "SPLIT_PRE": 12, "DEQUANT_SPLITS": 13, "MT_FUSED": 14, "MT4": 15, "SPLIT_EXACT": 16}
 
 
 class Problem(ctypes.Structure):

@@ -73,8 +73,9 @@ const char *const kTuneEnv[LUTGEMM_TUNE_COUNT] = {
     "LUTGEMM_TARGET_BLOCKS", "LUTGEMM_WHOLEK_MAX_KB", "LUTGEMM_GEMV_KIND", "LUTGEMM_GEMV_CFG",
     "LUTGEMM_SPLITS",        "LUTGEMM_KBS",           "LUTGEMM_MT16",      "LUTGEMM_MT_TARGET",
     "LUTGEMM_MT_SPLITS",     "LUTGEMM_MT_ORDER",      "LUTGEMM_DEQUANT_KIND", "LUTGEMM_LOG",
-    "LUTGEMM_SPLIT_PRE",     "LUTGEMM_DEQUANT_SPLITS", "LUTGEMM_MT_FUSED", "LUTGEMM_MT4"};
-const int kTuneDefault[LUTGEMM_TUNE_COUNT] = {256, 10000, -1, -1, 0, 0, 1, 8, 0, -1, -1, 0, 4, 0, -1, 1};
+    "LUTGEMM_SPLIT_PRE",     "LUTGEMM_DEQUANT_SPLITS", "LUTGEMM_MT_FUSED", "LUTGEMM_MT4",
+    "LUTGEMM_SPLIT_EXACT"};
+const int kTuneDefault[LUTGEMM_TUNE_COUNT] = {256, 10000, -1, -1, 0, 0, 1, 8, 0, -1, -1, 0, 4, 0, -1, 1, 1};
 std::atomic<int> g_tune[LUTGEMM_TUNE_COUNT];
 
 bool tune_value_ok(int key, int value) {
@@ -227,6 +228,12 @@ LutPlan plan_lut(const Layout &L, int64_t M, bool fused) {
         // (measured: 1 x 11008 x 4096 INT4, 43 splits: 15.5 us in the kernel, 11.8 us with
         // the finalize launch)
         P.inkernel = P.splits > 1 && P.splits <= INKERNEL_MAX_SPLITS;
+        // partial sums that are exact integers (INT8 activations; fixed-point FP16 tables
+        // on weights with one scale per column or tensor) are summed by one 64-bit atomic
+        // per output instead of the four memory round trips of the arrival protocol
+        const bool int_partials =
+            L.act == LUTGEMM_ACT_INT8 || (L.act == LUTGEMM_ACT_FP16 && L.Q == 1);
+        P.exact = P.inkernel && int_partials && M * L.N_pad <= EXACT_MAX && tuning(LUTGEMM_TUNE_SPLIT_EXACT) == 1;
     } else {
         P.kind = 1;
         // tokens per workgroup of the multi-token kernel (lut_mtok.hip): 16 from M = 16 on
@@ -301,6 +308,7 @@ static LutParams lut_params(const Layout &L, const LutPlan &plan, int64_t M, con
     lp.out = out;
     lp.part = plan.splits > 1 ? (float *)((char *)workspace + plan.part_off) : nullptr;
     lp.cnt = plan.kind == 2 && plan.inkernel ? (uint32_t *)workspace : nullptr;
+    lp.acc64 = plan.kind == 2 && plan.exact ? (unsigned long long *)((char *)workspace + CNT_BYTES) : nullptr;
     lp.M = M;
     lp.N = L.N;
     lp.N_pad = L.N_pad;

@@ -203,8 +203,8 @@ __global__ __launch_bounds__(256) void lut_gemv_split_kernel(LutParams p, int wf
     // conditional loads (epilogue operands) first, then the unconditional loads with
     // clamped indices (see lut_gemv2_kernel)
     Epi ep{};
-    if (p.splits == 1)
-        ep = load_epi<INT8>(p, wfmt, m, n, true);
+    if (p.splits == 1 || p.acc64)  // (exact completion: any split may be the one that stores)
+        ep = load_epi<INT8>(p, wfmt, m, n, split == 0);
     else if (INT8 && split == 0 && wfmt == LUTGEMM_WFMT_TERNARY)
         ep.s0 = ((const int *)p.S)[lane_value(m * p.Q)];
     const int s_total = ep.s0;
@@ -243,6 +243,7 @@ __global__ __launch_bounds__(256) void lut_gemv_split_kernel(LutParams p, int wf
 
     float yf = 0.f;
     int yi = s_total;
+    long long yx = 0;  // FP path, exact completion: the integer sum of the split's entries
 #pragma unroll
     for (int kbl = 0; kbl < KBS; ++kbl) {
         if (kbl < nkb) {
@@ -268,13 +269,18 @@ __global__ __launch_bounds__(256) void lut_gemv_split_kernel(LutParams p, int wf
             } else {
                 const float2 e = blk_epilogue(p, bm[kbl], kb0 + kbl);
                 yf = fmaf(e.x, (float)tot, yf) - e.y;
+                yx += tot;
             }
         }
     }
     tl_stamp(p, 2);
-    if (p.splits == 1)
+    if (p.splits == 1) {
         store_out<INT8>(p, wfmt, m, n, yf, yi, ep);
-    else if (p.cnt)
+    } else if (p.acc64) {
+        float2 e = make_float2(0.f, 0.f);
+        if constexpr (!INT8) e = blk_epilogue(p, bm[0], 0);  // the column's one group
+        split_complete_exact<INT8>(p, wfmt, m, n, INT8 ? (long long)yi : yx, e, ep);
+    } else if (p.cnt)
         split_complete<INT8>(p, wfmt, m, n, split, yf, yi, p.cnt + m * gridDim.x + blockIdx.x);
     else  // long K splits: lut_finalize_kernel adds the partials after this kernel
         p.part[((int64_t)split * p.M + m) * p.N_pad + n] = INT8 ? __int_as_float(yi) : yf;

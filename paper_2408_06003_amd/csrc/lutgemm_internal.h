@@ -44,12 +44,15 @@ constexpr int FIN_BATCH = 64;   // split partial sums the finalize kernel reques
 constexpr int TBLK = 96;        // activations per 3-in-5 block (32 triples)
 constexpr int TPB = 32;         // triples per 3-in-5 block
 constexpr int TENT = 16;        // stored entries per triple table (14 used, 2 zero)
-// Every workspace that is needed at all starts with this many bytes of arrival
-// counters (zero between calls, touched only by the split-K GEMV, which re-arms
-// them); partial sums and staged tables always come after it, so no call can leave
-// a nonzero value where a later call, of any problem, expects a zero counter.
-constexpr size_t CNT_AREA = 65536;
-constexpr int64_t CNT_MAX = (int64_t)(CNT_AREA / 4);
+// Every workspace that is needed at all starts with this many bytes that are zero
+// between calls (touched only by the split-K GEMV, which re-arms what it uses): the
+// 32-bit arrival counters in the first CNT_BYTES, then the 64-bit exact split-sum
+// words; partial sums and staged tables always come after it, so no call can leave
+// a nonzero value where a later call, of any problem, expects a zero.
+constexpr size_t CNT_AREA = LUTGEMM_WORKSPACE_ZERO_BYTES;
+constexpr size_t CNT_BYTES = 65536;
+constexpr int64_t CNT_MAX = (int64_t)(CNT_BYTES / 4);
+constexpr int64_t EXACT_MAX = (int64_t)((CNT_AREA - CNT_BYTES) / 8);  // exact split-sum words
 // Largest K split the split-K GEMV completes inside the kernel (one batch of partial
 // loads by the last workgroup); longer splits are summed by the finalize kernel.
 constexpr int INKERNEL_MAX_SPLITS = 32;
@@ -126,6 +129,7 @@ struct LutPlan {
     int kbs;         // 128-blocks of K per split
     int pre;         // split-K GEMV: weight words per lane requested before the tables are waited for
     bool inkernel;   // split-K GEMV: the K split is completed in the kernel (else by the finalize kernel)
+    bool exact;      // split-K GEMV: ... by one 64-bit atomic per output on exact integer partials
     int splits;      // K splits (1 = no workspace)
     int mt;          // tokens per workgroup (multi-token kernel)
     int64_t m_tiles; // token tiles
@@ -185,6 +189,7 @@ struct LutParams {
     unsigned long long *tl; // instrumented builds: per-wavefront phase stamps (see lut_common.h), else NULL
     float *part;           // split partial sums [splits][rows][N_pad] (float or int bits)
     uint32_t *cnt;         // split-K GEMV: arrival counters [M][n_tiles], zero between calls
+    unsigned long long *acc64;  // split-K GEMV, exact completion: words [M][N_pad], zero between calls
     int64_t M, N, N_pad, K, KB, J, Q, G;
     int splits, kbs, out_dtype, accumulate;
     int kpg;               // 128-blocks of K per quantization group (G / 128)

@@ -28,6 +28,17 @@ def test_every_declared_symbol_is_exported():
     assert sorted(L.EXPORTS) == names
 
 
+def test_header_constants_match_binding():
+    """The tuning keys and size constants of lutgemm.h equal the binding's."""
+    text = open(HEADER).read()
+    keys = dict(re.findall(r"LUTGEMM_TUNE_([A-Z_0-9]+)\s*=\s*(\d+)", text))
+    count = int(keys.pop("COUNT"))
+    assert {k: int(v) for k, v in keys.items()} == L.TUNE
+    assert count == len(L.TUNE)
+    m = re.search(r"#define LUTGEMM_WORKSPACE_ZERO_BYTES \(\(size_t\)1 << (\d+)\)", text)
+    assert m and (1 << int(m.group(1))) == L.WORKSPACE_ZERO_BYTES
+
+
 def test_version_and_status_strings():
     assert "gfx950" in L.version()
     for s in range(5):

@@ -82,6 +82,6 @@ def test_graph_of_split_calls_matches_eager(cid, sid, entry, tune):
         for i in range(CALLS):
             assert torch.equal(outs[i], refs[i]), f"replay {rep}, call {i}: differs from the eager result"
     if ws is not None:
-        assert not ws[:65536].any(), "arrival counters not re-armed"
+        assert not ws[:L.WORKSPACE_ZERO_BYTES].any(), "arrival counters not re-armed"
     if ws_fused is not None:
-        assert not ws_fused[:65536].any(), "arrival counters not re-armed"
+        assert not ws_fused[:L.WORKSPACE_ZERO_BYTES].any(), "arrival counters not re-armed"

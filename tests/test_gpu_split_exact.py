@@ -1,0 +1,97 @@
+"""GPU parity of the exact K-split completion of the single-token split-K GEMV.
+
+Where every K split's partial sum is an integer -- the INT32 sums of the INT8 path
+(Section 3.1.3 quantization, Eq. 3 epilogue), or on the FP16 path with one scale per
+column or per tensor the sum of the split's fixed-point table entries -- each split
+adds its partial and an arrival count to one 64-bit word per output with a single
+atomic, and the split that completes the count applies the output epilogue.  The
+sum is exact, so the result does not depend on the order in which splits arrive.
+
+Checked here, all outputs against the CPU oracle: 1-bit weights with a scale per
+column, 2-bit weights with a scale and zero point per column (the zero-point term
+applied once, by the completing split), ternary weights with one FP32 scale, INT8
+activations (bit for bit, and bit for bit equal to the split-order protocol), one and
+two tokens, ragged column tails, 2-8 blocks per split (4-32 splits), accumulation into the output,
+run-to-run determinism, and a layer too wide for the split-sum words (falls back to
+the arrival protocol).  That the words are left zero for the next call, also of
+another problem on the same workspace, is checked in test_gpu_workspace.py.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import workloads as W
+from helpers import GpuProblem, assert_fp_close
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+if not torch.cuda.is_available():
+    pytest.skip("no GPU", allow_module_level=True)
+
+import paper_2408_06003_amd as L  # noqa: E402
+
+
+def banner(msg):
+    print(f"\n[case] {msg}", flush=True)
+
+
+CASES = [
+    # (wfmt, bits, group (K: per column, 0: per tensor), act, FP32 scale, M, K, N, KBS forced)
+    (W.WFMT_BINARY, 1, "K", W.ACT_FP16, False, 1, 8192, 777, 0),
+    (W.WFMT_BINARY, 1, "K", W.ACT_FP16, False, 2, 8192, 300, 2),
+    (W.WFMT_UINT, 2, "K", W.ACT_FP16, False, 1, 4096, 520, 2),
+    (W.WFMT_UINT, 4, "K", W.ACT_FP16, False, 2, 6144, 260, 2),
+    (W.WFMT_TERNARY, 2, 0, W.ACT_FP16, True, 2, 4096, 700, 4),
+    (W.WFMT_TERNARY, 2, 0, W.ACT_INT8, True, 1, 8192, 777, 0),
+    (W.WFMT_BINARY, 1, "K", W.ACT_INT8, False, 2, 8192, 300, 2),
+    (W.WFMT_BINARY, 1, 0, W.ACT_INT8, True, 1, 4096, 1000, 8),
+]
+
+
+@pytest.mark.parametrize("wfmt,bits,G,act,sf,M,K,N,kbs", CASES)
+def test_exact_split_parity(wfmt, bits, G, act, sf, M, K, N, kbs, tune):
+    tune(GEMV_KIND=2, SPLIT_EXACT=1)
+    if kbs:
+        tune(KBS=kbs)
+    group = K if G == "K" else G
+    banner(f"exact split wfmt={wfmt} b={bits} G={group} act={act} M={M} K={K} N={N} kbs={kbs or 'planned'}")
+    inp = W.make_custom(wfmt, bits, group, act, M=M, K=K, N=N, seed=1200 + 17 * wfmt + bits + kbs, scale_fp32=sf)
+    gp = GpuProblem(inp)
+    base = torch.randn(M, N, device="cuda", dtype=torch.float32)
+    if act == W.ACT_INT8:
+        acc_ref, y_ref = oracle.reference_output(inp)
+        yi = gp.lut(out_dtype=torch.int32)
+        yf = gp.lut(out_dtype=torch.float32)
+        assert np.array_equal(yi.cpu().numpy().astype(np.int64), acc_ref), "INT32 accumulator differs from the oracle"
+        assert np.array_equal(yf.cpu().numpy(), y_ref), "FP32 output differs from the oracle"
+        assert torch.equal(gp.lut(out_dtype=torch.int32), yi), "not deterministic"
+        # the same integer sums as the split-order protocol
+        L.set_tuning("SPLIT_EXACT", 0)
+        assert torch.equal(gp.lut(out_dtype=torch.int32), yi), "differs from the arrival protocol"
+        assert torch.equal(gp.lut(out_dtype=torch.float32), yf), "differs from the arrival protocol"
+        L.set_tuning("SPLIT_EXACT", 1)
+    else:
+        ref = oracle.reference_output(inp)
+        for od in (torch.float16, torch.float32):
+            y = gp.lut(out_dtype=od)
+            fro, mx = assert_fp_close(y.float().cpu().numpy(), ref, f"exact split {od}")
+            print(f"[err] {od}: relFro {fro:.3e} max/rms {mx:.3e}", flush=True)
+            assert torch.equal(gp.lut(out_dtype=od), y), "not deterministic"
+        yf = gp.lut(out_dtype=torch.float32)
+    acc = base.clone()
+    gp.lut(out=acc, accumulate=True, out_dtype=torch.float32)
+    assert torch.equal(acc, base + yf), "accumulation through the exact completion"
+
+
+def test_exact_split_wide_layer_falls_back(tune):
+    """Two tokens of 65 536 columns need more split-sum words than the workspace's zero
+    region holds: the arrival protocol completes the split instead, same bar."""
+    tune(GEMV_KIND=2, KBS=2)
+    inp = W.make_custom(W.WFMT_BINARY, 1, 2048, W.ACT_FP16, M=2, K=2048, N=65536, seed=1301)
+    banner("exact split: 2 x 2048 x 65536, beyond the split-sum words")
+    gp = GpuProblem(inp)
+    ref = oracle.reference_output(inp)
+    fro, mx = assert_fp_close(gp.lut(out_dtype=torch.float32).cpu().numpy(), ref, "wide layer")
+    print(f"[err] relFro {fro:.3e} max/rms {mx:.3e}", flush=True)
+

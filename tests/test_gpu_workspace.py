@@ -3,7 +3,8 @@
 * One zero-filled workspace, sized for the largest call, is used in turn by calls on
   different problems: the multi-token kernel with a K split (partial sums summed by
   the finalize kernel), the single-token split-K GEMV (its K split completed inside
-  the kernel by arrival counters that must be zero when a call starts), the fused
+  the kernel by arrival counters, or for 1-bit weights with a scale per column by
+  exact split-sum words, that must be zero when a call starts), the fused
   entry point on both its fused and its precompute + mpGEMM path.  Every output must
   equal, bit for bit, the same call made with a fresh workspace of its own.
 * Guard bands (canaries) of 4 KiB filled with a byte pattern around the output, the
@@ -114,7 +115,7 @@ def test_shared_workspace_across_problems(tune):
         shared.check(f"{name}: shared workspace")
         assert torch.equal(y, ref), f"{name}: shared workspace changed the result"
         # the arrival counters are left zero for the next call
-        assert not shared.view(torch.uint8, (need,))[:65536].any(), f"{name}: counters not re-armed"
+        assert not shared.view(torch.uint8, (need,))[:L.WORKSPACE_ZERO_BYTES].any(), f"{name}: counters not re-armed"
 
 
 def test_guard_bands_dequant_and_noalloc():
