@@ -223,17 +223,18 @@ LutPlan plan_lut(const Layout &L, int64_t M, bool fused) {
         P.kbs = kbs;
         P.splits = (int)((L.KB + kbs - 1) / kbs);
         P.pre = tuning(LUTGEMM_TUNE_SPLIT_PRE);
-        // the last workgroup of a tile loads every split's partial sum in one batch: up to
-        // INKERNEL_MAX_SPLITS; beyond that the finalize kernel's wide batches are faster
-        // (measured: 1 x 11008 x 4096 INT4, 43 splits: 15.5 us in the kernel, 11.8 us with
-        // the finalize launch)
-        P.inkernel = P.splits > 1 && P.splits <= INKERNEL_MAX_SPLITS;
-        // partial sums that are exact integers (INT8 activations; fixed-point FP16 tables
-        // on weights with one scale per column or tensor) are summed by one 64-bit atomic
-        // per output instead of the four memory round trips of the arrival protocol
-        const bool int_partials =
-            L.act == LUTGEMM_ACT_INT8 || (L.act == LUTGEMM_ACT_FP16 && L.Q == 1);
-        P.exact = P.inkernel && int_partials && M * L.N_pad <= EXACT_MAX && tuning(LUTGEMM_TUNE_SPLIT_EXACT) == 1;
+        // Partial sums that are integers (INT8 activations; fixed-point FP16 table entries
+        // on weights with one scale per column or tensor) or fixed point (FP16
+        // activations, per-column exponent stored with the packed weights) are summed
+        // exactly by one 64-bit atomic per output: one memory round trip instead of the
+        // four of the arrival protocol, and no limit from a batch of partial loads
+        P.exact = P.splits > 1 && P.splits <= EXACT_MAX_SPLITS && L.act != LUTGEMM_ACT_FP16_LUT8 &&
+                  M * L.N_pad <= EXACT_MAX && tuning(LUTGEMM_TUNE_SPLIT_EXACT) == 1;
+        P.inkernel = P.exact || (P.splits > 1 && P.splits <= INKERNEL_MAX_SPLITS);
+        // (else the arrival protocol: the last workgroup of a tile loads every split's
+        // partial sum in one batch, up to INKERNEL_MAX_SPLITS; beyond that the finalize
+        // kernel's wide batches are faster -- measured: 1 x 11008 x 4096 INT4, 43 splits:
+        // 15.5 us in the kernel, 11.8 us with the finalize launch)
     } else {
         P.kind = 1;
         // tokens per workgroup of the multi-token kernel (lut_mtok.hip): 16 from M = 16 on
@@ -309,6 +310,7 @@ static LutParams lut_params(const Layout &L, const LutPlan &plan, int64_t M, con
     lp.part = plan.splits > 1 ? (float *)((char *)workspace + plan.part_off) : nullptr;
     lp.cnt = plan.kind == 2 && plan.inkernel ? (uint32_t *)workspace : nullptr;
     lp.acc64 = plan.kind == 2 && plan.exact ? (unsigned long long *)((char *)workspace + CNT_BYTES) : nullptr;
+    lp.bnd = (const int *)((const char *)packed + L.bnd_off);
     lp.M = M;
     lp.N = L.N;
     lp.N_pad = L.N_pad;
@@ -322,19 +324,7 @@ static LutParams lut_params(const Layout &L, const LutPlan &plan, int64_t M, con
     lp.kpg = (int)(L.G / KBLK);
     lp.per_tensor = L.per_tensor ? 1 : 0;
     lp.inv_kpg = 1.0f / (float)lp.kpg;
-    if (L.wfmt == LUTGEMM_WFMT_BINARY) {  // codes {0,1} read as {-1,+1}: s' = s, z' = 0
-        lp.cs = 1.f;
-        lp.cz = 0.f;
-        lp.c0 = 0.f;
-    } else if (L.wfmt == LUTGEMM_WFMT_TERNARY) {  // q = w + 1, z = 1, b = 2: s' = s/2, z' = -1
-        lp.cs = 0.5f;
-        lp.cz = 0.f;
-        lp.c0 = -1.f;
-    } else {  // Eq. 2: s' = s/2, z' = 2z + 1 - 2^b
-        lp.cs = 0.5f;
-        lp.cz = 2.f;
-        lp.c0 = 1.f - (float)(1 << L.bits);
-    }
+    format_consts(L.wfmt, L.bits, lp.cs, lp.cz, lp.c0);
     lp.out_dtype = out_dtype;
     lp.accumulate = accumulate;
 #ifdef LUTGEMM_TIMELINE
@@ -464,6 +454,7 @@ lutgemm_status_t lutgemm_pack_weights(const lutgemm_problem_t *problem, const vo
     pp.planes = (uint4 *)packed;
     pp.sgn = L.tri ? (uint32_t *)((char *)packed + L.sgn_off) : nullptr;
     pp.meta = (char *)packed + L.meta_off;
+    pp.bnd = (int *)((char *)packed + L.bnd_off);
     pp.K = L.K;
     pp.N = L.N;
     pp.N_pad = L.N_pad;

@@ -4,6 +4,8 @@
 #pragma once
 
 #include <hip/hip_runtime.h>
+
+#include <climits>
 #include <hip/hip_fp16.h>
 
 #include "lutgemm_internal.h"
@@ -518,33 +520,37 @@ __device__ __forceinline__ void split_complete(const LutParams &p, int wfmt, int
     asm volatile("; counter re-armed from %0" ::"v"(rearmed));
 }
 
-// Completes a K split by one 64-bit atomic per output, for partial sums that are
-// exact integers: the INT32 sums of the INT8 path, or on the FP16 path with one
-// scale per column or tensor the integer sum v of the split's fixed-point table
-// entries (every block of the column shares s', so its output is s' 2^-FIX_SHIFT
-// times the sum over all splits, minus the zero-point term).  The zeroed word of
-// (m, n) accumulates c 2^58 + V (c arrivals, V the signed sum so far, |V| < 2^57):
-// each split adds 2^58 + v with one agent-coherent atomic and gets the previous word
-// back, and the split that sees c = splits - 1 holds the exact total, which integer
-// addition gives whatever the order of arrival.  That split applies the epilogue
-// (operands loaded before the atomic, so only the atomic's round trip precedes the
-// store) and clears the word, waiting for the clear's return so that it is performed
-// before the kernel ends.  Bounds: |v| <= KBS 32 2^(FIX_SHIFT + 2) 2^b and the total
-// at most 2^13 times that (K <= 2^20), far below 2^57.  `e` = (s' 2^-FIX_SHIFT,
-// s' z' S) of the column (FP path).
+// Completes a K split by one 64-bit atomic per output, summing exactly.  A split's
+// partial sum v is an integer: the INT32 sum of the INT8 path; on the FP16 path with
+// one scale per column or tensor the integer sum of the split's fixed-point table
+// entries (every block shares s', so the output is s' 2^-FIX_SHIFT times the total
+// minus the zero-point term: sx, sy); otherwise the FP32 partial sum in fixed point,
+// v = rint(partial 2^-E) with the column's exponent E (|v| < 2^BND_BITS, see
+// pack_bound_kernel), the output 2^E times the total.  The zeroed word of (m, n)
+// accumulates c 2^57 + V (c arrivals, V the signed sum so far, |V| < 2^56): each split
+// adds 2^57 + v with one agent-coherent atomic and gets the previous word back, and
+// the split that sees c = splits - 1 holds the exact total, which integer addition
+// gives whatever the order of arrival.  That split applies the epilogue (operands
+// loaded before the atomic, so only the atomic's round trip precedes the store) and
+// clears the word, waiting for the clear's return so that it is performed before the
+// kernel ends.  E = INT_MIN selects the (sx, sy) form.
 template <bool INT8>
 __device__ __forceinline__ void split_complete_exact(const LutParams &p, int wfmt, int64_t m, int64_t n, long long v,
-                                                     float2 e, const Epi &ep) {
+                                                     float sx, float sy, int E, const Epi &ep) {
     unsigned long long *w = p.acc64 + m * p.N_pad + n;
-    const unsigned long long old = __hip_atomic_fetch_add(w, (1ull << 58) + (unsigned long long)v, __ATOMIC_RELAXED,
+    const unsigned long long old = __hip_atomic_fetch_add(w, (1ull << 57) + (unsigned long long)v, __ATOMIC_RELAXED,
                                                           __HIP_MEMORY_SCOPE_AGENT);
-    const unsigned long long c = (old + (1ull << 57)) >> 58;
+    const unsigned long long c = (old + (1ull << 56)) >> 57;
     if (c != (unsigned long long)(p.splits - 1)) return;
     const unsigned long long cleared = __hip_atomic_exchange(w, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    const long long tot = (long long)(old - (c << 58)) + v;
-    const float yf = INT8 ? 0.f : fmaf(e.x, (float)tot, -e.y);
+    const long long tot = (long long)(old - (c << 57)) + v;
+    float yf = 0.f;
+    if constexpr (!INT8) yf = E == INT_MIN ? fmaf(sx, (float)tot, -sy) : ldexpf((float)tot, E);
     store_out<INT8>(p, wfmt, m, n, yf, (int)tot, ep);
     asm volatile("; exact split word cleared from %0" ::"v"(cleared));
 }
+
+// The fixed-point value rint(x 2^-E) of an FP32 partial sum (|x 2^-E| < 2^BND_BITS).
+__device__ __forceinline__ long long to_fixed(float x, int E) { return (long long)rintf(ldexpf(x, -E)); }
 
 }  // namespace lutgemm

@@ -354,8 +354,9 @@ static void launch_fused_bits(const LutParams &p, const Layout &L, const LutPlan
 // amax / 127 as the precompute operator, then the exact INT32 entries of its
 // quantized group; the ternary offset S is summed over the workgroup's K range
 // (the ranges' sums add up to the token's).  Lookups and the split sum are exact,
-// so the output equals the two-call path's bit for bit; with short splits the INT32
-// partials are summed by one 64-bit atomic per output (split_complete_exact).
+// so the output equals the two-call path's bit for bit.  The split sum is completed
+// exactly by one 64-bit atomic per output (split_complete_exact): INT32 partials, or
+// FP32 partials in fixed point.
 template <int BITS, int KBS, int PRE, bool INT8>
 __global__ __launch_bounds__(256) void lut_fused_split_kernel(LutParams p, int wfmt) {
     constexpr int NWD = KBS * BITS;              // weight words per lane
@@ -377,8 +378,11 @@ __global__ __launch_bounds__(256) void lut_fused_split_kernel(LutParams p, int w
 
     // conditional loads first, then unconditional clamped ones (see lut_gemv_kernel)
     Epi ep{};
-    // (INT8 with the exact split completion: any split may be the one that stores)
-    if (p.splits == 1 || (INT8 && p.acc64)) ep = load_epi<INT8>(p, wfmt, m, n, false);
+    // (with the exact split completion any split may be the one that stores)
+    if (p.splits == 1 || p.acc64) ep = load_epi<INT8>(p, wfmt, m, n, false);
+    // exact completion of FP partial sums: fixed point in units of 2^(E + 16), E the
+    // column's exponent for activations below 1 (these tables hold them unscaled)
+    const int bndE = (!INT8 && p.acc64) ? p.bnd[lane_value(n)] + 16 : 0;
     // activations: lane g holds group g of the workgroup's range (KBS x 32 <= 256 groups)
     const uint16_t *arow = p.act + m * p.K;
     const int g = tid, gc = g < nkb * GPB ? g : nkb * GPB - 1;
@@ -533,9 +537,12 @@ __global__ __launch_bounds__(256) void lut_fused_split_kernel(LutParams p, int w
     if (p.splits == 1) {
         ep.tok = tok;
         store_out<INT8>(p, wfmt, m, n, yf, yi, ep);
-    } else if (INT8 && p.acc64) {  // exact INT32 partials: one atomic per output
+    } else if (p.acc64) {  // exact split sum: one atomic per output
         ep.tok = tok;
-        split_complete_exact<INT8>(p, wfmt, m, n, (long long)yi, make_float2(0.f, 0.f), ep);
+        if (INT8)
+            split_complete_exact<INT8>(p, wfmt, m, n, (long long)yi, 0.f, 0.f, INT_MIN, ep);
+        else
+            split_complete_exact<INT8>(p, wfmt, m, n, to_fixed(yf, bndE), 0.f, 0.f, bndE, ep);
     } else if (p.cnt) {
         split_complete<INT8>(p, wfmt, m, n, split, yf, yi, p.cnt + m * gridDim.x + blockIdx.x, INT8 ? tok : -1.f);
     } else {  // long K splits: lut_finalize_kernel adds the partials after this kernel

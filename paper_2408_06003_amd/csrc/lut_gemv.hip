@@ -208,6 +208,8 @@ __global__ __launch_bounds__(256) void lut_gemv_split_kernel(LutParams p, int wf
     else if (INT8 && split == 0 && wfmt == LUTGEMM_WFMT_TERNARY)
         ep.s0 = ((const int *)p.S)[lane_value(m * p.Q)];
     const int s_total = ep.s0;
+    // exact completion of FP partial sums in fixed point: the column's exponent
+    const int bndE = (!INT8 && p.acc64 && p.Q != 1) ? p.bnd[lane_value(n)] : 0;
     uint2 tq[QPT];
 #pragma unroll
     for (int r = 0; r < QPT; ++r) {
@@ -277,9 +279,14 @@ __global__ __launch_bounds__(256) void lut_gemv_split_kernel(LutParams p, int wf
     if (p.splits == 1) {
         store_out<INT8>(p, wfmt, m, n, yf, yi, ep);
     } else if (p.acc64) {
-        float2 e = make_float2(0.f, 0.f);
-        if constexpr (!INT8) e = blk_epilogue(p, bm[0], 0);  // the column's one group
-        split_complete_exact<INT8>(p, wfmt, m, n, INT8 ? (long long)yi : yx, e, ep);
+        if (INT8) {
+            split_complete_exact<INT8>(p, wfmt, m, n, (long long)yi, 0.f, 0.f, INT_MIN, ep);
+        } else if (p.Q == 1) {  // integer entries, the column's one group applied at the end
+            const float2 e = blk_epilogue(p, bm[0], 0);
+            split_complete_exact<INT8>(p, wfmt, m, n, yx, e.x, e.y, INT_MIN, ep);
+        } else {
+            split_complete_exact<INT8>(p, wfmt, m, n, to_fixed(yf, bndE), 0.f, 0.f, bndE, ep);
+        }
     } else if (p.cnt)
         split_complete<INT8>(p, wfmt, m, n, split, yf, yi, p.cnt + m * gridDim.x + blockIdx.x);
     else  // long K splits: lut_finalize_kernel adds the partials after this kernel

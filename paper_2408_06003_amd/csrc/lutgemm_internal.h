@@ -53,6 +53,11 @@ constexpr size_t CNT_AREA = LUTGEMM_WORKSPACE_ZERO_BYTES;
 constexpr size_t CNT_BYTES = 65536;
 constexpr int64_t CNT_MAX = (int64_t)(CNT_BYTES / 4);
 constexpr int64_t EXACT_MAX = (int64_t)((CNT_AREA - CNT_BYTES) / 8);  // exact split-sum words
+// Exact split completion: a split-sum word holds (arrivals) 2^57 + V with |V| < 2^56,
+// so at most 127 splits; FP partial sums are fixed point in units of 2^E with E
+// chosen per column so that the column's partial sums stay below 2^BND_BITS.
+constexpr int EXACT_MAX_SPLITS = 127;
+constexpr int BND_BITS = 54;
 // Largest K split the split-K GEMV completes inside the kernel (one batch of partial
 // loads by the last workgroup); longer splits are summed by the finalize kernel.
 constexpr int INKERNEL_MAX_SPLITS = 32;
@@ -66,8 +71,25 @@ struct Layout {
     int bits, wfmt, act;
     bool per_tensor;
     bool tri;                          // ternary 3-in-5: KB counts 96-blocks, J triples
-    size_t planes_bytes, sgn_off, meta_off, meta_bytes, packed_bytes;
+    size_t planes_bytes, sgn_off, meta_off, meta_bytes, bnd_off, packed_bytes;
 };
+
+// Eq. 2 reinterpretation constants of a weight format: s' = cs s, z' = cz z + c0.
+inline void format_consts(int wfmt, int bits, float &cs, float &cz, float &c0) {
+    if (wfmt == LUTGEMM_WFMT_BINARY) {  // codes {0,1} read as {-1,+1}: s' = s, z' = 0
+        cs = 1.f;
+        cz = 0.f;
+        c0 = 0.f;
+    } else if (wfmt == LUTGEMM_WFMT_TERNARY) {  // q = w + 1, z = 1, b = 2: s' = s/2, z' = -1
+        cs = 0.5f;
+        cz = 0.f;
+        c0 = -1.f;
+    } else {  // Eq. 2: s' = s/2, z' = 2z + 1 - 2^b
+        cs = 0.5f;
+        cz = 2.f;
+        c0 = 1.f - (float)(1 << bits);
+    }
+}
 
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
@@ -97,7 +119,10 @@ inline Layout make_layout(const lutgemm_problem_t &p) {
         L.meta_off = align256(L.planes_bytes);
     }
     L.meta_bytes = L.per_tensor ? 256 : (size_t)L.Q * L.N_pad * 4;
-    L.packed_bytes = L.meta_off + align256(L.meta_bytes);
+    // per column: the fixed-point exponent of the exact K-split completion (INT32;
+    // not kept for 3-in-5 weights, whose kernel never splits K)
+    L.bnd_off = L.meta_off + align256(L.meta_bytes);
+    L.packed_bytes = L.bnd_off + (L.tri ? 0 : align256((size_t)L.N_pad * 4));
     return L;
 }
 
@@ -160,6 +185,7 @@ struct PackParams {
     uint4 *planes;
     uint32_t *sgn;         // 3-in-5 sign words
     void *meta;
+    int *bnd;              // per-column fixed-point exponent of the exact split completion
     int64_t K, N, N_pad, KB, Q, G;
     int bits, wfmt, per_tensor, scale_fp32;
 };
@@ -190,6 +216,7 @@ struct LutParams {
     float *part;           // split partial sums [splits][rows][N_pad] (float or int bits)
     uint32_t *cnt;         // split-K GEMV: arrival counters [M][n_tiles], zero between calls
     unsigned long long *acc64;  // split-K GEMV, exact completion: words [M][N_pad], zero between calls
+    const int *bnd;        // per-column fixed-point exponent E of FP partial sums (packed weights)
     int64_t M, N, N_pad, K, KB, J, Q, G;
     int splits, kbs, out_dtype, accumulate;
     int kpg;               // 128-blocks of K per quantization group (G / 128)

@@ -142,6 +142,43 @@ __global__ __launch_bounds__(256) void pack_meta_kernel(PackParams p) {
     }
 }
 
+// Fixed-point exponent E of column n for the exact K-split completion of FP partial
+// sums (split_complete_exact).  With the token scaled to |x| < 1 by the precompute, a
+// table entry (a signed sum of 4 activations) is below 4 in magnitude, stored as at
+// most 4 2^FIX_SHIFT, so one 128-block of bit-plane t adds at most |s'| 2^t 128 to a
+// partial sum and the zero-point term of a group is at most |s' z'| G (|S| <= G).
+// Their sum over the column's groups, B (with 1/16 added for the FP32 rounding of the
+// partial sums), bounds every split's partial sum and their total; E is the smallest
+// integer with B < 2^(BND_BITS + E).  (The fused split kernel, whose tables hold the
+// unscaled FP16 activations, |x| <= 65504 < 2^16, uses E + 16.)  E = 0 for padding
+// columns and all-zero scales; B is not finite only for non-finite scales, whose
+// outputs are unspecified on this path.
+__global__ __launch_bounds__(256) void pack_bound_kernel(PackParams p, float cs, float cz, float c0) {
+    const int64_t n = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (n >= p.N_pad) return;
+    int E = 0;
+    if (n < p.N) {
+        const double kpg = (double)(p.G / KBLK), planes = (double)((1 << p.bits) - 1), G = (double)p.G;
+        double B = 0.0;
+        for (int64_t q = 0; q < p.Q; ++q) {
+            float s, z;
+            if (p.per_tensor) {
+                s = ((const float *)p.meta)[0];
+                z = ((const float *)p.meta)[1];
+            } else {
+                const uint32_t w = ((const uint32_t *)p.meta)[q * p.N_pad + n];
+                s = __half2float(__ushort_as_half((unsigned short)(w & 0xFFFFu)));
+                z = __half2float(__ushort_as_half((unsigned short)(w >> 16)));
+            }
+            const double sp = (double)cs * (double)s, zp = (double)cz * (double)z + (double)c0;
+            B += kpg * fabs(sp) * 128.0 * planes + fabs(sp * zp) * G;
+        }
+        B *= 1.0625;
+        if (B > 0.0 && B <= 1e300) E = ilogb(B) + 1 - BND_BITS;
+    }
+    p.bnd[n] = E;
+}
+
 int launch_pack(const PackParams &p, void *stream) {
     hipStream_t s = (hipStream_t)stream;
     int64_t total = p.N_pad * p.KB;
@@ -157,6 +194,12 @@ int launch_pack(const PackParams &p, void *stream) {
     int64_t mblocks = (mt + 255) / 256;
     if (mblocks > 65535 * 16) mblocks = 65535 * 16;
     hipLaunchKernelGGL(pack_meta_kernel, dim3((unsigned)mblocks), dim3(256), 0, s, p);
+    e = hipGetLastError();
+    if (e != hipSuccess) return (int)e;
+    if (p.wfmt == LUTGEMM_WFMT_TERNARY_3IN5) return (int)hipSuccess;
+    float cs, cz, c0;
+    format_consts(p.wfmt, p.bits, cs, cz, c0);
+    hipLaunchKernelGGL(pack_bound_kernel, dim3((unsigned)((p.N_pad + 255) / 256)), dim3(256), 0, s, p, cs, cz, c0);
     return (int)hipGetLastError();
 }
 

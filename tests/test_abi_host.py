@@ -112,7 +112,8 @@ def test_size_formulas():
     assert L.table_size(p, M) >= t_off + 4 * M
     n_pad = 1024
     planes = K * n_pad * 4 // 8
-    assert planes <= L.packed_weight_size(p) <= planes + (K // 128) * n_pad * 4 + 512
+    # planes, (s, z) per group and column, and one fixed-point exponent per column
+    assert planes <= L.packed_weight_size(p) <= planes + (K // 128) * n_pad * 4 + n_pad * 4 + 512
 
 
 def test_size_formulas_ternary_3in5():

@@ -1,20 +1,24 @@
 """GPU parity of the exact K-split completion of the single-token split-K GEMV.
 
-Where every K split's partial sum is an integer -- the INT32 sums of the INT8 path
-(Section 3.1.3 quantization, Eq. 3 epilogue), or on the FP16 path with one scale per
-column or per tensor the sum of the split's fixed-point table entries -- each split
-adds its partial and an arrival count to one 64-bit word per output with a single
-atomic, and the split that completes the count applies the output epilogue.  The
-sum is exact, so the result does not depend on the order in which splits arrive.
+Every K split turns its partial sum into an integer -- the INT32 sum of the INT8
+path (Section 3.1.3 quantization, Eq. 3 epilogue); on the FP16 path with one scale
+per column or per tensor the sum of the split's fixed-point table entries; otherwise
+the FP32 partial sum in fixed point with a per-column exponent that the packer
+derives from a bound on the column's partial sums -- and adds it with an arrival
+count to one 64-bit word per output with a single atomic; the split that completes
+the count applies the output epilogue.  The sum is exact, so the result does not
+depend on the order in which splits arrive.
 
 Checked here, all outputs against the CPU oracle: 1-bit weights with a scale per
-column, 2-bit weights with a scale and zero point per column (the zero-point term
-applied once, by the completing split), ternary weights with one FP32 scale, INT8
-activations (bit for bit, and bit for bit equal to the split-order protocol), one and
-two tokens, ragged column tails, 2-8 blocks per split (4-32 splits), accumulation into the output,
-run-to-run determinism, and a layer too wide for the split-sum words (falls back to
-the arrival protocol).  That the words are left zero for the next call, also of
-another problem on the same workspace, is checked in test_gpu_workspace.py.
+column, 2- and 4-bit weights with a scale and zero point per column (the zero-point
+term applied once, by the completing split) and per group of 128 (fixed point; up to
+64 splits, beyond the arrival protocol's 32), ternary weights with one FP32 scale,
+scales spread over 2^22 within a column, INT8 activations (bit for bit, and bit for
+bit equal to the split-order protocol), the fused entry point (tables built from the
+unscaled activations), one and two tokens, ragged column tails, accumulation into the
+output, run-to-run determinism, and a layer too wide for the split-sum words (falls
+back to the arrival protocol).  That the words are left zero for the next call, also
+of another problem on the same workspace, is checked in test_gpu_workspace.py.
 """
 import numpy as np
 import pytest
@@ -46,6 +50,10 @@ CASES = [
     (W.WFMT_TERNARY, 2, 0, W.ACT_INT8, True, 1, 8192, 777, 0),
     (W.WFMT_BINARY, 1, "K", W.ACT_INT8, False, 2, 8192, 300, 2),
     (W.WFMT_BINARY, 1, 0, W.ACT_INT8, True, 1, 4096, 1000, 8),
+    (W.WFMT_UINT, 4, 128, W.ACT_FP16, False, 1, 11008, 300, 0),
+    (W.WFMT_UINT, 2, 128, W.ACT_FP16, False, 2, 8192, 520, 1),
+    (W.WFMT_UINT, 2, 1024, W.ACT_FP16, False, 1, 4096, 777, 2),
+    (W.WFMT_TERNARY, 2, 128, W.ACT_FP16, False, 1, 4096, 260, 0),
 ]
 
 
@@ -95,3 +103,39 @@ def test_exact_split_wide_layer_falls_back(tune):
     fro, mx = assert_fp_close(gp.lut(out_dtype=torch.float32).cpu().numpy(), ref, "wide layer")
     print(f"[err] relFro {fro:.3e} max/rms {mx:.3e}", flush=True)
 
+
+
+@pytest.mark.parametrize("wfmt,bits,G,act,sf,M,K,N,kbs", [c for c in CASES if c[3] == W.ACT_FP16])
+def test_exact_split_fused_entry(wfmt, bits, G, act, sf, M, K, N, kbs, tune):
+    """The fused entry point's split-K kernel (tables built from the activations of its
+    K range, unscaled FP32 entries) with the fixed-point exact completion."""
+    tune(GEMV_KIND=2, SPLIT_EXACT=1)
+    if kbs:
+        tune(KBS=kbs)
+    group = K if G == "K" else G
+    banner(f"exact split, fused entry: wfmt={wfmt} b={bits} G={group} M={M} K={K} N={N} kbs={kbs or 'planned'}")
+    inp = W.make_custom(wfmt, bits, group, act, M=M, K=K, N=N, seed=1400 + 17 * wfmt + bits + kbs, scale_fp32=sf)
+    gp = GpuProblem(inp)
+    ref = oracle.reference_output(inp)
+    for od in (torch.float16, torch.float32):
+        y = gp.fused(out_dtype=od)
+        fro, mx = assert_fp_close(y.float().cpu().numpy(), ref, f"fused exact split {od}")
+        print(f"[err] {od}: relFro {fro:.3e} max/rms {mx:.3e}", flush=True)
+        assert torch.equal(gp.fused(out_dtype=od), y), "not deterministic"
+
+
+def test_exact_split_extreme_scales(tune):
+    """Scales 6e-5 and 300 in the same columns (2^22 apart) and a token scaled by 1000:
+    the fixed-point unit follows the largest scale of each column, the small groups
+    keep their precision within the FP bar."""
+    tune(GEMV_KIND=2, KBS=1, SPLIT_EXACT=1)
+    inp = W.make_custom(W.WFMT_UINT, 2, 128, W.ACT_FP16, M=2, K=4096, N=300, seed=1381)
+    inp.scales[:, 0::2] = np.float16(6e-5)
+    inp.scales[:, 1] = np.float16(300.0)
+    inp.act[1] = (inp.act[1].astype(np.float32) * 1000).astype(np.float16)
+    banner("exact split: extreme scales")
+    gp = GpuProblem(inp)
+    ref = oracle.reference_output(inp)
+    for run in (gp.lut, gp.fused):
+        fro, mx = assert_fp_close(run(out_dtype=torch.float32).cpu().numpy(), ref, "extreme scales")
+        print(f"[err] relFro {fro:.3e} max/rms {mx:.3e}", flush=True)
