@@ -160,6 +160,17 @@ LutPlan plan_lut(const Layout &L, int64_t M, bool fused) {
         return P;
     }
     int kind = M > 2 ? 1 : (weight_bytes <= (int64_t)tuning(LUTGEMM_TUNE_WHOLEK_MAX_KB) * 1000 ? 0 : 2);
+    // with FP16 activations the split-K GEMV and its exact completion also win on
+    // smaller layers once one 128-block per workgroup gives 2 x `target` workgroups
+    // (measured, table-fed / fused entry, us: INT4 1 x 4096 x 4096 5.3 / 5.5 against the
+    // whole-K GEMV's 5.8 / 7.4; INT2 1 x 1024 x 1024, 32 such workgroups, stays whole-K:
+    // 3.15 against 3.58); INT8 activations keep the whole-K GEMV (ternary 1 x 4096 x 4096:
+    // 4.66 / 4.79 against 4.20 / 4.83)
+    const bool exact_fmt = L.act != LUTGEMM_ACT_FP16_LUT8 && M * L.N_pad <= EXACT_MAX &&
+                           tuning(LUTGEMM_TUNE_SPLIT_EXACT) == 1;
+    if (kind == 0 && exact_fmt && L.act == LUTGEMM_ACT_FP16 && (L.N_pad / NTILE) * M * L.KB >= 2 * target &&
+        L.KB <= EXACT_MAX_SPLITS)
+        kind = 2;
     const int forced_kind = tuning(LUTGEMM_TUNE_GEMV_KIND);
     if (M <= 2 && (forced_kind == 0 || forced_kind == 1 || forced_kind == 2)) kind = forced_kind;
     // the split-K GEMV keeps one arrival counter per (token, 256-column tile); layers with
@@ -203,7 +214,11 @@ LutPlan plan_lut(const Layout &L, int64_t M, bool fused) {
         // K split completed inside the kernel.  About eight weight words per lane (KBS =
         // 8 / b): few, long-lived workgroups that the GPU holds all at once, so the
         // end-of-workgroup arrival protocol never delays a waiting workgroup; KBS is
-        // halved only while the grid would have fewer than 2 x `target` workgroups
+        // halved only while the grid would have fewer than 2 x `target` workgroups.
+        // With the exact completion nothing waits: shorter workgroups pay until about
+        // 6 x `target` of them, while at most 64 splits add into one output word
+        // (measured, us, KBS chosen / the next: INT4 1 x 4096 x 12288 8.4 / 8.9, INT4
+        // 1 x 11008 x 4096 8.5 / 9.6, 1-bit 1 x 8192 x 28672 9.7 / 10.7)
         P.kind = 2;
         P.mt = 1;
         P.m_tiles = M;
@@ -214,6 +229,8 @@ LutPlan plan_lut(const Layout &L, int64_t M, bool fused) {
         const int forced = tuning(LUTGEMM_TUNE_KBS);
         if (forced == 1 || forced == 2 || forced == 4 || forced == 8) {
             kbs = forced > kmax ? kmax : forced;
+        } else if (exact_fmt) {
+            while (kbs > 1 && P.n_tiles * M * n_splits(kbs) < 6 * target && n_splits(kbs >> 1) <= 64) kbs >>= 1;
         } else {
             while (kbs > 1 && P.n_tiles * M * n_splits(kbs) < 2 * target) kbs >>= 1;
             // 1-bit weights: four words per lane (twice the workgroups) while the split
@@ -228,8 +245,7 @@ LutPlan plan_lut(const Layout &L, int64_t M, bool fused) {
         // activations, per-column exponent stored with the packed weights) are summed
         // exactly by one 64-bit atomic per output: one memory round trip instead of the
         // four of the arrival protocol, and no limit from a batch of partial loads
-        P.exact = P.splits > 1 && P.splits <= EXACT_MAX_SPLITS && L.act != LUTGEMM_ACT_FP16_LUT8 &&
-                  M * L.N_pad <= EXACT_MAX && tuning(LUTGEMM_TUNE_SPLIT_EXACT) == 1;
+        P.exact = P.splits > 1 && P.splits <= EXACT_MAX_SPLITS && exact_fmt;
         P.inkernel = P.exact || (P.splits > 1 && P.splits <= INKERNEL_MAX_SPLITS);
         // (else the arrival protocol: the last workgroup of a tile loads every split's
         // partial sum in one batch, up to INKERNEL_MAX_SPLITS; beyond that the finalize
@@ -285,7 +301,8 @@ LutPlan plan_lut(const Layout &L, int64_t M, bool fused) {
     const int64_t rows = P.kind == 1 ? P.m_tiles * P.mt : M;
     // [arrival counters: CNT_AREA][partial sums]
     P.part_off = CNT_AREA;
-    P.ws_bytes = P.splits > 1 ? CNT_AREA + align256((size_t)P.splits * rows * L.N_pad * 4) : 0;
+    // (the exact completion needs only the zero region)
+    P.ws_bytes = P.splits > 1 ? CNT_AREA + (P.exact ? 0 : align256((size_t)P.splits * rows * L.N_pad * 4)) : 0;
     return P;
 }
 
@@ -307,7 +324,7 @@ static LutParams lut_params(const Layout &L, const LutPlan &plan, int64_t M, con
     lp.sgn = L.tri ? (const uint32_t *)((const char *)packed + L.sgn_off) : nullptr;
     lp.meta = (const char *)packed + L.meta_off;
     lp.out = out;
-    lp.part = plan.splits > 1 ? (float *)((char *)workspace + plan.part_off) : nullptr;
+    lp.part = plan.splits > 1 && !plan.exact ? (float *)((char *)workspace + plan.part_off) : nullptr;
     lp.cnt = plan.kind == 2 && plan.inkernel ? (uint32_t *)workspace : nullptr;
     lp.acc64 = plan.kind == 2 && plan.exact ? (unsigned long long *)((char *)workspace + CNT_BYTES) : nullptr;
     lp.bnd = (const int *)((const char *)packed + L.bnd_off);
@@ -359,8 +376,9 @@ static FusedScratch fused_scratch(const Layout &L, const LutPlan &plan, int64_t 
     if (f.fused && plan.kind == 1) {
         f.total = plan.ws_bytes;
     } else if (f.fused) {
+        // (token factors for the finalize kernel; not with the exact completion)
         f.tok_off = plan.ws_bytes;
-        f.total = plan.splits > 1 ? plan.ws_bytes + align256((size_t)M * 4) : 0;
+        f.total = plan.splits > 1 ? plan.ws_bytes + (plan.exact ? 0 : align256((size_t)M * 4)) : 0;
     } else {
         f.tables = make_table_layout(L, M).total;
         f.tables_off = align256(plan.ws_bytes);
@@ -556,7 +574,7 @@ lutgemm_status_t lutgemm_mpgemm_fused(const lutgemm_problem_t *problem, int64_t 
     if (plan.kind == 2) {  // tables from the activations of each K range, then the split sum
         // INT8: the kernel forms the token factor itself; the finalize kernel (long K
         // splits) takes it from the workspace
-        lp.tok_out = (L.act == LUTGEMM_ACT_INT8 && plan.splits > 1) ? (float *)(ws + fs.tok_off) : nullptr;
+        lp.tok_out = (L.act == LUTGEMM_ACT_INT8 && plan.splits > 1 && !plan.exact) ? (float *)(ws + fs.tok_off) : nullptr;
         int e = launch_fused_split(lp, L, plan, stream);
         if (e == 0 && plan.splits > 1 && !plan.inkernel) {
             lp.tok = lp.tok_out;

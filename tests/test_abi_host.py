@@ -8,6 +8,8 @@ import re
 
 import pytest
 
+from helpers import tuning
+
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "lutgemm.h")
 
@@ -212,10 +214,11 @@ def test_fused_entry_point_rejects_before_launch():
     assert f.lutgemm_mpgemm_fused(bp, 0, ok, ok, ok, L.OUT_INT32, 0, None, 0, None) == L.ERROR_INVALID_VALUE
     pf = L.problem(1024, 256, 2, L.WFMT_UINT, 128)
     assert f.lutgemm_mpgemm_fused(ctypes.byref(pf), 1, ok, ok, ok, L.OUT_INT32, 0, None, 0, None) == L.ERROR_NOT_SUPPORTED
-    # K split across workgroups: partial sums and per-token factors
+    # whole-K kernel with K split across workgroups (4 column tiles are too few for the
+    # split-K kernel): the zero region, partial sums and per-token factors
     ps = L.problem(8192, 1000, 2, L.WFMT_TERNARY, 0, L.ACT_INT8, True)
     need = L.fused_workspace_size(ps, 1)
-    assert need >= 2 * 1024 * 4 + 4
+    assert need >= L.WORKSPACE_ZERO_BYTES + 2 * 1024 * 4 + 4
     assert f.lutgemm_mpgemm_fused(ctypes.byref(ps), 1, ok, ok, ok, L.OUT_FP32, 0, None, need, None) == L.ERROR_INVALID_VALUE
     assert f.lutgemm_mpgemm_fused(ctypes.byref(ps), 1, ok, ok, ok, L.OUT_FP32, 0, ok, need - 1, None) == L.ERROR_INSUFFICIENT_SIZE
     # several tokens: tables (lutgemm_table_size) plus the table-fed kernel's workspace
@@ -266,12 +269,15 @@ def test_tuning_overrides():
     old = L.get_tuning("GEMV_KIND")
     p = L.problem(4096, 4096, 2, L.WFMT_UINT, 128)
     ws = L.workspace_size(p, 1)
+    assert ws == L.WORKSPACE_ZERO_BYTES  # planned: split-K GEMV, exact completion
     try:
-        L.set_tuning("GEMV_KIND", 2)   # the split-K kernel: partial sums need a workspace
-        assert L.get_tuning("GEMV_KIND") == 2
-        assert L.workspace_size(p, 1) > ws
+        L.set_tuning("GEMV_KIND", 0)   # the whole-K kernel: 256 column tiles, no K split
+        assert L.get_tuning("GEMV_KIND") == 0
+        assert L.workspace_size(p, 1) == 0
         L.set_tuning("GEMV_KIND", -1)
         assert L.get_tuning("GEMV_KIND") == -1
         assert L.workspace_size(p, 1) == ws
+        with tuning(SPLIT_EXACT=0):  # split-K GEMV with the arrival protocol: partial sums
+            assert L.workspace_size(L.problem(8192, 28672, 1, L.WFMT_BINARY, 8192), 1) > ws
     finally:
         L.set_tuning("GEMV_KIND", old)

@@ -46,12 +46,16 @@ CASES = [
 ]
 
 
-def test_noalloc_matches_mpgemm_two_calls():
+@pytest.mark.parametrize("exact", [0, 1])
+def test_noalloc_matches_mpgemm_two_calls(exact):
+    """Both K-split completions of the split-K kernel on the static scratch: partial
+    sums and arrival counters (exact = 0), or only the exact split-sum words (1)."""
     L.set_tuning("GEMV_KIND", 2)  # the split-K kernel, so both calls use the scratch
+    L.set_tuning("SPLIT_EXACT", exact)
     try:
         sizes = []
         for name, make in CASES:
-            print(f"\n[case] noalloc {name}", flush=True)
+            print(f"\n[case] noalloc {name} exact={exact}", flush=True)
             inp = make()
             gp = GpuProblem(inp)
             need = L.workspace_size(gp.p, inp.M)
@@ -62,9 +66,13 @@ def test_noalloc_matches_mpgemm_two_calls():
             rows, cols = np.arange(inp.M), np.unique(np.linspace(0, inp.N - 1, 512).astype(np.int64))
             want = oracle.reference_output(inp, rows=rows, cols=cols)
             assert_fp_close(y.float().cpu().numpy()[np.ix_(rows, cols)], want, f"noalloc {name}")
-        assert sizes[1] < sizes[0]
+        if exact:
+            assert sizes[1] == sizes[0] == L.WORKSPACE_ZERO_BYTES
+        else:
+            assert sizes[1] < sizes[0]
     finally:
         L.set_tuning("GEMV_KIND", -1)
+        L.set_tuning("SPLIT_EXACT", -1)
 
 
 def test_noalloc_int8_path_bit_exact():
