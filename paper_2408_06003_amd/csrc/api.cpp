@@ -291,6 +291,10 @@ LutPlan plan_lut(const Layout &L, int64_t M, bool fused) {
         if (kbs > L.KB) kbs = L.KB;
         P.kbs = (int)kbs;
         P.splits = (int)((L.KB + kbs - 1) / kbs);
+        // (the K split is summed by the finalize kernel: an exact completion with one
+        // atomic per output and split measured slower from M = 8 on -- 1-bit 8 x 8192 x
+        // 28672: 27-35 us against 23 us; 16 tokens: 48 against 36 us -- as the atomics
+        // grow with the token count; equal at M = 4)
         // workgroup order: with 16 or more token tiles and no K split, each XCD walks its
         // own contiguous share of the tiles in bands of 8 token tiles, tokens fastest
         // (the LLaMA-2-13B shape 1616 -> 1579 us, the 4096^3 prefill 704 -> 701 us); else

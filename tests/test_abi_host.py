@@ -37,8 +37,8 @@ def test_header_constants_match_binding():
     count = int(keys.pop("COUNT"))
     assert {k: int(v) for k, v in keys.items()} == L.TUNE
     assert count == len(L.TUNE)
-    m = re.search(r"#define LUTGEMM_WORKSPACE_ZERO_BYTES \(\(size_t\)1 << (\d+)\)", text)
-    assert m and (1 << int(m.group(1))) == L.WORKSPACE_ZERO_BYTES
+    m = re.search(r"#define LUTGEMM_WORKSPACE_ZERO_BYTES \(\(size_t\)(\d+) << (\d+)\)", text)
+    assert m and (int(m.group(1)) << int(m.group(2))) == L.WORKSPACE_ZERO_BYTES
 
 
 def test_version_and_status_strings():
