@@ -609,7 +609,9 @@ def summarize_trace(directory, command="", bench_logs=()):
            f"  {command}", "",
            "Average/min/max kernel durations in microseconds over all dispatches of the run",
            "(kernel start to end; the bench's per-launch times, measured with HIP events over",
-           "graph replays, also include the gap between back-to-back kernels).", "",
+           "graph replays, also include the gap between back-to-back kernels).  torch's",
+           "spin_kernel is the bench's bounded device-side hold ahead of each queued-timing batch",
+           "(no part of any step).", "",
            f"{'kernel':78s} {'calls':>7s} {'avg_us':>9s} {'min_us':>9s} {'max_us':>9s} {'%time':>6s}"]
     stats.sort(key=lambda r: -float(r["TotalDurationNs"]))
     for r in stats:
