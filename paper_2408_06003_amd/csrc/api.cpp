@@ -219,9 +219,14 @@ LutPlan plan_lut(const Layout &L, int64_t M, bool fused) {
         // 6 x `target` of them, while at most 64 splits add into one output word
         // (measured, us, KBS chosen / the next: INT4 1 x 4096 x 12288 8.4 / 8.9, INT4
         // 1 x 11008 x 4096 8.5 / 9.6, 1-bit 1 x 8192 x 28672 9.7 / 10.7)
+        // 1-bit weights, two tokens: both share each workgroup's pass over the weights
+        // (with the exact completion; 2 x 8192 x 28672: 17.1 -> 15.0-16.4 us, 2 x 28672 x
+        // 8192: 17.0 -> 15.2-15.7).  Wider weights keep a token per workgroup: their
+        // two-token kernels hold every lookup of a block in registers (2 x 4096 x 12288
+        // INT4: 23.6 against 16.5 us)
         P.kind = 2;
-        P.mt = 1;
-        P.m_tiles = M;
+        P.mt = (M == 2 && exact_fmt && L.bits == 1) ? 2 : 1;
+        P.m_tiles = (M + P.mt - 1) / P.mt;
         P.n_tiles = L.N_pad / NTILE;
         const int kmax = 8 / L.bits;
         auto n_splits = [&](int k) { return (L.KB + k - 1) / k; };
@@ -230,7 +235,8 @@ LutPlan plan_lut(const Layout &L, int64_t M, bool fused) {
         if (forced == 1 || forced == 2 || forced == 4 || forced == 8) {
             kbs = forced > kmax ? kmax : forced;
         } else if (exact_fmt) {
-            while (kbs > 1 && P.n_tiles * M * n_splits(kbs) < 6 * target && n_splits(kbs >> 1) <= 64) kbs >>= 1;
+            while (kbs > 1 && P.n_tiles * P.m_tiles * n_splits(kbs) < 6 * target && n_splits(kbs >> 1) <= 64)
+                kbs >>= 1;
         } else {
             while (kbs > 1 && P.n_tiles * M * n_splits(kbs) < 2 * target) kbs >>= 1;
             // 1-bit weights: four words per lane (twice the workgroups) while the split
@@ -247,6 +253,10 @@ LutPlan plan_lut(const Layout &L, int64_t M, bool fused) {
         // four of the arrival protocol, and no limit from a batch of partial loads
         P.exact = P.splits > 1 && P.splits <= EXACT_MAX_SPLITS && exact_fmt;
         P.inkernel = P.exact || (P.splits > 1 && P.splits <= INKERNEL_MAX_SPLITS);
+        if (P.inkernel && !P.exact) {  // the arrival protocol takes one token per workgroup
+            P.mt = 1;
+            P.m_tiles = M;
+        }
         // (else the arrival protocol: the last workgroup of a tile loads every split's
         // partial sum in one batch, up to INKERNEL_MAX_SPLITS; beyond that the finalize
         // kernel's wide batches are faster -- measured: 1 x 11008 x 4096 INT4, 43 splits:

@@ -534,20 +534,36 @@ __device__ __forceinline__ void split_complete(const LutParams &p, int wfmt, int
 // loaded before the atomic, so only the atomic's round trip precedes the store) and
 // clears the word, waiting for the clear's return so that it is performed before the
 // kernel ends.  E = INT_MIN selects the (sx, sy) form.
+// The two halves of split_complete_exact, so that a kernel with several outputs per
+// lane can have all its atomics in flight before it looks at any return: exact_add
+// issues the atomic and returns the previous word; exact_finish decides, for the
+// split that completed the count, the epilogue and the clear (returning the clear's
+// result, which the caller must consume before the kernel ends; 0 for the others).
+__device__ __forceinline__ unsigned long long exact_add(const LutParams &p, int64_t m, int64_t n, long long v) {
+    return __hip_atomic_fetch_add(p.acc64 + m * p.N_pad + n, (1ull << 57) + (unsigned long long)v, __ATOMIC_RELAXED,
+                                  __HIP_MEMORY_SCOPE_AGENT);
+}
+
 template <bool INT8>
-__device__ __forceinline__ void split_complete_exact(const LutParams &p, int wfmt, int64_t m, int64_t n, long long v,
-                                                     float sx, float sy, int E, const Epi &ep) {
-    unsigned long long *w = p.acc64 + m * p.N_pad + n;
-    const unsigned long long old = __hip_atomic_fetch_add(w, (1ull << 57) + (unsigned long long)v, __ATOMIC_RELAXED,
-                                                          __HIP_MEMORY_SCOPE_AGENT);
+__device__ __forceinline__ unsigned long long exact_finish(const LutParams &p, int wfmt, int64_t m, int64_t n,
+                                                           unsigned long long old, long long v, float sx, float sy,
+                                                           int E, const Epi &ep) {
     const unsigned long long c = (old + (1ull << 56)) >> 57;
-    if (c != (unsigned long long)(p.splits - 1)) return;
-    const unsigned long long cleared = __hip_atomic_exchange(w, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (c != (unsigned long long)(p.splits - 1)) return 0ull;
+    const unsigned long long cleared =
+        __hip_atomic_exchange(p.acc64 + m * p.N_pad + n, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     const long long tot = (long long)(old - (c << 57)) + v;
     float yf = 0.f;
     if constexpr (!INT8) yf = E == INT_MIN ? fmaf(sx, (float)tot, -sy) : ldexpf((float)tot, E);
     store_out<INT8>(p, wfmt, m, n, yf, (int)tot, ep);
-    asm volatile("; exact split word cleared from %0" ::"v"(cleared));
+    return cleared;
+}
+
+template <bool INT8>
+__device__ __forceinline__ void split_complete_exact(const LutParams &p, int wfmt, int64_t m, int64_t n, long long v,
+                                                     float sx, float sy, int E, const Epi &ep) {
+    const unsigned long long cleared = exact_finish<INT8>(p, wfmt, m, n, exact_add(p, m, n, v), v, sx, sy, E, ep);
+    asm volatile("; exact split word cleared: %0" ::"v"(cleared));
 }
 
 // The fixed-point value rint(x 2^-E) of an FP32 partial sum (|x 2^-E| < 2^BND_BITS).

@@ -183,46 +183,65 @@ __global__ __launch_bounds__(64 * NW) void lut_gemv2_kernel(LutParams p, int wfm
 // arrive, while the PRE early words keep HBM busy during the table latency.  The 4
 // wavefronts read the same table at a time (no bank conflicts) and the
 // compile-time table offsets leave one SDWA AND per lookup.  With more than one K
-// split the workgroups of a column tile complete the sum themselves
-// (split_complete: the last one to finish adds the partials in split order), so the
-// call is one launch.
-template <int BITS, int KBS, bool INT8, bool TQ, int PRE>
+// split the workgroups of a column tile complete the sum themselves, so the call is
+// one launch: by one exact 64-bit atomic per output (split_complete_exact), or with
+// INT8-quantized tables by the arrival protocol (split_complete: the last one to
+// finish adds the partials in split order).
+// TPW tokens per workgroup (1, or 2 for two tokens with 1-bit weights: the weight
+// words, their index decoding and the metadata then serve both tokens, whose tables
+// sit side by side in LDS, so two tokens cost one pass over the weights instead of
+// two; only with the exact completion, the finalize kernel or no K split).
+template <int BITS, int KBS, bool INT8, bool TQ, int PRE, int TPW>
 __global__ __launch_bounds__(256) void lut_gemv_split_kernel(LutParams p, int wfmt) {
     constexpr int QPT = (KBS * GPB * 4 + 255) / 256;  // table quantities per thread
     constexpr int NWD = KBS * BITS;                  // weight words per lane
     constexpr int NPRE = PRE < NWD ? PRE : NWD;      // of which issued before the table wait
-    __shared__ __attribute__((aligned(16))) char F[KBS * Tab<INT8>::BLK];
+    constexpr int FB = KBS * Tab<INT8>::BLK;         // LDS bytes of one token's tables
+    __shared__ __attribute__((aligned(16))) char F[TPW * FB];
     tl_stamp(p, 0);
     const int tid = threadIdx.x;
     const int64_t n = (int64_t)blockIdx.x * NTILE + tid;
     const int split = blockIdx.y;
-    const int64_t m = blockIdx.z;
+    const int64_t m0 = (int64_t)blockIdx.z * TPW;
+    // the workgroup's tokens; a row past M repeats row M - 1 and is never stored
+    int64_t mr[TPW];
+#pragma unroll
+    for (int u = 0; u < TPW; ++u) mr[u] = m0 + u < p.M ? m0 + u : p.M - 1;
     const int64_t kb0 = (int64_t)split * KBS;
     const int nkb = (int)((p.KB - kb0) < KBS ? (p.KB - kb0) : KBS);
 
     // conditional loads (epilogue operands) first, then the unconditional loads with
     // clamped indices (see lut_gemv2_kernel)
-    Epi ep{};
-    if (p.splits == 1 || p.acc64)  // (exact completion: any split may be the one that stores)
-        ep = load_epi<INT8>(p, wfmt, m, n, split == 0);
-    else if (INT8 && split == 0 && wfmt == LUTGEMM_WFMT_TERNARY)
-        ep.s0 = ((const int *)p.S)[lane_value(m * p.Q)];
-    const int s_total = ep.s0;
+    Epi ep[TPW];
+    int yi[TPW];
+#pragma unroll
+    for (int u = 0; u < TPW; ++u) {
+        ep[u] = Epi{};
+        if (p.splits == 1 || p.acc64)  // (exact completion: any split may be the one that stores)
+            ep[u] = load_epi<INT8>(p, wfmt, mr[u], n, split == 0);
+        else if (INT8 && split == 0 && wfmt == LUTGEMM_WFMT_TERNARY)
+            ep[u].s0 = ((const int *)p.S)[lane_value(mr[u] * p.Q)];
+        yi[u] = ep[u].s0;
+    }
     // exact completion of FP partial sums in fixed point: the column's exponent
     const int bndE = (!INT8 && p.acc64 && p.Q != 1) ? p.bnd[lane_value(n)] : 0;
-    uint2 tq[QPT];
+    uint2 tq[TPW][QPT];
 #pragma unroll
-    for (int r = 0; r < QPT; ++r) {
-        const int e = tid + 256 * r, g = e >> 2, gc = g < nkb * GPB ? g : nkb * GPB - 1;
-        tq[r] = load_quarter<TQ>(p, m * p.J + kb0 * GPB + gc, e & 1);
-    }
-    BlkMeta bm[KBS];
+    for (int u = 0; u < TPW; ++u)
+#pragma unroll
+        for (int r = 0; r < QPT; ++r) {
+            const int e = tid + 256 * r, g = e >> 2, gc = g < nkb * GPB ? g : nkb * GPB - 1;
+            tq[u][r] = load_quarter<TQ>(p, mr[u] * p.J + kb0 * GPB + gc, e & 1);
+        }
+    BlkMeta bm[TPW][KBS];
     if constexpr (!INT8) {
 #pragma unroll
-        for (int kbl = 0; kbl < KBS; ++kbl) {
-            const int kbc = kbl < nkb ? kbl : nkb - 1;
-            bm[kbl] = load_blk_meta(p, kb0 + kbc, m, lane_value(n));
-        }
+        for (int u = 0; u < TPW; ++u)
+#pragma unroll
+            for (int kbl = 0; kbl < KBS; ++kbl) {
+                const int kbc = kbl < nkb ? kbl : nkb - 1;
+                bm[u][kbl] = load_blk_meta(p, kb0 + kbc, mr[u], lane_value(n));
+            }
     }
     uint4 w[KBS][BITS];
     auto load_word = [&](int i) {
@@ -232,83 +251,138 @@ __global__ __launch_bounds__(256) void lut_gemv_split_kernel(LutParams p, int wf
 #pragma unroll
     for (int i = 0; i < NPRE; ++i) load_word(i);
 #pragma unroll
-    for (int r = 0; r < QPT; ++r) {
-        const int e = tid + 256 * r, g = e >> 2;
-        if (g < nkb * GPB)
-            store_quarter<INT8, TQ>(F, g / GPB, g % GPB, e & 3, tq[r]);
-    }
+    for (int u = 0; u < TPW; ++u)
+#pragma unroll
+        for (int r = 0; r < QPT; ++r) {
+            const int e = tid + 256 * r, g = e >> 2;
+            if (g < nkb * GPB)
+                store_quarter<INT8, TQ>(F + u * FB, g / GPB, g % GPB, e & 3, tq[u][r]);
+        }
     lds_barrier();
     asm volatile("" ::: "memory");  // the remaining weight loads stay after the table wait
     tl_stamp(p, 1);
 #pragma unroll
     for (int i = NPRE; i < NWD; ++i) load_word(i);
 
-    float yf = 0.f;
-    int yi = s_total;
-    long long yx = 0;  // FP path, exact completion: the integer sum of the split's entries
+    float yf[TPW];
+    long long yx[TPW];  // FP path, exact completion: the integer sum of the split's entries
+#pragma unroll
+    for (int u = 0; u < TPW; ++u) {
+        yf[u] = 0.f;
+        yx[u] = 0;
+    }
 #pragma unroll
     for (int kbl = 0; kbl < KBS; ++kbl) {
         if (kbl < nkb) {
-            int tot = 0;
+            int tot[TPW];
+#pragma unroll
+            for (int u = 0; u < TPW; ++u) tot[u] = 0;
 #pragma unroll
             for (int t = 0; t < BITS; ++t) {
                 const uint32_t wd[4] = {w[kbl][t].x, w[kbl][t].y, w[kbl][t].z, w[kbl][t].w};
-                int acc = 0;
+                int acc[TPW];
+#pragma unroll
+                for (int u = 0; u < TPW; ++u) acc[u] = 0;
 #pragma unroll
                 for (int d = 0; d < 4; ++d) {
                     constexpr int GS = Tab<INT8>::G;
                     const uint32_t lo = INT8 ? wd[d] << 1 : wd[d] << 2, hi = INT8 ? wd[d] >> 3 : wd[d] >> 2;
-                    const char *Fg = F + kbl * Tab<INT8>::BLK + d * 8 * GS;
-                    acc += lds_entry<INT8>(Fg + 0 * GS, idx_off<0, INT8>(lo)) + lds_entry<INT8>(Fg + 1 * GS, idx_off<0, INT8>(hi));
-                    acc += lds_entry<INT8>(Fg + 2 * GS, idx_off<1, INT8>(lo)) + lds_entry<INT8>(Fg + 3 * GS, idx_off<1, INT8>(hi));
-                    acc += lds_entry<INT8>(Fg + 4 * GS, idx_off<2, INT8>(lo)) + lds_entry<INT8>(Fg + 5 * GS, idx_off<2, INT8>(hi));
-                    acc += lds_entry<INT8>(Fg + 6 * GS, idx_off<3, INT8>(lo)) + lds_entry<INT8>(Fg + 7 * GS, idx_off<3, INT8>(hi));
+                    const uint32_t o0 = idx_off<0, INT8>(lo), o1 = idx_off<0, INT8>(hi), o2 = idx_off<1, INT8>(lo),
+                                   o3 = idx_off<1, INT8>(hi), o4 = idx_off<2, INT8>(lo), o5 = idx_off<2, INT8>(hi),
+                                   o6 = idx_off<3, INT8>(lo), o7 = idx_off<3, INT8>(hi);
+#pragma unroll
+                    for (int u = 0; u < TPW; ++u) {
+                        const char *Fg = F + u * FB + kbl * Tab<INT8>::BLK + d * 8 * GS;
+                        acc[u] += lds_entry<INT8>(Fg + 0 * GS, o0) + lds_entry<INT8>(Fg + 1 * GS, o1);
+                        acc[u] += lds_entry<INT8>(Fg + 2 * GS, o2) + lds_entry<INT8>(Fg + 3 * GS, o3);
+                        acc[u] += lds_entry<INT8>(Fg + 4 * GS, o4) + lds_entry<INT8>(Fg + 5 * GS, o5);
+                        acc[u] += lds_entry<INT8>(Fg + 6 * GS, o6) + lds_entry<INT8>(Fg + 7 * GS, o7);
+                    }
                 }
-                tot += acc << t;  // exact in INT32, see the kernel above
+#pragma unroll
+                for (int u = 0; u < TPW; ++u) tot[u] += acc[u] << t;  // exact in INT32, see the kernel above
             }
-            if constexpr (INT8) {
-                yi += tot;
-            } else {
-                const float2 e = blk_epilogue(p, bm[kbl], kb0 + kbl);
-                yf = fmaf(e.x, (float)tot, yf) - e.y;
-                yx += tot;
+#pragma unroll
+            for (int u = 0; u < TPW; ++u) {
+                if constexpr (INT8) {
+                    yi[u] += tot[u];
+                } else {
+                    const float2 e = blk_epilogue(p, bm[u][kbl], kb0 + kbl);
+                    yf[u] = fmaf(e.x, (float)tot[u], yf[u]) - e.y;
+                    yx[u] += tot[u];
+                }
             }
         }
     }
     tl_stamp(p, 2);
     if (p.splits == 1) {
-        store_out<INT8>(p, wfmt, m, n, yf, yi, ep);
+#pragma unroll
+        for (int u = 0; u < TPW; ++u)
+            if (m0 + u < p.M) store_out<INT8>(p, wfmt, m0 + u, n, yf[u], yi[u], ep[u]);
     } else if (p.acc64) {
-        if (INT8) {
-            split_complete_exact<INT8>(p, wfmt, m, n, (long long)yi, 0.f, 0.f, INT_MIN, ep);
-        } else if (p.Q == 1) {  // integer entries, the column's one group applied at the end
-            const float2 e = blk_epilogue(p, bm[0], 0);
-            split_complete_exact<INT8>(p, wfmt, m, n, yx, e.x, e.y, INT_MIN, ep);
-        } else {
-            split_complete_exact<INT8>(p, wfmt, m, n, to_fixed(yf, bndE), 0.f, 0.f, bndE, ep);
+        // every token's atomic in flight before any return is looked at
+        long long v[TPW];
+        float sx[TPW], sy[TPW];
+        unsigned long long old[TPW];
+#pragma unroll
+        for (int u = 0; u < TPW; ++u) {
+            sx[u] = 0.f;
+            sy[u] = 0.f;
+            if (INT8) {
+                v[u] = (long long)yi[u];
+            } else if (p.Q == 1) {  // integer entries, the column's one group applied at the end
+                const float2 e = blk_epilogue(p, bm[u][0], 0);
+                v[u] = yx[u];
+                sx[u] = e.x;
+                sy[u] = e.y;
+            } else {
+                v[u] = to_fixed(yf[u], bndE);
+            }
+            old[u] = m0 + u < p.M ? exact_add(p, m0 + u, n, v[u]) : 0ull;
         }
-    } else if (p.cnt)
-        split_complete<INT8>(p, wfmt, m, n, split, yf, yi, p.cnt + m * gridDim.x + blockIdx.x);
-    else  // long K splits: lut_finalize_kernel adds the partials after this kernel
-        p.part[((int64_t)split * p.M + m) * p.N_pad + n] = INT8 ? __int_as_float(yi) : yf;
+        const int E = (INT8 || p.Q == 1) ? INT_MIN : bndE;
+        unsigned long long cleared = 0ull;
+#pragma unroll
+        for (int u = 0; u < TPW; ++u)
+            if (m0 + u < p.M) cleared |= exact_finish<INT8>(p, wfmt, m0 + u, n, old[u], v[u], sx[u], sy[u], E, ep[u]);
+        asm volatile("; exact split words cleared: %0" ::"v"(cleared));
+    } else if (TPW == 1 && p.cnt) {
+        split_complete<INT8>(p, wfmt, m0, n, split, yf[0], yi[0], p.cnt + m0 * gridDim.x + blockIdx.x);
+    } else {  // long K splits: lut_finalize_kernel adds the partials after this kernel
+#pragma unroll
+        for (int u = 0; u < TPW; ++u)
+            if (m0 + u < p.M)
+                p.part[((int64_t)split * p.M + m0 + u) * p.N_pad + n] = INT8 ? __int_as_float(yi[u]) : yf[u];
+    }
     tl_stamp(p, 6);
+}
+
+template <int BITS, bool INT8, bool TQ, int PRE, int TPW>
+static void launch_split_tpw(const LutParams &p, const Layout &L, const LutPlan &plan, hipStream_t s) {
+    const dim3 grid((unsigned)(L.N_pad / NTILE), (unsigned)plan.splits, (unsigned)((p.M + TPW - 1) / TPW));
+    switch (plan.kbs) {  // at most 8 weight words per lane (the planner keeps KBS <= 8 / b)
+    case 1: hipLaunchKernelGGL((lut_gemv_split_kernel<BITS, 1, INT8, TQ, PRE, TPW>), grid, dim3(256), 0, s, p, L.wfmt); break;
+    case 2: hipLaunchKernelGGL((lut_gemv_split_kernel<BITS, 2, INT8, TQ, PRE, TPW>), grid, dim3(256), 0, s, p, L.wfmt); break;
+    case 4:
+        if constexpr (BITS <= 2)
+            hipLaunchKernelGGL((lut_gemv_split_kernel<BITS, 4, INT8, TQ, PRE, TPW>), grid, dim3(256), 0, s, p, L.wfmt);
+        break;
+    default:
+        if constexpr (BITS == 1)
+            hipLaunchKernelGGL((lut_gemv_split_kernel<BITS, 8, INT8, TQ, PRE, TPW>), grid, dim3(256), 0, s, p, L.wfmt);
+        break;
+    }
 }
 
 template <int BITS, bool INT8, bool TQ, int PRE>
 static void launch_split_pre(const LutParams &p, const Layout &L, const LutPlan &plan, hipStream_t s) {
-    const dim3 grid((unsigned)(L.N_pad / NTILE), (unsigned)plan.splits, (unsigned)p.M);
-    switch (plan.kbs) {  // at most 8 weight words per lane (the planner keeps KBS <= 8 / b)
-    case 1: hipLaunchKernelGGL((lut_gemv_split_kernel<BITS, 1, INT8, TQ, PRE>), grid, dim3(256), 0, s, p, L.wfmt); break;
-    case 2: hipLaunchKernelGGL((lut_gemv_split_kernel<BITS, 2, INT8, TQ, PRE>), grid, dim3(256), 0, s, p, L.wfmt); break;
-    case 4:
-        if constexpr (BITS <= 2)
-            hipLaunchKernelGGL((lut_gemv_split_kernel<BITS, 4, INT8, TQ, PRE>), grid, dim3(256), 0, s, p, L.wfmt);
-        break;
-    default:
-        if constexpr (BITS == 1)
-            hipLaunchKernelGGL((lut_gemv_split_kernel<BITS, 8, INT8, TQ, PRE>), grid, dim3(256), 0, s, p, L.wfmt);
-        break;
+    if constexpr (BITS == 1) {  // two tokens per workgroup: 1-bit weights only (planner)
+        if (plan.mt == 2) {
+            launch_split_tpw<BITS, INT8, TQ, PRE, 2>(p, L, plan, s);
+            return;
+        }
     }
+    launch_split_tpw<BITS, INT8, TQ, PRE, 1>(p, L, plan, s);
 }
 
 // weight words issued before the table wait: plan.pre (4 by default; 8 = all of them)

@@ -139,3 +139,24 @@ def test_exact_split_extreme_scales(tune):
     for run in (gp.lut, gp.fused):
         fro, mx = assert_fp_close(run(out_dtype=torch.float32).cpu().numpy(), ref, "extreme scales")
         print(f"[err] relFro {fro:.3e} max/rms {mx:.3e}", flush=True)
+
+
+@pytest.mark.parametrize("sid", [0, 1])
+def test_exact_split_two_tokens_full_size(sid):
+    """Two tokens of the 1-bit 70B layers at full size (planned: both tokens in each
+    workgroup of the split-K kernel), sampled outputs against the oracle, and the same
+    outputs as one token at a time."""
+    inp = W.make_inputs(5, sid, M=2)
+    banner(f"exact split, two tokens per workgroup: 2 x {inp.K} x {inp.N}")
+    gp = GpuProblem(inp)
+    y = gp.lut(out_dtype=torch.float32)
+    cols = np.unique(np.linspace(0, inp.N - 1, 512).astype(np.int64))
+    rows = np.arange(2)
+    ref = oracle.reference_output(inp, rows=rows, cols=cols)
+    fro, mx = assert_fp_close(y.cpu().numpy()[np.ix_(rows, cols)], ref, "two tokens")
+    print(f"[err] relFro {fro:.3e} max/rms {mx:.3e}", flush=True)
+    for m in range(2):  # token m alone: same integer sums, same output bits
+        one = W.make_inputs(5, sid, M=2)
+        one.act = one.act[m:m + 1].copy()
+        one.M = 1
+        assert torch.equal(GpuProblem(one).lut(out_dtype=torch.float32)[0], y[m]), f"token {m} differs alone"
