@@ -165,10 +165,10 @@ LutPlan plan_lut(const Layout &L, int64_t M, bool fused) {
     // (measured, table-fed / fused entry, us: INT4 1 x 4096 x 4096 5.3 / 5.5 against the
     // whole-K GEMV's 5.8 / 7.4; INT2 1 x 1024 x 1024, 32 such workgroups, stays whole-K:
     // 3.15 against 3.58); INT8 activations keep the whole-K GEMV (ternary 1 x 4096 x 4096:
-    // 4.66 / 4.79 against 4.20 / 4.83)
-    const bool exact_fmt = L.act != LUTGEMM_ACT_FP16_LUT8 && M * L.N_pad <= EXACT_MAX &&
-                           tuning(LUTGEMM_TUNE_SPLIT_EXACT) == 1;
-    if (kind == 0 && exact_fmt && L.act == LUTGEMM_ACT_FP16 && (L.N_pad / NTILE) * M * L.KB >= 2 * target &&
+    // 4.66 / 4.79 against 4.20 / 4.83).  (INT8-quantized tables are staged as fixed-point
+    // entries like FP16 ones, so their partial sums complete exactly too.)
+    const bool exact_fmt = M * L.N_pad <= EXACT_MAX && tuning(LUTGEMM_TUNE_SPLIT_EXACT) == 1;
+    if (kind == 0 && exact_fmt && L.act != LUTGEMM_ACT_INT8 && (L.N_pad / NTILE) * M * L.KB >= 2 * target &&
         L.KB <= EXACT_MAX_SPLITS)
         kind = 2;
     const int forced_kind = tuning(LUTGEMM_TUNE_GEMV_KIND);

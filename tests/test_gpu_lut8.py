@@ -124,3 +124,16 @@ def test_lut8_full_size_sampled(cid, sid):
     inp = lut8(W.make_inputs(cid, sid, M=M))
     rows, cols = sample_indices(M, N, seed=700 + cid * 10 + sid)
     check(GpuProblem(inp), f"lut8 full {cid}/{sid}", rows=rows, cols=cols, tight=(M <= 2))
+
+
+@pytest.mark.parametrize("cid,M,K,N,kbs", [(3, 1, 4096, 1000, 1), (3, 2, 2048, 777, 2), (5, 2, 4096, 600, 4),
+                                           (1, 1, 8192, 300, 1)])
+def test_lut8_split_k_exact(cid, M, K, N, kbs, tune):
+    """The split-K GEMV (forced) on INT8-quantized tables: staged as fixed-point entries
+    like FP16 tables, so the K split is completed exactly (one atomic per output; two
+    tokens per workgroup for 1-bit weights) -- within the tight bar of the single-token
+    kernels."""
+    tune(GEMV_KIND=2, KBS=kbs)
+    banner(f"lut8 split-K exact config={cid} M={M} K={K} N={N} kbs={kbs}")
+    inp = lut8(W.make_inputs(cid, 0, M=M, K=K, N=N))
+    check(GpuProblem(inp), f"lut8 split-K config {cid} M={M}")
