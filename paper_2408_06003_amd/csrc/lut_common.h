@@ -66,9 +66,11 @@ __device__ __forceinline__ float h2f(uint32_t bits16) {
 // quantizer, or the exact power-of-two token scaling of the FP path.
 template <bool INT8>
 __device__ __forceinline__ float act_value(uint32_t bits16, float scale) {
-    const float a = h2f(bits16);
-    if (INT8) return __builtin_amdgcn_fmed3f(rintf(a * scale), -127.f, 127.f);  // clamp to [-127, 127]
-    return a * scale;  // exact: scale is a power of two
+    // a * scale, one rounding, as a mixed-precision fma on the FP16 operand (adding -0
+    // leaves every product, signed zeros included, unchanged)
+    const float x = fmaf(h2f(bits16), scale, -0.0f);
+    if (INT8) return __builtin_amdgcn_fmed3f(rintf(x), -127.f, 127.f);  // clamp to [-127, 127]
+    return x;  // exact: scale is a power of two
 }
 
 __device__ __forceinline__ float absmax4(uint2 v) {
@@ -142,6 +144,24 @@ __device__ __forceinline__ uint32_t max_u16x2(uint32_t a, uint32_t b) {
     typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
     return __builtin_bit_cast(uint32_t,
                               __builtin_elementwise_max(__builtin_bit_cast(u16x2, a), __builtin_bit_cast(u16x2, b)));
+}
+
+// Maximum over the 64 lanes of an unsigned value (FP16 magnitude bits compare as
+// their values); in lane 63.
+__device__ __forceinline__ uint32_t wave_max_u(uint32_t v) {
+    v = max(v, (uint32_t)dpp_i<0x111, 0xF>((int)v));
+    v = max(v, (uint32_t)dpp_i<0x112, 0xF>((int)v));
+    v = max(v, (uint32_t)dpp_i<0x114, 0xF>((int)v));
+    v = max(v, (uint32_t)dpp_i<0x118, 0xF>((int)v));
+    v = max(v, (uint32_t)dpp_i<0x142, 0xA>((int)v));
+    v = max(v, (uint32_t)dpp_i<0x143, 0xC>((int)v));
+    return v;
+}
+
+// Largest FP16 magnitude bits of the 4 activations in v (as an unsigned value).
+__device__ __forceinline__ uint32_t absmax4_bits(uint2 v) {
+    const uint32_t m = max_u16x2(v.x & 0x7FFF7FFFu, v.y & 0x7FFF7FFFu);
+    return max(m & 0xFFFFu, m >> 16);
 }
 
 // Maximum over the 64 lanes (any order gives the same result); in lane 63.

@@ -60,13 +60,31 @@ __device__ __forceinline__ int quad_bcast(int v) {
 // exact integers (|T| <= 508).  Written as two 16-byte LDS stores.
 __device__ __forceinline__ void build_group_i16(char *dst, int q0, int q1, int q2, int q3) {
     const int b0 = -q0 - q1, b1 = -q0 + q1;
-    const int c0 = b0 - q2, c1 = b0 + q2, c2 = b1 - q2, c3 = b1 + q2;
-    const int t[8] = {c0 - q3, c0 + q3, c1 - q3, c1 + q3, c2 - q3, c2 + q3, c3 - q3, c3 + q3};
+    const int c[4] = {b0 - q2, b0 + q2, b1 - q2, b1 + q2};
+    // entries 2i, 2i + 1 = c_i -+ q3 as one packed INT16 add: (c_i, c_i) + (-q3, q3)
+    const uint32_t d = __builtin_amdgcn_perm((uint32_t)q3, (uint32_t)-q3, 0x05040100u);
     uint32_t pw[4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) pw[i] = ((uint32_t)t[2 * i] & 0xFFFFu) | ((uint32_t)t[2 * i + 1] << 16);
+    for (int i = 0; i < 4; ++i) {
+        const uint32_t cc = __builtin_amdgcn_perm((uint32_t)c[i], (uint32_t)c[i], 0x05040100u);
+        pw[i] = __builtin_bit_cast(uint32_t, __builtin_bit_cast(short2_v, cc) + __builtin_bit_cast(short2_v, d));
+    }
     *(uint4 *)dst = make_uint4(pw[0], pw[1], pw[2], pw[3]);
     *(uint4 *)(dst + 16) = make_uint4(neg_i16x2(pw[0]), neg_i16x2(pw[1]), neg_i16x2(pw[2]), neg_i16x2(pw[3]));
+}
+
+// The precompute's INT8 quantizer clamp(rint(a * scale), -127, 127) of FP16 half H of
+// the word w, the product formed by one mixed-precision fma (FP16 operand read in
+// place, one rounding, adding -0 leaves it unchanged), as act_value<true>.
+template <int H>
+__device__ __forceinline__ int quant8(uint32_t w, float scale) {
+    float x;
+    const uint32_t nz = 0x80000000u;  // -0.0f
+    if constexpr (H == 0)
+        asm("v_fma_mix_f32 %0, %1, %2, %3 op_sel_hi:[1,0,0]" : "=v"(x) : "v"(w), "v"(scale), "s"(nz));
+    else
+        asm("v_fma_mix_f32 %0, %1, %2, %3 op_sel:[1,0,0] op_sel_hi:[1,0,0]" : "=v"(x) : "v"(w), "v"(scale), "s"(nz));
+    return (int)__builtin_amdgcn_fmed3f(rintf(x), -127.f, 127.f);
 }
 
 template <int BITS, int PW, int SW, int TW, int NW, bool INT8>
@@ -88,10 +106,11 @@ __global__ __launch_bounds__(64 * NW) void lut_fused_gemv_kernel(LutParams p, in
     __shared__ int redi[NW][CW];
     __shared__ float hsf[QPT * NW];  // FP path: half-block activation sums, [round][wave]
     __shared__ int hsi[NW];          // INT8 path: activation sum of the K range, per wave
-    __shared__ float wmax[NW];
+    __shared__ uint32_t wmax[NW];
 
     tl_stamp(p, 0);
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: branches on it are scalar
     const int c = lane % CW;
     const int pl = (lane / CW) % PW;
     const int sl = lane / (CW * PW);
@@ -149,32 +168,38 @@ __global__ __launch_bounds__(64 * NW) void lut_fused_gemv_kernel(LutParams p, in
     load_acts(kbA, nkb);
     load_weights(kbA, nkb);
 
-    // 1. amax of the whole token: the first chunk from registers, the rest from memory
-    float amax = 0.f;
+    // 1. amax of the whole token: the first chunk from registers, the rest from memory;
+    // as FP16 magnitude bits (integer maxima: one DPP max per step of the reduction;
+    // the same maximum for finite activations)
+    uint32_t mbits = 0u;
     if constexpr (INT8) {
 #pragma unroll
-        for (int r = 0; r < GPT; ++r) amax = fmaxf(amax, absmax4(ag[r]));
+        for (int r = 0; r < GPT; ++r) mbits = max(mbits, absmax4_bits(ag[r]));
     } else {
 #pragma unroll
-        for (int r = 0; r < QPT; ++r) amax = fmaxf(amax, fabsf(h2f(av[r])));
+        for (int r = 0; r < QPT; ++r) mbits = max(mbits, av[r] & 0x7FFFu);
     }
     const int64_t j0 = kbA * GPB, j1 = j0 + (int64_t)nkb * GPB;
     if (j1 - j0 < p.J) {  // the token extends past the first chunk (several chunks or a K split)
         for (int64_t j = tid; j < p.J; j += NT)
-            if (j < j0 || j >= j1) amax = fmaxf(amax, absmax4(a4[j]));
+            if (j < j0 || j >= j1) mbits = max(mbits, absmax4_bits(a4[j]));
     }
-    amax = wave_max(amax);
-    if (lane == 63) wmax[wave] = amax;
+    mbits = wave_max_u(mbits);
+    if (lane == 63) wmax[wave] = mbits;
     lds_barrier();
     tl_stamp(p, 1);
     // the wavefront maxima, one per lane, reduced by DPP and broadcast from lane 63
-    amax = wave_max(lane < NW ? wmax[lane] : 0.f);
-    amax = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(amax), 63));
-    // the table scale and the output factor t[m] now (off the tail of the kernel)
-    float scale, tok;
+    mbits = wave_max_u(lane < NW ? wmax[lane] : 0u);
+    const float amax = h2f(__builtin_amdgcn_readlane(mbits, 63));
+    // the table scale and the output factor t[m] now (off the tail of the kernel); the
+    // factor only in the wavefront that applies the epilogue
+    float scale, tok = 1.f;
     if (INT8) {
         scale = amax == 0.f ? 0.f : __fdiv_rn(127.0f, amax);
-        tok = amax == 0.f ? 0.f : __fdiv_rn(amax, 127.0f);
+        if (wave == 0) {  // (a real branch: the other wavefronts skip the division)
+            asm volatile("");
+            tok = amax == 0.f ? 0.f : __fdiv_rn(amax, 127.0f);
+        }
     } else if (amax == 0.f) {
         scale = 1.f;
         tok = 1.f;
@@ -201,10 +226,8 @@ __global__ __launch_bounds__(64 * NW) void lut_fused_gemv_kernel(LutParams p, in
 #pragma unroll
             for (int r = 0; r < GPT; ++r) {
                 const int g = tid + NT * r;
-                const int q0 = (int)act_value<true>(ag[r].x & 0xFFFFu, scale);
-                const int q1 = (int)act_value<true>(ag[r].x >> 16, scale);
-                const int q2 = (int)act_value<true>(ag[r].y & 0xFFFFu, scale);
-                const int q3 = (int)act_value<true>(ag[r].y >> 16, scale);
+                const int q0 = quant8<0>(ag[r].x, scale), q1 = quant8<1>(ag[r].x, scale);
+                const int q2 = quant8<0>(ag[r].y, scale), q3 = quant8<1>(ag[r].y, scale);
                 s_tot += (q0 + q1) + (q2 + q3);
                 if (g < nkb * GPB) build_group_i16(F + (g / GPB) * Tab<true>::BLK + (g % GPB) * Tab<true>::G, q0, q1, q2, q3);
             }
