@@ -579,7 +579,7 @@ def stream_ceiling(sizes_mb=(4.2, 8.9, 26.8, 29.5, 48.0, 1024.0)):
 
 HEADLINE_KERNELS = {
     # kind in KERNEL_SOURCES -> name prefix of the kernel the headline step launches
-    "fused": "void lutgemm::lut_fused_gemv_kernel<2, 2, 2, 1, 16, true>",
+    "fused": "void lutgemm::lut_fused_gemv_kernel<2, 2, 2, 4, 4, true>",
     "mpgemm": "void lutgemm::lut_gemv2_kernel<2, 2, 2, 1, 16, true, false>",
 }
 COPY_KERNEL = "__amd_rocclr_copyBuffer"
