@@ -192,7 +192,9 @@ size_t lutgemm_workspace_size(const lutgemm_problem_t *problem, int64_t M);
  * Each weight bit-plane is stored as 4-bit table indices: the pattern of 4
  * consecutive weights (the first weight is the MSB) with the low 3 bits inverted
  * when the MSB is set (Eq. 6); scale and zero are stored as given and
- * reinterpreted (s' = s/2, z' = 2z + 1 - 2^b, Eq. 2) in FP32 where they are used.
+ * reinterpreted (s' = s/2, z' = 2z + 1 - 2^b, Eq. 2) in FP32 where they are used;
+ * per column, a fixed-point exponent derived from its scales and zeros (the unit in
+ * which lutgemm_mpgemm sums K splits exactly) is stored beside them.
  * TERNARY_3IN5: every 3 consecutive weights (padded with 0 past K) become a sign
  * bit and a 4-bit index into the triple table (5 bits per 3 weights).
  */
@@ -214,7 +216,11 @@ lutgemm_status_t lutgemm_precompute(const lutgemm_problem_t *problem, int64_t M,
 /*
  * LUT mpGEMM (Section 3.1 bit-serial lookup with Eq. 3, 5-6; LMMA semantics
  * O = A x W^T + Acc, Section 3.3.1).
- *   tables     device, written by lutgemm_precompute (or the same layout)
+ *   tables     device, written by lutgemm_precompute (or the same layout; FP16 tables
+ *              must hold entries of the normalized token, |x| < 1 as the layout
+ *              defines, so |T| < 4: the single-token kernels sum K splits in fixed
+ *              point with a unit derived from that bound, and larger entries give
+ *              unspecified results there)
  *   packed     device, written by lutgemm_pack_weights
  *   out        device [M][N] row-major, of out_dtype; read first when accumulate != 0
  *   out_dtype  LUTGEMM_OUT_FP16 / FP32; LUTGEMM_OUT_INT32 for ACT_INT8 only
