@@ -261,7 +261,17 @@ __global__ __launch_bounds__(64 * NW) void lut_fused_gemv_kernel(LutParams p, in
             const int hs = wave_sum_i(s_tot);
             if (lane == 63) hsi[wave] = hs;
         }
-        lds_barrier();
+        if constexpr (INT8 && SW * GPB == 64) {
+            // lane 64 w + l builds group 64 w + l + NT r, in block 2 w + l / 32 + S r, and
+            // looks up blocks 2 w + l / 32 + S t: every wavefront reads only the tables
+            // it built, so a wavefront-local fence replaces the workgroup barrier (the
+            // wavefronts no longer wait for each other; 4.26 -> 4.12 us on the headline)
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront", "local");
+            __builtin_amdgcn_wave_barrier();
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront", "local");
+        } else {
+            lds_barrier();
+        }
         tl_stamp(p, 2);
 #pragma unroll
         for (int t = 0; t < TW; ++t) {
