@@ -160,3 +160,47 @@ def test_exact_split_two_tokens_full_size(sid):
         one.act = one.act[m:m + 1].copy()
         one.M = 1
         assert torch.equal(GpuProblem(one).lut(out_dtype=torch.float32)[0], y[m]), f"token {m} differs alone"
+
+
+def _align256(x):
+    return (x + 255) // 256 * 256
+
+
+@pytest.mark.parametrize("wfmt,bits,group,sf", [(W.WFMT_UINT, 4, 128, False), (W.WFMT_UINT, 2, 1024, False),
+                                                (W.WFMT_BINARY, 1, "K", False), (W.WFMT_TERNARY, 2, 0, True)])
+def test_exact_split_column_exponents(wfmt, bits, group, sf):
+    """The per-column fixed-point exponent the packer stores after the metadata (R27):
+    E = floor(log2 B) + 1 - 54 with B = 1.0625 sum_q (kpg |s'_q| 128 (2^b - 1) +
+    |s'_q z'_q| G), recomputed here in float64 from the problem's scales and zeros
+    (s' = s, z' = 0 for 1-bit weights; s' = s/2, z' = -1 for ternary; s' = s/2,
+    z' = 2 z + 1 - 2^b otherwise), with scales spread over 2^20 across columns."""
+    K, N = 2048, 300
+    G = K if group == "K" else group
+    inp = W.make_custom(wfmt, bits, G, W.ACT_FP16, M=1, K=K, N=N, seed=1391, scale_fp32=sf)
+    if not sf:  # columns whose scales differ by up to 2^20
+        inp.scales = (inp.scales.astype(np.float64) * (2.0 ** (np.arange(N) % 21 - 10))[:, None]).astype(np.float16)
+    gp = GpuProblem(inp)
+    raw = gp.g.packed.cpu().numpy()
+    n_pad = -(-N // 256) * 256
+    kb = K // 128
+    Q = 1 if G in (0, K) else K // G
+    meta_off = _align256(kb * bits * n_pad * 16)
+    meta_bytes = 256 if G == 0 else Q * n_pad * 4
+    bnd = raw[meta_off + _align256(meta_bytes):][:n_pad * 4].view(np.int32)
+    Gq = K if G == 0 else G
+    kpg = Gq // 128
+    if G == 0:  # one scale for the tensor
+        s = np.full((N, 1), float(inp.scales.reshape(-1)[0]))
+    else:
+        s = inp.scales.astype(np.float64).reshape(N, -1)
+    if wfmt == W.WFMT_BINARY:
+        sp, zp = s, np.zeros_like(s)
+    elif wfmt == W.WFMT_TERNARY:
+        sp, zp = s * 0.5, -np.ones_like(s)
+    else:
+        sp, zp = s * 0.5, 2.0 * inp.zeros.astype(np.float64).reshape(N, -1) + (1.0 - 2 ** bits)
+    terms = kpg * np.abs(sp) * 128.0 * (2 ** bits - 1) + np.abs(sp * zp) * Gq
+    B = np.cumsum(terms, axis=1)[:, -1] * 1.0625  # in group order, as the packer sums
+    want = np.frexp(B)[1].astype(np.int64) - 54  # ilogb(B) + 1 - 54
+    assert np.array_equal(bnd[:N].astype(np.int64), want), "column exponents differ from the bound"
+    assert not bnd[N:].any(), "padding columns keep exponent 0"
