@@ -58,6 +58,9 @@ CASES = [
     (1, 1, 1024, 1000),
     (1, 2, 1024, 300),
     (2, 1, 4096, 4096),
+    (2, 1, 2560, 700),   # INT8, 4 wavefronts: 20 of the chunk's 32 blocks
+    (2, 2, 3968, 300),   # INT8, 4 wavefronts, 31 blocks, two tokens
+    (2, 1, 4096, 300),   # INT8, 4 wavefronts, K split (few column tiles)
     (2, 2, 2048, 777),
     (2, 1, 8192, 1000),
     (3, 1, 4096, 1000),
