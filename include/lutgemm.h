@@ -373,7 +373,8 @@ enum {
                                        others) (-1: planned)                                         */
     LUTGEMM_TUNE_LOG = 11,          /* LUTGEMM_LOG: 1 prints each launch plan to stderr (0)           */
     LUTGEMM_TUNE_SPLIT_PRE = 12,    /* LUTGEMM_SPLIT_PRE: weight words per lane the split-K kernel
-                                       requests before its tables arrive, 0, 2, 4 or 8 = all (4)    */
+                                       requests before its tables arrive, 0, 2, 4 or 8 = all
+                                       (-1: half of the lane's words)                              */
     LUTGEMM_TUNE_DEQUANT_SPLITS = 13, /* LUTGEMM_DEQUANT_SPLITS: K splits of the comparison kernel
                                        (0: planned)                                                  */
     LUTGEMM_TUNE_MT_FUSED = 14,     /* LUTGEMM_MT_FUSED: lutgemm_mpgemm_fused with FP16 activations and

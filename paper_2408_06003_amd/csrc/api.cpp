@@ -75,7 +75,7 @@ const char *const kTuneEnv[LUTGEMM_TUNE_COUNT] = {
     "LUTGEMM_MT_SPLITS",     "LUTGEMM_MT_ORDER",      "LUTGEMM_DEQUANT_KIND", "LUTGEMM_LOG",
     "LUTGEMM_SPLIT_PRE",     "LUTGEMM_DEQUANT_SPLITS", "LUTGEMM_MT_FUSED", "LUTGEMM_MT4",
     "LUTGEMM_SPLIT_EXACT"};
-const int kTuneDefault[LUTGEMM_TUNE_COUNT] = {256, 10000, -1, -1, 0, 0, 1, 8, 0, -1, -1, 0, 4, 0, -1, 1, 1};
+const int kTuneDefault[LUTGEMM_TUNE_COUNT] = {256, 10000, -1, -1, 0, 0, 1, 8, 0, -1, -1, 0, -1, 0, -1, 1, 1};
 std::atomic<int> g_tune[LUTGEMM_TUNE_COUNT];
 
 bool tune_value_ok(int key, int value) {
@@ -245,7 +245,13 @@ LutPlan plan_lut(const Layout &L, int64_t M, bool fused) {
         }
         P.kbs = kbs;
         P.splits = (int)((L.KB + kbs - 1) / kbs);
-        P.pre = tuning(LUTGEMM_TUNE_SPLIT_PRE);
+        // weight words per lane requested before the tables arrive: half of them
+        // (measured, table-fed / fused, us: INT4 1 x 4096 x 12288, 4 words: 8.6 / 8.4 at
+        // 2 against 9.0 / 8.9 at 4; INT4 1 x 11008 x 4096, 8 words: 8.6 / 8.9 at 4
+        // against 8.9 / 9.7 at 2; 1-bit 1 x 8192 x 28672, 4 words: 9.6 / 9.3 at 2
+        // against 9.7 / 9.5 at 4)
+        const int pre = tuning(LUTGEMM_TUNE_SPLIT_PRE);
+        P.pre = pre >= 0 ? pre : ((kbs * L.bits) / 2 > 1 ? (kbs * L.bits) / 2 : 1);
         // Partial sums that are integers (INT8 activations; fixed-point FP16 table entries
         // on weights with one scale per column or tensor) or fixed point (FP16
         // activations, per-column exponent stored with the packed weights) are summed

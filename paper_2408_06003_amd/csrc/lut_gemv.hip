@@ -385,7 +385,8 @@ static void launch_split_pre(const LutParams &p, const Layout &L, const LutPlan 
     launch_split_tpw<BITS, INT8, TQ, PRE, 1>(p, L, plan, s);
 }
 
-// weight words issued before the table wait: plan.pre (4 by default; 8 = all of them)
+// weight words issued before the table wait: plan.pre (half of the lane's words by
+// default, at least one; 8 = all of them)
 template <int BITS, bool INT8, bool TQ>
 static void launch_split(const LutParams &p, const Layout &L, const LutPlan &plan, hipStream_t s) {
     if (plan.pre == 0) launch_split_pre<BITS, INT8, TQ, 0>(p, L, plan, s);

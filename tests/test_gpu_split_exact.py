@@ -204,3 +204,18 @@ def test_exact_split_column_exponents(wfmt, bits, group, sf):
     want = np.frexp(B)[1].astype(np.int64) - 54  # ilogb(B) + 1 - 54
     assert np.array_equal(bnd[:N].astype(np.int64), want), "column exponents differ from the bound"
     assert not bnd[N:].any(), "padding columns keep exponent 0"
+
+
+@pytest.mark.parametrize("cid,sid", [(3, 0), (5, 0)])
+def test_split_prefetch_depth_same_bits(cid, sid, tune):
+    """How many weight words a lane requests before its tables arrive (SPLIT_PRE: none,
+    2, 4, all, or half by default) changes only when loads are issued: the outputs of
+    the full decode layer are equal bit for bit, table-fed and fused."""
+    inp = W.make_inputs(cid, sid, M=1)
+    banner(f"split-K prefetch depth 1 x {inp.K} x {inp.N}")
+    gp = GpuProblem(inp)
+    ref = (gp.lut(out_dtype=torch.float32), gp.fused(out_dtype=torch.float32))
+    for pre in (0, 2, 4, 8):
+        tune(SPLIT_PRE=pre)
+        assert torch.equal(gp.lut(out_dtype=torch.float32), ref[0]), f"SPLIT_PRE={pre}: table-fed output differs"
+        assert torch.equal(gp.fused(out_dtype=torch.float32), ref[1]), f"SPLIT_PRE={pre}: fused output differs"
