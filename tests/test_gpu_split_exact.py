@@ -17,7 +17,9 @@ scales spread over 2^22 within a column, INT8 activations (bit for bit, and bit 
 bit equal to the split-order protocol), the fused entry point (tables built from the
 unscaled activations), one and two tokens, ragged column tails, accumulation into the
 output, run-to-run determinism, and a layer too wide for the split-sum words (falls
-back to the arrival protocol).  That the words are left zero for the next call, also
+back to the arrival protocol), and the planner's limits: 127 splits and exactly the
+split-sum words of the zero region take the exact completion, one split or one column
+tile more fall back, all equal to the oracle.  That the words are left zero for the next call, also
 of another problem on the same workspace, is checked in test_gpu_workspace.py.
 """
 import numpy as np
@@ -219,3 +221,44 @@ def test_split_prefetch_depth_same_bits(cid, sid, tune):
         tune(SPLIT_PRE=pre)
         assert torch.equal(gp.lut(out_dtype=torch.float32), ref[0]), f"SPLIT_PRE={pre}: table-fed output differs"
         assert torch.equal(gp.fused(out_dtype=torch.float32), ref[1]), f"SPLIT_PRE={pre}: fused output differs"
+
+
+LIMITS = [
+    # (what, M, K, N, exact completion expected)
+    ("127 splits, the most one word counts", 1, 127 * 128, 300, True),
+    ("128 splits: the finalize kernel", 1, 128 * 128, 300, False),
+    ("two tokens, 127 splits", 2, 127 * 128, 260, True),
+    ("122880 words, exactly the zero region", 1, 512, 122880, True),
+    ("one column tile more: the arrival protocol", 1, 512, 122881, False),
+]
+
+
+@pytest.mark.parametrize("what,M,K,N,exact", LIMITS)
+def test_exact_split_limits(what, M, K, N, exact, tune):
+    """At the planner's limits of the exact completion (splits and split-sum words) and
+    one step beyond, INT8 ternary layers (one K block per split) equal the oracle bit
+    for bit.  Which completion ran is read from the workspace the plan asks for: the
+    exact one needs only the zero region, the others add FP32 partial sums."""
+    tune(GEMV_KIND=2, KBS=1, SPLIT_EXACT=1)
+    banner(f"exact split limits: {what}: M={M} K={K} N={N}")
+    inp = W.make_custom(W.WFMT_TERNARY, 2, 0, W.ACT_INT8, M=M, K=K, N=N, seed=1401 + K + N, scale_fp32=True)
+    gp = GpuProblem(inp)
+    ws = L.workspace_size(gp.p, M)
+    assert (ws == L.WORKSPACE_ZERO_BYTES) == exact, f"workspace {ws} B: exact completion {'not ' if exact else ''}planned"
+    acc_ref, y_ref = oracle.reference_output(inp)
+    yi = gp.lut(out_dtype=torch.int32)
+    assert np.array_equal(yi.cpu().numpy().astype(np.int64), acc_ref), "INT32 accumulator differs from the oracle"
+    assert np.array_equal(gp.lut(out_dtype=torch.float32).cpu().numpy(), y_ref), "FP32 output differs from the oracle"
+
+
+def test_exact_split_limit_fp16_fixed_point(tune):
+    """127 splits of 1-bit weights with one scale per column on FP16 activations: the
+    fixed-point form of the completion at its largest arrival count."""
+    tune(GEMV_KIND=2, KBS=1, SPLIT_EXACT=1)
+    banner("exact split limits: FP16 binary 1 x 16256 x 300, 127 splits")
+    inp = W.make_custom(W.WFMT_BINARY, 1, 127 * 128, W.ACT_FP16, M=1, K=127 * 128, N=300, seed=1409)
+    gp = GpuProblem(inp)
+    assert L.workspace_size(gp.p, 1) == L.WORKSPACE_ZERO_BYTES
+    ref = oracle.reference_output(inp)
+    fro, mx = assert_fp_close(gp.lut(out_dtype=torch.float32).cpu().numpy(), ref, "127 splits")
+    print(f"[err] relFro {fro:.3e} max/rms {mx:.3e}", flush=True)
